@@ -1,0 +1,359 @@
+"""Plain fp64 CPU oracle of one TNT memory layer (forward and backward).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import or run this module.  It shares
+no code with the HIP path and imports nothing from the package.
+
+What it computes (paper: "TNT: Improving Chunkwise Training for Test-Time
+Memorization", arXiv 2511.07343), per (batch, head) chain, in fp64:
+
+* Memory module f(W, x) = W2 sigma(W1 x), W1 in R^{h x d}, W2 in R^{d x h}
+  (Sec. 2.1, "deep memory modules"; no bias / residual / norm).
+* Inner loss l(W; k, v) = ||f(W, k) - v||^2 (Sec. 2.1 names MSE as the example)
+  and its gradient u = grad_W l (``inner_grad``).
+* Chunkwise rule (Sec. 2.2, chunkwise compression / retrieval equations): every
+  token of a chunk takes its gradient at the chunk-entry state.
+* Momentum and decay (App. D defers the gating to Titans): with u_t taken at
+  the chunk-entry state, S_t = beta_t S_{t-1} - eta_t u_t and
+  W_t = (1 - alpha_t) W_{t-1} + S_t.  beta = alpha = 0 is the paper's plain rule.
+* Global memory (Sec. 4.1.1 box, global update; App. E general form): chunks
+  of C_G, state carried across chunks, never reset; retrieval at the
+  chunk-entry state V_{xi(t, C_G)} (Sec. 4.1.2 box; App. E retrieval rule).
+* Local memories (Sec. 4.1.1 box, local update; App. E): chunks of C_L, state
+  reset to the learned init (and momentum to zero) every S_L tokens; retrieval
+  at W_t, i.e. after token t's own update (Sec. 2.1 / 2.2 retrieval rules).
+* Q-K projection (Sec. 4.1.2; App. C): local memory i is queried at
+  x_t = M_t q_t, M_t = sum of k k^T / ||k||^2 over the tokens since the last
+  shard start up to and including t (the appendix's running sum with reset);
+  ``qk_scope='chunk'`` takes the sum from the chunk start instead, which is the
+  literal reading of the retrieval box.
+* Output o_t = f(V_{xi(t,C_G)}, q_t) + sum_i f(W^(i)_t, x^(i)_t)
+  (Sec. 4.1.2 box; App. E generalised retrieval rule).
+
+Tokens are 0-indexed: the chunk of size C holding token t starts at
+xi(t, C) = t - (t mod C) (Sec. 1, notation).  The backward pass is autograd of
+sum <dO, o> through this forward, with full second-order terms (the inner
+gradient is differentiated, never stopped); chunk-level checkpointing only
+bounds memory.
+
+Every function here is pinned by tests under ``tests/test_oracle_*.py``
+(finite differences, closed forms, the per-token rule, brute-force sums,
+shard isolation, gradcheck).
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+import torch.utils.checkpoint as _ckpt
+
+DT = torch.float64
+_SQRT2 = math.sqrt(2.0)
+_INV_SQRT_2PI = 1.0 / math.sqrt(2.0 * math.pi)
+
+
+# --------------------------------------------------------------------------
+# activation and memory module (Sec. 2.1)
+# --------------------------------------------------------------------------
+def act(z: torch.Tensor, kind: str) -> torch.Tensor:
+    """sigma(z): exact (erf) GELU or SiLU."""
+    if kind == "gelu":
+        return 0.5 * z * (1.0 + torch.erf(z / _SQRT2))
+    if kind == "silu":
+        return z * torch.sigmoid(z)
+    raise ValueError(kind)
+
+
+def act_grad(z: torch.Tensor, kind: str) -> torch.Tensor:
+    """sigma'(z), written out by hand (differentiable, so the outer backward
+    sees second-order terms)."""
+    if kind == "gelu":
+        cdf = 0.5 * (1.0 + torch.erf(z / _SQRT2))
+        pdf = torch.exp(-0.5 * z * z) * _INV_SQRT_2PI
+        return cdf + z * pdf
+    if kind == "silu":
+        s = torch.sigmoid(z)
+        return s + z * s * (1.0 - s)
+    raise ValueError(kind)
+
+
+def memory_fn(W1: torch.Tensor, W2: torch.Tensor, x: torch.Tensor, kind: str) -> torch.Tensor:
+    """f(W, x) = W2 sigma(W1 x); W1 [...,h,d], W2 [...,d,h], x [...,d] -> [...,d]."""
+    z = torch.einsum("...hd,...d->...h", W1, x)
+    return torch.einsum("...dh,...h->...d", W2, act(z, kind))
+
+
+def recall_loss(W1, W2, k, v, kind) -> torch.Tensor:
+    """l(W; k, v) = ||f(W, k) - v||^2, summed over the last axis."""
+    e = memory_fn(W1, W2, k, kind) - v
+    return (e * e).sum(-1)
+
+
+def inner_grad(W1, W2, k, v, kind) -> Tuple[torch.Tensor, torch.Tensor]:
+    """u = grad_W ||f(W,k) - v||^2 written out by the chain rule.
+
+    z = W1 k, a = sigma(z), y = W2 a, r = 2 (y - v);
+    dl/dW2 = r a^T;  dl/dW1 = ((W2^T r) * sigma'(z)) k^T.
+    Leading axes broadcast (W [P,1,h,d] with k [P,C,d] gives one gradient
+    per token, all at the same W).
+    """
+    z = torch.einsum("...hd,...d->...h", W1, k)
+    a = act(z, kind)
+    y = torch.einsum("...dh,...h->...d", W2, a)
+    r = 2.0 * (y - v)
+    g2 = r[..., :, None] * a[..., None, :]
+    back = torch.einsum("...dh,...d->...h", W2, r) * act_grad(z, kind)
+    g1 = back[..., :, None] * k[..., None, :]
+    return g1, g2
+
+
+def _bc(x: torch.Tensor) -> torch.Tensor:
+    return x[:, None, None]
+
+
+def _gated_step(W1, W2, S1, S2, g1, g2, eta, beta, alpha):
+    """One token of the gated inner optimiser (momentum S, decay alpha)."""
+    S1 = _bc(beta) * S1 - _bc(eta) * g1
+    S2 = _bc(beta) * S2 - _bc(eta) * g2
+    W1 = _bc(1.0 - alpha) * W1 + S1
+    W2 = _bc(1.0 - alpha) * W2 + S2
+    return W1, W2, S1, S2
+
+
+# --------------------------------------------------------------------------
+# global memory (Sec. 4.1.1 global update, Sec. 4.1.2 retrieval at V_xi)
+# --------------------------------------------------------------------------
+def _global_retrieve(V1, V2, q, kind):
+    """f(V_hat, q_t) for every token of a chunk, V_hat = chunk-entry state."""
+    z = torch.einsum("phd,pcd->pch", V1, q)
+    return torch.einsum("pdh,pch->pcd", V2, act(z, kind))
+
+
+def _global_accumulate(V1, V2, S1, S2, V1h, V2h, k, v, eta, beta, alpha, kind):
+    """Gated accumulation of the tokens of (part of) a global chunk, every
+    gradient taken at the chunk-entry state (V1h, V2h)."""
+    g1, g2 = inner_grad(V1h[:, None], V2h[:, None], k, v, kind)
+    for i in range(k.shape[1]):
+        V1, V2, S1, S2 = _gated_step(V1, V2, S1, S2, g1[:, i], g2[:, i],
+                                     eta[:, i], beta[:, i], alpha[:, i])
+    return V1, V2, S1, S2
+
+
+def global_memory(q, k, v, eta, beta, alpha, W1, W2, C_G: int, kind: str,
+                  ckpt: bool = False, block: int = 64, states: Optional[list] = None):
+    """Global memory of every chain.  q,k,v [P,L,d]; gates [P,L]; W1 [P,h,d].
+
+    Returns (o [P,L,d], (V1, V2, S1, S2) after the last token).  When
+    ``states`` is a list, the chunk-entry states are appended to it.
+    """
+    P, L, d = q.shape
+    if L % C_G:
+        raise ValueError("L must be a multiple of C_G")
+    V1, V2 = W1, W2
+    S1 = torch.zeros_like(W1)
+    S2 = torch.zeros_like(W2)
+    outs = []
+    for n in range(L // C_G):
+        t0 = n * C_G
+        V1h, V2h = V1, V2
+        if states is not None:
+            states.append((V1, V2, S1, S2))
+        outs.append(_global_retrieve(V1h, V2h, q[:, t0:t0 + C_G], kind))
+        for b0 in range(t0, t0 + C_G, block):
+            b1 = min(b0 + block, t0 + C_G)
+            args = (V1, V2, S1, S2, V1h, V2h, k[:, b0:b1], v[:, b0:b1],
+                    eta[:, b0:b1], beta[:, b0:b1], alpha[:, b0:b1], kind)
+            if ckpt:
+                V1, V2, S1, S2 = _ckpt.checkpoint(_global_accumulate, *args, use_reentrant=False)
+            else:
+                V1, V2, S1, S2 = _global_accumulate(*args)
+    return torch.cat(outs, 1), (V1, V2, S1, S2)
+
+
+# --------------------------------------------------------------------------
+# local memories (Sec. 4.1.1 local update with reset, Sec. 4.1.2 Q-K projection)
+# --------------------------------------------------------------------------
+def _local_chunk(W1, W2, S1, S2, Mq, q, k, v, eta, beta, alpha, kind, qk_proj):
+    """One local chunk: gradients at the chunk-entry state, per-token gated
+    update, Q-K running sum including token t, retrieval at W_t."""
+    g1, g2 = inner_grad(W1[:, None], W2[:, None], k, v, kind)   # all at the entry state
+    outs = []
+    for i in range(k.shape[1]):
+        W1, W2, S1, S2 = _gated_step(W1, W2, S1, S2, g1[:, i], g2[:, i],
+                                     eta[:, i], beta[:, i], alpha[:, i])
+        kt = k[:, i]
+        Mq = Mq + kt[:, :, None] * kt[:, None, :] / (kt * kt).sum(-1)[:, None, None]
+        x = torch.einsum("pde,pe->pd", Mq, q[:, i]) if qk_proj else q[:, i]
+        outs.append(memory_fn(W1, W2, x, kind))
+    return W1, W2, S1, S2, Mq, torch.stack(outs, 1)
+
+
+def local_memory(q, k, v, eta, beta, alpha, W1i, W2i, C_L: int, S_L: int, kind: str,
+                 qk_proj: bool = True, qk_scope: str = "shard", ckpt: bool = False,
+                 shards: Optional[Sequence[int]] = None, final: Optional[list] = None):
+    """One local memory over every chain.  Returns o [P,L,d] (zero outside the
+    requested ``shards`` when a subset is given)."""
+    P, L, d = q.shape
+    if L % S_L or S_L % C_L:
+        raise ValueError("need S_L | L and C_L | S_L")
+    wanted = set(range(L // S_L)) if shards is None else set(shards)
+    per_shard = []
+    for s in range(L // S_L):
+        if s not in wanted:
+            per_shard.append(torch.zeros(P, S_L, d, dtype=q.dtype))
+            continue
+        W1, W2 = W1i, W2i                      # reset to the learned init
+        S1 = torch.zeros_like(W1i)
+        S2 = torch.zeros_like(W2i)
+        Mq = torch.zeros(P, d, d, dtype=q.dtype)
+        chunks = []
+        for c0 in range(s * S_L, (s + 1) * S_L, C_L):
+            if qk_scope == "chunk":
+                Mq = torch.zeros(P, d, d, dtype=q.dtype)
+            sl = slice(c0, c0 + C_L)
+            args = (W1, W2, S1, S2, Mq, q[:, sl], k[:, sl], v[:, sl],
+                    eta[:, sl], beta[:, sl], alpha[:, sl], kind, qk_proj)
+            if ckpt:
+                W1, W2, S1, S2, Mq, o = _ckpt.checkpoint(_local_chunk, *args, use_reentrant=False)
+            else:
+                W1, W2, S1, S2, Mq, o = _local_chunk(*args)
+            chunks.append(o)
+        per_shard.append(torch.cat(chunks, 1))
+        if final is not None:
+            final.append((W1, W2, S1, S2, Mq))
+    return torch.cat(per_shard, 1)
+
+
+# --------------------------------------------------------------------------
+# the layer
+# --------------------------------------------------------------------------
+_ACT_NAMES = {0: "gelu", 1: "silu"}
+
+
+def _kind(cfg) -> str:
+    a = getattr(cfg, "act")
+    return _ACT_NAMES[a] if isinstance(a, int) else a
+
+
+def _scope(cfg) -> str:
+    s = getattr(cfg, "qk_scope", 0)
+    return {0: "shard", 1: "chunk"}[s] if isinstance(s, int) else s
+
+
+def layer_forward(q, k, v, lr, mom, decay, W1, W2, cfg, ckpt: bool = False,
+                  shards: Optional[Sequence[int]] = None, with_final: bool = False):
+    """o for every chain.  q,k,v [P,L,d]; lr/mom/decay [M,P,L] (eta, beta,
+    alpha); W1 [M,P,h,d], W2 [M,P,d,h] (the head's init for every chain).
+
+    ``cfg`` supplies C_G, locals_ = ((C_L, S_L), ...), act, has_global,
+    qk_proj, qk_scope.  Memory 0 is the global memory when has_global.
+    ``shards`` restricts the local memories to some shards (for sampling; the
+    output is then only meaningful on those shards and without the global).
+    """
+    kind = _kind(cfg)
+    o = torch.zeros_like(q)
+    m = 0
+    final = None
+    if cfg.has_global:
+        og, final = global_memory(q, k, v, lr[0], mom[0], decay[0], W1[0], W2[0],
+                                  cfg.C_G, kind, ckpt=ckpt)
+        o = o + og
+        m = 1
+    for (C_L, S_L) in cfg.locals_:
+        o = o + local_memory(q, k, v, lr[m], mom[m], decay[m], W1[m], W2[m], C_L, S_L, kind,
+                             qk_proj=bool(cfg.qk_proj), qk_scope=_scope(cfg), ckpt=ckpt,
+                             shards=shards)
+        m += 1
+    if with_final:
+        return o, final
+    return o
+
+
+def layer_backward(q, k, v, lr, mom, decay, W1, W2, dO, cfg, ckpt: bool = True):
+    """Gradients of sum <dO, o> with respect to every input (autograd through
+    the fp64 forward).  Returns a dict with dq, dk, dv [P,L,d], dlr, dmom,
+    ddecay [M,P,L], dW1 [M,P,h,d], dW2 [M,P,d,h] (per chain: the caller sums
+    chains that share a head) and o."""
+    leaves = [t.detach().clone().requires_grad_(True) for t in (q, k, v, lr, mom, decay, W1, W2)]
+    o = layer_forward(*leaves, cfg, ckpt=ckpt)
+    grads = torch.autograd.grad((o * dO).sum(), leaves)
+    names = ["dq", "dk", "dv", "dlr", "dmom", "ddecay", "dW1", "dW2"]
+    out = {n: g.detach() for n, g in zip(names, grads)}
+    out["o"] = o.detach()
+    return out
+
+
+# --------------------------------------------------------------------------
+# the per-token rule (Sec. 2.1 compression / retrieval equations)
+# --------------------------------------------------------------------------
+def sequential(q, k, v, eta, beta, alpha, W1, W2, kind: str, reset: Optional[int] = None,
+               qk_proj: bool = False, retrieve_first: bool = False):
+    """Token-by-token deep memory with no chunking: each gradient is taken at
+    the current state W_{t-1}.  ``reset`` re-initialises W, S (and the Q-K sum)
+    every ``reset`` tokens; ``retrieve_first`` reads f(W_{t-1}, q_t) before the
+    update (what a chunk of one token gives under the global retrieval rule)."""
+    P, L, d = q.shape
+    outs = []
+    for t in range(L):
+        if t == 0 or (reset is not None and t % reset == 0):
+            Wa, Wb = W1, W2
+            Sa = torch.zeros_like(W1)
+            Sb = torch.zeros_like(W2)
+            Mq = torch.zeros(P, d, d, dtype=q.dtype)
+        if retrieve_first:
+            outs.append(memory_fn(Wa, Wb, q[:, t], kind))
+        ga, gb = inner_grad(Wa, Wb, k[:, t], v[:, t], kind)
+        Sa = _bc(beta[:, t]) * Sa - _bc(eta[:, t]) * ga
+        Sb = _bc(beta[:, t]) * Sb - _bc(eta[:, t]) * gb
+        Wa = _bc(1.0 - alpha[:, t]) * Wa + Sa
+        Wb = _bc(1.0 - alpha[:, t]) * Wb + Sb
+        kt = k[:, t]
+        Mq = Mq + torch.einsum("pd,pe->pde", kt, kt) / (kt * kt).sum(-1)[:, None, None]
+        if not retrieve_first:
+            x = torch.einsum("pde,pe->pd", Mq, q[:, t]) if qk_proj else q[:, t]
+            outs.append(memory_fn(Wa, Wb, x, kind))
+    return torch.stack(outs, 1), (Wa, Wb, Sa, Sb)
+
+
+# --------------------------------------------------------------------------
+# helpers to feed full [B,H,L,d] arrays (numpy) for a list of (b, h) chains
+# --------------------------------------------------------------------------
+def gather_pairs(inp, pairs: Sequence[Tuple[int, int]]):
+    """Pick the chains ``pairs`` out of full-size numpy arrays and return fp64
+    torch tensors in the oracle's per-chain layout."""
+    b = np.array([p[0] for p in pairs])
+    h = np.array([p[1] for p in pairs])
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64))
+    return dict(
+        q=t(inp.q[b, h]), k=t(inp.k[b, h]), v=t(inp.v[b, h]),
+        lr=t(inp.lr[:, b, h]), mom=t(inp.mom[:, b, h]), decay=t(inp.decay[:, b, h]),
+        W1=t(inp.W1[:, h]), W2=t(inp.W2[:, h]), dO=t(inp.dO[b, h]),
+    )
+
+
+def forward_pairs(inp, cfg, pairs, with_final: bool = False):
+    g = gather_pairs(inp, pairs)
+    with torch.no_grad():
+        return layer_forward(g["q"], g["k"], g["v"], g["lr"], g["mom"], g["decay"],
+                             g["W1"], g["W2"], cfg, with_final=with_final)
+
+
+def backward_pairs(inp, cfg, pairs):
+    g = gather_pairs(inp, pairs)
+    return layer_backward(g["q"], g["k"], g["v"], g["lr"], g["mom"], g["decay"],
+                          g["W1"], g["W2"], g["dO"], cfg)
+
+
+def all_pairs(cfg) -> List[Tuple[int, int]]:
+    return [(b, h) for b in range(cfg.B) for h in range(cfg.H)]
+
+
+def reduce_init_grads(dW: torch.Tensor, pairs, H: int) -> torch.Tensor:
+    """Sum per-chain init gradients [M,P,...] over the chains of each head
+    -> [M,H,...] (the init is shared across batch and shards)."""
+    out = torch.zeros((dW.shape[0], H) + tuple(dW.shape[2:]), dtype=dW.dtype)
+    for i, (_, h) in enumerate(pairs):
+        out[:, h] += dW[:, i]
+    return out

@@ -1,0 +1,385 @@
+"""Pins of the fp64 oracle against facts the paper and the mathematics fix.
+
+None of these re-types an oracle formula: each compares the oracle with an
+independent route to the same number (finite differences, a closed form of
+the gated recurrence built from explicit products, the paper's per-token rule,
+brute-force sums, shard isolation, autograd gradcheck).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2511_07343_amd.inputs import (ACT_GELU, ACT_SILU, F32, QK_CHUNK, QK_SHARD,
+                                         make_inputs, small_config)
+
+torch.set_num_threads(1)
+KINDS = ["gelu", "silu"]
+
+
+def _t(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64))
+
+
+def _rand_chain(rng, P, L, d, h, unit_keys=True, gates=True):
+    q = rng.standard_normal((P, L, d))
+    k = rng.standard_normal((P, L, d))
+    v = rng.standard_normal((P, L, d))
+    if unit_keys:
+        q /= np.linalg.norm(q, axis=-1, keepdims=True)
+        k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    eta = rng.uniform(0.01, 0.1, (P, L))
+    beta = rng.uniform(0.8, 0.95, (P, L)) if gates else np.zeros((P, L))
+    alpha = rng.uniform(0.0, 0.01, (P, L)) if gates else np.zeros((P, L))
+    std = math.sqrt(2.0 / (d + h))
+    W1 = rng.normal(0, std, (P, h, d))
+    W2 = rng.normal(0, std, (P, d, h))
+    return [_t(x) for x in (q, k, v, eta, beta, alpha, W1, W2)]
+
+
+# ---------------------------------------------------------------- activations
+def _gelu_ref(z):
+    return z * 0.5 * (1.0 + math.erf(z / math.sqrt(2.0)))
+
+
+def _silu_ref(z):
+    return z / (1.0 + math.exp(-z))
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_activation_matches_textbook(kind):
+    """GELU(z) = z Phi(z) (exact erf form), SiLU(z) = z / (1 + e^-z)."""
+    zs = [-6.0, -2.5, -1.0, -0.3, 0.0, 0.2, 1.0, 2.0, 5.5]
+    ref = _gelu_ref if kind == "gelu" else _silu_ref
+    got = O.act(torch.tensor(zs, dtype=torch.float64), kind).numpy()
+    np.testing.assert_allclose(got, [ref(z) for z in zs], rtol=1e-14, atol=1e-15)
+    # textbook constants: GELU(1) = Phi(1), SiLU(1) = 1 / (1 + e^-1)
+    if kind == "gelu":
+        assert abs(O.act(torch.tensor([1.0], dtype=torch.float64), kind).item()
+                   - 0.8413447460685429) < 1e-15
+    else:
+        assert abs(O.act(torch.tensor([1.0], dtype=torch.float64), kind).item()
+                   - 0.7310585786300049) < 1e-15
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_activation_derivative_finite_difference(kind):
+    z = torch.linspace(-5, 5, 101, dtype=torch.float64)
+    h = 1e-6
+    fd = (O.act(z + h, kind) - O.act(z - h, kind)) / (2 * h)
+    np.testing.assert_allclose(O.act_grad(z, kind).numpy(), fd.numpy(), rtol=1e-8, atol=1e-9)
+
+
+# ---------------------------------------------------------------- inner gradient
+@pytest.mark.parametrize("kind", KINDS)
+def test_inner_grad_central_differences(kind):
+    """u = grad_W ||f(W,k) - v||^2 (Sec. 2.1) against central differences."""
+    rng = np.random.default_rng(1)
+    P, d, h = 2, 5, 7
+    W1 = _t(rng.normal(0, 0.6, (P, h, d)))
+    W2 = _t(rng.normal(0, 0.6, (P, d, h)))
+    k = _t(rng.standard_normal((P, d)))
+    v = _t(rng.standard_normal((P, d)))
+    g1, g2 = O.inner_grad(W1, W2, k, v, kind)
+    eps = 1e-6
+    for W, g, which in ((W1, g1, 0), (W2, g2, 1)):
+        fd = torch.zeros_like(W)
+        for idx in np.ndindex(*W.shape[1:]):
+            for p in range(P):
+                Wp = W.clone(); Wm = W.clone()
+                Wp[(p,) + idx] += eps
+                Wm[(p,) + idx] -= eps
+                if which == 0:
+                    lp = O.recall_loss(Wp, W2, k, v, kind)[p]
+                    lm = O.recall_loss(Wm, W2, k, v, kind)[p]
+                else:
+                    lp = O.recall_loss(W1, Wp, k, v, kind)[p]
+                    lm = O.recall_loss(W1, Wm, k, v, kind)[p]
+                fd[(p,) + idx] = (lp - lm) / (2 * eps)
+        err = (g - fd).abs().max() / fd.abs().max()
+        assert err < 1e-6, err
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_inner_grad_matches_autograd_of_loss(kind):
+    rng = np.random.default_rng(2)
+    P, d, h = 3, 4, 6
+    W1 = _t(rng.normal(0, 0.5, (P, h, d))).requires_grad_(True)
+    W2 = _t(rng.normal(0, 0.5, (P, d, h))).requires_grad_(True)
+    k = _t(rng.standard_normal((P, d)))
+    v = _t(rng.standard_normal((P, d)))
+    a1, a2 = torch.autograd.grad(O.recall_loss(W1, W2, k, v, kind).sum(), (W1, W2))
+    g1, g2 = O.inner_grad(W1.detach(), W2.detach(), k, v, kind)
+    assert torch.allclose(g1, a1, rtol=1e-12, atol=1e-13)
+    assert torch.allclose(g2, a2, rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- C = 1 is the per-token rule
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("qk", [True, False])
+def test_local_chunk_one_is_per_token_rule(kind, qk):
+    """Chunk size 1 turns the chunkwise rule (Sec. 2.2) into the per-token
+    compression / retrieval equations (Sec. 2.1), resets included."""
+    rng = np.random.default_rng(3)
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, 2, 24, 4, 6)
+    o = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, 1, 8, kind, qk_proj=qk)
+    ref, _ = O.sequential(q, k, v, eta, beta, alpha, W1, W2, kind, reset=8, qk_proj=qk)
+    assert (o - ref).abs().max() < 1e-12
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_global_chunk_one_is_retrieve_then_update(kind):
+    """C_G = 1: the global rule reads V_{xi(t,1)} = V_{t-1}, then updates."""
+    rng = np.random.default_rng(4)
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, 2, 20, 4, 6)
+    o, fin = O.global_memory(q, k, v, eta, beta, alpha, W1, W2, 1, kind)
+    ref, rfin = O.sequential(q, k, v, eta, beta, alpha, W1, W2, kind, retrieve_first=True)
+    assert (o - ref).abs().max() < 1e-12
+    for a, b in zip(fin, rfin):
+        assert (a - b).abs().max() < 1e-12
+
+
+# ---------------------------------------------------------------- closed forms of the gated recurrence
+def _closed_form_coeffs(eta, beta, alpha, t):
+    """A_t = prod_{j<=t}(1-alpha_j); c_{t,tau} = eta_tau sum_{m=tau}^{t}
+    prod_{j=m+1}^{t}(1-alpha_j) prod_{j=tau+1}^{m} beta_j, and the momentum
+    weights b_{t,tau} = eta_tau prod_{j=tau+1}^{t} beta_j (explicit products,
+    0-indexed positions, inclusive t)."""
+    A = np.prod(1.0 - alpha[: t + 1])
+    c = np.zeros(t + 1)
+    b = np.zeros(t + 1)
+    for tau in range(t + 1):
+        s = 0.0
+        for m in range(tau, t + 1):
+            s += np.prod(1.0 - alpha[m + 1: t + 1]) * np.prod(beta[tau + 1: m + 1])
+        c[tau] = eta[tau] * s
+        b[tau] = eta[tau] * np.prod(beta[tau + 1: t + 1])
+    return A, c, b
+
+
+def _np_f(W1, W2, x, kind):
+    z = W1 @ x
+    s = np.array([_gelu_ref(zz) if kind == "gelu" else _silu_ref(zz) for zz in z])
+    return W2 @ s
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_global_chunk_equal_length_takes_every_gradient_at_init(kind):
+    """C_G = L: every global output is f(V_init, q_t) and the final state is the
+    closed form of the gated sum of gradients all taken at V_init."""
+    rng = np.random.default_rng(5)
+    P, L, d, h = 1, 12, 3, 5
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h)
+    o, (V1, V2, S1, S2) = O.global_memory(q, k, v, eta, beta, alpha, W1, W2, L, kind)
+    W1n, W2n = W1[0].numpy(), W2[0].numpy()
+    for t in range(L):
+        np.testing.assert_allclose(o[0, t].numpy(), _np_f(W1n, W2n, q[0, t].numpy(), kind),
+                                   rtol=1e-12, atol=1e-13)
+    A, c, b = _closed_form_coeffs(eta[0].numpy(), beta[0].numpy(), alpha[0].numpy(), L - 1)
+    u1 = np.zeros((L, h, d)); u2 = np.zeros((L, d, h))
+    for t in range(L):
+        g1, g2 = O.inner_grad(W1, W2, k[:, t], v[:, t], kind)
+        u1[t], u2[t] = g1[0].numpy(), g2[0].numpy()
+    V1_ref = A * W1n - np.einsum("t,thd->hd", c, u1)
+    V2_ref = A * W2n - np.einsum("t,tdh->dh", c, u2)
+    S1_ref = -np.einsum("t,thd->hd", b, u1)
+    S2_ref = -np.einsum("t,tdh->dh", b, u2)
+    for got, ref in ((V1, V1_ref), (V2, V2_ref), (S1, S1_ref), (S2, S2_ref)):
+        np.testing.assert_allclose(got[0].numpy(), ref, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_local_single_chunk_closed_form_with_brute_force_projection(kind):
+    """One local chunk (C_L = S_L = L): o_t = f(W_t, M_t q_t) with W_t from the
+    closed form (all gradients at W_init) and M_t the brute-force sum of
+    k k^T / ||k||^2 over tau <= t.  Keys are NOT unit here, so the
+    denominator matters."""
+    rng = np.random.default_rng(6)
+    P, L, d, h = 1, 10, 3, 5
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h, unit_keys=False)
+    o = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, L, L, kind, qk_proj=True)
+    W1n, W2n = W1[0].numpy(), W2[0].numpy()
+    u = [O.inner_grad(W1, W2, k[:, t], v[:, t], kind) for t in range(L)]
+    kn = k[0].numpy(); qn = q[0].numpy()
+    for t in range(L):
+        A, c, _ = _closed_form_coeffs(eta[0].numpy(), beta[0].numpy(), alpha[0].numpy(), t)
+        W1t = A * W1n - sum(c[s] * u[s][0][0].numpy() for s in range(t + 1))
+        W2t = A * W2n - sum(c[s] * u[s][1][0].numpy() for s in range(t + 1))
+        Mt = sum(np.outer(kn[s], kn[s]) / np.dot(kn[s], kn[s]) for s in range(t + 1))
+        np.testing.assert_allclose(o[0, t].numpy(), _np_f(W1t, W2t, Mt @ qn[t], kind),
+                                   rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_no_momentum_no_decay_is_the_papers_chunkwise_rule(kind):
+    """beta = alpha = 0 gives W_t = W_xi - sum_{tau=xi}^{t} eta_tau u_tau(W_xi)
+    (Sec. 2.2 chunkwise compression), evaluated here with a cumulative sum over
+    the chunk and retrieval at W_t without projection."""
+    rng = np.random.default_rng(7)
+    P, L, d, h, C = 2, 24, 3, 4, 6
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h, gates=False)
+    o = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, C, L, kind, qk_proj=False)
+    Wa, Wb = W1.clone(), W2.clone()
+    ref = torch.zeros_like(o)
+    for c0 in range(0, L, C):
+        g1, g2 = O.inner_grad(Wa[:, None], Wb[:, None], k[:, c0:c0 + C], v[:, c0:c0 + C], kind)
+        cs1 = torch.cumsum(eta[:, c0:c0 + C, None, None] * g1, 1)
+        cs2 = torch.cumsum(eta[:, c0:c0 + C, None, None] * g2, 1)
+        for i in range(C):
+            ref[:, c0 + i] = O.memory_fn(Wa - cs1[:, i], Wb - cs2[:, i], q[:, c0 + i], kind)
+        Wa, Wb = Wa - cs1[:, -1], Wb - cs2[:, -1]
+    assert (o - ref).abs().max() < 1e-12
+
+
+# ---------------------------------------------------------------- Q-K projection across chunks
+@pytest.mark.parametrize("scope", ["shard", "chunk"])
+def test_qk_projection_running_sum_brute_force(scope):
+    """With eta = 0 and alpha = 0 nothing is learned, so o_t = f(W_init, x_t)
+    and x_t exposes the projection: M_t = sum of k k^T/||k||^2 from the shard
+    start (or the chunk start under the chunk scope) to t (Sec. 4.1.2, App. C)."""
+    rng = np.random.default_rng(8)
+    P, L, d, h, C, S = 1, 24, 4, 5, 4, 12
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h, unit_keys=False)
+    eta = torch.zeros_like(eta)
+    alpha = torch.zeros_like(alpha)
+    o = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, C, S, "silu", qk_proj=True,
+                       qk_scope=scope)
+    kn, qn = k[0].numpy(), q[0].numpy()
+    for t in range(L):
+        start = (t - t % S) if scope == "shard" else (t - t % C)
+        Mt = sum(np.outer(kn[s], kn[s]) / np.dot(kn[s], kn[s]) for s in range(start, t + 1))
+        np.testing.assert_allclose(o[0, t].numpy(), _np_f(W1[0].numpy(), W2[0].numpy(), Mt @ qn[t], "silu"),
+                                   rtol=1e-12, atol=1e-13)
+
+
+def test_qk_unit_keys_is_linear_memory_prefix():
+    """For unit keys M_t = sum k k^T, a linear memory M'_t = M'_{t-1} + k_t k_t^T
+    (App. B), i.e. the prefix K_{s..t}^T K_{s..t} of a plain matrix product."""
+    rng = np.random.default_rng(9)
+    P, L, d, h, C, S = 1, 16, 4, 6, 4, 8
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h, unit_keys=True)
+    eta = torch.zeros_like(eta)
+    alpha = torch.zeros_like(alpha)
+    o = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, C, S, "gelu", qk_proj=True)
+    kn, qn = k[0].numpy(), q[0].numpy()
+    for t in range(L):
+        s0 = t - t % S
+        Ks = kn[s0:t + 1]
+        np.testing.assert_allclose(o[0, t].numpy(), _np_f(W1[0].numpy(), W2[0].numpy(), (Ks.T @ Ks) @ qn[t], "gelu"),
+                                   rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- reset invariant
+@pytest.mark.parametrize("kind", KINDS)
+def test_shard_isolation(kind):
+    """The reset (Sec. 4.1.1 local update) makes shards independent: running
+    shard s alone on its slice gives the same outputs as the full run."""
+    rng = np.random.default_rng(10)
+    P, d, h, C, S = 2, 4, 6, 4, 12
+    L = 4 * S
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h)
+    full = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, C, S, kind)
+    for s in range(L // S):
+        sl = slice(s * S, (s + 1) * S)
+        alone = O.local_memory(q[:, sl], k[:, sl], v[:, sl], eta[:, sl], beta[:, sl],
+                               alpha[:, sl], W1, W2, C, S, kind)
+        assert (full[:, sl] - alone).abs().max() < 1e-14
+        sub = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, C, S, kind, shards=[s])
+        assert (sub[:, sl] - alone).abs().max() < 1e-14
+
+
+# ---------------------------------------------------------------- the layer
+def _cfg(**kw):
+    base = dict(dtype=F32, act=ACT_GELU, B=1, H=2, L=32, d=4, hid=6, C_G=8,
+                locals_=((4, 16),))
+    base.update(kw)
+    return small_config(**base)
+
+
+def test_output_is_the_sum_of_memories():
+    """o = global + sum of locals (Sec. 4.1.2 box; App. E retrieval rule)."""
+    cfg = _cfg(locals_=((4, 16), (2, 8)))
+    inp = make_inputs(cfg, 11)
+    g = O.gather_pairs(inp, O.all_pairs(cfg))
+    args = [g[n] for n in ("q", "k", "v", "lr", "mom", "decay", "W1", "W2")]
+    full = O.layer_forward(*args, cfg)
+    only_g = O.layer_forward(*args[:3], *[a[:1] for a in args[3:]], cfg.replace(locals_=()))
+    loc = cfg.replace(has_global=0)
+    only_l = O.layer_forward(*args[:3], *[a[1:] for a in args[3:]], loc)
+    assert (full - only_g - only_l).abs().max() < 1e-13
+    l1 = O.layer_forward(*args[:3], *[a[1:2] for a in args[3:]], loc.replace(locals_=((4, 16),)))
+    l2 = O.layer_forward(*args[:3], *[a[2:3] for a in args[3:]], loc.replace(locals_=((2, 8),)))
+    assert (only_l - l1 - l2).abs().max() < 1e-13
+
+
+@pytest.mark.parametrize("act", [ACT_GELU, ACT_SILU])
+@pytest.mark.parametrize("scope", [QK_SHARD, QK_CHUNK])
+def test_backward_gradcheck(act, scope):
+    """Autograd of sum <dO, o> through the oracle matches finite differences
+    for every input (q, k, v, gates of every memory, both inits)."""
+    cfg = _cfg(act=act, qk_scope=scope, H=1, L=8, d=3, hid=4, C_G=4, locals_=((2, 4),))
+    inp = make_inputs(cfg, 12)
+    g = O.gather_pairs(inp, O.all_pairs(cfg))
+    names = ("q", "k", "v", "lr", "mom", "decay", "W1", "W2")
+    leaves = tuple(g[n].clone().requires_grad_(True) for n in names)
+    dO = g["dO"]
+
+    def fn(*xs):
+        return (O.layer_forward(*xs, cfg) * dO).sum()
+
+    assert torch.autograd.gradcheck(fn, leaves, eps=1e-6, atol=1e-7, rtol=1e-6)
+
+
+def test_checkpointed_backward_equals_plain():
+    cfg = _cfg(L=16, C_G=8, locals_=((2, 8),))
+    inp = make_inputs(cfg, 13)
+    g = O.gather_pairs(inp, O.all_pairs(cfg))
+    args = [g[n] for n in ("q", "k", "v", "lr", "mom", "decay", "W1", "W2")]
+    a = O.layer_backward(*args, g["dO"], cfg, ckpt=True)
+    b = O.layer_backward(*args, g["dO"], cfg, ckpt=False)
+    for n in a:
+        assert (a[n] - b[n]).abs().max() <= 1e-12 * max(1.0, b[n].abs().max().item())
+
+
+def test_adjoint_dot_product_identity():
+    """<dO, J delta> = <J^T dO, delta> for a random direction delta, J delta by
+    central differences, at the fp32 smoke shape's sizes (shortened)."""
+    cfg = _cfg(act=ACT_GELU, H=1, L=64, d=16, hid=32, C_G=16, locals_=((8, 32),), norm_v=True)
+    inp = make_inputs(cfg, 14)
+    g = O.gather_pairs(inp, O.all_pairs(cfg))
+    names = ("q", "k", "v", "lr", "mom", "decay", "W1", "W2")
+    x = [g[n] for n in names]
+    grads = O.layer_backward(*x, g["dO"], cfg)
+    gl = [grads[n] for n in ("dq", "dk", "dv", "dlr", "dmom", "ddecay", "dW1", "dW2")]
+    rng = np.random.default_rng(15)
+    delta = [_t(rng.standard_normal(t.shape)) * 1e-3 for t in x]
+    eps = 1e-4
+    with torch.no_grad():
+        fp = O.layer_forward(*[a + eps * dd for a, dd in zip(x, delta)], cfg)
+        fm = O.layer_forward(*[a - eps * dd for a, dd in zip(x, delta)], cfg)
+    lhs = ((fp - fm) / (2 * eps) * g["dO"]).sum().item()
+    rhs = sum((a * dd).sum().item() for a, dd in zip(gl, delta))
+    assert abs(lhs - rhs) <= 1e-7 * max(1.0, abs(rhs)), (lhs, rhs)
+
+
+# ---------------------------------------------------------------- planted mistakes are caught
+def test_planted_mistakes_fail_a_pin(monkeypatch):
+    """A wrong sign in the loss gradient, or retrieval before the update, must
+    break the pins above (checked on the oracle, CPU only)."""
+    rng = np.random.default_rng(16)
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, 1, 12, 3, 4)
+    good = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, 1, 12, "silu")
+    ref, _ = O.sequential(q, k, v, eta, beta, alpha, W1, W2, "silu", reset=12, qk_proj=True)
+    assert (good - ref).abs().max() < 1e-12
+
+    orig = O.inner_grad
+
+    def flipped(W1, W2, k, v, kind):
+        g1, g2 = orig(W1, W2, k, v, kind)
+        return g1, -g2
+
+    monkeypatch.setattr(O.tnt_oracle, "inner_grad", flipped)
+    bad = O.tnt_oracle.local_memory(q, k, v, eta, beta, alpha, W1, W2, 1, 12, "silu")
+    assert (bad - ref).abs().max() > 1e-6
