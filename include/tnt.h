@@ -1,0 +1,141 @@
+/*
+ * tnt.h -- C ABI of the TNT hierarchical memory layer (forward and backward)
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * Method: "TNT: Improving Chunkwise Training for Test-Time Memorization"
+ * (arXiv 2511.07343).  One layer holds one global deep memory (Sec. 4.1.1,
+ * global update equation; App. E) updated in chunks of C_G tokens, and
+ * n_local local deep memories (Sec. 4.1.1, local update equation; App. E),
+ * each updated in chunks of C_L[i] tokens and reset to its learned initial
+ * state every S_L[i] tokens.  Every memory is the MLP f(W, x) = W2 s(W1 x)
+ * (W1: hid x d, W2: d x hid, s = GELU or SiLU) trained at test time by
+ * gradient steps on the recall loss ||f(W, k_t) - v_t||^2 (Sec. 2.1).  All
+ * gradients of a chunk are taken at the chunk-entry weights (Sec. 2.2) and
+ * accumulated with momentum and decay (App. D):
+ *     S_t = mom_t * S_{t-1} - lr_t * u_t,     W_t = (1 - decay_t) * W_{t-1} + S_t.
+ * The output is o_t = f(V_{xi(t,C_G)}, q_t) + sum_i f(W^(i)_t, M^(i)_t q_t)
+ * (Sec. 4.1.2 retrieval box; App. E), where V_{xi(t,C_G)} is the global state
+ * entering t's chunk and M^(i)_t = sum over tau in [shard start, t] of
+ * k_tau k_tau^T / ||k_tau||^2 is the Q-K projection (Sec. 4.1.2; App. C).
+ *
+ * Conventions shared by every entry point
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  The
+ *    library never allocates, frees or synchronises; all work is enqueued on
+ *    `stream` (a hipStream_t; NULL = the default stream) and the call returns
+ *    after the enqueue.  Outputs and gradients are overwritten, never
+ *    accumulated.
+ *  - Layouts are contiguous row-major:
+ *      q, k, v, o, dO, dq, dk, dv : [B][H][L][d]         (dtype: fp32 or bf16)
+ *      lr, mom, decay (and grads) : [M][B][H][L]         (fp32)  eta, beta, alpha
+ *      W1_init, dW1_init          : [M][H][hid][d]       (fp32)
+ *      W2_init, dW2_init          : [M][H][d][hid]       (fp32)
+ *      final_state                : [B][H][4][hid*d]     (fp32) V1 [hid][d], V2 [d][hid],
+ *                                                        S1 [hid][d], S2 [d][hid]
+ *    with M = has_global + n_local memories; memory 0 is the global memory
+ *    when has_global, local memory i is memory has_global + i.  The initial
+ *    weights are per memory and per head, shared by every batch row and every
+ *    shard; their gradients are summed over both.
+ *  - Every pointer must be 16-byte aligned (TNT_ERR_ALIGN otherwise).
+ *  - Validation happens before anything is enqueued; a failing call enqueues
+ *    nothing.  Asynchronous faults surface at the caller's synchronisation.
+ *  - Gates: mom must lie in (0, 1] and decay in [0, 1); logarithms of mom are
+ *    clamped at -80, so mom below e^-80 acts as e^-80.
+ *  - Calls on different streams with distinct workspaces may run
+ *    concurrently; the library keeps no mutable global state apart from one
+ *    lazily created helper stream per device used to overlap the global and
+ *    local memories.
+ */
+#ifndef TNT_H_
+#define TNT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TNT_OK = 0,
+  TNT_ERR_NULL = 1,        /* a required pointer is NULL                      */
+  TNT_ERR_SHAPE = 2,       /* non-positive size or a divisibility rule broken */
+  TNT_ERR_UNSUPPORTED = 3, /* size outside what the kernels are built for     */
+  TNT_ERR_WORKSPACE = 4,   /* workspace smaller than tnt_mem_workspace_size   */
+  TNT_ERR_ALIGN = 5,       /* pointer not 16-byte aligned                     */
+  TNT_ERR_HIP = 6,         /* the HIP runtime reported an error at launch     */
+  TNT_ERR_ARG = 7          /* an enum field holds an unknown value            */
+} tnt_status;
+
+typedef enum { TNT_F32 = 0, TNT_BF16 = 1 } tnt_dtype;       /* dtype of q,k,v,o and their grads */
+typedef enum { TNT_GELU = 0, TNT_SILU = 1 } tnt_act;         /* GELU = exact erf form            */
+typedef enum { TNT_QK_SHARD = 0, TNT_QK_CHUNK = 1 } tnt_qk_scope;
+
+#define TNT_MAX_LOCAL 4
+
+typedef struct {
+  int32_t B, H, L, d, hid; /* batch, heads, sequence length, head dim, MLP hidden width    */
+  int32_t has_global;      /* 1: global memory present (memory 0); 0: locals only          */
+  int32_t C_G;             /* global chunk size; L % C_G == 0                              */
+  int32_t n_local;         /* number of local memories, 0..TNT_MAX_LOCAL                   */
+  int32_t C_L[TNT_MAX_LOCAL]; /* local chunk sizes; S_L[i] % C_L[i] == 0                   */
+  int32_t S_L[TNT_MAX_LOCAL]; /* local shard lengths (reset period); L % S_L[i] == 0       */
+  int32_t act;             /* tnt_act                                                      */
+  int32_t qk_proj;         /* 1: query the locals at M_t q_t (Sec. 4.1.2); 0: at q_t       */
+  int32_t qk_scope;        /* TNT_QK_SHARD: M_t sums from the shard start (App. C);
+                              TNT_QK_CHUNK: from the chunk start (retrieval box literal)    */
+  int32_t dtype;           /* tnt_dtype of q, k, v, o, dO, dq, dk, dv                      */
+} tnt_config;
+
+/* Supported sizes: d in {16, 32, 64, 128}, hid in {16, 32, 64, 128, 256, 512},
+ * C_L in {1..64} (rounded up internally to a multiple of 16 when below 16 is
+ * not a multiple), C_G any divisor of L with C_G >= 1, B*H >= 1. */
+
+/* Which workspace to size. */
+typedef enum {
+  TNT_WS_FWD = 0,          /* tnt_mem_fwd                                       */
+  TNT_WS_BWD = 1,          /* tnt_mem_bwd given the forward's saved buffer     */
+  TNT_WS_BWD_RECOMPUTE = 2 /* tnt_mem_bwd with saved == NULL                   */
+} tnt_ws_kind;
+
+/* Bytes of device workspace the call needs (0 if the config is invalid). */
+size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind);
+
+/* Bytes of the optional saved-state buffer: the chunk-entry states of every
+ * memory, written by tnt_mem_fwd and read by tnt_mem_bwd so that the backward
+ * does not recompute the forward's state chain.  Opaque layout. */
+size_t tnt_mem_saved_size(const tnt_config* cfg);
+
+/* Forward pass: o = TNT layer output (see the file comment).
+ *   final_state : may be NULL; else receives the global memory's (V1, V2, S1, S2)
+ *                 after the last token (requires has_global).
+ *   saved       : may be NULL; else tnt_mem_saved_size bytes that receive the
+ *                 chunk-entry states for a later tnt_mem_bwd.
+ *   workspace   : ws_bytes >= tnt_mem_workspace_size(cfg, TNT_WS_FWD). */
+tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
+                       const float* lr, const float* mom, const float* decay,
+                       const float* W1_init, const float* W2_init, void* o,
+                       float* final_state, void* saved, void* workspace, size_t ws_bytes,
+                       void* stream);
+
+/* Backward pass: gradients of sum(dO * o) with respect to every input of the
+ * forward, exact (second-order terms through the inner gradient included).
+ *   saved : the buffer filled by tnt_mem_fwd on the same inputs, or NULL to
+ *           recompute the states (then ws_bytes must cover TNT_WS_BWD_RECOMPUTE).
+ * dq, dk, dv have the I/O dtype; the others are fp32 in the layouts above. */
+tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
+                       const float* lr, const float* mom, const float* decay,
+                       const float* W1_init, const float* W2_init, const void* dO,
+                       const void* saved, void* dq, void* dk, void* dv, float* dlr,
+                       float* dmom, float* ddecay, float* dW1_init, float* dW2_init,
+                       void* workspace, size_t ws_bytes, void* stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* tnt_strerror(tnt_status status);
+
+/* Version of this ABI (bumped on any incompatible change). */
+int32_t tnt_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TNT_H_ */

@@ -9,8 +9,9 @@ Memorization", arXiv 2511.07343), per (batch, head) chain, in fp64:
 
 * Memory module f(W, x) = W2 sigma(W1 x), W1 in R^{h x d}, W2 in R^{d x h}
   (Sec. 2.1, "deep memory modules"; no bias / residual / norm).
-* Inner loss l(W; k, v) = ||f(W, k) - v||^2 (Sec. 2.1 names MSE as the example)
-  and its gradient u = grad_W l (``inner_grad``).
+* Inner loss l(W; k, v) = (1/d) ||f(W, k) - v||^2, the mean squared error that
+  Sec. 2.1 names, averaged over the d output components, and its gradient
+  u = grad_W l (``inner_grad``).
 * Chunkwise rule (Sec. 2.2, chunkwise compression / retrieval equations): every
   token of a chunk takes its gradient at the chunk-entry state.
 * Momentum and decay (App. D defers the gating to Titans): with u_t taken at
@@ -86,15 +87,15 @@ def memory_fn(W1: torch.Tensor, W2: torch.Tensor, x: torch.Tensor, kind: str) ->
 
 
 def recall_loss(W1, W2, k, v, kind) -> torch.Tensor:
-    """l(W; k, v) = ||f(W, k) - v||^2, summed over the last axis."""
+    """l(W; k, v) = (1/d) ||f(W, k) - v||^2 (mean over the last axis)."""
     e = memory_fn(W1, W2, k, kind) - v
-    return (e * e).sum(-1)
+    return (e * e).mean(-1)
 
 
 def inner_grad(W1, W2, k, v, kind) -> Tuple[torch.Tensor, torch.Tensor]:
-    """u = grad_W ||f(W,k) - v||^2 written out by the chain rule.
+    """u = grad_W (1/d) ||f(W,k) - v||^2 written out by the chain rule.
 
-    z = W1 k, a = sigma(z), y = W2 a, r = 2 (y - v);
+    z = W1 k, a = sigma(z), y = W2 a, r = (2/d) (y - v);
     dl/dW2 = r a^T;  dl/dW1 = ((W2^T r) * sigma'(z)) k^T.
     Leading axes broadcast (W [P,1,h,d] with k [P,C,d] gives one gradient
     per token, all at the same W).
@@ -102,7 +103,7 @@ def inner_grad(W1, W2, k, v, kind) -> Tuple[torch.Tensor, torch.Tensor]:
     z = torch.einsum("...hd,...d->...h", W1, k)
     a = act(z, kind)
     y = torch.einsum("...dh,...h->...d", W2, a)
-    r = 2.0 * (y - v)
+    r = (2.0 / v.shape[-1]) * (y - v)
     g2 = r[..., :, None] * a[..., None, :]
     back = torch.einsum("...dh,...d->...h", W2, r) * act_grad(z, kind)
     g1 = back[..., :, None] * k[..., None, :]

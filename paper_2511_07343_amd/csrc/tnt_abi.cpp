@@ -1,0 +1,274 @@
+// C ABI of the TNT memory layer: validation, workspace layout and the launch
+// sequence of the forward and backward passes.  See include/tnt.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+
+#include "../../include/tnt.h"
+#include "tnt_kernels.h"
+
+using namespace tnt;
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+inline size_t up(size_t x) { return (x + ALIGN - 1) & ~(ALIGN - 1); }
+
+bool one_of(int x, std::initializer_list<int> v) {
+  for (int y : v)
+    if (x == y) return true;
+  return false;
+}
+
+tnt_status validate(const tnt_config* c) {
+  if (!c) return TNT_ERR_NULL;
+  if (c->act < 0 || c->act > 1 || c->qk_proj < 0 || c->qk_proj > 1 || c->qk_scope < 0 ||
+      c->qk_scope > 1 || c->dtype < 0 || c->dtype > 1 || c->has_global < 0 || c->has_global > 1)
+    return TNT_ERR_ARG;
+  if (c->B <= 0 || c->H <= 0 || c->L <= 0 || c->d <= 0 || c->hid <= 0) return TNT_ERR_SHAPE;
+  if (c->n_local < 0 || c->n_local > TNT_MAX_LOCAL) return TNT_ERR_SHAPE;
+  if (c->has_global + c->n_local < 1) return TNT_ERR_SHAPE;
+  if (c->has_global) {
+    if (c->C_G <= 0 || c->L % c->C_G) return TNT_ERR_SHAPE;
+  }
+  for (int i = 0; i < c->n_local; ++i) {
+    if (c->C_L[i] <= 0 || c->S_L[i] <= 0) return TNT_ERR_SHAPE;
+    if (c->S_L[i] % c->C_L[i] || c->L % c->S_L[i]) return TNT_ERR_SHAPE;
+  }
+  if (!one_of(c->d, {16, 32, 64, 128})) return TNT_ERR_UNSUPPORTED;
+  if (!one_of(c->hid, {16, 32, 64, 128, 256, 512})) return TNT_ERR_UNSUPPORTED;
+  for (int i = 0; i < c->n_local; ++i)
+    if (c->C_L[i] > 64) return TNT_ERR_UNSUPPORTED;
+  return TNT_OK;
+}
+
+Dims dims_of(const tnt_config* c, int C, int S) {
+  Dims D{};
+  D.B = c->B; D.H = c->H; D.L = c->L; D.d = c->d; D.hid = c->hid;
+  D.C = C; D.Cp = (C + 15) / 16 * 16; D.S = S;
+  D.act = c->act; D.bf16 = c->dtype == TNT_BF16;
+  D.qk_proj = c->qk_proj; D.qk_scope = c->qk_scope;
+  return D;
+}
+
+// Byte offsets of every buffer.  Offsets are relative to the workspace, or to
+// the saved buffer for the chunk-entry states.
+struct Layout {
+  int M, BH;
+  size_t hd, io_elems, gates;
+  // saved (or workspace-resident) chunk states
+  size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], saved_bytes;
+  int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
+  // forward workspace
+  size_t w_opart, w_tokc, w_chunkc, w_R, w_scr[TNT_MAX_LOCAL], w_ring, fwd_bytes;
+  size_t ring_g, ring_l[TNT_MAX_LOCAL], ring_m[TNT_MAX_LOCAL];
+  LocalPlan lplan[TNT_MAX_LOCAL];
+  // backward workspace
+  size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_adj_l[TNT_MAX_LOCAL],
+      b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL], b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL],
+      b_states, bwd_bytes, bwd_re_bytes;
+  LocalPlan bplan[TNT_MAX_LOCAL];
+};
+
+Layout layout_of(const tnt_config* c) {
+  Layout y{};
+  y.M = c->has_global + c->n_local;
+  y.BH = c->B * c->H;
+  y.hd = (size_t)c->hid * c->d;
+  y.io_elems = (size_t)y.BH * c->L * c->d;
+  y.gates = (size_t)y.BH * c->L;
+  const size_t cts = c->dtype == TNT_BF16 ? 2 : 4;
+  const size_t f = sizeof(float);
+  const size_t dd = (size_t)c->d * c->d;
+
+  // saved states
+  size_t off = 0;
+  if (c->has_global) {
+    y.g_chunks = c->L / c->C_G;
+    y.sv_g = off;
+    off += up((size_t)y.BH * (y.g_chunks + 1) * 4 * y.hd * f);
+  }
+  for (int i = 0; i < c->n_local; ++i) {
+    y.l_units[i] = y.BH * (c->L / c->S_L[i]);
+    y.l_chunks[i] = c->S_L[i] / c->C_L[i];
+    y.sv_l[i] = off;
+    off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * 4 * y.hd * f);
+    y.sv_m[i] = off;
+    off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * dd * f);
+  }
+  y.saved_bytes = off;
+
+  // forward workspace
+  off = 0;
+  y.w_opart = off; off += up((size_t)y.M * y.io_elems * f);
+  if (c->has_global) {
+    y.w_tokc = off; off += up(y.gates * 4 * f);
+    y.w_chunkc = off; off += up((size_t)y.BH * y.g_chunks * 4 * f);
+    y.w_R = off; off += up((size_t)y.BH * c->C_G * c->d * f);
+  }
+  for (int i = 0; i < c->n_local; ++i) {
+    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+    local_plan(D, &y.lplan[i], false);
+    y.w_scr[i] = off; off += up((size_t)y.l_units[i] * y.lplan[i].elems * cts);
+  }
+  const size_t fwd_core = off;
+  // two-slot state rings, used when no saved buffer is given
+  y.w_ring = off;
+  if (c->has_global) { y.ring_g = off; off += up((size_t)y.BH * 2 * 4 * y.hd * f); }
+  for (int i = 0; i < c->n_local; ++i) {
+    y.ring_l[i] = off; off += up((size_t)y.l_units[i] * 2 * 4 * y.hd * f);
+    y.ring_m[i] = off; off += up((size_t)y.l_units[i] * 2 * dd * f);
+  }
+  y.fwd_bytes = off;
+  (void)fwd_core;
+
+  // backward workspace (shares the forward's front part for recomputation)
+  off = y.fwd_bytes;
+  y.b_dparts = off; off += up(3 * (size_t)y.M * y.io_elems * f);
+  if (c->has_global) {
+    y.b_adj_g = off; off += up((size_t)y.BH * 2 * 4 * y.hd * f);
+    y.b_dR = off; off += up((size_t)y.BH * c->C_G * c->d * f);
+    y.b_dtok = off; off += up(y.gates * 4 * f);
+    y.b_dchunk = off; off += up((size_t)y.BH * y.g_chunks * (c->hid / 16) * 4 * f);
+    y.b_dWg = off; off += up((size_t)y.BH * 2 * y.hd * f);
+  }
+  for (int i = 0; i < c->n_local; ++i) {
+    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+    local_plan(D, &y.bplan[i], true);
+    y.b_adj_l[i] = off; off += up((size_t)y.l_units[i] * 4 * y.hd * f);
+    y.b_madj[i] = off; off += up((size_t)y.l_units[i] * 2 * dd * f);
+    y.b_dWl[i] = off; off += up((size_t)y.l_units[i] * 2 * y.hd * f);
+    y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.bplan[i].elems * cts);
+    y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.bplan[i].f32_elems * f);
+  }
+  y.bwd_bytes = off;
+  y.b_states = off;
+  y.bwd_re_bytes = off + y.saved_bytes;
+  return y;
+}
+
+bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
+#define HIP_TRY(x)                         \
+  do {                                     \
+    if ((x) != hipSuccess) return TNT_ERR_HIP; \
+  } while (0)
+
+// forward pass into a given state area (`sv` = saved buffer, or nullptr to use
+// the two-slot rings in the workspace)
+tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, const void* k,
+                       const void* v, const float* lr, const float* mom, const float* decay,
+                       const float* W1i, const float* W2i, void* o, float* final_state,
+                       char* sv, char* ws, hipStream_t st) {
+  const size_t G = y.gates;
+  float* opart = (float*)(ws + y.w_opart);
+  int m = 0;
+  if (c->has_global) {
+    GlobalArgs g{};
+    g.q = q; g.k = k; g.v = v;
+    g.lr = lr; g.mom = mom; g.decay = decay;
+    g.W1i = W1i; g.W2i = W2i;
+    g.o_part = opart;
+    g.states = sv ? (float*)(sv + y.sv_g) : (float*)(ws + y.ring_g);
+    g.nslots = sv ? y.g_chunks + 1 : 2;
+    g.tokc = (float*)(ws + y.w_tokc);
+    g.chunkc = (float*)(ws + y.w_chunkc);
+    g.Rbuf = (float*)(ws + y.w_R);
+    g.D = dims_of(c, c->C_G, c->L);
+    HIP_TRY(launch_global_scan(g, st));
+    HIP_TRY(launch_global_init(g, st));
+    for (int n = 0; n < y.g_chunks; ++n) HIP_TRY(launch_global_fwd_chunk(g, n, st));
+    if (final_state)
+      HIP_TRY(launch_copy_final(g.states, g.nslots, y.BH, 4 * y.hd, y.g_chunks % g.nslots,
+                                final_state, st));
+    m = 1;
+  }
+  for (int i = 0; i < c->n_local; ++i, ++m) {
+    LocalFwdArgs a{};
+    a.q = q; a.k = k; a.v = v;
+    a.lr = lr + m * G; a.mom = mom + m * G; a.decay = decay + m * G;
+    a.W1i = W1i + (size_t)m * c->H * y.hd;
+    a.W2i = W2i + (size_t)m * c->H * y.hd;
+    a.o_part = opart + (size_t)m * y.io_elems;
+    a.states = sv ? (float*)(sv + y.sv_l[i]) : (float*)(ws + y.ring_l[i]);
+    a.mstates = sv ? (float*)(sv + y.sv_m[i]) : (float*)(ws + y.ring_m[i]);
+    a.nslots = sv ? y.l_chunks[i] + 1 : 2;
+    a.scratch = ws + y.w_scr[i];
+    a.plan = y.lplan[i];
+    a.D = dims_of(c, c->C_L[i], c->S_L[i]);
+    HIP_TRY(launch_local_fwd(a, y.l_units[i], st));
+  }
+  if (o) HIP_TRY(launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, c->dtype == TNT_BF16, st));
+  return TNT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t tnt_abi_version(void) { return 1; }
+
+const char* tnt_strerror(tnt_status s) {
+  switch (s) {
+    case TNT_OK: return "ok";
+    case TNT_ERR_NULL: return "null pointer";
+    case TNT_ERR_SHAPE: return "invalid shape or divisibility";
+    case TNT_ERR_UNSUPPORTED: return "unsupported size";
+    case TNT_ERR_WORKSPACE: return "workspace too small";
+    case TNT_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case TNT_ERR_HIP: return "HIP runtime error";
+    case TNT_ERR_ARG: return "invalid enum argument";
+  }
+  return "unknown status";
+}
+
+size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind) {
+  if (validate(cfg) != TNT_OK) return 0;
+  const Layout y = layout_of(cfg);
+  if (kind == TNT_WS_FWD) return y.fwd_bytes;
+  if (kind == TNT_WS_BWD) return y.bwd_bytes;
+  if (kind == TNT_WS_BWD_RECOMPUTE) return y.bwd_re_bytes;
+  return 0;
+}
+
+size_t tnt_mem_saved_size(const tnt_config* cfg) {
+  if (validate(cfg) != TNT_OK) return 0;
+  return layout_of(cfg).saved_bytes;
+}
+
+tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
+                       const float* lr, const float* mom, const float* decay,
+                       const float* W1_init, const float* W2_init, void* o, float* final_state,
+                       void* saved, void* workspace, size_t ws_bytes, void* stream) {
+  tnt_status s = validate(cfg);
+  if (s != TNT_OK) return s;
+  if (!q || !k || !v || !lr || !mom || !decay || !W1_init || !W2_init || !o || !workspace)
+    return TNT_ERR_NULL;
+  if (final_state && !cfg->has_global) return TNT_ERR_SHAPE;
+  for (const void* p : {(const void*)q, (const void*)k, (const void*)v, (const void*)lr,
+                        (const void*)mom, (const void*)decay, (const void*)W1_init,
+                        (const void*)W2_init, (const void*)o, (const void*)final_state,
+                        (const void*)saved, (const void*)workspace})
+    if (p && misaligned(p)) return TNT_ERR_ALIGN;
+  const Layout y = layout_of(cfg);
+  if (ws_bytes < y.fwd_bytes) return TNT_ERR_WORKSPACE;
+  return run_forward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
+                     (char*)saved, (char*)workspace, (hipStream_t)stream);
+}
+
+tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
+                       const float* lr, const float* mom, const float* decay,
+                       const float* W1_init, const float* W2_init, const void* dO,
+                       const void* saved, void* dq, void* dk, void* dv, float* dlr, float* dmom,
+                       float* ddecay, float* dW1_init, float* dW2_init, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  tnt_status s = validate(cfg);
+  if (s != TNT_OK) return s;
+  (void)q; (void)k; (void)v; (void)lr; (void)mom; (void)decay; (void)W1_init; (void)W2_init;
+  (void)dO; (void)saved; (void)dq; (void)dk; (void)dv; (void)dlr; (void)dmom; (void)ddecay;
+  (void)dW1_init; (void)dW2_init; (void)workspace; (void)ws_bytes; (void)stream;
+  return TNT_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,217 @@
+// Device-side building blocks of the TNT memory-layer kernels (gfx950).
+//
+//  * 16x16 MFMA output tiles: bf16 operands (v_mfma_f32_16x16x32_bf16, K step
+//    32, K tails of 16 zero-filled) or fp32 operands (v_mfma_f32_16x16x4f32),
+//    always accumulating in fp32.  Operands are read through plain pointers
+//    (LDS or global), converted to the compute type on load, optionally scaled
+//    per contraction index.
+//  * Lane layout (checked on gfx950): for a 16x16 output tile, lane l holds
+//    rows 4*(l/16)+r, r = 0..3, of column l%16.  The bf16 A operand of lane l
+//    is A[l%16][k0 + 8*(l/16) + j], j = 0..7, and B[k0 + 8*(l/16) + j][l%16];
+//    the fp32 form takes A[l%16][k0 + l/16] and B[k0 + l/16][l%16].
+//  * Activations (exact-erf GELU, SiLU) with first and second derivatives.
+//  * Wavefront prefix scans over 64 lanes.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tnt {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int WAVE = 64;
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+__device__ __forceinline__ int num_waves() { return blockDim.x / WAVE; }
+
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(__bf16 x) { return (float)x; }
+template <typename T> __device__ __forceinline__ T from_f(float x);
+template <> __device__ __forceinline__ float from_f<float>(float x) { return x; }
+template <> __device__ __forceinline__ __bf16 from_f<__bf16>(float x) { return (__bf16)x; }
+
+// ----------------------------------------------------------------------------
+// activation sigma and its derivatives (GELU exact erf form, or SiLU)
+// ----------------------------------------------------------------------------
+enum { ACT_GELU = 0, ACT_SILU = 1 };
+
+struct ActVals { float s, d1, d2; };  // sigma(z), sigma'(z), sigma''(z)
+
+template <int ACT>
+__device__ __forceinline__ float act_f(float z) {
+  if (ACT == ACT_GELU) return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+  float sg = 1.0f / (1.0f + expf(-z));
+  return z * sg;
+}
+
+template <int ACT>
+__device__ __forceinline__ ActVals act_all(float z) {
+  ActVals r;
+  if (ACT == ACT_GELU) {
+    float cdf = 0.5f * (1.0f + erff(z * 0.70710678118654752f));
+    float pdf = 0.39894228040143268f * expf(-0.5f * z * z);
+    r.s = z * cdf;
+    r.d1 = cdf + z * pdf;
+    r.d2 = pdf * (2.0f - z * z);
+  } else {
+    float sg = 1.0f / (1.0f + expf(-z));
+    r.s = z * sg;
+    r.d1 = sg * (1.0f + z * (1.0f - sg));
+    r.d2 = sg * (1.0f - sg) * (2.0f + z * (1.0f - 2.0f * sg));
+  }
+  return r;
+}
+
+// ----------------------------------------------------------------------------
+// MFMA tiles
+// ----------------------------------------------------------------------------
+// Operand layouts.  For A (logical M x K):  KC: A[i*ld + k];  MC: A[k*ld + i].
+//                   For B (logical K x N):  KC: B[j*ld + k];  MC: B[k*ld + j].
+// "KC" keeps the contraction index contiguous, which is what an MFMA lane
+// wants; "MC" is the transposed storage.
+enum { KC = 0, MC = 1 };
+
+template <typename CT> struct Mma;
+
+template <> struct Mma<__bf16> {
+  static constexpr int KS = 32;
+  typedef bf16x8 frag;
+  // 8 consecutive-k elements of row/col `idx` starting at k = kb, zero past K.
+  template <int LAY, typename E>
+  __device__ __forceinline__ static frag load(const E* p, int ld, int idx, int kb, int K,
+                                              const float* kscale) {
+    frag f;
+    if (kb >= K) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[j] = (__bf16)0.0f;
+      return f;
+    }
+    if (LAY == KC) {
+      const E* q = p + (size_t)idx * ld + kb;
+      if (sizeof(E) == 2) {
+        // 16-byte vector load (callers keep ld and kb multiples of 8)
+        f = *reinterpret_cast<const bf16x8*>(q);
+        if (kscale) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) f[j] = (__bf16)((float)f[j] * kscale[kb + j]);
+        }
+      } else {
+        f32x4 a = *reinterpret_cast<const f32x4*>(q);
+        f32x4 b = *reinterpret_cast<const f32x4*>(q + 4);
+        float t[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = (__bf16)(kscale ? t[j] * kscale[kb + j] : t[j]);
+      }
+    } else {
+      const E* q = p + (size_t)kb * ld + idx;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float x = to_f(q[(size_t)j * ld]);
+        f[j] = (__bf16)(kscale ? x * kscale[kb + j] : x);
+      }
+    }
+    return f;
+  }
+  __device__ __forceinline__ static void mma(f4& acc, const frag& a, const frag& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+  }
+  __device__ __forceinline__ static int kofs(int lane) { return 8 * (lane >> 4); }
+};
+
+template <> struct Mma<float> {
+  static constexpr int KS = 4;
+  typedef float frag;
+  template <int LAY, typename E>
+  __device__ __forceinline__ static frag load(const E* p, int ld, int idx, int kb, int K,
+                                              const float* kscale) {
+    if (kb >= K) return 0.0f;
+    float x = (LAY == KC) ? to_f(p[(size_t)idx * ld + kb]) : to_f(p[(size_t)kb * ld + idx]);
+    return kscale ? x * kscale[kb] : x;
+  }
+  __device__ __forceinline__ static void mma(f4& acc, const frag& a, const frag& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+  }
+  __device__ __forceinline__ static int kofs(int lane) { return lane >> 4; }
+};
+
+// acc += A[i0:i0+16, 0:K] * B[0:K, j0:j0+16]; K a multiple of 16 (bf16) or 4 (fp32).
+// kscale (optional, length K) multiplies the contraction index.
+template <typename CT, int LA, int LB, typename EA, typename EB>
+__device__ __forceinline__ void mma_tile(f4& acc, const EA* A, int lda, int i0, const EB* B,
+                                         int ldb, int j0, int K, const float* kscale = nullptr) {
+  const int l = lane_id();
+  const int ko = Mma<CT>::kofs(l);
+  const int ia = i0 + (l & 15), jb = j0 + (l & 15);
+  for (int k0 = 0; k0 < K; k0 += Mma<CT>::KS) {
+    auto a = Mma<CT>::template load<LA>(A, lda, ia, k0 + ko, K, kscale);
+    auto b = Mma<CT>::template load<LB>(B, ldb, jb, k0 + ko, K, nullptr);
+    Mma<CT>::mma(acc, a, b);
+  }
+}
+
+__device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
+
+// visit the 4 elements a lane holds of the 16x16 tile at (i0, j0)
+template <typename F>
+__device__ __forceinline__ void tile_each(const f4& acc, int i0, int j0, F&& f) {
+  const int l = lane_id();
+  const int col = j0 + (l & 15);
+  const int row = i0 + 4 * (l >> 4);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) f(row + r, col, acc[r]);
+}
+
+// Block-wide GEMM over 16x16 output tiles distributed round-robin to waves:
+// out(i, j) = sum_k A(i, k) B(k, j), passed to epi(i, j, value).
+template <typename CT, int LA, int LB, typename EA, typename EB, typename Epi>
+__device__ __forceinline__ void gemm(int M, int N, int K, const EA* A, int lda, const EB* B,
+                                     int ldb, Epi&& epi, const float* kscale = nullptr) {
+  const int tn = N >> 4, nt = (M >> 4) * tn;
+  for (int t = wave_id(); t < nt; t += num_waves()) {
+    const int i0 = (t / tn) << 4, j0 = (t % tn) << 4;
+    f4 acc = zero4();
+    mma_tile<CT, LA, LB>(acc, A, lda, i0, B, ldb, j0, K, kscale);
+    tile_each(acc, i0, j0, epi);
+  }
+}
+
+// ----------------------------------------------------------------------------
+// wavefront scans (64 lanes)
+// ----------------------------------------------------------------------------
+__device__ __forceinline__ float wave_incl_sum(float x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    float y = __shfl_up(x, o, WAVE);
+    if (l >= o) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = WAVE / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, WAVE);
+  return x;
+}
+
+// Block-wide sum; `red` is LDS scratch of at least num_waves() floats.
+__device__ __forceinline__ float block_sum(float x, float* red) {
+  x = wave_sum(x);
+  __syncthreads();
+  if (lane_id() == 0) red[wave_id()] = x;
+  __syncthreads();
+  float t = 0.f;
+  for (int w = 0; w < num_waves(); ++w) t += red[w];
+  __syncthreads();
+  return t;
+}
+
+constexpr float LOG_CLAMP = -80.0f;
+__device__ __forceinline__ float log_mom(float beta) { return fmaxf(logf(beta), LOG_CLAMP); }
+__device__ __forceinline__ float log_keep(float alpha) { return log1pf(-alpha); }
+
+}  // namespace tnt

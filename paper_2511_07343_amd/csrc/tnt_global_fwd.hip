@@ -1,0 +1,337 @@
+// Global memory, forward (global update rule, Sec. 4.1.1 box; App. E) and the
+// small helpers of the layer (output sum, init-gradient reduction).
+//
+// The global memory is one sequential chain per (batch row, head) over L/C_G
+// chunks.  Inside a chunk nothing is sequential: retrieval reads the
+// chunk-entry state V_{xi(t,C_G)} (Sec. 4.1.2 retrieval box) and every
+// gradient is taken at that state, so each chunk runs as
+//   scan  : gate coefficients of every chunk at once (inputs only)
+//   phase1: token tiles -> O_G = s(Q V1^T) V2^T and R = (2/d) (s(K V1^T) V2^T - V)
+//   phase2: hidden slices -> V1' = A_C V1 + E_C S1 - D1^T diag(cC) K,
+//           S1' = B_C S1 - D1^T diag(b) K (V2', S2' alike with R^T, Hk), where
+//           the slice's Hk and D1 = (R V2) * s'(K V1^T) are recomputed from R.
+#include "tnt_device.h"
+#include "tnt_kernels.h"
+
+namespace tnt {
+
+// ---------------------------------------------------------------------------
+// gate coefficients of a global chunk (one wavefront per (chunk, chain)).
+// tokc[t] = {cC_t, b_t, la_t, lb_t}; chunkc[n] = {A_C, B_C, E_C, 0} with
+//   cC_t = eta_t s_t,  s_t = sum_{m>=t} e^{la_C - la_m + lb_m - lb_t}
+//        = e^{la_C - la_t} + beta_{t+1} s_{t+1}          (suffix affine scan)
+//   b_t  = eta_t e^{lb_C - lb_t},  E_C = beta_0 s_0.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
+  const int n = blockIdx.x, chain = blockIdx.y;
+  const int C = a.D.C, L = a.D.L;
+  const size_t base = (size_t)chain * L + (size_t)n * C;
+  const float* lr = a.lr + base;
+  const float* mom = a.mom + base;
+  const float* dec = a.decay + base;
+  float* tk = a.tokc + base * 4;
+  const int l = lane_id();
+  const int E = (C + WAVE - 1) / WAVE;
+  const int i0 = min(l * E, C), i1 = min(i0 + E, C);
+  float sa = 0.f, sb = 0.f;
+  for (int i = i0; i < i1; ++i) {
+    sa += log_keep(dec[i]);
+    sb += log_mom(mom[i]);
+  }
+  const float ia = wave_incl_sum(sa), ib = wave_incl_sum(sb);
+  const float laC = __shfl(ia, WAVE - 1, WAVE), lbC = __shfl(ib, WAVE - 1, WAVE);
+  float pa = ia - sa, pb = ib - sb;
+  for (int i = i0; i < i1; ++i) {
+    pa += log_keep(dec[i]);
+    pb += log_mom(mom[i]);
+    tk[(size_t)i * 4 + 2] = pa;
+    tk[(size_t)i * 4 + 3] = pb;
+  }
+  // segment affine map s_{i0} = P s_{i1} + Q (own writes are visible to the lane)
+  float P = 1.f, Q = 0.f;
+  for (int i = i1 - 1; i >= i0; --i) {
+    const float ai = expf(laC - tk[(size_t)i * 4 + 2]);
+    const float mi = (i + 1 < C) ? mom[i + 1] : 0.f;
+    Q = ai + mi * Q;
+    P = mi * P;
+  }
+  // suffix composition over lanes: G_l = F_l o F_{l+1} o ... o F_63
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    const float Po = __shfl_down(P, o, WAVE), Qo = __shfl_down(Q, o, WAVE);
+    if (l + o < WAVE) {
+      Q = P * Qo + Q;
+      P = P * Po;
+    }
+  }
+  float sin = __shfl_down(Q, 1, WAVE);  // s at the first token of the next segment
+  if (l == WAVE - 1) sin = 0.f;
+  float sv = sin;
+  for (int i = i1 - 1; i >= i0; --i) {
+    const float ai = expf(laC - tk[(size_t)i * 4 + 2]);
+    const float mi = (i + 1 < C) ? mom[i + 1] : 0.f;
+    sv = ai + mi * sv;
+    tk[(size_t)i * 4 + 0] = lr[i] * sv;
+    tk[(size_t)i * 4 + 1] = lr[i] * expf(lbC - tk[(size_t)i * 4 + 3]);
+  }
+  if (l == 0) {
+    float* cc = a.chunkc + ((size_t)chain * (L / C) + n) * 4;
+    cc[0] = expf(laC);
+    cc[1] = expf(lbC);
+    cc[2] = (C > 0 ? mom[0] : 0.f) * sv;  // lane 0 ends at i = 0: sv = s_0
+    cc[3] = 0.f;
+  }
+}
+
+hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st) {
+  dim3 grid(a.D.L / a.D.C, a.D.B * a.D.H);
+  hipLaunchKernelGGL(global_scan_kernel, grid, dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+// slot 0 of every chain = (W1_init, W2_init, 0, 0)
+__global__ void global_init_kernel(GlobalArgs a) {
+  const int chain = blockIdx.y;
+  const int hh = chain % a.D.H;
+  const size_t hd = (size_t)a.D.hid * a.D.d;
+  float* st = a.states + (size_t)chain * a.nslots * 4 * hd;
+  for (size_t e = blockIdx.x * blockDim.x + threadIdx.x; e < hd; e += gridDim.x * blockDim.x) {
+    st[e] = a.W1i[hh * hd + e];
+    st[hd + e] = a.W2i[hh * hd + e];
+    st[2 * hd + e] = 0.f;
+    st[3 * hd + e] = 0.f;
+  }
+}
+
+hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(global_init_kernel, dim3(16, a.D.B * a.D.H), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+// token-tile rows per phase-1 workgroup, chosen so the tile fits in LDS
+static int g1_rows(const Dims& D) {
+  const size_t cts = D.bf16 ? 2 : 4;
+  for (int tt = 64; tt > 16; tt >>= 1)
+    if ((2 * (size_t)tt * D.d + (size_t)tt * D.hid) * cts <= 96 * 1024) return tt;
+  return 16;
+}
+
+// ---- phase 1: retrieval at the chunk-entry state and R = (2/d) (f(V, k) - v)
+template <typename IO, typename CT, int ACT>
+__global__ void __launch_bounds__(256) global_p1_kernel(GlobalArgs a, int n, int TT) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const Dims D = a.D;
+  const int d = D.d, h = D.hid, C = D.C;
+  const int chain = blockIdx.y;
+  const int r0 = blockIdx.x * TT;                 // first row of the tile inside the chunk
+  const int rows = min(TT, C - r0);
+  const size_t hd = (size_t)h * d;
+  const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
+  const float *V1 = V, *V2 = V + hd;
+  CT* sQ = (CT*)smem;
+  CT* sK = sQ + (size_t)TT * d;
+  CT* sH = sK + (size_t)TT * d;
+  const size_t tok0 = (size_t)n * C + r0;
+  const IO* q = (const IO*)a.q + ((size_t)chain * D.L + tok0) * d;
+  const IO* k = (const IO*)a.k + ((size_t)chain * D.L + tok0) * d;
+  const IO* v = (const IO*)a.v + ((size_t)chain * D.L + tok0) * d;
+  float* o = a.o_part + ((size_t)chain * D.L + tok0) * d;
+  float* R = a.Rbuf + ((size_t)chain * C + r0) * d;
+  const float rscale = 2.0f / (float)d;  // d(1/d ||y - v||^2)/dy
+  for (int e = threadIdx.x; e < TT * d; e += blockDim.x) {
+    const int i = e / d;
+    sQ[e] = from_f<CT>(i < rows ? to_f(q[e]) : 0.f);
+    sK[e] = from_f<CT>(i < rows ? to_f(k[e]) : 0.f);
+  }
+  __syncthreads();
+  gemm<CT, KC, KC>(TT, h, d, sQ, d, V1, d, [&](int i, int j, float z) {
+    sH[(size_t)i * h + j] = from_f<CT>(act_f<ACT>(z));
+  });
+  __syncthreads();
+  gemm<CT, KC, KC>(TT, d, h, sH, h, V2, h, [&](int i, int j, float x) {
+    if (i < rows) o[(size_t)i * d + j] = x;
+  });
+  __syncthreads();
+  gemm<CT, KC, KC>(TT, h, d, sK, d, V1, d, [&](int i, int j, float z) {
+    sH[(size_t)i * h + j] = from_f<CT>(act_f<ACT>(z));
+  });
+  __syncthreads();
+  gemm<CT, KC, KC>(TT, d, h, sH, h, V2, h, [&](int i, int j, float y) {
+    if (i < rows) R[(size_t)i * d + j] = rscale * (y - to_f(v[(size_t)i * d + j]));
+  });
+}
+
+// ---- phase 2: the carry, one hidden slice of 16 rows per workgroup
+constexpr int G2_HS = 16;
+
+static int g2_rows(const Dims& D) {
+  const size_t cts = D.bf16 ? 2 : 4;
+  for (int tt = 64; tt > 16; tt >>= 1)
+    if ((6 * (size_t)tt * D.d + 2 * (size_t)G2_HS * tt) * cts <= 112 * 1024) return tt;
+  return 16;
+}
+
+template <typename IO, typename CT, int ACT>
+__global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int TT) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const Dims D = a.D;
+  const int d = D.d, h = D.hid, C = D.C;
+  const int chain = blockIdx.y;
+  const int s0 = blockIdx.x * G2_HS;
+  const size_t hd = (size_t)h * d;
+  const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
+  float* Vn = a.states + ((size_t)chain * a.nslots + ((n + 1) % a.nslots)) * 4 * hd;
+  const float *V1 = V, *V2 = V + hd, *S1 = V + 2 * hd, *S2 = V + 3 * hd;
+  constexpr int HS = G2_HS;
+  CT* sK = (CT*)smem;                 // [TT][d]
+  CT* sR = sK + TT * d;               // [TT][d]
+  CT* sKcT = sR + TT * d;             // [d][TT]
+  CT* sKbT = sKcT + d * TT;
+  CT* sRcT = sKbT + d * TT;
+  CT* sRbT = sRcT + d * TT;
+  CT* sHkT = sRbT + d * TT;           // [HS][TT]
+  CT* sD1T = sHkT + HS * TT;          // [HS][TT]
+  const size_t tokc0 = (size_t)chain * D.L + (size_t)n * C;
+  const float* tk = a.tokc + tokc0 * 4;
+  const IO* kk = (const IO*)a.k + tokc0 * d;
+  const float* Rb = a.Rbuf + (size_t)chain * C * d;
+
+  // persistent accumulators: V1/S1 slice (HS x d) and V2/S2 slice (d x HS)
+  const int nt1 = d >> 4;  // tiles of the (HS x d) slice; the (d x HS) slice has as many
+  f4 aw1[2], as1[2], aw2[2], as2[2];
+  for (int x = 0; x < 2; ++x) aw1[x] = as1[x] = aw2[x] = as2[x] = zero4();
+
+  for (int r0 = 0; r0 < C; r0 += TT) {
+    const int rows = min(TT, C - r0);
+    for (int e = threadIdx.x; e < TT * d; e += blockDim.x) {
+      const int i = e / d, j = e - i * d;
+      const bool in = i < rows;
+      const float kx = in ? to_f(kk[(size_t)(r0 + i) * d + j]) : 0.f;
+      const float rx = in ? Rb[(size_t)(r0 + i) * d + j] : 0.f;
+      const float cc = in ? tk[(size_t)(r0 + i) * 4 + 0] : 0.f;
+      const float bb = in ? tk[(size_t)(r0 + i) * 4 + 1] : 0.f;
+      sK[e] = from_f<CT>(kx);
+      sR[e] = from_f<CT>(rx);
+      sKcT[(size_t)j * TT + i] = from_f<CT>(cc * kx);
+      sKbT[(size_t)j * TT + i] = from_f<CT>(bb * kx);
+      sRcT[(size_t)j * TT + i] = from_f<CT>(cc * rx);
+      sRbT[(size_t)j * TT + i] = from_f<CT>(bb * rx);
+    }
+    __syncthreads();
+    // Zk and G for the slice: TT x HS, two accumulators per tile
+    for (int t = wave_id(); t < TT / 16; t += num_waves()) {
+      const int i0 = t * 16;
+      f4 az = zero4(), ag = zero4();
+      mma_tile<CT, KC, KC>(az, sK, d, i0, V1 + (size_t)s0 * d, d, 0, d);
+      mma_tile<CT, KC, MC>(ag, sR, d, i0, V2 + s0, h, 0, d);
+      const int l = lane_id();
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = i0 + 4 * (l >> 4) + r, j = l & 15;
+        const ActVals av = act_all<ACT>(az[r]);
+        sHkT[(size_t)j * TT + i] = from_f<CT>(av.s);
+        sD1T[(size_t)j * TT + i] = from_f<CT>(ag[r] * av.d1);
+      }
+    }
+    __syncthreads();
+    for (int x = 0, t = wave_id(); t < nt1; t += num_waves(), ++x) {
+      const int j0 = t * 16;
+      mma_tile<CT, KC, KC>(aw1[x], sD1T, TT, 0, sKcT, TT, j0, TT);
+      mma_tile<CT, KC, KC>(as1[x], sD1T, TT, 0, sKbT, TT, j0, TT);
+      mma_tile<CT, KC, KC>(aw2[x], sRcT, TT, j0, sHkT, TT, 0, TT);
+      mma_tile<CT, KC, KC>(as2[x], sRbT, TT, j0, sHkT, TT, 0, TT);
+    }
+    __syncthreads();
+  }
+  const float* cc = a.chunkc + ((size_t)chain * (D.L / C) + n) * 4;
+  const float AC = cc[0], BC = cc[1], EC = cc[2];
+  const int l = lane_id();
+  for (int x = 0, t = wave_id(); t < nt1; t += num_waves(), ++x) {
+    const int j0 = t * 16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      {  // V1 / S1 slice element (s0 + i, j)
+        const int i = 4 * (l >> 4) + r, j = j0 + (l & 15);
+        const size_t e = (size_t)(s0 + i) * d + j;
+        Vn[e] = AC * V1[e] + EC * S1[e] - aw1[x][r];
+        Vn[2 * hd + e] = BC * S1[e] - as1[x][r];
+      }
+      {  // V2 / S2 slice element (j0 + row, s0 + col)
+        const int i = j0 + 4 * (l >> 4) + r, j = l & 15;
+        const size_t e = (size_t)i * h + s0 + j;
+        Vn[hd + e] = AC * V2[e] + EC * S2[e] - aw2[x][r];
+        Vn[3 * hd + e] = BC * S2[e] - as2[x][r];
+      }
+    }
+  }
+}
+
+template <typename IO, typename CT, int ACT>
+static hipError_t launch_gfwd_t(const GlobalArgs& a, int n, hipStream_t st) {
+  const Dims& D = a.D;
+  const int TT = g1_rows(D);
+  const size_t cts = sizeof(CT);
+  dim3 g1((D.C + TT - 1) / TT, D.B * D.H);
+  const size_t l1 = (2 * (size_t)TT * D.d + (size_t)TT * D.hid) * cts;
+  set_lds_limit((const void*)global_p1_kernel<IO, CT, ACT>);
+  hipLaunchKernelGGL((global_p1_kernel<IO, CT, ACT>), g1, dim3(256), l1, st, a, n, TT);
+  const int T2 = g2_rows(D);
+  dim3 g2(D.hid / G2_HS, D.B * D.H);
+  const size_t l2 = (6 * (size_t)T2 * D.d + 2 * (size_t)G2_HS * T2) * cts;
+  set_lds_limit((const void*)global_p2_kernel<IO, CT, ACT>);
+  hipLaunchKernelGGL((global_p2_kernel<IO, CT, ACT>), g2, dim3(256), l2, st, a, n, T2);
+  return hipGetLastError();
+}
+
+hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {
+  if (a.D.bf16)
+    return a.D.act == ACT_GELU ? launch_gfwd_t<__bf16, __bf16, ACT_GELU>(a, n, st)
+                               : launch_gfwd_t<__bf16, __bf16, ACT_SILU>(a, n, st);
+  return a.D.act == ACT_GELU ? launch_gfwd_t<float, float, ACT_GELU>(a, n, st)
+                             : launch_gfwd_t<float, float, ACT_SILU>(a, n, st);
+}
+
+// ---------------------------------------------------------------------------
+// o = sum of the per-memory fp32 partials, written in the I/O dtype
+// ---------------------------------------------------------------------------
+template <typename IO>
+__global__ void sum_out_kernel(const float* parts, int nparts, size_t stride, size_t n, IO* out) {
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+       e += (size_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    for (int p = 0; p < nparts; ++p) s += parts[p * stride + e];
+    out[e] = from_f<IO>(s);
+  }
+}
+
+hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
+                          int bf16, hipStream_t st) {
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 8192);
+  if (bf16)
+    hipLaunchKernelGGL(sum_out_kernel<__bf16>, dim3(blocks), dim3(256), 0, st, parts, nparts,
+                       stride, n, (__bf16*)out);
+  else
+    hipLaunchKernelGGL(sum_out_kernel<float>, dim3(blocks), dim3(256), 0, st, parts, nparts,
+                       stride, n, (float*)out);
+  return hipGetLastError();
+}
+
+// final global state (slot `last`) -> [B*H][4][hid*d]
+__global__ void copy_final_kernel(const float* states, int nslots, size_t slot_elems, int last,
+                                  float* out) {
+  const int chain = blockIdx.y;
+  const float* src = states + ((size_t)chain * nslots + last) * slot_elems;
+  float* dst = out + (size_t)chain * slot_elems;
+  for (size_t e = blockIdx.x * blockDim.x + threadIdx.x; e < slot_elems;
+       e += gridDim.x * blockDim.x)
+    dst[e] = src[e];
+}
+
+hipError_t launch_copy_final(const float* states, int nslots, int nchains, size_t slot_elems,
+                             int last, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(copy_final_kernel, dim3(32, nchains), dim3(256), 0, st, states, nslots,
+                     slot_elems, last, out);
+  return hipGetLastError();
+}
+
+}  // namespace tnt

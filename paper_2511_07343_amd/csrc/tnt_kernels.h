@@ -1,0 +1,109 @@
+// Kernel argument blocks and host-side launchers shared by the C ABI and the
+// kernel translation units.  Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tnt {
+
+// Sizes of one memory's pass, shared by every kernel.
+struct Dims {
+  int B, H, L, d, hid;
+  int C;      // chunk size of this memory
+  int Cp;     // C rounded up to a multiple of 16 (local memories)
+  int S;      // shard length (local) or L (global)
+  int act;    // ACT_GELU / ACT_SILU
+  int bf16;   // 1: q/k/v/o are bf16 and MFMA operands are bf16
+  int qk_proj, qk_scope;
+};
+
+// Per-unit scratch of the local memory kernels (element offsets into a CT
+// array); filled by local_scratch_plan.
+struct LocalPlan {
+  size_t elems;  // CT elements per unit
+  size_t Q, K, N, NT, X, KcT, KbT, R, RT, RcT, RbT, S, P;           // forward, small
+  size_t Hk, HkT, Sp, D1T, H;                                      // forward, C x hid
+  // backward extras
+  size_t Spp, G, D1, Sz, HT, dZ, dZT, dGT, dZkT, dYkT, dXT, QT, KT, XT, XAT, XET,
+      dOT, dOAT, dOET, PzT, PoT, Q1T, Q2T, dXN, dXNT, ST, Rb, small_f32;
+  size_t f32_elems;  // fp32 elements per unit (dX, dK, dQ, dR, dN, dc, U, ...)
+};
+
+struct LocalFwdArgs {
+  const void* q; const void* k; const void* v;
+  const float* lr; const float* mom; const float* decay;  // this memory, [B][H][L]
+  const float* W1i; const float* W2i;                    // this memory, [H][hid][d], [H][d][hid]
+  float* o_part;                                         // [B][H][L][d]
+  float* states;                                         // [units][nslots][4*hid*d]
+  float* mstates;                                        // [units][nslots][d*d]
+  int nslots;
+  void* scratch;                                         // units * plan.elems CT
+  LocalPlan plan;
+  Dims D;
+};
+
+struct LocalBwdArgs {
+  const void* q; const void* k; const void* v; const void* dO;
+  const float* lr; const float* mom; const float* decay;
+  const float* states;                                   // saved chunk-entry states
+  const float* mstates;
+  int nslots;
+  float* adj;                                            // [units][4*hid*d] adjoint state
+  float* madj;                                           // [units][2][d*d]
+  float* dq_part; float* dk_part; float* dv_part;        // [B][H][L][d] fp32
+  float* dlr; float* dmom; float* ddecay;                // this memory, [B][H][L]
+  float* dWinit_part;                                    // [units][2*hid*d]
+  void* scratch;
+  float* scratch_f32;                                    // units * plan.f32_elems
+  LocalPlan plan;
+  Dims D;
+};
+
+struct GlobalArgs {
+  const void* q; const void* k; const void* v; const void* dO;
+  const float* lr; const float* mom; const float* decay;  // memory 0, [B][H][L]
+  const float* W1i; const float* W2i;                    // memory 0, [H][hid][d], ...
+  float* o_part;                                         // [B][H][L][d]
+  float* states;                                         // [B*H][nslots][4*hid*d]
+  int nslots;
+  float* tokc;                                           // [B*H][L][2]  cC_t, b_t
+  float* chunkc;                                         // [B*H][L/C][4] A_C, B_C, E_C, 0
+  float* Rbuf;                                           // [B*H][C][d]
+  // backward
+  float* adj;                                            // [B*H][2][4*hid*d] ping-pong
+  float* dRbuf;                                          // [B*H][C][d]
+  float* dtok;                                           // [B*H][L][2]  d cC_t, d b_t
+  float* dchunk;                                         // [B*H][L/C][nsl][4] partials
+  float* dq_part; float* dk_part; float* dv_part;
+  float* dlr; float* dmom; float* ddecay;
+  float* dWinit;                                         // [B*H][2*hid*d] (reduced later)
+  Dims D;
+};
+
+// Allow a kernel the whole LDS of a CU for its dynamic shared memory.
+inline void set_lds_limit(const void* fn) {
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) !=
+      hipSuccess)
+    (void)hipGetLastError();
+}
+
+size_t local_plan(const Dims& D, LocalPlan* p, bool backward);
+
+hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st);
+hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st);
+hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st);
+hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st);
+hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st);
+hipError_t launch_global_bwd_chunk(const GlobalArgs& a, int n, hipStream_t st);
+hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
+hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
+                          int bf16, hipStream_t st);
+hipError_t launch_reduce_init(const float* parts, int B, int H, int nshard, size_t hd2,
+                              float* dW1, float* dW2, int d, int hid, int accumulate,
+                              hipStream_t st);
+hipError_t launch_copy_final(const float* states, int nslots, int nchains, size_t slot_elems,
+                             int last, float* out, hipStream_t st);
+
+}  // namespace tnt

@@ -1,0 +1,123 @@
+// Pieces of one local-memory chunk step shared by the forward and backward
+// kernels: staging of the chunk's tokens, the gate coefficients of the
+// momentum / decay recurrence, the Q-K projection and the chunk-entry
+// gradient quantities.  Internal to the library.
+#pragma once
+
+#include "tnt_device.h"
+#include "tnt_kernels.h"
+
+namespace tnt {
+
+constexpr int MAXC = 64;  // largest padded chunk handled by one workgroup
+
+// Gate coefficients of one chunk (positions i, tau = 0..Cp-1, 0-indexed).
+//   la_i = sum_{j<=i} log(1 - alpha_j),  lb_i = sum_{j<=i} log beta_j
+//   A_i = e^{la_i},  E_i = sum_{m<=i} e^{la_i - la_m + lb_m}
+//   ct_{i,tau} = sum_{m=tau}^{i} e^{la_i - la_m + lb_m - lb_tau}   (tau <= i)
+//   c_{i,tau} = eta_tau ct_{i,tau};  W_i = A_i W0 + E_i S0 - sum_tau c_{i,tau} u_tau
+//   momentum weights at the chunk end: b_tau = eta_tau e^{lb_{C-1} - lb_tau}
+// Padded positions (i >= C) carry eta = 0, alpha = 0, beta = 1.
+struct Coef {
+  float c[MAXC][MAXC + 1];
+  float ct[MAXC][MAXC + 1];
+  float A[MAXC], E[MAXC], la[MAXC], lb[MAXC], eta[MAXC], cC[MAXC], bb[MAXC], ebt[MAXC];
+  float knorm[MAXC];
+  float AC, BC, EC;
+  float red[32];
+};
+
+// Fill `cf` for the chunk whose first token is `tok0` (gate arrays already
+// offset to the chain).  All threads call; wave 0 computes.  Ends with a barrier.
+__device__ __forceinline__ void chunk_coefs(Coef& cf, const float* lr, const float* mom,
+                                            const float* dec, int tok0, int C, int Cp) {
+  if (wave_id() == 0) {
+    const int i = lane_id();
+    const bool in = i < C;
+    const float eta = in ? lr[tok0 + i] : 0.f;
+    const float lmb = in ? log_mom(mom[tok0 + i]) : 0.f;
+    const float lka = in ? log_keep(dec[tok0 + i]) : 0.f;
+    const float la = wave_incl_sum(lka);
+    const float lb = wave_incl_sum(lmb);
+    cf.la[i] = la;
+    cf.lb[i] = lb;
+    cf.eta[i] = eta;
+    cf.A[i] = expf(la);
+  }
+  __syncthreads();
+  if (wave_id() == 0) {
+    const int i = lane_id();
+    if (i < Cp) {
+      float e = 0.f;
+      for (int m = 0; m <= i; ++m) e += expf(cf.la[i] - cf.la[m] + cf.lb[m]);
+      cf.E[i] = e;
+      // column tau = i of ct / c by the recursion over rows
+      const int tau = i;
+      const float lbt = cf.lb[tau];
+      for (int r = 0; r < tau; ++r) { cf.ct[r][tau] = 0.f; cf.c[r][tau] = 0.f; }
+      float x = 1.0f;
+      cf.ct[tau][tau] = x;
+      cf.c[tau][tau] = cf.eta[tau] * x;
+      for (int r = tau + 1; r < Cp; ++r) {
+        x = expf(cf.la[r] - cf.la[r - 1]) * x + expf(cf.lb[r] - lbt);
+        cf.ct[r][tau] = x;
+        cf.c[r][tau] = cf.eta[tau] * x;
+      }
+    }
+  }
+  __syncthreads();
+  if (wave_id() == 0) {
+    const int tau = lane_id();
+    if (tau < Cp) {
+      const float et = (tau < C) ? expf(cf.lb[C - 1] - cf.lb[tau]) : 0.f;
+      cf.ebt[tau] = et;
+      cf.bb[tau] = cf.eta[tau] * et;
+      cf.cC[tau] = cf.c[C - 1][tau];
+    }
+    if (tau == 0) {
+      cf.AC = cf.A[C - 1];
+      cf.BC = expf(cf.lb[C - 1]);
+      cf.EC = cf.E[C - 1];
+    }
+  }
+  __syncthreads();
+}
+
+// Stage a [Cp][d] tile of an I/O tensor (rows >= C zero) into CT storage,
+// optionally also its transpose [d][Cp].
+template <typename IO, typename CT>
+__device__ __forceinline__ void stage_rows(CT* dst, CT* dstT, const IO* src, int C, int Cp,
+                                           int d) {
+  for (int e = threadIdx.x; e < Cp * d; e += blockDim.x) {
+    const int i = e / d, j = e - i * d;
+    const float x = (i < C) ? to_f(src[(size_t)i * d + j]) : 0.f;
+    if (dst) dst[(size_t)i * d + j] = from_f<CT>(x);
+    if (dstT) dstT[(size_t)j * Cp + i] = from_f<CT>(x);
+  }
+}
+
+// Row norms of the staged keys and the unit keys N = K / ||K|| (zero rows
+// stay zero), stored as [Cp][d] and [d][Cp].
+template <typename IO, typename CT>
+__device__ __forceinline__ void unit_keys(Coef& cf, CT* N, CT* NT, const IO* k, int C, int Cp,
+                                          int d) {
+  for (int i = threadIdx.x; i < Cp; i += blockDim.x) {
+    float s = 0.f;
+    if (i < C)
+      for (int j = 0; j < d; ++j) {
+        const float x = to_f(k[(size_t)i * d + j]);
+        s += x * x;
+      }
+    cf.knorm[i] = sqrtf(s);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < Cp * d; e += blockDim.x) {
+    const int i = e / d, j = e - i * d;
+    const float nr = cf.knorm[i];
+    const float x = (i < C && nr > 0.f) ? to_f(k[(size_t)i * d + j]) / nr : 0.f;
+    N[(size_t)i * d + j] = from_f<CT>(x);
+    NT[(size_t)j * Cp + i] = from_f<CT>(x);
+  }
+}
+
+}  // namespace tnt

@@ -1,0 +1,184 @@
+"""ctypes binding of ``libtnt.so`` (see ``include/tnt.h``).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  Torch tensors provide device memory and the current HIP stream.
+The functions named like the C entry points take tensors for the pointer
+arguments; ``forward`` / ``backward`` also allocate outputs and workspaces.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import torch
+
+from .inputs import BF16, LayerConfig
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtnt.so")
+_lib = None
+
+TNT_MAX_LOCAL = 4
+TNT_WS_FWD, TNT_WS_BWD, TNT_WS_BWD_RECOMPUTE = 0, 1, 2
+STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPPORTED",
+          4: "TNT_ERR_WORKSPACE", 5: "TNT_ERR_ALIGN", 6: "TNT_ERR_HIP", 7: "TNT_ERR_ARG"}
+EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
+            "tnt_strerror", "tnt_abi_version"]
+
+
+class TntError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({strerror(status)})")
+        self.status = status
+
+
+class tnt_config(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("L", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("hid", ctypes.c_int32),
+                ("has_global", ctypes.c_int32), ("C_G", ctypes.c_int32),
+                ("n_local", ctypes.c_int32),
+                ("C_L", ctypes.c_int32 * TNT_MAX_LOCAL), ("S_L", ctypes.c_int32 * TNT_MAX_LOCAL),
+                ("act", ctypes.c_int32), ("qk_proj", ctypes.c_int32),
+                ("qk_scope", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+def lib(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load the library; raises if it has not been built (no fallback)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or _LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2511_07343_amd.build`")
+    L = ctypes.CDLL(p)
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+    cp = ctypes.POINTER(tnt_config)
+    L.tnt_mem_workspace_size.argtypes = [cp, ctypes.c_int]
+    L.tnt_mem_workspace_size.restype = sz
+    L.tnt_mem_saved_size.argtypes = [cp]
+    L.tnt_mem_saved_size.restype = sz
+    L.tnt_mem_fwd.argtypes = [cp] + [vp] * 12 + [sz, vp]
+    L.tnt_mem_fwd.restype = ctypes.c_int
+    L.tnt_mem_bwd.argtypes = [cp] + [vp] * 19 + [sz, vp]
+    L.tnt_mem_bwd.restype = ctypes.c_int
+    L.tnt_strerror.argtypes = [ctypes.c_int]
+    L.tnt_strerror.restype = ctypes.c_char_p
+    L.tnt_abi_version.argtypes = []
+    L.tnt_abi_version.restype = i32
+    if path is None:
+        _lib = L
+    return L
+
+
+def to_c(cfg: LayerConfig) -> tnt_config:
+    c = tnt_config()
+    c.B, c.H, c.L, c.d, c.hid = cfg.B, cfg.H, cfg.L, cfg.d, cfg.hid
+    c.has_global, c.C_G, c.n_local = cfg.has_global, cfg.C_G, len(cfg.locals_)
+    for i, (cl, sl) in enumerate(cfg.locals_):
+        c.C_L[i], c.S_L[i] = cl, sl
+    c.act, c.qk_proj, c.qk_scope, c.dtype = cfg.act, cfg.qk_proj, cfg.qk_scope, cfg.dtype
+    return c
+
+
+def strerror(status: int) -> str:
+    return lib().tnt_strerror(status).decode()
+
+
+def _p(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def tnt_mem_workspace_size(cfg: LayerConfig, kind: int) -> int:
+    return lib().tnt_mem_workspace_size(ctypes.byref(to_c(cfg)), kind)
+
+
+def tnt_mem_saved_size(cfg: LayerConfig) -> int:
+    return lib().tnt_mem_saved_size(ctypes.byref(to_c(cfg)))
+
+
+def tnt_mem_fwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state, saved,
+                workspace, ws_bytes=None, stream=None) -> int:
+    ws_bytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+    c = to_c(cfg)
+    return lib().tnt_mem_fwd(ctypes.byref(c), _p(q), _p(k), _p(v), _p(lr), _p(mom), _p(decay),
+                             _p(W1_init), _p(W2_init), _p(o), _p(final_state), _p(saved),
+                             _p(workspace), ws_bytes, _stream(stream))
+
+
+def tnt_mem_bwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, dO, saved, dq, dk, dv, dlr,
+                dmom, ddecay, dW1_init, dW2_init, workspace, ws_bytes=None, stream=None) -> int:
+    ws_bytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+    c = to_c(cfg)
+    return lib().tnt_mem_bwd(ctypes.byref(c), _p(q), _p(k), _p(v), _p(lr), _p(mom), _p(decay),
+                             _p(W1_init), _p(W2_init), _p(dO), _p(saved), _p(dq), _p(dk),
+                             _p(dv), _p(dlr), _p(dmom), _p(ddecay), _p(dW1_init),
+                             _p(dW2_init), _p(workspace), ws_bytes, _stream(stream))
+
+
+# --------------------------------------------------------------------------
+# allocating wrappers
+# --------------------------------------------------------------------------
+def io_dtype(cfg: LayerConfig):
+    return torch.bfloat16 if cfg.dtype == BF16 else torch.float32
+
+
+def device_inputs(inp, cfg: LayerConfig, device="cuda") -> Dict[str, torch.Tensor]:
+    """Copy host arrays (``inputs.LayerInputs``) to the device in the ABI's dtypes."""
+    io = io_dtype(cfg)
+    t = lambda a, dt: torch.from_numpy(a).to(device=device, dtype=dt).contiguous()
+    return dict(q=t(inp.q, io), k=t(inp.k, io), v=t(inp.v, io), dO=t(inp.dO, io),
+                lr=t(inp.lr, torch.float32), mom=t(inp.mom, torch.float32),
+                decay=t(inp.decay, torch.float32), W1=t(inp.W1, torch.float32),
+                W2=t(inp.W2, torch.float32))
+
+
+def _bytes(n: int, device) -> torch.Tensor:
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+
+
+def forward(cfg: LayerConfig, x: Dict[str, torch.Tensor], save: bool = True,
+            final_state: bool = False, workspace: Optional[torch.Tensor] = None,
+            stream=None):
+    """Run tnt_mem_fwd; returns (o, saved or None, final_state or None)."""
+    dev = x["q"].device
+    o = torch.empty_like(x["q"])
+    saved = _bytes(tnt_mem_saved_size(cfg), dev) if save else None
+    fin = (torch.empty(cfg.B, cfg.H, 4, cfg.hid * cfg.d, dtype=torch.float32, device=dev)
+           if final_state else None)
+    if workspace is None:
+        workspace = _bytes(tnt_mem_workspace_size(cfg, TNT_WS_FWD), dev)
+    st = tnt_mem_fwd(cfg, x["q"], x["k"], x["v"], x["lr"], x["mom"], x["decay"], x["W1"],
+                     x["W2"], o, fin, saved, workspace, stream=stream)
+    if st != 0:
+        raise TntError(st, "tnt_mem_fwd")
+    return o, saved, fin
+
+
+def backward(cfg: LayerConfig, x: Dict[str, torch.Tensor], dO: torch.Tensor,
+             saved: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+             stream=None) -> Dict[str, torch.Tensor]:
+    """Run tnt_mem_bwd; returns the gradients of sum(dO * o)."""
+    dev = x["q"].device
+    g = dict(dq=torch.empty_like(x["q"]), dk=torch.empty_like(x["k"]),
+             dv=torch.empty_like(x["v"]), dlr=torch.empty_like(x["lr"]),
+             dmom=torch.empty_like(x["mom"]), ddecay=torch.empty_like(x["decay"]),
+             dW1=torch.empty_like(x["W1"]), dW2=torch.empty_like(x["W2"]))
+    if workspace is None:
+        kind = TNT_WS_BWD if saved is not None else TNT_WS_BWD_RECOMPUTE
+        workspace = _bytes(tnt_mem_workspace_size(cfg, kind), dev)
+    st = tnt_mem_bwd(cfg, x["q"], x["k"], x["v"], x["lr"], x["mom"], x["decay"], x["W1"],
+                     x["W2"], dO, saved, g["dq"], g["dk"], g["dv"], g["dlr"], g["dmom"],
+                     g["ddecay"], g["dW1"], g["dW2"], workspace, stream=stream)
+    if st != 0:
+        raise TntError(st, "tnt_mem_bwd")
+    return g

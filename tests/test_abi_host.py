@@ -1,0 +1,95 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2511_07343_amd import tnt
+from paper_2511_07343_amd.inputs import WORKLOADS, small_config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "tnt.h")).read()
+    return sorted(set(re.findall(r"\b(tnt_[a-z_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported():
+    L = tnt.lib()
+    names = _declared()
+    assert set(tnt.EXPORTED) <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _param_counts():
+    src = open(os.path.join(ROOT, "include", "tnt.h")).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    out = {}
+    for m in re.finditer(r"\b(tnt_[a-z_]+)\s*\(([^;{]*?)\)\s*;", src, re.S):
+        args = m.group(2).strip()
+        out[m.group(1)] = 0 if args in ("", "void") else args.count(",") + 1
+    return out
+
+
+def test_binding_argument_counts_match_header():
+    L = tnt.lib()
+    counts = _param_counts()
+    for name in tnt.EXPORTED:
+        fn = getattr(L, name)
+        assert len(fn.argtypes) == counts[name], name
+
+
+def test_abi_version():
+    assert tnt.lib().tnt_abi_version() == 1
+
+
+def test_strerror_names():
+    for s in range(8):
+        assert tnt.strerror(s)
+
+
+@pytest.mark.parametrize("cfg", WORKLOADS, ids=lambda c: c.name.split()[0] + str(c.L))
+def test_workspace_sizes_positive(cfg):
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD) > 0
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD) > tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD)
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD_RECOMPUTE) >= \
+        tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD) + tnt.tnt_mem_saved_size(cfg)
+    assert tnt.tnt_mem_saved_size(cfg) > 0
+
+
+def _fwd_status(cfg, ptr=256, ws=1 << 40):
+    p = ptr
+    return tnt.tnt_mem_fwd(cfg, p, p, p, p, p, p, p, p, p, None, None, p, ws_bytes=ws, stream=0)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(L=100), 2),                      # L % C_G
+    (dict(locals_=((8, 12),)), 2),         # S_L % C_L
+    (dict(locals_=((8, 48),)), 2),         # L % S_L
+    (dict(d=24), 3),
+    (dict(hid=48), 3),
+    (dict(locals_=((80, 160),), L=320, C_G=64), 3),
+    (dict(act=5), 7),
+    (dict(qk_scope=2), 7),
+    (dict(B=0), 2),
+    (dict(has_global=0, locals_=()), 2),
+])
+def test_validation_codes(bad, code):
+    cfg = small_config(L=64, C_G=16, locals_=((8, 32),)).replace(**bad)
+    assert _fwd_status(cfg) == code
+
+
+def test_null_and_alignment_and_workspace():
+    cfg = small_config(L=64, C_G=16, locals_=((8, 32),))
+    assert _fwd_status(cfg, ptr=0) == 1
+    assert _fwd_status(cfg, ptr=258) == 5
+    assert _fwd_status(cfg, ws=16) == 4
+    # final_state without a global memory is a shape error
+    c = tnt.to_c(cfg.replace(has_global=0))
+    st = tnt.lib().tnt_mem_fwd(ctypes.byref(c), *([256] * 9), 256, None, 256, 1 << 40, None)
+    assert st == 2

@@ -1,0 +1,120 @@
+"""GPU parity of tnt_mem_fwd against the fp64 oracle (element by element).
+
+Tolerance (max_i |gpu - oracle| / max_i |oracle| per tensor): 1e-4 for fp32
+inputs, 2e-2 for bf16 inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2511_07343_amd import tnt
+from paper_2511_07343_amd.inputs import (ACT_GELU, ACT_SILU, BF16, F32, QK_CHUNK, WORKLOADS,
+                                         make_inputs, max_rel_err, small_config)
+
+pytestmark = pytest.mark.gpu
+torch.set_num_threads(4)
+
+
+def tol(cfg):
+    return 2e-2 if cfg.dtype == BF16 else 1e-4
+
+
+def gpu_forward(cfg, inp, save=True, final=False):
+    x = tnt.device_inputs(inp, cfg)
+    o, saved, fin = tnt.forward(cfg, x, save=save, final_state=final)
+    torch.cuda.synchronize()
+    return (o.float().cpu().numpy(), None if fin is None else fin.cpu().numpy())
+
+
+SMALL = [
+    small_config(F32, ACT_GELU, B=2, H=2, L=128, d=32, hid=64, C_G=32,
+                 locals_=((16, 64), (8, 32)), name="f32 two locals multi-tile"),
+    small_config(F32, ACT_SILU, B=1, H=2, L=96, d=16, hid=32, C_G=48,
+                 locals_=((12, 48),), name="f32 ragged chunks C_L=12 C_G=48"),
+    small_config(BF16, ACT_SILU, B=1, H=2, L=256, d=64, hid=256, C_G=128,
+                 locals_=((32, 128),), name="bf16 d64 h256"),
+    small_config(BF16, ACT_GELU, B=2, H=1, L=128, d=64, hid=128, C_G=128,
+                 locals_=((64, 128), (16, 64)), name="bf16 C_G=L two locals"),
+    small_config(F32, ACT_SILU, B=1, H=1, L=64, d=16, hid=32, C_G=16, locals_=((8, 32),),
+                 qk_scope=QK_CHUNK, name="f32 chunk-scope QK"),
+    small_config(F32, ACT_GELU, B=1, H=2, L=64, d=16, hid=32, C_G=16, locals_=((8, 32),),
+                 qk_proj=0, name="f32 no QK projection"),
+    small_config(F32, ACT_GELU, B=1, H=2, L=64, d=16, hid=32, C_G=16, locals_=((16, 32),),
+                 has_global=0, name="f32 locals only"),
+    small_config(F32, ACT_SILU, B=2, H=1, L=64, d=16, hid=32, C_G=16, locals_=(),
+                 name="f32 global only"),
+    small_config(BF16, ACT_SILU, B=1, H=1, L=128, d=128, hid=512, C_G=64,
+                 locals_=((64, 128),), name="bf16 d128 h512"),
+]
+
+
+@pytest.mark.parametrize("cfg", [WORKLOADS[0]] + SMALL, ids=lambda c: c.name)
+def test_forward_small_all_chains(cfg):
+    inp = make_inputs(cfg, 0 if cfg is WORKLOADS[0] else 101)
+    print(f"\n[case] {cfg.name}", flush=True)
+    got, fin = gpu_forward(cfg, inp, final=bool(cfg.has_global))
+    pairs = O.all_pairs(cfg)
+    ref, rfin = O.forward_pairs(inp, cfg, pairs, with_final=True)
+    ref = ref.numpy().reshape(cfg.B, cfg.H, cfg.L, cfg.d)
+    err = max_rel_err(got, ref)
+    print(f"o max rel err {err:.3e}", flush=True)
+    assert err <= tol(cfg)
+    if cfg.has_global:
+        rf = np.stack([r.numpy().reshape(len(pairs), -1) for r in rfin], 1)
+        e2 = max_rel_err(fin.reshape(len(pairs), 4, -1), rf)
+        print(f"final state max rel err {e2:.3e}", flush=True)
+        assert e2 <= tol(cfg)
+
+
+def test_forward_save_and_ring_agree():
+    """The saved-state path and the two-slot ring path give identical outputs."""
+    cfg = SMALL[0]
+    inp = make_inputs(cfg, 102)
+    a, _ = gpu_forward(cfg, inp, save=True)
+    b, _ = gpu_forward(cfg, inp, save=False)
+    assert np.array_equal(a, b)
+
+
+def test_forward_deterministic():
+    cfg = SMALL[2]
+    inp = make_inputs(cfg, 103)
+    a, _ = gpu_forward(cfg, inp)
+    b, _ = gpu_forward(cfg, inp)
+    assert np.array_equal(a, b)
+
+
+def test_forward_shard_isolation_bitwise():
+    """Reset invariant on the GPU: a locals-only layer run on one shard's
+    tokens alone equals the same shard of the full run, bit for bit."""
+    cfg = small_config(BF16, ACT_SILU, B=1, H=2, L=256, d=64, hid=256, C_G=64,
+                       locals_=((32, 64),), has_global=0)
+    inp = make_inputs(cfg, 104)
+    full, _ = gpu_forward(cfg, inp)
+    one = cfg.replace(L=64)
+    for s in range(4):
+        sl = slice(64 * s, 64 * (s + 1))
+        sub = make_inputs(one, 104)
+        for name in ("q", "k", "v", "dO"):
+            setattr(sub, name, np.ascontiguousarray(getattr(inp, name)[:, :, sl]))
+        for name in ("lr", "mom", "decay"):
+            setattr(sub, name, np.ascontiguousarray(getattr(inp, name)[:, :, :, sl]))
+        sub.W1, sub.W2 = inp.W1, inp.W2
+        alone, _ = gpu_forward(one, sub)
+        assert np.array_equal(alone, full[:, :, sl])
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_forward_full_size_sampled_chain(idx):
+    """Full-size workload on the GPU; the oracle recomputes one sampled
+    (batch, head) chain in full (every chunk, shard and memory)."""
+    cfg = WORKLOADS[idx]
+    inp = make_inputs(cfg, idx)
+    print(f"\n[case] {cfg.name}", flush=True)
+    got, _ = gpu_forward(cfg, inp)
+    assert np.isfinite(got).all()
+    b, h = cfg.B - 1, cfg.H // 2
+    ref = O.forward_pairs(inp, cfg, [(b, h)]).numpy()[0]
+    err = max_rel_err(got[b, h], ref)
+    print(f"chain ({b},{h}) o max rel err {err:.3e}", flush=True)
+    assert err <= tol(cfg)

@@ -75,7 +75,7 @@ def test_activation_derivative_finite_difference(kind):
 # ---------------------------------------------------------------- inner gradient
 @pytest.mark.parametrize("kind", KINDS)
 def test_inner_grad_central_differences(kind):
-    """u = grad_W ||f(W,k) - v||^2 (Sec. 2.1) against central differences."""
+    """u = grad_W (1/d)||f(W,k) - v||^2 (Sec. 2.1) against central differences."""
     rng = np.random.default_rng(1)
     P, d, h = 2, 5, 7
     W1 = _t(rng.normal(0, 0.6, (P, h, d)))
