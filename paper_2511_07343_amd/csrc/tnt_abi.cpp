@@ -7,6 +7,7 @@
 
 #include "../../include/tnt.h"
 #include "tnt_kernels.h"
+#include "tnt_local_bwd_layout.h"
 
 using namespace tnt;
 
@@ -65,10 +66,10 @@ struct Layout {
   size_t ring_g, ring_l[TNT_MAX_LOCAL], ring_m[TNT_MAX_LOCAL];
   LocalPlan lplan[TNT_MAX_LOCAL];
   // backward workspace
-  size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_adj_l[TNT_MAX_LOCAL],
-      b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL], b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL],
-      b_states, bwd_bytes, bwd_re_bytes;
-  LocalPlan bplan[TNT_MAX_LOCAL];
+  size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32,
+      b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
+      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_states, bwd_bytes, bwd_re_bytes;
+  BwdLayout blay[TNT_MAX_LOCAL];
 };
 
 Layout layout_of(const tnt_config* c) {
@@ -103,7 +104,7 @@ Layout layout_of(const tnt_config* c) {
   off = 0;
   y.w_opart = off; off += up((size_t)y.M * y.io_elems * f);
   if (c->has_global) {
-    y.w_tokc = off; off += up(y.gates * 4 * f);
+    y.w_tokc = off; off += up(y.gates * TKS * f);
     y.w_chunkc = off; off += up((size_t)y.BH * y.g_chunks * 4 * f);
     y.w_R = off; off += up((size_t)y.BH * c->C_G * c->d * f);
   }
@@ -132,15 +133,18 @@ Layout layout_of(const tnt_config* c) {
     y.b_dtok = off; off += up(y.gates * 4 * f);
     y.b_dchunk = off; off += up((size_t)y.BH * y.g_chunks * (c->hid / 16) * 4 * f);
     y.b_dWg = off; off += up((size_t)y.BH * 2 * y.hd * f);
+    const Dims D = dims_of(c, c->C_G, c->L);
+    y.b_gscr = off;
+    off += up(global_bwd_scratch_bytes(D, &y.b_gscr_f32));
   }
   for (int i = 0; i < c->n_local; ++i) {
     const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
-    local_plan(D, &y.bplan[i], true);
+    bwd_layout(D.Cp, D.d, D.hid, &y.blay[i]);
     y.b_adj_l[i] = off; off += up((size_t)y.l_units[i] * 4 * y.hd * f);
-    y.b_madj[i] = off; off += up((size_t)y.l_units[i] * 2 * dd * f);
+    y.b_madj[i] = off; off += up((size_t)y.l_units[i] * dd * f);
     y.b_dWl[i] = off; off += up((size_t)y.l_units[i] * 2 * y.hd * f);
-    y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.bplan[i].elems * cts);
-    y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.bplan[i].f32_elems * f);
+    y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].ct_elems * cts);
+    y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].f32_elems * f);
   }
   y.bwd_bytes = off;
   y.b_states = off;
@@ -200,6 +204,73 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     HIP_TRY(launch_local_fwd(a, y.l_units[i], st));
   }
   if (o) HIP_TRY(launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, c->dtype == TNT_BF16, st));
+  return TNT_OK;
+}
+
+tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, const void* k,
+                        const void* v, const float* lr, const float* mom, const float* decay,
+                        const float* W1i, const float* W2i, const void* dO, char* sv,
+                        void* dq, void* dk, void* dv, float* dlr, float* dmom, float* ddecay,
+                        float* dW1, float* dW2, char* ws, hipStream_t st) {
+  const size_t G = y.gates;
+  float* dparts = (float*)(ws + y.b_dparts);
+  float* dqp = dparts;
+  float* dkp = dparts + (size_t)y.M * y.io_elems;
+  float* dvp = dparts + 2 * (size_t)y.M * y.io_elems;
+  int m = 0;
+  if (c->has_global) {
+    GlobalArgs g{};
+    g.q = q; g.k = k; g.v = v; g.dO = dO;
+    g.lr = lr; g.mom = mom; g.decay = decay;
+    g.W1i = W1i; g.W2i = W2i;
+    g.states = (float*)(sv + y.sv_g);
+    g.nslots = y.g_chunks + 1;
+    g.tokc = (float*)(ws + y.w_tokc);
+    g.chunkc = (float*)(ws + y.w_chunkc);
+    g.Rbuf = (float*)(ws + y.w_R);
+    g.adj = (float*)(ws + y.b_adj_g);
+    g.dRbuf = (float*)(ws + y.b_dR);
+    g.dtok = (float*)(ws + y.b_dtok);
+    g.dchunk = (float*)(ws + y.b_dchunk);
+    g.dWinit = (float*)(ws + y.b_dWg);
+    g.scratch = ws + y.b_gscr;
+    g.scratch_f32_off = y.b_gscr_f32;
+    g.dq_part = dqp; g.dk_part = dkp; g.dv_part = dvp;
+    g.dlr = dlr; g.dmom = dmom; g.ddecay = ddecay;
+    g.D = dims_of(c, c->C_G, c->L);
+    HIP_TRY(launch_global_scan(g, st));
+    HIP_TRY(launch_global_bwd_zero(g, y.g_chunks & 1, st));
+    for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TRY(launch_global_bwd_chunk(g, n, st));
+    HIP_TRY(launch_global_gate_bwd(g, st));
+    HIP_TRY(launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
+    m = 1;
+  }
+  for (int i = 0; i < c->n_local; ++i, ++m) {
+    LocalBwdArgs a{};
+    a.q = q; a.k = k; a.v = v; a.dO = dO;
+    a.lr = lr + m * G; a.mom = mom + m * G; a.decay = decay + m * G;
+    a.states = (const float*)(sv + y.sv_l[i]);
+    a.mstates = (const float*)(sv + y.sv_m[i]);
+    a.nslots = y.l_chunks[i] + 1;
+    a.adj = (float*)(ws + y.b_adj_l[i]);
+    a.madj = (float*)(ws + y.b_madj[i]);
+    a.dq_part = dqp + (size_t)m * y.io_elems;
+    a.dk_part = dkp + (size_t)m * y.io_elems;
+    a.dv_part = dvp + (size_t)m * y.io_elems;
+    a.dlr = dlr + m * G; a.dmom = dmom + m * G; a.ddecay = ddecay + m * G;
+    a.dWinit_part = (float*)(ws + y.b_dWl[i]);
+    a.scratch = ws + y.b_scr[i];
+    a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
+    a.D = dims_of(c, c->C_L[i], c->S_L[i]);
+    HIP_TRY(launch_local_bwd(a, y.l_units[i], st));
+    HIP_TRY(launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
+                               dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
+                               c->d, c->hid, 0, st));
+  }
+  const int bf = c->dtype == TNT_BF16;
+  HIP_TRY(launch_sum_out(dqp, y.M, y.io_elems, y.io_elems, dq, bf, st));
+  HIP_TRY(launch_sum_out(dkp, y.M, y.io_elems, y.io_elems, dk, bf, st));
+  HIP_TRY(launch_sum_out(dvp, y.M, y.io_elems, y.io_elems, dv, bf, st));
   return TNT_OK;
 }
 
@@ -265,10 +336,28 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
                        size_t ws_bytes, void* stream) {
   tnt_status s = validate(cfg);
   if (s != TNT_OK) return s;
-  (void)q; (void)k; (void)v; (void)lr; (void)mom; (void)decay; (void)W1_init; (void)W2_init;
-  (void)dO; (void)saved; (void)dq; (void)dk; (void)dv; (void)dlr; (void)dmom; (void)ddecay;
-  (void)dW1_init; (void)dW2_init; (void)workspace; (void)ws_bytes; (void)stream;
-  return TNT_ERR_UNSUPPORTED;
+  if (!q || !k || !v || !lr || !mom || !decay || !W1_init || !W2_init || !dO || !dq || !dk ||
+      !dv || !dlr || !dmom || !ddecay || !dW1_init || !dW2_init || !workspace)
+    return TNT_ERR_NULL;
+  for (const void* p : {(const void*)q, (const void*)k, (const void*)v, (const void*)lr,
+                        (const void*)mom, (const void*)decay, (const void*)W1_init,
+                        (const void*)W2_init, (const void*)dO, (const void*)saved,
+                        (const void*)dq, (const void*)dk, (const void*)dv, (const void*)dlr,
+                        (const void*)dmom, (const void*)ddecay, (const void*)dW1_init,
+                        (const void*)dW2_init, (const void*)workspace})
+    if (p && misaligned(p)) return TNT_ERR_ALIGN;
+  const Layout y = layout_of(cfg);
+  if (ws_bytes < (saved ? y.bwd_bytes : y.bwd_re_bytes)) return TNT_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  char* sv = saved ? (char*)saved : ws + y.b_states;
+  hipStream_t st = (hipStream_t)stream;
+  if (!saved) {
+    s = run_forward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, nullptr, nullptr, sv, ws,
+                    st);
+    if (s != TNT_OK) return s;
+  }
+  return run_backward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, dO, sv, dq, dk, dv,
+                      dlr, dmom, ddecay, dW1_init, dW2_init, ws, st);
 }
 
 }  // extern "C"

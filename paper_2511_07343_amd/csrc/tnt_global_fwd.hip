@@ -17,7 +17,7 @@ namespace tnt {
 
 // ---------------------------------------------------------------------------
 // gate coefficients of a global chunk (one wavefront per (chunk, chain)).
-// tokc[t] = {cC_t, b_t, la_t, lb_t}; chunkc[n] = {A_C, B_C, E_C, 0} with
+// tokc[t] = {cC_t, b_t, la_t, lb_t, s_t, e^{lb_C - lb_t}}; chunkc[n] = {A_C, B_C, E_C, 0} with
 //   cC_t = eta_t s_t,  s_t = sum_{m>=t} e^{la_C - la_m + lb_m - lb_t}
 //        = e^{la_C - la_t} + beta_{t+1} s_{t+1}          (suffix affine scan)
 //   b_t  = eta_t e^{lb_C - lb_t},  E_C = beta_0 s_0.
@@ -29,7 +29,7 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
   const float* lr = a.lr + base;
   const float* mom = a.mom + base;
   const float* dec = a.decay + base;
-  float* tk = a.tokc + base * 4;
+  float* tk = a.tokc + base * TKS;
   const int l = lane_id();
   const int E = (C + WAVE - 1) / WAVE;
   const int i0 = min(l * E, C), i1 = min(i0 + E, C);
@@ -44,13 +44,13 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
   for (int i = i0; i < i1; ++i) {
     pa += log_keep(dec[i]);
     pb += log_mom(mom[i]);
-    tk[(size_t)i * 4 + 2] = pa;
-    tk[(size_t)i * 4 + 3] = pb;
+    tk[(size_t)i * TKS + 2] = pa;
+    tk[(size_t)i * TKS + 3] = pb;
   }
   // segment affine map s_{i0} = P s_{i1} + Q (own writes are visible to the lane)
   float P = 1.f, Q = 0.f;
   for (int i = i1 - 1; i >= i0; --i) {
-    const float ai = expf(laC - tk[(size_t)i * 4 + 2]);
+    const float ai = expf(laC - tk[(size_t)i * TKS + 2]);
     const float mi = (i + 1 < C) ? mom[i + 1] : 0.f;
     Q = ai + mi * Q;
     P = mi * P;
@@ -68,11 +68,14 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
   if (l == WAVE - 1) sin = 0.f;
   float sv = sin;
   for (int i = i1 - 1; i >= i0; --i) {
-    const float ai = expf(laC - tk[(size_t)i * 4 + 2]);
+    const float ai = expf(laC - tk[(size_t)i * TKS + 2]);
     const float mi = (i + 1 < C) ? mom[i + 1] : 0.f;
     sv = ai + mi * sv;
-    tk[(size_t)i * 4 + 0] = lr[i] * sv;
-    tk[(size_t)i * 4 + 1] = lr[i] * expf(lbC - tk[(size_t)i * 4 + 3]);
+    const float ebt = expf(lbC - tk[(size_t)i * TKS + 3]);
+    tk[(size_t)i * TKS + 0] = lr[i] * sv;
+    tk[(size_t)i * TKS + 1] = lr[i] * ebt;
+    tk[(size_t)i * TKS + 4] = sv;
+    tk[(size_t)i * TKS + 5] = ebt;
   }
   if (l == 0) {
     float* cc = a.chunkc + ((size_t)chain * (L / C) + n) * 4;
@@ -192,7 +195,7 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
   CT* sHkT = sRbT + d * TT;           // [HS][TT]
   CT* sD1T = sHkT + HS * TT;          // [HS][TT]
   const size_t tokc0 = (size_t)chain * D.L + (size_t)n * C;
-  const float* tk = a.tokc + tokc0 * 4;
+  const float* tk = a.tokc + tokc0 * TKS;
   const IO* kk = (const IO*)a.k + tokc0 * d;
   const float* Rb = a.Rbuf + (size_t)chain * C * d;
 
@@ -208,8 +211,8 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
       const bool in = i < rows;
       const float kx = in ? to_f(kk[(size_t)(r0 + i) * d + j]) : 0.f;
       const float rx = in ? Rb[(size_t)(r0 + i) * d + j] : 0.f;
-      const float cc = in ? tk[(size_t)(r0 + i) * 4 + 0] : 0.f;
-      const float bb = in ? tk[(size_t)(r0 + i) * 4 + 1] : 0.f;
+      const float cc = in ? tk[(size_t)(r0 + i) * TKS + 0] : 0.f;
+      const float bb = in ? tk[(size_t)(r0 + i) * TKS + 1] : 0.f;
       sK[e] = from_f<CT>(kx);
       sR[e] = from_f<CT>(rx);
       sKcT[(size_t)j * TT + i] = from_f<CT>(cc * kx);

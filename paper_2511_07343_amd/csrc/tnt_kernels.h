@@ -68,19 +68,23 @@ struct GlobalArgs {
   float* o_part;                                         // [B][H][L][d]
   float* states;                                         // [B*H][nslots][4*hid*d]
   int nslots;
-  float* tokc;                                           // [B*H][L][2]  cC_t, b_t
+  float* tokc;                                           // [B*H][L][TKS] cC, b, la, lb, s, e^{lb_C-lb}
   float* chunkc;                                         // [B*H][L/C][4] A_C, B_C, E_C, 0
   float* Rbuf;                                           // [B*H][C][d]
   // backward
   float* adj;                                            // [B*H][2][4*hid*d] ping-pong
   float* dRbuf;                                          // [B*H][C][d]
-  float* dtok;                                           // [B*H][L][2]  d cC_t, d b_t
+  float* dtok;                                           // [B*H][L][4]  d cC_t, d b_t
   float* dchunk;                                         // [B*H][L/C][nsl][4] partials
   float* dq_part; float* dk_part; float* dv_part;
   float* dlr; float* dmom; float* ddecay;
   float* dWinit;                                         // [B*H][2*hid*d] (reduced later)
+  void* scratch;                                         // phase-A scratch of the backward
+  size_t scratch_f32_off;
   Dims D;
 };
+
+constexpr int TKS = 8;  // floats per token in GlobalArgs::tokc
 
 // Allow a kernel the whole LDS of a CU for its dynamic shared memory.
 inline void set_lds_limit(const void* fn) {
@@ -97,6 +101,10 @@ hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st);
 hipError_t launch_global_bwd_chunk(const GlobalArgs& a, int n, hipStream_t st);
+hipError_t launch_global_bwd_zero(const GlobalArgs& a, int slot, hipStream_t st);
+hipError_t launch_reduce_global_init(const float* part, int B, int H, size_t hd, float* dW1,
+                                     float* dW2, hipStream_t st);
+size_t global_bwd_scratch_bytes(const Dims& D, size_t* f32_off);
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
                           int bf16, hipStream_t st);
