@@ -1,0 +1,203 @@
+#!/usr/bin/env python3
+"""Benchmark of the TNT memory layer (forward + backward) on one MI355X.
+
+A step is one tnt_mem_fwd (saving the chunk-entry states) followed by one
+tnt_mem_bwd on the same synthetic batch, i.e. every kernel of the hot path.
+Default workload: batch 4, 8 heads, head dim 64, sequence 8192, MLP 64-256-64
+(SiLU), global chunk 2048, one local memory with chunk 64 and shard 2048, bf16
+inputs (seeded synthetic data; no dataset).
+
+Prints one JSON line with the throughput (tokens/s of fwd+bwd), the roofline
+position of the dominant kernel (algorithmic MFMA FLOPs per launch over its
+HIP-event launch time measured inside the timed region) and the fp64 CPU
+oracle's throughput on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+PEAK_FP32 = 157.3e12    # MI355X fp32, FLOP/s
+METRIC = "memory-layer fwd+bwd tokens/sec at seq 8192; % MFMA bf16 peak (rocprof)"
+
+
+# ----------------------------------------------------------------------------
+# algorithmic FLOPs (GEMM work the method needs, per token and head)
+# ----------------------------------------------------------------------------
+def local_fwd_flops(d, h, C, qk=True):
+    # chunk gradients 6dh, dual-form retrieval 8dh + 4C(d+h), state carry 8dh,
+    # Q-K projection 4d^2 + 4Cd
+    return 22 * d * h + 4 * C * (d + h) + ((4 * d * d + 4 * C * d) if qk else 0)
+
+
+def local_bwd_flops(d, h, C, qk=True):
+    # adjoints of retrieval, carry and inner gradient 44dh + 8Ch + 8Cd,
+    # of the Q-K projection 8Cd + 6d^2
+    return 44 * d * h + 8 * C * h + 8 * C * d + ((8 * C * d + 6 * d * d) if qk else 0)
+
+
+def global_fwd_flops(d, h):
+    return 18 * d * h     # chunk gradients 6dh, retrieval 4dh, carry 8dh
+
+
+def global_bwd_flops(d, h):
+    return 36 * d * h
+
+
+def step_flops(cfg):
+    tok = cfg.B * cfg.H * cfg.L
+    f = 0
+    if cfg.has_global:
+        f += (global_fwd_flops(cfg.d, cfg.hid) + global_bwd_flops(cfg.d, cfg.hid)) * tok
+    for (C, _) in cfg.locals_:
+        f += (local_fwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj) +
+              local_bwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj)) * tok
+    return f
+
+
+def launch_flops(cfg, name):
+    """Algorithmic FLOPs one launch of `name` processes (None if not a GEMM kernel)."""
+    tok = cfg.B * cfg.H * cfg.L
+    C = cfg.locals_[0][0] if cfg.locals_ else 0
+    if name == "local_fwd":
+        return local_fwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj) * tok
+    if name == "local_bwd":
+        return local_bwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj) * tok
+    per_chunk = cfg.B * cfg.H * cfg.C_G
+    if name == "global_fwd_chunk":
+        return global_fwd_flops(cfg.d, cfg.hid) * per_chunk
+    if name == "global_bwd_chunk":
+        return global_bwd_flops(cfg.d, cfg.hid) * per_chunk
+    return None
+
+
+# ----------------------------------------------------------------------------
+def cpu_baseline(cfg, inp, budget_tokens):
+    """fp64 oracle, fwd + bwd, on one (batch 0, head 0) chain restricted to its
+    first `budget_tokens` tokens (one local shard and one global chunk at the
+    default workload)."""
+    import torch
+    import oracle as O
+
+    n = len(os.sched_getaffinity(0))
+    torch.set_num_threads(n)
+    L = budget_tokens
+    sub = cfg.replace(L=L, B=1, H=1)
+    g = O.gather_pairs(inp, [(0, 0)])
+    cut = lambda t, ax: t.narrow(ax, 0, L).contiguous()
+    args = [cut(g["q"], 1), cut(g["k"], 1), cut(g["v"], 1), cut(g["lr"], 2), cut(g["mom"], 2),
+            cut(g["decay"], 2), g["W1"], g["W2"]]
+    t0 = time.perf_counter()
+    O.layer_backward(*args, cut(g["dO"], 1), sub)
+    dt = time.perf_counter() - t0
+    return {"value": L / dt, "unit": "tokens/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"fwd+bwd of one (batch 0, head 0) chain, first {L} tokens "
+                      f"(fp64 torch CPU autograd, {dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=0,
+                    help="tokens of the CPU-oracle sample (default: one local shard)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the layer's multi-GPU split is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2511_07343_amd import inputs, tnt
+
+    cfg = inputs.WORKLOADS[args.workload]
+    inp = inputs.make_inputs(cfg, args.workload)
+    dev = torch.device("cuda:0")
+    x = tnt.device_inputs(inp, cfg, device=dev)
+    u8 = lambda n: torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
+    o = torch.empty_like(x["q"])
+    saved = u8(tnt.tnt_mem_saved_size(cfg))
+    ws_f = u8(tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD))
+    ws_b = u8(tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD))
+    g = {k: torch.empty_like(x[s]) for k, s in
+         (("dq", "q"), ("dk", "k"), ("dv", "v"), ("dlr", "lr"), ("dmom", "mom"),
+          ("ddecay", "decay"), ("dW1", "W1"), ("dW2", "W2"))}
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        s1 = tnt.tnt_mem_fwd(cfg, x["q"], x["k"], x["v"], x["lr"], x["mom"], x["decay"], x["W1"],
+                             x["W2"], o, None, saved, ws_f, stream=stream)
+        s2 = tnt.tnt_mem_bwd(cfg, x["q"], x["k"], x["v"], x["lr"], x["mom"], x["decay"],
+                             x["W1"], x["W2"], x["dO"], saved, g["dq"], g["dk"], g["dv"],
+                             g["dlr"], g["dmom"], g["ddecay"], g["dW1"], g["dW2"], ws_b,
+                             stream=stream)
+        if s1 or s2:
+            raise tnt.TntError(s1 or s2, "step")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    tnt.tnt_timing_read()
+    tnt.tnt_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    tnt.tnt_timing_enable(False)
+    kt = tnt.tnt_timing_read()
+    assert torch.isfinite(o.float()).all() and torch.isfinite(g["dq"].float()).all()
+
+    elapsed = t1 - t0
+    ms_step = 1e3 * elapsed / args.steps
+    tokens = cfg.B * cfg.L
+    value = tokens * args.steps / elapsed
+    flops = step_flops(cfg)
+    bf = cfg.dtype == inputs.BF16
+    peak = PEAK_BF16 if bf else PEAK_FP32
+
+    # dominant kernel by total event time in the timed region
+    dom = max(kt.items(), key=lambda kv: kv[1][0])
+    name, (tot_ms, n) = dom
+    fl = launch_flops(cfg, name)
+    avg_ms = tot_ms / n
+    roof = {"bound": "mfma", "kernel": name, "achieved": None, "peak": peak / 1e12,
+            "unit": "TFLOP/s", "frac": None, "traffic": None, "avg_launch_ms": avg_ms,
+            "launches": n}
+    if fl is not None:
+        ach = fl / (avg_ms * 1e-3) / 1e12
+        roof.update(achieved=ach, frac=ach * 1e12 / peak, flops_per_launch=fl)
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if bf else "f32", "data": "synthetic (seeded Gaussian, unit q/k)",
+        "config": {"workload": cfg.name, "global_batch": cfg.B, "seq_len": cfg.L,
+                   "heads": cfg.H, "head_dim": cfg.d, "hidden": cfg.hid, "C_G": cfg.C_G,
+                   "locals": [list(t) for t in cfg.locals_], "parallelism": "single GPU"},
+        "algorithmic_tflops": flops / elapsed * args.steps / 1e12,
+        "algorithmic_frac_of_peak": flops / elapsed * args.steps / peak,
+        "roofline": roof,
+        "kernels_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())},
+    }
+    if not args.no_cpu_baseline:
+        ctoks = args.cpu_tokens or (cfg.locals_[0][1] if cfg.locals_ else cfg.C_G)
+        res["cpu_baseline"] = cpu_baseline(cfg, inp, ctoks)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

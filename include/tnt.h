@@ -135,6 +135,17 @@ const char* tnt_strerror(tnt_status status);
 /* Version of this ABI (bumped on any incompatible change). */
 int32_t tnt_abi_version(void);
 
+/* Opt-in kernel timing, for benchmarks.  While enabled (on != 0), every
+ * kernel launch of tnt_mem_fwd / tnt_mem_bwd is bracketed by a pair of
+ * hipEvents recorded on the launch stream (at most 65536 launches are kept).
+ * tnt_timing_read synchronises on the recorded events, writes one entry per
+ * kernel name (names: 32-byte NUL-terminated slots; total_ms: summed event
+ * time; launches: number of launches), clears the record, and returns the
+ * number of entries (at most max), or -1 on a HIP error.  Not thread-safe:
+ * use from one host thread while enabled.  Returns the previous setting. */
+int32_t tnt_timing_enable(int32_t on);
+int32_t tnt_timing_read(int32_t max, char* names, double* total_ms, int32_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

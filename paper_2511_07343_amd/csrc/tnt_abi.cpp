@@ -4,6 +4,8 @@
 
 #include <algorithm>
 #include <cstring>
+#include <string>
+#include <vector>
 
 #include "../../include/tnt.h"
 #include "tnt_kernels.h"
@@ -154,10 +156,46 @@ Layout layout_of(const tnt_config* c) {
 
 bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
 
+// ---- opt-in launch timing (hipEvent pairs per launch)
+struct TimedLaunch {
+  const char* name;
+  hipEvent_t a, b;
+};
+struct Timing {
+  bool on = false;
+  std::vector<TimedLaunch> rec;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Timing g_timing;
+constexpr size_t TIMING_CAP = 65536;
+
+template <typename F>
+hipError_t timed(const char* name, hipStream_t st, F&& launch) {
+  if (!g_timing.on || g_timing.rec.size() >= TIMING_CAP) return launch();
+  TimedLaunch t{name, g_timing.get(), g_timing.get()};
+  if (!t.a || !t.b) return launch();
+  hipEventRecord(t.a, st);
+  const hipError_t e = launch();
+  hipEventRecord(t.b, st);
+  g_timing.rec.push_back(t);
+  return e;
+}
+
 #define HIP_TRY(x)                         \
   do {                                     \
     if ((x) != hipSuccess) return TNT_ERR_HIP; \
   } while (0)
+#define HIP_TIMED(name, x) HIP_TRY(timed(name, st, [&]() { return (x); }))
 
 // forward pass into a given state area (`sv` = saved buffer, or nullptr to use
 // the two-slot rings in the workspace)
@@ -180,11 +218,11 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     g.chunkc = (float*)(ws + y.w_chunkc);
     g.Rbuf = (float*)(ws + y.w_R);
     g.D = dims_of(c, c->C_G, c->L);
-    HIP_TRY(launch_global_scan(g, st));
-    HIP_TRY(launch_global_init(g, st));
-    for (int n = 0; n < y.g_chunks; ++n) HIP_TRY(launch_global_fwd_chunk(g, n, st));
+    HIP_TIMED("global_scan", launch_global_scan(g, st));
+    HIP_TIMED("global_init", launch_global_init(g, st));
+    for (int n = 0; n < y.g_chunks; ++n) HIP_TIMED("global_fwd_chunk", launch_global_fwd_chunk(g, n, st));
     if (final_state)
-      HIP_TRY(launch_copy_final(g.states, g.nslots, y.BH, 4 * y.hd, y.g_chunks % g.nslots,
+      HIP_TIMED("copy_final", launch_copy_final(g.states, g.nslots, y.BH, 4 * y.hd, y.g_chunks % g.nslots,
                                 final_state, st));
     m = 1;
   }
@@ -201,9 +239,9 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.scratch = ws + y.w_scr[i];
     a.plan = y.lplan[i];
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
-    HIP_TRY(launch_local_fwd(a, y.l_units[i], st));
+    HIP_TIMED("local_fwd", launch_local_fwd(a, y.l_units[i], st));
   }
-  if (o) HIP_TRY(launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, c->dtype == TNT_BF16, st));
+  if (o) HIP_TIMED("sum_out", launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, c->dtype == TNT_BF16, st));
   return TNT_OK;
 }
 
@@ -238,11 +276,11 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     g.dq_part = dqp; g.dk_part = dkp; g.dv_part = dvp;
     g.dlr = dlr; g.dmom = dmom; g.ddecay = ddecay;
     g.D = dims_of(c, c->C_G, c->L);
-    HIP_TRY(launch_global_scan(g, st));
-    HIP_TRY(launch_global_bwd_zero(g, y.g_chunks & 1, st));
-    for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TRY(launch_global_bwd_chunk(g, n, st));
-    HIP_TRY(launch_global_gate_bwd(g, st));
-    HIP_TRY(launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
+    HIP_TIMED("global_scan", launch_global_scan(g, st));
+    HIP_TIMED("global_bwd_zero", launch_global_bwd_zero(g, y.g_chunks & 1, st));
+    for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TIMED("global_bwd_chunk", launch_global_bwd_chunk(g, n, st));
+    HIP_TIMED("global_gate_bwd", launch_global_gate_bwd(g, st));
+    HIP_TIMED("reduce_init", launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
     m = 1;
   }
   for (int i = 0; i < c->n_local; ++i, ++m) {
@@ -262,15 +300,15 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.scratch = ws + y.b_scr[i];
     a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
-    HIP_TRY(launch_local_bwd(a, y.l_units[i], st));
-    HIP_TRY(launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
+    HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
+    HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
                                c->d, c->hid, 0, st));
   }
   const int bf = c->dtype == TNT_BF16;
-  HIP_TRY(launch_sum_out(dqp, y.M, y.io_elems, y.io_elems, dq, bf, st));
-  HIP_TRY(launch_sum_out(dkp, y.M, y.io_elems, y.io_elems, dk, bf, st));
-  HIP_TRY(launch_sum_out(dvp, y.M, y.io_elems, y.io_elems, dv, bf, st));
+  HIP_TIMED("sum_grads", launch_sum_out(dqp, y.M, y.io_elems, y.io_elems, dq, bf, st));
+  HIP_TIMED("sum_grads", launch_sum_out(dkp, y.M, y.io_elems, y.io_elems, dk, bf, st));
+  HIP_TIMED("sum_grads", launch_sum_out(dvp, y.M, y.io_elems, y.io_elems, dv, bf, st));
   return TNT_OK;
 }
 
@@ -279,6 +317,47 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
 extern "C" {
 
 int32_t tnt_abi_version(void) { return 1; }
+
+int32_t tnt_timing_enable(int32_t on) {
+  const int32_t prev = g_timing.on ? 1 : 0;
+  g_timing.on = on != 0;
+  return prev;
+}
+
+int32_t tnt_timing_read(int32_t max, char* names, double* total_ms, int32_t* launches) {
+  std::vector<std::string> keys;
+  std::vector<double> ms;
+  std::vector<int32_t> cnt;
+  int32_t status = 0;
+  for (const TimedLaunch& t : g_timing.rec) {
+    float e = 0.f;
+    if (hipEventSynchronize(t.b) != hipSuccess || hipEventElapsedTime(&e, t.a, t.b) != hipSuccess)
+      status = -1;
+    size_t i = 0;
+    while (i < keys.size() && keys[i] != t.name) ++i;
+    if (i == keys.size()) {
+      keys.emplace_back(t.name);
+      ms.push_back(0.0);
+      cnt.push_back(0);
+    }
+    ms[i] += e;
+    cnt[i] += 1;
+    g_timing.pool.push_back(t.a);
+    g_timing.pool.push_back(t.b);
+  }
+  g_timing.rec.clear();
+  if (status) return status;
+  const int32_t n = std::min<int32_t>(max, (int32_t)keys.size());
+  for (int32_t i = 0; i < n; ++i) {
+    if (names) {
+      std::strncpy(names + 32 * i, keys[i].c_str(), 31);
+      names[32 * i + 31] = 0;
+    }
+    if (total_ms) total_ms[i] = ms[i];
+    if (launches) launches[i] = cnt[i];
+  }
+  return n;
+}
 
 const char* tnt_strerror(tnt_status s) {
   switch (s) {

@@ -23,7 +23,7 @@ TNT_WS_FWD, TNT_WS_BWD, TNT_WS_BWD_RECOMPUTE = 0, 1, 2
 STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPPORTED",
           4: "TNT_ERR_WORKSPACE", 5: "TNT_ERR_ALIGN", 6: "TNT_ERR_HIP", 7: "TNT_ERR_ARG"}
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
-            "tnt_strerror", "tnt_abi_version"]
+            "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read"]
 
 
 class TntError(RuntimeError):
@@ -65,6 +65,11 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_strerror.restype = ctypes.c_char_p
     L.tnt_abi_version.argtypes = []
     L.tnt_abi_version.restype = i32
+    L.tnt_timing_enable.argtypes = [i32]
+    L.tnt_timing_enable.restype = i32
+    L.tnt_timing_read.argtypes = [i32, ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(i32)]
+    L.tnt_timing_read.restype = i32
     if path is None:
         _lib = L
     return L
@@ -123,6 +128,26 @@ def tnt_mem_bwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, dO, saved, dq, d
                              _p(W1_init), _p(W2_init), _p(dO), _p(saved), _p(dq), _p(dk),
                              _p(dv), _p(dlr), _p(dmom), _p(ddecay), _p(dW1_init),
                              _p(dW2_init), _p(workspace), ws_bytes, _stream(stream))
+
+
+def tnt_timing_enable(on: bool) -> int:
+    return lib().tnt_timing_enable(1 if on else 0)
+
+
+def tnt_timing_read(max_entries: int = 64) -> Dict[str, tuple]:
+    """{kernel name: (total ms, launches)} of the launches recorded while
+    timing was enabled; clears the record."""
+    names = ctypes.create_string_buffer(32 * max_entries)
+    ms = (ctypes.c_double * max_entries)()
+    cnt = (ctypes.c_int32 * max_entries)()
+    n = lib().tnt_timing_read(max_entries, names, ms, cnt)
+    if n < 0:
+        raise RuntimeError("tnt_timing_read: HIP error")
+    out = {}
+    for i in range(n):
+        nm = names.raw[32 * i: 32 * i + 32].split(b"\0", 1)[0].decode()
+        out[nm] = (ms[i], cnt[i])
+    return out
 
 
 # --------------------------------------------------------------------------
