@@ -9,7 +9,8 @@
  * each updated in chunks of C_L[i] tokens and reset to its learned initial
  * state every S_L[i] tokens.  Every memory is the MLP f(W, x) = W2 s(W1 x)
  * (W1: hid x d, W2: d x hid, s = GELU or SiLU) trained at test time by
- * gradient steps on the recall loss ||f(W, k_t) - v_t||^2 (Sec. 2.1).  All
+ * gradient steps on the recall loss (1/d) ||f(W, k_t) - v_t||^2, the mean
+ * squared error of Sec. 2.1.  All
  * gradients of a chunk are taken at the chunk-entry weights (Sec. 2.2) and
  * accumulated with momentum and decay (App. D):
  *     S_t = mom_t * S_{t-1} - lr_t * u_t,     W_t = (1 - decay_t) * W_{t-1} + S_t.
@@ -40,10 +41,11 @@
  *    nothing.  Asynchronous faults surface at the caller's synchronisation.
  *  - Gates: mom must lie in (0, 1] and decay in [0, 1); logarithms of mom are
  *    clamped at -80, so mom below e^-80 acts as e^-80.
- *  - Calls on different streams with distinct workspaces may run
- *    concurrently; the library keeps no mutable global state apart from one
- *    lazily created helper stream per device used to overlap the global and
- *    local memories.
+ *  - The global memory's chunk chain runs on a helper stream that the library
+ *    creates (default priority) on first use for each device, forked from and
+ *    joined back into `stream` with events, so it overlaps the local memories.
+ *    Calls from several host threads serialise their enqueue on a lock; calls
+ *    on different streams with distinct workspaces may run concurrently.
  */
 #ifndef TNT_H_
 #define TNT_H_

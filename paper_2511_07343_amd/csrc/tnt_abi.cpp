@@ -3,7 +3,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -156,6 +158,13 @@ Layout layout_of(const tnt_config* c) {
 
 bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
 
+// TNT_GENERIC_KERNELS=1 in the environment routes every shape through the
+// runtime-sized kernels (used by the tests to cover both kernel families).
+int generic_only() {
+  const char* e = std::getenv("TNT_GENERIC_KERNELS");
+  return (e && e[0] == '1') ? 1 : 0;
+}
+
 // ---- opt-in launch timing (hipEvent pairs per launch)
 struct TimedLaunch {
   const char* name;
@@ -191,6 +200,33 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
   return e;
 }
 
+// ---- helper stream per device: the global memory's chain runs on it while
+// the local shards run on the caller's stream (they only meet at the sums).
+// Default priority; events are reused under a lock, so concurrent host
+// threads serialise their enqueues here.
+struct Fork {
+  hipStream_t side = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+};
+constexpr int MAX_DEV = 64;
+Fork g_fork[MAX_DEV];
+std::mutex g_fork_mu;
+
+hipError_t fork_of(Fork** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= MAX_DEV) return hipErrorInvalidDevice;
+  Fork& f = g_fork[dev];
+  if (!f.side) {
+    if ((e = hipStreamCreateWithFlags(&f.side, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.e0, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.e1, hipEventDisableTiming)) != hipSuccess) return e;
+  }
+  *out = &f;
+  return hipSuccess;
+}
+
 #define HIP_TRY(x)                         \
   do {                                     \
     if ((x) != hipSuccess) return TNT_ERR_HIP; \
@@ -206,6 +242,15 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
   const size_t G = y.gates;
   float* opart = (float*)(ws + y.w_opart);
   int m = 0;
+  std::unique_lock<std::mutex> lock(g_fork_mu);
+  Fork* fk = nullptr;
+  const hipStream_t main_st = st;
+  if (c->has_global && c->n_local) {
+    HIP_TRY(fork_of(&fk));
+    HIP_TRY(hipEventRecord(fk->e0, main_st));
+    HIP_TRY(hipStreamWaitEvent(fk->side, fk->e0, 0));
+    st = fk->side;
+  }
   if (c->has_global) {
     GlobalArgs g{};
     g.q = q; g.k = k; g.v = v;
@@ -218,6 +263,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     g.chunkc = (float*)(ws + y.w_chunkc);
     g.Rbuf = (float*)(ws + y.w_R);
     g.D = dims_of(c, c->C_G, c->L);
+    g.force_generic = generic_only();
     HIP_TIMED("global_scan", launch_global_scan(g, st));
     HIP_TIMED("global_init", launch_global_init(g, st));
     for (int n = 0; n < y.g_chunks; ++n) HIP_TIMED("global_fwd_chunk", launch_global_fwd_chunk(g, n, st));
@@ -226,6 +272,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
                                 final_state, st));
     m = 1;
   }
+  st = main_st;
   for (int i = 0; i < c->n_local; ++i, ++m) {
     LocalFwdArgs a{};
     a.q = q; a.k = k; a.v = v;
@@ -239,7 +286,12 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.scratch = ws + y.w_scr[i];
     a.plan = y.lplan[i];
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
+    a.force_generic = generic_only();
     HIP_TIMED("local_fwd", launch_local_fwd(a, y.l_units[i], st));
+  }
+  if (fk) {
+    HIP_TRY(hipEventRecord(fk->e1, fk->side));
+    HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
   }
   if (o) HIP_TIMED("sum_out", launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, c->dtype == TNT_BF16, st));
   return TNT_OK;
@@ -256,6 +308,15 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
   float* dkp = dparts + (size_t)y.M * y.io_elems;
   float* dvp = dparts + 2 * (size_t)y.M * y.io_elems;
   int m = 0;
+  std::unique_lock<std::mutex> lock(g_fork_mu);
+  Fork* fk = nullptr;
+  const hipStream_t main_st = st;
+  if (c->has_global && c->n_local) {
+    HIP_TRY(fork_of(&fk));
+    HIP_TRY(hipEventRecord(fk->e0, main_st));
+    HIP_TRY(hipStreamWaitEvent(fk->side, fk->e0, 0));
+    st = fk->side;
+  }
   if (c->has_global) {
     GlobalArgs g{};
     g.q = q; g.k = k; g.v = v; g.dO = dO;
@@ -276,6 +337,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     g.dq_part = dqp; g.dk_part = dkp; g.dv_part = dvp;
     g.dlr = dlr; g.dmom = dmom; g.ddecay = ddecay;
     g.D = dims_of(c, c->C_G, c->L);
+    g.force_generic = generic_only();
     HIP_TIMED("global_scan", launch_global_scan(g, st));
     HIP_TIMED("global_bwd_zero", launch_global_bwd_zero(g, y.g_chunks & 1, st));
     for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TIMED("global_bwd_chunk", launch_global_bwd_chunk(g, n, st));
@@ -283,6 +345,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     HIP_TIMED("reduce_init", launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
     m = 1;
   }
+  st = main_st;
   for (int i = 0; i < c->n_local; ++i, ++m) {
     LocalBwdArgs a{};
     a.q = q; a.k = k; a.v = v; a.dO = dO;
@@ -300,10 +363,15 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.scratch = ws + y.b_scr[i];
     a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
+    a.force_generic = generic_only();
     HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
     HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
                                c->d, c->hid, 0, st));
+  }
+  if (fk) {
+    HIP_TRY(hipEventRecord(fk->e1, fk->side));
+    HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
   }
   const int bf = c->dtype == TNT_BF16;
   HIP_TIMED("sum_grads", launch_sum_out(dqp, y.M, y.io_elems, y.io_elems, dq, bf, st));

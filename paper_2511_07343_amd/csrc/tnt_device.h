@@ -146,6 +146,7 @@ __device__ __forceinline__ void mma_tile(f4& acc, const EA* A, int lda, int i0, 
   const int l = lane_id();
   const int ko = Mma<CT>::kofs(l);
   const int ia = i0 + (l & 15), jb = j0 + (l & 15);
+#pragma unroll
   for (int k0 = 0; k0 < K; k0 += Mma<CT>::KS) {
     auto a = Mma<CT>::template load<LA>(A, lda, ia, k0 + ko, K, kscale);
     auto b = Mma<CT>::template load<LB>(B, ldb, jb, k0 + ko, K, nullptr);

@@ -59,11 +59,11 @@ size_t global_bwd_scratch_bytes(const Dims& D, size_t* f32_off) {
   return ct_bytes + wgs * y.f_elems * sizeof(float);
 }
 
-template <typename IO, typename CT, int ACT>
+template <typename IO, typename CT, int ACT, int D_, int H_>
 __global__ void __launch_bounds__(256) gbwd_a_kernel(GlobalArgs a, int n, void* scratch,
                                                      size_t f32_off) {
   const Dims D = a.D;
-  const int d = D.d, h = D.hid, C = D.C;
+  const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, C = D.C;
   const int chain = blockIdx.y;
   const int r0 = blockIdx.x * GB_TT;
   const int rows = min(GB_TT, C - r0);
@@ -243,11 +243,11 @@ __global__ void __launch_bounds__(256) gbwd_a_kernel(GlobalArgs a, int n, void* 
 constexpr int GBB_HS = 16;
 constexpr int GBB_TT = 32;
 
-template <typename IO, typename CT, int ACT>
+template <typename IO, typename CT, int ACT, int D_, int H_>
 __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
   extern __shared__ __align__(16) unsigned char smem[];
   const Dims D = a.D;
-  const int d = D.d, h = D.hid, C = D.C;
+  const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, C = D.C;
   const int chain = blockIdx.y, hh = chain % D.H;
   const int s0 = blockIdx.x * GBB_HS;
   const size_t hd = (size_t)h * d;
@@ -392,17 +392,34 @@ __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
   (void)hh;
 }
 
+template <typename IO, typename CT, int ACT, int D_, int H_>
+static hipError_t launch_gbwd_dims(const GlobalArgs& a, int n, void* scratch, size_t f32_off,
+                                   hipStream_t st) {
+  const Dims& D = a.D;
+  dim3 ga((D.C + GB_TT - 1) / GB_TT, D.B * D.H);
+  hipLaunchKernelGGL((gbwd_a_kernel<IO, CT, ACT, D_, H_>), ga, dim3(256), 0, st, a, n, scratch, f32_off);
+  dim3 gb(D.hid / GBB_HS, D.B * D.H);
+  const size_t lds = (10 * (size_t)GBB_TT * D.d + 5 * GBB_HS * GBB_TT) * sizeof(CT);
+  set_lds_limit((const void*)gbwd_b_kernel<IO, CT, ACT, D_, H_>);
+  hipLaunchKernelGGL((gbwd_b_kernel<IO, CT, ACT, D_, H_>), gb, dim3(256), lds, st, a, n);
+  return hipGetLastError();
+}
+
 template <typename IO, typename CT, int ACT>
 static hipError_t launch_gbwd_t(const GlobalArgs& a, int n, void* scratch, size_t f32_off,
                                 hipStream_t st) {
-  const Dims& D = a.D;
-  dim3 ga((D.C + GB_TT - 1) / GB_TT, D.B * D.H);
-  hipLaunchKernelGGL((gbwd_a_kernel<IO, CT, ACT>), ga, dim3(256), 0, st, a, n, scratch, f32_off);
-  dim3 gb(D.hid / GBB_HS, D.B * D.H);
-  const size_t lds = (10 * (size_t)GBB_TT * D.d + 5 * GBB_HS * GBB_TT) * sizeof(CT);
-  set_lds_limit((const void*)gbwd_b_kernel<IO, CT, ACT>);
-  hipLaunchKernelGGL((gbwd_b_kernel<IO, CT, ACT>), gb, dim3(256), lds, st, a, n);
-  return hipGetLastError();
+  if (!a.force_generic) {
+    if constexpr (sizeof(IO) == 2) {
+      if (a.D.d == 64 && a.D.hid == 256)
+        return launch_gbwd_dims<IO, CT, ACT, 64, 256>(a, n, scratch, f32_off, st);
+      if (a.D.d == 128 && a.D.hid == 512)
+        return launch_gbwd_dims<IO, CT, ACT, 128, 512>(a, n, scratch, f32_off, st);
+    } else {
+      if (a.D.d == 16 && a.D.hid == 32)
+        return launch_gbwd_dims<IO, CT, ACT, 16, 32>(a, n, scratch, f32_off, st);
+    }
+  }
+  return launch_gbwd_dims<IO, CT, ACT, 0, 0>(a, n, scratch, f32_off, st);
 }
 
 hipError_t launch_global_bwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {

@@ -120,11 +120,11 @@ static int g1_rows(const Dims& D) {
 }
 
 // ---- phase 1: retrieval at the chunk-entry state and R = (2/d) (f(V, k) - v)
-template <typename IO, typename CT, int ACT>
+template <typename IO, typename CT, int ACT, int D_, int H_>
 __global__ void __launch_bounds__(256) global_p1_kernel(GlobalArgs a, int n, int TT) {
   extern __shared__ __align__(16) unsigned char smem[];
   const Dims D = a.D;
-  const int d = D.d, h = D.hid, C = D.C;
+  const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, C = D.C;
   const int chain = blockIdx.y;
   const int r0 = blockIdx.x * TT;                 // first row of the tile inside the chunk
   const int rows = min(TT, C - r0);
@@ -174,11 +174,11 @@ static int g2_rows(const Dims& D) {
   return 16;
 }
 
-template <typename IO, typename CT, int ACT>
+template <typename IO, typename CT, int ACT, int D_, int H_>
 __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int TT) {
   extern __shared__ __align__(16) unsigned char smem[];
   const Dims D = a.D;
-  const int d = D.d, h = D.hid, C = D.C;
+  const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, C = D.C;
   const int chain = blockIdx.y;
   const int s0 = blockIdx.x * G2_HS;
   const size_t hd = (size_t)h * d;
@@ -269,21 +269,35 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
   }
 }
 
-template <typename IO, typename CT, int ACT>
-static hipError_t launch_gfwd_t(const GlobalArgs& a, int n, hipStream_t st) {
+template <typename IO, typename CT, int ACT, int D_, int H_>
+static hipError_t launch_gfwd_dims(const GlobalArgs& a, int n, hipStream_t st) {
   const Dims& D = a.D;
   const int TT = g1_rows(D);
   const size_t cts = sizeof(CT);
   dim3 g1((D.C + TT - 1) / TT, D.B * D.H);
   const size_t l1 = (2 * (size_t)TT * D.d + (size_t)TT * D.hid) * cts;
-  set_lds_limit((const void*)global_p1_kernel<IO, CT, ACT>);
-  hipLaunchKernelGGL((global_p1_kernel<IO, CT, ACT>), g1, dim3(256), l1, st, a, n, TT);
+  set_lds_limit((const void*)global_p1_kernel<IO, CT, ACT, D_, H_>);
+  hipLaunchKernelGGL((global_p1_kernel<IO, CT, ACT, D_, H_>), g1, dim3(256), l1, st, a, n, TT);
   const int T2 = g2_rows(D);
   dim3 g2(D.hid / G2_HS, D.B * D.H);
   const size_t l2 = (6 * (size_t)T2 * D.d + 2 * (size_t)G2_HS * T2) * cts;
-  set_lds_limit((const void*)global_p2_kernel<IO, CT, ACT>);
-  hipLaunchKernelGGL((global_p2_kernel<IO, CT, ACT>), g2, dim3(256), l2, st, a, n, T2);
+  set_lds_limit((const void*)global_p2_kernel<IO, CT, ACT, D_, H_>);
+  hipLaunchKernelGGL((global_p2_kernel<IO, CT, ACT, D_, H_>), g2, dim3(256), l2, st, a, n, T2);
   return hipGetLastError();
+}
+
+template <typename IO, typename CT, int ACT>
+static hipError_t launch_gfwd_t(const GlobalArgs& a, int n, hipStream_t st) {
+  if (!a.force_generic) {
+    if constexpr (sizeof(IO) == 2) {
+      if (a.D.d == 64 && a.D.hid == 256) return launch_gfwd_dims<IO, CT, ACT, 64, 256>(a, n, st);
+      if (a.D.d == 128 && a.D.hid == 512)
+        return launch_gfwd_dims<IO, CT, ACT, 128, 512>(a, n, st);
+    } else {
+      if (a.D.d == 16 && a.D.hid == 32) return launch_gfwd_dims<IO, CT, ACT, 16, 32>(a, n, st);
+    }
+  }
+  return launch_gfwd_dims<IO, CT, ACT, 0, 0>(a, n, st);
 }
 
 hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {

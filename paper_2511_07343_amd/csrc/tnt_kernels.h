@@ -42,6 +42,7 @@ struct LocalFwdArgs {
   void* scratch;                                         // units * plan.elems CT
   LocalPlan plan;
   Dims D;
+  int force_generic;                                     // 1: skip fixed-size kernels
 };
 
 struct LocalBwdArgs {
@@ -59,6 +60,7 @@ struct LocalBwdArgs {
   float* scratch_f32;                                    // units * plan.f32_elems
   LocalPlan plan;
   Dims D;
+  int force_generic;                                     // 1: skip fixed-size kernels
 };
 
 struct GlobalArgs {
@@ -82,6 +84,7 @@ struct GlobalArgs {
   void* scratch;                                         // phase-A scratch of the backward
   size_t scratch_f32_off;
   Dims D;
+  int force_generic;                                     // 1: skip fixed-size kernels
 };
 
 constexpr int TKS = 8;  // floats per token in GlobalArgs::tokc
@@ -96,6 +99,7 @@ inline void set_lds_limit(const void* fn) {
 size_t local_plan(const Dims& D, LocalPlan* p, bool backward);
 
 hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st);
+bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err);
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st);
 hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st);

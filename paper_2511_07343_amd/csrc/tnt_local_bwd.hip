@@ -42,13 +42,16 @@ __device__ __forceinline__ void tiles(int M, int N, F&& f) {
   for (int t = wave_id(); t < nt; t += num_waves()) f((t / tn) << 4, (t % tn) << 4);
 }
 
-template <typename IO, typename CT, int ACT>
+// D_, H_, CP_ > 0 fix the head dim, hidden width and padded chunk at compile
+// time (all loops unrolled, buffer offsets constant); 0 reads them from `a`.
+template <typename IO, typename CT, int ACT, int D_, int H_, int CP_>
 __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
   __shared__ Coef cf;
   __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC], gEta[MAXC], gLa[MAXC], gLb[MAXC];
   __shared__ float red[32];
   const Dims D = a.D;
-  const int d = D.d, h = D.hid, C = D.C, Cp = D.Cp;
+  const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, Cp = CP_ ? CP_ : D.Cp;
+  const int C = D.C;
   const int nshard = D.L / D.S;
   const int u = blockIdx.x;
   const int b = u / (D.H * nshard), hh = (u / nshard) % D.H, s = u % nshard;
@@ -554,19 +557,37 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
   for (size_t e = threadIdx.x; e < 2 * hd; e += blockDim.x) dst[e] = adj[e];
 }
 
-template <typename IO, typename CT>
-static hipError_t launch_local_bwd_t(const LocalBwdArgs& a, int units, hipStream_t st) {
-  dim3 grid(units), block(512);
-  if (a.D.act == ACT_GELU)
-    hipLaunchKernelGGL((local_bwd_kernel<IO, CT, ACT_GELU>), grid, block, 0, st, a);
-  else
-    hipLaunchKernelGGL((local_bwd_kernel<IO, CT, ACT_SILU>), grid, block, 0, st, a);
-  return hipGetLastError();
+template <typename IO, typename CT, int ACT, int D_, int H_, int CP_>
+static bool try_bwd(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err) {
+  if (D_ && (a.D.d != D_ || a.D.hid != H_ || a.D.Cp != CP_)) return false;
+  if (a.D.act != ACT) return false;
+  hipLaunchKernelGGL((local_bwd_kernel<IO, CT, ACT, D_, H_, CP_>), dim3(units), dim3(512), 0,
+                     st, a);
+  *err = hipGetLastError();
+  return true;
 }
 
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st) {
-  if (a.D.bf16) return launch_local_bwd_t<__bf16, __bf16>(a, units, st);
-  return launch_local_bwd_t<float, float>(a, units, st);
+  hipError_t e = hipSuccess;
+  const bool fixed = !a.force_generic;
+  if (a.D.bf16) {
+    if (fixed && (try_bwd<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, units, st, &e) ||
+                  try_bwd<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, units, st, &e) ||
+                  try_bwd<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, units, st, &e) ||
+                  try_bwd<__bf16, __bf16, ACT_SILU, 128, 512, 64>(a, units, st, &e)))
+      return e;
+    if (try_bwd<__bf16, __bf16, ACT_GELU, 0, 0, 0>(a, units, st, &e) ||
+        try_bwd<__bf16, __bf16, ACT_SILU, 0, 0, 0>(a, units, st, &e))
+      return e;
+  } else {
+    if (fixed && (try_bwd<float, float, ACT_GELU, 16, 32, 16>(a, units, st, &e) ||
+                  try_bwd<float, float, ACT_SILU, 16, 32, 16>(a, units, st, &e)))
+      return e;
+    if (try_bwd<float, float, ACT_GELU, 0, 0, 0>(a, units, st, &e) ||
+        try_bwd<float, float, ACT_SILU, 0, 0, 0>(a, units, st, &e))
+      return e;
+  }
+  return hipErrorInvalidValue;
 }
 
 // dW_init[h] = sum over batch rows and shards of the per-unit adjoints

@@ -250,6 +250,8 @@ static hipError_t launch_local_fwd_t(const LocalFwdArgs& a, int units, hipStream
 }
 
 hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st) {
+  hipError_t e = hipSuccess;
+  if (!a.force_generic && launch_local_fwd_fast(a, units, st, &e)) return e;
   if (a.D.bf16) return launch_local_fwd_t<__bf16, __bf16>(a, units, st);
   return launch_local_fwd_t<float, float>(a, units, st);
 }

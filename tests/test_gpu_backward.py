@@ -101,3 +101,14 @@ def test_backward_deterministic():
     b = gpu_backward(cfg, inp)
     for n in GRADS:
         assert np.array_equal(a[n], b[n]), n
+
+
+@pytest.mark.parametrize("cfg", [WORKLOADS[0], SMALL[2], SMALL[7]], ids=lambda c: c.name)
+def test_backward_generic_kernels(cfg, monkeypatch):
+    """The runtime-sized kernels against the oracle (the fixed-size ones are
+    what the default path takes for these shapes)."""
+    inp = make_inputs(cfg, 204)
+    monkeypatch.setenv("TNT_GENERIC_KERNELS", "1")
+    print(f"\n[case] generic {cfg.name}", flush=True)
+    got = gpu_backward(cfg, inp)
+    check(cfg, got, oracle_backward(cfg, inp))

@@ -118,3 +118,17 @@ def test_forward_full_size_sampled_chain(idx):
     err = max_rel_err(got[b, h], ref)
     print(f"chain ({b},{h}) o max rel err {err:.3e}", flush=True)
     assert err <= tol(cfg)
+
+
+@pytest.mark.parametrize("cfg", [WORKLOADS[0], SMALL[0], SMALL[2], SMALL[4]], ids=lambda c: c.name)
+def test_forward_generic_kernels(cfg, monkeypatch):
+    """The runtime-sized kernels (used for shapes without a fixed-size kernel)
+    against the oracle, and against the fixed-size kernels where both exist."""
+    inp = make_inputs(cfg, 105)
+    fast, _ = gpu_forward(cfg, inp)
+    monkeypatch.setenv("TNT_GENERIC_KERNELS", "1")
+    gen, _ = gpu_forward(cfg, inp)
+    ref = O.forward_pairs(inp, cfg, O.all_pairs(cfg)).numpy().reshape(gen.shape)
+    e_gen, e_fast = max_rel_err(gen, ref), max_rel_err(fast, ref)
+    print(f"\n[case] {cfg.name}: generic {e_gen:.3e} fixed-size {e_fast:.3e}", flush=True)
+    assert e_gen <= tol(cfg) and e_fast <= tol(cfg)
