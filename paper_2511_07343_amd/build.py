@@ -23,7 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wno-unused-result", "-I", os.path.join(ROOT, "include"),
+    "-Wno-unused-result", "-Wno-pass-failed", "-I", os.path.join(ROOT, "include"),
 ]
 
 

@@ -156,6 +156,39 @@ __device__ __forceinline__ void mma_tile(f4& acc, const EA* A, int lda, int i0, 
 
 __device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
 
+// A fragment loaded raw from a contraction-contiguous (KC) source and
+// converted to the MFMA operand type later, so that many loads can be in
+// flight before the first conversion waits for its data.
+template <typename CT, typename E> struct RawFrag;
+template <> struct RawFrag<__bf16, float> {
+  f32x4 a, b;
+  __device__ __forceinline__ void load(const float* p, int ld, int idx, int kb) {
+    const float* q = p + (size_t)idx * ld + kb;
+    a = *reinterpret_cast<const f32x4*>(q);
+    b = *reinterpret_cast<const f32x4*>(q + 4);
+  }
+  __device__ __forceinline__ bf16x8 get() const {
+    bf16x8 f;
+    f[0] = (__bf16)a[0]; f[1] = (__bf16)a[1]; f[2] = (__bf16)a[2]; f[3] = (__bf16)a[3];
+    f[4] = (__bf16)b[0]; f[5] = (__bf16)b[1]; f[6] = (__bf16)b[2]; f[7] = (__bf16)b[3];
+    return f;
+  }
+};
+template <> struct RawFrag<__bf16, __bf16> {
+  bf16x8 v;
+  __device__ __forceinline__ void load(const __bf16* p, int ld, int idx, int kb) {
+    v = *reinterpret_cast<const bf16x8*>(p + (size_t)idx * ld + kb);
+  }
+  __device__ __forceinline__ bf16x8 get() const { return v; }
+};
+template <> struct RawFrag<float, float> {
+  float v;
+  __device__ __forceinline__ void load(const float* p, int ld, int idx, int kb) {
+    v = p[(size_t)idx * ld + kb];
+  }
+  __device__ __forceinline__ float get() const { return v; }
+};
+
 // visit the 4 elements a lane holds of the 16x16 tile at (i0, j0)
 template <typename F>
 __device__ __forceinline__ void tile_each(const f4& acc, int i0, int j0, F&& f) {

@@ -4,9 +4,10 @@
 // a compile-time trip count and every chunk intermediate stays on chip:
 //
 //   LDS  Hk [CP][HID]   s(K W1^T)                         bf16/fp32 (CT)
-//        D1 [CP][HID]   (R W2) * s'(K W1^T)
-//        U  [CP][HID]   reused in turn: Q-K temporaries (Q, N, N^T, tril(Q N^T)),
-//                       then the chunk-entry W2 (CT copy, [D][HID]), then H = s(Z)
+//        D1^T [HID][CP] ((R W2) * s'(K W1^T))^T
+//        U              reused in turn: Q-K temporaries (Q, N, N^T, tril(Q N^T)),
+//                       the chunk-entry W2 (CT copy, [D][HID]), K^T and R^T for the
+//                       carry, then H = s(Z) [CP][HID]
 //        X, K, R [CP][D], P [CP][CP], gate coefficients
 //   VGPR s'(K W1^T) between the two GEMMs that share its output tiles
 //
@@ -103,8 +104,12 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   using Ly = FwdLds<D, HID, CP>;
   constexpr int NW = 8;                       // waves
   constexpr int TNH = HID / 16, TMC = CP / 16;
-  constexpr int TILES_CH = TMC * TNH;         // tiles of a CP x HID result
-  constexpr int PER_WAVE = (TILES_CH + NW - 1) / NW;
+  constexpr int KS = Mma<CT>::KS;
+  constexpr int NKD = D / KS, NKH = HID / KS;
+  constexpr int NS = (TNH + NW - 1) / NW;     // 16-column strips of HID per wave
+  static_assert(NW % (D / 16) == 0, "one column strip of D per wave");
+  static_assert((HID / 16) * (D / 16) % NW == 0, "state tiles spread evenly over waves");
+  static_assert((size_t)HID * D % (512 * 4) == 0, "W2 copy in whole float4s per thread");
   CT* L = (CT*)smem;
   CT *sHk = L + Ly::Hk, *sD1 = L + Ly::D1, *sU = L + Ly::U, *sX = L + Ly::X, *sK = L + Ly::K,
      *sR = L + Ly::R, *sP = L + Ly::P;
@@ -132,6 +137,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
   const float rscale = 2.0f / (float)D;
   const int l = lane_id(), w = wave_id();
+  const int ko = Mma<CT>::kofs(l);
 
   {
     const float* W1i = a.W1i + hh * hd;
@@ -159,31 +165,41 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     const float* Mc = mst + (size_t)(n % a.nslots) * D * D;
     float* Mn = mst + (size_t)((n + 1) % a.nslots) * D * D;
 
-    // ---- stage Q, K (rows >= C zero), unit keys, gate coefficients
-    for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
-      const int i = e / D;
-      const bool in = i < C;
-      sQ[e] = from_f<CT>(in ? to_f(q[(size_t)tok0 * D + e]) : 0.f);
-      sK[e] = from_f<CT>(in ? to_f(k[(size_t)tok0 * D + e]) : 0.f);
-    }
-    if (qk) {
-      for (int i = w; i < CP; i += NW) {
-        float ss = 0.f;
-        if (i < C)
-          for (int j = l; j < D; j += WAVE) {
-            const float x = to_f(k[(size_t)(tok0 + i) * D + j]);
-            ss += x * x;
+    // ---- stage Q, K (16-byte loads; rows >= C zero), gate coefficients
+    {
+      constexpr int VEC = 16 / sizeof(IO);
+      for (int e = threadIdx.x * VEC; e < CP * D; e += blockDim.x * VEC) {
+        const int i = e / D;
+        if (i < C) {
+          const IO* pq = q + (size_t)tok0 * D + e;
+          const IO* pk = k + (size_t)tok0 * D + e;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) {
+            sQ[e + j] = from_f<CT>(to_f(pq[j]));
+            sK[e + j] = from_f<CT>(to_f(pk[j]));
           }
+        } else {
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) sQ[e + j] = sK[e + j] = from_f<CT>(0.f);
+        }
+      }
+    }
+    chunk_coefs_f(cf, lr, mom, dec, tok0, C, CP);  // barriers inside (K staged)
+    if (qk) {
+      for (int i = w; i < CP; i += NW) {  // key norms from LDS
+        float ss = 0.f;
+        for (int j = l; j < D; j += WAVE) {
+          const float x = to_f(sK[(size_t)i * D + j]);
+          ss += x * x;
+        }
         ss = wave_sum(ss);
         if (l == 0) cf.knorm[i] = sqrtf(ss);
       }
-    }
-    chunk_coefs_f(cf, lr, mom, dec, tok0, C, CP);  // barriers inside
-    if (qk) {
+      __syncthreads();
       for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
         const int i = e / D, j = e - i * D;
         const float nr = cf.knorm[i];
-        const float x = (i < C && nr > 0.f) ? to_f(k[(size_t)(tok0 + i) * D + j]) / nr : 0.f;
+        const float x = (i < C && nr > 0.f) ? to_f(sK[e]) / nr : 0.f;
         sN[e] = from_f<CT>(x);
         sNT[(size_t)j * CP + i] = from_f<CT>(x);
       }
@@ -193,115 +209,231 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       });
       __syncthreads();
       {
+        // X tiles: one column strip of D per wave (NW % (D/16) == 0)
         constexpr int tn = D / 16, nt = TMC * tn;
+        RawFrag<CT, float> bm[NKD];  // converted at use (small)
+        const int cs = w % tn;
+        if (shard_qk)
+#pragma unroll
+          for (int ks = 0; ks < NKD; ++ks) bm[ks].load(Mc, D, cs * 16 + (l & 15), ks * KS + ko);
         for (int t = w; t < nt; t += NW) {
-          const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
+          const int i0 = (t / tn) * 16, j0 = cs * 16;
           f4 acc = zero4();
-          if (shard_qk) mma_tile<CT, KC, KC>(acc, sQ, D, i0, Mc, D, j0, D);
+          if (shard_qk) {
+#pragma unroll
+            for (int ks = 0; ks < NKD; ++ks) {
+              auto a = Mma<CT>::template load<KC>(sQ, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
+              Mma<CT>::mma(acc, a, bm[ks].get());
+            }
+          }
           mma_tile<CT, KC, KC>(acc, sS, CP, i0, sNT, CP, j0, CP);
           tile_each(acc, i0, j0, [&](int i, int j, float x) { sX[(size_t)i * D + j] = from_f<CT>(x); });
         }
       }
-      if (shard_qk)
-        gemm<CT, KC, KC>(D, D, CP, sNT, CP, sNT, CP, [&](int i, int j, float x) {
-          Mn[(size_t)i * D + j] = Mc[(size_t)i * D + j] + x;
-        });
+      if (shard_qk) {
+        constexpr int tn = D / 16, nt = tn * tn;
+        for (int t = w; t < nt; t += NW) {
+          const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
+          float mo[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mo[r] = Mc[(size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15)];
+          f4 acc = zero4();
+          mma_tile<CT, KC, KC>(acc, sNT, CP, i0, sNT, CP, j0, CP);
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Mn[(size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15)] = mo[r] + acc[r];
+        }
+      }
     } else {
       for (int e = threadIdx.x; e < CP * D; e += blockDim.x) sX[e] = sQ[e];
     }
 
-    // ---- Zk = K W1^T -> Hk (LDS), s'(Zk) (registers)
-    f4 spr[PER_WAVE];
+    // ---- Zk = K W1^T -> Hk (LDS), s'(Zk) (registers); each wave owns NS column strips
+    CT spr[NS][TMC][4];  // s'(Zk) in the compute type
+    {
+      typename Mma<CT>::frag bw[NS][NKD];
+      {
+        RawFrag<CT, float> raw[NS][NKD];
 #pragma unroll
-    for (int x = 0; x < PER_WAVE; ++x) {
-      const int t = w + x * NW;
-      if (t < TILES_CH) {
-        const int i0 = (t / TNH) * 16, j0 = (t % TNH) * 16;
-        f4 acc = zero4();
-        mma_tile<CT, KC, KC>(acc, sK, D, i0, W1, D, j0, D);
+        for (int y = 0; y < NS; ++y) {
+          const int sidx = w + NW * y;
+          if (sidx < TNH)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          const ActVals av = act_all<ACT>(acc[r]);
-          sHk[(size_t)i * HID + j] = from_f<CT>(av.s);
-          spr[x][r] = av.d1;
+            for (int ks = 0; ks < NKD; ++ks) raw[y][ks].load(W1, D, sidx * 16 + (l & 15), ks * KS + ko);
+        }
+#pragma unroll
+        for (int y = 0; y < NS; ++y)
+#pragma unroll
+          for (int ks = 0; ks < NKD; ++ks) bw[y][ks] = raw[y][ks].get();
+      }
+#pragma unroll
+      for (int y = 0; y < NS; ++y) {
+        const int sidx = w + NW * y;
+        if (sidx >= TNH) continue;
+#pragma unroll
+        for (int it = 0; it < TMC; ++it) {
+          const int i0 = it * 16, j0 = sidx * 16;
+          f4 acc = zero4();
+#pragma unroll
+          for (int ks = 0; ks < NKD; ++ks) {
+            auto a = Mma<CT>::template load<KC>(sK, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
+            Mma<CT>::mma(acc, a, bw[y][ks]);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
+            const ActVals av = act_all<ACT>(acc[r]);
+            sHk[(size_t)i * HID + j] = from_f<CT>(av.s);
+            spr[y][it][r] = from_f<CT>(av.d1);
+          }
         }
       }
     }
     __syncthreads();  // Q-K temporaries in U are dead from here
-    // chunk-entry W2 -> U as CT [D][HID]
-    for (int e = threadIdx.x * 4; e < (int)hd; e += blockDim.x * 4) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(W2 + e);
+    // chunk-entry W2 -> U as CT [D][HID] (all loads first, then the LDS writes)
+    {
+      constexpr int PER = (int)(hd / (512 * 4));
+      f32x4 x[PER];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sW2[e + j] = from_f<CT>(x[j]);
+      for (int p = 0; p < PER; ++p)
+        x[p] = *reinterpret_cast<const f32x4*>(W2 + (size_t)(threadIdx.x + 512 * p) * 4);
+#pragma unroll
+      for (int p = 0; p < PER; ++p)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sW2[(size_t)(threadIdx.x + 512 * p) * 4 + j] = from_f<CT>(x[p][j]);
     }
     __syncthreads();
 
     // ---- R = (2/d) (Hk W2^T - V)
     {
       constexpr int tn = D / 16, nt = TMC * tn;
-      for (int t = w; t < nt; t += NW) {
+      constexpr int PT = (nt + NW - 1) / NW;
+      float vv[PT][4];
+#pragma unroll
+      for (int x = 0; x < PT; ++x) {
+        const int t = w + NW * x;
+        const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = i0 + 4 * (l >> 4) + r;
+          vv[x][r] = (t < nt && i < C) ? to_f(v[(size_t)(tok0 + i) * D + j0 + (l & 15)]) : 0.f;
+        }
+      }
+#pragma unroll
+      for (int x = 0; x < PT; ++x) {
+        const int t = w + NW * x;
+        if (t >= nt) continue;
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
         mma_tile<CT, KC, KC>(acc, sHk, HID, i0, sW2, HID, j0, HID);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          const float rv = (i < C) ? rscale * (acc[r] - to_f(v[(size_t)(tok0 + i) * D + j])) : 0.f;
+          const float rv = (i < C) ? rscale * (acc[r] - vv[x][r]) : 0.f;
           sR[(size_t)i * D + j] = from_f<CT>(rv);
         }
       }
     }
     __syncthreads();
 
-    // ---- D1 = (R W2) * s'(Zk), same tiles as Zk
+    // ---- D1 = (R W2) * s'(Zk), same strips as Zk
 #pragma unroll
-    for (int x = 0; x < PER_WAVE; ++x) {
-      const int t = w + x * NW;
-      if (t < TILES_CH) {
-        const int i0 = (t / TNH) * 16, j0 = (t % TNH) * 16;
+    for (int y = 0; y < NS; ++y) {
+      const int sidx = w + NW * y;
+      if (sidx >= TNH) continue;
+#pragma unroll
+      for (int it = 0; it < TMC; ++it) {
+        const int i0 = it * 16, j0 = sidx * 16;
         f4 acc = zero4();
         mma_tile<CT, KC, MC>(acc, sR, D, i0, sW2, HID, j0, D);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          sD1[(size_t)i * HID + j] = from_f<CT>(acc[r] * spr[x][r]);
+          sD1[(size_t)j * CP + i] = from_f<CT>(acc[r] * to_f(spr[y][it][r]));  // D1^T
         }
       }
     }
     __syncthreads();
 
-    // ---- carry into the next slot
+    // ---- K^T, R^T into U (the W2 copy is dead), then the carry
+    CT* sKT = sU;              // [D][CP]
+    CT* sRT = sU + CP * D;     // [D][CP]
+    for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
+      const int i = e / D, j = e - i * D;
+      sKT[(size_t)j * CP + i] = sK[e];
+      sRT[(size_t)j * CP + i] = sR[e];
+    }
+    __syncthreads();
     {
       constexpr int tn = D / 16, nt = (HID / 16) * tn;  // W1', S1' : HID x D
-      for (int t = w; t < nt; t += NW) {
+      constexpr int PT = nt / NW, BT = PT < 4 ? PT : 4;
+#pragma unroll 1
+      for (int xb = 0; xb < PT; xb += BT) {
+      float pw[BT][4], ps[BT][4];
+#pragma unroll
+      for (int xx = 0; xx < BT; ++xx) {
+        const int x = xb + xx;
+        const int t = w + NW * x;
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
-        f4 aw = zero4(), as = zero4();
-        // A[i][tau] = D1[tau][i] (x cC_tau or b_tau), B[tau][j] = K[tau][j]
-        mma_tile<CT, MC, MC>(aw, sD1, HID, i0, sK, D, j0, CP, cf.cC);
-        mma_tile<CT, MC, MC>(as, sD1, HID, i0, sK, D, j0, CP, cf.bb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15);
-          W1n[e] = cf.AC * W1[e] + cf.EC * S1[e] - aw[r];
-          S1n[e] = cf.BC * S1[e] - as[r];
+          pw[xx][r] = W1[e];
+          ps[xx][r] = S1[e];
         }
+      }
+#pragma unroll
+      for (int xx = 0; xx < BT; ++xx) {
+        const int x = xb + xx;
+        const int t = w + NW * x;
+        const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
+        f4 aw = zero4(), as = zero4();
+        // A[i][tau] = D1^T[i][tau] (x cC_tau or b_tau), B[tau][j] = K^T[j][tau]
+        mma_tile<CT, KC, KC>(aw, sD1, CP, i0, sKT, CP, j0, CP, cf.cC);
+        mma_tile<CT, KC, KC>(as, sD1, CP, i0, sKT, CP, j0, CP, cf.bb);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15);
+          W1n[e] = cf.AC * pw[xx][r] + cf.EC * ps[xx][r] - aw[r];
+          S1n[e] = cf.BC * ps[xx][r] - as[r];
+        }
+      }
       }
     }
     {
       constexpr int tn = HID / 16, nt = (D / 16) * tn;  // W2', S2' : D x HID
-      for (int t = w; t < nt; t += NW) {
+      constexpr int PT = nt / NW, BT = PT < 4 ? PT : 4;
+#pragma unroll 1
+      for (int xb = 0; xb < PT; xb += BT) {
+      float pw[BT][4], ps[BT][4];
+#pragma unroll
+      for (int xx = 0; xx < BT; ++xx) {
+        const int x = xb + xx;
+        const int t = w + NW * x;
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
-        f4 aw = zero4(), as = zero4();
-        // A[i][tau] = R[tau][i] (x cC_tau or b_tau), B[tau][j] = Hk[tau][j]
-        mma_tile<CT, MC, MC>(aw, sR, D, i0, sHk, HID, j0, CP, cf.cC);
-        mma_tile<CT, MC, MC>(as, sR, D, i0, sHk, HID, j0, CP, cf.bb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * HID + j0 + (l & 15);
-          W2n[e] = cf.AC * W2[e] + cf.EC * S2[e] - aw[r];
-          S2n[e] = cf.BC * S2[e] - as[r];
+          pw[xx][r] = W2[e];
+          ps[xx][r] = S2[e];
         }
+      }
+#pragma unroll
+      for (int xx = 0; xx < BT; ++xx) {
+        const int x = xb + xx;
+        const int t = w + NW * x;
+        const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
+        f4 aw = zero4(), as = zero4();
+        // A[i][tau] = R^T[i][tau] (x cC_tau or b_tau), B[tau][j] = Hk[tau][j]
+        mma_tile<CT, KC, MC>(aw, sRT, CP, i0, sHk, HID, j0, CP, cf.cC);
+        mma_tile<CT, KC, MC>(as, sRT, CP, i0, sHk, HID, j0, CP, cf.bb);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * HID + j0 + (l & 15);
+          W2n[e] = cf.AC * pw[xx][r] + cf.EC * ps[xx][r] - aw[r];
+          S2n[e] = cf.BC * ps[xx][r] - as[r];
+        }
+      }
       }
     }
 
@@ -317,21 +449,43 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         });
       }
     }
-    __syncthreads();  // P ready; the W2 copy in U is dead
+    {
+      __syncthreads();  // P ready; K^T / R^T in U are dead
 #pragma unroll
-    for (int x = 0; x < PER_WAVE; ++x) {
-      const int t = w + x * NW;
-      if (t < TILES_CH) {
-        const int i0 = (t / TNH) * 16, j0 = (t % TNH) * 16;
-        f4 a1 = zero4(), a2 = zero4(), a3 = zero4();
-        mma_tile<CT, KC, KC>(a1, sX, D, i0, W1, D, j0, D);
-        mma_tile<CT, KC, KC>(a2, sX, D, i0, S1, D, j0, D);
-        mma_tile<CT, KC, MC>(a3, sP, CP, i0, sD1, HID, j0, CP);
+      for (int y = 0; y < NS; ++y) {
+        const int sidx = w + NW * y;
+        if (sidx >= TNH) continue;
+        typename Mma<CT>::frag bw[NKD], bs[NKD];
+        {
+          RawFrag<CT, float> rw[NKD], rs[NKD];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          const float z = cf.A[i] * a1[r] + cf.E[i] * a2[r] - a3[r];
-          sH[(size_t)i * HID + j] = from_f<CT>(act_f<ACT>(z));
+          for (int ks = 0; ks < NKD; ++ks) {
+            rw[ks].load(W1, D, sidx * 16 + (l & 15), ks * KS + ko);
+            rs[ks].load(S1, D, sidx * 16 + (l & 15), ks * KS + ko);
+          }
+#pragma unroll
+          for (int ks = 0; ks < NKD; ++ks) {
+            bw[ks] = rw[ks].get();
+            bs[ks] = rs[ks].get();
+          }
+        }
+#pragma unroll 1
+        for (int it = 0; it < TMC; ++it) {
+          const int i0 = it * 16, j0 = sidx * 16;
+          f4 a1 = zero4(), a2 = zero4(), a3 = zero4();
+#pragma unroll
+          for (int ks = 0; ks < NKD; ++ks) {
+            auto a = Mma<CT>::template load<KC>(sX, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
+            Mma<CT>::mma(a1, a, bw[ks]);
+            Mma<CT>::mma(a2, a, bs[ks]);
+          }
+          mma_tile<CT, KC, KC>(a3, sP, CP, i0, sD1, CP, j0, CP);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
+            const float z = cf.A[i] * a1[r] + cf.E[i] * a2[r] - a3[r];
+            sH[(size_t)i * HID + j] = from_f<CT>(act_f<ACT>(z));
+          }
         }
       }
     }
@@ -347,19 +501,64 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         });
       }
     }
-    __syncthreads();
+    // O: one column strip of D per wave; the W2 / S2 strip is loaded in halves of HID
     {
       constexpr int tn = D / 16, nt = TMC * tn;
-      for (int t = w; t < nt; t += NW) {
-        const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
-        f4 a1 = zero4(), a2 = zero4(), a3 = zero4();
-        mma_tile<CT, KC, KC>(a1, sH, HID, i0, W2, HID, j0, HID);
-        mma_tile<CT, KC, KC>(a2, sH, HID, i0, S2, HID, j0, HID);
+      constexpr int PT = (nt + NW - 1) / NW;
+      constexpr int HALF = NKH < 2 ? NKH : 2;  // k-steps per batch of W2 / S2 loads
+      const int cs = w % tn;
+      f4 a1[PT], a2[PT];
+#pragma unroll
+      for (int x = 0; x < PT; ++x) a1[x] = a2[x] = zero4();
+      bool synced = false;
+#pragma unroll
+      for (int hb = 0; hb < NKH; hb += HALF) {
+        typename Mma<CT>::frag bw[HALF], bs[HALF];
+        {
+          RawFrag<CT, float> rw[HALF], rs[HALF];
+#pragma unroll
+          for (int kk = 0; kk < HALF; ++kk)
+            if (hb + kk < NKH) {
+              rw[kk].load(W2, HID, cs * 16 + (l & 15), (hb + kk) * KS + ko);
+              rs[kk].load(S2, HID, cs * 16 + (l & 15), (hb + kk) * KS + ko);
+            }
+#pragma unroll
+          for (int kk = 0; kk < HALF; ++kk) {
+            bw[kk] = rw[kk].get();
+            bs[kk] = rs[kk].get();
+          }
+        }
+        if (!synced) {
+          __syncthreads();  // Po ready
+          synced = true;
+        }
+#pragma unroll
+        for (int x = 0; x < PT; ++x) {
+          const int t = w + NW * x;
+          if (t >= nt) continue;
+          const int i0 = (t / tn) * 16;
+#pragma unroll
+          for (int kk = 0; kk < HALF; ++kk)
+            if (hb + kk < NKH) {
+              auto a = Mma<CT>::template load<KC>(sH, HID, i0 + (l & 15), (hb + kk) * KS + ko, HID,
+                                                  nullptr);
+              Mma<CT>::mma(a1[x], a, bw[kk]);
+              Mma<CT>::mma(a2[x], a, bs[kk]);
+            }
+        }
+      }
+#pragma unroll
+      for (int x = 0; x < PT; ++x) {
+        const int t = w + NW * x;
+        if (t >= nt) continue;
+        const int i0 = (t / tn) * 16, j0 = cs * 16;
+        f4 a3 = zero4();
         mma_tile<CT, KC, MC>(a3, sP, CP, i0, sR, D, j0, CP);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          if (i < C) o[(size_t)(tok0 + i) * D + j] = cf.A[i] * a1[r] + cf.E[i] * a2[r] - a3[r];
+          if (i < C)
+            o[(size_t)(tok0 + i) * D + j] = cf.A[i] * a1[x][r] + cf.E[i] * a2[x][r] - a3[r];
         }
       }
     }
@@ -388,8 +587,7 @@ bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hip
            try_fast<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, units, st, err) ||
            try_fast<__bf16, __bf16, ACT_GELU, 64, 256, 16>(a, units, st, err);
   }
-  return try_fast<float, float, ACT_GELU, 16, 32, 16>(a, units, st, err) ||
-         try_fast<float, float, ACT_SILU, 16, 32, 16>(a, units, st, err);
+  return false;  // fp32 shapes (the tiny smoke workload) take the runtime-sized kernel
 }
 
 }  // namespace tnt
