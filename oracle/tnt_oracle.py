@@ -273,17 +273,150 @@ def layer_forward(q, k, v, lr, mom, decay, W1, W2, cfg, ckpt: bool = False,
 
 
 def layer_backward(q, k, v, lr, mom, decay, W1, W2, dO, cfg, ckpt: bool = True):
-    """Gradients of sum <dO, o> with respect to every input (autograd through
-    the fp64 forward).  Returns a dict with dq, dk, dv [P,L,d], dlr, dmom,
-    ddecay [M,P,L], dW1 [M,P,h,d], dW2 [M,P,d,h] (per chain: the caller sums
-    chains that share a head) and o."""
-    leaves = [t.detach().clone().requires_grad_(True) for t in (q, k, v, lr, mom, decay, W1, W2)]
-    o = layer_forward(*leaves, cfg, ckpt=ckpt)
-    grads = torch.autograd.grad((o * dO).sum(), leaves)
-    names = ["dq", "dk", "dv", "dlr", "dmom", "ddecay", "dW1", "dW2"]
-    out = {n: g.detach() for n, g in zip(names, grads)}
-    out["o"] = o.detach()
+    """Gradients of sum <dO, o> with respect to every input.  Returns a dict
+    with dq, dk, dv [P,L,d], dlr, dmom, ddecay [M,P,L], dW1 [M,P,h,d],
+    dW2 [M,P,d,h] (per chain: the caller sums chains that share a head) and o.
+
+    ``ckpt=False``: one autograd pass through the whole forward (memory grows
+    with L).  ``ckpt=True``: the same gradients segment by segment -- a forward
+    without autograd stores the state entering each segment (a global chunk's
+    sub-block, a local chunk), then the segments are walked in reverse and each
+    one is differentiated by autograd of the same per-token code, the
+    adjoint of its exit state flowing into its entry state."""
+    if not ckpt:
+        leaves = [t.detach().clone().requires_grad_(True) for t in (q, k, v, lr, mom, decay, W1, W2)]
+        o = layer_forward(*leaves, cfg)
+        grads = torch.autograd.grad((o * dO).sum(), leaves)
+        names = ["dq", "dk", "dv", "dlr", "dmom", "ddecay", "dW1", "dW2"]
+        out = {n: g.detach() for n, g in zip(names, grads)}
+        out["o"] = o.detach()
+        return out
+    kind = _kind(cfg)
+    out = dict(dq=torch.zeros_like(q), dk=torch.zeros_like(k), dv=torch.zeros_like(v),
+               dlr=torch.zeros_like(lr), dmom=torch.zeros_like(mom),
+               ddecay=torch.zeros_like(decay), dW1=torch.zeros_like(W1),
+               dW2=torch.zeros_like(W2), o=torch.zeros_like(q))
+    m = 0
+    if cfg.has_global:
+        _global_backward(q, k, v, lr[0], mom[0], decay[0], W1[0], W2[0], dO, cfg.C_G, kind, out, 0)
+        m = 1
+    for (C_L, S_L) in cfg.locals_:
+        _local_backward(q, k, v, lr[m], mom[m], decay[m], W1[m], W2[m], dO, C_L, S_L, kind,
+                        bool(cfg.qk_proj), _scope(cfg), out, m)
+        m += 1
     return out
+
+
+def _vjp(fn, args, diff, grad_outs):
+    """Evaluate fn(*args) with autograd on the positions `diff` of args and
+    return (outputs, grads of sum_i <grad_outs[i], outputs[i]> for each diff
+    position); grad_outs entries may be None (no incoming gradient)."""
+    args = list(args)
+    leaves = []
+    for i in diff:
+        args[i] = args[i].detach().requires_grad_(True)
+        leaves.append(args[i])
+    with torch.enable_grad():
+        outs = fn(*args)
+        pairs = [(o, g) for o, g in zip(outs, grad_outs) if g is not None]
+        gs = torch.autograd.grad([o for o, _ in pairs], leaves, [g for _, g in pairs],
+                                 allow_unused=True)
+    gs = [torch.zeros_like(x) if g is None else g for g, x in zip(gs, leaves)]
+    return [o.detach() for o in outs], gs
+
+
+def _global_backward(q, k, v, eta, beta, alpha, W1, W2, dO, C_G, kind, out, m, block=64):
+    P, L, d = q.shape
+    V1, V2 = W1, W2
+    S1 = torch.zeros_like(W1)
+    S2 = torch.zeros_like(W2)
+    chunks = []
+    with torch.no_grad():
+        for n in range(L // C_G):
+            t0 = n * C_G
+            blocks = []
+            V1h, V2h = V1, V2                      # chunk-entry state
+            for b0 in range(t0, t0 + C_G, block):
+                b1 = min(b0 + block, t0 + C_G)
+                blocks.append((b0, b1, V1, V2, S1, S2))
+                V1, V2, S1, S2 = _global_accumulate(V1, V2, S1, S2, V1h, V2h, k[:, b0:b1],
+                                                    v[:, b0:b1], eta[:, b0:b1], beta[:, b0:b1],
+                                                    alpha[:, b0:b1], kind)
+            chunks.append((t0, blocks))
+    dV1, dV2 = torch.zeros_like(W1), torch.zeros_like(W2)
+    dS1, dS2 = torch.zeros_like(W1), torch.zeros_like(W2)
+    for t0, blocks in reversed(chunks):
+        V1h, V2h = chunks_entry(blocks)
+        dV1h, dV2h = torch.zeros_like(W1), torch.zeros_like(W2)
+        for (b0, b1, a1, a2, s1, s2) in reversed(blocks):
+            args = (a1, a2, s1, s2, V1h, V2h, k[:, b0:b1], v[:, b0:b1], eta[:, b0:b1],
+                    beta[:, b0:b1], alpha[:, b0:b1], kind)
+            _, g = _vjp(_global_accumulate, args, range(11), (dV1, dV2, dS1, dS2))
+            dV1, dV2, dS1, dS2 = g[0], g[1], g[2], g[3]
+            dV1h = dV1h + g[4]
+            dV2h = dV2h + g[5]
+            out["dk"][:, b0:b1] += g[6]
+            out["dv"][:, b0:b1] += g[7]
+            out["dlr"][m, :, b0:b1] += g[8]
+            out["dmom"][m, :, b0:b1] += g[9]
+            out["ddecay"][m, :, b0:b1] += g[10]
+        sl = slice(t0, t0 + C_G)
+        o, g = _vjp(lambda a, b, x, kd: (_global_retrieve(a, b, x, kd),), (V1h, V2h, q[:, sl], kind),
+                    range(3), (dO[:, sl],))
+        out["o"][:, sl] += o[0]
+        dV1h = dV1h + g[0]
+        dV2h = dV2h + g[1]
+        out["dq"][:, sl] += g[2]
+        # the chunk-entry state is both the running state and V_hat
+        dV1 = dV1 + dV1h
+        dV2 = dV2 + dV2h
+    out["dW1"][m] += dV1
+    out["dW2"][m] += dV2
+
+
+def chunks_entry(blocks):
+    """(V1, V2) entering the chunk whose sub-blocks are listed."""
+    return blocks[0][2], blocks[0][3]
+
+
+def _local_backward(q, k, v, eta, beta, alpha, W1i, W2i, dO, C_L, S_L, kind, qk_proj, qk_scope,
+                    out, m):
+    P, L, d = q.shape
+    for s in range(L // S_L):
+        W1, W2 = W1i, W2i
+        S1 = torch.zeros_like(W1i)
+        S2 = torch.zeros_like(W2i)
+        Mq = torch.zeros(P, d, d, dtype=q.dtype)
+        entries = []
+        with torch.no_grad():
+            for c0 in range(s * S_L, (s + 1) * S_L, C_L):
+                if qk_scope == "chunk":
+                    Mq = torch.zeros(P, d, d, dtype=q.dtype)
+                entries.append((c0, W1, W2, S1, S2, Mq))
+                sl = slice(c0, c0 + C_L)
+                W1, W2, S1, S2, Mq, _ = _local_chunk(W1, W2, S1, S2, Mq, q[:, sl], k[:, sl], v[:, sl],
+                                                     eta[:, sl], beta[:, sl], alpha[:, sl], kind,
+                                                     qk_proj)
+        dW1, dW2 = torch.zeros_like(W1i), torch.zeros_like(W2i)
+        dS1, dS2 = torch.zeros_like(W1i), torch.zeros_like(W2i)
+        dM = torch.zeros(P, d, d, dtype=q.dtype)
+        for (c0, a1, a2, s1, s2, mq) in reversed(entries):
+            sl = slice(c0, c0 + C_L)
+            args = (a1, a2, s1, s2, mq, q[:, sl], k[:, sl], v[:, sl], eta[:, sl], beta[:, sl],
+                    alpha[:, sl], kind, qk_proj)
+            gM = None if qk_scope == "chunk" else dM
+            o, g = _vjp(_local_chunk, args, range(11), (dW1, dW2, dS1, dS2, gM, dO[:, sl]))
+            out["o"][:, sl] += o[5]
+            dW1, dW2, dS1, dS2 = g[0], g[1], g[2], g[3]
+            dM = g[4] if qk_scope != "chunk" else torch.zeros_like(dM)
+            out["dq"][:, sl] += g[5]
+            out["dk"][:, sl] += g[6]
+            out["dv"][:, sl] += g[7]
+            out["dlr"][m, :, sl] += g[8]
+            out["dmom"][m, :, sl] += g[9]
+            out["ddecay"][m, :, sl] += g[10]
+        out["dW1"][m] += dW1
+        out["dW2"][m] += dW2
 
 
 # --------------------------------------------------------------------------

@@ -66,7 +66,7 @@ struct Layout {
   size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], saved_bytes;
   int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
   // forward workspace
-  size_t w_opart, w_tokc, w_chunkc, w_R, w_scr[TNT_MAX_LOCAL], w_ring, fwd_bytes;
+  size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_scr[TNT_MAX_LOCAL], w_ring, fwd_bytes;
   size_t ring_g, ring_l[TNT_MAX_LOCAL], ring_m[TNT_MAX_LOCAL];
   LocalPlan lplan[TNT_MAX_LOCAL];
   // backward workspace
@@ -111,6 +111,9 @@ Layout layout_of(const tnt_config* c) {
     y.w_tokc = off; off += up(y.gates * TKS * f);
     y.w_chunkc = off; off += up((size_t)y.BH * y.g_chunks * 4 * f);
     y.w_R = off; off += up((size_t)y.BH * c->C_G * c->d * f);
+    const Dims D = dims_of(c, c->C_G, c->L);
+    const int ns = std::max(global_fwd_splits(D), global_bwd_splits(D));
+    y.w_part = off; off += up((size_t)y.BH * ns * 4 * y.hd * f);
   }
   for (int i = 0; i < c->n_local; ++i) {
     const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
@@ -135,7 +138,7 @@ Layout layout_of(const tnt_config* c) {
     y.b_adj_g = off; off += up((size_t)y.BH * 2 * 4 * y.hd * f);
     y.b_dR = off; off += up((size_t)y.BH * c->C_G * c->d * f);
     y.b_dtok = off; off += up(y.gates * 4 * f);
-    y.b_dchunk = off; off += up((size_t)y.BH * y.g_chunks * (c->hid / 16) * 4 * f);
+    y.b_dchunk = off; off += up((size_t)y.BH * y.g_chunks * GRED_BLOCKS * 4 * f);
     y.b_dWg = off; off += up((size_t)y.BH * 2 * y.hd * f);
     const Dims D = dims_of(c, c->C_G, c->L);
     y.b_gscr = off;
@@ -262,6 +265,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     g.tokc = (float*)(ws + y.w_tokc);
     g.chunkc = (float*)(ws + y.w_chunkc);
     g.Rbuf = (float*)(ws + y.w_R);
+    g.part = (float*)(ws + y.w_part);
     g.D = dims_of(c, c->C_G, c->L);
     g.force_generic = generic_only();
     HIP_TIMED("global_scan", launch_global_scan(g, st));
@@ -327,6 +331,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     g.tokc = (float*)(ws + y.w_tokc);
     g.chunkc = (float*)(ws + y.w_chunkc);
     g.Rbuf = (float*)(ws + y.w_R);
+    g.part = (float*)(ws + y.w_part);
     g.adj = (float*)(ws + y.b_adj_g);
     g.dRbuf = (float*)(ws + y.b_dR);
     g.dtok = (float*)(ws + y.b_dtok);

@@ -20,6 +20,8 @@
 #include "tnt_device.h"
 #include "tnt_kernels.h"
 
+#include <algorithm>
+
 namespace tnt {
 
 template <typename F>
@@ -248,16 +250,17 @@ __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
   extern __shared__ __align__(16) unsigned char smem[];
   const Dims D = a.D;
   const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, C = D.C;
-  const int chain = blockIdx.y, hh = chain % D.H;
+  const int chain = blockIdx.z;
   const int s0 = blockIdx.x * GBB_HS;
+  const int split = blockIdx.y, nsplit = gridDim.y;
   const size_t hd = (size_t)h * d;
   const int l = lane_id();
   constexpr int TT = GBB_TT, HS = GBB_HS;
   const float* V = a.states + ((size_t)chain * a.nslots + n) * 4 * hd;
-  const float *V1 = V, *V2 = V + hd, *S1 = V + 2 * hd, *S2 = V + 3 * hd;
+  const float *V1 = V, *V2 = V + hd;
   const float* Ab = a.adj + ((size_t)chain * 2 + ((n + 1) & 1)) * 4 * hd;
   const float *Vb1 = Ab, *Vb2 = Ab + hd, *Sb1 = Ab + 2 * hd, *Sb2 = Ab + 3 * hd;
-  float* An = a.adj + ((size_t)chain * 2 + (n & 1)) * 4 * hd;
+  float* P = a.part + ((size_t)chain * nsplit + split) * 4 * hd;
   CT* sK = (CT*)smem;            // [TT][d]
   CT* sQ = sK + TT * d;
   CT* sdO = sQ + TT * d;
@@ -274,7 +277,6 @@ __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
   CT* sHkT = sGbT + HS * TT;
   CT* sHqT = sHkT + HS * TT;
   __shared__ float cC[TT], bb[TT];
-  __shared__ float red[16];
   const size_t cb0 = (size_t)chain * D.L + (size_t)n * C;
   const IO* qg = (const IO*)a.q + cb0 * d;
   const IO* kg = (const IO*)a.k + cb0 * d;
@@ -287,7 +289,9 @@ __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
   f4 av1[2], av2[2];
   for (int x = 0; x < 2; ++x) av1[x] = av2[x] = zero4();
 
-  for (int r0 = 0; r0 < C; r0 += TT) {
+  const int ntile = (C + TT - 1) / TT;
+  const int tb = split * ntile / nsplit, te = (split + 1) * ntile / nsplit;
+  for (int r0 = tb * TT; r0 < te * TT; r0 += TT) {
     const int rows = min(TT, C - r0);
     for (int e = threadIdx.x; e < TT * d; e += blockDim.x) {
       const int i = e / d, j = e - i * d;
@@ -348,34 +352,60 @@ __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
     }
     __syncthreads();
   }
-  const float* cc = a.chunkc + ((size_t)chain * (D.L / C) + n) * 4;
-  const float AC = cc[0], BC = cc[1], EC = cc[2];
-  float pa = 0.f, pe = 0.f, pb = 0.f;
+  // partial sums of this token split (combined in fixed order by gbwd_state_reduce)
   for (int x = 0, t = wave_id(); t < nt1; t += num_waves(), ++x) {
     const int j0 = t * 16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       {
         const int i = 4 * (l >> 4) + r, j = j0 + (l & 15);
-        const size_t e = (size_t)(s0 + i) * d + j;
-        const float w = Vb1[e], sv = Sb1[e];
-        pa += w * V1[e];
-        pe += w * S1[e];
-        pb += sv * S1[e];
-        An[e] = AC * w + av1[x][r];
-        An[2 * hd + e] = EC * w + BC * sv;
-        if (n == 0) a.dWinit[(size_t)chain * 2 * hd + e] = An[e];
+        P[(size_t)(s0 + i) * d + j] = av1[x][r];
       }
       {
         const int i = j0 + 4 * (l >> 4) + r, j = l & 15;
-        const size_t e = (size_t)i * h + s0 + j;
-        const float w = Vb2[e], sv = Sb2[e];
-        pa += w * V2[e];
-        pe += w * S2[e];
-        pb += sv * S2[e];
-        An[hd + e] = AC * w + av2[x][r];
-        An[3 * hd + e] = EC * w + BC * sv;
-        if (n == 0) a.dWinit[(size_t)chain * 2 * hd + hd + e] = An[hd + e];
+        P[hd + (size_t)i * h + s0 + j] = av2[x][r];
+      }
+    }
+  }
+}
+
+// adjoint of the chunk-entry state from the split partials (fixed order):
+//   V1bar = A_C V1bar' + sum dV1,  S1bar = E_C V1bar' + B_C S1bar'   (and V2, S2 alike)
+// plus the state dot products that give the adjoints of A_C, E_C, B_C.
+__global__ void __launch_bounds__(256) gbwd_state_reduce(GlobalArgs a, int n, int nsplit) {
+  const Dims D = a.D;
+  const int chain = blockIdx.y;
+  const size_t hd = (size_t)D.hid * D.d;
+  const float* V = a.states + ((size_t)chain * a.nslots + n) * 4 * hd;
+  const float* Ab = a.adj + ((size_t)chain * 2 + ((n + 1) & 1)) * 4 * hd;
+  float* An = a.adj + ((size_t)chain * 2 + (n & 1)) * 4 * hd;
+  const float* P = a.part + (size_t)chain * nsplit * 4 * hd;
+  const float* cc = a.chunkc + ((size_t)chain * (D.L / D.C) + n) * 4;
+  const float AC = cc[0], BC = cc[1], EC = cc[2];
+  __shared__ float red[16];
+  float pa = 0.f, pe = 0.f, pb = 0.f;
+  for (size_t e4 = blockIdx.x * blockDim.x + threadIdx.x; e4 < hd / 4;
+       e4 += gridDim.x * blockDim.x) {
+    const size_t e = e4 * 4;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {  // m = 0: (V1, S1), m = 1: (V2, S2)
+      const size_t ew = (size_t)m * hd + e, es = (size_t)(2 + m) * hd + e;
+      f32x4 dv = {0.f, 0.f, 0.f, 0.f};
+      for (int sp = 0; sp < nsplit; ++sp)
+        dv += *reinterpret_cast<const f32x4*>(P + (size_t)sp * 4 * hd + ew);
+      const f32x4 w = *reinterpret_cast<const f32x4*>(Ab + ew);
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(Ab + es);
+      const f32x4 vw = *reinterpret_cast<const f32x4*>(V + ew);
+      const f32x4 vs = *reinterpret_cast<const f32x4*>(V + es);
+      const f32x4 nw = AC * w + dv;
+      *reinterpret_cast<f32x4*>(An + ew) = nw;
+      *reinterpret_cast<f32x4*>(An + es) = EC * w + BC * sv;
+      if (n == 0) *reinterpret_cast<f32x4*>(a.dWinit + (size_t)chain * 2 * hd + ew) = nw;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        pa += w[j] * vw[j];
+        pe += w[j] * vs[j];
+        pb += sv[j] * vs[j];
       }
     }
   }
@@ -383,13 +413,17 @@ __global__ void __launch_bounds__(256) gbwd_b_kernel(GlobalArgs a, int n) {
   pe = block_sum(pe, red);
   pb = block_sum(pb, red);
   if (threadIdx.x == 0) {
-    float* dc = a.dchunk + (((size_t)chain * (D.L / C) + n) * gridDim.x + blockIdx.x) * 4;
+    float* dc = a.dchunk + (((size_t)chain * (D.L / D.C) + n) * gridDim.x + blockIdx.x) * 4;
     dc[0] = pa;
     dc[1] = pe;
     dc[2] = pb;
     dc[3] = 0.f;
   }
-  (void)hh;
+}
+
+int global_bwd_splits(const Dims& D) {
+  const int tiles = (D.C + GBB_TT - 1) / GBB_TT;
+  return std::max(1, std::min(16, tiles / 4));
 }
 
 template <typename IO, typename CT, int ACT, int D_, int H_>
@@ -398,10 +432,12 @@ static hipError_t launch_gbwd_dims(const GlobalArgs& a, int n, void* scratch, si
   const Dims& D = a.D;
   dim3 ga((D.C + GB_TT - 1) / GB_TT, D.B * D.H);
   hipLaunchKernelGGL((gbwd_a_kernel<IO, CT, ACT, D_, H_>), ga, dim3(256), 0, st, a, n, scratch, f32_off);
-  dim3 gb(D.hid / GBB_HS, D.B * D.H);
+  const int ns = global_bwd_splits(D);
+  dim3 gb(D.hid / GBB_HS, ns, D.B * D.H);
   const size_t lds = (10 * (size_t)GBB_TT * D.d + 5 * GBB_HS * GBB_TT) * sizeof(CT);
   set_lds_limit((const void*)gbwd_b_kernel<IO, CT, ACT, D_, H_>);
   hipLaunchKernelGGL((gbwd_b_kernel<IO, CT, ACT, D_, H_>), gb, dim3(256), lds, st, a, n);
+  hipLaunchKernelGGL(gbwd_state_reduce, dim3(GRED_BLOCKS, D.B * D.H), dim3(256), 0, st, a, n, ns);
   return hipGetLastError();
 }
 
@@ -547,7 +583,7 @@ __global__ void __launch_bounds__(64) global_gate_bwd_kernel(GlobalArgs a, int n
 
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st) {
   dim3 grid(a.D.L / a.D.C, a.D.B * a.D.H);
-  hipLaunchKernelGGL(global_gate_bwd_kernel, grid, dim3(64), 0, st, a, a.D.hid / GBB_HS);
+  hipLaunchKernelGGL(global_gate_bwd_kernel, grid, dim3(64), 0, st, a, GRED_BLOCKS);
   return hipGetLastError();
 }
 

@@ -13,6 +13,8 @@
 #include "tnt_device.h"
 #include "tnt_kernels.h"
 
+#include <algorithm>
+
 namespace tnt {
 
 // ---------------------------------------------------------------------------
@@ -179,12 +181,13 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
   extern __shared__ __align__(16) unsigned char smem[];
   const Dims D = a.D;
   const int d = D_ ? D_ : D.d, h = H_ ? H_ : D.hid, C = D.C;
-  const int chain = blockIdx.y;
+  const int chain = blockIdx.z;
   const int s0 = blockIdx.x * G2_HS;
+  const int split = blockIdx.y, nsplit = gridDim.y;
   const size_t hd = (size_t)h * d;
   const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
-  float* Vn = a.states + ((size_t)chain * a.nslots + ((n + 1) % a.nslots)) * 4 * hd;
-  const float *V1 = V, *V2 = V + hd, *S1 = V + 2 * hd, *S2 = V + 3 * hd;
+  const float *V1 = V, *V2 = V + hd;
+  float* P = a.part + ((size_t)chain * nsplit + split) * 4 * hd;  // this split's partial sums
   constexpr int HS = G2_HS;
   CT* sK = (CT*)smem;                 // [TT][d]
   CT* sR = sK + TT * d;               // [TT][d]
@@ -204,7 +207,9 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
   f4 aw1[2], as1[2], aw2[2], as2[2];
   for (int x = 0; x < 2; ++x) aw1[x] = as1[x] = aw2[x] = as2[x] = zero4();
 
-  for (int r0 = 0; r0 < C; r0 += TT) {
+  const int ntile = (C + TT - 1) / TT;
+  const int tb = split * ntile / nsplit, te = (split + 1) * ntile / nsplit;
+  for (int r0 = tb * TT; r0 < te * TT; r0 += TT) {
     const int rows = min(TT, C - r0);
     for (int e = threadIdx.x; e < TT * d; e += blockDim.x) {
       const int i = e / d, j = e - i * d;
@@ -246,8 +251,7 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
     }
     __syncthreads();
   }
-  const float* cc = a.chunkc + ((size_t)chain * (D.L / C) + n) * 4;
-  const float AC = cc[0], BC = cc[1], EC = cc[2];
+  // partial sums of this token split (combined in fixed order by global_carry_reduce)
   const int l = lane_id();
   for (int x = 0, t = wave_id(); t < nt1; t += num_waves(), ++x) {
     const int j0 = t * 16;
@@ -256,17 +260,51 @@ __global__ void __launch_bounds__(256) global_p2_kernel(GlobalArgs a, int n, int
       {  // V1 / S1 slice element (s0 + i, j)
         const int i = 4 * (l >> 4) + r, j = j0 + (l & 15);
         const size_t e = (size_t)(s0 + i) * d + j;
-        Vn[e] = AC * V1[e] + EC * S1[e] - aw1[x][r];
-        Vn[2 * hd + e] = BC * S1[e] - as1[x][r];
+        P[e] = aw1[x][r];
+        P[2 * hd + e] = as1[x][r];
       }
       {  // V2 / S2 slice element (j0 + row, s0 + col)
         const int i = j0 + 4 * (l >> 4) + r, j = l & 15;
         const size_t e = (size_t)i * h + s0 + j;
-        Vn[hd + e] = AC * V2[e] + EC * S2[e] - aw2[x][r];
-        Vn[3 * hd + e] = BC * S2[e] - as2[x][r];
+        P[hd + e] = aw2[x][r];
+        P[3 * hd + e] = as2[x][r];
       }
     }
   }
+}
+
+// V' = A_C V + E_C S - sum_splits dV,  S' = B_C S - sum_splits dS  (fixed split order)
+__global__ void __launch_bounds__(256) global_carry_reduce(GlobalArgs a, int n, int nsplit) {
+  const Dims D = a.D;
+  const int chain = blockIdx.y;
+  const size_t hd = (size_t)D.hid * D.d;
+  const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
+  float* Vn = a.states + ((size_t)chain * a.nslots + ((n + 1) % a.nslots)) * 4 * hd;
+  const float* P = a.part + (size_t)chain * nsplit * 4 * hd;
+  const float* cc = a.chunkc + ((size_t)chain * (D.L / D.C) + n) * 4;
+  const float AC = cc[0], BC = cc[1], EC = cc[2];
+  for (size_t e4 = blockIdx.x * blockDim.x + threadIdx.x; e4 < hd / 4;
+       e4 += gridDim.x * blockDim.x) {
+    const size_t e = e4 * 4;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {  // m = 0: (W1, S1), m = 1: (W2, S2)
+      const size_t ew = (size_t)m * hd + e, es = (size_t)(2 + m) * hd + e;
+      f32x4 dw = {0.f, 0.f, 0.f, 0.f}, ds = dw;
+      for (int sp = 0; sp < nsplit; ++sp) {
+        dw += *reinterpret_cast<const f32x4*>(P + (size_t)sp * 4 * hd + ew);
+        ds += *reinterpret_cast<const f32x4*>(P + (size_t)sp * 4 * hd + es);
+      }
+      const f32x4 w = *reinterpret_cast<const f32x4*>(V + ew);
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(V + es);
+      *reinterpret_cast<f32x4*>(Vn + ew) = AC * w + EC * sv - dw;
+      *reinterpret_cast<f32x4*>(Vn + es) = BC * sv - ds;
+    }
+  }
+}
+
+int global_fwd_splits(const Dims& D) {
+  const int tiles = (D.C + 63) / 64;
+  return std::max(1, std::min(16, tiles / 4));
 }
 
 template <typename IO, typename CT, int ACT, int D_, int H_>
@@ -279,10 +317,13 @@ static hipError_t launch_gfwd_dims(const GlobalArgs& a, int n, hipStream_t st) {
   set_lds_limit((const void*)global_p1_kernel<IO, CT, ACT, D_, H_>);
   hipLaunchKernelGGL((global_p1_kernel<IO, CT, ACT, D_, H_>), g1, dim3(256), l1, st, a, n, TT);
   const int T2 = g2_rows(D);
-  dim3 g2(D.hid / G2_HS, D.B * D.H);
+  const int ns = global_fwd_splits(D);
+  dim3 g2(D.hid / G2_HS, ns, D.B * D.H);
   const size_t l2 = (6 * (size_t)T2 * D.d + 2 * (size_t)G2_HS * T2) * cts;
   set_lds_limit((const void*)global_p2_kernel<IO, CT, ACT, D_, H_>);
   hipLaunchKernelGGL((global_p2_kernel<IO, CT, ACT, D_, H_>), g2, dim3(256), l2, st, a, n, T2);
+  hipLaunchKernelGGL(global_carry_reduce, dim3(GRED_BLOCKS, D.B * D.H), dim3(256), 0, st, a, n,
+                     ns);
   return hipGetLastError();
 }
 

@@ -83,6 +83,7 @@ struct GlobalArgs {
   float* dWinit;                                         // [B*H][2*hid*d] (reduced later)
   void* scratch;                                         // phase-A scratch of the backward
   size_t scratch_f32_off;
+  float* part;                                           // [B*H][nsplit][4*hid*d] split partials
   Dims D;
   int force_generic;                                     // 1: skip fixed-size kernels
 };
@@ -109,6 +110,9 @@ hipError_t launch_global_bwd_zero(const GlobalArgs& a, int slot, hipStream_t st)
 hipError_t launch_reduce_global_init(const float* part, int B, int H, size_t hd, float* dW1,
                                      float* dW2, hipStream_t st);
 size_t global_bwd_scratch_bytes(const Dims& D, size_t* f32_off);
+int global_fwd_splits(const Dims& D);
+int global_bwd_splits(const Dims& D);
+constexpr int GRED_BLOCKS = 16;  // blocks per chain of the split reductions
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
                           int bf16, hipStream_t st);

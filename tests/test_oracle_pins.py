@@ -383,3 +383,18 @@ def test_planted_mistakes_fail_a_pin(monkeypatch):
     monkeypatch.setattr(O.tnt_oracle, "inner_grad", flipped)
     bad = O.tnt_oracle.local_memory(q, k, v, eta, beta, alpha, W1, W2, 1, 12, "silu")
     assert (bad - ref).abs().max() > 1e-6
+
+
+@pytest.mark.parametrize("scope", [QK_SHARD, QK_CHUNK])
+def test_segmented_backward_equals_plain_autograd(scope):
+    """The segment-by-segment backward (stored segment-entry states, autograd
+    per segment in reverse) equals one autograd pass through the whole layer."""
+    cfg = _cfg(act=ACT_SILU, qk_scope=scope, B=2, H=1, L=32, d=4, hid=6, C_G=16,
+               locals_=((4, 16), (8, 8)))
+    inp = make_inputs(cfg, 17)
+    g = O.gather_pairs(inp, O.all_pairs(cfg))
+    args = [g[n] for n in ("q", "k", "v", "lr", "mom", "decay", "W1", "W2")]
+    a = O.layer_backward(*args, g["dO"], cfg, ckpt=True)
+    b = O.layer_backward(*args, g["dO"], cfg, ckpt=False)
+    for n in b:
+        assert (a[n] - b[n]).abs().max() <= 1e-12 * max(1.0, b[n].abs().max().item()), n
