@@ -72,7 +72,8 @@ struct Layout {
   // backward workspace
   size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32,
       b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
-      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_states, bwd_bytes, bwd_re_bytes;
+      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_stT[TNT_MAX_LOCAL], b_states, bwd_bytes,
+      bwd_re_bytes;
   BwdLayout blay[TNT_MAX_LOCAL];
 };
 
@@ -152,6 +153,8 @@ Layout layout_of(const tnt_config* c) {
     y.b_dWl[i] = off; off += up((size_t)y.l_units[i] * 2 * y.hd * f);
     y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].ct_elems * cts);
     y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].f32_elems * f);
+    y.b_stT[i] = off;
+    off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * (4 * y.hd + dd) * cts);
   }
   y.bwd_bytes = off;
   y.b_states = off;
@@ -358,6 +361,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.states = (const float*)(sv + y.sv_l[i]);
     a.mstates = (const float*)(sv + y.sv_m[i]);
     a.nslots = y.l_chunks[i] + 1;
+    a.statesT = ws + y.b_stT[i];
     a.adj = (float*)(ws + y.b_adj_l[i]);
     a.madj = (float*)(ws + y.b_madj[i]);
     a.dq_part = dqp + (size_t)m * y.io_elems;
@@ -369,6 +373,10 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
     a.force_generic = generic_only();
+    HIP_TIMED("pack_states", launch_pack_states(a.states, a.mstates, ws + y.b_stT[i], y.l_units[i],
+                                                a.nslots, c->d, c->hid,
+                                                c->qk_proj && c->qk_scope == TNT_QK_SHARD,
+                                                c->dtype == TNT_BF16, st));
     HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
     HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,

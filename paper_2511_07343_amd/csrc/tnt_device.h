@@ -25,6 +25,14 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int WAVE = 64;
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
+// The lane index through an opaque move: values derived from it are
+// recomputed where they are used instead of being hoisted out of loops and
+// kept live (per-lane operand addresses of a long kernel).
+__device__ __forceinline__ int lane_id_local() {
+  int l = threadIdx.x & (WAVE - 1);
+  asm volatile("" : "+v"(l));
+  return l;
+}
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
 __device__ __forceinline__ int num_waves() { return blockDim.x / WAVE; }
 
@@ -211,6 +219,129 @@ __device__ __forceinline__ void gemm(int M, int N, int K, const EA* A, int lda, 
     mma_tile<CT, LA, LB>(acc, A, lda, i0, B, ldb, j0, K, kscale);
     tile_each(acc, i0, j0, epi);
   }
+}
+
+// ----------------------------------------------------------------------------
+// Register-blocked wave tiles.  An M x N output (multiples of 16, sizes known
+// at compile time) is cut into blocks of RB x CB 16x16 tiles: T/8 tiles per
+// block (1..8), shaped to need the fewest operand fragments.  Blocks go to the
+// waves round-robin.  A wave issues every fragment load of a K step of its
+// block before the MFMAs, so a block costs one memory round trip per K step
+// rather than one per tile.
+// ----------------------------------------------------------------------------
+template <int M, int N, int NWAVE = 8> struct Blk {
+  static constexpr int TM = M / 16, TN = N / 16, T = TM * TN;
+  static constexpr int TPW = T / NWAVE < 1 ? 1 : (T / NWAVE > 8 ? 8 : T / NWAVE);
+  static constexpr int pick_rb() {
+    int best = 0, cost = 1 << 20;
+    for (int rb = 1; rb <= 8; rb <<= 1) {
+      const int cb = TPW / rb;
+      if (cb < 1 || rb * cb != TPW || rb > TM || cb > TN || TM % rb || TN % cb) continue;
+      if (rb + cb <= cost) {  // ties go to the taller block
+        cost = rb + cb;
+        best = rb;
+      }
+    }
+    return best;
+  }
+  static constexpr int RB = pick_rb(), CB = RB ? TPW / RB : 0;
+  static constexpr int NBM = RB ? TM / RB : 0, NBN = CB ? TN / CB : 0, NB = NBM * NBN;
+  static_assert(RB > 0 && CB > 0 && M % 16 == 0 && N % 16 == 0, "unsupported block shape");
+};
+
+// visit the wave's blocks of an M x N output: f(i0, j0) at each block corner
+template <int M, int N, typename F>
+__device__ __forceinline__ void for_blocks(F&& f) {
+  using BK = Blk<M, N>;
+  for (int b = wave_id(); b < BK::NB; b += num_waves())
+    f((b / BK::NBN) * BK::RB * 16, (b % BK::NBN) * BK::CB * 16);
+}
+
+template <int RB, int CB>
+__device__ __forceinline__ void zero_blk(f4 (&a)[RB][CB]) {
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < CB; ++c) a[r][c] = zero4();
+}
+
+// acc[r][c] += A[i0+16r .., 0:K] B[0:K, j0+16c ..] (K a compile-time constant).
+// The K loop stays rolled and double-buffered: the fragments of step k+1 are
+// requested before the MFMAs of step k, so one term costs about one memory
+// round trip and the live operand registers stay at two steps' worth.
+template <typename CT, int LA, int LB, int RB, int CB, int K, typename EA, typename EB>
+__device__ __forceinline__ void mma_blk(f4 (&acc)[RB][CB], const EA* A, int lda, int i0,
+                                        const EB* B, int ldb, int j0,
+                                        const float* kscale = nullptr) {
+  typedef Mma<CT> MM;
+  const int l = lane_id_local();
+  const int ko = MM::kofs(l);
+  typename MM::frag fa[RB], fb[CB];
+  auto fetch = [&](int k0, typename MM::frag(&xa)[RB], typename MM::frag(&xb)[CB]) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+      xa[r] = MM::template load<LA>(A, lda, i0 + 16 * r + (l & 15), k0 + ko, K, kscale);
+#pragma unroll
+    for (int c = 0; c < CB; ++c)
+      xb[c] = MM::template load<LB>(B, ldb, j0 + 16 * c + (l & 15), k0 + ko, K, nullptr);
+  };
+  auto apply = [&](const typename MM::frag(&xa)[RB], const typename MM::frag(&xb)[CB]) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int c = 0; c < CB; ++c) MM::mma(acc[r][c], xa[r], xb[c]);
+  };
+  fetch(0, fa, fb);
+#pragma unroll 1
+  for (int k0 = MM::KS; k0 < K; k0 += MM::KS) {
+    typename MM::frag na[RB], nb[CB];
+    fetch(k0, na, nb);
+    apply(fa, fb);
+#pragma unroll
+    for (int r = 0; r < RB; ++r) fa[r] = na[r];
+#pragma unroll
+    for (int c = 0; c < CB; ++c) fb[c] = nb[c];
+  }
+  apply(fa, fb);
+}
+
+// f(rb, cb, i, j) once per tile of the block: the lane's rows i .. i+3 of
+// column j are acc[rb][cb][0..3]
+template <int RB, int CB, typename F>
+__device__ __forceinline__ void blk_each4(int i0, int j0, F&& f) {
+  const int l = lane_id_local();
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) f(rb, cb, i0 + 16 * rb + 4 * (l >> 4), j0 + 16 * cb + (l & 15));
+}
+
+// Block GEMM over the whole output with a per-element epilogue epi(i, j, v).
+template <typename CT, int LA, int LB, int M, int N, int K, typename EA, typename EB, typename Epi>
+__device__ __forceinline__ void gemm_blk(const EA* A, int lda, const EB* B, int ldb, Epi&& epi,
+                                         const float* kscale = nullptr) {
+  using BK = Blk<M, N>;
+  for_blocks<M, N>([&](int i0, int j0) {
+    f4 acc[BK::RB][BK::CB];
+    zero_blk(acc);
+    mma_blk<CT, LA, LB, BK::RB, BK::CB, K>(acc, A, lda, i0, B, ldb, j0, kscale);
+    blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) epi(i + r, j, acc[rb][cb][r]);
+    });
+  });
+}
+
+// four consecutive compute-type elements from one f4 (8- or 16-byte store)
+template <typename CT> __device__ __forceinline__ void store4(CT* p, const f4& v);
+template <> __device__ __forceinline__ void store4<float>(float* p, const f4& v) {
+  *reinterpret_cast<f32x4*>(p) = v;
+}
+template <> __device__ __forceinline__ void store4<__bf16>(__bf16* p, const f4& v) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  bf16x4 b;
+  b[0] = (__bf16)v[0]; b[1] = (__bf16)v[1]; b[2] = (__bf16)v[2]; b[3] = (__bf16)v[3];
+  *reinterpret_cast<bf16x4*>(p) = b;
 }
 
 // ----------------------------------------------------------------------------

@@ -50,6 +50,8 @@ struct LocalBwdArgs {
   const float* lr; const float* mom; const float* decay;
   const float* states;                                   // saved chunk-entry states
   const float* mstates;
+  const void* statesT;                                   // CT [units][nslots][4*hid*d + d*d]:
+                                                         // W1^T, W2^T, S1^T, S2^T, M^T
   int nslots;
   float* adj;                                            // [units][4*hid*d] adjoint state
   float* madj;                                           // [units][2][d*d]
@@ -101,7 +103,10 @@ size_t local_plan(const Dims& D, LocalPlan* p, bool backward);
 
 hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st);
 bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err);
+hipError_t launch_pack_states(const float* states, const float* mstates, void* out, int units,
+                               int nslots, int d, int hid, int with_m, int bf16, hipStream_t st);
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st);
+bool launch_local_bwd_blk(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err);
 hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st);

@@ -75,6 +75,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
      *GbT = B_(bGbT);
   CT *Ykb = B_(bYkb), *YkbT = B_(bYkbT), *Zkb = B_(bZkb), *ZkbT = B_(bZkbT), *Xb = B_(bXb),
      *XbT = B_(bXbT), *dXN = B_(bdXN), *dXNT = B_(bdXNT);
+  CT *Wb1T = B_(bWb1T), *Sb1T = B_(bSb1T), *Wb2T = B_(bWb2T), *Sb2T = B_(bSb2T);
   float *fXK = F_(E_XK), *fHH = F_(E_HH), *fdOR = F_(E_dOR), *fdZD1 = F_(E_dZD1), *fCb = F_(E_Cbar),
         *fU = F_(E_U), *fKb = F_(E_Kbar), *fRb = F_(E_Rbar), *fXb = F_(E_Xbar), *fT3 = F_(E_T3),
         *fT4 = F_(E_T4), *fT5 = F_(E_T5), *fT6 = F_(E_T6), *fZkp = F_(E_Zkp), *fMs = F_(E_Msym),
@@ -103,7 +104,10 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
   const bool shard_qk = D.qk_proj && D.qk_scope == 0;
   const float rscale = 2.0f / (float)d;
 
-  for (size_t e = threadIdx.x; e < 4 * hd; e += blockDim.x) adj[e] = 0.f;
+  for (size_t e = threadIdx.x; e < 4 * hd; e += blockDim.x) {
+    adj[e] = 0.f;
+    Wb1T[e] = from_f<CT>(0.f);  // the four transposed copies are contiguous
+  }
   for (int e = threadIdx.x; e < d * d; e += blockDim.x) madj[e] = 0.f;
   __syncthreads();
 
@@ -113,6 +117,9 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
     const float *W1 = st, *W2 = st + hd, *S1 = st + 2 * hd, *S2 = st + 3 * hd;
     const float* Mc = a.mstates + ((size_t)u * a.nslots + n) * d * d;
+    // transposed CT copies of the same state (contraction-contiguous operands)
+    const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
+    const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd, *McT = pk + 4 * hd;
 
     // ================= recompute the chunk's forward quantities
     stage_rows<IO, CT>(Q, QT, qg + (size_t)tok0 * d, C, Cp, d);
@@ -168,7 +175,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       RT[(size_t)j * Cp + i] = from_f<CT>(r);
     });
     __syncthreads();
-    gemm<CT, KC, MC>(Cp, h, d, R, d, W2, h, [&](int i, int j, float g) {
+    gemm<CT, KC, KC>(Cp, h, d, R, d, W2T, d, [&](int i, int j, float g) {
       const float d1 = g * to_f(Sp[(size_t)i * h + j]);
       G[(size_t)i * h + j] = from_f<CT>(g);
       D1[(size_t)i * h + j] = from_f<CT>(d1);
@@ -218,8 +225,8 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)
     tiles(Cp, h, [&](int i0, int j0) {
       f4 a1 = zero4(), a2 = zero4(), a3 = zero4();
-      mma_tile<CT, KC, MC>(a1, dO, d, i0, W2, h, j0, d);
-      mma_tile<CT, KC, MC>(a2, dO, d, i0, S2, h, j0, d);
+      mma_tile<CT, KC, KC>(a1, dO, d, i0, W2T, d, j0, d);
+      mma_tile<CT, KC, KC>(a2, dO, d, i0, S2T, d, j0, d);
       mma_tile<CT, KC, KC>(a3, Q1, Cp, i0, HkT, Cp, j0, Cp);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -259,8 +266,8 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     // Xbar = diag(A) Zbar W1 + diag(E) Zbar S1 - Q2 K
     tiles(Cp, d, [&](int i0, int j0) {
       f4 a1 = zero4(), a2 = zero4(), a3 = zero4();
-      mma_tile<CT, KC, MC>(a1, Zb, h, i0, W1, d, j0, h);
-      mma_tile<CT, KC, MC>(a2, Zb, h, i0, S1, d, j0, h);
+      mma_tile<CT, KC, KC>(a1, Zb, h, i0, W1T, h, j0, h);
+      mma_tile<CT, KC, KC>(a2, Zb, h, i0, S1T, h, j0, h);
       mma_tile<CT, KC, KC>(a3, Q2, Cp, i0, KT, Cp, j0, Cp);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -309,8 +316,8 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     // T3 = D1 W1bar', T4 = D1 S1bar', T5 = Hk W2bar'^T, T6 = Hk S2bar'^T  (C x d)
     tiles(Cp, d, [&](int i0, int j0) {
       f4 a3 = zero4(), a4 = zero4(), a5 = zero4(), a6 = zero4();
-      mma_tile<CT, KC, MC>(a3, D1, h, i0, Wb1, d, j0, h);
-      mma_tile<CT, KC, MC>(a4, D1, h, i0, Sb1, d, j0, h);
+      mma_tile<CT, KC, KC>(a3, D1, h, i0, Wb1T, h, j0, h);
+      mma_tile<CT, KC, KC>(a4, D1, h, i0, Sb1T, h, j0, h);
       mma_tile<CT, KC, KC>(a5, Hk, h, i0, Wb2, h, j0, h);
       mma_tile<CT, KC, KC>(a6, Hk, h, i0, Sb2, h, j0, h);
 #pragma unroll
@@ -362,9 +369,9 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     tiles(Cp, h, [&](int i0, int j0) {
       f4 a1 = zero4(), a2 = zero4(), a3 = zero4(), a4 = zero4();
       mma_tile<CT, KC, KC>(a1, Q1T, Cp, i0, HT, Cp, j0, Cp);
-      mma_tile<CT, KC, MC>(a2, R, d, i0, Wb2, h, j0, d);
-      mma_tile<CT, KC, MC>(a3, R, d, i0, Sb2, h, j0, d);
-      mma_tile<CT, KC, MC>(a4, Ykb, d, i0, W2, h, j0, d);
+      mma_tile<CT, KC, KC>(a2, R, d, i0, Wb2T, d, j0, d);
+      mma_tile<CT, KC, KC>(a3, R, d, i0, Sb2T, d, j0, d);
+      mma_tile<CT, KC, KC>(a4, Ykb, d, i0, W2T, d, j0, d);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -380,7 +387,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     tiles(Cp, d, [&](int i0, int j0) {
       f4 a1 = zero4(), a2 = zero4();
       mma_tile<CT, KC, KC>(a1, Q2T, Cp, i0, XT, Cp, j0, Cp);
-      mma_tile<CT, KC, MC>(a2, Zkb, h, i0, W1, d, j0, h);
+      mma_tile<CT, KC, KC>(a2, Zkb, h, i0, W1T, h, j0, h);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -404,7 +411,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       // Qbar = Xbar M0 + tril(Xbar N^T) N ; Nbar = Str^T Xbar + tril(Xbar N^T)^T Q + N (Mb' + Mb'^T)
       tiles(Cp, d, [&](int i0, int j0) {
         f4 q1 = zero4(), n1 = zero4();
-        if (shard_qk) mma_tile<CT, KC, MC>(q1, Xb, d, i0, Mc, d, j0, d);
+        if (shard_qk) mma_tile<CT, KC, KC>(q1, Xb, d, i0, McT, d, j0, d);
         mma_tile<CT, KC, KC>(q1, dXN, Cp, i0, NT, Cp, j0, Cp);
         mma_tile<CT, KC, KC>(n1, StrT, Cp, i0, XbT, Cp, j0, Cp);
         mma_tile<CT, KC, KC>(n1, dXNT, Cp, i0, QT, Cp, j0, Cp);
@@ -518,13 +525,20 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       mma_tile<CT, KC, KC>(a1, ZbT, Cp, i0, XAT, Cp, j0, Cp);
       mma_tile<CT, KC, KC>(a2, ZkbT, Cp, i0, KT, Cp, j0, Cp);
       mma_tile<CT, KC, KC>(a3, ZbT, Cp, i0, XET, Cp, j0, Cp);
+      f4 nw, ns;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * d + j0 + (l & 15);
         const float w = Wb1[e], sv = Sb1[e];
-        Wb1[e] = cf.AC * w + a1[r] + a2[r];
-        Sb1[e] = cf.EC * w + cf.BC * sv + a3[r];
+        nw[r] = cf.AC * w + a1[r] + a2[r];
+        ns[r] = cf.EC * w + cf.BC * sv + a3[r];
+        Wb1[e] = nw[r];
+        Sb1[e] = ns[r];
       }
+      // the lane's 4 rows are consecutive in the transposed copies
+      const size_t et = (size_t)(j0 + (l & 15)) * h + i0 + 4 * (l >> 4);
+      store4<CT>(Wb1T + et, nw);
+      store4<CT>(Sb1T + et, ns);
     });
     tiles(d, h, [&](int i0, int j0) {  // W2bar, S2bar : d x h
       f4 a1 = zero4(), a2 = zero4(), a3 = zero4(), a4 = zero4();
@@ -532,13 +546,19 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       mma_tile<CT, KC, KC>(a2, RT, Cp, i0, GbT, Cp, j0, Cp);
       mma_tile<CT, KC, KC>(a3, YkbT, Cp, i0, HkT, Cp, j0, Cp);
       mma_tile<CT, KC, KC>(a4, dOET, Cp, i0, HT, Cp, j0, Cp);
+      f4 nw, ns;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * h + j0 + (l & 15);
         const float w = Wb2[e], sv = Sb2[e];
-        Wb2[e] = cf.AC * w + a1[r] + a2[r] + a3[r];
-        Sb2[e] = cf.EC * w + cf.BC * sv + a4[r];
+        nw[r] = cf.AC * w + a1[r] + a2[r] + a3[r];
+        ns[r] = cf.EC * w + cf.BC * sv + a4[r];
+        Wb2[e] = nw[r];
+        Sb2[e] = ns[r];
       }
+      const size_t et = (size_t)(j0 + (l & 15)) * d + i0 + 4 * (l >> 4);
+      store4<CT>(Wb2T + et, nw);
+      store4<CT>(Sb2T + et, ns);
     });
     if (shard_qk)
       tiles(d, d, [&](int i0, int j0) {
@@ -569,20 +589,12 @@ static bool try_bwd(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t
 
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st) {
   hipError_t e = hipSuccess;
-  const bool fixed = !a.force_generic;
+  if (!a.force_generic && launch_local_bwd_blk(a, units, st, &e)) return e;
   if (a.D.bf16) {
-    if (fixed && (try_bwd<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, units, st, &e) ||
-                  try_bwd<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, units, st, &e) ||
-                  try_bwd<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, units, st, &e) ||
-                  try_bwd<__bf16, __bf16, ACT_SILU, 128, 512, 64>(a, units, st, &e)))
-      return e;
     if (try_bwd<__bf16, __bf16, ACT_GELU, 0, 0, 0>(a, units, st, &e) ||
         try_bwd<__bf16, __bf16, ACT_SILU, 0, 0, 0>(a, units, st, &e))
       return e;
   } else {
-    if (fixed && (try_bwd<float, float, ACT_GELU, 16, 32, 16>(a, units, st, &e) ||
-                  try_bwd<float, float, ACT_SILU, 16, 32, 16>(a, units, st, &e)))
-      return e;
     if (try_bwd<float, float, ACT_GELU, 0, 0, 0>(a, units, st, &e) ||
         try_bwd<float, float, ACT_SILU, 0, 0, 0>(a, units, st, &e))
       return e;
@@ -616,6 +628,53 @@ hipError_t launch_reduce_init(const float* parts, int B, int H, int nshard, size
   const size_t hd = hd2 / 2;
   hipLaunchKernelGGL(reduce_init_kernel, dim3(32, H), dim3(256), 0, st, parts, B, H, nshard, hd,
                      dW1, dW2);
+  return hipGetLastError();
+}
+
+
+// Transposed compute-type copies of the saved chunk-entry states, one
+// 32 x 32 tile per workgroup and slot: W1 (hid x d) -> W1^T, W2 (d x hid) ->
+// W2^T, S1, S2 likewise, and the Q-K sum M (d x d) -> M^T when `with_m`.
+// `slots` = units * nslots; out holds 4*hid*d + d*d elements per slot.
+template <typename CT>
+__global__ void __launch_bounds__(256) pack_states_kernel(const float* st, const float* mst, CT* out,
+                                                          size_t slots, int d, int h, int with_m) {
+  __shared__ float t[32][33];
+  const int m = blockIdx.z;
+  if (m == 4 && !with_m) return;
+  const size_t hd = (size_t)h * d, slot = 4 * hd + (size_t)d * d;
+  const int R = (m == 4 || (m & 1)) ? d : h, Cc = (m != 4 && (m & 1)) ? h : d;
+  const int tc = (Cc + 31) / 32, ntiles = ((R + 31) / 32) * tc;
+  if ((int)blockIdx.x >= ntiles) return;
+  const int r0 = (blockIdx.x / tc) * 32, c0 = (blockIdx.x % tc) * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (size_t z = blockIdx.y; z < slots; z += gridDim.y) {
+    const float* src = m == 4 ? mst + z * d * d : st + z * 4 * hd + m * hd;
+    CT* dst = out + z * slot + (m == 4 ? 4 * hd : m * hd);
+    for (int k = ty; k < 32; k += 8) {
+      const int r = r0 + k, c = c0 + tx;
+      t[k][tx] = (r < R && c < Cc) ? src[(size_t)r * Cc + c] : 0.f;
+    }
+    __syncthreads();
+    for (int k = ty; k < 32; k += 8) {
+      const int c = c0 + k, r = r0 + tx;
+      if (c < Cc && r < R) dst[(size_t)c * R + r] = from_f<CT>(t[tx][k]);
+    }
+    __syncthreads();
+  }
+}
+
+hipError_t launch_pack_states(const float* states, const float* mstates, void* out, int units,
+                              int nslots, int d, int hid, int with_m, int bf16, hipStream_t st) {
+  const int tiles = ((hid + 31) / 32) * ((d + 31) / 32);
+  const size_t slots = (size_t)units * nslots;
+  const dim3 grid(tiles, (unsigned)std::min<size_t>(slots, 65535), 5);
+  if (bf16)
+    hipLaunchKernelGGL(pack_states_kernel<__bf16>, grid, dim3(256), 0, st, states, mstates,
+                       (__bf16*)out, slots, d, hid, with_m);
+  else
+    hipLaunchKernelGGL(pack_states_kernel<float>, grid, dim3(256), 0, st, states, mstates,
+                       (float*)out, slots, d, hid, with_m);
   return hipGetLastError();
 }
 

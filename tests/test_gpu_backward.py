@@ -72,6 +72,10 @@ SMALL = [
                  name="bf16 d64 h256"),
     small_config(BF16, ACT_SILU, B=1, H=1, L=128, d=128, hid=512, C_G=128,
                  locals_=((64, 128),), name="bf16 d128 h512"),
+    small_config(BF16, ACT_SILU, B=1, H=2, L=256, d=64, hid=256, C_G=128,
+                 locals_=((64, 128),), name="bf16 d64 h256 C64"),
+    small_config(BF16, ACT_SILU, B=1, H=1, L=192, d=64, hid=256, C_G=96,
+                 locals_=((48, 96),), name="bf16 d64 h256 C48 ragged"),
 ]
 
 
