@@ -79,6 +79,47 @@ def launch_flops(cfg, name):
 
 
 # ----------------------------------------------------------------------------
+# measured HBM traffic of a launch (rocprofv3 FETCH_SIZE / WRITE_SIZE, calibrated
+# against a plain copy; committed under profiles/), valid while the sources of
+# the launch's kernels still hash to the recorded value
+# ----------------------------------------------------------------------------
+TRAFFIC_FILE = {2: "hbm_traffic_pretrain_B4H8L8192.txt"}
+_COMMON = ["tnt_device.h", "tnt_kernels.h"]
+LAUNCH_SOURCES = {
+    "local_bwd": ["tnt_local_bwd_blk.hip", "tnt_local_bwd_layout.h", "tnt_local_common.h"] + _COMMON,
+    "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_common.h"] + _COMMON,
+    "global_bwd_chunk": ["tnt_global_bwd.hip"] + _COMMON,
+    "global_fwd_chunk": ["tnt_global_fwd.hip"] + _COMMON,
+    "pack_states": ["tnt_local_bwd.hip"] + _COMMON,
+}
+
+
+def sources_hash(label):
+    import hashlib
+    h = hashlib.sha256()
+    for fn in LAUNCH_SOURCES[label]:
+        with open(os.path.join(ROOT, "paper_2511_07343_amd", "csrc", fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, label):
+    """HBM bytes per launch of `label` from the committed counter summary, or None."""
+    fn = TRAFFIC_FILE.get(workload)
+    if fn is None or label not in LAUNCH_SOURCES:
+        return None
+    path = os.path.join(ROOT, "profiles", fn)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            t = line.split()
+            if len(t) >= 10 and t[0] == "launch" and t[1] == label:
+                return float(t[9]) if t[3] == sources_hash(label) else None
+    return None
+
+
+# ----------------------------------------------------------------------------
 def cpu_baseline(cfg, inp, budget_tokens):
     """fp64 oracle, fwd + bwd, on one (batch 0, head 0) chain restricted to its
     first `budget_tokens` tokens (one local shard and one global chunk at the
@@ -112,6 +153,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=0,
                     help="tokens of the CPU-oracle sample (default: one local shard)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="run one plain device copy of BYTES before the warmup (the "
+                         "reference dispatch that scales HBM traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -134,6 +178,12 @@ def main():
          (("dq", "q"), ("dk", "k"), ("dv", "v"), ("dlr", "lr"), ("dmom", "mom"),
           ("ddecay", "decay"), ("dW1", "W1"), ("dW2", "W2"))}
     stream = torch.cuda.current_stream(dev)
+    if args.copy_probe:
+        src = torch.ones(args.copy_probe, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         s1 = tnt.tnt_mem_fwd(cfg, x["q"], x["k"], x["v"], x["lr"], x["mom"], x["decay"], x["W1"],
@@ -179,6 +229,13 @@ def main():
     if fl is not None:
         ach = fl / (avg_ms * 1e-3) / 1e12
         roof.update(achieved=ach, frac=ach * 1e12 / peak, flops_per_launch=fl)
+    roof["traffic"] = measured_traffic(args.workload, name)
+    props = torch.cuda.get_device_properties(dev)
+    clk = getattr(props, "clock_rate", None)
+    device = {"name": props.name, "compute_units": props.multi_processor_count,
+              "clock_mhz": (clk / 1e3) if clk else None,
+              "peak_used_tflops": peak / 1e12,
+              "peak_note": "published MI355X dense peak (bf16 MFMA 2.5 PFLOP/s, fp32 157.3 TFLOP/s)"}
 
     res = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1,
@@ -191,6 +248,7 @@ def main():
         "algorithmic_tflops": flops / elapsed * args.steps / 1e12,
         "algorithmic_frac_of_peak": flops / elapsed * args.steps / peak,
         "roofline": roof,
+        "device": device,
         "kernels_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())},
     }
     if not args.no_cpu_baseline:

@@ -291,6 +291,19 @@ __device__ __forceinline__ void mma_blk(f4 (&acc)[RB][CB], const EA* A, int lda,
 #pragma unroll
       for (int c = 0; c < CB; ++c) MM::mma(acc[r][c], xa[r], xb[c]);
   };
+  constexpr int NS = (K + MM::KS - 1) / MM::KS;
+  constexpr int FRAG_REGS = sizeof(typename MM::frag) / 4;
+  constexpr int REGS_A = RB * (sizeof(EA) > sizeof(CT) ? 2 : 1) * FRAG_REGS;
+  constexpr int REGS_B = CB * (sizeof(EB) > sizeof(CT) ? 2 : 1) * FRAG_REGS;
+  if constexpr (NS > 2 && NS * (REGS_A + REGS_B) <= 128) {
+    // small block, long K: every step's loads in flight at once
+    typename MM::frag ga[NS][RB], gb[NS][CB];
+#pragma unroll
+    for (int t = 0; t < NS; ++t) fetch(t * MM::KS, ga[t], gb[t]);
+#pragma unroll
+    for (int t = 0; t < NS; ++t) apply(ga[t], gb[t]);
+    return;
+  }
   fetch(0, fa, fb);
 #pragma unroll 1
   for (int k0 = MM::KS; k0 < K; k0 += MM::KS) {

@@ -26,6 +26,38 @@ __device__ __forceinline__ float sum16b(float v) {
   return v;
 }
 
+template <typename IO>
+__device__ __forceinline__ void load8(const IO* p, float (&x)[8]);
+template <>
+__device__ __forceinline__ void load8<__bf16>(const __bf16* p, float (&x)[8]) {
+  const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int t = 0; t < 8; ++t) x[t] = (float)v[t];
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float (&x)[8]) {
+  const f32x4 u = *reinterpret_cast<const f32x4*>(p), v = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    x[t] = u[t];
+    x[t + 4] = v[t];
+  }
+}
+template <typename CT>
+__device__ __forceinline__ void store8(CT* p, const float (&x)[8]);
+template <>
+__device__ __forceinline__ void store8<__bf16>(__bf16* p, const float (&x)[8]) {
+  bf16x8 v;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) v[t] = (__bf16)x[t];
+  *reinterpret_cast<bf16x8*>(p) = v;
+}
+template <>
+__device__ __forceinline__ void store8<float>(float* p, const float (&x)[8]) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{x[0], x[1], x[2], x[3]};
+  *reinterpret_cast<f32x4*>(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+}
+
 }  // namespace
 
 template <int CP, int D, int H>
@@ -40,6 +72,7 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
   __shared__ Coef cf;
   __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC], gEta[MAXC], gLa[MAXC], gLb[MAXC];
   __shared__ float dpart[3][16];
+  __shared__ float kss[16][MAXC];  // partial squared key norms per 8-column block
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int d = D, h = H, Cp = CP;
   constexpr int HP = (H / 16 > D / 16 ? H / 16 : D / 16);
@@ -155,22 +188,74 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
     }
 
     // ================= recompute the chunk's forward quantities
-    stage_rows<IO, CT>(Q, QT, qg + (size_t)tok0 * d, C, Cp, d);
-    stage_rows<IO, CT>(K, KT, kg + (size_t)tok0 * d, C, Cp, d);
-    stage_rows<IO, CT>(dO, dOT, dOg + (size_t)tok0 * d, C, Cp, d);
-    if (Dm.qk_proj) unit_keys<IO, CT>(cf, N, NT, kg + (size_t)tok0 * d, C, Cp, d);
-    chunk_coefs(cf, lr, mom, dec, tok0, C, Cp);
-    for (int e = threadIdx.x; e < Cp * d; e += blockDim.x) {
-      const int i = e % Cp, j = e / Cp;  // consecutive threads: consecutive rows
-      const size_t en = (size_t)i * d + j, et = (size_t)j * Cp + i;
-      const float x = to_f(dO[en]), kx = to_f(K[en]);
-      dOAT[et] = from_f<CT>(cf.A[i] * x);
-      dOET[et] = from_f<CT>(cf.E[i] * x);
-      dOA[en] = from_f<CT>(cf.A[i] * x);
-      dOE[en] = from_f<CT>(cf.E[i] * x);
-      KcC[en] = from_f<CT>(cf.cC[i] * kx);
-      Kb[en] = from_f<CT>(cf.bb[i] * kx);
+    // Stage Q, K, dO rows and their transposes: one (row, 8-column block)
+    // per thread, consecutive threads on consecutive rows (the transposed
+    // writes coalesce); partial squared key norms go to LDS.
+    constexpr int JB = D / 8, ITEMS = CP * JB, PER = (ITEMS + 511) / 512;
+    float kx[PER][8], ox[PER][8];
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = threadIdx.x + p * 512;
+      if (e < ITEMS) {
+        const int i = e % CP, j0 = (e / CP) * 8;
+        const size_t gofs = (size_t)(tok0 + i) * d + j0, en = (size_t)i * d + j0;
+        float qx[8];
+        if (i < C) {
+          load8(qg + gofs, qx);
+          load8(kg + gofs, kx[p]);
+          load8(dOg + gofs, ox[p]);
+        } else {
+#pragma unroll
+          for (int t = 0; t < 8; ++t) qx[t] = kx[p][t] = ox[p][t] = 0.f;
+        }
+        store8<CT>(Q + en, qx);
+        store8<CT>(K + en, kx[p]);
+        store8<CT>(dO + en, ox[p]);
+        float ss = 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const size_t et = (size_t)(j0 + t) * Cp + i;
+          QT[et] = from_f<CT>(qx[t]);
+          KT[et] = from_f<CT>(kx[p][t]);
+          dOT[et] = from_f<CT>(ox[p][t]);
+          ss += kx[p][t] * kx[p][t];
+        }
+        kss[j0 / 8][i] = ss;
+      }
     }
+    chunk_coefs(cf, lr, mom, dec, tok0, C, Cp);  // ends with a barrier
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = threadIdx.x + p * 512;
+      if (e < ITEMS) {
+        const int i = e % CP, j0 = (e / CP) * 8;
+        const size_t en = (size_t)i * d + j0;
+        float n2 = 0.f;
+#pragma unroll
+        for (int t = 0; t < JB; ++t) n2 += kss[t][i];  // fixed order: deterministic
+        const float nr = sqrtf(n2);
+        if (j0 == 0) cf.knorm[i] = nr;
+        float va[8], ve[8], vc[8], vb[8], vn[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const size_t et = (size_t)(j0 + t) * Cp + i;
+          va[t] = cf.A[i] * ox[p][t];
+          ve[t] = cf.E[i] * ox[p][t];
+          vc[t] = cf.cC[i] * kx[p][t];
+          vb[t] = cf.bb[i] * kx[p][t];
+          vn[t] = (i < C && nr > 0.f) ? kx[p][t] / nr : 0.f;
+          dOAT[et] = from_f<CT>(va[t]);
+          dOET[et] = from_f<CT>(ve[t]);
+          if (Dm.qk_proj) NT[et] = from_f<CT>(vn[t]);
+        }
+        store8<CT>(dOA + en, va);
+        store8<CT>(dOE + en, ve);
+        store8<CT>(KcC + en, vc);
+        store8<CT>(Kb + en, vb);
+        if (Dm.qk_proj) store8<CT>(N + en, vn);
+      }
+    }
+    __syncthreads();
     if (threadIdx.x < MAXC) {
       gA[threadIdx.x] = gE[threadIdx.x] = gCC[threadIdx.x] = gB[threadIdx.x] = 0.f;
     }
