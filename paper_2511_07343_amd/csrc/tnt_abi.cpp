@@ -66,11 +66,12 @@ struct Layout {
   size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], saved_bytes;
   int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
   // forward workspace
-  size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_scr[TNT_MAX_LOCAL], w_ring, fwd_bytes;
+  size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL], w_ring,
+      fwd_bytes;
   size_t ring_g, ring_l[TNT_MAX_LOCAL], ring_m[TNT_MAX_LOCAL];
   LocalPlan lplan[TNT_MAX_LOCAL];
   // backward workspace
-  size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32,
+  size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32, b_gpackA, b_gop,
       b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
       b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_stT[TNT_MAX_LOCAL], b_states, bwd_bytes,
       bwd_re_bytes;
@@ -113,8 +114,11 @@ Layout layout_of(const tnt_config* c) {
     y.w_chunkc = off; off += up((size_t)y.BH * y.g_chunks * 4 * f);
     y.w_R = off; off += up((size_t)y.BH * c->C_G * c->d * f);
     const Dims D = dims_of(c, c->C_G, c->L);
-    const int ns = std::max(global_fwd_splits(D), global_bwd_splits(D));
+    const int ns = std::max({global_fwd_splits(D), global_bwd_splits(D), global_blk_splits(D), 1});
     y.w_part = off; off += up((size_t)y.BH * ns * 4 * y.hd * f);
+    // transposed state copies and the chunk operands of the fixed-size global kernels
+    y.w_gpack = off; off += up((size_t)y.BH * 4 * y.hd * cts);
+    y.w_gop = off; off += up((size_t)y.BH * (2 * (size_t)c->hid + 4 * (size_t)c->d) * c->C_G * cts);
   }
   for (int i = 0; i < c->n_local; ++i) {
     const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
@@ -144,6 +148,8 @@ Layout layout_of(const tnt_config* c) {
     const Dims D = dims_of(c, c->C_G, c->L);
     y.b_gscr = off;
     off += up(global_bwd_scratch_bytes(D, &y.b_gscr_f32));
+    y.b_gpackA = off; off += up((size_t)y.BH * 4 * y.hd * cts);
+    y.b_gop = off; off += up((size_t)y.BH * 5 * ((size_t)c->hid + c->d) * c->C_G * cts);
   }
   for (int i = 0; i < c->n_local; ++i) {
     const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
@@ -269,6 +275,8 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     g.chunkc = (float*)(ws + y.w_chunkc);
     g.Rbuf = (float*)(ws + y.w_R);
     g.part = (float*)(ws + y.w_part);
+    g.packT = ws + y.w_gpack;
+    g.opT = ws + y.w_gop;
     g.D = dims_of(c, c->C_G, c->L);
     g.force_generic = generic_only();
     HIP_TIMED("global_scan", launch_global_scan(g, st));
@@ -344,6 +352,9 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     g.scratch_f32_off = y.b_gscr_f32;
     g.dq_part = dqp; g.dk_part = dkp; g.dv_part = dvp;
     g.dlr = dlr; g.dmom = dmom; g.ddecay = ddecay;
+    g.packT = ws + y.w_gpack;
+    g.packA = ws + y.b_gpackA;
+    g.opT = ws + y.b_gop;
     g.D = dims_of(c, c->C_G, c->L);
     g.force_generic = generic_only();
     HIP_TIMED("global_scan", launch_global_scan(g, st));

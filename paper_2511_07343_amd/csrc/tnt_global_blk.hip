@@ -1,0 +1,620 @@
+// Global memory, fixed sizes: the chunk phases of the runtime-sized global
+// kernels (same quantities and formulas, written out there), restructured
+// around register-blocked wave tiles and contraction-contiguous operands:
+//
+//  forward chunk n   transpose  V1^T, V2^T of the chunk-entry state (bf16)
+//                    tile       token tiles: O_G, R, Hk, D1 with every
+//                               intermediate in LDS; writes the carry operands
+//                               D1^T, Hk^T (hid x C) and (cC K)^T, (b K)^T,
+//                               (cC R)^T, (b R)^T (d x C) in bf16
+//                    carry      split-K GEMMs over the chunk's tokens into the
+//                               split partials that global_carry_reduce sums
+//  backward chunk n  transpose  V1^T, V2^T and the exit adjoint's four
+//                               transposes
+//                    tile       token tiles: the per-token adjoints (d q, d k,
+//                               d v, coefficient adjoints) with intermediates in
+//                               LDS; writes the operands of the entry adjoint
+//                               Zkbar^T, Zqbar^T, Gbar^T, Hk^T, Hq^T (hid x C)
+//                               and K^T, Q^T, R^T, Ykbar^T, dO^T (d x C)
+//                    state      split-K GEMMs into the partials that
+//                               gbwd_state_reduce sums
+#include "tnt_device.h"
+#include "tnt_kernels.h"
+
+#include <algorithm>
+
+namespace tnt {
+
+namespace {
+
+constexpr int GTK = 256;  // tokens per split of the carry / state GEMMs
+
+template <int H>
+constexpr int gtile_rows() {
+  return H <= 256 ? 64 : 32;
+}
+
+template <typename IO>
+__device__ __forceinline__ void gload8(const IO* p, float (&x)[8]);
+template <>
+__device__ __forceinline__ void gload8<__bf16>(const __bf16* p, float (&x)[8]) {
+  const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int t = 0; t < 8; ++t) x[t] = (float)v[t];
+}
+template <>
+__device__ __forceinline__ void gload8<float>(const float* p, float (&x)[8]) {
+  const f32x4 u = *reinterpret_cast<const f32x4*>(p), v = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    x[t] = u[t];
+    x[t + 4] = v[t];
+  }
+}
+template <typename CT>
+__device__ __forceinline__ void gstore8(CT* p, const float (&x)[8]);
+template <>
+__device__ __forceinline__ void gstore8<__bf16>(__bf16* p, const float (&x)[8]) {
+  bf16x8 v;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) v[t] = (__bf16)x[t];
+  *reinterpret_cast<bf16x8*>(p) = v;
+}
+
+__device__ __forceinline__ float gsum16(float v) {
+  v += __shfl_xor(v, 1, WAVE);
+  v += __shfl_xor(v, 2, WAVE);
+  v += __shfl_xor(v, 4, WAVE);
+  v += __shfl_xor(v, 8, WAVE);
+  return v;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Transposed bf16 copies of a chain's four state matrices: W1 (hid x d) ->
+// [d][hid], W2 (d x hid) -> [hid][d], S1, S2 alike; `mask` bit m selects
+// matrix m.  One 32 x 32 tile per workgroup.
+// ---------------------------------------------------------------------------
+template <typename CT>
+__global__ void __launch_bounds__(256) gtranspose_kernel(const float* src, size_t src_stride,
+                                                         CT* dst, int d, int h, int mask) {
+  __shared__ float t[32][33];
+  const int m = blockIdx.z;
+  if (!((mask >> m) & 1)) return;
+  const int chain = blockIdx.y;
+  const size_t hd = (size_t)h * d;
+  const int R = (m & 1) ? d : h, Cc = (m & 1) ? h : d;
+  const int tc = Cc / 32;
+  const int r0 = (blockIdx.x / tc) * 32, c0 = (blockIdx.x % tc) * 32;
+  const float* s = src + chain * src_stride + m * hd;
+  CT* o = dst + (size_t)chain * 4 * hd + m * hd;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8) t[k][tx] = s[(size_t)(r0 + k) * Cc + c0 + tx];
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) o[(size_t)(c0 + k) * R + r0 + tx] = from_f<CT>(t[tx][k]);
+}
+
+template <typename CT>
+static void launch_gtranspose(const float* src, size_t src_stride, CT* dst, int chains, int d,
+                              int h, int mask, hipStream_t st) {
+  const dim3 grid((h / 32) * (d / 32), chains, 4);
+  hipLaunchKernelGGL(gtranspose_kernel<CT>, grid, dim3(256), 0, st, src, src_stride, dst, d, h,
+                     mask);
+}
+
+// ---------------------------------------------------------------------------
+// forward, token tiles of TT rows of chunk n
+// ---------------------------------------------------------------------------
+template <typename IO, typename CT, int ACT, int D, int H>
+__global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
+  constexpr int TT = gtile_rows<H>();
+  extern __shared__ __align__(16) unsigned char smem[];
+  CT* sQ = reinterpret_cast<CT*>(smem);  // [TT][D], later R
+  CT* sK = sQ + TT * D;                  // [TT][D]
+  CT* sHq = sK + TT * D;                 // [TT][H]
+  CT* sHk = sHq + TT * H;                // [TT][H]
+  CT* sSp = sHk + TT * H;                // [TT][H]  s'(Zk)
+  __shared__ float cC[TT], bb[TT];
+  const Dims Dm = a.D;
+  const int C = Dm.C;
+  const int chain = blockIdx.y, r0 = blockIdx.x * TT;
+  constexpr size_t hd = (size_t)H * D;
+  const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
+  const float *V1 = V, *V2 = V + hd;
+  const CT* V2T = (const CT*)a.packT + (size_t)chain * 4 * hd + hd;  // [H][D]
+  CT* op = (CT*)a.opT + (size_t)chain * (2 * (size_t)H + 4 * (size_t)D) * C;
+  CT *D1T = op, *HkT = D1T + (size_t)H * C, *KcT = HkT + (size_t)H * C, *KbT = KcT + (size_t)D * C,
+     *RcT = KbT + (size_t)D * C, *RbT = RcT + (size_t)D * C;
+  const size_t tok0 = (size_t)n * C + r0;
+  const size_t cb = (size_t)chain * Dm.L + tok0;
+  const IO* q = (const IO*)a.q + cb * D;
+  const IO* k = (const IO*)a.k + cb * D;
+  const IO* v = (const IO*)a.v + cb * D;
+  float* o = a.o_part + cb * D;
+  const float* tk = a.tokc + cb * TKS;
+  const float rscale = 2.0f / (float)D;
+
+  if (threadIdx.x < TT) {
+    cC[threadIdx.x] = tk[(size_t)threadIdx.x * TKS + 0];
+    bb[threadIdx.x] = tk[(size_t)threadIdx.x * TKS + 1];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < TT * (D / 8); e += blockDim.x) {
+    const int i = e % TT, j0 = (e / TT) * 8;
+    float qx[8], kx[8];
+    gload8(q + (size_t)i * D + j0, qx);
+    gload8(k + (size_t)i * D + j0, kx);
+    gstore8<CT>(sQ + (size_t)i * D + j0, qx);
+    gstore8<CT>(sK + (size_t)i * D + j0, kx);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const size_t et = (size_t)(j0 + t) * C + r0 + i;
+      KcT[et] = from_f<CT>(cC[i] * kx[t]);
+      KbT[et] = from_f<CT>(bb[i] * kx[t]);
+    }
+  }
+  __syncthreads();
+  using BH = Blk<TT, H>;
+  using BD = Blk<TT, D>;
+  // Zq = Q V1^T -> Hq ; Zk = K V1^T -> Hk, s'(Zk)
+  for_blocks<TT, H>([&](int i0, int j0) {
+    f4 aq[BH::RB][BH::CB], ak[BH::RB][BH::CB];
+    zero_blk(aq);
+    zero_blk(ak);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(aq, sQ, D, i0, V1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ak, sK, D, i0, V1, D, j0);
+    blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 hv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t e = (size_t)(i + r) * H + j;
+        const ActVals z = act_all<ACT>(ak[rb][cb_][r]);
+        sHq[e] = from_f<CT>(act_f<ACT>(aq[rb][cb_][r]));
+        sHk[e] = from_f<CT>(z.s);
+        sSp[e] = from_f<CT>(z.d1);
+        hv[r] = z.s;
+      }
+      store4<CT>(HkT + (size_t)j * C + r0 + i, hv);
+    });
+  });
+  __syncthreads();
+  // O_G = Hq V2^T ; R = (2/d)(Hk V2^T - V)
+  CT* sR = sQ;
+  for_blocks<TT, D>([&](int i0, int j0) {
+    f4 ao[BD::RB][BD::CB], ay[BD::RB][BD::CB];
+    zero_blk(ao);
+    zero_blk(ay);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ao, sHq, H, i0, V2, H, j0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ay, sHk, H, i0, V2, H, j0);
+    blk_each4<BD::RB, BD::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 rc, rbv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ii = i + r;
+        const size_t e = (size_t)ii * D + j;
+        o[e] = ao[rb][cb_][r];
+        const float rv = rscale * (ay[rb][cb_][r] - to_f(v[e]));
+        sR[e] = from_f<CT>(rv);
+        rc[r] = cC[ii] * rv;
+        rbv[r] = bb[ii] * rv;
+      }
+      store4<CT>(RcT + (size_t)j * C + r0 + i, rc);
+      store4<CT>(RbT + (size_t)j * C + r0 + i, rbv);
+    });
+  });
+  __syncthreads();
+  // G = R V2, D1 = G * s'(Zk)
+  for_blocks<TT, H>([&](int i0, int j0) {
+    f4 ag[BH::RB][BH::CB];
+    zero_blk(ag);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ag, sR, D, i0, V2T, D, j0);
+    blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 dv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dv[r] = ag[rb][cb_][r] * to_f(sSp[(size_t)(i + r) * H + j]);
+      store4<CT>(D1T + (size_t)j * C + r0 + i, dv);
+    });
+  });
+}
+
+// ---------------------------------------------------------------------------
+// forward carry partials of token split `blockIdx.x`:
+//   m = 0: D1^T (cC K) -> V1 slot,  m = 1: D1^T (b K) -> S1 slot   (hid x d)
+//   m = 2: (cC R)^T Hk -> V2 slot,  m = 3: (b R)^T Hk -> S2 slot   (d x hid)
+// ---------------------------------------------------------------------------
+template <typename CT, int D, int H>
+__global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
+  const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
+  const int C = a.D.C;
+  constexpr size_t hd = (size_t)H * D;
+  const CT* op = (const CT*)a.opT + (size_t)chain * (2 * (size_t)H + 4 * (size_t)D) * C;
+  const CT *D1T = op, *HkT = D1T + (size_t)H * C, *KcT = HkT + (size_t)H * C,
+           *KbT = KcT + (size_t)D * C, *RcT = KbT + (size_t)D * C, *RbT = RcT + (size_t)D * C;
+  const size_t k0 = (size_t)split * GTK;
+  float* P = a.part + ((size_t)chain * ns + split) * 4 * hd;
+  if (m < 2) {
+    using BK = Blk<H, D>;
+    const CT* B = (m == 0 ? KcT : KbT) + k0;
+    float* out = P + (m == 0 ? 0 : 2 * hd);
+    for_blocks<H, D>([&](int i0, int j0) {
+      f4 acc[BK::RB][BK::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, D1T + k0, C, i0, B, C, j0);
+      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
+      });
+    });
+  } else {
+    using BK = Blk<D, H>;
+    const CT* A = (m == 2 ? RcT : RbT) + k0;
+    float* out = P + (m == 2 ? hd : 3 * hd);
+    for_blocks<D, H>([&](int i0, int j0) {
+      f4 acc[BK::RB][BK::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, A, C, i0, HkT + k0, C, j0);
+      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * H + j] = acc[rb][cb_][r];
+      });
+    });
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward, token tiles of TT rows of chunk n (exit adjoint in slot (n+1)&1)
+// ---------------------------------------------------------------------------
+template <typename IO, typename CT, int ACT, int D, int H>
+__global__ void __launch_bounds__(512) gbwd_tile_kernel(GlobalArgs a, int n) {
+  constexpr int TT = gtile_rows<H>();
+  constexpr int TN = D / 16;
+  extern __shared__ __align__(16) unsigned char smem[];
+  CT* rA = reinterpret_cast<CT*>(smem);  // [TT][D] K
+  CT* rB = rA + TT * D;                  // [TT][D] Q, then R
+  CT* rC = rB + TT * D;                  // [TT][D] dO, then Ykbar
+  CT* rD = rC + TT * D;                  // [TT][H] Zk
+  CT* rE = rD + TT * H;                  // [TT][H] Hk, then D1, then Zkbar
+  CT* rF = rE + TT * H;                  // [TT][H] Zqbar, then Gbar
+  CT* rG = rF + TT * H;                  // [TT][H] D1bar G s''(Zk)
+  CT *sK = rA, *sQ = rB, *sR = rB, *sdO = rC, *sYkb = rC, *sZk = rD, *sHk = rE, *sD1 = rE,
+     *sZkb = rE, *sZqb = rF, *sGb = rF, *sZkp = rG;
+  __shared__ float cC[TT], bb[TT];
+  __shared__ float gp[2][TN][TT];
+  const Dims Dm = a.D;
+  const int C = Dm.C;
+  const int chain = blockIdx.y, r0 = blockIdx.x * TT;
+  constexpr size_t hd = (size_t)H * D;
+  const float* V = a.states + ((size_t)chain * a.nslots + n) * 4 * hd;
+  const float *V1 = V, *V2 = V + hd;
+  const float* Ab = a.adj + ((size_t)chain * 2 + ((n + 1) & 1)) * 4 * hd;
+  const float *Vb1 = Ab, *Vb2 = Ab + hd, *Sb1 = Ab + 2 * hd, *Sb2 = Ab + 3 * hd;
+  const CT* pS = (const CT*)a.packT + (size_t)chain * 4 * hd;
+  const CT *V1T = pS, *V2T = pS + hd;  // [D][H], [H][D]
+  const CT* pA = (const CT*)a.packA + (size_t)chain * 4 * hd;
+  const CT *Vb1T = pA, *Vb2T = pA + hd, *Sb1T = pA + 2 * hd, *Sb2T = pA + 3 * hd;
+  CT* op = (CT*)a.opT + (size_t)chain * 5 * ((size_t)H + D) * C;
+  CT *ZkbT = op, *ZqbT = ZkbT + (size_t)H * C, *GbT = ZqbT + (size_t)H * C,
+     *HkT = GbT + (size_t)H * C, *HqT = HkT + (size_t)H * C, *KT = HqT + (size_t)H * C,
+     *QT = KT + (size_t)D * C, *RT = QT + (size_t)D * C, *YkbT = RT + (size_t)D * C,
+     *dOT = YkbT + (size_t)D * C;
+  const size_t tok0 = (size_t)n * C + r0;
+  const size_t cb = (size_t)chain * Dm.L + tok0;
+  const IO* q = (const IO*)a.q + cb * D;
+  const IO* k = (const IO*)a.k + cb * D;
+  const IO* v = (const IO*)a.v + cb * D;
+  const IO* dO = (const IO*)a.dO + cb * D;
+  const float* tk = a.tokc + cb * TKS;
+  float* dtk = a.dtok + cb * 4;
+  float* dqp = a.dq_part + cb * D;
+  float* dkp = a.dk_part + cb * D;
+  float* dvp = a.dv_part + cb * D;
+  const float rscale = 2.0f / (float)D;
+  const int l = lane_id();
+
+  if (threadIdx.x < TT) {
+    cC[threadIdx.x] = tk[(size_t)threadIdx.x * TKS + 0];
+    bb[threadIdx.x] = tk[(size_t)threadIdx.x * TKS + 1];
+  }
+  for (int e = threadIdx.x; e < TT * (D / 8); e += blockDim.x) {
+    const int i = e % TT, j0 = (e / TT) * 8;
+    float qx[8], kx[8], ox[8];
+    gload8(q + (size_t)i * D + j0, qx);
+    gload8(k + (size_t)i * D + j0, kx);
+    gload8(dO + (size_t)i * D + j0, ox);
+    gstore8<CT>(sQ + (size_t)i * D + j0, qx);
+    gstore8<CT>(sK + (size_t)i * D + j0, kx);
+    gstore8<CT>(sdO + (size_t)i * D + j0, ox);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const size_t et = (size_t)(j0 + t) * C + r0 + i;
+      KT[et] = from_f<CT>(kx[t]);
+      QT[et] = from_f<CT>(qx[t]);
+      dOT[et] = from_f<CT>(ox[t]);
+    }
+  }
+  __syncthreads();
+  using BH = Blk<TT, H>;
+  using BD = Blk<TT, D>;
+  // Zk -> Hk ; Zq -> Hq ; Zqbar = (dO V2) * s'(Zq)
+  for_blocks<TT, H>([&](int i0, int j0) {
+    f4 ak[BH::RB][BH::CB], aq[BH::RB][BH::CB], ap[BH::RB][BH::CB];
+    zero_blk(ak);
+    zero_blk(aq);
+    zero_blk(ap);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ak, sK, D, i0, V1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(aq, sQ, D, i0, V1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ap, sdO, D, i0, V2T, D, j0);
+    blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 hk, hq, zq;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t e = (size_t)(i + r) * H + j;
+        const float zk = ak[rb][cb_][r];
+        const ActVals z = act_all<ACT>(aq[rb][cb_][r]);
+        hk[r] = act_f<ACT>(zk);
+        hq[r] = z.s;
+        zq[r] = ap[rb][cb_][r] * z.d1;
+        sZk[e] = from_f<CT>(zk);
+        sHk[e] = from_f<CT>(hk[r]);
+        sZqb[e] = from_f<CT>(zq[r]);
+      }
+      const size_t et = (size_t)j * C + r0 + i;
+      store4<CT>(HkT + et, hk);
+      store4<CT>(HqT + et, hq);
+      store4<CT>(ZqbT + et, zq);
+    });
+  });
+  __syncthreads();
+  // R = (2/d)(Hk V2^T - V) ; T5 = Hk V2bar'^T ; T6 = Hk S2bar'^T ; dq = Zqbar V1
+  f4 t3[BD::RB][BD::CB], t4[BD::RB][BD::CB], t5[BD::RB][BD::CB], t6[BD::RB][BD::CB];
+  static_assert(BD::NB <= 8, "one (TT x D) block per wave");
+  const bool own = wave_id() < BD::NB;
+  const int di0 = (wave_id() / BD::NBN) * BD::RB * 16, dj0 = (wave_id() % BD::NBN) * BD::CB * 16;
+  zero_blk(t5);
+  zero_blk(t6);
+  if (own) {
+    f4 ay[BD::RB][BD::CB], aq[BD::RB][BD::CB];
+    zero_blk(ay);
+    zero_blk(aq);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ay, sHk, H, di0, V2, H, dj0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(t5, sHk, H, di0, Vb2, H, dj0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(t6, sHk, H, di0, Sb2, H, dj0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(aq, sZqb, H, di0, V1T, H, dj0);
+    blk_each4<BD::RB, BD::CB>(di0, dj0, [&](int rb, int cb_, int i, int j) {
+      f4 rv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t e = (size_t)(i + r) * D + j;
+        rv[r] = rscale * (ay[rb][cb_][r] - to_f(v[e]));
+        dqp[e] = aq[rb][cb_][r];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sR[(size_t)(i + r) * D + j] = from_f<CT>(rv[r]);  // Q is dead
+      store4<CT>(RT + (size_t)j * C + r0 + i, rv);
+    });
+  }
+  __syncthreads();
+  // G = R V2 ; D1 = G s'(Zk) ; D1bar = -cC K V1bar'^T - b K S1bar'^T ; Gbar ; Zkp
+  for_blocks<TT, H>([&](int i0, int j0) {
+    f4 ag[BH::RB][BH::CB], a1[BH::RB][BH::CB], a2[BH::RB][BH::CB];
+    zero_blk(ag);
+    zero_blk(a1);
+    zero_blk(a2);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ag, sR, D, i0, V2T, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(a1, sK, D, i0, Vb1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(a2, sK, D, i0, Sb1, D, j0);
+    blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 gv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ii = i + r;
+        const size_t e = (size_t)ii * H + j;
+        const ActVals z = act_all<ACT>(to_f(sZk[e]));
+        const float g = ag[rb][cb_][r];
+        const float d1b = -cC[ii] * a1[rb][cb_][r] - bb[ii] * a2[rb][cb_][r];
+        sD1[e] = from_f<CT>(g * z.d1);
+        gv[r] = d1b * z.d1;
+        sGb[e] = from_f<CT>(gv[r]);
+        sZkp[e] = from_f<CT>(d1b * g * z.d2);
+      }
+      store4<CT>(GbT + (size_t)j * C + r0 + i, gv);
+    });
+  });
+  __syncthreads();
+  // T3 = D1 V1bar', T4 = D1 S1bar' ; Rbar = -cC T5 - b T6 + Gbar V2^T ; Ykbar ; Vbar ;
+  // adjoints of cC_t, b_t: -(K . T3 + R . T5), -(K . T4 + R . T6)
+  if (own) {
+    f4 ag[BD::RB][BD::CB];
+    zero_blk(t3);
+    zero_blk(t4);
+    zero_blk(ag);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(t3, sD1, H, di0, Vb1T, H, dj0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(t4, sD1, H, di0, Sb1T, H, dj0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ag, sGb, H, di0, V2, H, dj0);
+    blk_each4<BD::RB, BD::CB>(di0, dj0, [&](int rb, int cb_, int i, int j) {
+      f4 yv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ii = i + r;
+        const size_t e = (size_t)ii * D + j;
+        const float rbv = -cC[ii] * t5[rb][cb_][r] - bb[ii] * t6[rb][cb_][r] + ag[rb][cb_][r];
+        yv[r] = rscale * rbv;
+        sYkb[e] = from_f<CT>(yv[r]);
+        dvp[e] = -yv[r];
+        const float kx = to_f(sK[e]), rx = to_f(sR[e]);
+        const float s1 = gsum16(kx * t3[rb][cb_][r] + rx * t5[rb][cb_][r]);
+        const float s2 = gsum16(kx * t4[rb][cb_][r] + rx * t6[rb][cb_][r]);
+        if ((l & 15) == 0) {
+          gp[0][j >> 4][ii] = s1;
+          gp[1][j >> 4][ii] = s2;
+        }
+      }
+      store4<CT>(YkbT + (size_t)j * C + r0 + i, yv);
+    });
+  }
+  __syncthreads();
+  if (threadIdx.x < TT) {
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+      s1 += gp[0][t][threadIdx.x];
+      s2 += gp[1][t][threadIdx.x];
+    }
+    dtk[(size_t)threadIdx.x * 4 + 0] = -s1;
+    dtk[(size_t)threadIdx.x * 4 + 1] = -s2;
+  }
+  // Hkbar = -cC R V2bar' - b R S2bar' + Ykbar V2 ; Zkbar = Hkbar s'(Zk) + Zkp
+  for_blocks<TT, H>([&](int i0, int j0) {
+    f4 a7[BH::RB][BH::CB], a8[BH::RB][BH::CB], ay[BH::RB][BH::CB];
+    zero_blk(a7);
+    zero_blk(a8);
+    zero_blk(ay);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(a7, sR, D, i0, Vb2T, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(a8, sR, D, i0, Sb2T, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ay, sYkb, D, i0, V2T, D, j0);
+    blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 zv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ii = i + r;
+        const size_t e = (size_t)ii * H + j;
+        const ActVals z = act_all<ACT>(to_f(sZk[e]));
+        const float hkb = -cC[ii] * a7[rb][cb_][r] - bb[ii] * a8[rb][cb_][r] + ay[rb][cb_][r];
+        zv[r] = hkb * z.d1 + to_f(sZkp[e]);
+        sZkb[e] = from_f<CT>(zv[r]);
+      }
+      store4<CT>(ZkbT + (size_t)j * C + r0 + i, zv);
+    });
+  });
+  __syncthreads();
+  // dk = -cC T3 - b T4 + Zkbar V1
+  if (own) {
+    f4 ak[BD::RB][BD::CB];
+    zero_blk(ak);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ak, sZkb, H, di0, V1T, H, dj0);
+    blk_each4<BD::RB, BD::CB>(di0, dj0, [&](int rb, int cb_, int i, int j) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int ii = i + r;
+        dkp[(size_t)ii * D + j] =
+            -cC[ii] * t3[rb][cb_][r] - bb[ii] * t4[rb][cb_][r] + ak[rb][cb_][r];
+      }
+    });
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward entry-adjoint partials of token split `blockIdx.x`:
+//   m = 0: Zkbar^T K + Zqbar^T Q            -> V1 slot (hid x d)
+//   m = 1: R^T Gbar + Ykbar^T Hk + dO^T Hq  -> V2 slot (d x hid)
+// ---------------------------------------------------------------------------
+template <typename CT, int D, int H>
+__global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
+  const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
+  const int C = a.D.C;
+  constexpr size_t hd = (size_t)H * D;
+  const CT* op = (const CT*)a.opT + (size_t)chain * 5 * ((size_t)H + D) * C;
+  const CT *ZkbT = op, *ZqbT = ZkbT + (size_t)H * C, *GbT = ZqbT + (size_t)H * C,
+           *HkT = GbT + (size_t)H * C, *HqT = HkT + (size_t)H * C, *KT = HqT + (size_t)H * C,
+           *QT = KT + (size_t)D * C, *RT = QT + (size_t)D * C, *YkbT = RT + (size_t)D * C,
+           *dOT = YkbT + (size_t)D * C;
+  const size_t k0 = (size_t)split * GTK;
+  float* P = a.part + ((size_t)chain * ns + split) * 4 * hd;
+  if (m == 0) {
+    using BK = Blk<H, D>;
+    for_blocks<H, D>([&](int i0, int j0) {
+      f4 acc[BK::RB][BK::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, ZkbT + k0, C, i0, KT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, ZqbT + k0, C, i0, QT + k0, C, j0);
+      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) P[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
+      });
+    });
+  } else {
+    using BK = Blk<D, H>;
+    for_blocks<D, H>([&](int i0, int j0) {
+      f4 acc[BK::RB][BK::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, RT + k0, C, i0, GbT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, YkbT + k0, C, i0, HkT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, dOT + k0, C, i0, HqT + k0, C, j0);
+      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) P[hd + (size_t)(i + r) * H + j] = acc[rb][cb_][r];
+      });
+    });
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers: true when the fixed-size path handles the shape
+// ---------------------------------------------------------------------------
+template <int D, int H>
+static bool gblk_shape(const GlobalArgs& a) {
+  return a.D.bf16 && a.D.d == D && a.D.hid == H && a.D.C % GTK == 0 &&
+         a.D.C % gtile_rows<H>() == 0 && a.packT && a.opT;
+}
+
+template <typename IO, typename ACT_T, int ACT, int D, int H>
+static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
+  typedef __bf16 CT;
+  constexpr int TT = gtile_rows<H>();
+  const int chains = a.D.B * a.D.H, C = a.D.C;
+  constexpr size_t hd = (size_t)H * D;
+  launch_gtranspose<CT>(a.states + (size_t)(n % a.nslots) * 4 * hd, (size_t)a.nslots * 4 * hd,
+                        (CT*)a.packT, chains, D, H, 0x3, st);
+  const size_t l1 = (2 * (size_t)TT * D + 3 * (size_t)TT * H) * sizeof(CT);
+  auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H>;
+  set_lds_limit((const void*)k1);
+  hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
+  const int ns = C / GTK;
+  hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H>), dim3(ns, 4, chains), dim3(512), 0, st, a);
+  return launch_global_carry_reduce(a, n, ns, st);
+}
+
+template <typename IO, typename ACT_T, int ACT, int D, int H>
+static hipError_t gbwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
+  typedef __bf16 CT;
+  constexpr int TT = gtile_rows<H>();
+  const int chains = a.D.B * a.D.H, C = a.D.C;
+  constexpr size_t hd = (size_t)H * D;
+  launch_gtranspose<CT>(a.states + (size_t)n * 4 * hd, (size_t)a.nslots * 4 * hd, (CT*)a.packT,
+                        chains, D, H, 0x3, st);
+  launch_gtranspose<CT>(a.adj + (size_t)((n + 1) & 1) * 4 * hd, 2 * 4 * hd, (CT*)a.packA, chains,
+                        D, H, 0xf, st);
+  const size_t l1 = (3 * (size_t)TT * D + 4 * (size_t)TT * H) * sizeof(CT);
+  auto k1 = gbwd_tile_kernel<IO, CT, ACT, D, H>;
+  set_lds_limit((const void*)k1);
+  hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
+  const int ns = C / GTK;
+  hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H>), dim3(ns, 2, chains), dim3(512), 0, st, a);
+  return launch_gbwd_state_reduce(a, n, ns, st);
+}
+
+bool launch_global_fwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err) {
+  if (a.force_generic) return false;
+  if (gblk_shape<64, 256>(a)) {
+    *err = a.D.act == ACT_SILU ? gfwd_blk_chunk<__bf16, void, ACT_SILU, 64, 256>(a, n, st)
+                               : gfwd_blk_chunk<__bf16, void, ACT_GELU, 64, 256>(a, n, st);
+    return true;
+  }
+  return false;
+}
+
+bool launch_global_bwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err) {
+  if (a.force_generic || !a.packA) return false;
+  if (gblk_shape<64, 256>(a)) {
+    *err = a.D.act == ACT_SILU ? gbwd_blk_chunk<__bf16, void, ACT_SILU, 64, 256>(a, n, st)
+                               : gbwd_blk_chunk<__bf16, void, ACT_GELU, 64, 256>(a, n, st);
+    return true;
+  }
+  return false;
+}
+
+// splits used by the fixed-size path (the partial buffer must hold them)
+int global_blk_splits(const Dims& D) { return D.C / GTK; }
+
+}  // namespace tnt

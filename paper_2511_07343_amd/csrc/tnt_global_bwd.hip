@@ -421,6 +421,12 @@ __global__ void __launch_bounds__(256) gbwd_state_reduce(GlobalArgs a, int n, in
   }
 }
 
+hipError_t launch_gbwd_state_reduce(const GlobalArgs& a, int n, int nsplit, hipStream_t st) {
+  hipLaunchKernelGGL(gbwd_state_reduce, dim3(GRED_BLOCKS, a.D.B * a.D.H), dim3(256), 0, st, a, n,
+                     nsplit);
+  return hipGetLastError();
+}
+
 int global_bwd_splits(const Dims& D) {
   const int tiles = (D.C + GBB_TT - 1) / GBB_TT;
   return std::max(1, std::min(16, tiles / 4));
@@ -459,6 +465,8 @@ static hipError_t launch_gbwd_t(const GlobalArgs& a, int n, void* scratch, size_
 }
 
 hipError_t launch_global_bwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {
+  hipError_t err = hipSuccess;
+  if (launch_global_bwd_blk(a, n, st, &err)) return err;
   void* sc = a.scratch;
   const size_t fo = a.scratch_f32_off;
   if (a.D.bf16)

@@ -302,6 +302,12 @@ __global__ void __launch_bounds__(256) global_carry_reduce(GlobalArgs a, int n, 
   }
 }
 
+hipError_t launch_global_carry_reduce(const GlobalArgs& a, int n, int nsplit, hipStream_t st) {
+  hipLaunchKernelGGL(global_carry_reduce, dim3(GRED_BLOCKS, a.D.B * a.D.H), dim3(256), 0, st, a, n,
+                     nsplit);
+  return hipGetLastError();
+}
+
 int global_fwd_splits(const Dims& D) {
   const int tiles = (D.C + 63) / 64;
   return std::max(1, std::min(16, tiles / 4));
@@ -342,6 +348,8 @@ static hipError_t launch_gfwd_t(const GlobalArgs& a, int n, hipStream_t st) {
 }
 
 hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {
+  hipError_t err = hipSuccess;
+  if (launch_global_fwd_blk(a, n, st, &err)) return err;
   if (a.D.bf16)
     return a.D.act == ACT_GELU ? launch_gfwd_t<__bf16, __bf16, ACT_GELU>(a, n, st)
                                : launch_gfwd_t<__bf16, __bf16, ACT_SILU>(a, n, st);

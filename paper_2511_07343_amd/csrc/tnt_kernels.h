@@ -86,6 +86,9 @@ struct GlobalArgs {
   void* scratch;                                         // phase-A scratch of the backward
   size_t scratch_f32_off;
   float* part;                                           // [B*H][nsplit][4*hid*d] split partials
+  void* packT;                                           // CT [B*H][4*hid*d] transposed state
+  void* packA;                                           // CT [B*H][4*hid*d] transposed adjoint
+  void* opT;                                             // CT per-chain transposed chunk operands
   Dims D;
   int force_generic;                                     // 1: skip fixed-size kernels
 };
@@ -116,6 +119,11 @@ hipError_t launch_reduce_global_init(const float* part, int B, int H, size_t hd,
                                      float* dW2, hipStream_t st);
 size_t global_bwd_scratch_bytes(const Dims& D, size_t* f32_off);
 int global_fwd_splits(const Dims& D);
+int global_blk_splits(const Dims& D);
+hipError_t launch_global_carry_reduce(const GlobalArgs& a, int n, int nsplit, hipStream_t st);
+hipError_t launch_gbwd_state_reduce(const GlobalArgs& a, int n, int nsplit, hipStream_t st);
+bool launch_global_fwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err);
+bool launch_global_bwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err);
 int global_bwd_splits(const Dims& D);
 constexpr int GRED_BLOCKS = 16;  // blocks per chain of the split reductions
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
