@@ -60,11 +60,13 @@ __device__ __forceinline__ void store8<float>(float* p, const float (&x)[8]) {
 
 }  // namespace
 
-template <int CP, int D, int H>
+// dynamic LDS: cbar (CP x CP fp32), per-tile partial row sums pA, pE
+// ((D/16) x CP fp32 each) and three CP x H compute-type slots for the C x h
+// operands of the contractions over h (slot lifetimes in the kernel)
+template <typename CT, int CP, int D, int H>
 constexpr size_t bwd_blk_lds_bytes() {
-  // fXK, fHH, fCb, fU (CP x CP fp32) + per-tile partial sums pA, pE
-  constexpr int hp = (H / 16 > D / 16 ? H / 16 : D / 16);
-  return (4 * (size_t)CP * CP + 2 * (size_t)hp * CP) * sizeof(float);
+  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) +
+         3 * (size_t)CP * H * sizeof(CT);
 }
 
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
@@ -72,16 +74,18 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
   __shared__ Coef cf;
   __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC], gEta[MAXC], gLa[MAXC], gLb[MAXC];
   __shared__ float dpart[3][16];
-  __shared__ float kss[16][MAXC];  // partial squared key norms per 8-column block
+  __shared__ float kss[D / 8][MAXC];  // partial squared key norms per 8-column block
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int d = D, h = H, Cp = CP;
-  constexpr int HP = (H / 16 > D / 16 ? H / 16 : D / 16);
-  float* fXK = reinterpret_cast<float*>(smem);
-  float* fHH = fXK + Cp * Cp;
-  float* fCb = fHH + Cp * Cp;
-  float* fU = fCb + Cp * Cp;
-  float* pA = fU + Cp * Cp;
-  float* pE = pA + HP * Cp;
+  float* fCb = reinterpret_cast<float*>(smem);
+  float* pA = fCb + Cp * Cp;
+  float* pE = pA + (D / 16) * Cp;
+  // C x h slots: S1 = Hk (Zk .. T5/T6), then Zkbar (Hkbar .. Kbar);
+  // S2 = H (Z .. H W2^T), then Zbar (Hbar .. Xbar); S3 = D1 (G .. T3/T4), then U
+  CT* slot1 = reinterpret_cast<CT*>(pE + (D / 16) * Cp);
+  CT* slot2 = slot1 + Cp * h;
+  CT* slot3 = slot2 + Cp * h;
+  float* fU = reinterpret_cast<float*>(slot3);
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -137,18 +141,19 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
   CT *Q = B_(bQ), *QT = B_(bQT), *K = B_(bK), *KT = B_(bKT), *N = B_(bN), *NT = B_(bNT);
   CT *X = B_(bX), *XT = B_(bXT), *XAT = B_(bXAT), *XET = B_(bXET), *Str = B_(bStr),
      *StrT = B_(bStrT);
-  CT *Hk = B_(bHk), *HkT = B_(bHkT), *Sp = B_(bSp), *Spp = B_(bSpp), *R = B_(bR), *RT = B_(bRT);
-  CT *G = B_(bG), *D1 = B_(bD1), *D1T = B_(bD1T), *H_ = B_(bH), *HT = B_(bHT), *Sz = B_(bSz);
+  CT *Hk = slot1, *HkT = B_(bHkT), *Sp = B_(bSp), *Spp = B_(bSpp), *R = B_(bR), *RT = B_(bRT);
+  CT *G = B_(bG), *D1 = slot3, *D1T = B_(bD1T), *H_ = slot2, *HT = B_(bHT), *Sz = B_(bSz);
   CT *Pz = B_(bPz), *PzT = B_(bPzT), *Po = B_(bPo), *PoT = B_(bPoT);
   CT *dO = B_(bdO), *dOT = B_(bdOT), *dOAT = B_(bdOAT), *dOET = B_(bdOET), *Q1 = B_(bQ1),
      *Q1T = B_(bQ1T);
-  CT *Zb = B_(bZb), *ZbT = B_(bZbT), *Q2 = B_(bQ2), *Q2T = B_(bQ2T), *Gb = B_(bGb),
+  CT *Zb = slot2, *ZbT = B_(bZbT), *Q2 = B_(bQ2), *Q2T = B_(bQ2T), *Gb = B_(bGb),
      *GbT = B_(bGbT);
-  CT *Ykb = B_(bYkb), *YkbT = B_(bYkbT), *Zkb = B_(bZkb), *ZkbT = B_(bZkbT), *Xb = B_(bXb),
+  CT *Ykb = B_(bYkb), *YkbT = B_(bYkbT), *Zkb = slot1, *ZkbT = B_(bZkbT), *Xb = B_(bXb),
      *XbT = B_(bXbT), *dXN = B_(bdXN), *dXNT = B_(bdXNT);
   CT *Wb1T = B_(bWb1T), *Sb1T = B_(bSb1T), *Wb2T = B_(bWb2T), *Sb2T = B_(bSb2T);
   CT *XA = B_(bXA), *XE = B_(bXE), *dOA = B_(bdOA), *dOE = B_(bdOE), *KcC = B_(bKcC),
      *Kb = B_(bKb), *RcC = B_(bRcC), *Rb = B_(bRb);
+  float *fXK = F_(E_XK), *fHH = F_(E_HH);
   float *fKb = F_(E_Kbar), *fT3 = F_(E_T3), *fT4 = F_(E_T4), *fT5 = F_(E_T5), *fT6 = F_(E_T6),
         *fZkp = F_(E_Zkp), *fMs = F_(E_Msym);
 #undef B_
@@ -875,7 +880,8 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
 static bool try_blk(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err) {
   if (a.D.d != D || a.D.hid != H || a.D.Cp != CP || a.D.act != ACT) return false;
-  constexpr size_t lds = bwd_blk_lds_bytes<CP, D, H>();
+  constexpr size_t lds = bwd_blk_lds_bytes<CT, CP, D, H>();
+  if (lds + 40 * 1024 > 160 * 1024) return false;  // static LDS is just under 40 KB
   auto kern = local_bwd_blk_kernel<IO, CT, ACT, D, H, CP>;
   set_lds_limit((const void*)kern);
   hipLaunchKernelGGL(kern, dim3(units), dim3(512), lds, st, a);
