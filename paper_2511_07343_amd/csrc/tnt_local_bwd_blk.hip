@@ -58,6 +58,19 @@ __device__ __forceinline__ void store8<float>(float* p, const float (&x)[8]) {
   *reinterpret_cast<f32x4*>(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
 }
 
+template <typename CT>
+__device__ __forceinline__ f4 load4(const CT* p);
+template <>
+__device__ __forceinline__ f4 load4<float>(const float* p) {
+  return *reinterpret_cast<const f32x4*>(p);
+}
+template <>
+__device__ __forceinline__ f4 load4<__bf16>(const __bf16* p) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+  return f4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+
 }  // namespace
 
 // dynamic LDS: cbar (CP x CP fp32), per-tile partial row sums pA, pE
@@ -282,6 +295,14 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
     using BCD = Blk<CP, D>;
     using BCH = Blk<CP, H>;
     using BCC = Blk<CP, CP>;
+    // Elementwise C x h intermediates (s'(Zk), s''(Zk), G, s'(Z), the
+    // second-order Zkbar part) are written and read by the same wave at the
+    // same block position, so they are stored fragment-major: each lane's
+    // four values of a tile are contiguous (one vector access per tile).
+    auto fofs = [&](int i0, int j0, int rb, int cb) -> size_t {
+      const int blk = (i0 / (BCH::RB * 16)) * BCH::NBN + j0 / (BCH::CB * 16);
+      return ((size_t)((blk * BCH::RB + rb) * BCH::CB + cb) * WAVE + l) * 4;
+    };
     if (Dm.qk_proj) {
       for_blocks<CP, CP>([&](int i0, int j0) {
         f4 acc[BCC::RB][BCC::CB];
@@ -321,16 +342,18 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(acc, K, d, i0, W1, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 hv;
+        f4 hv, sp, spp;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const ActVals av = act_all<ACT>(acc[rb][cb][r]);
-          const size_t e = (size_t)(i + r) * h + j;
-          Hk[e] = from_f<CT>(av.s);
-          Sp[e] = from_f<CT>(av.d1);
-          Spp[e] = from_f<CT>(av.d2);
+          Hk[(size_t)(i + r) * h + j] = from_f<CT>(av.s);
           hv[r] = av.s;
+          sp[r] = av.d1;
+          spp[r] = av.d2;
         }
+        const size_t fo = fofs(i0, j0, rb, cb);
+        store4<CT>(Sp + fo, sp);
+        store4<CT>(Spp + fo, spp);
         store4<CT>(HkT + (size_t)j * Cp + i, hv);
       });
     });
@@ -360,15 +383,15 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(acc, R, d, i0, W2T, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofs(i0, j0, rb, cb);
+        const f4 sp = load4<CT>(Sp + fo);
         f4 dv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const size_t e = (size_t)(i + r) * h + j;
-          const float g = acc[rb][cb][r];
-          dv[r] = g * to_f(Sp[e]);
-          G[e] = from_f<CT>(g);
-          D1[e] = from_f<CT>(dv[r]);
+          dv[r] = acc[rb][cb][r] * sp[r];
+          D1[(size_t)(i + r) * h + j] = from_f<CT>(dv[r]);
         }
+        store4<CT>(G + fo, acc[rb][cb]);
         store4<CT>(D1T + (size_t)j * Cp + i, dv);
       });
     });
@@ -399,15 +422,15 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, XE, d, i0, S1, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Pz, Cp, i0, D1T, Cp, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 hv;
+        f4 hv, sz;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int ii = i + r;
           const ActVals av = act_all<ACT>(a1[rb][cb][r] - a3[rb][cb][r]);
-          H_[(size_t)ii * h + j] = from_f<CT>(av.s);
-          Sz[(size_t)ii * h + j] = from_f<CT>(av.d1);
+          H_[(size_t)(i + r) * h + j] = from_f<CT>(av.s);
           hv[r] = av.s;
+          sz[r] = av.d1;
         }
+        store4<CT>(Sz + fofs(i0, j0, rb, cb), sz);
         store4<CT>(HT + (size_t)j * Cp + i, hv);
       });
     });
@@ -482,12 +505,12 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dOE, d, i0, S2T, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Q1, Cp, i0, HkT, Cp, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const f4 sz = load4<CT>(Sz + fofs(i0, j0, rb, cb));
         f4 zv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const size_t e = (size_t)(i + r) * h + j;
-          zv[r] = (a1[rb][cb][r] - a3[rb][cb][r]) * to_f(Sz[e]);
-          Zb[e] = from_f<CT>(zv[r]);
+          zv[r] = (a1[rb][cb][r] - a3[rb][cb][r]) * sz[r];
+          Zb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
         }
         store4<CT>(ZbT + (size_t)j * Cp + i, zv);
       });
@@ -530,15 +553,17 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, KcC, d, i0, Wb1, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, Kb, d, i0, Sb1, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 gv;
+        const size_t fo = fofs(i0, j0, rb, cb);
+        const f4 sp = load4<CT>(Sp + fo), g = load4<CT>(G + fo), spp = load4<CT>(Spp + fo);
+        f4 gv, zp;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const size_t e = (size_t)(i + r) * h + j;
           const float d1b = -a1[rb][cb][r];
-          gv[r] = d1b * to_f(Sp[e]);
-          Gb[e] = from_f<CT>(gv[r]);
-          fZkp[e] = d1b * to_f(G[e]) * to_f(Spp[e]);
+          gv[r] = d1b * sp[r];
+          zp[r] = d1b * g[r] * spp[r];
+          Gb[(size_t)(i + r) * h + j] = from_f<CT>(gv[r]);
         }
+        store4<float>(fZkp + fo, zp);
         store4<CT>(GbT + (size_t)j * Cp + i, gv);
       });
     });
@@ -651,13 +676,13 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, Rb, d, i0, Sb2T, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a4, Ykb, d, i0, W2T, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofs(i0, j0, rb, cb);
+        const f4 sp = load4<CT>(Sp + fo), zp = load4<float>(fZkp + fo);
         f4 zv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const size_t e = (size_t)(i + r) * h + j;
-          const float hkb = a4[rb][cb][r] - a1[rb][cb][r];
-          zv[r] = hkb * to_f(Sp[e]) + fZkp[e];
-          Zkb[e] = from_f<CT>(zv[r]);
+          zv[r] = (a4[rb][cb][r] - a1[rb][cb][r]) * sp[r] + zp[r];
+          Zkb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
         }
         store4<CT>(ZkbT + (size_t)j * Cp + i, zv);
       });
@@ -816,7 +841,15 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
     using BDH = Blk<D, H>;
     using BDD = Blk<D, D>;
     for_blocks<H, D>([&](int i0, int j0) {  // W1bar, S1bar : h x d
-      f4 a1[BHD::RB][BHD::CB], a3[BHD::RB][BHD::CB];
+      f4 a1[BHD::RB][BHD::CB], a3[BHD::RB][BHD::CB], ow[BHD::RB][BHD::CB], os[BHD::RB][BHD::CB];
+      // the carried adjoint at this block, requested before the MFMAs
+      blk_each4<BHD::RB, BHD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          ow[rb][cb][r] = Wb1[(size_t)(i + r) * d + j];
+          os[rb][cb][r] = Sb1[(size_t)(i + r) * d + j];
+        }
+      });
       zero_blk(a1);
       zero_blk(a3);
       mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a1, ZbT, Cp, i0, XAT, Cp, j0);
@@ -827,7 +860,7 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i + r) * d + j;
-          const float w = Wb1[e], sv = Sb1[e];
+          const float w = ow[rb][cb][r], sv = os[rb][cb][r];
           nw[r] = cf.AC * w + a1[rb][cb][r];
           ns[r] = cf.EC * w + cf.BC * sv + a3[rb][cb][r];
           Wb1[e] = nw[r];
@@ -838,7 +871,14 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       });
     });
     for_blocks<D, H>([&](int i0, int j0) {  // W2bar, S2bar : d x h
-      f4 a1[BDH::RB][BDH::CB], a4[BDH::RB][BDH::CB];
+      f4 a1[BDH::RB][BDH::CB], a4[BDH::RB][BDH::CB], ow[BDH::RB][BDH::CB], os[BDH::RB][BDH::CB];
+      blk_each4<BDH::RB, BDH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          ow[rb][cb][r] = Wb2[(size_t)(i + r) * h + j];
+          os[rb][cb][r] = Sb2[(size_t)(i + r) * h + j];
+        }
+      });
       zero_blk(a1);
       zero_blk(a4);
       mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, dOAT, Cp, i0, HT, Cp, j0);
@@ -850,7 +890,7 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i + r) * h + j;
-          const float w = Wb2[e], sv = Sb2[e];
+          const float w = ow[rb][cb][r], sv = os[rb][cb][r];
           nw[r] = cf.AC * w + a1[rb][cb][r];
           ns[r] = cf.EC * w + cf.BC * sv + a4[rb][cb][r];
           Wb2[e] = nw[r];
