@@ -179,17 +179,24 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
     const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd, *McT = pk + 4 * hd;
 
-    // ================= adjoint . state dot products (d A_C, d E_C, d B_C)
+    // ================= adjoint . state dot products (d A_C, d E_C, d B_C), from
+    // the transposed bf16 copies of the carried adjoint and of the entry state
     {
       float pa = 0.f, pe = 0.f, pb = 0.f;
-#pragma unroll 4
-      for (size_t e = threadIdx.x * 4; e < hd; e += blockDim.x * 4) {
-        const f32x4 w1 = *(const f32x4*)(W1 + e), w2 = *(const f32x4*)(W2 + e);
-        const f32x4 s1 = *(const f32x4*)(S1 + e), s2 = *(const f32x4*)(S2 + e);
-        const f32x4 b1 = *(const f32x4*)(Wb1 + e), b2 = *(const f32x4*)(Wb2 + e);
-        const f32x4 c1 = *(const f32x4*)(Sb1 + e), c2 = *(const f32x4*)(Sb2 + e);
+      const CT* adjT = Wb1T;  // Wb1^T, Sb1^T, Wb2^T, Sb2^T contiguous
+#pragma unroll 2
+      for (size_t e = threadIdx.x * 8; e < hd; e += blockDim.x * 8) {
+        float w1[8], s1[8], w2[8], s2[8], b1[8], c1[8], b2[8], c2[8];
+        load8(W1T + e, w1);
+        load8(S1T + e, s1);
+        load8(W2T + e, w2);
+        load8(S2T + e, s2);
+        load8(adjT + e, b1);
+        load8(adjT + hd + e, c1);
+        load8(adjT + 2 * hd + e, b2);
+        load8(adjT + 3 * hd + e, c2);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < 8; ++t) {
           pa += b1[t] * w1[t] + b2[t] * w2[t];
           pe += b1[t] * s1[t] + b2[t] * s2[t];
           pb += c1[t] * s1[t] + c2[t] * s2[t];
