@@ -85,7 +85,7 @@ constexpr size_t bwd_blk_lds_bytes() {
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
 __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
   __shared__ Coef cf;
-  __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC], gEta[MAXC], gLa[MAXC], gLb[MAXC];
+  __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC];
   __shared__ float dpart[3][16];
   __shared__ float kss[D / 8][MAXC];  // partial squared key norms per 8-column block
   extern __shared__ __align__(16) unsigned char smem[];
@@ -93,7 +93,7 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
   float* fCb = reinterpret_cast<float*>(smem);
   float* pA = fCb + Cp * Cp;
   float* pE = pA + (D / 16) * Cp;
-  // C x h slots: S1 = Hk (Zk .. T5/T6), then Zkbar (Hkbar .. Kbar);
+  // C x h slots: S1 = Hk (Zk .. T5/T6), then Gbar (D1bar .. Rbar), then Zkbar (Hkbar .. Kbar);
   // S2 = H (Z .. H W2^T), then Zbar (Hbar .. Xbar); S3 = D1 (G .. T3/T4), then U
   CT* slot1 = reinterpret_cast<CT*>(pE + (D / 16) * Cp);
   CT* slot2 = slot1 + Cp * h;
@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
   CT *Pz = B_(bPz), *PzT = B_(bPzT), *Po = B_(bPo), *PoT = B_(bPoT);
   CT *dO = B_(bdO), *dOT = B_(bdOT), *dOAT = B_(bdOAT), *dOET = B_(bdOET), *Q1 = B_(bQ1),
      *Q1T = B_(bQ1T);
-  CT *Zb = slot2, *ZbT = B_(bZbT), *Q2 = B_(bQ2), *Q2T = B_(bQ2T), *Gb = B_(bGb),
+  CT *Zb = slot2, *ZbT = B_(bZbT), *Q2 = B_(bQ2), *Q2T = B_(bQ2T), *Gb = slot1,
      *GbT = B_(bGbT);
   CT *Ykb = B_(bYkb), *YkbT = B_(bYkbT), *Zkb = slot1, *ZkbT = B_(bZkbT), *Xb = B_(bXb),
      *XbT = B_(bXbT), *dXN = B_(bdXN), *dXNT = B_(bdXNT);
@@ -503,6 +503,23 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       });
     });
     __syncthreads();
+    // T5 = Hk W2bar'^T, T6 = Hk S2bar'^T  (C x d; the last reads of Hk, so slot S1 is free
+    // for Gbar in the next phase)
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a5[BCD::RB][BCD::CB], a6[BCD::RB][BCD::CB];
+      zero_blk(a5);
+      zero_blk(a6);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a5, Hk, h, i0, Wb2, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a6, Hk, h, i0, Sb2, h, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (size_t)(i + r) * d + j;
+          fT5[e] = a5[rb][cb][r];
+          fT6[e] = a6[rb][cb][r];
+        }
+      });
+    });
     // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)
     for_blocks<CP, H>([&](int i0, int j0) {
       f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
@@ -574,25 +591,19 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
         store4<CT>(GbT + (size_t)j * Cp + i, gv);
       });
     });
-    // T3 = D1 W1bar', T4 = D1 S1bar', T5 = Hk W2bar'^T, T6 = Hk S2bar'^T  (C x d)
+    // T3 = D1 W1bar', T4 = D1 S1bar'  (C x d)
     for_blocks<CP, D>([&](int i0, int j0) {
-      f4 a3[BCD::RB][BCD::CB], a4[BCD::RB][BCD::CB], a5[BCD::RB][BCD::CB], a6[BCD::RB][BCD::CB];
+      f4 a3[BCD::RB][BCD::CB], a4[BCD::RB][BCD::CB];
       zero_blk(a3);
       zero_blk(a4);
-      zero_blk(a5);
-      zero_blk(a6);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a3, D1, h, i0, Wb1T, h, j0);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a4, D1, h, i0, Sb1T, h, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a5, Hk, h, i0, Wb2, h, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a6, Hk, h, i0, Sb2, h, j0);
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i + r) * d + j;
           fT3[e] = a3[rb][cb][r];
           fT4[e] = a4[rb][cb][r];
-          fT5[e] = a5[rb][cb][r];
-          fT6[e] = a6[rb][cb][r];
         }
       });
     });
@@ -770,7 +781,8 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
     __syncthreads();
     for (int e = threadIdx.x; e < C * d; e += blockDim.x) dkp[(size_t)tok0 * d + e] = fKb[e];
 
-    // ================= gate adjoints (wave 0; lanes are chunk positions)
+    // ================= gate adjoints (lanes are chunk positions; the sums over
+    // positions are split in 8-row blocks over the waves, partials in slots S1-S2)
     if (wave_id() == 0) {
       const int i = l;
       float dAC = 0.f, dEC = 0.f;
@@ -786,48 +798,88 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       }
     }
     __syncthreads();
-    if (wave_id() == 0) {
-      const int i = l;
-      float eb = 0.f, rows = 0.f, cols = 0.f, Ui = 0.f;
+    // [5][8][Cp] partial sums; slots S1 and S2 (contiguous) are free here
+    static_assert(5 * 8 * CP * sizeof(float) <= 2 * (size_t)CP * H * sizeof(CT), "gate partials");
+    float* gpart = reinterpret_cast<float*>(slot1);
+    {
+      const int w = wave_id(), i = l;
+      const int r0 = w * (Cp / 8), r1 = r0 + Cp / 8;
+      // column sums of cbar o ct, cbar o c over rows r in this block (r >= i),
+      // row sums of cbar o c over columns t in this block (t <= i)
+      float eb = 0.f, cols = 0.f, rows = 0.f;
       if (i < Cp) {
-        // eta_bar, column sums, row sums of cbar o c
-        for (int r = i; r < Cp; ++r) {
-          const float cb = fCb[r * Cp + i];
-          eb += cb * cf.ct[r][i];
-          cols += cb * cf.c[r][i];
-        }
-        eb += gB[i] * cf.ebt[i];
-        for (int t = 0; t <= i; ++t) rows += fCb[i * Cp + t] * cf.c[i][t];
-        // U_{i, j}, j = 0..i
-        float lbp = 0.f;
-        for (int j = 0; j <= i; ++j) {
-          Ui = expf(cf.lb[j] - lbp) * Ui + fCb[i * Cp + j] * cf.eta[j];
-          lbp = cf.lb[j];
-          fU[i * Cp + j] = Ui;
+#pragma unroll 4
+        for (int r = r0; r < r1; ++r) {
+          if (r >= i) {
+            const float cb = fCb[r * Cp + i];
+            eb += cb * cf.ct[r][i];
+            cols += cb * cf.c[r][i];
+          }
+          if (r <= i) rows += fCb[i * Cp + r] * cf.c[i][r];
         }
       }
-      gEta[i] = eb;
-      gLa[i] = rows;
-      gLb[i] = -cols;
+      if (i < Cp) {
+        gpart[(0 * 8 + w) * Cp + i] = eb;
+        gpart[(1 * 8 + w) * Cp + i] = cols;
+        gpart[(2 * 8 + w) * Cp + i] = rows;
+      }
+      // U_{i, j} = beta'_j U_{i, j-1} + cbar_{i j} eta_j (j <= i), beta'_j = e^{lb_j - lb_{j-1}},
+      // for this wave's rows i, as an affine scan over the lanes j
+      const int j = l;
+      const float aj = (j < Cp) ? expf(cf.lb[j] - (j > 0 ? cf.lb[j - 1] : 0.f)) : 0.f;
+      for (int ri = r0; ri < r1; ++ri) {
+        float sa = aj, sx = (j <= ri && j < Cp) ? fCb[ri * Cp + j] * cf.eta[j] : 0.f;
+#pragma unroll
+        for (int o = 1; o < WAVE; o <<= 1) {
+          const float pa_ = __shfl_up(sa, o, WAVE), px = __shfl_up(sx, o, WAVE);
+          if (j >= o) {
+            sx = sa * px + sx;
+            sa = sa * pa_;
+          }
+        }
+        if (j < Cp) fU[ri * Cp + j] = (j <= ri) ? sx : 0.f;
+      }
+    }
+    __syncthreads();
+    {
+      // T_j = sum_{i >= j} e^{la_i - la_j} U_{i j},  Y_j = sum_{i >= j} e^{la_i - la_j} Ebar_i
+      const int w = wave_id(), j = l;
+      const int r0 = w * (Cp / 8), r1 = r0 + Cp / 8;
+      float T = 0.f, Yv = 0.f;
+      if (j < C) {
+#pragma unroll 4
+        for (int i = r0; i < r1; ++i)
+          if (i >= j) {
+            const float e = expf(cf.la[i] - cf.la[j]);
+            T += e * fU[i * Cp + j];
+            Yv += e * gE[i];
+          }
+      }
+      if (j < Cp) {
+        gpart[(3 * 8 + w) * Cp + j] = T;
+        gpart[(4 * 8 + w) * Cp + j] = Yv;
+      }
     }
     __syncthreads();
     if (wave_id() == 0) {
       const int j = l;
+      float sum[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+      if (j < Cp)
+#pragma unroll
+        for (int k = 0; k < 5; ++k)
+#pragma unroll
+          for (int w = 0; w < 8; ++w) sum[k] += gpart[(k * 8 + w) * Cp + j];
+      const float eb = sum[0] + (j < Cp ? gB[j] * cf.ebt[j] : 0.f);
+      const float cols = sum[1], rows = sum[2], T = sum[3], Yv = sum[4];
       float la_b = 0.f, lb_b = 0.f;
       float dBC = 0.f;
 #pragma unroll
       for (int w = 0; w < 8; ++w) dBC += dpart[2][w];
       const float bsum = wave_sum(j < Cp ? gB[j] * cf.bb[j] : 0.f);
       if (j < C) {
-        float T = 0.f, Yv = 0.f;
-        for (int i = j; i < Cp; ++i) {
-          const float w = expf(cf.la[i] - cf.la[j]);
-          T += w * fU[i * Cp + j];
-          Yv += w * gE[i];
-        }
         const float yl = Yv * expf(cf.lb[j]);
-        la_b = gA[j] * cf.A[j] + gE[j] * cf.E[j] + gLa[j] - T - yl;
-        lb_b = T + gLb[j] + yl - gB[j] * cf.bb[j];
+        la_b = gA[j] * cf.A[j] + gE[j] * cf.E[j] + rows - T - yl;
+        lb_b = T - cols + yl - gB[j] * cf.bb[j];
         if (j == C - 1) lb_b += dBC * cf.BC + bsum;
       }
       // suffix sums over positions
@@ -837,7 +889,7 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
       if (j < C) {
         const size_t t = (size_t)tok0 + j;
         const float al = dec[t], be = mom[t];
-        dlr[t] = gEta[j];
+        dlr[t] = eb;
         ddec[t] = -sla / (1.0f - al);
         dmom[t] = (logf(be) > LOG_CLAMP) ? slb / be : 0.f;
       }
