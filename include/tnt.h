@@ -103,8 +103,9 @@ typedef enum {
 size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind);
 
 /* Bytes of the optional saved-state buffer: the chunk-entry states of every
- * memory, written by tnt_mem_fwd and read by tnt_mem_bwd so that the backward
- * does not recompute the forward's state chain.  Opaque layout. */
+ * memory (fp32, plus transposed copies of the local memories' states in the
+ * compute type), written by tnt_mem_fwd and read by tnt_mem_bwd so that the
+ * backward does not recompute the forward's state chain.  Opaque layout. */
 size_t tnt_mem_saved_size(const tnt_config* cfg);
 
 /* Forward pass: o = TNT layer output (see the file comment).

@@ -63,7 +63,7 @@ struct Layout {
   int M, BH;
   size_t hd, io_elems, gates;
   // saved (or workspace-resident) chunk states
-  size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], saved_bytes;
+  size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], sv_t[TNT_MAX_LOCAL], saved_bytes;
   int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
   // forward workspace
   size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL], w_ring,
@@ -73,7 +73,7 @@ struct Layout {
   // backward workspace
   size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32, b_gpackA, b_gop,
       b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
-      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_stT[TNT_MAX_LOCAL], b_states, bwd_bytes,
+      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_states, bwd_bytes,
       bwd_re_bytes;
   BwdLayout blay[TNT_MAX_LOCAL];
 };
@@ -103,6 +103,8 @@ Layout layout_of(const tnt_config* c) {
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * 4 * y.hd * f);
     y.sv_m[i] = off;
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * dd * f);
+    y.sv_t[i] = off;  // CT transposes of every slot, written by the forward
+    off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * (4 * y.hd + dd) * cts);
   }
   y.saved_bytes = off;
 
@@ -159,8 +161,6 @@ Layout layout_of(const tnt_config* c) {
     y.b_dWl[i] = off; off += up((size_t)y.l_units[i] * 2 * y.hd * f);
     y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].ct_elems * cts);
     y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].f32_elems * f);
-    y.b_stT[i] = off;
-    off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * (4 * y.hd + dd) * cts);
   }
   y.bwd_bytes = off;
   y.b_states = off;
@@ -297,6 +297,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.o_part = opart + (size_t)m * y.io_elems;
     a.states = sv ? (float*)(sv + y.sv_l[i]) : (float*)(ws + y.ring_l[i]);
     a.mstates = sv ? (float*)(sv + y.sv_m[i]) : (float*)(ws + y.ring_m[i]);
+    a.statesT = sv ? (void*)(sv + y.sv_t[i]) : nullptr;
     a.nslots = sv ? y.l_chunks[i] + 1 : 2;
     a.scratch = ws + y.w_scr[i];
     a.plan = y.lplan[i];
@@ -372,7 +373,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.states = (const float*)(sv + y.sv_l[i]);
     a.mstates = (const float*)(sv + y.sv_m[i]);
     a.nslots = y.l_chunks[i] + 1;
-    a.statesT = ws + y.b_stT[i];
+    a.statesT = sv + y.sv_t[i];
     a.adj = (float*)(ws + y.b_adj_l[i]);
     a.madj = (float*)(ws + y.b_madj[i]);
     a.dq_part = dqp + (size_t)m * y.io_elems;
@@ -384,10 +385,6 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
     a.force_generic = generic_only();
-    HIP_TIMED("pack_states", launch_pack_states(a.states, a.mstates, ws + y.b_stT[i], y.l_units[i],
-                                                a.nslots, c->d, c->hid,
-                                                c->qk_proj && c->qk_scope == TNT_QK_SHARD,
-                                                c->dtype == TNT_BF16, st));
     HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
     HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,

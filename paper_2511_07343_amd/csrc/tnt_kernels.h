@@ -38,6 +38,8 @@ struct LocalFwdArgs {
   float* o_part;                                         // [B][H][L][d]
   float* states;                                         // [units][nslots][4*hid*d]
   float* mstates;                                        // [units][nslots][d*d]
+  void* statesT;                                         // null, or CT [units][nslots][4*hid*d + d*d]:
+                                                         // W1^T, W2^T, S1^T, S2^T, M^T of every slot
   int nslots;
   void* scratch;                                         // units * plan.elems CT
   LocalPlan plan;

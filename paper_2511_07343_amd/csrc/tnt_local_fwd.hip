@@ -252,8 +252,12 @@ static hipError_t launch_local_fwd_t(const LocalFwdArgs& a, int units, hipStream
 hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st) {
   hipError_t e = hipSuccess;
   if (!a.force_generic && launch_local_fwd_fast(a, units, st, &e)) return e;
-  if (a.D.bf16) return launch_local_fwd_t<__bf16, __bf16>(a, units, st);
-  return launch_local_fwd_t<float, float>(a, units, st);
+  e = a.D.bf16 ? launch_local_fwd_t<__bf16, __bf16>(a, units, st)
+               : launch_local_fwd_t<float, float>(a, units, st);
+  if (e != hipSuccess || !a.statesT) return e;
+  // the runtime-sized kernel writes fp32 states only: transpose them in one pass
+  return launch_pack_states(a.states, a.mstates, a.statesT, units, a.nslots, a.D.d, a.D.hid,
+                            a.D.qk_proj && a.D.qk_scope == 0, a.D.bf16, st);
 }
 
 }  // namespace tnt

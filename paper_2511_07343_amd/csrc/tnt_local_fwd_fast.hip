@@ -13,7 +13,11 @@
 //
 // The fp32 state (W1, W2, S1, S2 and the Q-K sum) lives in global memory,
 // one slot per chunk boundary; contraction-contiguous operands are read from
-// it directly, the carry reads the entry slot and writes the next one.
+// it directly, the carry reads the entry slot and writes the next one.  When
+// the states are saved for the backward pass, the carry also writes the CT
+// transposes of the new state (W1^T, W2^T, S1^T, S2^T, M^T) from the same
+// registers: four consecutive rows of an MFMA output tile are four contiguous
+// elements of the transpose.
 #include "tnt_local_common.h"
 
 namespace tnt {
@@ -133,6 +137,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const float* dec = a.decay + chain * Dm.L;
   float* st = a.states + (size_t)u * a.nslots * 4 * hd;
   float* mst = a.mstates + (size_t)u * a.nslots * D * D;
+  constexpr size_t PS = 4 * hd + (size_t)D * D;  // CT elements per transposed slot
+  CT* const pku = a.statesT ? (CT*)a.statesT + (size_t)u * a.nslots * PS : nullptr;
   const bool qk = Dm.qk_proj;
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
   const float rscale = 2.0f / (float)D;
@@ -152,6 +158,17 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     }
     if (shard_qk)
       for (int e = threadIdx.x; e < D * D; e += blockDim.x) mst[e] = 0.f;
+    if (pku) {  // slot 0 transposes; destination-ordered writes
+      for (int e = threadIdx.x; e < (int)hd; e += blockDim.x) {
+        const int c1 = e / HID, r1 = e - c1 * HID;  // W1^T [D][HID]
+        const int c2 = e / D, r2 = e - c2 * D;      // W2^T [HID][D]
+        pku[e] = from_f<CT>(W1i[(size_t)r1 * D + c1]);
+        pku[hd + e] = from_f<CT>(W2i[(size_t)r2 * HID + c2]);
+        pku[2 * hd + e] = pku[3 * hd + e] = from_f<CT>(0.f);
+      }
+      if (shard_qk)
+        for (int e = threadIdx.x; e < D * D; e += blockDim.x) pku[4 * hd + e] = from_f<CT>(0.f);
+    }
   }
   __syncthreads();
 
@@ -164,6 +181,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     float *W1n = nxt, *W2n = nxt + hd, *S1n = nxt + 2 * hd, *S2n = nxt + 3 * hd;
     const float* Mc = mst + (size_t)(n % a.nslots) * D * D;
     float* Mn = mst + (size_t)((n + 1) % a.nslots) * D * D;
+    CT* const pkn = pku ? pku + (size_t)((n + 1) % a.nslots) * PS : nullptr;
 
     // ---- stage Q, K (16-byte loads; rows >= C zero), gate coefficients
     {
@@ -240,8 +258,11 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           f4 acc = zero4();
           mma_tile<CT, KC, KC>(acc, sNT, CP, i0, sNT, CP, j0, CP);
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            Mn[(size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15)] = mo[r] + acc[r];
+          for (int r = 0; r < 4; ++r) {
+            acc[r] += mo[r];
+            Mn[(size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15)] = acc[r];
+          }
+          if (pkn) store4<CT>(pkn + 4 * hd + (size_t)(j0 + (l & 15)) * D + i0 + 4 * (l >> 4), acc);
         }
       }
     } else {
@@ -394,8 +415,15 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15);
-          W1n[e] = cf.AC * pw[xx][r] + cf.EC * ps[xx][r] - aw[r];
-          S1n[e] = cf.BC * ps[xx][r] - as[r];
+          aw[r] = cf.AC * pw[xx][r] + cf.EC * ps[xx][r] - aw[r];
+          as[r] = cf.BC * ps[xx][r] - as[r];
+          W1n[e] = aw[r];
+          S1n[e] = as[r];
+        }
+        if (pkn) {
+          const size_t et = (size_t)(j0 + (l & 15)) * HID + i0 + 4 * (l >> 4);
+          store4<CT>(pkn + et, aw);
+          store4<CT>(pkn + 2 * hd + et, as);
         }
       }
       }
@@ -430,8 +458,15 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * HID + j0 + (l & 15);
-          W2n[e] = cf.AC * pw[xx][r] + cf.EC * ps[xx][r] - aw[r];
-          S2n[e] = cf.BC * ps[xx][r] - as[r];
+          aw[r] = cf.AC * pw[xx][r] + cf.EC * ps[xx][r] - aw[r];
+          as[r] = cf.BC * ps[xx][r] - as[r];
+          W2n[e] = aw[r];
+          S2n[e] = as[r];
+        }
+        if (pkn) {
+          const size_t et = (size_t)(j0 + (l & 15)) * D + i0 + 4 * (l >> 4);
+          store4<CT>(pkn + hd + et, aw);
+          store4<CT>(pkn + 3 * hd + et, as);
         }
       }
       }
