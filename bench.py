@@ -88,9 +88,8 @@ _COMMON = ["tnt_device.h", "tnt_kernels.h"]
 LAUNCH_SOURCES = {
     "local_bwd": ["tnt_local_bwd_blk.hip", "tnt_local_bwd_layout.h", "tnt_local_common.h"] + _COMMON,
     "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_common.h"] + _COMMON,
-    "global_bwd_chunk": ["tnt_global_bwd.hip"] + _COMMON,
-    "global_fwd_chunk": ["tnt_global_fwd.hip"] + _COMMON,
-    "pack_states": ["tnt_local_bwd.hip"] + _COMMON,
+    "global_bwd_chunk": ["tnt_global_bwd.hip", "tnt_global_blk.hip"] + _COMMON,
+    "global_fwd_chunk": ["tnt_global_fwd.hip", "tnt_global_blk.hip"] + _COMMON,
 }
 
 
