@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -73,7 +74,7 @@ struct Layout {
   // backward workspace
   size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32, b_gpackA, b_gop,
       b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
-      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_states, bwd_bytes,
+      b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_split[TNT_MAX_LOCAL], b_states, bwd_bytes,
       bwd_re_bytes;
   BwdLayout blay[TNT_MAX_LOCAL];
 };
@@ -161,6 +162,9 @@ Layout layout_of(const tnt_config* c) {
     y.b_dWl[i] = off; off += up((size_t)y.l_units[i] * 2 * y.hd * f);
     y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].ct_elems * cts);
     y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].f32_elems * f);
+    const size_t sb = local_bwd_split_bytes(D, y.l_units[i]);
+    y.b_split[i] = sb ? off : SIZE_MAX;
+    off += up(sb);
   }
   y.bwd_bytes = off;
   y.b_states = off;
@@ -174,6 +178,13 @@ bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
 // runtime-sized kernels (used by the tests to cover both kernel families).
 int generic_only() {
   const char* e = std::getenv("TNT_GENERIC_KERNELS");
+  return (e && e[0] == '1') ? 1 : 0;
+}
+
+// TNT_LOCAL_BWD_SINGLE=1 keeps the local backward in one reverse walk per unit
+// (the single-walk fixed-size kernel) instead of the three-pass kernels.
+int single_walk_only() {
+  const char* e = std::getenv("TNT_LOCAL_BWD_SINGLE");
   return (e && e[0] == '1') ? 1 : 0;
 }
 
@@ -383,6 +394,8 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.dWinit_part = (float*)(ws + y.b_dWl[i]);
     a.scratch = ws + y.b_scr[i];
     a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
+    a.split_ws = y.b_split[i] != SIZE_MAX ? (void*)(ws + y.b_split[i]) : nullptr;
+    a.single_walk = single_walk_only();
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
     a.force_generic = generic_only();
     HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));

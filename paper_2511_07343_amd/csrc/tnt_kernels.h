@@ -64,6 +64,9 @@ struct LocalBwdArgs {
   float* scratch_f32;                                    // units * plan.f32_elems
   LocalPlan plan;
   Dims D;
+  void* split_ws;                                        // null, or local_bwd_split_bytes(D, units)
+                                                         // bytes for the three-pass fixed-size kernels
+  int single_walk;                                       // 1: the one-walk fixed-size kernel
   int force_generic;                                     // 1: skip fixed-size kernels
 };
 
@@ -112,6 +115,8 @@ hipError_t launch_pack_states(const float* states, const float* mstates, void* o
                                int nslots, int d, int hid, int with_m, int bf16, hipStream_t st);
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st);
 bool launch_local_bwd_blk(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err);
+size_t local_bwd_split_bytes(const Dims& D, int units);  // 0: no three-pass kernels for D
+bool launch_local_bwd_split(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err);
 hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st);

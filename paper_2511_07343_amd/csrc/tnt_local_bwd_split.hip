@@ -1,0 +1,1294 @@
+// Local memories, backward, fixed sizes, in three passes.
+//
+// The backward of one chunk is affine in the carried adjoint of the chunk's
+// exit state (W1', S1', W2', S2' bar): the recomputed forward values, the
+// backward of the retrieval (driven by dO), the query / key / value adjoints it
+// feeds and the Q-K projection do not depend on it.  So the reverse walk over a
+// shard's chunks is split:
+//
+//   pass A  (all chunks of all units at once, a persistent grid)  recomputes
+//           the chunk's forward quantities, takes the backward of the
+//           retrieval, writes its dq and its share of dk, and leaves a chunk
+//           record: the operands the walk needs, the retrieval's gate
+//           cotangents (cbar, dA, dE) and X^T Q for the Q-K state adjoint;
+//   pass B  (one workgroup per unit, chunks in reverse) walks the carried
+//           adjoint back: T3..T6, D1bar / Gbar, Rbar (dv), Zkbar, the carried
+//           part of Kbar and the chunk-entry adjoint, four block barriers a chunk;
+//   scan    turns the per-chunk X^T Q into the suffix sums the Q-K projection
+//           carries back to each chunk (shard-scoped projection only);
+//   pass C  (all chunks at once) finishes the gate adjoints (dlr, dmom,
+//           ddecay) and adds the carried Q-K term to dk.
+//
+// Each step's formulas are those of the single-walk kernels (the runtime-sized
+// kernel writes them out); only the place where each term is taken differs.
+// Wave-block GEMMs (Blk / mma_blk) and fragment-major elementwise buffers as
+// in the single-walk fixed-size kernel; passes A and B use the same block
+// mapping for C x h tiles, so fragment-major records written by A are read by B.
+#include "tnt_local_common.h"
+#include "tnt_local_bwd_helpers.h"
+
+namespace tnt {
+
+using namespace bwdh;
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// buffer layouts (element offsets; CT = compute type)
+// ---------------------------------------------------------------------------
+// chunk record, one per (unit, chunk): written by pass A, read by B and C
+enum RecCT {
+  rHk, rHkT, rD1, rZbT, rHT, rSp, rSpp, rG,        // C x h  (Sp, Spp, G fragment-major)
+  rPzT, rQ1T, rPoT,                                // C x C
+  rK, rKT, rKcC, rKb, rR, rRT, rRcC, rRb, rdOT,    // C x d
+  rXAT, rXET, rdOAT, rdOET, rN, REC_CT
+};
+enum RecF {
+  rCb,                     // C x C  retrieval part of cbar
+  rgA, rgE, rkn, rcC, rbb, // C      retrieval dA, dE; key norms; cC, b
+  rsc,                     // 4      A_C, B_C, E_C
+  rXbQ,                    // d x d  Xbar^T Q (then the suffix sum over later chunks)
+  rgCC, rgB,               // C      carried cC-bar, b-bar (pass B)
+  rdot,                    // 4      dA_C, dE_C, dB_C (pass B)
+  REC_F
+};
+// pass-A temporaries, one set per resident workgroup
+enum ATmpCT {
+  aQ, aQT, aNT, aX, aXT, aXA, aXE, adO, adOA, adOE, aXb, aXbT,  // C x d
+  aStr, aStrT, aPz, aPo, aQ1, aQ2, aQ2T, adXN, adXNT,          // C x C
+  aD1T, aSz,                                                   // C x h (Sz fragment-major)
+  A_CT
+};
+enum ATmpF { aXK, aHH, aNb, aKb, A_F };
+// pass-B temporaries, one set per unit
+enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, tGbT, tZkbT, tYkb, tYkbT, B_CT };
+enum BTmpF { tZkp, tT3, tT4, tT5, tT6, B_F };
+
+template <int NB>
+struct Lay {
+  size_t o[NB];
+  size_t n;
+};
+
+// offsets rounded to 8 elements: 16-byte alignment for bf16 and fp32 vectors
+template <int NB>
+constexpr Lay<NB> make_lay(const size_t (&sz)[NB]) {
+  Lay<NB> y{};
+  size_t off = 0;
+  for (int i = 0; i < NB; ++i) {
+    y.o[i] = off;
+    off += (sz[i] + 7) & ~size_t(7);
+  }
+  y.n = off;
+  return y;
+}
+
+struct SplitLayout {
+  Lay<REC_CT> rc;
+  Lay<REC_F> rf;
+  Lay<A_CT> ac;
+  Lay<A_F> af;
+  Lay<B_CT> bc;
+  Lay<B_F> bf;
+};
+
+constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
+  const size_t C = Cp, Cd = C * d, Ch = C * h, CC = C * C, HD = (size_t)h * d, dd = (size_t)d * d;
+  const size_t src[REC_CT] = {Ch, Ch, Ch, Ch, Ch, Ch, Ch, Ch, CC, CC, CC, Cd, Cd, Cd, Cd,
+                              Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd};
+  const size_t srf[REC_F] = {CC, C, C, C, C, C, 4, dd, C, C, 4};
+  const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd,
+                            CC, CC, CC, CC, CC, CC, CC, CC, CC, Ch, Ch};
+  const size_t saf[A_F] = {CC, CC, Cd, Cd};
+  const size_t sbc[B_CT] = {HD, HD, HD, HD, Ch, Ch, Cd, Cd};
+  const size_t sbf[B_F] = {Ch, Cd, Cd, Cd, Cd};
+  return SplitLayout{make_lay(src), make_lay(srf), make_lay(sac), make_lay(saf), make_lay(sbc),
+                     make_lay(sbf)};
+}
+
+constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
+
+// dynamic LDS of pass A: cbar (CP x CP fp32), partial row sums pA, pE
+// ((D/16) x CP fp32 each), three CP x H compute-type slots
+template <typename CT, int CP, int D, int H>
+constexpr size_t split_a_lds() {
+  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + 3 * (size_t)CP * H * sizeof(CT);
+}
+// pass B: one CP x H compute-type slot (Gbar, then Zkbar)
+template <typename CT, int CP, int H>
+constexpr size_t split_b_lds() {
+  return (size_t)CP * H * sizeof(CT);
+}
+// pass C: cbar, U (CP x CP fp32 each) and the gate partials (5 x 8 x CP fp32);
+// the Q-K term uses the same space first (Nbar: CP x D, Msym: D x D fp32)
+template <int CP, int D>
+constexpr size_t split_c_lds() {
+  const size_t gate = (2 * (size_t)CP * CP + 40 * (size_t)CP) * sizeof(float);
+  const size_t qk = ((size_t)CP * D + (size_t)D * D) * sizeof(float);
+  return gate > qk ? gate : qk;
+}
+
+}  // namespace
+
+struct SplitPtrs {
+  void* rec;        // CT   [units * nch][rc.n]
+  float* rec_f;     // fp32 [units * nch][rf.n]
+  void* tmpA;       // CT   [SPLIT_GRID_A][ac.n]
+  float* tmpA_f;    // fp32 [SPLIT_GRID_A][af.n]
+  void* tmpB;       // CT   [units][bc.n]
+  float* tmpB_f;    // fp32 [units][bf.n]
+  int units;
+};
+
+// ===========================================================================
+// pass A: retrieval backward of every chunk
+// ===========================================================================
+template <typename IO, typename CT, int ACT, int D, int H, int CP>
+__global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
+  __shared__ Coef cf;
+  __shared__ float gA[MAXC], gE[MAXC];
+  __shared__ float kss[D / 8][MAXC];  // partial squared key norms per 8-column block
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int d = D, h = H, Cp = CP;
+  float* fCb = reinterpret_cast<float*>(smem);
+  float* pA = fCb + Cp * Cp;
+  float* pE = pA + (D / 16) * Cp;
+  // C x h slots: S1 = Hk, S2 = H (Z .. H W2^T) then Zbar, S3 = D1
+  CT* slot1 = reinterpret_cast<CT*>(pE + (D / 16) * Cp);
+  CT* slot2 = slot1 + Cp * h;
+  CT* slot3 = slot2 + Cp * h;
+
+  const Dims Dm = a.D;
+  const int C = Dm.C;
+  const int nshard = Dm.L / Dm.S;
+  const int nch = Dm.S / C;
+  const int total = P.units * nch;
+  constexpr size_t hd = (size_t)h * d;
+  constexpr SplitLayout Y = make_split_layout(CP, D, H);
+  const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
+  const float rscale = 2.0f / (float)d;
+  CT* const ta0 = (CT*)P.tmpA + (size_t)blockIdx.x * Y.ac.n;
+  float* const tf0 = P.tmpA_f + (size_t)blockIdx.x * Y.af.n;
+
+  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+    const int u = t / nch, n = t - u * nch;
+    const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
+    CT* rc = (CT*)P.rec + (size_t)t * Y.rc.n;
+    float* rf = P.rec_f + (size_t)t * Y.rf.n;
+    CT* ta = ta0;
+    float* tf = tf0;
+    asm volatile("" : "+s"(rc), "+s"(rf), "+s"(ta), "+s"(tf));
+    const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
+    const IO* qg = (const IO*)a.q + cbase * d;
+    const IO* kg = (const IO*)a.k + cbase * d;
+    const IO* vg = (const IO*)a.v + cbase * d;
+    const IO* dOg = (const IO*)a.dO + cbase * d;
+    float* dqp = a.dq_part + cbase * d;
+    float* dkp = a.dk_part + cbase * d;
+#define R_(x) (rc + Y.rc.o[x])
+#define RF_(x) (rf + Y.rf.o[x])
+#define A_(x) (ta + Y.ac.o[x])
+#define AF_(x) (tf + Y.af.o[x])
+    CT *Hk = slot1, *HkT = R_(rHkT), *D1 = slot3, *H_ = slot2, *Zb = slot2;
+    CT *ZbT = R_(rZbT), *HT = R_(rHT), *Sp = R_(rSp), *Spp = R_(rSpp), *G = R_(rG);
+    CT *PzT = R_(rPzT), *Q1T = R_(rQ1T), *PoT = R_(rPoT);
+    CT *K = R_(rK), *KT = R_(rKT), *KcC = R_(rKcC), *Kb = R_(rKb), *R = R_(rR), *RT = R_(rRT),
+       *RcC = R_(rRcC), *Rb = R_(rRb), *dOT = R_(rdOT);
+    CT *XAT = R_(rXAT), *XET = R_(rXET), *dOAT = R_(rdOAT), *dOET = R_(rdOET), *N = R_(rN);
+    CT *Q = A_(aQ), *QT = A_(aQT), *NT = A_(aNT), *X = A_(aX), *XT = A_(aXT), *XA = A_(aXA),
+       *XE = A_(aXE), *dO = A_(adO), *dOA = A_(adOA), *dOE = A_(adOE), *Xb = A_(aXb),
+       *XbT = A_(aXbT);
+    CT *Str = A_(aStr), *StrT = A_(aStrT), *Pz = A_(aPz), *Po = A_(aPo), *Q1 = A_(aQ1),
+       *Q2 = A_(aQ2), *Q2T = A_(aQ2T), *dXN = A_(adXN), *dXNT = A_(adXNT);
+    CT *D1T = A_(aD1T), *Sz = A_(aSz);
+    float *fXK = AF_(aXK), *fHH = AF_(aHH), *fNb = AF_(aNb), *fKb = AF_(aKb);
+    const int tok0 = s * Dm.S + n * C;
+    const int l = lane_id_local();
+    const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
+    const float *W1 = st, *W2 = st + hd, *S1 = st + 2 * hd, *S2 = st + 3 * hd;
+    const float* Mc = a.mstates + ((size_t)u * a.nslots + n) * d * d;
+    const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
+    const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd, *McT = pk + 4 * hd;
+
+    // ---- stage Q, K, dO rows and their transposes (one (row, 8-column block)
+    // per thread, consecutive threads on consecutive rows); partial key norms
+    constexpr int JB = D / 8, ITEMS = CP * JB, PER = (ITEMS + 511) / 512;
+    float kx[PER][8], ox[PER][8];
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = threadIdx.x + p * 512;
+      if (e < ITEMS) {
+        const int i = e % CP, j0 = (e / CP) * 8;
+        const size_t gofs = (size_t)(tok0 + i) * d + j0, en = (size_t)i * d + j0;
+        float qx[8];
+        if (i < C) {
+          load8(qg + gofs, qx);
+          load8(kg + gofs, kx[p]);
+          load8(dOg + gofs, ox[p]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) qx[q] = kx[p][q] = ox[p][q] = 0.f;
+        }
+        store8<CT>(Q + en, qx);
+        store8<CT>(K + en, kx[p]);
+        store8<CT>(dO + en, ox[p]);
+        float ss = 0.f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const size_t et = (size_t)(j0 + q) * Cp + i;
+          QT[et] = from_f<CT>(qx[q]);
+          KT[et] = from_f<CT>(kx[p][q]);
+          dOT[et] = from_f<CT>(ox[p][q]);
+          ss += kx[p][q] * kx[p][q];
+        }
+        kss[j0 / 8][i] = ss;
+      }
+    }
+    chunk_coefs(cf, a.lr + cbase, a.mom + cbase, a.decay + cbase, tok0, C, Cp);  // ends with a barrier
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = threadIdx.x + p * 512;
+      if (e < ITEMS) {
+        const int i = e % CP, j0 = (e / CP) * 8;
+        const size_t en = (size_t)i * d + j0;
+        float n2 = 0.f;
+#pragma unroll
+        for (int q = 0; q < JB; ++q) n2 += kss[q][i];  // fixed order: deterministic
+        const float nr = sqrtf(n2);
+        if (j0 == 0) cf.knorm[i] = nr;
+        float va[8], ve[8], vc[8], vb[8], vn[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const size_t et = (size_t)(j0 + q) * Cp + i;
+          va[q] = cf.A[i] * ox[p][q];
+          ve[q] = cf.E[i] * ox[p][q];
+          vc[q] = cf.cC[i] * kx[p][q];
+          vb[q] = cf.bb[i] * kx[p][q];
+          vn[q] = (i < C && nr > 0.f) ? kx[p][q] / nr : 0.f;
+          dOAT[et] = from_f<CT>(va[q]);
+          dOET[et] = from_f<CT>(ve[q]);
+          if (Dm.qk_proj) NT[et] = from_f<CT>(vn[q]);
+        }
+        store8<CT>(dOA + en, va);
+        store8<CT>(dOE + en, ve);
+        store8<CT>(KcC + en, vc);
+        store8<CT>(Kb + en, vb);
+        if (Dm.qk_proj) store8<CT>(N + en, vn);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < MAXC) gA[threadIdx.x] = gE[threadIdx.x] = 0.f;
+    auto put_x4 = [&](int i, int j, const f4& x) {
+      f4 xa, xe;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const size_t e = (size_t)(i + r) * d + j;
+        X[e] = from_f<CT>(x[r]);
+        xa[r] = cf.A[i + r] * x[r];
+        xe[r] = cf.E[i + r] * x[r];
+        XA[e] = from_f<CT>(xa[r]);
+        XE[e] = from_f<CT>(xe[r]);
+      }
+      store4<CT>(XT + (size_t)j * Cp + i, x);
+      store4<CT>(XAT + (size_t)j * Cp + i, xa);
+      store4<CT>(XET + (size_t)j * Cp + i, xe);
+    };
+    using BCD = Blk<CP, D>;
+    using BCH = Blk<CP, H>;
+    using BCC = Blk<CP, CP>;
+    using BDD = Blk<D, D>;
+    auto fofs = [&](int i0, int j0, int rb, int cb) -> size_t {
+      const int blk = (i0 / (BCH::RB * 16)) * BCH::NBN + j0 / (BCH::CB * 16);
+      return ((size_t)((blk * BCH::RB + rb) * BCH::CB + cb) * WAVE + l) * 4;
+    };
+    if (Dm.qk_proj) {
+      for_blocks<CP, CP>([&](int i0, int j0) {
+        f4 acc[BCC::RB][BCC::CB];
+        zero_blk(acc);
+        mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, Q, d, i0, N, d, j0);
+        blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+          f4 y;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            y[r] = j <= i + r ? acc[rb][cb][r] : 0.f;
+            Str[(size_t)(i + r) * Cp + j] = from_f<CT>(y[r]);
+          }
+          store4<CT>(StrT + (size_t)j * Cp + i, y);
+        });
+      });
+      __syncthreads();
+      for_blocks<CP, D>([&](int i0, int j0) {
+        f4 acc[BCD::RB][BCD::CB];
+        zero_blk(acc);
+        if (shard_qk) mma_blk<CT, KC, KC, BCD::RB, BCD::CB, D>(acc, Q, d, i0, Mc, d, j0);
+        mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(acc, Str, Cp, i0, NT, Cp, j0);
+        blk_each4<BCD::RB, BCD::CB>(i0, j0,
+                                    [&](int rb, int cb, int i, int j) { put_x4(i, j, acc[rb][cb]); });
+      });
+    } else {
+      for (int e = threadIdx.x; e < Cp * d / 4; e += blockDim.x) {
+        const int i = (e % (Cp / 4)) * 4, j = e / (Cp / 4);
+        f4 x;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = to_f(Q[(size_t)(i + r) * d + j]);
+        put_x4(i, j, x);
+      }
+    }
+    // Zk = K W1^T -> Hk (LDS and record), s'(Zk), s''(Zk)
+    for_blocks<CP, H>([&](int i0, int j0) {
+      f4 acc[BCH::RB][BCH::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(acc, K, d, i0, W1, d, j0);
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 hv, sp, spp;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const ActVals av = act_all<ACT>(acc[rb][cb][r]);
+          const CT hx = from_f<CT>(av.s);
+          Hk[(size_t)(i + r) * h + j] = hx;
+          R_(rHk)[(size_t)(i + r) * h + j] = hx;
+          hv[r] = av.s;
+          sp[r] = av.d1;
+          spp[r] = av.d2;
+        }
+        const size_t fo = fofs(i0, j0, rb, cb);
+        store4<CT>(Sp + fo, sp);
+        store4<CT>(Spp + fo, spp);
+        store4<CT>(HkT + (size_t)j * Cp + i, hv);
+      });
+    });
+    __syncthreads();
+    // R = (2/d)(Hk W2^T - V)
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 acc[BCD::RB][BCD::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(acc, Hk, h, i0, W2, h, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 rv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          rv[r] = (ii < C) ? rscale * (acc[rb][cb][r] - to_f(vg[(size_t)(tok0 + ii) * d + j])) : 0.f;
+          R[(size_t)ii * d + j] = from_f<CT>(rv[r]);
+          RcC[(size_t)ii * d + j] = from_f<CT>(cf.cC[ii] * rv[r]);
+          Rb[(size_t)ii * d + j] = from_f<CT>(cf.bb[ii] * rv[r]);
+        }
+        store4<CT>(RT + (size_t)j * Cp + i, rv);
+      });
+    });
+    __syncthreads();
+    // G = R W2, D1 = G * s'(Zk) (LDS and record) ;  XK = X K^T, Pz = c o XK
+    for_blocks<CP, H>([&](int i0, int j0) {
+      f4 acc[BCH::RB][BCH::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(acc, R, d, i0, W2T, d, j0);
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofs(i0, j0, rb, cb);
+        const f4 sp = load4<CT>(Sp + fo);
+        f4 dv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          dv[r] = acc[rb][cb][r] * sp[r];
+          const CT dx = from_f<CT>(dv[r]);
+          D1[(size_t)(i + r) * h + j] = dx;
+          R_(rD1)[(size_t)(i + r) * h + j] = dx;
+        }
+        store4<CT>(G + fo, acc[rb][cb]);
+        store4<CT>(D1T + (size_t)j * Cp + i, dv);
+      });
+    });
+    for_blocks<CP, CP>([&](int i0, int j0) {
+      f4 acc[BCC::RB][BCC::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, X, d, i0, K, d, j0);
+      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 pv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const float x = acc[rb][cb][r];
+          fXK[ii * Cp + j] = x;
+          pv[r] = j <= ii ? cf.c[ii][j] * x : 0.f;
+          Pz[(size_t)ii * Cp + j] = from_f<CT>(pv[r]);
+        }
+        store4<CT>(PzT + (size_t)j * Cp + i, pv);
+      });
+    });
+    __syncthreads();
+    // Z = diag(A) X W1^T + diag(E) X S1^T - Pz D1 -> H, s'(Z)
+    for_blocks<CP, H>([&](int i0, int j0) {
+      f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
+      zero_blk(a1);
+      zero_blk(a3);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, XA, d, i0, W1, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, XE, d, i0, S1, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Pz, Cp, i0, D1T, Cp, j0);
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 hv, sz;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const ActVals av = act_all<ACT>(a1[rb][cb][r] - a3[rb][cb][r]);
+          H_[(size_t)(i + r) * h + j] = from_f<CT>(av.s);
+          hv[r] = av.s;
+          sz[r] = av.d1;
+        }
+        store4<CT>(Sz + fofs(i0, j0, rb, cb), sz);
+        store4<CT>(HT + (size_t)j * Cp + i, hv);
+      });
+    });
+    __syncthreads();
+    // HH = H Hk^T, Po = c o HH
+    for_blocks<CP, CP>([&](int i0, int j0) {
+      f4 acc[BCC::RB][BCC::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCC::RB, BCC::CB, H>(acc, H_, h, i0, Hk, h, j0);
+      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 pv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const float x = acc[rb][cb][r];
+          fHH[ii * Cp + j] = x;
+          pv[r] = j <= ii ? cf.c[ii][j] * x : 0.f;
+          Po[(size_t)ii * Cp + j] = from_f<CT>(pv[r]);
+        }
+        store4<CT>(PoT + (size_t)j * Cp + i, pv);
+      });
+    });
+    // dA, dE of the retrieval: sum_j (dO W2)_ij H_ij = sum_k dO_ik (H W2^T)_ik (S2 likewise)
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a1[BCD::RB][BCD::CB], a2[BCD::RB][BCD::CB];
+      zero_blk(a1);
+      zero_blk(a2);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a1, H_, h, i0, W2, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, H_, h, i0, S2, h, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const float ov = to_f(dO[(size_t)ii * d + j]);
+          const float sa = sum16b(a1[rb][cb][r] * ov), se = sum16b(a2[rb][cb][r] * ov);
+          if ((l & 15) == 0) {
+            pA[(j >> 4) * Cp + ii] = sa;
+            pE[(j >> 4) * Cp + ii] = se;
+          }
+        }
+      });
+    });
+    __syncthreads();
+    // dOR = dO R^T ; Q1 = c o dOR ; cbar = -HH o dOR
+    for_blocks<CP, CP>([&](int i0, int j0) {
+      f4 acc[BCC::RB][BCC::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, dO, d, i0, R, d, j0);
+      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 qv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const float x = acc[rb][cb][r];
+          const bool lo = j <= ii;
+          qv[r] = lo ? cf.c[ii][j] * x : 0.f;
+          Q1[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
+          fCb[ii * Cp + j] = lo ? -fHH[ii * Cp + j] * x : 0.f;
+        }
+        store4<CT>(Q1T + (size_t)j * Cp + i, qv);
+      });
+    });
+    __syncthreads();
+    // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)  (slot S2: H is dead)
+    for_blocks<CP, H>([&](int i0, int j0) {
+      f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
+      zero_blk(a1);
+      zero_blk(a3);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dOA, d, i0, W2T, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dOE, d, i0, S2T, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Q1, Cp, i0, HkT, Cp, j0);
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const f4 sz = load4<CT>(Sz + fofs(i0, j0, rb, cb));
+        f4 zv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          zv[r] = (a1[rb][cb][r] - a3[rb][cb][r]) * sz[r];
+          Zb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
+        }
+        store4<CT>(ZbT + (size_t)j * Cp + i, zv);
+      });
+    });
+    __syncthreads();
+    for (int i = threadIdx.x; i < Cp; i += blockDim.x) {
+      float sa = 0.f, se = 0.f;
+#pragma unroll
+      for (int q = 0; q < (d >> 4); ++q) {
+        sa += pA[q * Cp + i];
+        se += pE[q * Cp + i];
+      }
+      gA[i] += sa;
+      gE[i] += se;
+    }
+    // dZD1 = Zbar D1^T ; Q2 = c o dZD1 ; cbar -= XK o dZD1
+    for_blocks<CP, CP>([&](int i0, int j0) {
+      f4 acc[BCC::RB][BCC::CB];
+      zero_blk(acc);
+      mma_blk<CT, KC, KC, BCC::RB, BCC::CB, H>(acc, Zb, h, i0, D1, h, j0);
+      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 qv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const float x = acc[rb][cb][r];
+          const bool lo = j <= ii;
+          qv[r] = lo ? cf.c[ii][j] * x : 0.f;
+          Q2[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
+          if (lo) fCb[ii * Cp + j] -= fXK[ii * Cp + j] * x;
+        }
+        store4<CT>(Q2T + (size_t)j * Cp + i, qv);
+      });
+    });
+    __syncthreads();
+    // Xbar = diag(A) Zbar W1 + diag(E) Zbar S1 - Q2 K
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a1[BCD::RB][BCD::CB], a2[BCD::RB][BCD::CB], a3[BCD::RB][BCD::CB];
+      zero_blk(a1);
+      zero_blk(a2);
+      zero_blk(a3);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a1, Zb, h, i0, W1T, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Zb, h, i0, S1T, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(a3, Q2, Cp, i0, KT, Cp, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 xv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const float x = to_f(X[(size_t)ii * d + j]);
+          xv[r] = cf.A[ii] * a1[rb][cb][r] + cf.E[ii] * a2[rb][cb][r] - a3[rb][cb][r];
+          Xb[(size_t)ii * d + j] = from_f<CT>(xv[r]);
+          if (!Dm.qk_proj && ii < C) dqp[(size_t)(tok0 + ii) * d + j] = xv[r];
+          const float sa = sum16b(a1[rb][cb][r] * x), se = sum16b(a2[rb][cb][r] * x);
+          if ((l & 15) == 0) {
+            pA[(j >> 4) * Cp + ii] = sa;
+            pE[(j >> 4) * Cp + ii] = se;
+          }
+        }
+        store4<CT>(XbT + (size_t)j * Cp + i, xv);
+      });
+    });
+    // Kbar (retrieval part) = -Q2^T X
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a1[BCD::RB][BCD::CB];
+      zero_blk(a1);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(a1, Q2T, Cp, i0, XT, Cp, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) fKb[(size_t)(i + r) * d + j] = -a1[rb][cb][r];
+      });
+    });
+    __syncthreads();
+    for (int i = threadIdx.x; i < Cp; i += blockDim.x) {
+      float sa = 0.f, se = 0.f;
+#pragma unroll
+      for (int q = 0; q < (d >> 4); ++q) {
+        sa += pA[q * Cp + i];
+        se += pE[q * Cp + i];
+      }
+      rf[Y.rf.o[rgA] + i] = gA[i] + sa;
+      rf[Y.rf.o[rgE] + i] = gE[i] + se;
+      rf[Y.rf.o[rkn] + i] = cf.knorm[i];
+      rf[Y.rf.o[rcC] + i] = cf.cC[i];
+      rf[Y.rf.o[rbb] + i] = cf.bb[i];
+    }
+    if (threadIdx.x == 0) {
+      rf[Y.rf.o[rsc] + 0] = cf.AC;
+      rf[Y.rf.o[rsc] + 1] = cf.BC;
+      rf[Y.rf.o[rsc] + 2] = cf.EC;
+    }
+    for (int e = threadIdx.x * 4; e < Cp * Cp; e += blockDim.x * 4)
+      *reinterpret_cast<f32x4*>(RF_(rCb) + e) = *reinterpret_cast<const f32x4*>(fCb + e);
+    if (Dm.qk_proj) {
+      // dXN = tril(Xbar N^T)
+      for_blocks<CP, CP>([&](int i0, int j0) {
+        f4 acc[BCC::RB][BCC::CB];
+        zero_blk(acc);
+        mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, Xb, d, i0, N, d, j0);
+        blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+          f4 y;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            y[r] = j <= i + r ? acc[rb][cb][r] : 0.f;
+            dXN[(size_t)(i + r) * Cp + j] = from_f<CT>(y[r]);
+          }
+          store4<CT>(dXNT + (size_t)j * Cp + i, y);
+        });
+      });
+      // Xbar^T Q for the carried Q-K state adjoint
+      if (shard_qk)
+        for_blocks<D, D>([&](int i0, int j0) {
+          f4 a1[BDD::RB][BDD::CB];
+          zero_blk(a1);
+          mma_blk<CT, KC, KC, BDD::RB, BDD::CB, CP>(a1, XbT, Cp, i0, QT, Cp, j0);
+          blk_each4<BDD::RB, BDD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) RF_(rXbQ)[(size_t)(i + r) * d + j] = a1[rb][cb][r];
+          });
+        });
+      __syncthreads();
+      // Qbar = Xbar M0 + tril(Xbar N^T) N ; Nbar (this chunk's terms) = Str^T Xbar + dXN^T Q
+      for_blocks<CP, D>([&](int i0, int j0) {
+        f4 q1[BCD::RB][BCD::CB], n1[BCD::RB][BCD::CB];
+        zero_blk(q1);
+        zero_blk(n1);
+        if (shard_qk) mma_blk<CT, KC, KC, BCD::RB, BCD::CB, D>(q1, Xb, d, i0, McT, d, j0);
+        mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(q1, dXN, Cp, i0, NT, Cp, j0);
+        mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(n1, StrT, Cp, i0, XbT, Cp, j0);
+        mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(n1, dXNT, Cp, i0, QT, Cp, j0);
+        blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int ii = i + r;
+            if (ii < C) dqp[(size_t)(tok0 + ii) * d + j] = q1[rb][cb][r];
+            fNb[(size_t)ii * d + j] = n1[rb][cb][r];
+          }
+        });
+      });
+      __syncthreads();
+      // Kbar += (Nbar - N (N . Nbar)) / ||k||
+      for (int i = wave_id(); i < C; i += num_waves()) {
+        const float nr = cf.knorm[i];
+        float dt = 0.f;
+        for (int j = l; j < d; j += WAVE) dt += to_f(N[(size_t)i * d + j]) * fNb[(size_t)i * d + j];
+        dt = wave_sum(dt);
+        if (nr > 0.f)
+          for (int j = l; j < d; j += WAVE) {
+            const size_t e = (size_t)i * d + j;
+            fKb[e] += (fNb[e] - to_f(N[e]) * dt) / nr;
+          }
+      }
+      __syncthreads();
+    }
+    for (int e = threadIdx.x * 4; e < C * d; e += blockDim.x * 4)
+      *reinterpret_cast<f32x4*>(dkp + (size_t)tok0 * d + e) = *reinterpret_cast<const f32x4*>(fKb + e);
+    __syncthreads();  // the next chunk reuses LDS and the temporaries
+#undef R_
+#undef RF_
+#undef A_
+#undef AF_
+  }
+}
+
+// ===========================================================================
+// pass B: the carried adjoint, walked back through a unit's chunks
+// ===========================================================================
+template <typename IO, typename CT, int ACT, int D, int H, int CP>
+__global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, SplitPtrs P) {
+  __shared__ float sC[MAXC], sB[MAXC], sc3[4];
+  __shared__ float dpart[3][16];
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int d = D, h = H, Cp = CP;
+  CT* slot1 = reinterpret_cast<CT*>(smem);  // Gbar (D1bar .. Rbar), then Zkbar (Hkbar .. Kbar)
+
+  const Dims Dm = a.D;
+  const int C = Dm.C;
+  const int nshard = Dm.L / Dm.S;
+  const int nch = Dm.S / C;
+  const int u = blockIdx.x;
+  const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
+  constexpr size_t hd = (size_t)h * d;
+  constexpr SplitLayout Y = make_split_layout(CP, D, H);
+  const float rscale = 2.0f / (float)d;
+  const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
+  float* dkp = a.dk_part + cbase * d;
+  float* dvp = a.dv_part + cbase * d;
+  float* const adj0 = a.adj + (size_t)u * 4 * hd;
+  CT* const tb0 = (CT*)P.tmpB + (size_t)u * Y.bc.n;
+  float* const tbf0 = P.tmpB_f + (size_t)u * Y.bf.n;
+
+  for (size_t e = threadIdx.x; e < 4 * hd; e += blockDim.x) {
+    adj0[e] = 0.f;
+    tb0[Y.bc.o[tWb1T] + e] = from_f<CT>(0.f);  // the four transposed adjoint copies
+  }
+  __syncthreads();
+
+  for (int n = nch - 1; n >= 0; --n) {
+    const size_t t = (size_t)u * nch + n;
+    CT* rc = (CT*)P.rec + t * Y.rc.n;
+    float* rf = P.rec_f + t * Y.rf.n;
+    CT* tb = tb0;
+    float* tbf = tbf0;
+    float* adj = adj0;
+    asm volatile("" : "+s"(rc), "+s"(rf), "+s"(tb), "+s"(tbf), "+s"(adj));
+#define R_(x) (rc + Y.rc.o[x])
+#define RF_(x) (rf + Y.rf.o[x])
+#define T_(x) (tb + Y.bc.o[x])
+#define TF_(x) (tbf + Y.bf.o[x])
+    float *Wb1 = adj, *Wb2 = adj + hd, *Sb1 = adj + 2 * hd, *Sb2 = adj + 3 * hd;
+    CT *Wb1T = T_(tWb1T), *Sb1T = T_(tSb1T), *Wb2T = T_(tWb2T), *Sb2T = T_(tSb2T);
+    CT *GbT = T_(tGbT), *ZkbT = T_(tZkbT), *Ykb = T_(tYkb), *YkbT = T_(tYkbT);
+    CT *Gb = slot1, *Zkb = slot1;
+    float *fZkp = TF_(tZkp), *fT3 = TF_(tT3), *fT4 = TF_(tT4), *fT5 = TF_(tT5), *fT6 = TF_(tT6);
+    const CT *Hk = R_(rHk), *HkT = R_(rHkT), *D1 = R_(rD1), *ZbT = R_(rZbT), *HT = R_(rHT),
+             *Sp = R_(rSp), *Spp = R_(rSpp), *G = R_(rG), *PzT = R_(rPzT), *Q1T = R_(rQ1T),
+             *PoT = R_(rPoT), *K = R_(rK), *KT = R_(rKT), *KcC = R_(rKcC), *Kb = R_(rKb), *R = R_(rR),
+             *RT = R_(rRT), *RcC = R_(rRcC), *Rb = R_(rRb), *dOT = R_(rdOT), *XAT = R_(rXAT),
+             *XET = R_(rXET), *dOAT = R_(rdOAT), *dOET = R_(rdOET);
+    const int tok0 = s * Dm.S + n * C;
+    const int l = lane_id_local();
+    const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
+    const float *W2 = st + hd;
+    const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
+    const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd;
+    using BCD = Blk<CP, D>;
+    using BCH = Blk<CP, H>;
+    auto fofs = [&](int i0, int j0, int rb, int cb) -> size_t {
+      const int blk = (i0 / (BCH::RB * 16)) * BCH::NBN + j0 / (BCH::CB * 16);
+      return ((size_t)((blk * BCH::RB + rb) * BCH::CB + cb) * WAVE + l) * 4;
+    };
+
+    // ---- phase 1: chunk coefficients; adjoint . state dot products (dA_C,
+    // dE_C, dB_C); T3..T6; D1bar -> Gbar; the first part of Hkbar
+    if (threadIdx.x < Cp) {
+      sC[threadIdx.x] = RF_(rcC)[threadIdx.x];
+      sB[threadIdx.x] = RF_(rbb)[threadIdx.x];
+    }
+    if (threadIdx.x < 3) sc3[threadIdx.x] = RF_(rsc)[threadIdx.x];
+    {
+      float pa = 0.f, pe = 0.f, pb = 0.f;
+      const CT* adjT = Wb1T;  // Wb1^T, Sb1^T, Wb2^T, Sb2^T contiguous
+#pragma unroll 2
+      for (size_t e = threadIdx.x * 8; e < hd; e += blockDim.x * 8) {
+        float w1[8], s1[8], w2[8], s2[8], b1[8], c1[8], b2[8], c2[8];
+        load8(W1T + e, w1);
+        load8(S1T + e, s1);
+        load8(W2T + e, w2);
+        load8(S2T + e, s2);
+        load8(adjT + e, b1);
+        load8(adjT + hd + e, c1);
+        load8(adjT + 2 * hd + e, b2);
+        load8(adjT + 3 * hd + e, c2);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          pa += b1[q] * w1[q] + b2[q] * w2[q];
+          pe += b1[q] * s1[q] + b2[q] * s2[q];
+          pb += c1[q] * s1[q] + c2[q] * s2[q];
+        }
+      }
+      pa = wave_sum(pa);
+      pe = wave_sum(pe);
+      pb = wave_sum(pb);
+      if (l == 0) {
+        dpart[0][wave_id()] = pa;
+        dpart[1][wave_id()] = pe;
+        dpart[2][wave_id()] = pb;
+      }
+    }
+    // T3 = D1 W1bar', T4 = D1 S1bar', T5 = Hk W2bar'^T, T6 = Hk S2bar'^T  (C x d)
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a3[BCD::RB][BCD::CB], a4[BCD::RB][BCD::CB], a5[BCD::RB][BCD::CB], a6[BCD::RB][BCD::CB];
+      zero_blk(a3);
+      zero_blk(a4);
+      zero_blk(a5);
+      zero_blk(a6);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a3, D1, h, i0, Wb1T, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a4, D1, h, i0, Sb1T, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a5, Hk, h, i0, Wb2, h, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a6, Hk, h, i0, Sb2, h, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (size_t)(i + r) * d + j;
+          fT3[e] = a3[rb][cb][r];
+          fT4[e] = a4[rb][cb][r];
+          fT5[e] = a5[rb][cb][r];
+          fT6[e] = a6[rb][cb][r];
+        }
+      });
+    });
+    // D1bar = -Pz^T Zbar - diag(cC) K W1bar'^T - diag(b) K S1bar'^T ; Gbar = D1bar * s'(Zk);
+    // Hkbar so far = -Q1^T H - diag(cC) R W2bar' - diag(b) R S2bar' ; the Zkbar terms known
+    // now, D1bar * G * s''(Zk) + Hkbar * s'(Zk), are kept per fragment
+    for_blocks<CP, H>([&](int i0, int j0) {
+      f4 a1[BCH::RB][BCH::CB], a2[BCH::RB][BCH::CB];
+      zero_blk(a1);
+      zero_blk(a2);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a1, PzT, Cp, i0, ZbT, Cp, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, KcC, d, i0, Wb1, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, Kb, d, i0, Sb1, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a2, Q1T, Cp, i0, HT, Cp, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, RcC, d, i0, Wb2T, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, Rb, d, i0, Sb2T, d, j0);
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofs(i0, j0, rb, cb);
+        const f4 sp = load4<CT>(Sp + fo), g = load4<CT>(G + fo), spp = load4<CT>(Spp + fo);
+        f4 gv, zp;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d1b = -a1[rb][cb][r];
+          gv[r] = d1b * sp[r];
+          zp[r] = d1b * g[r] * spp[r] - a2[rb][cb][r] * sp[r];
+          Gb[(size_t)(i + r) * h + j] = from_f<CT>(gv[r]);
+        }
+        store4<float>(fZkp + fo, zp);
+        store4<CT>(GbT + (size_t)j * Cp + i, gv);
+      });
+    });
+    __syncthreads();
+
+    // ---- phase 2: cC_bar = -K.T3 - R.T5, b_bar = -K.T4 - R.T6 (row dots);
+    // Rbar = -Po^T dO - diag(cC) T5 - diag(b) T6 + Gbar W2^T ; Ykbar = (2/d) Rbar ; Vbar = -Ykbar
+    for (int i = wave_id(); i < Cp; i += num_waves()) {
+      float sc_ = 0.f, sb_ = 0.f;
+      for (int j = l; j < d; j += WAVE) {
+        const size_t e = (size_t)i * d + j;
+        const float kx = to_f(K[e]), rx = to_f(R[e]);
+        sc_ += kx * fT3[e] + rx * fT5[e];
+        sb_ += kx * fT4[e] + rx * fT6[e];
+      }
+      sc_ = wave_sum(sc_);
+      sb_ = wave_sum(sb_);
+      if (l == 0) {
+        RF_(rgCC)[i] = -sc_;
+        RF_(rgB)[i] = -sb_;
+      }
+    }
+    if (threadIdx.x < 3) {
+      float x = 0.f;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) x += dpart[threadIdx.x][w];
+      RF_(rdot)[threadIdx.x] = x;
+    }
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a1[BCD::RB][BCD::CB], a2[BCD::RB][BCD::CB];
+      zero_blk(a1);
+      zero_blk(a2);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(a1, PoT, Cp, i0, dOT, Cp, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Gb, h, i0, W2, h, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 yv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const size_t e = (size_t)ii * d + j;
+          const float rb_ = -a1[rb][cb][r] - sC[ii] * fT5[e] - sB[ii] * fT6[e] + a2[rb][cb][r];
+          yv[r] = (ii < C) ? rscale * rb_ : 0.f;
+          Ykb[e] = from_f<CT>(yv[r]);
+          if (ii < C) dvp[(size_t)(tok0 + ii) * d + j] = -yv[r];
+        }
+        store4<CT>(YkbT + (size_t)j * Cp + i, yv);
+      });
+    });
+    __syncthreads();
+
+    // ---- phase 3: Zkbar = (Hkbar + Ykbar W2) * s'(Zk) + D1bar * G * s''(Zk)  (slot: Gbar is dead)
+    for_blocks<CP, H>([&](int i0, int j0) {
+      f4 a4[BCH::RB][BCH::CB];
+      zero_blk(a4);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a4, Ykb, d, i0, W2T, d, j0);
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofs(i0, j0, rb, cb);
+        const f4 sp = load4<CT>(Sp + fo), zp = load4<float>(fZkp + fo);
+        f4 zv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          zv[r] = a4[rb][cb][r] * sp[r] + zp[r];
+          Zkb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
+        }
+        store4<CT>(ZkbT + (size_t)j * Cp + i, zv);
+      });
+    });
+    __syncthreads();
+
+    // ---- phase 4: Kbar (carried part) = -diag(cC) T3 - diag(b) T4 + Zkbar W1 ;
+    // adjoint of the chunk-entry state (in place, with its transposed copies)
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 a2[BCD::RB][BCD::CB];
+      zero_blk(a2);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Zkb, h, i0, W1T, h, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ii = i + r;
+          const size_t e = (size_t)ii * d + j;
+          if (ii < C)
+            dkp[(size_t)(tok0 + ii) * d + j] += -sC[ii] * fT3[e] - sB[ii] * fT4[e] + a2[rb][cb][r];
+        }
+      });
+    });
+    const float AC = sc3[0], BC = sc3[1], EC = sc3[2];
+    using BHD = Blk<H, D>;
+    using BDH = Blk<D, H>;
+    for_blocks<H, D>([&](int i0, int j0) {  // W1bar, S1bar : h x d
+      f4 a1[BHD::RB][BHD::CB], a3[BHD::RB][BHD::CB], ow[BHD::RB][BHD::CB], os[BHD::RB][BHD::CB];
+      blk_each4<BHD::RB, BHD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          ow[rb][cb][r] = Wb1[(size_t)(i + r) * d + j];
+          os[rb][cb][r] = Sb1[(size_t)(i + r) * d + j];
+        }
+      });
+      zero_blk(a1);
+      zero_blk(a3);
+      mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a1, ZbT, Cp, i0, XAT, Cp, j0);
+      mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a1, ZkbT, Cp, i0, KT, Cp, j0);
+      mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a3, ZbT, Cp, i0, XET, Cp, j0);
+      blk_each4<BHD::RB, BHD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 nw, ns;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (size_t)(i + r) * d + j;
+          const float w = ow[rb][cb][r], sv = os[rb][cb][r];
+          nw[r] = AC * w + a1[rb][cb][r];
+          ns[r] = EC * w + BC * sv + a3[rb][cb][r];
+          Wb1[e] = nw[r];
+          Sb1[e] = ns[r];
+        }
+        store4<CT>(Wb1T + (size_t)j * h + i, nw);
+        store4<CT>(Sb1T + (size_t)j * h + i, ns);
+      });
+    });
+    for_blocks<D, H>([&](int i0, int j0) {  // W2bar, S2bar : d x h
+      f4 a1[BDH::RB][BDH::CB], a4[BDH::RB][BDH::CB], ow[BDH::RB][BDH::CB], os[BDH::RB][BDH::CB];
+      blk_each4<BDH::RB, BDH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          ow[rb][cb][r] = Wb2[(size_t)(i + r) * h + j];
+          os[rb][cb][r] = Sb2[(size_t)(i + r) * h + j];
+        }
+      });
+      zero_blk(a1);
+      zero_blk(a4);
+      mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, dOAT, Cp, i0, HT, Cp, j0);
+      mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, RT, Cp, i0, GbT, Cp, j0);
+      mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, YkbT, Cp, i0, HkT, Cp, j0);
+      mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a4, dOET, Cp, i0, HT, Cp, j0);
+      blk_each4<BDH::RB, BDH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        f4 nw, ns;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const size_t e = (size_t)(i + r) * h + j;
+          const float w = ow[rb][cb][r], sv = os[rb][cb][r];
+          nw[r] = AC * w + a1[rb][cb][r];
+          ns[r] = EC * w + BC * sv + a4[rb][cb][r];
+          Wb2[e] = nw[r];
+          Sb2[e] = ns[r];
+        }
+        store4<CT>(Wb2T + (size_t)j * d + i, nw);
+        store4<CT>(Sb2T + (size_t)j * d + i, ns);
+      });
+    });
+    __syncthreads();
+#undef R_
+#undef RF_
+#undef T_
+#undef TF_
+  }
+  // adjoint of the learned init for this unit
+  float* dst = a.dWinit_part + (size_t)u * 2 * hd;
+  for (size_t e = threadIdx.x; e < 2 * hd; e += blockDim.x) dst[e] = adj0[e];
+}
+
+// ===========================================================================
+// Q-K state adjoint: per unit, the suffix sums over later chunks of Xbar^T Q
+// (in place: chunk n's slot ends up holding the sum over chunks m > n)
+// ===========================================================================
+__global__ void __launch_bounds__(256) split_madj_scan_kernel(float* rec_f, size_t rec_stride,
+                                                              size_t off, int units, int nch, int dd) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t u = idx / dd, e = idx - u * dd;
+  if (u >= (size_t)units) return;
+  float run = 0.f;
+  for (int n = nch - 1; n >= 0; --n) {
+    float* p = rec_f + (u * nch + n) * rec_stride + off + e;
+    const float x = *p;
+    *p = run;
+    run += x;
+  }
+}
+
+// ===========================================================================
+// pass C: gate adjoints and the carried Q-K term of dk, every chunk at once
+// ===========================================================================
+template <typename CT, int D, int H, int CP>
+__global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, SplitPtrs P) {
+  __shared__ Coef cf;
+  __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC], dots[4];
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int d = D, Cp = CP;
+  float* fCb = reinterpret_cast<float*>(smem);
+  float* fU = fCb + Cp * Cp;
+  float* gpart = fU + Cp * Cp;  // [5][8][Cp]
+  float* fNb = fCb;             // Q-K term first: Nbar [Cp][d], Msym [d][d]
+  float* fMs = fCb + Cp * d;
+
+  const Dims Dm = a.D;
+  const int C = Dm.C;
+  const int nshard = Dm.L / Dm.S;
+  const int nch = Dm.S / C;
+  const int t = blockIdx.x;
+  const int u = t / nch, n = t - u * nch;
+  const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
+  constexpr SplitLayout Y = make_split_layout(CP, D, H);
+  const CT* rc = (const CT*)P.rec + (size_t)t * Y.rc.n;
+  const float* rf = P.rec_f + (size_t)t * Y.rf.n;
+  const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
+  const float* mom = a.mom + cbase;
+  const float* dec = a.decay + cbase;
+  const int tok0 = s * Dm.S + n * C;
+  const int l = lane_id();
+  const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
+
+  if (shard_qk && n < nch - 1) {
+    // Kbar += (Nbar' - N (N . Nbar')) / ||k||, Nbar' = N (Mbar + Mbar^T), Mbar the
+    // suffix sum of Xbar^T Q over the shard's later chunks
+    const CT* N = rc + Y.rc.o[rN];
+    const float* Mb = rf + Y.rf.o[rXbQ];
+    for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
+      const int i = e / d, j = e - i * d;
+      fMs[e] = Mb[e] + Mb[(size_t)j * d + i];
+    }
+    __syncthreads();
+    using BCD = Blk<CP, D>;
+    for_blocks<CP, D>([&](int i0, int j0) {
+      f4 n1[BCD::RB][BCD::CB];
+      zero_blk(n1);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, D>(n1, N, d, i0, fMs, d, j0);
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) fNb[(size_t)(i + r) * d + j] = n1[rb][cb][r];
+      });
+    });
+    __syncthreads();
+    float* dkp = a.dk_part + (cbase + tok0) * d;
+    const float* kn = rf + Y.rf.o[rkn];
+    for (int i = wave_id(); i < C; i += num_waves()) {
+      const float nr = kn[i];
+      float dt = 0.f;
+      for (int j = l; j < d; j += WAVE) dt += to_f(N[(size_t)i * d + j]) * fNb[(size_t)i * d + j];
+      dt = wave_sum(dt);
+      if (nr > 0.f)
+        for (int j = l; j < d; j += WAVE) {
+          const size_t e = (size_t)i * d + j;
+          dkp[e] += (fNb[e] - to_f(N[e]) * dt) / nr;
+        }
+    }
+    __syncthreads();  // LDS is reused below
+  }
+
+  chunk_coefs(cf, a.lr + cbase, mom, dec, tok0, C, Cp);  // ends with a barrier
+  for (int e = threadIdx.x * 4; e < Cp * Cp; e += blockDim.x * 4)
+    *reinterpret_cast<f32x4*>(fCb + e) = *reinterpret_cast<const f32x4*>(rf + Y.rf.o[rCb] + e);
+  if (threadIdx.x < Cp) {
+    const int i = threadIdx.x;
+    gA[i] = rf[Y.rf.o[rgA] + i];
+    gE[i] = rf[Y.rf.o[rgE] + i];
+    gCC[i] = rf[Y.rf.o[rgCC] + i];
+    gB[i] = rf[Y.rf.o[rgB] + i];
+  }
+  if (threadIdx.x < 3) dots[threadIdx.x] = rf[Y.rf.o[rdot] + threadIdx.x];
+  __syncthreads();
+  if (wave_id() == 0) {
+    const int i = l;
+    if (i < Cp) fCb[(C - 1) * Cp + i] += gCC[i];
+    if (i == 0) {
+      gA[C - 1] += dots[0];
+      gE[C - 1] += dots[1];
+    }
+  }
+  __syncthreads();
+  {
+    const int w = wave_id(), i = l;
+    const int r0 = w * (Cp / 8), r1 = r0 + Cp / 8;
+    // column sums of cbar o ct, cbar o c over rows r in this block (r >= i),
+    // row sums of cbar o c over columns t in this block (t <= i)
+    float eb = 0.f, cols = 0.f, rows = 0.f;
+    if (i < Cp) {
+#pragma unroll 4
+      for (int r = r0; r < r1; ++r) {
+        if (r >= i) {
+          const float cb = fCb[r * Cp + i];
+          eb += cb * cf.ct[r][i];
+          cols += cb * cf.c[r][i];
+        }
+        if (r <= i) rows += fCb[i * Cp + r] * cf.c[i][r];
+      }
+      gpart[(0 * 8 + w) * Cp + i] = eb;
+      gpart[(1 * 8 + w) * Cp + i] = cols;
+      gpart[(2 * 8 + w) * Cp + i] = rows;
+    }
+    // U_{i, j} = beta'_j U_{i, j-1} + cbar_{i j} eta_j (j <= i), beta'_j = e^{lb_j - lb_{j-1}},
+    // for this wave's rows i, as an affine scan over the lanes j
+    const int j = l;
+    const float aj = (j < Cp) ? expf(cf.lb[j] - (j > 0 ? cf.lb[j - 1] : 0.f)) : 0.f;
+    for (int ri = r0; ri < r1; ++ri) {
+      float sa = aj, sx = (j <= ri && j < Cp) ? fCb[ri * Cp + j] * cf.eta[j] : 0.f;
+#pragma unroll
+      for (int o = 1; o < WAVE; o <<= 1) {
+        const float pa_ = __shfl_up(sa, o, WAVE), px = __shfl_up(sx, o, WAVE);
+        if (j >= o) {
+          sx = sa * px + sx;
+          sa = sa * pa_;
+        }
+      }
+      if (j < Cp) fU[ri * Cp + j] = (j <= ri) ? sx : 0.f;
+    }
+  }
+  __syncthreads();
+  {
+    // T_j = sum_{i >= j} e^{la_i - la_j} U_{i j},  Y_j = sum_{i >= j} e^{la_i - la_j} Ebar_i
+    const int w = wave_id(), j = l;
+    const int r0 = w * (Cp / 8), r1 = r0 + Cp / 8;
+    float T = 0.f, Yv = 0.f;
+    if (j < C) {
+#pragma unroll 4
+      for (int i = r0; i < r1; ++i)
+        if (i >= j) {
+          const float e = expf(cf.la[i] - cf.la[j]);
+          T += e * fU[i * Cp + j];
+          Yv += e * gE[i];
+        }
+    }
+    if (j < Cp) {
+      gpart[(3 * 8 + w) * Cp + j] = T;
+      gpart[(4 * 8 + w) * Cp + j] = Yv;
+    }
+  }
+  __syncthreads();
+  if (wave_id() == 0) {
+    const int j = l;
+    float sum[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+    if (j < Cp)
+#pragma unroll
+      for (int k = 0; k < 5; ++k)
+#pragma unroll
+        for (int w = 0; w < 8; ++w) sum[k] += gpart[(k * 8 + w) * Cp + j];
+    const float eb = sum[0] + (j < Cp ? gB[j] * cf.ebt[j] : 0.f);
+    const float cols = sum[1], rows = sum[2], T = sum[3], Yv = sum[4];
+    float la_b = 0.f, lb_b = 0.f;
+    const float dBC = dots[2];
+    const float bsum = wave_sum(j < Cp ? gB[j] * cf.bb[j] : 0.f);
+    if (j < C) {
+      const float yl = Yv * expf(cf.lb[j]);
+      la_b = gA[j] * cf.A[j] + gE[j] * cf.E[j] + rows - T - yl;
+      lb_b = T - cols + yl - gB[j] * cf.bb[j];
+      if (j == C - 1) lb_b += dBC * cf.BC + bsum;
+    }
+    // suffix sums over positions
+    const float pla = wave_incl_sum(la_b), plb = wave_incl_sum(lb_b);
+    const float tla = __shfl(pla, WAVE - 1, WAVE), tlb = __shfl(plb, WAVE - 1, WAVE);
+    const float sla = tla - pla + la_b, slb = tlb - plb + lb_b;
+    if (j < C) {
+      const size_t tt = cbase + tok0 + j;
+      const float al = a.decay[tt], be = a.mom[tt];
+      a.dlr[tt] = eb;
+      a.ddecay[tt] = -sla / (1.0f - al);
+      a.dmom[tt] = (logf(be) > LOG_CLAMP) ? slb / be : 0.f;
+    }
+  }
+}
+
+// ===========================================================================
+// host side
+// ===========================================================================
+namespace {
+
+template <typename CT, int CP, int D, int H>
+constexpr bool split_fits() {
+  // static LDS of pass A (Coef + norms) is under 40 KB; pass C's under 40 KB
+  return split_a_lds<CT, CP, D, H>() + 40 * 1024 <= 160 * 1024 &&
+         split_c_lds<CP, D>() + 40 * 1024 <= 160 * 1024;
+}
+
+struct SplitSizes {
+  size_t rec_ct, rec_f, a_ct, a_f, b_ct, b_f;  // elements
+};
+
+template <typename CT, int CP, int D, int H>
+SplitSizes split_sizes(int units, int nch) {
+  constexpr SplitLayout Y = make_split_layout(CP, D, H);
+  const size_t t = (size_t)units * nch;
+  return SplitSizes{t * Y.rc.n, t * Y.rf.n, (size_t)SPLIT_GRID_A * Y.ac.n, (size_t)SPLIT_GRID_A * Y.af.n,
+                    (size_t)units * Y.bc.n, (size_t)units * Y.bf.n};
+}
+
+size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
+
+template <typename CT>
+size_t total_bytes(const SplitSizes& z) {
+  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) + up256(z.a_ct * sizeof(CT)) +
+         up256(z.a_f * 4) + up256(z.b_ct * sizeof(CT)) + up256(z.b_f * 4);
+}
+
+template <typename CT>
+SplitPtrs carve(void* ws, const SplitSizes& z, int units) {
+  char* p = (char*)ws;
+  SplitPtrs P{};
+  P.rec = p; p += up256(z.rec_ct * sizeof(CT));
+  P.rec_f = (float*)p; p += up256(z.rec_f * 4);
+  P.tmpA = p; p += up256(z.a_ct * sizeof(CT));
+  P.tmpA_f = (float*)p; p += up256(z.a_f * 4);
+  P.tmpB = p; p += up256(z.b_ct * sizeof(CT));
+  P.tmpB_f = (float*)p;
+  P.units = units;
+  return P;
+}
+
+template <typename IO, typename CT, int ACT, int D, int H, int CP>
+bool split_match(const Dims& Dm) {
+  return Dm.d == D && Dm.hid == H && Dm.Cp == CP && Dm.act == ACT && split_fits<CT, CP, D, H>();
+}
+
+// size query (ws == nullptr) or launch
+template <typename IO, typename CT, int ACT, int D, int H, int CP>
+bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipStream_t st,
+               hipError_t* err, size_t* bytes) {
+  if (!split_match<IO, CT, ACT, D, H, CP>(Dm)) return false;
+  const int nch = Dm.S / Dm.C;
+  const SplitSizes z = split_sizes<CT, CP, D, H>(units, nch);
+  if (bytes) *bytes = total_bytes<CT>(z);
+  if (!a) return true;
+  const SplitPtrs P = carve<CT>(ws, z, units);
+  constexpr SplitLayout Y = make_split_layout(CP, D, H);
+  const int total = units * nch;
+  auto ka = local_bwd_ret_kernel<IO, CT, ACT, D, H, CP>;
+  auto kb = local_bwd_chain_kernel<IO, CT, ACT, D, H, CP>;
+  auto kc = local_bwd_gate_kernel<CT, D, H, CP>;
+  set_lds_limit((const void*)ka);
+  set_lds_limit((const void*)kb);
+  set_lds_limit((const void*)kc);
+  constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, H>(),
+                   lds_c = split_c_lds<CP, D>();
+  hipLaunchKernelGGL(ka, dim3(std::min(total, SPLIT_GRID_A)), dim3(512), lds_a, st, *a, P);
+  hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
+  if (Dm.qk_proj && Dm.qk_scope == 0) {
+    const size_t thr = (size_t)units * D * D;
+    hipLaunchKernelGGL(split_madj_scan_kernel, dim3((unsigned)((thr + 255) / 256)), dim3(256), 0, st,
+                       P.rec_f, Y.rf.n, Y.rf.o[rXbQ], units, nch, D * D);
+  }
+  hipLaunchKernelGGL(kc, dim3(total), dim3(512), lds_c, st, *a, P);
+  *err = hipGetLastError();
+  return true;
+}
+
+bool dispatch_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipStream_t st,
+                    hipError_t* err, size_t* bytes) {
+  if (Dm.bf16)
+    return try_split<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes) ||
+           try_split<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, Dm, units, ws, st, err, bytes) ||
+           try_split<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, Dm, units, ws, st, err, bytes) ||
+           try_split<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes);
+  return try_split<float, float, ACT_GELU, 16, 32, 16>(a, Dm, units, ws, st, err, bytes) ||
+         try_split<float, float, ACT_SILU, 16, 32, 16>(a, Dm, units, ws, st, err, bytes);
+}
+
+}  // namespace
+
+size_t local_bwd_split_bytes(const Dims& D, int units) {
+  size_t bytes = 0;
+  hipError_t e = hipSuccess;
+  return dispatch_split(nullptr, D, units, nullptr, nullptr, &e, &bytes) ? bytes : 0;
+}
+
+bool launch_local_bwd_split(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err) {
+  if (!a.split_ws) return false;
+  return dispatch_split(&a, a.D, units, a.split_ws, st, err, nullptr);
+}
+
+}  // namespace tnt

@@ -116,3 +116,16 @@ def test_backward_generic_kernels(cfg, monkeypatch):
     print(f"\n[case] generic {cfg.name}", flush=True)
     got = gpu_backward(cfg, inp)
     check(cfg, got, oracle_backward(cfg, inp))
+
+
+@pytest.mark.parametrize("cfg", [WORKLOADS[0], SMALL[3], SMALL[7], SMALL[9], SMALL[10]],
+                         ids=lambda c: c.name)
+def test_backward_single_walk(cfg, monkeypatch):
+    """The fixed-size local backward as one reverse walk per unit (the default
+    splits it into a chunk-parallel pass, the walk of the carried adjoint and a
+    chunk-parallel gate pass)."""
+    inp = make_inputs(cfg, 205)
+    monkeypatch.setenv("TNT_LOCAL_BWD_SINGLE", "1")
+    print(f"\n[case] single walk {cfg.name}", flush=True)
+    got = gpu_backward(cfg, inp)
+    check(cfg, got, oracle_backward(cfg, inp))
