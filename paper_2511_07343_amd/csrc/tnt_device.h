@@ -33,6 +33,17 @@ __device__ __forceinline__ int lane_id_local() {
   asm volatile("" : "+v"(l));
   return l;
 }
+// A global-memory pointer through an opaque move: addresses derived from it
+// are not hoisted out of loops, and the move is made on the global address
+// space, so the loads through it stay global loads (their completion counter
+// can be waited on partially) instead of becoming flat loads.
+template <typename T>
+__device__ __forceinline__ T* launder_global(T* p) {
+  typedef __attribute__((address_space(1))) T gT;
+  gT* g = (gT*)p;
+  asm volatile("" : "+s"(g));
+  return (T*)g;
+}
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
 __device__ __forceinline__ int num_waves() { return blockDim.x / WAVE; }
 

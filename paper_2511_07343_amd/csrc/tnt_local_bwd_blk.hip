@@ -93,7 +93,10 @@ __global__ void __launch_bounds__(512) local_bwd_blk_kernel(LocalBwdArgs a) {
     float* sf = sf0;
     float* adj = adj0;
     float* madj = madj0;
-    asm volatile("" : "+s"(sc), "+s"(sf), "+s"(adj), "+s"(madj));
+    sc = launder_global(sc);
+    sf = launder_global(sf);
+    adj = launder_global(adj);
+    madj = launder_global(madj);
     float *Wb1 = adj, *Wb2 = adj + hd, *Sb1 = adj + 2 * hd, *Sb2 = adj + 3 * hd;
 #define B_(x) (sc + Y.ct[x])
 #define F_(x) (sf + Y.f32[x])

@@ -177,7 +177,10 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     float* rf = P.rec_f + (size_t)t * Y.rf.n;
     CT* ta = ta0;
     float* tf = tf0;
-    asm volatile("" : "+s"(rc), "+s"(rf), "+s"(ta), "+s"(tf));
+    rc = launder_global(rc);
+    rf = launder_global(rf);
+    ta = launder_global(ta);
+    tf = launder_global(tf);
     const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
     const IO* qg = (const IO*)a.q + cbase * d;
     const IO* kg = (const IO*)a.k + cbase * d;
@@ -715,7 +718,11 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     CT* tb = tb0;
     float* tbf = tbf0;
     float* adj = adj0;
-    asm volatile("" : "+s"(rc), "+s"(rf), "+s"(tb), "+s"(tbf), "+s"(adj));
+    rc = launder_global(rc);
+    rf = launder_global(rf);
+    tb = launder_global(tb);
+    tbf = launder_global(tbf);
+    adj = launder_global(adj);
 #define R_(x) (rc + Y.rc.o[x])
 #define RF_(x) (rf + Y.rf.o[x])
 #define T_(x) (tb + Y.bc.o[x])
