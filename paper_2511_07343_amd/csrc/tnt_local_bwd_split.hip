@@ -61,8 +61,8 @@ enum ATmpCT {
 };
 enum ATmpF { aXK, aHH, aNb, aKb, A_F };
 // pass-B temporaries, one set per unit
-enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, tGbT, tZkbT, tYkb, tYkbT, B_CT };
-enum BTmpF { tZkp, tT3, tT4, tT5, tT6, B_F };
+enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, tGbT, B_CT };
+enum BTmpF { tZkp, B_F };
 
 template <int NB>
 struct Lay {
@@ -100,8 +100,8 @@ constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
   const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd,
                             CC, CC, CC, CC, CC, CC, CC, CC, CC, Ch, Ch};
   const size_t saf[A_F] = {CC, CC, Cd, Cd};
-  const size_t sbc[B_CT] = {HD, HD, HD, HD, Ch, Ch, Cd, Cd};
-  const size_t sbf[B_F] = {Ch, Cd, Cd, Cd, Cd};
+  const size_t sbc[B_CT] = {HD, HD, HD, HD, Ch};
+  const size_t sbf[B_F] = {Ch};
   return SplitLayout{make_lay(src), make_lay(srf), make_lay(sac), make_lay(saf), make_lay(sbc),
                      make_lay(sbf)};
 }
@@ -114,10 +114,25 @@ template <typename CT, int CP, int D, int H>
 constexpr size_t split_a_lds() {
   return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + 3 * (size_t)CP * H * sizeof(CT);
 }
-// pass B: one CP x H compute-type slot (Gbar, then Zkbar)
-template <typename CT, int CP, int H>
+// pass B: a CP x H compute-type slot (Gbar, then Zkbar); T3, T4 and T5, T6
+// (fragment-major fp32, CP x D each; the T5/T6 space holds Zkbar^T, H x CP
+// compute type, from phase 3 on); Ykbar and Ykbar^T (CP x D compute type each);
+// per-column-tile partial row sums for cC_bar, b_bar ((D/16) x CP fp32 each)
+template <typename CT, int CP, int D, int H>
+struct SplitBLds {
+  static constexpr size_t cmax(size_t x, size_t y) { return x > y ? x : y; }
+  static constexpr size_t slot = (size_t)CP * H * sizeof(CT);
+  static constexpr size_t t34 = slot;
+  static constexpr size_t t56 = t34 + 2 * (size_t)CP * D * sizeof(float);
+  static constexpr size_t ykb = t56 + cmax(2 * (size_t)CP * D * sizeof(float), (size_t)H * CP * sizeof(CT));
+  static constexpr size_t ykbt = ykb + (size_t)CP * D * sizeof(CT);
+  static constexpr size_t pc = ykbt + (size_t)CP * D * sizeof(CT);
+  static constexpr size_t pb = pc + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t total = pb + (size_t)(D / 16) * CP * sizeof(float);
+};
+template <typename CT, int CP, int D, int H>
 constexpr size_t split_b_lds() {
-  return (size_t)CP * H * sizeof(CT);
+  return SplitBLds<CT, CP, D, H>::total;
 }
 // pass C: cbar, U (CP x CP fp32 each) and the gate partials (5 x 8 x CP fp32);
 // the Q-K term uses the same space first (Nbar: CP x D, Msym: D x D fp32)
@@ -687,7 +702,17 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
   __shared__ float dpart[3][16];
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int d = D, h = H, Cp = CP;
+  using LB = SplitBLds<CT, CP, D, H>;
   CT* slot1 = reinterpret_cast<CT*>(smem);  // Gbar (D1bar .. Rbar), then Zkbar (Hkbar .. Kbar)
+  float* const fT3 = reinterpret_cast<float*>(smem + LB::t34);
+  float* const fT4 = fT3 + CP * D;
+  float* const fT5 = reinterpret_cast<float*>(smem + LB::t56);
+  float* const fT6 = fT5 + CP * D;
+  CT* const ZkbT = reinterpret_cast<CT*>(smem + LB::t56);  // T5, T6 are dead from phase 3 on
+  CT* const Ykb = reinterpret_cast<CT*>(smem + LB::ykb);
+  CT* const YkbT = reinterpret_cast<CT*>(smem + LB::ykbt);
+  float* const pC = reinterpret_cast<float*>(smem + LB::pc);
+  float* const pB = reinterpret_cast<float*>(smem + LB::pb);
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -729,9 +754,9 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 #define TF_(x) (tbf + Y.bf.o[x])
     float *Wb1 = adj, *Wb2 = adj + hd, *Sb1 = adj + 2 * hd, *Sb2 = adj + 3 * hd;
     CT *Wb1T = T_(tWb1T), *Sb1T = T_(tSb1T), *Wb2T = T_(tWb2T), *Sb2T = T_(tSb2T);
-    CT *GbT = T_(tGbT), *ZkbT = T_(tZkbT), *Ykb = T_(tYkb), *YkbT = T_(tYkbT);
+    CT* GbT = T_(tGbT);
     CT *Gb = slot1, *Zkb = slot1;
-    float *fZkp = TF_(tZkp), *fT3 = TF_(tT3), *fT4 = TF_(tT4), *fT5 = TF_(tT5), *fT6 = TF_(tT6);
+    float* fZkp = TF_(tZkp);
     const CT *Hk = R_(rHk), *HkT = R_(rHkT), *D1 = R_(rD1), *ZbT = R_(rZbT), *HT = R_(rHT),
              *Sp = R_(rSp), *Spp = R_(rSpp), *G = R_(rG), *PzT = R_(rPzT), *Q1T = R_(rQ1T),
              *PoT = R_(rPoT), *K = R_(rK), *KT = R_(rKT), *KcC = R_(rKcC), *Kb = R_(rKb), *R = R_(rR),
@@ -748,6 +773,10 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     auto fofs = [&](int i0, int j0, int rb, int cb) -> size_t {
       const int blk = (i0 / (BCH::RB * 16)) * BCH::NBN + j0 / (BCH::CB * 16);
       return ((size_t)((blk * BCH::RB + rb) * BCH::CB + cb) * WAVE + l) * 4;
+    };
+    auto fofsD = [&](int i0, int j0, int rb, int cb) -> size_t {  // C x d tiles, fragment-major
+      const int blk = (i0 / (BCD::RB * 16)) * BCD::NBN + j0 / (BCD::CB * 16);
+      return ((size_t)((blk * BCD::RB + rb) * BCD::CB + cb) * WAVE + l) * 4;
     };
 
     // ---- phase 1: chunk coefficients; adjoint . state dot products (dA_C,
@@ -798,14 +827,24 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a4, D1, h, i0, Sb1T, h, j0);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a5, Hk, h, i0, Wb2, h, j0);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a6, Hk, h, i0, Sb2, h, j0);
+      // kept in LDS at their fragment positions; the cC_bar / b_bar row dots
+      // (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofsD(i0, j0, rb, cb);
+        store4<float>(fT3 + fo, a3[rb][cb]);
+        store4<float>(fT4 + fo, a4[rb][cb]);
+        store4<float>(fT5 + fo, a5[rb][cb]);
+        store4<float>(fT6 + fo, a6[rb][cb]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i + r) * d + j;
-          fT3[e] = a3[rb][cb][r];
-          fT4[e] = a4[rb][cb][r];
-          fT5[e] = a5[rb][cb][r];
-          fT6[e] = a6[rb][cb][r];
+          const float kx = to_f(K[e]), rx = to_f(R[e]);
+          const float sc_ = sum16b(kx * a3[rb][cb][r] + rx * a5[rb][cb][r]);
+          const float sb_ = sum16b(kx * a4[rb][cb][r] + rx * a6[rb][cb][r]);
+          if ((l & 15) == 0) {
+            pC[(j >> 4) * Cp + i + r] = sc_;
+            pB[(j >> 4) * Cp + i + r] = sb_;
+          }
         }
       });
     });
@@ -841,20 +880,15 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 
     // ---- phase 2: cC_bar = -K.T3 - R.T5, b_bar = -K.T4 - R.T6 (row dots);
     // Rbar = -Po^T dO - diag(cC) T5 - diag(b) T6 + Gbar W2^T ; Ykbar = (2/d) Rbar ; Vbar = -Ykbar
-    for (int i = wave_id(); i < Cp; i += num_waves()) {
+    for (int i = threadIdx.x; i < Cp; i += blockDim.x) {
       float sc_ = 0.f, sb_ = 0.f;
-      for (int j = l; j < d; j += WAVE) {
-        const size_t e = (size_t)i * d + j;
-        const float kx = to_f(K[e]), rx = to_f(R[e]);
-        sc_ += kx * fT3[e] + rx * fT5[e];
-        sb_ += kx * fT4[e] + rx * fT6[e];
+#pragma unroll
+      for (int q = 0; q < (d >> 4); ++q) {  // fixed order: deterministic
+        sc_ += pC[q * Cp + i];
+        sb_ += pB[q * Cp + i];
       }
-      sc_ = wave_sum(sc_);
-      sb_ = wave_sum(sb_);
-      if (l == 0) {
-        RF_(rgCC)[i] = -sc_;
-        RF_(rgB)[i] = -sb_;
-      }
+      RF_(rgCC)[i] = -sc_;
+      RF_(rgB)[i] = -sb_;
     }
     if (threadIdx.x < 3) {
       float x = 0.f;
@@ -869,12 +903,14 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(a1, PoT, Cp, i0, dOT, Cp, j0);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Gb, h, i0, W2, h, j0);
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofsD(i0, j0, rb, cb);
+        const f4 t5 = load4<float>(fT5 + fo), t6 = load4<float>(fT6 + fo);
         f4 yv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int ii = i + r;
           const size_t e = (size_t)ii * d + j;
-          const float rb_ = -a1[rb][cb][r] - sC[ii] * fT5[e] - sB[ii] * fT6[e] + a2[rb][cb][r];
+          const float rb_ = -a1[rb][cb][r] - sC[ii] * t5[r] - sB[ii] * t6[r] + a2[rb][cb][r];
           yv[r] = (ii < C) ? rscale * rb_ : 0.f;
           Ykb[e] = from_f<CT>(yv[r]);
           if (ii < C) dvp[(size_t)(tok0 + ii) * d + j] = -yv[r];
@@ -910,12 +946,13 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       zero_blk(a2);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Zkb, h, i0, W1T, h, j0);
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const size_t fo = fofsD(i0, j0, rb, cb);
+        const f4 t3 = load4<float>(fT3 + fo), t4 = load4<float>(fT4 + fo);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int ii = i + r;
-          const size_t e = (size_t)ii * d + j;
           if (ii < C)
-            dkp[(size_t)(tok0 + ii) * d + j] += -sC[ii] * fT3[e] - sB[ii] * fT4[e] + a2[rb][cb][r];
+            dkp[(size_t)(tok0 + ii) * d + j] += -sC[ii] * t3[r] - sB[ii] * t4[r] + a2[rb][cb][r];
         }
       });
     });
@@ -1200,6 +1237,7 @@ template <typename CT, int CP, int D, int H>
 constexpr bool split_fits() {
   // static LDS of pass A (Coef + norms) is under 40 KB; pass C's under 40 KB
   return split_a_lds<CT, CP, D, H>() + 40 * 1024 <= 160 * 1024 &&
+         split_b_lds<CT, CP, D, H>() + 2 * 1024 <= 160 * 1024 &&
          split_c_lds<CP, D>() + 40 * 1024 <= 160 * 1024;
 }
 
@@ -1260,7 +1298,7 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   set_lds_limit((const void*)ka);
   set_lds_limit((const void*)kb);
   set_lds_limit((const void*)kc);
-  constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, H>(),
+  constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, D, H>(),
                    lds_c = split_c_lds<CP, D>();
   hipLaunchKernelGGL(ka, dim3(std::min(total, SPLIT_GRID_A)), dim3(512), lds_a, st, *a, P);
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
