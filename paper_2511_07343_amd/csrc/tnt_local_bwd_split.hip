@@ -61,8 +61,7 @@ enum ATmpCT {
 };
 enum ATmpF { aXK, aHH, aNb, aKb, A_F };
 // pass-B temporaries, one set per unit
-enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, tGbT, B_CT };
-enum BTmpF { tZkp, B_F };
+enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, B_CT };
 
 template <int NB>
 struct Lay {
@@ -89,7 +88,6 @@ struct SplitLayout {
   Lay<A_CT> ac;
   Lay<A_F> af;
   Lay<B_CT> bc;
-  Lay<B_F> bf;
 };
 
 constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
@@ -100,10 +98,8 @@ constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
   const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd,
                             CC, CC, CC, CC, CC, CC, CC, CC, CC, Ch, Ch};
   const size_t saf[A_F] = {CC, CC, Cd, Cd};
-  const size_t sbc[B_CT] = {HD, HD, HD, HD, Ch};
-  const size_t sbf[B_F] = {Ch};
-  return SplitLayout{make_lay(src), make_lay(srf), make_lay(sac), make_lay(saf), make_lay(sbc),
-                     make_lay(sbf)};
+  const size_t sbc[B_CT] = {HD, HD, HD, HD};
+  return SplitLayout{make_lay(src), make_lay(srf), make_lay(sac), make_lay(saf), make_lay(sbc)};
 }
 
 constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
@@ -117,7 +113,8 @@ constexpr size_t split_a_lds() {
 // pass B: a CP x H compute-type slot (Gbar, then Zkbar); T3, T4 and T5, T6
 // (fragment-major fp32, CP x D each; the T5/T6 space holds Zkbar^T, H x CP
 // compute type, from phase 3 on); Ykbar and Ykbar^T (CP x D compute type each);
-// per-column-tile partial row sums for cC_bar, b_bar ((D/16) x CP fp32 each)
+// per-column-tile partial row sums for cC_bar, b_bar ((D/16) x CP fp32 each);
+// Gbar^T (H x CP compute type)
 template <typename CT, int CP, int D, int H>
 struct SplitBLds {
   static constexpr size_t cmax(size_t x, size_t y) { return x > y ? x : y; }
@@ -128,7 +125,8 @@ struct SplitBLds {
   static constexpr size_t ykbt = ykb + (size_t)CP * D * sizeof(CT);
   static constexpr size_t pc = ykbt + (size_t)CP * D * sizeof(CT);
   static constexpr size_t pb = pc + (size_t)(D / 16) * CP * sizeof(float);
-  static constexpr size_t total = pb + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t gbt = pb + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t total = gbt + (size_t)H * CP * sizeof(CT);
 };
 template <typename CT, int CP, int D, int H>
 constexpr size_t split_b_lds() {
@@ -151,7 +149,6 @@ struct SplitPtrs {
   void* tmpA;       // CT   [SPLIT_GRID_A][ac.n]
   float* tmpA_f;    // fp32 [SPLIT_GRID_A][af.n]
   void* tmpB;       // CT   [units][bc.n]
-  float* tmpB_f;    // fp32 [units][bf.n]
   int units;
 };
 
@@ -713,6 +710,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
   CT* const YkbT = reinterpret_cast<CT*>(smem + LB::ykbt);
   float* const pC = reinterpret_cast<float*>(smem + LB::pc);
   float* const pB = reinterpret_cast<float*>(smem + LB::pb);
+  CT* const GbT = reinterpret_cast<CT*>(smem + LB::gbt);
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -728,7 +726,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
   float* dvp = a.dv_part + cbase * d;
   float* const adj0 = a.adj + (size_t)u * 4 * hd;
   CT* const tb0 = (CT*)P.tmpB + (size_t)u * Y.bc.n;
-  float* const tbf0 = P.tmpB_f + (size_t)u * Y.bf.n;
+  using BCH0 = Blk<CP, H>;
+  static_assert(BCH0::NB <= 8, "each wave owns at most one C x h block");
 
   for (size_t e = threadIdx.x; e < 4 * hd; e += blockDim.x) {
     adj0[e] = 0.f;
@@ -741,22 +740,20 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     CT* rc = (CT*)P.rec + t * Y.rc.n;
     float* rf = P.rec_f + t * Y.rf.n;
     CT* tb = tb0;
-    float* tbf = tbf0;
     float* adj = adj0;
     rc = launder_global(rc);
     rf = launder_global(rf);
     tb = launder_global(tb);
-    tbf = launder_global(tbf);
     adj = launder_global(adj);
 #define R_(x) (rc + Y.rc.o[x])
 #define RF_(x) (rf + Y.rf.o[x])
 #define T_(x) (tb + Y.bc.o[x])
-#define TF_(x) (tbf + Y.bf.o[x])
     float *Wb1 = adj, *Wb2 = adj + hd, *Sb1 = adj + 2 * hd, *Sb2 = adj + 3 * hd;
     CT *Wb1T = T_(tWb1T), *Sb1T = T_(tSb1T), *Wb2T = T_(tWb2T), *Sb2T = T_(tSb2T);
-    CT* GbT = T_(tGbT);
     CT *Gb = slot1, *Zkb = slot1;
-    float* fZkp = TF_(tZkp);
+    // the Zkbar terms known after phase 1, kept by the wave that owns the block
+    // until phase 3 (both phases walk the same C x h blocks)
+    f4 zkp[BCH0::RB][BCH0::CB];
     const CT *Hk = R_(rHk), *HkT = R_(rHkT), *D1 = R_(rD1), *ZbT = R_(rZbT), *HT = R_(rHT),
              *Sp = R_(rSp), *Spp = R_(rSpp), *G = R_(rG), *PzT = R_(rPzT), *Q1T = R_(rQ1T),
              *PoT = R_(rPoT), *K = R_(rK), *KT = R_(rKT), *KcC = R_(rKcC), *Kb = R_(rKb), *R = R_(rR),
@@ -872,7 +869,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
           zp[r] = d1b * g[r] * spp[r] - a2[rb][cb][r] * sp[r];
           Gb[(size_t)(i + r) * h + j] = from_f<CT>(gv[r]);
         }
-        store4<float>(fZkp + fo, zp);
+        zkp[rb][cb] = zp;
         store4<CT>(GbT + (size_t)j * Cp + i, gv);
       });
     });
@@ -927,7 +924,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a4, Ykb, d, i0, W2T, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         const size_t fo = fofs(i0, j0, rb, cb);
-        const f4 sp = load4<CT>(Sp + fo), zp = load4<float>(fZkp + fo);
+        const f4 sp = load4<CT>(Sp + fo), zp = zkp[rb][cb];
         f4 zv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1022,7 +1019,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 #undef R_
 #undef RF_
 #undef T_
-#undef TF_
   }
   // adjoint of the learned init for this unit
   float* dst = a.dWinit_part + (size_t)u * 2 * hd;
@@ -1242,7 +1238,7 @@ constexpr bool split_fits() {
 }
 
 struct SplitSizes {
-  size_t rec_ct, rec_f, a_ct, a_f, b_ct, b_f;  // elements
+  size_t rec_ct, rec_f, a_ct, a_f, b_ct;  // elements
 };
 
 template <typename CT, int CP, int D, int H>
@@ -1250,7 +1246,7 @@ SplitSizes split_sizes(int units, int nch) {
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const size_t t = (size_t)units * nch;
   return SplitSizes{t * Y.rc.n, t * Y.rf.n, (size_t)SPLIT_GRID_A * Y.ac.n, (size_t)SPLIT_GRID_A * Y.af.n,
-                    (size_t)units * Y.bc.n, (size_t)units * Y.bf.n};
+                    (size_t)units * Y.bc.n};
 }
 
 size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1258,7 +1254,7 @@ size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 template <typename CT>
 size_t total_bytes(const SplitSizes& z) {
   return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) + up256(z.a_ct * sizeof(CT)) +
-         up256(z.a_f * 4) + up256(z.b_ct * sizeof(CT)) + up256(z.b_f * 4);
+         up256(z.a_f * 4) + up256(z.b_ct * sizeof(CT));
 }
 
 template <typename CT>
@@ -1269,8 +1265,7 @@ SplitPtrs carve(void* ws, const SplitSizes& z, int units) {
   P.rec_f = (float*)p; p += up256(z.rec_f * 4);
   P.tmpA = p; p += up256(z.a_ct * sizeof(CT));
   P.tmpA_f = (float*)p; p += up256(z.a_f * 4);
-  P.tmpB = p; p += up256(z.b_ct * sizeof(CT));
-  P.tmpB_f = (float*)p;
+  P.tmpB = p;
   P.units = units;
   return P;
 }
