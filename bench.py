@@ -86,7 +86,7 @@ def launch_flops(cfg, name):
 TRAFFIC_FILE = {2: "hbm_traffic_pretrain_B4H8L8192.txt"}
 _COMMON = ["tnt_device.h", "tnt_kernels.h"]
 LAUNCH_SOURCES = {
-    "local_bwd": ["tnt_local_bwd_blk.hip", "tnt_local_bwd_layout.h", "tnt_local_common.h"] + _COMMON,
+    "local_bwd": ["tnt_local_bwd_split.hip", "tnt_local_bwd_helpers.h", "tnt_local_common.h"] + _COMMON,
     "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_common.h"] + _COMMON,
     "global_bwd_chunk": ["tnt_global_bwd.hip", "tnt_global_blk.hip"] + _COMMON,
     "global_fwd_chunk": ["tnt_global_fwd.hip", "tnt_global_blk.hip"] + _COMMON,
@@ -121,8 +121,8 @@ def measured_traffic(workload, label):
 # ----------------------------------------------------------------------------
 def cpu_baseline(cfg, inp, budget_tokens):
     """fp64 oracle, fwd + bwd, on one (batch 0, head 0) chain restricted to its
-    first `budget_tokens` tokens (one local shard and one global chunk at the
-    default workload)."""
+    first `budget_tokens` tokens (the whole 8192-token chain, four local shards
+    and four global chunks, at the default workload)."""
     import torch
     import oracle as O
 
@@ -151,7 +151,8 @@ def main():
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=0,
-                    help="tokens of the CPU-oracle sample (default: one local shard)")
+                    help="tokens of the CPU-oracle sample (default: one chain, at most "
+                         "four local shards)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the warmup (the "
                          "reference dispatch that scales HBM traffic counters)")
@@ -251,7 +252,8 @@ def main():
         "kernels_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())},
     }
     if not args.no_cpu_baseline:
-        ctoks = args.cpu_tokens or (cfg.locals_[0][1] if cfg.locals_ else cfg.C_G)
+        unit = cfg.locals_[0][1] if cfg.locals_ else cfg.C_G
+        ctoks = args.cpu_tokens or min(cfg.L, 4 * unit)
         res["cpu_baseline"] = cpu_baseline(cfg, inp, ctoks)
     print(json.dumps(res), flush=True)
 
