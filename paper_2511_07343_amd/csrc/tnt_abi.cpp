@@ -229,7 +229,7 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
 // threads serialise their enqueues here.
 struct Fork {
   hipStream_t side = nullptr;
-  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr;
 };
 constexpr int MAX_DEV = 64;
 Fork g_fork[MAX_DEV];
@@ -245,6 +245,7 @@ hipError_t fork_of(Fork** out) {
     if ((e = hipStreamCreateWithFlags(&f.side, hipStreamNonBlocking)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.e0, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.e1, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.ea, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &f;
   return hipSuccess;
@@ -334,17 +335,46 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
   float* dqp = dparts;
   float* dkp = dparts + (size_t)y.M * y.io_elems;
   float* dvp = dparts + 2 * (size_t)y.M * y.io_elems;
-  int m = 0;
   std::unique_lock<std::mutex> lock(g_fork_mu);
   Fork* fk = nullptr;
   const hipStream_t main_st = st;
-  if (c->has_global && c->n_local) {
-    HIP_TRY(fork_of(&fk));
-    HIP_TRY(hipEventRecord(fk->e0, main_st));
-    HIP_TRY(hipStreamWaitEvent(fk->side, fk->e0, 0));
-    st = fk->side;
+  // The local memories go first on the caller's stream; the global chain runs on
+  // the helper stream from the moment the first local memory's chunk-parallel
+  // pass is done (that pass fills the chip; the walk after it leaves half the
+  // CUs to the global chain).
+  if (c->has_global && c->n_local) HIP_TRY(fork_of(&fk));
+  for (int i = 0, m = c->has_global; i < c->n_local; ++i, ++m) {
+    LocalBwdArgs a{};
+    a.q = q; a.k = k; a.v = v; a.dO = dO;
+    a.lr = lr + m * G; a.mom = mom + m * G; a.decay = decay + m * G;
+    a.states = (const float*)(sv + y.sv_l[i]);
+    a.mstates = (const float*)(sv + y.sv_m[i]);
+    a.nslots = y.l_chunks[i] + 1;
+    a.statesT = sv + y.sv_t[i];
+    a.adj = (float*)(ws + y.b_adj_l[i]);
+    a.madj = (float*)(ws + y.b_madj[i]);
+    a.dq_part = dqp + (size_t)m * y.io_elems;
+    a.dk_part = dkp + (size_t)m * y.io_elems;
+    a.dv_part = dvp + (size_t)m * y.io_elems;
+    a.dlr = dlr + m * G; a.dmom = dmom + m * G; a.ddecay = ddecay + m * G;
+    a.dWinit_part = (float*)(ws + y.b_dWl[i]);
+    a.scratch = ws + y.b_scr[i];
+    a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
+    a.split_ws = y.b_split[i] != SIZE_MAX ? (void*)(ws + y.b_split[i]) : nullptr;
+    a.single_walk = single_walk_only();
+    a.D = dims_of(c, c->C_L[i], c->S_L[i]);
+    a.force_generic = generic_only();
+    a.pass_a_done = (fk && i == 0) ? fk->ea : nullptr;
+    HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
+    HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
+                               dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
+                               c->d, c->hid, 0, st));
   }
   if (c->has_global) {
+    if (fk) {
+      HIP_TRY(hipStreamWaitEvent(fk->side, fk->ea, 0));
+      st = fk->side;
+    }
     GlobalArgs g{};
     g.q = q; g.k = k; g.v = v; g.dO = dO;
     g.lr = lr; g.mom = mom; g.decay = decay;
@@ -374,35 +404,8 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TIMED("global_bwd_chunk", launch_global_bwd_chunk(g, n, st));
     HIP_TIMED("global_gate_bwd", launch_global_gate_bwd(g, st));
     HIP_TIMED("reduce_init", launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
-    m = 1;
   }
   st = main_st;
-  for (int i = 0; i < c->n_local; ++i, ++m) {
-    LocalBwdArgs a{};
-    a.q = q; a.k = k; a.v = v; a.dO = dO;
-    a.lr = lr + m * G; a.mom = mom + m * G; a.decay = decay + m * G;
-    a.states = (const float*)(sv + y.sv_l[i]);
-    a.mstates = (const float*)(sv + y.sv_m[i]);
-    a.nslots = y.l_chunks[i] + 1;
-    a.statesT = sv + y.sv_t[i];
-    a.adj = (float*)(ws + y.b_adj_l[i]);
-    a.madj = (float*)(ws + y.b_madj[i]);
-    a.dq_part = dqp + (size_t)m * y.io_elems;
-    a.dk_part = dkp + (size_t)m * y.io_elems;
-    a.dv_part = dvp + (size_t)m * y.io_elems;
-    a.dlr = dlr + m * G; a.dmom = dmom + m * G; a.ddecay = ddecay + m * G;
-    a.dWinit_part = (float*)(ws + y.b_dWl[i]);
-    a.scratch = ws + y.b_scr[i];
-    a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
-    a.split_ws = y.b_split[i] != SIZE_MAX ? (void*)(ws + y.b_split[i]) : nullptr;
-    a.single_walk = single_walk_only();
-    a.D = dims_of(c, c->C_L[i], c->S_L[i]);
-    a.force_generic = generic_only();
-    HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
-    HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
-                               dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
-                               c->d, c->hid, 0, st));
-  }
   if (fk) {
     HIP_TRY(hipEventRecord(fk->e1, fk->side));
     HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));

@@ -67,6 +67,9 @@ struct LocalBwdArgs {
   void* split_ws;                                        // null, or local_bwd_split_bytes(D, units)
                                                          // bytes for the three-pass fixed-size kernels
   int single_walk;                                       // 1: the one-walk fixed-size kernel
+  hipEvent_t pass_a_done;                                // null, or recorded on the stream once the
+                                                         // chunk-parallel pass is done (at once when
+                                                         // the backward has no such pass)
   int force_generic;                                     // 1: skip fixed-size kernels
 };
 

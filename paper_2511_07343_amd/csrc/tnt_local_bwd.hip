@@ -590,6 +590,10 @@ static bool try_bwd(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st) {
   hipError_t e = hipSuccess;
   if (!a.force_generic && !a.single_walk && launch_local_bwd_split(a, units, st, &e)) return e;
+  if (a.pass_a_done) {
+    e = hipEventRecord(a.pass_a_done, st);
+    if (e != hipSuccess) return e;
+  }
   if (!a.force_generic && launch_local_bwd_blk(a, units, st, &e)) return e;
   if (a.D.bf16) {
     if (try_bwd<__bf16, __bf16, ACT_GELU, 0, 0, 0>(a, units, st, &e) ||

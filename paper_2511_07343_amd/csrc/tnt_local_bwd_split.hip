@@ -1296,6 +1296,7 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, D, H>(),
                    lds_c = split_c_lds<CP, D>();
   hipLaunchKernelGGL(ka, dim3(std::min(total, SPLIT_GRID_A)), dim3(512), lds_a, st, *a, P);
+  if (a->pass_a_done) hipEventRecord(a->pass_a_done, st);
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
   if (Dm.qk_proj && Dm.qk_scope == 0) {
     const size_t thr = (size_t)units * D * D;
