@@ -67,7 +67,8 @@ struct Layout {
   size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], sv_t[TNT_MAX_LOCAL], saved_bytes;
   int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
   // forward workspace
-  size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL], w_ring,
+  size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL],
+      w_fsplit[TNT_MAX_LOCAL], w_ring,
       fwd_bytes;
   size_t ring_g, ring_l[TNT_MAX_LOCAL], ring_m[TNT_MAX_LOCAL];
   LocalPlan lplan[TNT_MAX_LOCAL];
@@ -127,6 +128,9 @@ Layout layout_of(const tnt_config* c) {
     const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
     local_plan(D, &y.lplan[i], false);
     y.w_scr[i] = off; off += up((size_t)y.l_units[i] * y.lplan[i].elems * cts);
+    const size_t fb = local_fwd_split_bytes(D, y.l_units[i]);
+    y.w_fsplit[i] = fb ? off : SIZE_MAX;
+    off += up(fb);
   }
   const size_t fwd_core = off;
   // two-slot state rings, used when no saved buffer is given
@@ -312,6 +316,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.statesT = sv ? (void*)(sv + y.sv_t[i]) : nullptr;
     a.nslots = sv ? y.l_chunks[i] + 1 : 2;
     a.scratch = ws + y.w_scr[i];
+    a.fsplit = y.w_fsplit[i] != SIZE_MAX ? (void*)(ws + y.w_fsplit[i]) : nullptr;
     a.plan = y.lplan[i];
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
     a.force_generic = generic_only();

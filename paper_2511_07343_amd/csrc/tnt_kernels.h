@@ -40,6 +40,8 @@ struct LocalFwdArgs {
   float* mstates;                                        // [units][nslots][d*d]
   void* statesT;                                         // null, or CT [units][nslots][4*hid*d + d*d]:
                                                          // W1^T, W2^T, S1^T, S2^T, M^T of every slot
+  void* fsplit;                                          // null, or local_fwd_split_bytes(D, units)
+                                                         // bytes: the split forward (saved states only)
   int nslots;
   void* scratch;                                         // units * plan.elems CT
   LocalPlan plan;
@@ -113,6 +115,7 @@ inline void set_lds_limit(const void* fn) {
 size_t local_plan(const Dims& D, LocalPlan* p, bool backward);
 
 hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st);
+size_t local_fwd_split_bytes(const Dims& D, int units);  // 0: no fixed-size forward for D
 bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err);
 hipError_t launch_pack_states(const float* states, const float* mstates, void* out, int units,
                                int nslots, int d, int hid, int with_m, int bf16, hipStream_t st);

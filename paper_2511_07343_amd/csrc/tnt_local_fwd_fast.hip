@@ -101,8 +101,23 @@ constexpr size_t fwd_fast_lds_bytes() {
   return (size_t)FwdLds<D, HID, CP>::total * sizeof(CT);
 }
 
-template <typename IO, typename CT, int ACT, int D, int HID, int CP>
+// Modes of the kernel.  FWD_FULL: one workgroup per unit walks its chunks and
+// does everything.  When every chunk-entry state is saved, the walk is split:
+// FWD_CHAIN walks the chunks doing only what the next state needs (keys, the
+// chunk gradient, the carry, the Q-K sum) and leaves Hk, D1^T and R of every
+// chunk in a buffer; FWD_RET then takes the retrieval of every (unit, chunk) at
+// once, one workgroup each, from the saved entry state and that buffer.
+enum { FWD_FULL = 0, FWD_CHAIN = 1, FWD_RET = 2 };
+
+// per-chunk buffer of the split forward: Hk [CP][HID], D1^T [HID][CP], R [CP][D]
+template <int D, int HID, int CP>
+constexpr size_t fwd_split_elems() {
+  return 2 * (size_t)CP * HID + (size_t)CP * D;
+}
+
+template <typename IO, typename CT, int ACT, int D, int HID, int CP, int MODE>
 __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
+  constexpr bool WALK = MODE != FWD_RET, RETR = MODE != FWD_CHAIN;
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ CoefF cf;
   using Ly = FwdLds<D, HID, CP>;
@@ -114,6 +129,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   static_assert(NW % (D / 16) == 0, "one column strip of D per wave");
   static_assert((HID / 16) * (D / 16) % NW == 0, "state tiles spread evenly over waves");
   static_assert((size_t)HID * D % (512 * 4) == 0, "W2 copy in whole float4s per thread");
+  static_assert(sizeof(CT) == 2, "the fixed-size forward computes in bf16");
   CT* L = (CT*)smem;
   CT *sHk = L + Ly::Hk, *sD1 = L + Ly::D1, *sU = L + Ly::U, *sX = L + Ly::X, *sK = L + Ly::K,
      *sR = L + Ly::R, *sP = L + Ly::P;
@@ -124,7 +140,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const Dims Dm = a.D;
   const int C = Dm.C;
   const int nshard = Dm.L / Dm.S;
-  const int u = blockIdx.x;
+  const int nch = Dm.S / C;
+  const int u = MODE == FWD_RET ? (int)blockIdx.x / nch : (int)blockIdx.x;
   const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
   constexpr size_t hd = (size_t)HID * D;
   const size_t chain = (size_t)b * Dm.H + hh;
@@ -144,8 +161,9 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const float rscale = 2.0f / (float)D;
   const int l = lane_id(), w = wave_id();
   const int ko = Mma<CT>::kofs(l);
+  constexpr size_t FS = fwd_split_elems<D, HID, CP>();
 
-  {
+  if (WALK) {
     const float* W1i = a.W1i + hh * hd;
     const float* W2i = a.W2i + hh * hd;
     for (int e = threadIdx.x * 4; e < (int)hd; e += blockDim.x * 4) {
@@ -172,8 +190,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   }
   __syncthreads();
 
-  const int nch = Dm.S / C;
-  for (int n = 0; n < nch; ++n) {
+  const int n_begin = MODE == FWD_RET ? (int)blockIdx.x % nch : 0;
+  const int n_end = MODE == FWD_RET ? n_begin + 1 : nch;
+  for (int n = n_begin; n < n_end; ++n) {
+    CT* const fsn = (MODE == FWD_FULL) ? nullptr : (CT*)a.fsplit + ((size_t)u * nch + n) * FS;
     const int tok0 = s * Dm.S + n * C;
     const float* cur = st + (size_t)(n % a.nslots) * 4 * hd;
     float* nxt = st + (size_t)((n + 1) % a.nslots) * 4 * hd;
@@ -193,12 +213,15 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           const IO* pk = k + (size_t)tok0 * D + e;
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
-            sQ[e + j] = from_f<CT>(to_f(pq[j]));
+            if (RETR) sQ[e + j] = from_f<CT>(to_f(pq[j]));
             sK[e + j] = from_f<CT>(to_f(pk[j]));
           }
         } else {
 #pragma unroll
-          for (int j = 0; j < VEC; ++j) sQ[e + j] = sK[e + j] = from_f<CT>(0.f);
+          for (int j = 0; j < VEC; ++j) {
+            if (RETR) sQ[e + j] = from_f<CT>(0.f);
+            sK[e + j] = from_f<CT>(0.f);
+          }
         }
       }
     }
@@ -222,6 +245,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         sNT[(size_t)j * CP + i] = from_f<CT>(x);
       }
       __syncthreads();
+      if (RETR) {
       gemm<CT, KC, KC>(CP, CP, D, sQ, D, sN, D, [&](int i, int j, float x) {
         sS[(size_t)i * CP + j] = from_f<CT>(j <= i ? x : 0.f);
       });
@@ -248,7 +272,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           tile_each(acc, i0, j0, [&](int i, int j, float x) { sX[(size_t)i * D + j] = from_f<CT>(x); });
         }
       }
-      if (shard_qk) {
+      }
+      if (WALK && shard_qk) {
         constexpr int tn = D / 16, nt = tn * tn;
         for (int t = w; t < nt; t += NW) {
           const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
@@ -265,10 +290,23 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           if (pkn) store4<CT>(pkn + 4 * hd + (size_t)(j0 + (l & 15)) * D + i0 + 4 * (l >> 4), acc);
         }
       }
-    } else {
+    } else if (RETR) {
       for (int e = threadIdx.x; e < CP * D; e += blockDim.x) sX[e] = sQ[e];
     }
 
+    if constexpr (MODE == FWD_RET) {
+      // Hk, D1^T, R of this chunk, left by the walk
+      constexpr int V8 = 16 / sizeof(CT);
+      for (size_t e = threadIdx.x * V8; e < FS; e += blockDim.x * V8) {
+        const bf16x8 x = *reinterpret_cast<const bf16x8*>(fsn + e);
+        CT* dst = e < (size_t)CP * HID ? sHk + e
+                  : e < 2 * (size_t)CP * HID ? sD1 + (e - (size_t)CP * HID)
+                                             : sR + (e - 2 * (size_t)CP * HID);
+        *reinterpret_cast<bf16x8*>(dst) = x;
+      }
+      __syncthreads();
+    }
+    if constexpr (WALK) {
     // ---- Zk = K W1^T -> Hk (LDS), s'(Zk) (registers); each wave owns NS column strips
     CT spr[NS][TMC][4];  // s'(Zk) in the compute type
     {
@@ -385,6 +423,15 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       sRT[(size_t)j * CP + i] = sR[e];
     }
     __syncthreads();
+    if constexpr (MODE == FWD_CHAIN) {
+      // Hk, D1^T, R for the retrieval pass (LDS reads only; overlaps the carry)
+      for (size_t e = threadIdx.x * 8; e < FS; e += blockDim.x * 8) {
+        const CT* src = e < (size_t)CP * HID ? sHk + e
+                        : e < 2 * (size_t)CP * HID ? sD1 + (e - (size_t)CP * HID)
+                                                   : sR + (e - 2 * (size_t)CP * HID);
+        *reinterpret_cast<bf16x8*>(fsn + e) = *reinterpret_cast<const bf16x8*>(src);
+      }
+    }
     {
       constexpr int tn = D / 16, nt = (HID / 16) * tn;  // W1', S1' : HID x D
       constexpr int PT = nt / NW, BT = PT < 4 ? PT : 4;
@@ -472,7 +519,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       }
     }
 
+    }  // WALK
+
     // ---- retrieval, dual form
+    if constexpr (RETR) {
     {
       constexpr int tn = CP / 16, nt = TMC * tn;
       for (int t = w; t < nt; t += NW) {
@@ -597,32 +647,61 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         }
       }
     }
+    }  // RETR
     __syncthreads();
   }
 }
 
 template <typename IO, typename CT, int ACT, int D, int HID, int CP>
-static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err) {
+static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err, size_t* bytes) {
   if (a.D.d != D || a.D.hid != HID || a.D.Cp != CP || a.D.act != ACT) return false;
   constexpr size_t lds = fwd_fast_lds_bytes<CT, D, HID, CP>();
   if (lds + sizeof(CoefF) > 160 * 1024) return false;
-  auto kern = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP>;
-  set_lds_limit((const void*)kern);
-  hipLaunchKernelGGL(kern, dim3(units), dim3(512), lds, st, a);
+  const int nch = a.D.S / a.D.C;
+  if (bytes) {  // size query: the split forward's per-chunk buffer
+    *bytes = (size_t)units * nch * fwd_split_elems<D, HID, CP>() * sizeof(CT);
+    return true;
+  }
+  if (a.fsplit && a.statesT && a.nslots > nch) {
+    auto kc = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
+    auto kr = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
+    set_lds_limit((const void*)kc);
+    set_lds_limit((const void*)kr);
+    hipLaunchKernelGGL(kc, dim3(units), dim3(512), lds, st, a);
+    hipLaunchKernelGGL(kr, dim3(units * nch), dim3(512), lds, st, a);
+  } else {
+    auto kern = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_FULL>;
+    set_lds_limit((const void*)kern);
+    hipLaunchKernelGGL(kern, dim3(units), dim3(512), lds, st, a);
+  }
   *err = hipGetLastError();
   return true;
 }
 
-// Returns true (and the launch status) when a fixed-size kernel handles `a`.
-bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err) {
+static bool dispatch_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err,
+                          size_t* bytes) {
   if (a.D.bf16) {
-    return try_fast<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, units, st, err) ||
-           try_fast<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, units, st, err) ||
-           try_fast<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, units, st, err) ||
-           try_fast<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, units, st, err) ||
-           try_fast<__bf16, __bf16, ACT_GELU, 64, 256, 16>(a, units, st, err);
+    return try_fast<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, units, st, err, bytes) ||
+           try_fast<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, units, st, err, bytes) ||
+           try_fast<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, units, st, err, bytes) ||
+           try_fast<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, units, st, err, bytes) ||
+           try_fast<__bf16, __bf16, ACT_GELU, 64, 256, 16>(a, units, st, err, bytes);
   }
   return false;  // fp32 shapes (the tiny smoke workload) take the runtime-sized kernel
+}
+
+// Returns true (and the launch status) when a fixed-size kernel handles `a`.
+bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err) {
+  return dispatch_fast(a, units, st, err, nullptr);
+}
+
+// Bytes of the per-chunk buffer of the split forward (0: no fixed-size kernel for D).
+size_t local_fwd_split_bytes(const Dims& D, int units) {
+  LocalFwdArgs a{};
+  a.D = D;
+  size_t bytes = 0;
+  hipError_t e = hipSuccess;
+  return dispatch_fast(a, units, nullptr, &e, &bytes) ? bytes : 0;
 }
 
 }  // namespace tnt

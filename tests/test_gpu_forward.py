@@ -67,9 +67,20 @@ def test_forward_small_all_chains(cfg):
         assert e2 <= tol(cfg)
 
 
-def test_forward_save_and_ring_agree():
-    """The saved-state path and the two-slot ring path give identical outputs."""
-    cfg = SMALL[0]
+SAVE_RING = [
+    SMALL[0], SMALL[2],
+    small_config(BF16, ACT_SILU, B=1, H=2, L=256, d=64, hid=256, C_G=128, locals_=((64, 128),),
+                 name="bf16 d64 h256 C64"),
+    small_config(BF16, ACT_SILU, B=1, H=1, L=192, d=64, hid=256, C_G=96, locals_=((48, 96),),
+                 qk_scope=QK_CHUNK, name="bf16 C48 ragged chunk-scope QK"),
+]
+
+
+@pytest.mark.parametrize("cfg", SAVE_RING, ids=lambda c: c.name)
+def test_forward_save_and_ring_agree(cfg):
+    """The saved-state path and the two-slot ring path give identical outputs
+    (for the fixed-size bf16 kernels: the walk plus the chunk-parallel retrieval
+    against the one-walk kernel)."""
     inp = make_inputs(cfg, 102)
     a, _ = gpu_forward(cfg, inp, save=True)
     b, _ = gpu_forward(cfg, inp, save=False)
