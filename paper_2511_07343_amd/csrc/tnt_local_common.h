@@ -27,8 +27,47 @@ struct Coef {
   float red[32];
 };
 
+// Columns of the coefficient matrix, one prefix affine scan over the rows
+// (lanes) per column tau, the columns dealt to the waves:
+//   ct_{r,tau} = e^{la_r - la_{r-1}} ct_{r-1,tau} + e^{lb_r - lb_tau}  (r >= tau),
+//   ct_{r,tau} = 0 (r < tau), c = eta_tau ct.  Every multiplier and term is at most 1.
+// Wave 0 also scans E_i = e^{la_i - la_{i-1}} E_{i-1} + e^{lb_i}.  The prefix
+// arrays la, lb, eta must be in LDS.  No barrier.
+__device__ __forceinline__ void affine_scan_up(float& a, float& b) {  // inclusive, over lanes
+  const int r = lane_id();
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    const float pa = __shfl_up(a, o, WAVE), pb = __shfl_up(b, o, WAVE);
+    if (r >= o) {
+      b = a * pb + b;
+      a = a * pa;
+    }
+  }
+}
+template <int STRIDE>
+__device__ __forceinline__ void coef_columns(const float* la, const float* lb, const float* eta,
+                                             int Cp, float (*ct)[STRIDE], float (*c)[STRIDE],
+                                             float* E) {
+  const int r = lane_id();
+  const float lar = la[r < Cp ? r : Cp - 1], lbr = lb[r < Cp ? r : Cp - 1];
+  const float ar = r > 0 && r < Cp ? expf(lar - la[r - 1]) : 0.f;
+  for (int tau = wave_id(); tau < Cp; tau += num_waves()) {
+    float a = ar, b = (r >= tau && r < Cp) ? expf(lbr - lb[tau]) : 0.f;
+    affine_scan_up(a, b);
+    if (r < Cp) {
+      if (ct) ct[r][tau] = b;
+      c[r][tau] = eta[tau] * b;
+    }
+  }
+  if (wave_id() == 0) {
+    float a = ar, b = r < Cp ? expf(lbr) : 0.f;
+    affine_scan_up(a, b);
+    if (r < Cp) E[r] = b;
+  }
+}
+
 // Fill `cf` for the chunk whose first token is `tok0` (gate arrays already
-// offset to the chain).  All threads call; wave 0 computes.  Ends with a barrier.
+// offset to the chain).  All threads call.  Ends with a barrier.
 __device__ __forceinline__ void chunk_coefs(Coef& cf, const float* lr, const float* mom,
                                             const float* dec, int tok0, int C, int Cp) {
   if (wave_id() == 0) {
@@ -45,26 +84,7 @@ __device__ __forceinline__ void chunk_coefs(Coef& cf, const float* lr, const flo
     cf.A[i] = expf(la);
   }
   __syncthreads();
-  if (wave_id() == 0) {
-    const int i = lane_id();
-    if (i < Cp) {
-      float e = 0.f;
-      for (int m = 0; m <= i; ++m) e += expf(cf.la[i] - cf.la[m] + cf.lb[m]);
-      cf.E[i] = e;
-      // column tau = i of ct / c by the recursion over rows
-      const int tau = i;
-      const float lbt = cf.lb[tau];
-      for (int r = 0; r < tau; ++r) { cf.ct[r][tau] = 0.f; cf.c[r][tau] = 0.f; }
-      float x = 1.0f;
-      cf.ct[tau][tau] = x;
-      cf.c[tau][tau] = cf.eta[tau] * x;
-      for (int r = tau + 1; r < Cp; ++r) {
-        x = expf(cf.la[r] - cf.la[r - 1]) * x + expf(cf.lb[r] - lbt);
-        cf.ct[r][tau] = x;
-        cf.c[r][tau] = cf.eta[tau] * x;
-      }
-    }
-  }
+  coef_columns(cf.la, cf.lb, cf.eta, Cp, cf.ct, cf.c, cf.E);
   __syncthreads();
   if (wave_id() == 0) {
     const int tau = lane_id();

@@ -45,23 +45,7 @@ __device__ __forceinline__ void chunk_coefs_f(CoefF& cf, const float* lr, const 
     cf.A[i] = expf(la);
   }
   __syncthreads();
-  if (wave_id() == 0) {
-    const int i = lane_id();
-    if (i < Cp) {
-      float e = 0.f;
-      for (int m = 0; m <= i; ++m) e += expf(cf.la[i] - cf.la[m] + cf.lb[m]);
-      cf.E[i] = e;
-      const int tau = i;
-      const float lbt = cf.lb[tau];
-      for (int r = 0; r < tau; ++r) cf.c[r][tau] = 0.f;
-      float x = 1.0f;
-      cf.c[tau][tau] = cf.eta[tau];
-      for (int r = tau + 1; r < Cp; ++r) {
-        x = expf(cf.la[r] - cf.la[r - 1]) * x + expf(cf.lb[r] - lbt);
-        cf.c[r][tau] = cf.eta[tau] * x;
-      }
-    }
-  }
+  coef_columns<MAXC + 1>(cf.la, cf.lb, cf.eta, Cp, nullptr, cf.c, cf.E);
   __syncthreads();
   if (wave_id() == 0) {
     const int tau = lane_id();
