@@ -416,9 +416,11 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
   }
   const int bf = c->dtype == TNT_BF16;
-  HIP_TIMED("sum_grads", launch_sum_out(dqp, y.M, y.io_elems, y.io_elems, dq, bf, st));
-  HIP_TIMED("sum_grads", launch_sum_out(dkp, y.M, y.io_elems, y.io_elems, dk, bf, st));
-  HIP_TIMED("sum_grads", launch_sum_out(dvp, y.M, y.io_elems, y.io_elems, dv, bf, st));
+  SumJobs jobs{};
+  jobs.parts[0] = dqp; jobs.out[0] = dq;
+  jobs.parts[1] = dkp; jobs.out[1] = dk;
+  jobs.parts[2] = dvp; jobs.out[2] = dv;
+  HIP_TIMED("sum_grads", launch_sum_outs(jobs, 3, y.M, y.io_elems, y.io_elems, bf, st));
   return TNT_OK;
 }
 

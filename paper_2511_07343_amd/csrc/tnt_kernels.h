@@ -140,6 +140,12 @@ bool launch_global_bwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_
 int global_bwd_splits(const Dims& D);
 constexpr int GRED_BLOCKS = 16;  // blocks per chain of the split reductions
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
+struct SumJobs {  // up to three (partials, output) pairs summed by one launch
+  const float* parts[3];
+  void* out[3];
+};
+hipError_t launch_sum_outs(const SumJobs& jobs, int njobs, int nparts, size_t stride, size_t n,
+                           int bf16, hipStream_t st);
 hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
                           int bf16, hipStream_t st);
 hipError_t launch_reduce_init(const float* parts, int B, int H, int nshard, size_t hd2,

@@ -228,18 +228,23 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     float* Mn = mst + (size_t)((n + 1) % a.nslots) * D * D;
     CT* const pkn = pku ? pku + (size_t)((n + 1) % a.nslots) * PS : nullptr;
 
-    // ---- stage Q, K (16-byte loads; rows >= C zero), gate coefficients
+    // ---- stage Q, K (16-byte loads; rows >= C zero), key norms, gate coefficients
     {
-      constexpr int VEC = 16 / sizeof(IO);
+      constexpr int VEC = 16 / sizeof(IO), LPR = D / VEC;  // lanes per row
+      static_assert(LPR >= 1 && LPR <= WAVE && (LPR & (LPR - 1)) == 0, "rows within one wave");
+      static_assert((CP * D / VEC) % WAVE == 0, "whole waves stage");
       for (int e = threadIdx.x * VEC; e < CP * D; e += blockDim.x * VEC) {
         const int i = e / D;
+        float ss = 0.f;
         if (i < C) {
           const IO* pq = q + (size_t)tok0 * D + e;
           const IO* pk = k + (size_t)tok0 * D + e;
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
             if (RETR) sQ[e + j] = from_f<CT>(to_f(pq[j]));
-            sK[e + j] = from_f<CT>(to_f(pk[j]));
+            const CT kv = from_f<CT>(to_f(pk[j]));
+            sK[e + j] = kv;
+            ss += to_f(kv) * to_f(kv);
           }
         } else {
 #pragma unroll
@@ -248,21 +253,14 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             sK[e + j] = from_f<CT>(0.f);
           }
         }
+#pragma unroll
+        for (int o = 1; o < LPR; o <<= 1) ss += __shfl_xor(ss, o, WAVE);
+        if ((threadIdx.x & (LPR - 1)) == 0) cf.knorm[i] = sqrtf(ss);  // visible after the coefficients' barrier
       }
     }
     if (RETR) chunk_coefs_f(cf, lr, mom, dec, tok0, C, CP);  // barriers inside (K staged)
     if (WALK) carry_coefs(cf, lr, mom, dec, tok0, C, CP);
     if (qk) {
-      for (int i = w; i < CP; i += NW) {  // key norms from LDS
-        float ss = 0.f;
-        for (int j = l; j < D; j += WAVE) {
-          const float x = to_f(sK[(size_t)i * D + j]);
-          ss += x * x;
-        }
-        ss = wave_sum(ss);
-        if (l == 0) cf.knorm[i] = sqrtf(ss);
-      }
-      __syncthreads();
       for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
         const int i = e / D, j = e - i * D;
         const float nr = cf.knorm[i];
