@@ -22,47 +22,6 @@
 
 namespace tnt {
 
-struct CoefF {  // forward-only gate coefficients (no ct)
-  float c[MAXC][MAXC + 1];
-  float A[MAXC], E[MAXC], la[MAXC], lb[MAXC], eta[MAXC], cC[MAXC], bb[MAXC];
-  float knorm[MAXC];
-  float AC, BC, EC;
-};
-
-__device__ __forceinline__ void chunk_coefs_f(CoefF& cf, const float* lr, const float* mom,
-                                              const float* dec, int tok0, int C, int Cp) {
-  if (wave_id() == 0) {
-    const int i = lane_id();
-    const bool in = i < C;
-    const float eta = in ? lr[tok0 + i] : 0.f;
-    const float lmb = in ? log_mom(mom[tok0 + i]) : 0.f;
-    const float lka = in ? log_keep(dec[tok0 + i]) : 0.f;
-    const float la = wave_incl_sum(lka);
-    const float lb = wave_incl_sum(lmb);
-    cf.la[i] = la;
-    cf.lb[i] = lb;
-    cf.eta[i] = eta;
-    cf.A[i] = expf(la);
-  }
-  __syncthreads();
-  coef_columns<MAXC + 1>(cf.la, cf.lb, cf.eta, Cp, nullptr, cf.c, cf.E);
-  __syncthreads();
-  if (wave_id() == 0) {
-    const int tau = lane_id();
-    if (tau < Cp) {
-      const float et = (tau < C) ? expf(cf.lb[C - 1] - cf.lb[tau]) : 0.f;
-      cf.bb[tau] = cf.eta[tau] * et;
-      cf.cC[tau] = cf.c[C - 1][tau];
-    }
-    if (tau == 0) {
-      cf.AC = cf.A[C - 1];
-      cf.BC = expf(cf.lb[C - 1]);
-      cf.EC = cf.E[C - 1];
-    }
-  }
-  __syncthreads();
-}
-
 // The carry's coefficients only (cC, b, A_C, B_C, E_C), without the C x C
 // matrix: cC_t = eta_t y_t with y_t = sum_{m >= t} e^{(la_C - la_m) + (lb_m - lb_t)}
 // obeys y_t = e^{la_C - la_t} + e^{lb_{t+1} - lb_t} y_{t+1}, a suffix affine scan
