@@ -13,6 +13,7 @@
 #include "../../include/tnt.h"
 #include "tnt_kernels.h"
 #include "tnt_local_bwd_layout.h"
+#include "tnt_local_record.h"
 
 using namespace tnt;
 
@@ -64,7 +65,8 @@ struct Layout {
   int M, BH;
   size_t hd, io_elems, gates;
   // saved (or workspace-resident) chunk states
-  size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], sv_t[TNT_MAX_LOCAL], saved_bytes;
+  size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], sv_t[TNT_MAX_LOCAL],
+      sv_fr[TNT_MAX_LOCAL], sv_frf[TNT_MAX_LOCAL], saved_bytes;
   int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
   // forward workspace
   size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL],
@@ -107,6 +109,15 @@ Layout layout_of(const tnt_config* c) {
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * dd * f);
     y.sv_t[i] = off;  // CT transposes of every slot, written by the forward
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * (4 * y.hd + dd) * cts);
+    // forward records of the chunk-parallel passes (shapes with both split kernels)
+    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+    y.sv_fr[i] = y.sv_frf[i] = SIZE_MAX;
+    if (local_fwd_split_bytes(D, y.l_units[i]) && local_bwd_split_bytes(D, y.l_units[i])) {
+      const rec::RecLayout R = rec::make_rec_layout(D.Cp, D.d, D.hid);
+      const size_t items = (size_t)y.l_units[i] * y.l_chunks[i];
+      y.sv_fr[i] = off; off += up(items * R.fc.n * cts);
+      y.sv_frf[i] = off; off += up(items * R.ff.n * f);
+    }
   }
   y.saved_bytes = off;
 
@@ -314,6 +325,8 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.states = sv ? (float*)(sv + y.sv_l[i]) : (float*)(ws + y.ring_l[i]);
     a.mstates = sv ? (float*)(sv + y.sv_m[i]) : (float*)(ws + y.ring_m[i]);
     a.statesT = sv ? (void*)(sv + y.sv_t[i]) : nullptr;
+    a.frec = (sv && y.sv_fr[i] != SIZE_MAX) ? (void*)(sv + y.sv_fr[i]) : nullptr;
+    a.frec_f = (sv && y.sv_frf[i] != SIZE_MAX) ? (float*)(sv + y.sv_frf[i]) : nullptr;
     a.nslots = sv ? y.l_chunks[i] + 1 : 2;
     a.scratch = ws + y.w_scr[i];
     a.fsplit = y.w_fsplit[i] != SIZE_MAX ? (void*)(ws + y.w_fsplit[i]) : nullptr;
@@ -356,6 +369,8 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.mstates = (const float*)(sv + y.sv_m[i]);
     a.nslots = y.l_chunks[i] + 1;
     a.statesT = sv + y.sv_t[i];
+    a.frec = y.sv_fr[i] != SIZE_MAX ? (const void*)(sv + y.sv_fr[i]) : nullptr;
+    a.frec_f = y.sv_frf[i] != SIZE_MAX ? (const float*)(sv + y.sv_frf[i]) : nullptr;
     a.adj = (float*)(ws + y.b_adj_l[i]);
     a.madj = (float*)(ws + y.b_madj[i]);
     a.dq_part = dqp + (size_t)m * y.io_elems;

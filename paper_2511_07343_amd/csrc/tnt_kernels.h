@@ -42,6 +42,8 @@ struct LocalFwdArgs {
                                                          // W1^T, W2^T, S1^T, S2^T, M^T of every slot
   void* fsplit;                                          // null, or local_fwd_split_bytes(D, units)
                                                          // bytes: the split forward (saved states only)
+  void* frec; float* frec_f;                             // null, or the forward records (saved
+                                                         // buffer) the backward passes read
   int nslots;
   void* scratch;                                         // units * plan.elems CT
   LocalPlan plan;
@@ -66,6 +68,8 @@ struct LocalBwdArgs {
   float* scratch_f32;                                    // units * plan.f32_elems
   LocalPlan plan;
   Dims D;
+  const void* frec; const float* frec_f;                 // forward records (written by the split
+                                                         // forward; required by the split backward)
   void* split_ws;                                        // null, or local_bwd_split_bytes(D, units)
                                                          // bytes for the three-pass fixed-size kernels
   int single_walk;                                       // 1: the one-walk fixed-size kernel

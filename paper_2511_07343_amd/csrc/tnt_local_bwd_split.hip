@@ -1,31 +1,32 @@
 // Local memories, backward, fixed sizes, in three passes.
 //
 // The backward of one chunk is affine in the carried adjoint of the chunk's
-// exit state (W1', S1', W2', S2' bar): the recomputed forward values, the
-// backward of the retrieval (driven by dO), the query / key / value adjoints it
-// feeds and the Q-K projection do not depend on it.  So the reverse walk over a
-// shard's chunks is split:
+// exit state (W1', S1', W2', S2' bar): the backward of the retrieval (driven by
+// dO), the query / key / value adjoints it feeds and the Q-K projection do not
+// depend on it.  The forward already wrote every forward quantity of every
+// chunk that the backward needs into the chunk's forward record (see
+// tnt_local_record.h), so the reverse walk over a shard's chunks is split:
 //
-//   pass A  (all chunks of all units at once, a persistent grid)  recomputes
-//           the chunk's forward quantities, takes the backward of the
-//           retrieval, writes its dq and its share of dk, and leaves a chunk
-//           record: the operands the walk needs, the retrieval's gate
-//           cotangents (cbar, dA, dE) and X^T Q for the Q-K state adjoint;
+//   pass A  (all chunks of all units at once, a persistent grid) takes the
+//           backward of the retrieval from dO and the forward record, writes
+//           the chunk's dq and its share of dk, and leaves a backward record:
+//           the dO operands the walk contracts, the retrieval's gate
+//           cotangents (cbar, dA, dE) and Xbar^T Q for the Q-K state adjoint;
 //   pass B  (one workgroup per unit, chunks in reverse) walks the carried
 //           adjoint back: T3..T6, D1bar / Gbar, Rbar (dv), Zkbar, the carried
 //           part of Kbar and the chunk-entry adjoint, four block barriers a chunk;
-//   scan    turns the per-chunk X^T Q into the suffix sums the Q-K projection
+//   scan    turns the per-chunk Xbar^T Q into the suffix sums the Q-K projection
 //           carries back to each chunk (shard-scoped projection only);
 //   pass C  (all chunks at once) finishes the gate adjoints (dlr, dmom,
 //           ddecay) and adds the carried Q-K term to dk.
 //
 // Each step's formulas are those of the single-walk kernels (the runtime-sized
 // kernel writes them out); only the place where each term is taken differs.
-// Wave-block GEMMs (Blk / mma_blk) and fragment-major elementwise buffers as
-// in the single-walk fixed-size kernel; passes A and B use the same block
-// mapping for C x h tiles, so fragment-major records written by A are read by B.
+// Wave-block GEMMs (Blk / mma_blk) and fragment-major elementwise factors as in
+// the single-walk fixed-size kernel.
 #include "tnt_local_common.h"
 #include "tnt_local_bwd_helpers.h"
+#include "tnt_local_record.h"
 
 namespace tnt {
 
@@ -34,82 +35,43 @@ using namespace bwdh;
 namespace {
 
 // ---------------------------------------------------------------------------
-// buffer layouts (element offsets; CT = compute type)
+// temporaries (element offsets; CT = compute type)
 // ---------------------------------------------------------------------------
-// chunk record, one per (unit, chunk): written by pass A, read by B and C
-enum RecCT {
-  rHk, rHkT, rD1, rZbT, rHT, rSp, rSpp, rG,        // C x h  (Sp, Spp, G fragment-major)
-  rPzT, rQ1T, rPoT,                                // C x C
-  rK, rKT, rKcC, rKb, rR, rRT, rRcC, rRb, rdOT,    // C x d
-  rXAT, rXET, rdOAT, rdOET, rN, REC_CT
-};
-enum RecF {
-  rCb,                     // C x C  retrieval part of cbar
-  rgA, rgE, rkn, rcC, rbb, // C      retrieval dA, dE; key norms; cC, b
-  rsc,                     // 4      A_C, B_C, E_C
-  rXbQ,                    // d x d  Xbar^T Q (then the suffix sum over later chunks)
-  rgCC, rgB,               // C      carried cC-bar, b-bar (pass B)
-  rdot,                    // 4      dA_C, dE_C, dB_C (pass B)
-  REC_F
-};
 // pass-A temporaries, one set per resident workgroup
 enum ATmpCT {
-  aQ, aQT, aNT, aX, aXT, aXA, aXE, adO, adOA, adOE, aXb, aXbT,  // C x d
-  aStr, aStrT, aPz, aPo, aQ1, aQ2, aQ2T, adXN, adXNT,          // C x C
-  aD1T, aSz,                                                   // C x h (Sz fragment-major)
+  adO, adOA, adOE, aXb, aXbT,          // C x d
+  aQ1, aQ2, aQ2T, adXN, adXNT,         // C x C
   A_CT
 };
-enum ATmpF { aXK, aHH, aNb, aKb, A_F };
+enum ATmpF { aNb, aKb, A_F };
 // pass-B temporaries, one set per unit
 enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, B_CT };
 
-template <int NB>
-struct Lay {
-  size_t o[NB];
-  size_t n;
-};
-
-// offsets rounded to 8 elements: 16-byte alignment for bf16 and fp32 vectors
-template <int NB>
-constexpr Lay<NB> make_lay(const size_t (&sz)[NB]) {
-  Lay<NB> y{};
-  size_t off = 0;
-  for (int i = 0; i < NB; ++i) {
-    y.o[i] = off;
-    off += (sz[i] + 7) & ~size_t(7);
-  }
-  y.n = off;
-  return y;
-}
-
 struct SplitLayout {
-  Lay<REC_CT> rc;
-  Lay<REC_F> rf;
-  Lay<A_CT> ac;
-  Lay<A_F> af;
-  Lay<B_CT> bc;
+  rec::RecLayout r;
+  rec::Lay<A_CT> ac;
+  rec::Lay<A_F> af;
+  rec::Lay<B_CT> bc;
 };
 
 constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
-  const size_t C = Cp, Cd = C * d, Ch = C * h, CC = C * C, HD = (size_t)h * d, dd = (size_t)d * d;
-  const size_t src[REC_CT] = {Ch, Ch, Ch, Ch, Ch, Ch, Ch, Ch, CC, CC, CC, Cd, Cd, Cd, Cd,
-                              Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd};
-  const size_t srf[REC_F] = {CC, C, C, C, C, C, 4, dd, C, C, 4};
-  const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd,
-                            CC, CC, CC, CC, CC, CC, CC, CC, CC, Ch, Ch};
-  const size_t saf[A_F] = {CC, CC, Cd, Cd};
+  const size_t C = Cp, Cd = C * d, CC = C * C, HD = (size_t)h * d;
+  const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, CC, CC, CC, CC, CC};
+  const size_t saf[A_F] = {Cd, Cd};
   const size_t sbc[B_CT] = {HD, HD, HD, HD};
-  return SplitLayout{make_lay(src), make_lay(srf), make_lay(sac), make_lay(saf), make_lay(sbc)};
+  return SplitLayout{rec::make_rec_layout(Cp, d, h), rec::make_lay(sac), rec::make_lay(saf),
+                     rec::make_lay(sbc)};
 }
 
 constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
 
 // dynamic LDS of pass A: cbar (CP x CP fp32), partial row sums pA, pE
-// ((D/16) x CP fp32 each), three CP x H compute-type slots
+// ((D/16) x CP fp32 each), one CP x H compute-type slot (Zbar)
 template <typename CT, int CP, int D, int H>
 constexpr size_t split_a_lds() {
-  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + 3 * (size_t)CP * H * sizeof(CT);
+  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + (size_t)CP * H * sizeof(CT);
 }
+
 // pass B: a CP x H compute-type slot (Gbar, then Zkbar); T3, T4 and T5, T6
 // (fragment-major fp32, CP x D each; the T5/T6 space holds Zkbar^T, H x CP
 // compute type, from phase 3 on); Ykbar and Ykbar^T (CP x D compute type each);
@@ -144,8 +106,8 @@ constexpr size_t split_c_lds() {
 }  // namespace
 
 struct SplitPtrs {
-  void* rec;        // CT   [units * nch][rc.n]
-  float* rec_f;     // fp32 [units * nch][rf.n]
+  void* brec;       // CT   [units * nch][r.bc.n]  backward records
+  float* brec_f;    // fp32 [units * nch][r.bf.n]
   void* tmpA;       // CT   [SPLIT_GRID_A][ac.n]
   float* tmpA_f;    // fp32 [SPLIT_GRID_A][af.n]
   void* tmpB;       // CT   [units][bc.n]
@@ -153,22 +115,19 @@ struct SplitPtrs {
 };
 
 // ===========================================================================
-// pass A: retrieval backward of every chunk
+// pass A: backward of the retrieval of every chunk, from dO and the forward record
 // ===========================================================================
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
 __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
-  __shared__ Coef cf;
+  __shared__ CoefF cf;
   __shared__ float gA[MAXC], gE[MAXC];
-  __shared__ float kss[D / 8][MAXC];  // partial squared key norms per 8-column block
+  __shared__ float dpa[D / 8][MAXC], dpe[D / 8][MAXC];  // partial dA, dE per 8-column block
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int d = D, h = H, Cp = CP;
   float* fCb = reinterpret_cast<float*>(smem);
   float* pA = fCb + Cp * Cp;
   float* pE = pA + (D / 16) * Cp;
-  // C x h slots: S1 = Hk, S2 = H (Z .. H W2^T) then Zbar, S3 = D1
-  CT* slot1 = reinterpret_cast<CT*>(pE + (D / 16) * Cp);
-  CT* slot2 = slot1 + Cp * h;
-  CT* slot3 = slot2 + Cp * h;
+  CT* Zb = reinterpret_cast<CT*>(pE + (D / 16) * Cp);  // C x h slot
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -178,136 +137,102 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
   constexpr size_t hd = (size_t)h * d;
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
-  const float rscale = 2.0f / (float)d;
   CT* const ta0 = (CT*)P.tmpA + (size_t)blockIdx.x * Y.ac.n;
   float* const tf0 = P.tmpA_f + (size_t)blockIdx.x * Y.af.n;
 
   for (int t = blockIdx.x; t < total; t += gridDim.x) {
     const int u = t / nch, n = t - u * nch;
     const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
-    CT* rc = (CT*)P.rec + (size_t)t * Y.rc.n;
-    float* rf = P.rec_f + (size_t)t * Y.rf.n;
+    const CT* fr = (const CT*)a.frec + (size_t)t * Y.r.fc.n;
+    const float* frf = a.frec_f + (size_t)t * Y.r.ff.n;
+    CT* br = (CT*)P.brec + (size_t)t * Y.r.bc.n;
+    float* brf = P.brec_f + (size_t)t * Y.r.bf.n;
     CT* ta = ta0;
     float* tf = tf0;
-    rc = launder_global(rc);
-    rf = launder_global(rf);
+    fr = launder_global(fr);
+    frf = launder_global(frf);
+    br = launder_global(br);
+    brf = launder_global(brf);
     ta = launder_global(ta);
     tf = launder_global(tf);
     const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
-    const IO* qg = (const IO*)a.q + cbase * d;
-    const IO* kg = (const IO*)a.k + cbase * d;
-    const IO* vg = (const IO*)a.v + cbase * d;
     const IO* dOg = (const IO*)a.dO + cbase * d;
     float* dqp = a.dq_part + cbase * d;
     float* dkp = a.dk_part + cbase * d;
-#define R_(x) (rc + Y.rc.o[x])
-#define RF_(x) (rf + Y.rf.o[x])
+#define FR_(x) (fr + Y.r.fc.o[rec::x])
+#define FRF_(x) (frf + Y.r.ff.o[rec::x])
+#define BR_(x) (br + Y.r.bc.o[rec::x])
+#define BRF_(x) (brf + Y.r.bf.o[rec::x])
 #define A_(x) (ta + Y.ac.o[x])
 #define AF_(x) (tf + Y.af.o[x])
-    CT *Hk = slot1, *HkT = R_(rHkT), *D1 = slot3, *H_ = slot2, *Zb = slot2;
-    CT *ZbT = R_(rZbT), *HT = R_(rHT), *Sp = R_(rSp), *Spp = R_(rSpp), *G = R_(rG);
-    CT *PzT = R_(rPzT), *Q1T = R_(rQ1T), *PoT = R_(rPoT);
-    CT *K = R_(rK), *KT = R_(rKT), *KcC = R_(rKcC), *Kb = R_(rKb), *R = R_(rR), *RT = R_(rRT),
-       *RcC = R_(rRcC), *Rb = R_(rRb), *dOT = R_(rdOT);
-    CT *XAT = R_(rXAT), *XET = R_(rXET), *dOAT = R_(rdOAT), *dOET = R_(rdOET), *N = R_(rN);
-    CT *Q = A_(aQ), *QT = A_(aQT), *NT = A_(aNT), *X = A_(aX), *XT = A_(aXT), *XA = A_(aXA),
-       *XE = A_(aXE), *dO = A_(adO), *dOA = A_(adOA), *dOE = A_(adOE), *Xb = A_(aXb),
-       *XbT = A_(aXbT);
-    CT *Str = A_(aStr), *StrT = A_(aStrT), *Pz = A_(aPz), *Po = A_(aPo), *Q1 = A_(aQ1),
-       *Q2 = A_(aQ2), *Q2T = A_(aQ2T), *dXN = A_(adXN), *dXNT = A_(adXNT);
-    CT *D1T = A_(aD1T), *Sz = A_(aSz);
-    float *fXK = AF_(aXK), *fHH = AF_(aHH), *fNb = AF_(aNb), *fKb = AF_(aKb);
+    const CT *HkT = FR_(HkT), *D1 = FR_(D1), *Sz = FR_(Sz), *KT = FR_(KT), *R = FR_(R),
+             *X = FR_(X), *XT = FR_(XT), *N = FR_(N), *NT = FR_(NT), *QT = FR_(QT),
+             *StrT = FR_(StrT);
+    const float *fXK = FRF_(XK), *fHH = FRF_(HH), *fHW2 = FRF_(HW2), *fHS2 = FRF_(HS2),
+                *knorm = FRF_(kn);
+    CT *ZbT = BR_(ZbT), *Q1T = BR_(Q1T), *dOT = BR_(dOT), *dOAT = BR_(dOAT), *dOET = BR_(dOET);
+    CT *dO = A_(adO), *dOA = A_(adOA), *dOE = A_(adOE), *Xb = A_(aXb), *XbT = A_(aXbT);
+    CT *Q1 = A_(aQ1), *Q2 = A_(aQ2), *Q2T = A_(aQ2T), *dXN = A_(adXN), *dXNT = A_(adXNT);
+    float *fNb = AF_(aNb), *fKb = AF_(aKb);
     const int tok0 = s * Dm.S + n * C;
     const int l = lane_id_local();
-    const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
-    const float *W1 = st, *W2 = st + hd, *S1 = st + 2 * hd, *S2 = st + 3 * hd;
-    const float* Mc = a.mstates + ((size_t)u * a.nslots + n) * d * d;
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
     const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd, *McT = pk + 4 * hd;
 
-    // ---- stage Q, K, dO rows and their transposes (one (row, 8-column block)
-    // per thread, consecutive threads on consecutive rows); partial key norms
+    // ---- chunk coefficients; stage dO (one (row, 8-column block) per thread,
+    // consecutive threads on consecutive rows) with its scaled and transposed
+    // forms; partial dA, dE of the retrieval, sum_k dO_ik (H W2^T)_ik (S2 likewise)
+    chunk_coefs_f(cf, a.lr + cbase, a.mom + cbase, a.decay + cbase, tok0, C, Cp);  // ends with a barrier
     constexpr int JB = D / 8, ITEMS = CP * JB, PER = (ITEMS + 511) / 512;
-    float kx[PER][8], ox[PER][8];
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int e = threadIdx.x + p * 512;
-      if (e < ITEMS) {
-        const int i = e % CP, j0 = (e / CP) * 8;
-        const size_t gofs = (size_t)(tok0 + i) * d + j0, en = (size_t)i * d + j0;
-        float qx[8];
-        if (i < C) {
-          load8(qg + gofs, qx);
-          load8(kg + gofs, kx[p]);
-          load8(dOg + gofs, ox[p]);
-        } else {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) qx[q] = kx[p][q] = ox[p][q] = 0.f;
-        }
-        store8<CT>(Q + en, qx);
-        store8<CT>(K + en, kx[p]);
-        store8<CT>(dO + en, ox[p]);
-        float ss = 0.f;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const size_t et = (size_t)(j0 + q) * Cp + i;
-          QT[et] = from_f<CT>(qx[q]);
-          KT[et] = from_f<CT>(kx[p][q]);
-          dOT[et] = from_f<CT>(ox[p][q]);
-          ss += kx[p][q] * kx[p][q];
-        }
-        kss[j0 / 8][i] = ss;
-      }
-    }
-    chunk_coefs(cf, a.lr + cbase, a.mom + cbase, a.decay + cbase, tok0, C, Cp);  // ends with a barrier
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int e = threadIdx.x + p * 512;
       if (e < ITEMS) {
         const int i = e % CP, j0 = (e / CP) * 8;
         const size_t en = (size_t)i * d + j0;
-        float n2 = 0.f;
+        float ox[8], va[8], ve[8];
+        if (i < C) {
+          load8(dOg + (size_t)(tok0 + i) * d + j0, ox);
+        } else {
 #pragma unroll
-        for (int q = 0; q < JB; ++q) n2 += kss[q][i];  // fixed order: deterministic
-        const float nr = sqrtf(n2);
-        if (j0 == 0) cf.knorm[i] = nr;
-        float va[8], ve[8], vc[8], vb[8], vn[8];
+          for (int q = 0; q < 8; ++q) ox[q] = 0.f;
+        }
+        float w2[8], s2[8];
+        load8(fHW2 + en, w2);
+        load8(fHS2 + en, s2);
+        float sa = 0.f, se = 0.f;
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           const size_t et = (size_t)(j0 + q) * Cp + i;
-          va[q] = cf.A[i] * ox[p][q];
-          ve[q] = cf.E[i] * ox[p][q];
-          vc[q] = cf.cC[i] * kx[p][q];
-          vb[q] = cf.bb[i] * kx[p][q];
-          vn[q] = (i < C && nr > 0.f) ? kx[p][q] / nr : 0.f;
+          va[q] = cf.A[i] * ox[q];
+          ve[q] = cf.E[i] * ox[q];
+          dOT[et] = from_f<CT>(ox[q]);
           dOAT[et] = from_f<CT>(va[q]);
           dOET[et] = from_f<CT>(ve[q]);
-          if (Dm.qk_proj) NT[et] = from_f<CT>(vn[q]);
+          const float oq = to_f(from_f<CT>(ox[q]));  // dO as the contractions see it
+          sa += oq * w2[q];
+          se += oq * s2[q];
         }
+        store8<CT>(dO + en, ox);
         store8<CT>(dOA + en, va);
         store8<CT>(dOE + en, ve);
-        store8<CT>(KcC + en, vc);
-        store8<CT>(Kb + en, vb);
-        if (Dm.qk_proj) store8<CT>(N + en, vn);
+        dpa[j0 / 8][i] = sa;
+        dpe[j0 / 8][i] = se;
       }
     }
     __syncthreads();
-    if (threadIdx.x < MAXC) gA[threadIdx.x] = gE[threadIdx.x] = 0.f;
-    auto put_x4 = [&](int i, int j, const f4& x) {
-      f4 xa, xe;
+    if (threadIdx.x < MAXC) {
+      const int i = threadIdx.x;
+      float sa = 0.f, se = 0.f;
+      if (i < Cp)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const size_t e = (size_t)(i + r) * d + j;
-        X[e] = from_f<CT>(x[r]);
-        xa[r] = cf.A[i + r] * x[r];
-        xe[r] = cf.E[i + r] * x[r];
-        XA[e] = from_f<CT>(xa[r]);
-        XE[e] = from_f<CT>(xe[r]);
-      }
-      store4<CT>(XT + (size_t)j * Cp + i, x);
-      store4<CT>(XAT + (size_t)j * Cp + i, xa);
-      store4<CT>(XET + (size_t)j * Cp + i, xe);
-    };
+        for (int q = 0; q < JB; ++q) {  // fixed order: deterministic
+          sa += dpa[q][i];
+          se += dpe[q][i];
+        }
+      gA[i] = sa;
+      gE[i] = se;
+    }
     using BCD = Blk<CP, D>;
     using BCH = Blk<CP, H>;
     using BCC = Blk<CP, CP>;
@@ -316,181 +241,6 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       const int blk = (i0 / (BCH::RB * 16)) * BCH::NBN + j0 / (BCH::CB * 16);
       return ((size_t)((blk * BCH::RB + rb) * BCH::CB + cb) * WAVE + l) * 4;
     };
-    if (Dm.qk_proj) {
-      for_blocks<CP, CP>([&](int i0, int j0) {
-        f4 acc[BCC::RB][BCC::CB];
-        zero_blk(acc);
-        mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, Q, d, i0, N, d, j0);
-        blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-          f4 y;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            y[r] = j <= i + r ? acc[rb][cb][r] : 0.f;
-            Str[(size_t)(i + r) * Cp + j] = from_f<CT>(y[r]);
-          }
-          store4<CT>(StrT + (size_t)j * Cp + i, y);
-        });
-      });
-      __syncthreads();
-      for_blocks<CP, D>([&](int i0, int j0) {
-        f4 acc[BCD::RB][BCD::CB];
-        zero_blk(acc);
-        if (shard_qk) mma_blk<CT, KC, KC, BCD::RB, BCD::CB, D>(acc, Q, d, i0, Mc, d, j0);
-        mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(acc, Str, Cp, i0, NT, Cp, j0);
-        blk_each4<BCD::RB, BCD::CB>(i0, j0,
-                                    [&](int rb, int cb, int i, int j) { put_x4(i, j, acc[rb][cb]); });
-      });
-    } else {
-      for (int e = threadIdx.x; e < Cp * d / 4; e += blockDim.x) {
-        const int i = (e % (Cp / 4)) * 4, j = e / (Cp / 4);
-        f4 x;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) x[r] = to_f(Q[(size_t)(i + r) * d + j]);
-        put_x4(i, j, x);
-      }
-    }
-    // Zk = K W1^T -> Hk (LDS and record), s'(Zk), s''(Zk)
-    for_blocks<CP, H>([&](int i0, int j0) {
-      f4 acc[BCH::RB][BCH::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(acc, K, d, i0, W1, d, j0);
-      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 hv, sp, spp;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const ActVals av = act_all<ACT>(acc[rb][cb][r]);
-          const CT hx = from_f<CT>(av.s);
-          Hk[(size_t)(i + r) * h + j] = hx;
-          R_(rHk)[(size_t)(i + r) * h + j] = hx;
-          hv[r] = av.s;
-          sp[r] = av.d1;
-          spp[r] = av.d2;
-        }
-        const size_t fo = fofs(i0, j0, rb, cb);
-        store4<CT>(Sp + fo, sp);
-        store4<CT>(Spp + fo, spp);
-        store4<CT>(HkT + (size_t)j * Cp + i, hv);
-      });
-    });
-    __syncthreads();
-    // R = (2/d)(Hk W2^T - V)
-    for_blocks<CP, D>([&](int i0, int j0) {
-      f4 acc[BCD::RB][BCD::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(acc, Hk, h, i0, W2, h, j0);
-      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 rv;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ii = i + r;
-          rv[r] = (ii < C) ? rscale * (acc[rb][cb][r] - to_f(vg[(size_t)(tok0 + ii) * d + j])) : 0.f;
-          R[(size_t)ii * d + j] = from_f<CT>(rv[r]);
-          RcC[(size_t)ii * d + j] = from_f<CT>(cf.cC[ii] * rv[r]);
-          Rb[(size_t)ii * d + j] = from_f<CT>(cf.bb[ii] * rv[r]);
-        }
-        store4<CT>(RT + (size_t)j * Cp + i, rv);
-      });
-    });
-    __syncthreads();
-    // G = R W2, D1 = G * s'(Zk) (LDS and record) ;  XK = X K^T, Pz = c o XK
-    for_blocks<CP, H>([&](int i0, int j0) {
-      f4 acc[BCH::RB][BCH::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(acc, R, d, i0, W2T, d, j0);
-      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const size_t fo = fofs(i0, j0, rb, cb);
-        const f4 sp = load4<CT>(Sp + fo);
-        f4 dv;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          dv[r] = acc[rb][cb][r] * sp[r];
-          const CT dx = from_f<CT>(dv[r]);
-          D1[(size_t)(i + r) * h + j] = dx;
-          R_(rD1)[(size_t)(i + r) * h + j] = dx;
-        }
-        store4<CT>(G + fo, acc[rb][cb]);
-        store4<CT>(D1T + (size_t)j * Cp + i, dv);
-      });
-    });
-    for_blocks<CP, CP>([&](int i0, int j0) {
-      f4 acc[BCC::RB][BCC::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, X, d, i0, K, d, j0);
-      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 pv;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ii = i + r;
-          const float x = acc[rb][cb][r];
-          fXK[ii * Cp + j] = x;
-          pv[r] = j <= ii ? cf.c[ii][j] * x : 0.f;
-          Pz[(size_t)ii * Cp + j] = from_f<CT>(pv[r]);
-        }
-        store4<CT>(PzT + (size_t)j * Cp + i, pv);
-      });
-    });
-    __syncthreads();
-    // Z = diag(A) X W1^T + diag(E) X S1^T - Pz D1 -> H, s'(Z)
-    for_blocks<CP, H>([&](int i0, int j0) {
-      f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
-      zero_blk(a1);
-      zero_blk(a3);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, XA, d, i0, W1, d, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, XE, d, i0, S1, d, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Pz, Cp, i0, D1T, Cp, j0);
-      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 hv, sz;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const ActVals av = act_all<ACT>(a1[rb][cb][r] - a3[rb][cb][r]);
-          H_[(size_t)(i + r) * h + j] = from_f<CT>(av.s);
-          hv[r] = av.s;
-          sz[r] = av.d1;
-        }
-        store4<CT>(Sz + fofs(i0, j0, rb, cb), sz);
-        store4<CT>(HT + (size_t)j * Cp + i, hv);
-      });
-    });
-    __syncthreads();
-    // HH = H Hk^T, Po = c o HH
-    for_blocks<CP, CP>([&](int i0, int j0) {
-      f4 acc[BCC::RB][BCC::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BCC::RB, BCC::CB, H>(acc, H_, h, i0, Hk, h, j0);
-      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        f4 pv;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ii = i + r;
-          const float x = acc[rb][cb][r];
-          fHH[ii * Cp + j] = x;
-          pv[r] = j <= ii ? cf.c[ii][j] * x : 0.f;
-          Po[(size_t)ii * Cp + j] = from_f<CT>(pv[r]);
-        }
-        store4<CT>(PoT + (size_t)j * Cp + i, pv);
-      });
-    });
-    // dA, dE of the retrieval: sum_j (dO W2)_ij H_ij = sum_k dO_ik (H W2^T)_ik (S2 likewise)
-    for_blocks<CP, D>([&](int i0, int j0) {
-      f4 a1[BCD::RB][BCD::CB], a2[BCD::RB][BCD::CB];
-      zero_blk(a1);
-      zero_blk(a2);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a1, H_, h, i0, W2, h, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, H_, h, i0, S2, h, j0);
-      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ii = i + r;
-          const float ov = to_f(dO[(size_t)ii * d + j]);
-          const float sa = sum16b(a1[rb][cb][r] * ov), se = sum16b(a2[rb][cb][r] * ov);
-          if ((l & 15) == 0) {
-            pA[(j >> 4) * Cp + ii] = sa;
-            pE[(j >> 4) * Cp + ii] = se;
-          }
-        }
-      });
-    });
-    __syncthreads();
     // dOR = dO R^T ; Q1 = c o dOR ; cbar = -HH o dOR
     for_blocks<CP, CP>([&](int i0, int j0) {
       f4 acc[BCC::RB][BCC::CB];
@@ -511,7 +261,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       });
     });
     __syncthreads();
-    // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)  (slot S2: H is dead)
+    // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)
     for_blocks<CP, H>([&](int i0, int j0) {
       f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
       zero_blk(a1);
@@ -531,16 +281,6 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       });
     });
     __syncthreads();
-    for (int i = threadIdx.x; i < Cp; i += blockDim.x) {
-      float sa = 0.f, se = 0.f;
-#pragma unroll
-      for (int q = 0; q < (d >> 4); ++q) {
-        sa += pA[q * Cp + i];
-        se += pE[q * Cp + i];
-      }
-      gA[i] += sa;
-      gE[i] += se;
-    }
     // dZD1 = Zbar D1^T ; Q2 = c o dZD1 ; cbar -= XK o dZD1
     for_blocks<CP, CP>([&](int i0, int j0) {
       f4 acc[BCC::RB][BCC::CB];
@@ -606,19 +346,11 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
         sa += pA[q * Cp + i];
         se += pE[q * Cp + i];
       }
-      rf[Y.rf.o[rgA] + i] = gA[i] + sa;
-      rf[Y.rf.o[rgE] + i] = gE[i] + se;
-      rf[Y.rf.o[rkn] + i] = cf.knorm[i];
-      rf[Y.rf.o[rcC] + i] = cf.cC[i];
-      rf[Y.rf.o[rbb] + i] = cf.bb[i];
-    }
-    if (threadIdx.x == 0) {
-      rf[Y.rf.o[rsc] + 0] = cf.AC;
-      rf[Y.rf.o[rsc] + 1] = cf.BC;
-      rf[Y.rf.o[rsc] + 2] = cf.EC;
+      BRF_(gA)[i] = gA[i] + sa;
+      BRF_(gE)[i] = gE[i] + se;
     }
     for (int e = threadIdx.x * 4; e < Cp * Cp; e += blockDim.x * 4)
-      *reinterpret_cast<f32x4*>(RF_(rCb) + e) = *reinterpret_cast<const f32x4*>(fCb + e);
+      *reinterpret_cast<f32x4*>(BRF_(Cb) + e) = *reinterpret_cast<const f32x4*>(fCb + e);
     if (Dm.qk_proj) {
       // dXN = tril(Xbar N^T)
       for_blocks<CP, CP>([&](int i0, int j0) {
@@ -643,7 +375,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
           mma_blk<CT, KC, KC, BDD::RB, BDD::CB, CP>(a1, XbT, Cp, i0, QT, Cp, j0);
           blk_each4<BDD::RB, BDD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) RF_(rXbQ)[(size_t)(i + r) * d + j] = a1[rb][cb][r];
+            for (int r = 0; r < 4; ++r) BRF_(XbQ)[(size_t)(i + r) * d + j] = a1[rb][cb][r];
           });
         });
       __syncthreads();
@@ -668,7 +400,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       __syncthreads();
       // Kbar += (Nbar - N (N . Nbar)) / ||k||
       for (int i = wave_id(); i < C; i += num_waves()) {
-        const float nr = cf.knorm[i];
+        const float nr = knorm[i];
         float dt = 0.f;
         for (int j = l; j < d; j += WAVE) dt += to_f(N[(size_t)i * d + j]) * fNb[(size_t)i * d + j];
         dt = wave_sum(dt);
@@ -683,8 +415,10 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     for (int e = threadIdx.x * 4; e < C * d; e += blockDim.x * 4)
       *reinterpret_cast<f32x4*>(dkp + (size_t)tok0 * d + e) = *reinterpret_cast<const f32x4*>(fKb + e);
     __syncthreads();  // the next chunk reuses LDS and the temporaries
-#undef R_
-#undef RF_
+#undef FR_
+#undef FRF_
+#undef BR_
+#undef BRF_
 #undef A_
 #undef AF_
   }
@@ -737,16 +471,22 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 
   for (int n = nch - 1; n >= 0; --n) {
     const size_t t = (size_t)u * nch + n;
-    CT* rc = (CT*)P.rec + t * Y.rc.n;
-    float* rf = P.rec_f + t * Y.rf.n;
+    const CT* rc = (const CT*)a.frec + t * Y.r.fc.n;
+    const float* rf = a.frec_f + t * Y.r.ff.n;
+    CT* bq = (CT*)P.brec + t * Y.r.bc.n;
+    float* bqf = P.brec_f + t * Y.r.bf.n;
     CT* tb = tb0;
     float* adj = adj0;
     rc = launder_global(rc);
     rf = launder_global(rf);
+    bq = launder_global(bq);
+    bqf = launder_global(bqf);
     tb = launder_global(tb);
     adj = launder_global(adj);
-#define R_(x) (rc + Y.rc.o[x])
-#define RF_(x) (rf + Y.rf.o[x])
+#define R_(x) (rc + Y.r.fc.o[rec::x])
+#define RF_(x) (rf + Y.r.ff.o[rec::x])
+#define BQ_(x) (bq + Y.r.bc.o[rec::x])
+#define BQF_(x) (bqf + Y.r.bf.o[rec::x])
 #define T_(x) (tb + Y.bc.o[x])
     float *Wb1 = adj, *Wb2 = adj + hd, *Sb1 = adj + 2 * hd, *Sb2 = adj + 3 * hd;
     CT *Wb1T = T_(tWb1T), *Sb1T = T_(tSb1T), *Wb2T = T_(tWb2T), *Sb2T = T_(tSb2T);
@@ -754,11 +494,11 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     // the Zkbar terms known after phase 1, kept by the wave that owns the block
     // until phase 3 (both phases walk the same C x h blocks)
     f4 zkp[BCH0::RB][BCH0::CB];
-    const CT *Hk = R_(rHk), *HkT = R_(rHkT), *D1 = R_(rD1), *ZbT = R_(rZbT), *HT = R_(rHT),
-             *Sp = R_(rSp), *Spp = R_(rSpp), *G = R_(rG), *PzT = R_(rPzT), *Q1T = R_(rQ1T),
-             *PoT = R_(rPoT), *K = R_(rK), *KT = R_(rKT), *KcC = R_(rKcC), *Kb = R_(rKb), *R = R_(rR),
-             *RT = R_(rRT), *RcC = R_(rRcC), *Rb = R_(rRb), *dOT = R_(rdOT), *XAT = R_(rXAT),
-             *XET = R_(rXET), *dOAT = R_(rdOAT), *dOET = R_(rdOET);
+    const CT *Hk = R_(Hk), *HkT = R_(HkT), *D1 = R_(D1), *ZbT = BQ_(ZbT), *HT = R_(HT),
+             *Sp = R_(Sp), *Spp = R_(Spp), *G = R_(G), *PzT = R_(PzT), *Q1T = BQ_(Q1T),
+             *PoT = R_(PoT), *K = R_(K), *KT = R_(KT), *KcC = R_(KcC), *Kb = R_(Kb), *R = R_(R),
+             *RT = R_(RT), *RcC = R_(RcC), *Rb = R_(Rb), *dOT = BQ_(dOT), *XAT = R_(XAT),
+             *XET = R_(XET), *dOAT = BQ_(dOAT), *dOET = BQ_(dOET);
     const int tok0 = s * Dm.S + n * C;
     const int l = lane_id_local();
     const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
@@ -779,10 +519,10 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     // ---- phase 1: chunk coefficients; adjoint . state dot products (dA_C,
     // dE_C, dB_C); T3..T6; D1bar -> Gbar; the first part of Hkbar
     if (threadIdx.x < Cp) {
-      sC[threadIdx.x] = RF_(rcC)[threadIdx.x];
-      sB[threadIdx.x] = RF_(rbb)[threadIdx.x];
+      sC[threadIdx.x] = RF_(cC)[threadIdx.x];
+      sB[threadIdx.x] = RF_(bb)[threadIdx.x];
     }
-    if (threadIdx.x < 3) sc3[threadIdx.x] = RF_(rsc)[threadIdx.x];
+    if (threadIdx.x < 3) sc3[threadIdx.x] = RF_(sc)[threadIdx.x];
     {
       float pa = 0.f, pe = 0.f, pb = 0.f;
       const CT* adjT = Wb1T;  // Wb1^T, Sb1^T, Wb2^T, Sb2^T contiguous
@@ -884,14 +624,14 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         sc_ += pC[q * Cp + i];
         sb_ += pB[q * Cp + i];
       }
-      RF_(rgCC)[i] = -sc_;
-      RF_(rgB)[i] = -sb_;
+      BQF_(gCC)[i] = -sc_;
+      BQF_(gB)[i] = -sb_;
     }
     if (threadIdx.x < 3) {
       float x = 0.f;
 #pragma unroll
       for (int w = 0; w < 8; ++w) x += dpart[threadIdx.x][w];
-      RF_(rdot)[threadIdx.x] = x;
+      BQF_(dots)[threadIdx.x] = x;
     }
     for_blocks<CP, D>([&](int i0, int j0) {
       f4 a1[BCD::RB][BCD::CB], a2[BCD::RB][BCD::CB];
@@ -1018,6 +758,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     __syncthreads();
 #undef R_
 #undef RF_
+#undef BQ_
+#undef BQF_
 #undef T_
   }
   // adjoint of the learned init for this unit
@@ -1066,8 +808,9 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
   const int u = t / nch, n = t - u * nch;
   const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
-  const CT* rc = (const CT*)P.rec + (size_t)t * Y.rc.n;
-  const float* rf = P.rec_f + (size_t)t * Y.rf.n;
+  const CT* rc = (const CT*)a.frec + (size_t)t * Y.r.fc.n;
+  const float* rf = a.frec_f + (size_t)t * Y.r.ff.n;
+  const float* bqf = P.brec_f + (size_t)t * Y.r.bf.n;
   const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
   const float* mom = a.mom + cbase;
   const float* dec = a.decay + cbase;
@@ -1078,8 +821,8 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
   if (shard_qk && n < nch - 1) {
     // Kbar += (Nbar' - N (N . Nbar')) / ||k||, Nbar' = N (Mbar + Mbar^T), Mbar the
     // suffix sum of Xbar^T Q over the shard's later chunks
-    const CT* N = rc + Y.rc.o[rN];
-    const float* Mb = rf + Y.rf.o[rXbQ];
+    const CT* N = rc + Y.r.fc.o[rec::N];
+    const float* Mb = bqf + Y.r.bf.o[rec::XbQ];
     for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
       const int i = e / d, j = e - i * d;
       fMs[e] = Mb[e] + Mb[(size_t)j * d + i];
@@ -1097,7 +840,7 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
     });
     __syncthreads();
     float* dkp = a.dk_part + (cbase + tok0) * d;
-    const float* kn = rf + Y.rf.o[rkn];
+    const float* kn = rf + Y.r.ff.o[rec::kn];
     for (int i = wave_id(); i < C; i += num_waves()) {
       const float nr = kn[i];
       float dt = 0.f;
@@ -1114,15 +857,15 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
 
   chunk_coefs(cf, a.lr + cbase, mom, dec, tok0, C, Cp);  // ends with a barrier
   for (int e = threadIdx.x * 4; e < Cp * Cp; e += blockDim.x * 4)
-    *reinterpret_cast<f32x4*>(fCb + e) = *reinterpret_cast<const f32x4*>(rf + Y.rf.o[rCb] + e);
+    *reinterpret_cast<f32x4*>(fCb + e) = *reinterpret_cast<const f32x4*>(bqf + Y.r.bf.o[rec::Cb] + e);
   if (threadIdx.x < Cp) {
     const int i = threadIdx.x;
-    gA[i] = rf[Y.rf.o[rgA] + i];
-    gE[i] = rf[Y.rf.o[rgE] + i];
-    gCC[i] = rf[Y.rf.o[rgCC] + i];
-    gB[i] = rf[Y.rf.o[rgB] + i];
+    gA[i] = bqf[Y.r.bf.o[rec::gA] + i];
+    gE[i] = bqf[Y.r.bf.o[rec::gE] + i];
+    gCC[i] = bqf[Y.r.bf.o[rec::gCC] + i];
+    gB[i] = bqf[Y.r.bf.o[rec::gB] + i];
   }
-  if (threadIdx.x < 3) dots[threadIdx.x] = rf[Y.rf.o[rdot] + threadIdx.x];
+  if (threadIdx.x < 3) dots[threadIdx.x] = bqf[Y.r.bf.o[rec::dots] + threadIdx.x];
   __syncthreads();
   if (wave_id() == 0) {
     const int i = l;
@@ -1245,7 +988,7 @@ template <typename CT, int CP, int D, int H>
 SplitSizes split_sizes(int units, int nch) {
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const size_t t = (size_t)units * nch;
-  return SplitSizes{t * Y.rc.n, t * Y.rf.n, (size_t)SPLIT_GRID_A * Y.ac.n, (size_t)SPLIT_GRID_A * Y.af.n,
+  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n, (size_t)SPLIT_GRID_A * Y.ac.n, (size_t)SPLIT_GRID_A * Y.af.n,
                     (size_t)units * Y.bc.n};
 }
 
@@ -1261,8 +1004,8 @@ template <typename CT>
 SplitPtrs carve(void* ws, const SplitSizes& z, int units) {
   char* p = (char*)ws;
   SplitPtrs P{};
-  P.rec = p; p += up256(z.rec_ct * sizeof(CT));
-  P.rec_f = (float*)p; p += up256(z.rec_f * 4);
+  P.brec = p; p += up256(z.rec_ct * sizeof(CT));
+  P.brec_f = (float*)p; p += up256(z.rec_f * 4);
   P.tmpA = p; p += up256(z.a_ct * sizeof(CT));
   P.tmpA_f = (float*)p; p += up256(z.a_f * 4);
   P.tmpB = p;
@@ -1301,7 +1044,7 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   if (Dm.qk_proj && Dm.qk_scope == 0) {
     const size_t thr = (size_t)units * D * D;
     hipLaunchKernelGGL(split_madj_scan_kernel, dim3((unsigned)((thr + 255) / 256)), dim3(256), 0, st,
-                       P.rec_f, Y.rf.n, Y.rf.o[rXbQ], units, nch, D * D);
+                       P.brec_f, Y.r.bf.n, Y.r.bf.o[rec::XbQ], units, nch, D * D);
   }
   hipLaunchKernelGGL(kc, dim3(total), dim3(512), lds_c, st, *a, P);
   *err = hipGetLastError();
@@ -1328,7 +1071,7 @@ size_t local_bwd_split_bytes(const Dims& D, int units) {
 }
 
 bool launch_local_bwd_split(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err) {
-  if (!a.split_ws) return false;
+  if (!a.split_ws || !a.frec || !a.frec_f) return false;  // needs the forward's records
   return dispatch_split(&a, a.D, units, a.split_ws, st, err, nullptr);
 }
 

@@ -19,6 +19,7 @@
 // registers: four consecutive rows of an MFMA output tile are four contiguous
 // elements of the transpose.
 #include "tnt_local_common.h"
+#include "tnt_local_record.h"
 
 namespace tnt {
 
@@ -146,6 +147,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const int l = lane_id(), w = wave_id();
   const int ko = Mma<CT>::kofs(l);
   constexpr size_t FS = fwd_split_elems<D, HID, CP>();
+  constexpr rec::RecLayout RL = rec::make_rec_layout(CP, D, HID);
 
   if (WALK) {
     const float* W1i = a.W1i + hh * hd;
@@ -178,6 +180,9 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const int n_end = MODE == FWD_RET ? n_begin + 1 : nch;
   for (int n = n_begin; n < n_end; ++n) {
     CT* const fsn = (MODE == FWD_FULL) ? nullptr : (CT*)a.fsplit + ((size_t)u * nch + n) * FS;
+    // the chunk's forward record (walk: s'(Zk), s''(Zk), G; retrieval: the rest)
+    CT* const fr = (MODE != FWD_FULL && a.frec) ? (CT*)a.frec + ((size_t)u * nch + n) * RL.fc.n : nullptr;
+    float* const frf = fr ? a.frec_f + ((size_t)u * nch + n) * RL.ff.n : nullptr;
     const int tok0 = s * Dm.S + n * C;
     const float* cur = st + (size_t)(n % a.nslots) * 4 * hd;
     float* nxt = st + (size_t)((n + 1) % a.nslots) * 4 * hd;
@@ -288,6 +293,57 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         *reinterpret_cast<bf16x8*>(dst) = x;
       }
       __syncthreads();
+      if (fr) {
+        // the forward record: K, Q, N, Str, X, R, Hk, D1 and their scaled / transposed
+        // forms from LDS (destination-ordered writes), per-position coefficients
+        CT* const rp = fr;
+        for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
+          const int i = e / D;                     // row of the row-major element
+          const int jt = e / CP, it = e - jt * CP;  // transposed element [D][CP]
+          const float kx = to_f(sK[e]), rx = to_f(sR[e]);
+          rp[RL.fc.o[rec::K] + e] = sK[e];
+          rp[RL.fc.o[rec::KcC] + e] = from_f<CT>(cf.cC[i] * kx);
+          rp[RL.fc.o[rec::Kb] + e] = from_f<CT>(cf.bb[i] * kx);
+          rp[RL.fc.o[rec::R] + e] = sR[e];
+          rp[RL.fc.o[rec::RcC] + e] = from_f<CT>(cf.cC[i] * rx);
+          rp[RL.fc.o[rec::Rb] + e] = from_f<CT>(cf.bb[i] * rx);
+          rp[RL.fc.o[rec::X] + e] = sX[e];
+          const size_t et = (size_t)it * D + jt;
+          rp[RL.fc.o[rec::KT] + e] = sK[et];
+          rp[RL.fc.o[rec::RT] + e] = sR[et];
+          rp[RL.fc.o[rec::XT] + e] = sX[et];
+          rp[RL.fc.o[rec::XAT] + e] = from_f<CT>(cf.A[it] * to_f(sX[et]));
+          rp[RL.fc.o[rec::XET] + e] = from_f<CT>(cf.E[it] * to_f(sX[et]));
+          rp[RL.fc.o[rec::QT] + e] = sQ[et];
+          if (qk) {
+            rp[RL.fc.o[rec::N] + e] = sN[e];
+            rp[RL.fc.o[rec::NT] + e] = sNT[e];
+          }
+        }
+        if (qk)
+          for (int e = threadIdx.x; e < CP * CP; e += blockDim.x) {
+            const int jt = e / CP, it = e - jt * CP;
+            rp[RL.fc.o[rec::StrT] + e] = sS[(size_t)it * CP + jt];
+          }
+        for (size_t e = threadIdx.x; e < (size_t)CP * HID; e += blockDim.x) {
+          const size_t jt = e / CP, it = e - jt * CP;  // [HID][CP] element
+          const size_t i = e / HID, j = e - i * HID;   // [CP][HID] element
+          rp[RL.fc.o[rec::Hk] + e] = sHk[e];
+          rp[RL.fc.o[rec::HkT] + e] = sHk[it * HID + jt];
+          rp[RL.fc.o[rec::D1] + e] = sD1[j * CP + i];
+        }
+        if (threadIdx.x < CP) {
+          const int i = threadIdx.x;
+          frf[RL.ff.o[rec::kn] + i] = cf.knorm[i];
+          frf[RL.ff.o[rec::cC] + i] = cf.cC[i];
+          frf[RL.ff.o[rec::bb] + i] = cf.bb[i];
+        }
+        if (threadIdx.x == 0) {
+          frf[RL.ff.o[rec::sc] + 0] = cf.AC;
+          frf[RL.ff.o[rec::sc] + 1] = cf.BC;
+          frf[RL.ff.o[rec::sc] + 2] = cf.EC;
+        }
+      }
     }
     if constexpr (WALK) {
     // ---- Zk = K W1^T -> Hk (LDS), s'(Zk) (registers); each wave owns NS column strips
@@ -321,12 +377,20 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             auto a = Mma<CT>::template load<KC>(sK, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
             Mma<CT>::mma(acc, a, bw[y][ks]);
           }
+          f4 d1v, d2v;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
             const ActVals av = act_all<ACT>(acc[r]);
             sHk[(size_t)i * HID + j] = from_f<CT>(av.s);
             spr[y][it][r] = from_f<CT>(av.d1);
+            d1v[r] = av.d1;
+            d2v[r] = av.d2;
+          }
+          if (MODE == FWD_CHAIN && fr) {
+            const size_t fo = frag_ofs<CP, HID>(i0, j0, l);
+            store4<CT>(fr + RL.fc.o[rec::Sp] + fo, d1v);
+            store4<CT>(fr + RL.fc.o[rec::Spp] + fo, d2v);
           }
         }
       }
@@ -393,6 +457,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
           sD1[(size_t)j * CP + i] = from_f<CT>(acc[r] * to_f(spr[y][it][r]));  // D1^T
         }
+        if (MODE == FWD_CHAIN && fr) store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(i0, j0, l), acc);
       }
     }
     __syncthreads();
@@ -513,7 +578,12 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         f4 acc = zero4();
         mma_tile<CT, KC, KC>(acc, sX, D, i0, sK, D, j0, D);
         tile_each(acc, i0, j0, [&](int i, int j, float x) {
-          sP[(size_t)i * CP + j] = from_f<CT>(j <= i ? cf.c[i][j] * x : 0.f);
+          const CT pv = from_f<CT>(j <= i ? cf.c[i][j] * x : 0.f);
+          sP[(size_t)i * CP + j] = pv;
+          if (fr) {
+            frf[RL.ff.o[rec::XK] + (size_t)i * CP + j] = x;
+            fr[RL.fc.o[rec::PzT] + (size_t)j * CP + i] = pv;
+          }
         });
       }
     }
@@ -548,11 +618,23 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             Mma<CT>::mma(a2, a, bs[ks]);
           }
           mma_tile<CT, KC, KC>(a3, sP, CP, i0, sD1, CP, j0, CP);
+          f4 hv, szv;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
             const float z = cf.A[i] * a1[r] + cf.E[i] * a2[r] - a3[r];
-            sH[(size_t)i * HID + j] = from_f<CT>(act_f<ACT>(z));
+            if (fr) {
+              const ActVals av = act_all<ACT>(z);
+              sH[(size_t)i * HID + j] = from_f<CT>(av.s);
+              hv[r] = av.s;
+              szv[r] = av.d1;
+            } else {
+              sH[(size_t)i * HID + j] = from_f<CT>(act_f<ACT>(z));
+            }
+          }
+          if (fr) {
+            store4<CT>(fr + RL.fc.o[rec::HT] + (size_t)(j0 + (l & 15)) * CP + i0 + 4 * (l >> 4), hv);
+            store4<CT>(fr + RL.fc.o[rec::Sz] + frag_ofs<CP, HID>(i0, j0, l), szv);
           }
         }
       }
@@ -565,7 +647,12 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         f4 acc = zero4();
         mma_tile<CT, KC, KC>(acc, sH, HID, i0, sHk, HID, j0, HID);
         tile_each(acc, i0, j0, [&](int i, int j, float x) {
-          sP[(size_t)i * CP + j] = from_f<CT>(j <= i ? cf.c[i][j] * x : 0.f);
+          const CT pv = from_f<CT>(j <= i ? cf.c[i][j] * x : 0.f);
+          sP[(size_t)i * CP + j] = pv;
+          if (fr) {
+            frf[RL.ff.o[rec::HH] + (size_t)i * CP + j] = x;
+            fr[RL.fc.o[rec::PoT] + (size_t)j * CP + i] = pv;
+          }
         });
       }
     }
@@ -627,6 +714,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
           if (i < C)
             o[(size_t)(tok0 + i) * D + j] = cf.A[i] * a1[x][r] + cf.E[i] * a2[x][r] - a3[r];
+          if (fr) {
+            frf[RL.ff.o[rec::HW2] + (size_t)i * D + j] = a1[x][r];
+            frf[RL.ff.o[rec::HS2] + (size_t)i * D + j] = a2[x][r];
+          }
         }
       }
     }
