@@ -247,6 +247,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, dO, d, i0, R, d, j0);
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const f4 hh = load4<float>(fHH + frag_ofs<CP, CP>(i0 + 16 * rb, j0 + 16 * cb, l));
         f4 qv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -255,7 +256,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
           const bool lo = j <= ii;
           qv[r] = lo ? cf.c[ii][j] * x : 0.f;
           Q1[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
-          fCb[ii * Cp + j] = lo ? -fHH[ii * Cp + j] * x : 0.f;
+          fCb[ii * Cp + j] = lo ? -hh[r] * x : 0.f;
         }
         store4<CT>(Q1T + (size_t)j * Cp + i, qv);
       });
@@ -287,6 +288,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCC::RB, BCC::CB, H>(acc, Zb, h, i0, D1, h, j0);
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        const f4 xk = load4<float>(fXK + frag_ofs<CP, CP>(i0 + 16 * rb, j0 + 16 * cb, l));
         f4 qv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -295,7 +297,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
           const bool lo = j <= ii;
           qv[r] = lo ? cf.c[ii][j] * x : 0.f;
           Q2[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
-          if (lo) fCb[ii * Cp + j] -= fXK[ii * Cp + j] * x;
+          if (lo) fCb[ii * Cp + j] -= xk[r] * x;
         }
         store4<CT>(Q2T + (size_t)j * Cp + i, qv);
       });

@@ -297,40 +297,77 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         // the forward record: K, Q, N, Str, X, R, Hk, D1 and their scaled / transposed
         // forms from LDS (destination-ordered writes), per-position coefficients
         CT* const rp = fr;
-        for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
-          const int i = e / D;                     // row of the row-major element
-          const int jt = e / CP, it = e - jt * CP;  // transposed element [D][CP]
-          const float kx = to_f(sK[e]), rx = to_f(sR[e]);
-          rp[RL.fc.o[rec::K] + e] = sK[e];
-          rp[RL.fc.o[rec::KcC] + e] = from_f<CT>(cf.cC[i] * kx);
-          rp[RL.fc.o[rec::Kb] + e] = from_f<CT>(cf.bb[i] * kx);
-          rp[RL.fc.o[rec::R] + e] = sR[e];
-          rp[RL.fc.o[rec::RcC] + e] = from_f<CT>(cf.cC[i] * rx);
-          rp[RL.fc.o[rec::Rb] + e] = from_f<CT>(cf.bb[i] * rx);
-          rp[RL.fc.o[rec::X] + e] = sX[e];
-          const size_t et = (size_t)it * D + jt;
-          rp[RL.fc.o[rec::KT] + e] = sK[et];
-          rp[RL.fc.o[rec::RT] + e] = sR[et];
-          rp[RL.fc.o[rec::XT] + e] = sX[et];
-          rp[RL.fc.o[rec::XAT] + e] = from_f<CT>(cf.A[it] * to_f(sX[et]));
-          rp[RL.fc.o[rec::XET] + e] = from_f<CT>(cf.E[it] * to_f(sX[et]));
-          rp[RL.fc.o[rec::QT] + e] = sQ[et];
+        // eight destination elements per thread, 16-byte stores; transposed
+        // destinations gather their eight sources from LDS
+        auto st8 = [&](int field, size_t e0, const float (&x)[8]) {
+          bf16x8 v;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] = (__bf16)x[q];
+          *reinterpret_cast<bf16x8*>(rp + RL.fc.o[field] + e0) = v;
+        };
+        auto cp8 = [&](int field, size_t e0, const CT* src) {
+          *reinterpret_cast<bf16x8*>(rp + RL.fc.o[field] + e0) = *reinterpret_cast<const bf16x8*>(src);
+        };
+        for (int v = threadIdx.x; v < CP * D / 8; v += blockDim.x) {
+          const size_t e0 = (size_t)v * 8;
+          const int i = (int)(e0 / D);                       // row-major: one row
+          const int jt = (int)(e0 / CP), it = (int)(e0 % CP);  // transposed [D][CP]: rows it..it+7
+          cp8(rec::K, e0, sK + e0);
+          cp8(rec::R, e0, sR + e0);
+          cp8(rec::X, e0, sX + e0);
+          float kc[8], kb[8], rc[8], rb[8], kt[8], rt[8], xt[8], xa[8], xe[8], qt[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float kx = to_f(sK[e0 + q]), rx = to_f(sR[e0 + q]);
+            kc[q] = cf.cC[i] * kx;
+            kb[q] = cf.bb[i] * kx;
+            rc[q] = cf.cC[i] * rx;
+            rb[q] = cf.bb[i] * rx;
+            const size_t es = (size_t)(it + q) * D + jt;
+            kt[q] = to_f(sK[es]);
+            rt[q] = to_f(sR[es]);
+            xt[q] = to_f(sX[es]);
+            xa[q] = cf.A[it + q] * xt[q];
+            xe[q] = cf.E[it + q] * xt[q];
+            qt[q] = to_f(sQ[es]);
+          }
+          st8(rec::KcC, e0, kc);
+          st8(rec::Kb, e0, kb);
+          st8(rec::RcC, e0, rc);
+          st8(rec::Rb, e0, rb);
+          st8(rec::KT, e0, kt);
+          st8(rec::RT, e0, rt);
+          st8(rec::XT, e0, xt);
+          st8(rec::XAT, e0, xa);
+          st8(rec::XET, e0, xe);
+          st8(rec::QT, e0, qt);
           if (qk) {
-            rp[RL.fc.o[rec::N] + e] = sN[e];
-            rp[RL.fc.o[rec::NT] + e] = sNT[e];
+            cp8(rec::N, e0, sN + e0);
+            cp8(rec::NT, e0, sNT + e0);
           }
         }
         if (qk)
-          for (int e = threadIdx.x; e < CP * CP; e += blockDim.x) {
-            const int jt = e / CP, it = e - jt * CP;
-            rp[RL.fc.o[rec::StrT] + e] = sS[(size_t)it * CP + jt];
+          for (int v = threadIdx.x; v < CP * CP / 8; v += blockDim.x) {
+            const size_t e0 = (size_t)v * 8;
+            const int jt = (int)(e0 / CP), it = (int)(e0 % CP);
+            float x[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) x[q] = to_f(sS[(size_t)(it + q) * CP + jt]);
+            st8(rec::StrT, e0, x);
           }
-        for (size_t e = threadIdx.x; e < (size_t)CP * HID; e += blockDim.x) {
-          const size_t jt = e / CP, it = e - jt * CP;  // [HID][CP] element
-          const size_t i = e / HID, j = e - i * HID;   // [CP][HID] element
-          rp[RL.fc.o[rec::Hk] + e] = sHk[e];
-          rp[RL.fc.o[rec::HkT] + e] = sHk[it * HID + jt];
-          rp[RL.fc.o[rec::D1] + e] = sD1[j * CP + i];
+        for (int v = threadIdx.x; v < CP * HID / 8; v += blockDim.x) {
+          const size_t e0 = (size_t)v * 8;
+          const int jt = (int)(e0 / CP), it = (int)(e0 % CP);    // [HID][CP]
+          const int i = (int)(e0 / HID), j = (int)(e0 % HID);    // [CP][HID]
+          cp8(rec::Hk, e0, sHk + e0);
+          float ht[8], d1[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            ht[q] = to_f(sHk[(size_t)(it + q) * HID + jt]);
+            d1[q] = to_f(sD1[(size_t)(j + q) * CP + i]);
+          }
+          st8(rec::HkT, e0, ht);
+          st8(rec::D1, e0, d1);
         }
         if (threadIdx.x < CP) {
           const int i = threadIdx.x;
@@ -577,14 +614,17 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
         mma_tile<CT, KC, KC>(acc, sX, D, i0, sK, D, j0, D);
-        tile_each(acc, i0, j0, [&](int i, int j, float x) {
-          const CT pv = from_f<CT>(j <= i ? cf.c[i][j] * x : 0.f);
-          sP[(size_t)i * CP + j] = pv;
-          if (fr) {
-            frf[RL.ff.o[rec::XK] + (size_t)i * CP + j] = x;
-            fr[RL.fc.o[rec::PzT] + (size_t)j * CP + i] = pv;
-          }
-        });
+        f4 pv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
+          pv[r] = j <= i ? cf.c[i][j] * acc[r] : 0.f;
+          sP[(size_t)i * CP + j] = from_f<CT>(pv[r]);
+        }
+        if (fr) {
+          store4<float>(frf + RL.ff.o[rec::XK] + frag_ofs<CP, CP>(i0, j0, l), acc);
+          store4<CT>(fr + RL.fc.o[rec::PzT] + (size_t)(j0 + (l & 15)) * CP + i0 + 4 * (l >> 4), pv);
+        }
       }
     }
     {
@@ -646,14 +686,17 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
         mma_tile<CT, KC, KC>(acc, sH, HID, i0, sHk, HID, j0, HID);
-        tile_each(acc, i0, j0, [&](int i, int j, float x) {
-          const CT pv = from_f<CT>(j <= i ? cf.c[i][j] * x : 0.f);
-          sP[(size_t)i * CP + j] = pv;
-          if (fr) {
-            frf[RL.ff.o[rec::HH] + (size_t)i * CP + j] = x;
-            fr[RL.fc.o[rec::PoT] + (size_t)j * CP + i] = pv;
-          }
-        });
+        f4 pv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
+          pv[r] = j <= i ? cf.c[i][j] * acc[r] : 0.f;
+          sP[(size_t)i * CP + j] = from_f<CT>(pv[r]);
+        }
+        if (fr) {
+          store4<float>(frf + RL.ff.o[rec::HH] + frag_ofs<CP, CP>(i0, j0, l), acc);
+          store4<CT>(fr + RL.fc.o[rec::PoT] + (size_t)(j0 + (l & 15)) * CP + i0 + 4 * (l >> 4), pv);
+        }
       }
     }
     // O: one column strip of D per wave; the W2 / S2 strip is loaded in halves of HID

@@ -31,7 +31,7 @@ enum FwdCT {
 };
 // forward record, fp32
 enum FwdF {
-  XK, HH,        // C x C  X K^T, H Hk^T (unmasked)
+  XK, HH,        // C x C  X K^T, H Hk^T (unmasked; fragment-major over Blk<Cp, Cp>)
   HW2, HS2,      // C x d  H W2^T, H S2^T
   kn, cC, bb,    // C      key norms, cC, b
   sc,            // 4      A_C, B_C, E_C
