@@ -197,21 +197,19 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 #pragma unroll
           for (int q = 0; q < 8; ++q) ox[q] = 0.f;
         }
-        float w2[8], s2[8];
-        load8(fHW2 + en, w2);
-        load8(fHS2 + en, s2);
         float sa = 0.f, se = 0.f;
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-          const size_t et = (size_t)(j0 + q) * Cp + i;
+          const size_t et = (size_t)(j0 + q) * Cp + i;  // consecutive lanes: consecutive i
+          const float w2 = fHW2[et], s2 = fHS2[et];
           va[q] = cf.A[i] * ox[q];
           ve[q] = cf.E[i] * ox[q];
           dOT[et] = from_f<CT>(ox[q]);
           dOAT[et] = from_f<CT>(va[q]);
           dOET[et] = from_f<CT>(ve[q]);
           const float oq = to_f(from_f<CT>(ox[q]));  // dO as the contractions see it
-          sa += oq * w2[q];
-          se += oq * s2[q];
+          sa += oq * w2;
+          se += oq * s2;
         }
         store8<CT>(dO + en, ox);
         store8<CT>(dOA + en, va);

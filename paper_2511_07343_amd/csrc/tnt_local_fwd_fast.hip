@@ -757,10 +757,11 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
           if (i < C)
             o[(size_t)(tok0 + i) * D + j] = cf.A[i] * a1[x][r] + cf.E[i] * a2[x][r] - a3[r];
-          if (fr) {
-            frf[RL.ff.o[rec::HW2] + (size_t)i * D + j] = a1[x][r];
-            frf[RL.ff.o[rec::HS2] + (size_t)i * D + j] = a2[x][r];
-          }
+        }
+        if (fr) {  // transposed [D][CP]: the lane's four rows are contiguous
+          const size_t et = (size_t)(j0 + (l & 15)) * CP + i0 + 4 * (l >> 4);
+          store4<float>(frf + RL.ff.o[rec::HW2] + et, a1[x]);
+          store4<float>(frf + RL.ff.o[rec::HS2] + et, a2[x]);
         }
       }
     }

@@ -32,7 +32,7 @@ enum FwdCT {
 // forward record, fp32
 enum FwdF {
   XK, HH,        // C x C  X K^T, H Hk^T (unmasked; fragment-major over Blk<Cp, Cp>)
-  HW2, HS2,      // C x d  H W2^T, H S2^T
+  HW2, HS2,      // d x C  (H W2^T)^T, (H S2^T)^T
   kn, cC, bb,    // C      key norms, cC, b
   sc,            // 4      A_C, B_C, E_C
   FWD_F
