@@ -1051,15 +1051,15 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   return true;
 }
 
+// The shapes of the fixed-size bf16 forward (whose split passes write the forward
+// records these passes read); other shapes take the one-walk kernels.
 bool dispatch_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipStream_t st,
                     hipError_t* err, size_t* bytes) {
-  if (Dm.bf16)
-    return try_split<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes) ||
-           try_split<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, Dm, units, ws, st, err, bytes) ||
-           try_split<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, Dm, units, ws, st, err, bytes) ||
-           try_split<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes);
-  return try_split<float, float, ACT_GELU, 16, 32, 16>(a, Dm, units, ws, st, err, bytes) ||
-         try_split<float, float, ACT_SILU, 16, 32, 16>(a, Dm, units, ws, st, err, bytes);
+  if (!Dm.bf16) return false;
+  return try_split<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes) ||
+         try_split<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, Dm, units, ws, st, err, bytes) ||
+         try_split<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, Dm, units, ws, st, err, bytes) ||
+         try_split<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes);
 }
 
 }  // namespace
