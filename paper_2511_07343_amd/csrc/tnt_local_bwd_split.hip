@@ -75,7 +75,8 @@ constexpr size_t split_a_lds() {
 // pass B: a CP x H compute-type slot (Gbar, then Zkbar); T3, T4 and T5, T6
 // (fragment-major fp32, CP x D each; the T5/T6 space holds Zkbar^T, H x CP
 // compute type, from phase 3 on); Ykbar and Ykbar^T (CP x D compute type each);
-// per-column-tile partial row sums for cC_bar, b_bar ((D/16) x CP fp32 each);
+// per-column-tile partial row sums for cC_bar, b_bar (K . T3, K . T4, R . T5, R . T6:
+// (D/16) x CP fp32 each);
 // Gbar^T (H x CP compute type)
 template <typename CT, int CP, int D, int H>
 struct SplitBLds {
@@ -87,7 +88,9 @@ struct SplitBLds {
   static constexpr size_t ykbt = ykb + (size_t)CP * D * sizeof(CT);
   static constexpr size_t pc = ykbt + (size_t)CP * D * sizeof(CT);
   static constexpr size_t pb = pc + (size_t)(D / 16) * CP * sizeof(float);
-  static constexpr size_t gbt = pb + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t pc2 = pb + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t pb2 = pc2 + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t gbt = pb2 + (size_t)(D / 16) * CP * sizeof(float);
   static constexpr size_t total = gbt + (size_t)H * CP * sizeof(CT);
 };
 template <typename CT, int CP, int D, int H>
@@ -424,6 +427,40 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
   }
 }
 
+// Two products sharing their A operand over all CP rows, for one 16-column strip
+// j0 of the outputs: t0 += A B0[j0.., :]^T, t1 += A B1[j0.., :]^T (A rows and B rows
+// contraction-contiguous, K long).  The K steps go in groups of G with every
+// load of a group in flight before its MFMAs.
+template <typename CT, int RBN, int K, int G, typename EB>
+__device__ __forceinline__ void mma_pair(f4 (&t0)[RBN], f4 (&t1)[RBN], const CT* A, int lda,
+                                         const EB* B0, const EB* B1, int ldb, int j0) {
+  typedef Mma<CT> MM;
+  const int l = lane_id_local();
+  const int ko = MM::kofs(l);
+  constexpr int NS = K / MM::KS;
+  static_assert(K % MM::KS == 0 && NS % G == 0, "whole groups of K steps");
+#pragma unroll 1
+  for (int g0 = 0; g0 < NS; g0 += G) {
+    typename MM::frag fa[G][RBN], f0[G], f1[G];
+#pragma unroll
+    for (int st = 0; st < G; ++st) {
+      const int k0 = (g0 + st) * MM::KS + ko;
+#pragma unroll
+      for (int r = 0; r < RBN; ++r)
+        fa[st][r] = MM::template load<KC>(A, lda, 16 * r + (l & 15), k0, K, nullptr);
+      f0[st] = MM::template load<KC>(B0, ldb, j0 + (l & 15), k0, K, nullptr);
+      f1[st] = MM::template load<KC>(B1, ldb, j0 + (l & 15), k0, K, nullptr);
+    }
+#pragma unroll
+    for (int st = 0; st < G; ++st)
+#pragma unroll
+      for (int r = 0; r < RBN; ++r) {
+        MM::mma(t0[r], fa[st][r], f0[st]);
+        MM::mma(t1[r], fa[st][r], f1[st]);
+      }
+  }
+}
+
 // ===========================================================================
 // pass B: the carried adjoint, walked back through a unit's chunks
 // ===========================================================================
@@ -444,6 +481,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
   CT* const YkbT = reinterpret_cast<CT*>(smem + LB::ykbt);
   float* const pC = reinterpret_cast<float*>(smem + LB::pc);
   float* const pB = reinterpret_cast<float*>(smem + LB::pb);
+  float* const pC2 = reinterpret_cast<float*>(smem + LB::pc2);
+  float* const pB2 = reinterpret_cast<float*>(smem + LB::pb2);
   CT* const GbT = reinterpret_cast<CT*>(smem + LB::gbt);
 
   const Dims Dm = a.D;
@@ -553,38 +592,43 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         dpart[2][wave_id()] = pb;
       }
     }
-    // T3 = D1 W1bar', T4 = D1 S1bar', T5 = Hk W2bar'^T, T6 = Hk S2bar'^T  (C x d)
-    for_blocks<CP, D>([&](int i0, int j0) {
-      f4 a3[BCD::RB][BCD::CB], a4[BCD::RB][BCD::CB], a5[BCD::RB][BCD::CB], a6[BCD::RB][BCD::CB];
-      zero_blk(a3);
-      zero_blk(a4);
-      zero_blk(a5);
-      zero_blk(a6);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a3, D1, h, i0, Wb1T, h, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a4, D1, h, i0, Sb1T, h, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a5, Hk, h, i0, Wb2, h, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a6, Hk, h, i0, Sb2, h, j0);
-      // kept in LDS at their fragment positions; the cC_bar / b_bar row dots
-      // (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns
-      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const size_t fo = fofsD(i0, j0, rb, cb);
-        store4<float>(fT3 + fo, a3[rb][cb]);
-        store4<float>(fT4 + fo, a4[rb][cb]);
-        store4<float>(fT5 + fo, a5[rb][cb]);
-        store4<float>(fT6 + fo, a6[rb][cb]);
+    // T3 = D1 W1bar', T4 = D1 S1bar' (waves 0-3), T5 = Hk W2bar'^T, T6 = Hk S2bar'^T (waves
+    // 4-7), C x d each: a wave takes one 16-column strip of a pair over all rows, the pair
+    // sharing its A fragments.  Kept in LDS at their fragment positions; the cC_bar / b_bar
+    // row dots (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns.
+    {
+      static_assert(D == 64, "two pairs of four column strips for eight waves");
+      constexpr int RBN = CP / 16;
+      const int pair = wave_id() >> 2, j0 = 16 * (wave_id() & 3);
+      f4 t0[RBN], t1[RBN];
+#pragma unroll
+      for (int r = 0; r < RBN; ++r) t0[r] = t1[r] = zero4();
+      if (pair == 0)
+        mma_pair<CT, RBN, H, 4>(t0, t1, D1, h, Wb1T, Sb1T, h, j0);
+      else
+        mma_pair<CT, RBN, H, 4>(t0, t1, Hk, h, Wb2, Sb2, h, j0);
+      const CT* M = pair == 0 ? K : R;
+      float* const q0 = pair == 0 ? pC : pC2;
+      float* const q1 = pair == 0 ? pB : pB2;
+      float* const f0 = pair == 0 ? fT3 : fT5;
+      float* const f1 = pair == 0 ? fT4 : fT6;
+#pragma unroll
+      for (int rb = 0; rb < RBN; ++rb) {
+        const size_t fo = frag_ofs<CP, D>(16 * rb, j0, l);
+        store4<float>(f0 + fo, t0[rb]);
+        store4<float>(f1 + fo, t1[rb]);
+        const int i = 16 * rb + 4 * (l >> 4), j = j0 + (l & 15);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const size_t e = (size_t)(i + r) * d + j;
-          const float kx = to_f(K[e]), rx = to_f(R[e]);
-          const float sc_ = sum16b(kx * a3[rb][cb][r] + rx * a5[rb][cb][r]);
-          const float sb_ = sum16b(kx * a4[rb][cb][r] + rx * a6[rb][cb][r]);
+          const float mx = to_f(M[(size_t)(i + r) * d + j]);
+          const float s0 = sum16b(mx * t0[rb][r]), s1 = sum16b(mx * t1[rb][r]);
           if ((l & 15) == 0) {
-            pC[(j >> 4) * Cp + i + r] = sc_;
-            pB[(j >> 4) * Cp + i + r] = sb_;
+            q0[(j >> 4) * Cp + i + r] = s0;
+            q1[(j >> 4) * Cp + i + r] = s1;
           }
         }
-      });
-    });
+      }
+    }
     // D1bar = -Pz^T Zbar - diag(cC) K W1bar'^T - diag(b) K S1bar'^T ; Gbar = D1bar * s'(Zk);
     // Hkbar so far = -Q1^T H - diag(cC) R W2bar' - diag(b) R S2bar' ; the Zkbar terms known
     // now, D1bar * G * s''(Zk) + Hkbar * s'(Zk), are kept per fragment
@@ -621,8 +665,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       float sc_ = 0.f, sb_ = 0.f;
 #pragma unroll
       for (int q = 0; q < (d >> 4); ++q) {  // fixed order: deterministic
-        sc_ += pC[q * Cp + i];
-        sb_ += pB[q * Cp + i];
+        sc_ += pC[q * Cp + i] + pC2[q * Cp + i];
+        sb_ += pB[q * Cp + i] + pB2[q * Cp + i];
       }
       BQF_(gCC)[i] = -sc_;
       BQF_(gB)[i] = -sb_;
