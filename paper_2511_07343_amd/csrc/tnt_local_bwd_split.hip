@@ -430,34 +430,58 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 // Two products sharing their A operand over all CP rows, for one 16-column strip
 // j0 of the outputs: t0 += A B0[j0.., :]^T, t1 += A B1[j0.., :]^T (A rows and B rows
 // contraction-contiguous, K long).  The K steps go in groups of G with every
-// load of a group in flight before its MFMAs.
-template <typename CT, int RBN, int K, int G, typename EB>
-__device__ __forceinline__ void mma_pair(f4 (&t0)[RBN], f4 (&t1)[RBN], const CT* A, int lda,
-                                         const EB* B0, const EB* B1, int ldb, int j0) {
-  typedef Mma<CT> MM;
+// load of a group in flight before its MFMAs.  Alongside, the strip's share of
+// the elementwise products with two same-layout matrices S0, S1:
+// pa += B0 . S0, pe += B0 . S1, pb += B1 . S1.
+template <typename E> __device__ __forceinline__ float raw_elem(const RawFrag<__bf16, E>& f, int q);
+template <> __device__ __forceinline__ float raw_elem(const RawFrag<__bf16, __bf16>& f, int q) {
+  return (float)f.v[q];
+}
+template <> __device__ __forceinline__ float raw_elem(const RawFrag<__bf16, float>& f, int q) {
+  return q < 4 ? f.a[q] : f.b[q - 4];
+}
+template <int RBN, int K, int G, typename EB>
+__device__ __forceinline__ void mma_pair_dots(f4 (&t0)[RBN], f4 (&t1)[RBN], const __bf16* A,
+                                              int lda, const EB* B0, const EB* B1, int ldb,
+                                              int j0, const EB* S0, const EB* S1, float& pa,
+                                              float& pe, float& pb) {
+  typedef Mma<__bf16> MM;
   const int l = lane_id_local();
-  const int ko = MM::kofs(l);
+  const int ko = MM::kofs(l), jr = j0 + (l & 15);
   constexpr int NS = K / MM::KS;
   static_assert(K % MM::KS == 0 && NS % G == 0, "whole groups of K steps");
 #pragma unroll 1
   for (int g0 = 0; g0 < NS; g0 += G) {
-    typename MM::frag fa[G][RBN], f0[G], f1[G];
+    typename MM::frag fa[G][RBN];
+    RawFrag<__bf16, EB> f0[G], f1[G], s0[G], s1[G];
 #pragma unroll
     for (int st = 0; st < G; ++st) {
       const int k0 = (g0 + st) * MM::KS + ko;
 #pragma unroll
       for (int r = 0; r < RBN; ++r)
         fa[st][r] = MM::template load<KC>(A, lda, 16 * r + (l & 15), k0, K, nullptr);
-      f0[st] = MM::template load<KC>(B0, ldb, j0 + (l & 15), k0, K, nullptr);
-      f1[st] = MM::template load<KC>(B1, ldb, j0 + (l & 15), k0, K, nullptr);
+      f0[st].load(B0, ldb, jr, k0);
+      f1[st].load(B1, ldb, jr, k0);
+      s0[st].load(S0, ldb, jr, k0);
+      s1[st].load(S1, ldb, jr, k0);
     }
 #pragma unroll
-    for (int st = 0; st < G; ++st)
+    for (int st = 0; st < G; ++st) {
+      const auto b0 = f0[st].get(), b1 = f1[st].get();
 #pragma unroll
       for (int r = 0; r < RBN; ++r) {
-        MM::mma(t0[r], fa[st][r], f0[st]);
-        MM::mma(t1[r], fa[st][r], f1[st]);
+        MM::mma(t0[r], fa[st][r], b0);
+        MM::mma(t1[r], fa[st][r], b1);
       }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float x0 = raw_elem(f0[st], q), x1 = raw_elem(f1[st], q);
+        const float y0 = raw_elem(s0[st], q), y1 = raw_elem(s1[st], q);
+        pa += x0 * y0;
+        pe += x0 * y1;
+        pb += x1 * y1;
+      }
+    }
   }
 }
 
@@ -541,7 +565,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     const int tok0 = s * Dm.S + n * C;
     const int l = lane_id_local();
     const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
-    const float *W2 = st + hd;
+    const float *W2 = st + hd, *S2 = st + 3 * hd;
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
     const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd;
     using BCD = Blk<CP, D>;
@@ -555,34 +579,33 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       return ((size_t)((blk * BCD::RB + rb) * BCD::CB + cb) * WAVE + l) * 4;
     };
 
-    // ---- phase 1: chunk coefficients; adjoint . state dot products (dA_C,
-    // dE_C, dB_C); T3..T6; D1bar -> Gbar; the first part of Hkbar
+    // ---- phase 1: chunk coefficients; T3..T6 with the adjoint . state dot products
+    // (dA_C, dE_C, dB_C); D1bar -> Gbar; the first part of Hkbar
     if (threadIdx.x < Cp) {
       sC[threadIdx.x] = RF_(cC)[threadIdx.x];
       sB[threadIdx.x] = RF_(bb)[threadIdx.x];
     }
     if (threadIdx.x < 3) sc3[threadIdx.x] = RF_(sc)[threadIdx.x];
+    // T3 = D1 W1bar', T4 = D1 S1bar' (waves 0-3), T5 = Hk W2bar'^T, T6 = Hk S2bar'^T (waves
+    // 4-7), C x d each: a wave takes one 16-column strip of a pair over all rows, the pair
+    // sharing its A fragments.  Kept in LDS at their fragment positions; the cC_bar / b_bar
+    // row dots (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns.
+    // The strips of the adjoint's B operands cover it whole: the adjoint . state products
+    // are taken from the same fragments (W1bar', S1bar' as bf16 with W1, S1 in the
+    // transposed bf16 copy of the state; W2bar', S2bar' and W2, S2 in fp32).
     {
-      float pa = 0.f, pe = 0.f, pb = 0.f;
-      const CT* adjT = Wb1T;  // Wb1^T, Sb1^T, Wb2^T, Sb2^T contiguous
-#pragma unroll 2
-      for (size_t e = threadIdx.x * 8; e < hd; e += blockDim.x * 8) {
-        float w1[8], s1[8], w2[8], s2[8], b1[8], c1[8], b2[8], c2[8];
-        load8(W1T + e, w1);
-        load8(S1T + e, s1);
-        load8(W2T + e, w2);
-        load8(S2T + e, s2);
-        load8(adjT + e, b1);
-        load8(adjT + hd + e, c1);
-        load8(adjT + 2 * hd + e, b2);
-        load8(adjT + 3 * hd + e, c2);
+      static_assert(D == 64, "two pairs of four column strips for eight waves");
+      static_assert(sizeof(CT) == 2, "bf16 operands");
+      constexpr int RBN = CP / 16;
+      const int pair = wave_id() >> 2, j0 = 16 * (wave_id() & 3);
+      f4 t0[RBN], t1[RBN];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          pa += b1[q] * w1[q] + b2[q] * w2[q];
-          pe += b1[q] * s1[q] + b2[q] * s2[q];
-          pb += c1[q] * s1[q] + c2[q] * s2[q];
-        }
-      }
+      for (int r = 0; r < RBN; ++r) t0[r] = t1[r] = zero4();
+      float pa = 0.f, pe = 0.f, pb = 0.f;
+      if (pair == 0)
+        mma_pair_dots<RBN, H, 4>(t0, t1, D1, h, Wb1T, Sb1T, h, j0, W1T, S1T, pa, pe, pb);
+      else
+        mma_pair_dots<RBN, H, 2>(t0, t1, Hk, h, Wb2, Sb2, h, j0, W2, S2, pa, pe, pb);
       pa = wave_sum(pa);
       pe = wave_sum(pe);
       pb = wave_sum(pb);
@@ -591,22 +614,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         dpart[1][wave_id()] = pe;
         dpart[2][wave_id()] = pb;
       }
-    }
-    // T3 = D1 W1bar', T4 = D1 S1bar' (waves 0-3), T5 = Hk W2bar'^T, T6 = Hk S2bar'^T (waves
-    // 4-7), C x d each: a wave takes one 16-column strip of a pair over all rows, the pair
-    // sharing its A fragments.  Kept in LDS at their fragment positions; the cC_bar / b_bar
-    // row dots (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns.
-    {
-      static_assert(D == 64, "two pairs of four column strips for eight waves");
-      constexpr int RBN = CP / 16;
-      const int pair = wave_id() >> 2, j0 = 16 * (wave_id() & 3);
-      f4 t0[RBN], t1[RBN];
-#pragma unroll
-      for (int r = 0; r < RBN; ++r) t0[r] = t1[r] = zero4();
-      if (pair == 0)
-        mma_pair<CT, RBN, H, 4>(t0, t1, D1, h, Wb1T, Sb1T, h, j0);
-      else
-        mma_pair<CT, RBN, H, 4>(t0, t1, Hk, h, Wb2, Sb2, h, j0);
       const CT* M = pair == 0 ? K : R;
       float* const q0 = pair == 0 ? pC : pC2;
       float* const q1 = pair == 0 ? pB : pB2;
