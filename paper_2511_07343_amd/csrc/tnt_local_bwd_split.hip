@@ -66,11 +66,15 @@ constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
 constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
 
 // dynamic LDS of pass A: cbar (CP x CP fp32), partial row sums pA, pE
-// ((D/16) x CP fp32 each), one CP x H compute-type slot (Zbar)
+// ((D/16) x CP fp32 each), one CP x H compute-type slot (Zbar), the chunk's
+// compute-type temporaries (dO and its scaled forms, Xbar, Q1, Q2, dXN, ...)
 template <typename CT, int CP, int D, int H>
 constexpr size_t split_a_lds() {
-  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + (size_t)CP * H * sizeof(CT);
+  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + (size_t)CP * H * sizeof(CT) +
+         make_split_layout(CP, D, H).ac.n * sizeof(CT);
 }
+// static LDS of pass A: the chunk coefficients and the per-row partial sums
+constexpr size_t SPLIT_A_STATIC = 24 * 1024;
 
 // pass B: a CP x H compute-type slot (Gbar, then Zkbar); T3, T4 and T5, T6
 // (fragment-major fp32, CP x D each; the T5/T6 space holds Zkbar^T, H x CP
@@ -111,7 +115,6 @@ constexpr size_t split_c_lds() {
 struct SplitPtrs {
   void* brec;       // CT   [units * nch][r.bc.n]  backward records
   float* brec_f;    // fp32 [units * nch][r.bf.n]
-  void* tmpA;       // CT   [SPLIT_GRID_A][ac.n]
   float* tmpA_f;    // fp32 [SPLIT_GRID_A][af.n]
   void* tmpB;       // CT   [units][bc.n]
   int units;
@@ -131,6 +134,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
   float* pA = fCb + Cp * Cp;
   float* pE = pA + (D / 16) * Cp;
   CT* Zb = reinterpret_cast<CT*>(pE + (D / 16) * Cp);  // C x h slot
+  CT* const ta = Zb + CP * H;                           // compute-type temporaries
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -140,7 +144,6 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
   constexpr size_t hd = (size_t)h * d;
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
-  CT* const ta0 = (CT*)P.tmpA + (size_t)blockIdx.x * Y.ac.n;
   float* const tf0 = P.tmpA_f + (size_t)blockIdx.x * Y.af.n;
 
   for (int t = blockIdx.x; t < total; t += gridDim.x) {
@@ -150,13 +153,11 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     const float* frf = a.frec_f + (size_t)t * Y.r.ff.n;
     CT* br = (CT*)P.brec + (size_t)t * Y.r.bc.n;
     float* brf = P.brec_f + (size_t)t * Y.r.bf.n;
-    CT* ta = ta0;
     float* tf = tf0;
     fr = launder_global(fr);
     frf = launder_global(frf);
     br = launder_global(br);
     brf = launder_global(brf);
-    ta = launder_global(ta);
     tf = launder_global(tf);
     const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
     const IO* dOg = (const IO*)a.dO + cbase * d;
@@ -1025,21 +1026,21 @@ namespace {
 
 template <typename CT, int CP, int D, int H>
 constexpr bool split_fits() {
-  // static LDS of pass A (Coef + norms) is under 40 KB; pass C's under 40 KB
-  return split_a_lds<CT, CP, D, H>() + 40 * 1024 <= 160 * 1024 &&
+  // pass C's static LDS is under 40 KB
+  return split_a_lds<CT, CP, D, H>() + SPLIT_A_STATIC <= 160 * 1024 &&
          split_b_lds<CT, CP, D, H>() + 2 * 1024 <= 160 * 1024 &&
          split_c_lds<CP, D>() + 40 * 1024 <= 160 * 1024;
 }
 
 struct SplitSizes {
-  size_t rec_ct, rec_f, a_ct, a_f, b_ct;  // elements
+  size_t rec_ct, rec_f, a_f, b_ct;  // elements
 };
 
 template <typename CT, int CP, int D, int H>
 SplitSizes split_sizes(int units, int nch) {
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const size_t t = (size_t)units * nch;
-  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n, (size_t)SPLIT_GRID_A * Y.ac.n, (size_t)SPLIT_GRID_A * Y.af.n,
+  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n, (size_t)SPLIT_GRID_A * Y.af.n,
                     (size_t)units * Y.bc.n};
 }
 
@@ -1047,7 +1048,7 @@ size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
 template <typename CT>
 size_t total_bytes(const SplitSizes& z) {
-  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) + up256(z.a_ct * sizeof(CT)) +
+  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) +
          up256(z.a_f * 4) + up256(z.b_ct * sizeof(CT));
 }
 
@@ -1057,7 +1058,6 @@ SplitPtrs carve(void* ws, const SplitSizes& z, int units) {
   SplitPtrs P{};
   P.brec = p; p += up256(z.rec_ct * sizeof(CT));
   P.brec_f = (float*)p; p += up256(z.rec_f * 4);
-  P.tmpA = p; p += up256(z.a_ct * sizeof(CT));
   P.tmpA_f = (float*)p; p += up256(z.a_f * 4);
   P.tmpB = p;
   P.units = units;
