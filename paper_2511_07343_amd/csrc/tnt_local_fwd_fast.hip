@@ -191,6 +191,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     const float* Mc = mst + (size_t)(n % a.nslots) * D * D;
     float* Mn = mst + (size_t)((n + 1) % a.nslots) * D * D;
     CT* const pkn = pku ? pku + (size_t)((n + 1) % a.nslots) * PS : nullptr;
+    const CT* const pkc = pku ? pku + (size_t)(n % a.nslots) * PS : nullptr;  // entry state, bf16 T
 
     // ---- stage Q, K (16-byte loads; rows >= C zero), key norms, gate coefficients
     {
@@ -634,7 +635,16 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int sidx = w + NW * y;
         if (sidx >= TNH) continue;
         typename Mma<CT>::frag bw[NKD], bs[NKD];
-        {
+        if constexpr (MODE == FWD_RET) {
+          // the walk's bf16 copies W1^T, S1^T [D][HID] (the same rounding as a
+          // conversion of the fp32 state at load): contraction-major reads, half the bytes
+#pragma unroll
+          for (int ks = 0; ks < NKD; ++ks) {
+            bw[ks] = Mma<CT>::template load<MC>(pkc, HID, sidx * 16 + (l & 15), ks * KS + ko, D, nullptr);
+            bs[ks] = Mma<CT>::template load<MC>(pkc + 2 * hd, HID, sidx * 16 + (l & 15), ks * KS + ko, D,
+                                                nullptr);
+          }
+        } else {
           RawFrag<CT, float> rw[NKD], rs[NKD];
 #pragma unroll
           for (int ks = 0; ks < NKD; ++ks) {
@@ -712,7 +722,16 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
       for (int hb = 0; hb < NKH; hb += HALF) {
         typename Mma<CT>::frag bw[HALF], bs[HALF];
-        {
+        if constexpr (MODE == FWD_RET) {  // W2^T, S2^T [HID][D] of the walk
+#pragma unroll
+          for (int kk = 0; kk < HALF; ++kk)
+            if (hb + kk < NKH) {
+              bw[kk] = Mma<CT>::template load<MC>(pkc + hd, D, cs * 16 + (l & 15), (hb + kk) * KS + ko,
+                                                  HID, nullptr);
+              bs[kk] = Mma<CT>::template load<MC>(pkc + 3 * hd, D, cs * 16 + (l & 15),
+                                                  (hb + kk) * KS + ko, HID, nullptr);
+            }
+        } else {
           RawFrag<CT, float> rw[HALF], rs[HALF];
 #pragma unroll
           for (int kk = 0; kk < HALF; ++kk)
