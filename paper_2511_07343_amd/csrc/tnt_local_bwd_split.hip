@@ -432,20 +432,15 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 // j0 of the outputs: t0 += A B0[j0.., :]^T, t1 += A B1[j0.., :]^T (A rows and B rows
 // contraction-contiguous, K long).  The K steps go in groups of G with every
 // load of a group in flight before its MFMAs.  Alongside, the strip's share of
-// the elementwise products with two same-layout matrices S0, S1:
+// the elementwise products with two compute-type matrices S0, S1 of the B
+// operands' shape (layout SL: KC as the B operands, MC transposed, leading
+// dimension lds), both sides as the MFMAs see them (compute type):
 // pa += B0 . S0, pe += B0 . S1, pb += B1 . S1.
-template <typename E> __device__ __forceinline__ float raw_elem(const RawFrag<__bf16, E>& f, int q);
-template <> __device__ __forceinline__ float raw_elem(const RawFrag<__bf16, __bf16>& f, int q) {
-  return (float)f.v[q];
-}
-template <> __device__ __forceinline__ float raw_elem(const RawFrag<__bf16, float>& f, int q) {
-  return q < 4 ? f.a[q] : f.b[q - 4];
-}
-template <int RBN, int K, int G, typename EB>
+template <int RBN, int K, int G, int SL, typename EB>
 __device__ __forceinline__ void mma_pair_dots(f4 (&t0)[RBN], f4 (&t1)[RBN], const __bf16* A,
                                               int lda, const EB* B0, const EB* B1, int ldb,
-                                              int j0, const EB* S0, const EB* S1, float& pa,
-                                              float& pe, float& pb) {
+                                              int j0, const __bf16* S0, const __bf16* S1,
+                                              int lds, float& pa, float& pe, float& pb) {
   typedef Mma<__bf16> MM;
   const int l = lane_id_local();
   const int ko = MM::kofs(l), jr = j0 + (l & 15);
@@ -453,31 +448,29 @@ __device__ __forceinline__ void mma_pair_dots(f4 (&t0)[RBN], f4 (&t1)[RBN], cons
   static_assert(K % MM::KS == 0 && NS % G == 0, "whole groups of K steps");
 #pragma unroll 1
   for (int g0 = 0; g0 < NS; g0 += G) {
-    typename MM::frag fa[G][RBN];
-    RawFrag<__bf16, EB> f0[G], f1[G], s0[G], s1[G];
+    typename MM::frag fa[G][RBN], f0[G], f1[G], s0[G], s1[G];
 #pragma unroll
     for (int st = 0; st < G; ++st) {
       const int k0 = (g0 + st) * MM::KS + ko;
 #pragma unroll
       for (int r = 0; r < RBN; ++r)
         fa[st][r] = MM::template load<KC>(A, lda, 16 * r + (l & 15), k0, K, nullptr);
-      f0[st].load(B0, ldb, jr, k0);
-      f1[st].load(B1, ldb, jr, k0);
-      s0[st].load(S0, ldb, jr, k0);
-      s1[st].load(S1, ldb, jr, k0);
+      f0[st] = MM::template load<KC>(B0, ldb, jr, k0, K, nullptr);
+      f1[st] = MM::template load<KC>(B1, ldb, jr, k0, K, nullptr);
+      s0[st] = MM::template load<SL>(S0, lds, jr, k0, K, nullptr);
+      s1[st] = MM::template load<SL>(S1, lds, jr, k0, K, nullptr);
     }
 #pragma unroll
     for (int st = 0; st < G; ++st) {
-      const auto b0 = f0[st].get(), b1 = f1[st].get();
 #pragma unroll
       for (int r = 0; r < RBN; ++r) {
-        MM::mma(t0[r], fa[st][r], b0);
-        MM::mma(t1[r], fa[st][r], b1);
+        MM::mma(t0[r], fa[st][r], f0[st]);
+        MM::mma(t1[r], fa[st][r], f1[st]);
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        const float x0 = raw_elem(f0[st], q), x1 = raw_elem(f1[st], q);
-        const float y0 = raw_elem(s0[st], q), y1 = raw_elem(s1[st], q);
+        const float x0 = (float)f0[st][q], x1 = (float)f1[st][q];
+        const float y0 = (float)s0[st][q], y1 = (float)s1[st][q];
         pa += x0 * y0;
         pe += x0 * y1;
         pb += x1 * y1;
@@ -565,8 +558,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
              *XET = R_(XET), *dOAT = BQ_(dOAT), *dOET = BQ_(dOET);
     const int tok0 = s * Dm.S + n * C;
     const int l = lane_id_local();
-    const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
-    const float *W2 = st + hd, *S2 = st + 3 * hd;
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
     const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd;
     using BCD = Blk<CP, D>;
@@ -592,8 +583,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     // sharing its A fragments.  Kept in LDS at their fragment positions; the cC_bar / b_bar
     // row dots (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns.
     // The strips of the adjoint's B operands cover it whole: the adjoint . state products
-    // are taken from the same fragments (W1bar', S1bar' as bf16 with W1, S1 in the
-    // transposed bf16 copy of the state; W2bar', S2bar' and W2, S2 in fp32).
+    // are taken from the same fragments, both sides as the MFMAs see them (the adjoint
+    // rounded to the compute type, the state from its transposed compute-type copy).
     {
       static_assert(D == 64, "two pairs of four column strips for eight waves");
       static_assert(sizeof(CT) == 2, "bf16 operands");
@@ -604,9 +595,9 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       for (int r = 0; r < RBN; ++r) t0[r] = t1[r] = zero4();
       float pa = 0.f, pe = 0.f, pb = 0.f;
       if (pair == 0)
-        mma_pair_dots<RBN, H, 4>(t0, t1, D1, h, Wb1T, Sb1T, h, j0, W1T, S1T, pa, pe, pb);
+        mma_pair_dots<RBN, H, 4, KC>(t0, t1, D1, h, Wb1T, Sb1T, h, j0, W1T, S1T, h, pa, pe, pb);
       else
-        mma_pair_dots<RBN, H, 2>(t0, t1, Hk, h, Wb2, Sb2, h, j0, W2, S2, pa, pe, pb);
+        mma_pair_dots<RBN, H, 4, MC>(t0, t1, Hk, h, Wb2, Sb2, h, j0, W2T, S2T, d, pa, pe, pb);
       pa = wave_sum(pa);
       pe = wave_sum(pe);
       pb = wave_sum(pb);
@@ -690,7 +681,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       zero_blk(a1);
       zero_blk(a2);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, CP>(a1, PoT, Cp, i0, dOT, Cp, j0);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Gb, h, i0, W2, h, j0);
+      mma_blk<CT, KC, MC, BCD::RB, BCD::CB, H>(a2, Gb, h, i0, W2T, d, j0);
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         const size_t fo = fofsD(i0, j0, rb, cb);
         const f4 t5 = load4<float>(fT5 + fo), t6 = load4<float>(fT6 + fo);
@@ -1090,7 +1081,13 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, D, H>(),
                    lds_c = split_c_lds<CP, D>();
   hipLaunchKernelGGL(ka, dim3(std::min(total, SPLIT_GRID_A)), dim3(512), lds_a, st, *a, P);
-  if (a->pass_a_done) hipEventRecord(a->pass_a_done, st);
+  if (a->pass_a_done) {
+    const hipError_t e = hipEventRecord(a->pass_a_done, st);
+    if (e != hipSuccess) {
+      *err = e;
+      return true;
+    }
+  }
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
   if (Dm.qk_proj && Dm.qk_scope == 0) {
     const size_t thr = (size_t)units * D * D;
