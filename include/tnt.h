@@ -105,7 +105,16 @@ size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind);
 /* Bytes of the optional saved-state buffer: the chunk-entry states of every
  * memory (fp32, plus transposed copies of the local memories' states in the
  * compute type), written by tnt_mem_fwd and read by tnt_mem_bwd so that the
- * backward does not recompute the forward's state chain.  Opaque layout. */
+ * backward does not recompute the forward's state chain.  Opaque layout.  For
+ * the local-memory shapes whose backward runs chunk-parallel from forward
+ * records (also saved here), the backward reads the local states only through
+ * their compute-type copies, and the forward leaves their fp32 slots unwritten
+ * beyond a two-slot ring.  The environment switches TNT_GENERIC_KERNELS and
+ * TNT_LOCAL_BWD_SINGLE (kernel selection for testing) make the forward write
+ * every fp32 slot, which the kernels they select read: set them alike for a
+ * tnt_mem_fwd and the tnt_mem_bwd that uses its buffer (the size and layout do
+ * not depend on them); with them differing, that backward reads unwritten
+ * slots (inside the buffer) and its results are undefined. */
 size_t tnt_mem_saved_size(const tnt_config* cfg);
 
 /* Forward pass: o = TNT layer output (see the file comment).

@@ -68,6 +68,7 @@ struct Layout {
   size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], sv_t[TNT_MAX_LOCAL],
       sv_fr[TNT_MAX_LOCAL], sv_frf[TNT_MAX_LOCAL], saved_bytes;
   int g_chunks, l_units[TNT_MAX_LOCAL], l_chunks[TNT_MAX_LOCAL];
+  int l_fslots[TNT_MAX_LOCAL];  // 0: every fp32 chunk-entry state saved; else the walk's ring
   // forward workspace
   size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL],
       w_fsplit[TNT_MAX_LOCAL], w_ring,
@@ -81,6 +82,9 @@ struct Layout {
       bwd_re_bytes;
   BwdLayout blay[TNT_MAX_LOCAL];
 };
+
+int generic_only();
+int single_walk_only();
 
 Layout layout_of(const tnt_config* c) {
   Layout y{};
@@ -103,6 +107,14 @@ Layout layout_of(const tnt_config* c) {
   for (int i = 0; i < c->n_local; ++i) {
     y.l_units[i] = y.BH * (c->L / c->S_L[i]);
     y.l_chunks[i] = c->S_L[i] / c->C_L[i];
+    // Shapes with both chunk-parallel kernels save forward records, and their
+    // backward reads the states only through the compute-type transposes: the
+    // walk then cycles its fp32 carry through two slots instead of writing every
+    // slot (unless a switch asks for the kernels that recompute from the fp32
+    // states).  The space stays reserved, so the layout does not depend on it.
+    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+    const bool recs = local_fwd_split_bytes(D, y.l_units[i]) && local_bwd_split_bytes(D, y.l_units[i]);
+    y.l_fslots[i] = (recs && !single_walk_only() && !generic_only()) ? 2 : 0;
     y.sv_l[i] = off;
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * 4 * y.hd * f);
     y.sv_m[i] = off;
@@ -110,9 +122,8 @@ Layout layout_of(const tnt_config* c) {
     y.sv_t[i] = off;  // CT transposes of every slot, written by the forward
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * (4 * y.hd + dd) * cts);
     // forward records of the chunk-parallel passes (shapes with both split kernels)
-    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
     y.sv_fr[i] = y.sv_frf[i] = SIZE_MAX;
-    if (local_fwd_split_bytes(D, y.l_units[i]) && local_bwd_split_bytes(D, y.l_units[i])) {
+    if (recs) {
       const rec::RecLayout R = rec::make_rec_layout(D.Cp, D.d, D.hid);
       const size_t items = (size_t)y.l_units[i] * y.l_chunks[i];
       y.sv_fr[i] = off; off += up(items * R.fc.n * cts);
@@ -328,6 +339,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.frec = (sv && y.sv_fr[i] != SIZE_MAX) ? (void*)(sv + y.sv_fr[i]) : nullptr;
     a.frec_f = (sv && y.sv_frf[i] != SIZE_MAX) ? (float*)(sv + y.sv_frf[i]) : nullptr;
     a.nslots = sv ? y.l_chunks[i] + 1 : 2;
+    a.fslots = sv ? y.l_fslots[i] : 0;
     a.scratch = ws + y.w_scr[i];
     a.fsplit = y.w_fsplit[i] != SIZE_MAX ? (void*)(ws + y.w_fsplit[i]) : nullptr;
     a.plan = y.lplan[i];
@@ -368,6 +380,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.states = (const float*)(sv + y.sv_l[i]);
     a.mstates = (const float*)(sv + y.sv_m[i]);
     a.nslots = y.l_chunks[i] + 1;
+    a.fslots = y.l_fslots[i];
     a.statesT = sv + y.sv_t[i];
     a.frec = y.sv_fr[i] != SIZE_MAX ? (const void*)(sv + y.sv_fr[i]) : nullptr;
     a.frec_f = y.sv_frf[i] != SIZE_MAX ? (const float*)(sv + y.sv_frf[i]) : nullptr;

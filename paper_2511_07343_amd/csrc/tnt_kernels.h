@@ -45,6 +45,10 @@ struct LocalFwdArgs {
   void* frec; float* frec_f;                             // null, or the forward records (saved
                                                          // buffer) the backward passes read
   int nslots;
+  int fslots;                                            // 0: the walk writes every fp32 slot;
+                                                         // else it cycles through the first
+                                                         // fslots of each unit's nslots (the
+                                                         // backward then reads only statesT)
   void* scratch;                                         // units * plan.elems CT
   LocalPlan plan;
   Dims D;
@@ -59,6 +63,8 @@ struct LocalBwdArgs {
   const void* statesT;                                   // CT [units][nslots][4*hid*d + d*d]:
                                                          // W1^T, W2^T, S1^T, S2^T, M^T
   int nslots;
+  int fslots;                                            // nonzero: `states` holds only the walk's
+                                                         // ring, not every chunk-entry state
   float* adj;                                            // [units][4*hid*d] adjoint state
   float* madj;                                           // [units][2][d*d]
   float* dq_part; float* dk_part; float* dv_part;        // [B][H][L][d] fp32

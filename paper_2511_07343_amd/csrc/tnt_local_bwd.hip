@@ -590,6 +590,9 @@ static bool try_bwd(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st) {
   hipError_t e = hipSuccess;
   if (!a.force_generic && !a.single_walk && launch_local_bwd_split(a, units, st, &e)) return e;
+  // the other kernels recompute from the fp32 chunk-entry states, which a forward
+  // that kept them in a ring did not save
+  if (a.fslots) return hipErrorInvalidValue;
   if (a.pass_a_done) {
     e = hipEventRecord(a.pass_a_done, st);
     if (e != hipSuccess) return e;

@@ -137,6 +137,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const float* lr = a.lr + chain * Dm.L;
   const float* mom = a.mom + chain * Dm.L;
   const float* dec = a.decay + chain * Dm.L;
+  const int fsl = a.fslots ? a.fslots : a.nslots;  // fp32 state slots the walk cycles through
   float* st = a.states + (size_t)u * a.nslots * 4 * hd;
   float* mst = a.mstates + (size_t)u * a.nslots * D * D;
   constexpr size_t PS = 4 * hd + (size_t)D * D;  // CT elements per transposed slot
@@ -184,8 +185,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     CT* const fr = (MODE != FWD_FULL && a.frec) ? (CT*)a.frec + ((size_t)u * nch + n) * RL.fc.n : nullptr;
     float* const frf = fr ? a.frec_f + ((size_t)u * nch + n) * RL.ff.n : nullptr;
     const int tok0 = s * Dm.S + n * C;
-    const float* cur = st + (size_t)(n % a.nslots) * 4 * hd;
-    float* nxt = st + (size_t)((n + 1) % a.nslots) * 4 * hd;
+    const float* cur = st + (size_t)(n % fsl) * 4 * hd;
+    float* nxt = st + (size_t)((n + 1) % fsl) * 4 * hd;
     const float *W1 = cur, *W2 = cur + hd, *S1 = cur + 2 * hd, *S2 = cur + 3 * hd;
     float *W1n = nxt, *W2n = nxt + hd, *S1n = nxt + 2 * hd, *S2n = nxt + 3 * hd;
     const float* Mc = mst + (size_t)(n % a.nslots) * D * D;

@@ -87,6 +87,19 @@ def test_forward_save_and_ring_agree(cfg):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("cfg", SAVE_RING[2:], ids=lambda c: c.name)
+def test_forward_state_ring_agrees(cfg, monkeypatch):
+    """With forward records saved, the walk cycles its fp32 carry through two
+    slots; a kernel-selection switch makes it write every slot instead.  The
+    outputs are the same bits either way."""
+    inp = make_inputs(cfg, 106)
+    print(f"\n[case] state ring {cfg.name}", flush=True)
+    a, _ = gpu_forward(cfg, inp, save=True)
+    monkeypatch.setenv("TNT_LOCAL_BWD_SINGLE", "1")
+    b, _ = gpu_forward(cfg, inp, save=True)
+    assert np.array_equal(a, b)
+
+
 def test_forward_deterministic():
     cfg = SMALL[2]
     inp = make_inputs(cfg, 103)
