@@ -119,7 +119,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   CT *sHk = L + Ly::Hk, *sD1 = L + Ly::D1, *sU = L + Ly::U, *sX = L + Ly::X, *sK = L + Ly::K,
      *sR = L + Ly::R, *sP = L + Ly::P;
   CT *sQ = L + Ly::uQ, *sN = L + Ly::uN, *sNT = L + Ly::uNT, *sS = L + Ly::uS;
-  CT* sW2 = sU;  // chunk-entry W2 copy [D][HID]
+  CT* sW2 = sU;  // chunk-entry W2 copy: [D][HID], or W2^T [HID][D] in the walk
   CT* sH = sU;
 
   const Dims Dm = a.D;
@@ -389,7 +389,19 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     CT spr[NS][TMC][4];  // s'(Zk) in the compute type
     {
       typename Mma<CT>::frag bw[NS][NKD];
-      {
+      if constexpr (MODE == FWD_CHAIN) {
+        // W1 from the entry state's compute-type transpose W1^T [D][HID] (written by the
+        // previous step's carry; the same rounding as a conversion of the fp32 state)
+#pragma unroll
+        for (int y = 0; y < NS; ++y) {
+          const int sidx = w + NW * y;
+          if (sidx < TNH)
+#pragma unroll
+            for (int ks = 0; ks < NKD; ++ks)
+              bw[y][ks] = Mma<CT>::template load<MC>(pkc, HID, sidx * 16 + (l & 15), ks * KS + ko, D,
+                                                     nullptr);
+        }
+      } else {
         RawFrag<CT, float> raw[NS][NKD];
 #pragma unroll
         for (int y = 0; y < NS; ++y) {
@@ -435,8 +447,19 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       }
     }
     __syncthreads();  // Q-K temporaries in U are dead from here
-    // chunk-entry W2 -> U as CT [D][HID] (all loads first, then the LDS writes)
-    {
+    // chunk-entry W2 -> U: the walk copies its compute-type transpose W2^T [HID][D];
+    // the one-walk kernel converts the fp32 state to CT [D][HID] (all loads first)
+    if constexpr (MODE == FWD_CHAIN) {
+      constexpr int V8 = 16 / sizeof(CT), PER = (int)(hd / (512 * V8));
+      static_assert(hd % (512 * V8) == 0, "W2^T copy in whole 16-byte vectors per thread");
+      bf16x8 x[PER];
+#pragma unroll
+      for (int p = 0; p < PER; ++p)
+        x[p] = *reinterpret_cast<const bf16x8*>(pkc + hd + (size_t)(threadIdx.x + 512 * p) * V8);
+#pragma unroll
+      for (int p = 0; p < PER; ++p)
+        *reinterpret_cast<bf16x8*>(sW2 + (size_t)(threadIdx.x + 512 * p) * V8) = x[p];
+    } else {
       constexpr int PER = (int)(hd / (512 * 4));
       f32x4 x[PER];
 #pragma unroll
@@ -470,7 +493,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         if (t >= nt) continue;
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
-        mma_tile<CT, KC, KC>(acc, sHk, HID, i0, sW2, HID, j0, HID);
+        if constexpr (MODE == FWD_CHAIN)
+          mma_tile<CT, KC, MC>(acc, sHk, HID, i0, sW2, D, j0, HID);  // sW2 = W2^T
+        else
+          mma_tile<CT, KC, KC>(acc, sHk, HID, i0, sW2, HID, j0, HID);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -490,7 +516,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       for (int it = 0; it < TMC; ++it) {
         const int i0 = it * 16, j0 = sidx * 16;
         f4 acc = zero4();
-        mma_tile<CT, KC, MC>(acc, sR, D, i0, sW2, HID, j0, D);
+        if constexpr (MODE == FWD_CHAIN)
+          mma_tile<CT, KC, KC>(acc, sR, D, i0, sW2, D, j0, D);  // sW2 = W2^T
+        else
+          mma_tile<CT, KC, MC>(acc, sR, D, i0, sW2, HID, j0, D);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
