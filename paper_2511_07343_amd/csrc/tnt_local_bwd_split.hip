@@ -43,24 +43,20 @@ enum ATmpCT {
   aQ1, aQ2, aQ2T, adXN, adXNT,         // C x C
   A_CT
 };
-enum ATmpF { aNb, aKb, A_F };
 // pass-B temporaries, one set per unit
 enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, B_CT };
 
 struct SplitLayout {
   rec::RecLayout r;
   rec::Lay<A_CT> ac;
-  rec::Lay<A_F> af;
   rec::Lay<B_CT> bc;
 };
 
 constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
   const size_t C = Cp, Cd = C * d, CC = C * C, HD = (size_t)h * d;
   const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, CC, CC, CC, CC, CC};
-  const size_t saf[A_F] = {Cd, Cd};
   const size_t sbc[B_CT] = {HD, HD, HD, HD};
-  return SplitLayout{rec::make_rec_layout(Cp, d, h), rec::make_lay(sac), rec::make_lay(saf),
-                     rec::make_lay(sbc)};
+  return SplitLayout{rec::make_rec_layout(Cp, d, h), rec::make_lay(sac), rec::make_lay(sbc)};
 }
 
 constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
@@ -115,7 +111,6 @@ constexpr size_t split_c_lds() {
 struct SplitPtrs {
   void* brec;       // CT   [units * nch][r.bc.n]  backward records
   float* brec_f;    // fp32 [units * nch][r.bf.n]
-  float* tmpA_f;    // fp32 [SPLIT_GRID_A][af.n]
   void* tmpB;       // CT   [units][bc.n]
   int units;
 };
@@ -144,7 +139,6 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
   constexpr size_t hd = (size_t)h * d;
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
-  float* const tf0 = P.tmpA_f + (size_t)blockIdx.x * Y.af.n;
 
   for (int t = blockIdx.x; t < total; t += gridDim.x) {
     const int u = t / nch, n = t - u * nch;
@@ -153,12 +147,10 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     const float* frf = a.frec_f + (size_t)t * Y.r.ff.n;
     CT* br = (CT*)P.brec + (size_t)t * Y.r.bc.n;
     float* brf = P.brec_f + (size_t)t * Y.r.bf.n;
-    float* tf = tf0;
     fr = launder_global(fr);
     frf = launder_global(frf);
     br = launder_global(br);
     brf = launder_global(brf);
-    tf = launder_global(tf);
     const size_t cbase = ((size_t)b * Dm.H + hh) * Dm.L;
     const IO* dOg = (const IO*)a.dO + cbase * d;
     float* dqp = a.dq_part + cbase * d;
@@ -168,7 +160,6 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 #define BR_(x) (br + Y.r.bc.o[rec::x])
 #define BRF_(x) (brf + Y.r.bf.o[rec::x])
 #define A_(x) (ta + Y.ac.o[x])
-#define AF_(x) (tf + Y.af.o[x])
     const CT *HkT = FR_(HkT), *D1 = FR_(D1), *Sz = FR_(Sz), *KT = FR_(KT), *R = FR_(R),
              *X = FR_(X), *XT = FR_(XT), *N = FR_(N), *NT = FR_(NT), *QT = FR_(QT),
              *StrT = FR_(StrT);
@@ -177,7 +168,9 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     CT *ZbT = BR_(ZbT), *Q1T = BR_(Q1T), *dOT = BR_(dOT), *dOAT = BR_(dOAT), *dOET = BR_(dOET);
     CT *dO = A_(adO), *dOA = A_(adOA), *dOE = A_(adOE), *Xb = A_(aXb), *XbT = A_(aXbT);
     CT *Q1 = A_(aQ1), *Q2 = A_(aQ2), *Q2T = A_(aQ2T), *dXN = A_(adXN), *dXNT = A_(adXNT);
-    float *fNb = AF_(aNb), *fKb = AF_(aKb);
+    // Kbar and Nbar (fp32 C x d each) take the Zbar slot once Xbar has read it
+    static_assert((size_t)CP * H * sizeof(CT) >= 2 * (size_t)CP * D * sizeof(float), "Zbar slot");
+    float *fKb = reinterpret_cast<float*>(Zb), *fNb = fKb + CP * D;
     const int tok0 = s * Dm.S + n * C;
     const int l = lane_id_local();
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
@@ -332,6 +325,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
         store4<CT>(XbT + (size_t)j * Cp + i, xv);
       });
     });
+    __syncthreads();  // Zbar is dead: its slot takes Kbar, Nbar
     // Kbar (retrieval part) = -Q2^T X
     for_blocks<CP, D>([&](int i0, int j0) {
       f4 a1[BCD::RB][BCD::CB];
@@ -424,7 +418,6 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 #undef BR_
 #undef BRF_
 #undef A_
-#undef AF_
   }
 }
 
@@ -1024,14 +1017,14 @@ constexpr bool split_fits() {
 }
 
 struct SplitSizes {
-  size_t rec_ct, rec_f, a_f, b_ct;  // elements
+  size_t rec_ct, rec_f, b_ct;  // elements
 };
 
 template <typename CT, int CP, int D, int H>
 SplitSizes split_sizes(int units, int nch) {
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const size_t t = (size_t)units * nch;
-  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n, (size_t)SPLIT_GRID_A * Y.af.n,
+  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n,
                     (size_t)units * Y.bc.n};
 }
 
@@ -1039,8 +1032,7 @@ size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
 template <typename CT>
 size_t total_bytes(const SplitSizes& z) {
-  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) +
-         up256(z.a_f * 4) + up256(z.b_ct * sizeof(CT));
+  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) + up256(z.b_ct * sizeof(CT));
 }
 
 template <typename CT>
@@ -1049,7 +1041,6 @@ SplitPtrs carve(void* ws, const SplitSizes& z, int units) {
   SplitPtrs P{};
   P.brec = p; p += up256(z.rec_ct * sizeof(CT));
   P.brec_f = (float*)p; p += up256(z.rec_f * 4);
-  P.tmpA_f = (float*)p; p += up256(z.a_f * 4);
   P.tmpB = p;
   P.units = units;
   return P;
