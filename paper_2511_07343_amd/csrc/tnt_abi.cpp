@@ -255,7 +255,7 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
 // threads serialise their enqueues here.
 struct Fork {
   hipStream_t side = nullptr;
-  hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr, eb = nullptr, eg = nullptr;
 };
 constexpr int MAX_DEV = 64;
 Fork g_fork[MAX_DEV];
@@ -272,6 +272,8 @@ hipError_t fork_of(Fork** out) {
     if ((e = hipEventCreateWithFlags(&f.e0, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.e1, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.ea, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.eb, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.eg, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &f;
   return hipSuccess;
@@ -398,10 +400,15 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.D = dims_of(c, c->C_L[i], c->S_L[i]);
     a.force_generic = generic_only();
     a.pass_a_done = (fk && i == 0) ? fk->ea : nullptr;
+    // the last local memory's walk is the point after which dq, dv and every dW_init
+    // part are final: the helper stream reduces them beside its gate pass
+    const bool last = i == c->n_local - 1;
+    a.pass_b_done = (fk && last) ? fk->eb : nullptr;
     HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
-    HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
-                               dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
-                               c->d, c->hid, 0, st));
+    if (!(fk && last))
+      HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
+                                 dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
+                                 c->d, c->hid, 0, st));
   }
   if (c->has_global) {
     if (fk) {
@@ -435,15 +442,38 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     HIP_TIMED("global_scan", launch_global_scan(g, st));
     HIP_TIMED("global_bwd_zero", launch_global_bwd_zero(g, y.g_chunks & 1, st));
     for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TIMED("global_bwd_chunk", launch_global_bwd_chunk(g, n, st));
+    if (fk) {
+      // the global memory's dq, dk, dv are final: the helper stream sums dq and dv once
+      // the last local memory's walk is done too; the main stream sums dk after the
+      // gate pass
+      HIP_TRY(hipEventRecord(fk->eg, fk->side));
+      HIP_TRY(hipStreamWaitEvent(fk->side, fk->eb, 0));
+      SumJobs side{};
+      side.parts[0] = dqp; side.out[0] = dq;
+      side.parts[1] = dvp; side.out[1] = dv;
+      HIP_TIMED("sum_grads", launch_sum_outs(side, 2, y.M, y.io_elems, y.io_elems,
+                                             c->dtype == TNT_BF16, st));
+    }
     HIP_TIMED("global_gate_bwd", launch_global_gate_bwd(g, st));
     HIP_TIMED("reduce_init", launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
   }
-  st = main_st;
-  if (fk) {
-    HIP_TRY(hipEventRecord(fk->e1, fk->side));
-    HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
-  }
   const int bf = c->dtype == TNT_BF16;
+  if (fk) {
+    // helper stream, last: the last local memory's dW_init reduction (its walk is done)
+    const int i = c->n_local - 1, m = c->has_global + i;
+    HIP_TIMED("reduce_init", launch_reduce_init((float*)(ws + y.b_dWl[i]), c->B, c->H, c->L / c->S_L[i],
+                               2 * y.hd, dW1 + (size_t)m * c->H * y.hd,
+                               dW2 + (size_t)m * c->H * y.hd, c->d, c->hid, 0, st));
+    HIP_TRY(hipEventRecord(fk->e1, fk->side));
+    st = main_st;
+    HIP_TRY(hipStreamWaitEvent(main_st, fk->eg, 0));
+    SumJobs mainj{};
+    mainj.parts[0] = dkp; mainj.out[0] = dk;
+    HIP_TIMED("sum_grads", launch_sum_outs(mainj, 1, y.M, y.io_elems, y.io_elems, bf, st));
+    HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
+    return TNT_OK;
+  }
+  st = main_st;
   SumJobs jobs{};
   jobs.parts[0] = dqp; jobs.out[0] = dq;
   jobs.parts[1] = dkp; jobs.out[1] = dk;

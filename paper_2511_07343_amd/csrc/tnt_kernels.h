@@ -82,6 +82,10 @@ struct LocalBwdArgs {
   hipEvent_t pass_a_done;                                // null, or recorded on the stream once the
                                                          // chunk-parallel pass is done (at once when
                                                          // the backward has no such pass)
+  hipEvent_t pass_b_done;                                // null, or recorded on the stream once dq,
+                                                         // dv and dWinit_part are final (after the
+                                                         // walk; before the gate pass, which adds
+                                                         // only to dk and the gate adjoints)
   int force_generic;                                     // 1: skip fixed-size kernels
 };
 

@@ -587,9 +587,19 @@ static bool try_bwd(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t
   return true;
 }
 
+static hipError_t launch_local_bwd_rest(const LocalBwdArgs& a, int units, hipStream_t st);
+
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st) {
   hipError_t e = hipSuccess;
   if (!a.force_generic && !a.single_walk && launch_local_bwd_split(a, units, st, &e)) return e;
+  e = launch_local_bwd_rest(a, units, st);
+  if (e == hipSuccess && a.pass_b_done) e = hipEventRecord(a.pass_b_done, st);
+  return e;
+}
+
+// the one-walk kernels (fixed-size, then runtime-sized)
+static hipError_t launch_local_bwd_rest(const LocalBwdArgs& a, int units, hipStream_t st) {
+  hipError_t e = hipSuccess;
   // the other kernels recompute from the fp32 chunk-entry states, which a forward
   // that kept them in a ring did not save
   if (a.fslots) return hipErrorInvalidValue;

@@ -1080,6 +1080,13 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
     }
   }
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
+  if (a->pass_b_done) {
+    const hipError_t e = hipEventRecord(a->pass_b_done, st);
+    if (e != hipSuccess) {
+      *err = e;
+      return true;
+    }
+  }
   if (Dm.qk_proj && Dm.qk_scope == 0) {
     const size_t thr = (size_t)units * D * D;
     hipLaunchKernelGGL(split_madj_scan_kernel, dim3((unsigned)((thr + 255) / 256)), dim3(256), 0, st,
