@@ -177,7 +177,7 @@ Layout layout_of(const tnt_config* c) {
     const Dims D = dims_of(c, c->C_G, c->L);
     y.b_gscr = off;
     off += up(global_bwd_scratch_bytes(D, &y.b_gscr_f32));
-    y.b_gpackA = off; off += up((size_t)y.BH * 4 * y.hd * cts);
+    y.b_gpackA = off; off += up((size_t)y.BH * 8 * y.hd * cts);  // transposed and as they are
     y.b_gop = off; off += up((size_t)y.BH * 5 * ((size_t)c->hid + c->d) * c->C_G * cts);
   }
   for (int i = 0; i < c->n_local; ++i) {

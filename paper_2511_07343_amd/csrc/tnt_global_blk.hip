@@ -72,13 +72,16 @@ __device__ __forceinline__ float gsum16(float v) {
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// Transposed bf16 copies of a chain's four state matrices: W1 (hid x d) ->
-// [d][hid], W2 (d x hid) -> [hid][d], S1, S2 alike; `mask` bit m selects
-// matrix m.  One 32 x 32 tile per workgroup.
+// bf16 copies of a chain's four state matrices: transposed into dst (W1 (hid x
+// d) -> [d][hid], W2 (d x hid) -> [hid][d], S1, S2 alike, chain stride
+// dst_stride) and as they are into dstn (chain stride dstn_stride); `mask` bit
+// m selects matrix m.  One 32 x 32 tile per workgroup.
 // ---------------------------------------------------------------------------
 template <typename CT>
 __global__ void __launch_bounds__(256) gtranspose_kernel(const float* src, size_t src_stride,
-                                                         CT* dst, int d, int h, int mask) {
+                                                         CT* dst, size_t dst_stride, CT* dstn,
+                                                         size_t dstn_stride, int d, int h,
+                                                         int mask) {
   __shared__ float t[32][33];
   const int m = blockIdx.z;
   if (!((mask >> m) & 1)) return;
@@ -88,19 +91,26 @@ __global__ void __launch_bounds__(256) gtranspose_kernel(const float* src, size_
   const int tc = Cc / 32;
   const int r0 = (blockIdx.x / tc) * 32, c0 = (blockIdx.x % tc) * 32;
   const float* s = src + chain * src_stride + m * hd;
-  CT* o = dst + (size_t)chain * 4 * hd + m * hd;
+  CT* o = dst + (size_t)chain * dst_stride + m * hd;
+  CT* on = dstn + (size_t)chain * dstn_stride + m * hd;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  for (int k = ty; k < 32; k += 8) t[k][tx] = s[(size_t)(r0 + k) * Cc + c0 + tx];
+  for (int k = ty; k < 32; k += 8) {
+    const size_t e = (size_t)(r0 + k) * Cc + c0 + tx;
+    const float x = s[e];
+    t[k][tx] = x;
+    on[e] = from_f<CT>(x);
+  }
   __syncthreads();
   for (int k = ty; k < 32; k += 8) o[(size_t)(c0 + k) * R + r0 + tx] = from_f<CT>(t[tx][k]);
 }
 
 template <typename CT>
-static void launch_gtranspose(const float* src, size_t src_stride, CT* dst, int chains, int d,
-                              int h, int mask, hipStream_t st) {
+static void launch_gtranspose(const float* src, size_t src_stride, CT* dst, size_t dst_stride,
+                              CT* dstn, size_t dstn_stride, int chains, int d, int h, int mask,
+                              hipStream_t st) {
   const dim3 grid((h / 32) * (d / 32), chains, 4);
-  hipLaunchKernelGGL(gtranspose_kernel<CT>, grid, dim3(256), 0, st, src, src_stride, dst, d, h,
-                     mask);
+  hipLaunchKernelGGL(gtranspose_kernel<CT>, grid, dim3(256), 0, st, src, src_stride, dst,
+                     dst_stride, dstn, dstn_stride, d, h, mask);
 }
 
 // ---------------------------------------------------------------------------
@@ -120,9 +130,9 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   const int C = Dm.C;
   const int chain = blockIdx.y, r0 = blockIdx.x * TT;
   constexpr size_t hd = (size_t)H * D;
-  const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
-  const float *V1 = V, *V2 = V + hd;
-  const CT* V2T = (const CT*)a.packT + (size_t)chain * 4 * hd + hd;  // [H][D]
+  // the chunk-entry state in bf16: V1^T [D][H], V2^T [H][D], V1 [H][D], V2 [D][H]
+  const CT* pS = (const CT*)a.packT + (size_t)chain * 4 * hd;
+  const CT *V2T = pS + hd, *V1 = pS + 2 * hd, *V2 = pS + 3 * hd;
   CT* op = (CT*)a.opT + (size_t)chain * (2 * (size_t)H + 4 * (size_t)D) * C;
   CT *D1T = op, *HkT = D1T + (size_t)H * C, *KcT = HkT + (size_t)H * C, *KbT = KcT + (size_t)D * C,
      *RcT = KbT + (size_t)D * C, *RbT = RcT + (size_t)D * C;
@@ -285,14 +295,12 @@ __global__ void __launch_bounds__(512) gbwd_tile_kernel(GlobalArgs a, int n) {
   const int C = Dm.C;
   const int chain = blockIdx.y, r0 = blockIdx.x * TT;
   constexpr size_t hd = (size_t)H * D;
-  const float* V = a.states + ((size_t)chain * a.nslots + n) * 4 * hd;
-  const float *V1 = V, *V2 = V + hd;
-  const float* Ab = a.adj + ((size_t)chain * 2 + ((n + 1) & 1)) * 4 * hd;
-  const float *Vb1 = Ab, *Vb2 = Ab + hd, *Sb1 = Ab + 2 * hd, *Sb2 = Ab + 3 * hd;
+  // bf16 copies of the chunk-entry state and the exit adjoint, transposed and as they are
   const CT* pS = (const CT*)a.packT + (size_t)chain * 4 * hd;
-  const CT *V1T = pS, *V2T = pS + hd;  // [D][H], [H][D]
-  const CT* pA = (const CT*)a.packA + (size_t)chain * 4 * hd;
+  const CT *V1T = pS, *V2T = pS + hd, *V1 = pS + 2 * hd, *V2 = pS + 3 * hd;
+  const CT* pA = (const CT*)a.packA + (size_t)chain * 8 * hd;
   const CT *Vb1T = pA, *Vb2T = pA + hd, *Sb1T = pA + 2 * hd, *Sb2T = pA + 3 * hd;
+  const CT *Vb1 = pA + 4 * hd, *Vb2 = pA + 5 * hd, *Sb1 = pA + 6 * hd, *Sb2 = pA + 7 * hd;
   CT* op = (CT*)a.opT + (size_t)chain * 5 * ((size_t)H + D) * C;
   CT *ZkbT = op, *ZqbT = ZkbT + (size_t)H * C, *GbT = ZqbT + (size_t)H * C,
      *HkT = GbT + (size_t)H * C, *HqT = HkT + (size_t)H * C, *KT = HqT + (size_t)H * C,
@@ -565,7 +573,7 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   const int chains = a.D.B * a.D.H, C = a.D.C;
   constexpr size_t hd = (size_t)H * D;
   launch_gtranspose<CT>(a.states + (size_t)(n % a.nslots) * 4 * hd, (size_t)a.nslots * 4 * hd,
-                        (CT*)a.packT, chains, D, H, 0x3, st);
+                        (CT*)a.packT, 4 * hd, (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
   const size_t l1 = (2 * (size_t)TT * D + 3 * (size_t)TT * H) * sizeof(CT);
   auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H>;
   set_lds_limit((const void*)k1);
@@ -582,9 +590,9 @@ static hipError_t gbwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   const int chains = a.D.B * a.D.H, C = a.D.C;
   constexpr size_t hd = (size_t)H * D;
   launch_gtranspose<CT>(a.states + (size_t)n * 4 * hd, (size_t)a.nslots * 4 * hd, (CT*)a.packT,
-                        chains, D, H, 0x3, st);
-  launch_gtranspose<CT>(a.adj + (size_t)((n + 1) & 1) * 4 * hd, 2 * 4 * hd, (CT*)a.packA, chains,
-                        D, H, 0xf, st);
+                        4 * hd, (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
+  launch_gtranspose<CT>(a.adj + (size_t)((n + 1) & 1) * 4 * hd, 2 * 4 * hd, (CT*)a.packA, 8 * hd,
+                        (CT*)a.packA + 4 * hd, 8 * hd, chains, D, H, 0xf, st);
   const size_t l1 = (3 * (size_t)TT * D + 4 * (size_t)TT * H) * sizeof(CT);
   auto k1 = gbwd_tile_kernel<IO, CT, ACT, D, H>;
   set_lds_limit((const void*)k1);

@@ -110,8 +110,9 @@ struct GlobalArgs {
   void* scratch;                                         // phase-A scratch of the backward
   size_t scratch_f32_off;
   float* part;                                           // [B*H][nsplit][4*hid*d] split partials
-  void* packT;                                           // CT [B*H][4*hid*d] transposed state
-  void* packA;                                           // CT [B*H][4*hid*d] transposed adjoint
+  void* packT;                                           // CT [B*H][4*hid*d]: W1^T, W2^T, W1, W2
+  void* packA;                                           // CT [B*H][8*hid*d]: the adjoint's four
+                                                         // matrices transposed, then as they are
   void* opT;                                             // CT per-chain transposed chunk operands
   Dims D;
   int force_generic;                                     // 1: skip fixed-size kernels
