@@ -329,6 +329,47 @@ __device__ __forceinline__ void mma_blk(f4 (&acc)[RB][CB], const EA* A, int lda,
   apply(fa, fb);
 }
 
+// Two block GEMMs sharing one operand, every K step's fragments in flight before
+// the MFMAs (short contractions): x += A B0, y += A B1 (SHARE_A) or
+// x += A0 B, y += A1 B (shared B); all operands contraction-contiguous.
+template <typename CT, int RB, int CB, int K, bool SHARE_A, typename EA, typename EB>
+__device__ __forceinline__ void mma_blk_shared(f4 (&x)[RB][CB], f4 (&y)[RB][CB], const EA* A0,
+                                               const EA* A1, int lda, int i0, const EB* B0,
+                                               const EB* B1, int ldb, int j0) {
+  typedef Mma<CT> MM;
+  const int l = lane_id_local();
+  const int ko = MM::kofs(l);
+  constexpr int NS = (K + MM::KS - 1) / MM::KS;
+  static_assert(NS <= 4, "short contractions only: all steps stay in registers");
+  typename MM::frag fa[NS][RB], fa1[NS][SHARE_A ? 1 : RB], fb[NS][CB], fb1[NS][SHARE_A ? CB : 1];
+#pragma unroll
+  for (int t = 0; t < NS; ++t) {
+    const int k0 = t * MM::KS + ko;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      fa[t][r] = MM::template load<KC>(A0, lda, i0 + 16 * r + (l & 15), k0, K, nullptr);
+      if constexpr (!SHARE_A) fa1[t][r] = MM::template load<KC>(A1, lda, i0 + 16 * r + (l & 15), k0, K, nullptr);
+    }
+#pragma unroll
+    for (int c = 0; c < CB; ++c) {
+      fb[t][c] = MM::template load<KC>(B0, ldb, j0 + 16 * c + (l & 15), k0, K, nullptr);
+      if constexpr (SHARE_A) fb1[t][c] = MM::template load<KC>(B1, ldb, j0 + 16 * c + (l & 15), k0, K, nullptr);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NS; ++t)
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        MM::mma(x[r][c], fa[t][r], fb[t][c]);
+        if constexpr (SHARE_A)
+          MM::mma(y[r][c], fa[t][r], fb1[t][c]);
+        else
+          MM::mma(y[r][c], fa1[t][r], fb[t][c]);
+      }
+}
+
 // f(rb, cb, i, j) once per tile of the block: the lane's rows i .. i+3 of
 // column j are acc[rb][cb][0..3]
 template <int RB, int CB, typename F>

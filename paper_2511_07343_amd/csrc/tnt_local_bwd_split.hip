@@ -743,9 +743,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       });
       zero_blk(a1);
       zero_blk(a3);
-      mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a1, ZbT, Cp, i0, XAT, Cp, j0);
+      mma_blk_shared<CT, BHD::RB, BHD::CB, CP, true>(a1, a3, ZbT, ZbT, Cp, i0, XAT, XET, Cp, j0);
       mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a1, ZkbT, Cp, i0, KT, Cp, j0);
-      mma_blk<CT, KC, KC, BHD::RB, BHD::CB, CP>(a3, ZbT, Cp, i0, XET, Cp, j0);
       blk_each4<BHD::RB, BHD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         f4 nw, ns;
 #pragma unroll
@@ -772,10 +771,9 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       });
       zero_blk(a1);
       zero_blk(a4);
-      mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, dOAT, Cp, i0, HT, Cp, j0);
+      mma_blk_shared<CT, BDH::RB, BDH::CB, CP, false>(a1, a4, dOAT, dOET, Cp, i0, HT, HT, Cp, j0);
       mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, RT, Cp, i0, GbT, Cp, j0);
       mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a1, YkbT, Cp, i0, HkT, Cp, j0);
-      mma_blk<CT, KC, KC, BDH::RB, BDH::CB, CP>(a4, dOET, Cp, i0, HT, Cp, j0);
       blk_each4<BDH::RB, BDH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         f4 nw, ns;
 #pragma unroll
