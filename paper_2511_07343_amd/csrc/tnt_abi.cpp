@@ -442,11 +442,13 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     HIP_TIMED("global_scan", launch_global_scan(g, st));
     HIP_TIMED("global_bwd_zero", launch_global_bwd_zero(g, y.g_chunks & 1, st));
     for (int n = y.g_chunks - 1; n >= 0; --n) HIP_TIMED("global_bwd_chunk", launch_global_bwd_chunk(g, n, st));
+    // the global memory's dq, dk, dv are final here (the main stream sums dk after its
+    // gate pass); its gate adjoints and dW_init follow while the local walk still runs
+    if (fk) HIP_TRY(hipEventRecord(fk->eg, fk->side));
+    HIP_TIMED("global_gate_bwd", launch_global_gate_bwd(g, st));
+    HIP_TIMED("reduce_init", launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
     if (fk) {
-      // the global memory's dq, dk, dv are final: the helper stream sums dq and dv once
-      // the last local memory's walk is done too; the main stream sums dk after the
-      // gate pass
-      HIP_TRY(hipEventRecord(fk->eg, fk->side));
+      // dq and dv are final once the last local memory's walk is done too
       HIP_TRY(hipStreamWaitEvent(fk->side, fk->eb, 0));
       SumJobs side{};
       side.parts[0] = dqp; side.out[0] = dq;
@@ -454,8 +456,6 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
       HIP_TIMED("sum_grads", launch_sum_outs(side, 2, y.M, y.io_elems, y.io_elems,
                                              c->dtype == TNT_BF16, st));
     }
-    HIP_TIMED("global_gate_bwd", launch_global_gate_bwd(g, st));
-    HIP_TIMED("reduce_init", launch_reduce_global_init(g.dWinit, c->B, c->H, y.hd, dW1, dW2, st));
   }
   const int bf = c->dtype == TNT_BF16;
   if (fk) {
