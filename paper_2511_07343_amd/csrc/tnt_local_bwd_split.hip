@@ -695,16 +695,20 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 
     // ---- phase 3: Zkbar = (Hkbar + Ykbar W2) * s'(Zk) + D1bar * G * s''(Zk)  (slot: Gbar is dead)
     for_blocks<CP, H>([&](int i0, int j0) {
+      typedef CT ct4 __attribute__((ext_vector_type(4)));
+      ct4 spv[BCH::RB][BCH::CB];  // s'(Zk), requested ahead of the product
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int, int) {
+        spv[rb][cb] = *reinterpret_cast<const ct4*>(Sp + fofs(i0, j0, rb, cb));
+      });
       f4 a4[BCH::RB][BCH::CB];
       zero_blk(a4);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a4, Ykb, d, i0, W2T, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const size_t fo = fofs(i0, j0, rb, cb);
-        const f4 sp = load4<CT>(Sp + fo), zp = zkp[rb][cb];
+        const f4 zp = zkp[rb][cb];
         f4 zv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          zv[r] = a4[rb][cb][r] * sp[r] + zp[r];
+          zv[r] = a4[rb][cb][r] * to_f(spv[rb][cb][r]) + zp[r];
           Zkb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
         }
         store4<CT>(ZkbT + (size_t)j * Cp + i, zv);
@@ -715,6 +719,12 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     // ---- phase 4: Kbar (carried part) = -diag(cC) T3 - diag(b) T4 + Zkbar W1 ;
     // adjoint of the chunk-entry state (in place, with its transposed copies)
     for_blocks<CP, D>([&](int i0, int j0) {
+      f4 kold[BCD::RB][BCD::CB];  // dk so far, requested ahead of the product
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          kold[rb][cb][r] = (i + r < C) ? dkp[(size_t)(tok0 + i + r) * d + j] : 0.f;
+      });
       f4 a2[BCD::RB][BCD::CB];
       zero_blk(a2);
       mma_blk<CT, KC, KC, BCD::RB, BCD::CB, H>(a2, Zkb, h, i0, W1T, h, j0);
@@ -725,7 +735,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         for (int r = 0; r < 4; ++r) {
           const int ii = i + r;
           if (ii < C)
-            dkp[(size_t)(tok0 + ii) * d + j] += -sC[ii] * t3[r] - sB[ii] * t4[r] + a2[rb][cb][r];
+            dkp[(size_t)(tok0 + ii) * d + j] =
+                kold[rb][cb][r] + (-sC[ii] * t3[r] - sB[ii] * t4[r] + a2[rb][cb][r]);
         }
       });
     });
