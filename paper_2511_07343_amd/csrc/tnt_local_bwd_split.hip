@@ -238,11 +238,15 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     };
     // dOR = dO R^T ; Q1 = c o dOR ; cbar = -HH o dOR
     for_blocks<CP, CP>([&](int i0, int j0) {
+      f4 hhv[BCC::RB][BCC::CB];  // H Hk^T, requested ahead of the product
+      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int, int) {
+        hhv[rb][cb] = load4<float>(fHH + frag_ofs<CP, CP>(i0 + 16 * rb, j0 + 16 * cb, l));
+      });
       f4 acc[BCC::RB][BCC::CB];
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, dO, d, i0, R, d, j0);
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const f4 hh = load4<float>(fHH + frag_ofs<CP, CP>(i0 + 16 * rb, j0 + 16 * cb, l));
+        const f4 hh = hhv[rb][cb];
         f4 qv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -259,6 +263,11 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     __syncthreads();
     // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)
     for_blocks<CP, H>([&](int i0, int j0) {
+      typedef CT ct4 __attribute__((ext_vector_type(4)));
+      ct4 szv[BCH::RB][BCH::CB];  // s'(Z), requested ahead of the products
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int, int) {
+        szv[rb][cb] = *reinterpret_cast<const ct4*>(Sz + fofs(i0, j0, rb, cb));
+      });
       f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
       zero_blk(a1);
       zero_blk(a3);
@@ -266,11 +275,10 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dOE, d, i0, S2T, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Q1, Cp, i0, HkT, Cp, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const f4 sz = load4<CT>(Sz + fofs(i0, j0, rb, cb));
         f4 zv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          zv[r] = (a1[rb][cb][r] - a3[rb][cb][r]) * sz[r];
+          zv[r] = (a1[rb][cb][r] - a3[rb][cb][r]) * to_f(szv[rb][cb][r]);
           Zb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
         }
         store4<CT>(ZbT + (size_t)j * Cp + i, zv);
@@ -279,11 +287,15 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     __syncthreads();
     // dZD1 = Zbar D1^T ; Q2 = c o dZD1 ; cbar -= XK o dZD1
     for_blocks<CP, CP>([&](int i0, int j0) {
+      f4 xkv[BCC::RB][BCC::CB];  // X K^T, requested ahead of the product
+      blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int, int) {
+        xkv[rb][cb] = load4<float>(fXK + frag_ofs<CP, CP>(i0 + 16 * rb, j0 + 16 * cb, l));
+      });
       f4 acc[BCC::RB][BCC::CB];
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCC::RB, BCC::CB, H>(acc, Zb, h, i0, D1, h, j0);
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const f4 xk = load4<float>(fXK + frag_ofs<CP, CP>(i0 + 16 * rb, j0 + 16 * cb, l));
+        const f4 xk = xkv[rb][cb];
         f4 qv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -300,6 +312,11 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
     __syncthreads();
     // Xbar = diag(A) Zbar W1 + diag(E) Zbar S1 - Q2 K
     for_blocks<CP, D>([&](int i0, int j0) {
+      typedef CT ct4 __attribute__((ext_vector_type(4)));
+      ct4 xv4[BCD::RB][BCD::CB];  // X, the lane's four rows from X^T, ahead of the products
+      blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+        xv4[rb][cb] = *reinterpret_cast<const ct4*>(XT + (size_t)j * Cp + i);
+      });
       f4 a1[BCD::RB][BCD::CB], a2[BCD::RB][BCD::CB], a3[BCD::RB][BCD::CB];
       zero_blk(a1);
       zero_blk(a2);
@@ -312,7 +329,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int ii = i + r;
-          const float x = to_f(X[(size_t)ii * d + j]);
+          const float x = to_f(xv4[rb][cb][r]);
           xv[r] = cf.A[ii] * a1[rb][cb][r] + cf.E[ii] * a2[rb][cb][r] - a3[rb][cb][r];
           Xb[(size_t)ii * d + j] = from_f<CT>(xv[r]);
           if (!Dm.qk_proj && ii < C) dqp[(size_t)(tok0 + ii) * d + j] = xv[r];
@@ -587,6 +604,16 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 #pragma unroll
       for (int r = 0; r < RBN; ++r) t0[r] = t1[r] = zero4();
       float pa = 0.f, pe = 0.f, pb = 0.f;
+      // the row-dot factors (K for T3, T4; R for T5, T6), the lane's four rows of its
+      // column from the transposed record, requested ahead of the products
+      typedef CT ct4 __attribute__((ext_vector_type(4)));
+      ct4 mxv[RBN];
+      {
+        const CT* MT = pair == 0 ? KT : RT;
+#pragma unroll
+        for (int rb = 0; rb < RBN; ++rb)
+          mxv[rb] = *reinterpret_cast<const ct4*>(MT + (size_t)(j0 + (l & 15)) * Cp + 16 * rb + 4 * (l >> 4));
+      }
       if (pair == 0)
         mma_pair_dots<RBN, H, 4, KC>(t0, t1, D1, h, Wb1T, Sb1T, h, j0, W1T, S1T, h, pa, pe, pb);
       else
@@ -599,7 +626,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         dpart[1][wave_id()] = pe;
         dpart[2][wave_id()] = pb;
       }
-      const CT* M = pair == 0 ? K : R;
       float* const q0 = pair == 0 ? pC : pC2;
       float* const q1 = pair == 0 ? pB : pB2;
       float* const f0 = pair == 0 ? fT3 : fT5;
@@ -612,7 +638,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         const int i = 16 * rb + 4 * (l >> 4), j = j0 + (l & 15);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float mx = to_f(M[(size_t)(i + r) * d + j]);
+          const float mx = to_f(mxv[rb][r]);
           const float s0 = sum16b(mx * t0[rb][r]), s1 = sum16b(mx * t1[rb][r]);
           if ((l & 15) == 0) {
             q0[(j >> 4) * Cp + i + r] = s0;
@@ -625,6 +651,14 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     // Hkbar so far = -Q1^T H - diag(cC) R W2bar' - diag(b) R S2bar' ; the Zkbar terms known
     // now, D1bar * G * s''(Zk) + Hkbar * s'(Zk), are kept per fragment
     for_blocks<CP, H>([&](int i0, int j0) {
+      typedef CT ct4 __attribute__((ext_vector_type(4)));
+      ct4 spv[BCH::RB][BCH::CB], gv4[BCH::RB][BCH::CB], sppv[BCH::RB][BCH::CB];  // ahead of the products
+      blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int, int) {
+        const size_t fo = fofs(i0, j0, rb, cb);
+        spv[rb][cb] = *reinterpret_cast<const ct4*>(Sp + fo);
+        gv4[rb][cb] = *reinterpret_cast<const ct4*>(G + fo);
+        sppv[rb][cb] = *reinterpret_cast<const ct4*>(Spp + fo);
+      });
       f4 a1[BCH::RB][BCH::CB], a2[BCH::RB][BCH::CB];
       zero_blk(a1);
       zero_blk(a2);
@@ -635,14 +669,12 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, RcC, d, i0, Wb2T, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, Rb, d, i0, Sb2T, d, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const size_t fo = fofs(i0, j0, rb, cb);
-        const f4 sp = load4<CT>(Sp + fo), g = load4<CT>(G + fo), spp = load4<CT>(Spp + fo);
         f4 gv, zp;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float d1b = -a1[rb][cb][r];
-          gv[r] = d1b * sp[r];
-          zp[r] = d1b * g[r] * spp[r] - a2[rb][cb][r] * sp[r];
+          const float d1b = -a1[rb][cb][r], sp = to_f(spv[rb][cb][r]);
+          gv[r] = d1b * sp;
+          zp[r] = d1b * to_f(gv4[rb][cb][r]) * to_f(sppv[rb][cb][r]) - a2[rb][cb][r] * sp;
           Gb[(size_t)(i + r) * h + j] = from_f<CT>(gv[r]);
         }
         zkp[rb][cb] = zp;
