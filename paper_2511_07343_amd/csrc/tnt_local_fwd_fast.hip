@@ -659,6 +659,23 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       }
     }
     {
+      // the retrieval's W1, S1 from the walk's bf16 copies W1^T, S1^T [D][HID] (the same
+      // rounding as a conversion of the fp32 state at load): contraction-major reads, half
+      // the bytes, every strip's requested before the barrier
+      typename Mma<CT>::frag bwr[MODE == FWD_RET ? NS : 1][NKD], bsr[MODE == FWD_RET ? NS : 1][NKD];
+      if constexpr (MODE == FWD_RET)
+#pragma unroll
+        for (int y = 0; y < NS; ++y) {
+          const int sidx = w + NW * y;
+          if (sidx < TNH)
+#pragma unroll
+            for (int ks = 0; ks < NKD; ++ks) {
+              bwr[y][ks] = Mma<CT>::template load<MC>(pkc, HID, sidx * 16 + (l & 15), ks * KS + ko, D,
+                                                      nullptr);
+              bsr[y][ks] = Mma<CT>::template load<MC>(pkc + 2 * hd, HID, sidx * 16 + (l & 15),
+                                                      ks * KS + ko, D, nullptr);
+            }
+        }
       __syncthreads();  // P ready; K^T / R^T in U are dead
 #pragma unroll
       for (int y = 0; y < NS; ++y) {
@@ -666,13 +683,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         if (sidx >= TNH) continue;
         typename Mma<CT>::frag bw[NKD], bs[NKD];
         if constexpr (MODE == FWD_RET) {
-          // the walk's bf16 copies W1^T, S1^T [D][HID] (the same rounding as a
-          // conversion of the fp32 state at load): contraction-major reads, half the bytes
 #pragma unroll
           for (int ks = 0; ks < NKD; ++ks) {
-            bw[ks] = Mma<CT>::template load<MC>(pkc, HID, sidx * 16 + (l & 15), ks * KS + ko, D, nullptr);
-            bs[ks] = Mma<CT>::template load<MC>(pkc + 2 * hd, HID, sidx * 16 + (l & 15), ks * KS + ko, D,
-                                                nullptr);
+            bw[ks] = bwr[y][ks];
+            bs[ks] = bsr[y][ks];
           }
         } else {
           RawFrag<CT, float> rw[NKD], rs[NKD];
