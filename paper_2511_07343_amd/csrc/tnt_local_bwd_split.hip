@@ -43,20 +43,16 @@ enum ATmpCT {
   aQ1, aQ2, aQ2T, adXN, adXNT,         // C x C
   A_CT
 };
-// pass-B temporaries, one set per unit
-enum BTmpCT { tWb1T, tSb1T, tWb2T, tSb2T, B_CT };
 
 struct SplitLayout {
   rec::RecLayout r;
   rec::Lay<A_CT> ac;
-  rec::Lay<B_CT> bc;
 };
 
 constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
-  const size_t C = Cp, Cd = C * d, CC = C * C, HD = (size_t)h * d;
+  const size_t C = Cp, Cd = C * d, CC = C * C;
   const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, CC, CC, CC, CC, CC};
-  const size_t sbc[B_CT] = {HD, HD, HD, HD};
-  return SplitLayout{rec::make_rec_layout(Cp, d, h), rec::make_lay(sac), rec::make_lay(sbc)};
+  return SplitLayout{rec::make_rec_layout(Cp, d, h), rec::make_lay(sac)};
 }
 
 constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
@@ -111,7 +107,6 @@ constexpr size_t split_c_lds() {
 struct SplitPtrs {
   void* brec;       // CT   [units * nch][r.bc.n]  backward records
   float* brec_f;    // fp32 [units * nch][r.bf.n]
-  void* tmpB;       // CT   [units][bc.n]
   int units;
 };
 
@@ -446,7 +441,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
 // operands' shape (layout SL: KC as the B operands, MC transposed, leading
 // dimension lds), both sides as the MFMAs see them (compute type):
 // pa += B0 . S0, pe += B0 . S1, pb += B1 . S1.
-template <int RBN, int K, int G, int SL, typename EB>
+template <int RBN, int K, int G, int SL, int BL = KC, typename EB = float>
 __device__ __forceinline__ void mma_pair_dots(f4 (&t0)[RBN], f4 (&t1)[RBN], const __bf16* A,
                                               int lda, const EB* B0, const EB* B1, int ldb,
                                               int j0, const __bf16* S0, const __bf16* S1,
@@ -465,8 +460,8 @@ __device__ __forceinline__ void mma_pair_dots(f4 (&t0)[RBN], f4 (&t1)[RBN], cons
 #pragma unroll
       for (int r = 0; r < RBN; ++r)
         fa[st][r] = MM::template load<KC>(A, lda, 16 * r + (l & 15), k0, K, nullptr);
-      f0[st] = MM::template load<KC>(B0, ldb, jr, k0, K, nullptr);
-      f1[st] = MM::template load<KC>(B1, ldb, jr, k0, K, nullptr);
+      f0[st] = MM::template load<BL>(B0, ldb, jr, k0, K, nullptr);
+      f1[st] = MM::template load<BL>(B1, ldb, jr, k0, K, nullptr);
       s0[st] = MM::template load<SL>(S0, lds, jr, k0, K, nullptr);
       s1[st] = MM::template load<SL>(S1, lds, jr, k0, K, nullptr);
     }
@@ -526,13 +521,11 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
   float* dkp = a.dk_part + cbase * d;
   float* dvp = a.dv_part + cbase * d;
   float* const adj0 = a.adj + (size_t)u * 4 * hd;
-  CT* const tb0 = (CT*)P.tmpB + (size_t)u * Y.bc.n;
   using BCH0 = Blk<CP, H>;
   static_assert(BCH0::NB <= 8, "each wave owns at most one C x h block");
 
   for (size_t e = threadIdx.x; e < 4 * hd; e += blockDim.x) {
     adj0[e] = 0.f;
-    tb0[Y.bc.o[tWb1T] + e] = from_f<CT>(0.f);  // the four transposed adjoint copies
   }
   __syncthreads();
 
@@ -542,21 +535,17 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     const float* rf = a.frec_f + t * Y.r.ff.n;
     CT* bq = (CT*)P.brec + t * Y.r.bc.n;
     float* bqf = P.brec_f + t * Y.r.bf.n;
-    CT* tb = tb0;
     float* adj = adj0;
     rc = launder_global(rc);
     rf = launder_global(rf);
     bq = launder_global(bq);
     bqf = launder_global(bqf);
-    tb = launder_global(tb);
     adj = launder_global(adj);
 #define R_(x) (rc + Y.r.fc.o[rec::x])
 #define RF_(x) (rf + Y.r.ff.o[rec::x])
 #define BQ_(x) (bq + Y.r.bc.o[rec::x])
 #define BQF_(x) (bqf + Y.r.bf.o[rec::x])
-#define T_(x) (tb + Y.bc.o[x])
     float *Wb1 = adj, *Wb2 = adj + hd, *Sb1 = adj + 2 * hd, *Sb2 = adj + 3 * hd;
-    CT *Wb1T = T_(tWb1T), *Sb1T = T_(tSb1T), *Wb2T = T_(tWb2T), *Sb2T = T_(tSb2T);
     CT *Gb = slot1, *Zkb = slot1;
     // the Zkbar terms known after phase 1, kept by the wave that owns the block
     // until phase 3 (both phases walk the same C x h blocks)
@@ -594,7 +583,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     // row dots (-K.T3 - R.T5, -K.T4 - R.T6) as partial sums over each tile's 16 columns.
     // The strips of the adjoint's B operands cover it whole: the adjoint . state products
     // are taken from the same fragments, both sides as the MFMAs see them (the adjoint
-    // rounded to the compute type, the state from its transposed compute-type copy).
+    // read down its fp32 columns and rounded to the compute type, the state from its
+    // transposed compute-type copy).
     {
       static_assert(D == 64, "two pairs of four column strips for eight waves");
       static_assert(sizeof(CT) == 2, "bf16 operands");
@@ -615,7 +605,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
           mxv[rb] = *reinterpret_cast<const ct4*>(MT + (size_t)(j0 + (l & 15)) * Cp + 16 * rb + 4 * (l >> 4));
       }
       if (pair == 0)
-        mma_pair_dots<RBN, H, 4, KC>(t0, t1, D1, h, Wb1T, Sb1T, h, j0, W1T, S1T, h, pa, pe, pb);
+        mma_pair_dots<RBN, H, 4, KC, MC>(t0, t1, D1, h, Wb1, Sb1, d, j0, W1T, S1T, h, pa, pe, pb);
       else
         mma_pair_dots<RBN, H, 4, MC>(t0, t1, Hk, h, Wb2, Sb2, h, j0, W2T, S2T, d, pa, pe, pb);
       pa = wave_sum(pa);
@@ -666,8 +656,8 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, KcC, d, i0, Wb1, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, Kb, d, i0, Sb1, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a2, Q1T, Cp, i0, HT, Cp, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, RcC, d, i0, Wb2T, d, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, Rb, d, i0, Sb2T, d, j0);
+      mma_blk<CT, KC, MC, BCH::RB, BCH::CB, D>(a2, RcC, d, i0, Wb2, h, j0);
+      mma_blk<CT, KC, MC, BCH::RB, BCH::CB, D>(a2, Rb, d, i0, Sb2, h, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         f4 gv, zp;
 #pragma unroll
@@ -749,7 +739,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     __syncthreads();
 
     // ---- phase 4: Kbar (carried part) = -diag(cC) T3 - diag(b) T4 + Zkbar W1 ;
-    // adjoint of the chunk-entry state (in place, with its transposed copies)
+    // adjoint of the chunk-entry state (in place, fp32)
     for_blocks<CP, D>([&](int i0, int j0) {
       f4 kold[BCD::RB][BCD::CB];  // dk so far, requested ahead of the product
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
@@ -799,8 +789,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
           Wb1[e] = nw[r];
           Sb1[e] = ns[r];
         }
-        store4<CT>(Wb1T + (size_t)j * h + i, nw);
-        store4<CT>(Sb1T + (size_t)j * h + i, ns);
       });
     });
     for_blocks<D, H>([&](int i0, int j0) {  // W2bar, S2bar : d x h
@@ -828,8 +816,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
           Wb2[e] = nw[r];
           Sb2[e] = ns[r];
         }
-        store4<CT>(Wb2T + (size_t)j * d + i, nw);
-        store4<CT>(Sb2T + (size_t)j * d + i, ns);
       });
     });
     __syncthreads();
@@ -837,7 +823,6 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 #undef RF_
 #undef BQ_
 #undef BQF_
-#undef T_
   }
   // adjoint of the learned init for this unit
   float* dst = a.dWinit_part + (size_t)u * 2 * hd;
@@ -1058,22 +1043,21 @@ constexpr bool split_fits() {
 }
 
 struct SplitSizes {
-  size_t rec_ct, rec_f, b_ct;  // elements
+  size_t rec_ct, rec_f;  // elements
 };
 
 template <typename CT, int CP, int D, int H>
 SplitSizes split_sizes(int units, int nch) {
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const size_t t = (size_t)units * nch;
-  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n,
-                    (size_t)units * Y.bc.n};
+  return SplitSizes{t * Y.r.bc.n, t * Y.r.bf.n};
 }
 
 size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
 template <typename CT>
 size_t total_bytes(const SplitSizes& z) {
-  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4) + up256(z.b_ct * sizeof(CT));
+  return up256(z.rec_ct * sizeof(CT)) + up256(z.rec_f * 4);
 }
 
 template <typename CT>
@@ -1081,8 +1065,7 @@ SplitPtrs carve(void* ws, const SplitSizes& z, int units) {
   char* p = (char*)ws;
   SplitPtrs P{};
   P.brec = p; p += up256(z.rec_ct * sizeof(CT));
-  P.brec_f = (float*)p; p += up256(z.rec_f * 4);
-  P.tmpB = p;
+  P.brec_f = (float*)p;
   P.units = units;
   return P;
 }
