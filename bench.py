@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
 PEAK_FP32 = 157.3e12    # MI355X fp32, FLOP/s
+PEAK_HBM = 8.0e12       # MI355X HBM3E, bytes/s
 METRIC = "memory-layer fwd+bwd tokens/sec at seq 8192; % MFMA bf16 peak (rocprof)"
 
 
@@ -62,6 +63,36 @@ def step_flops(cfg):
     return f
 
 
+def hbm_bytes(cfg, name):
+    """Algorithmic HBM bytes of one launch of the gate scan or of one global
+    state-carry step (None for other labels).
+
+    global_scan (one per pass): reads the three gates (fp32) of every token of
+    every chain and writes six fp32 coefficients per token, plus four per chunk.
+    global_carry (one forward chunk): reads the chunk's carry operands D1^T, Hk^T
+    (C x hid each) and the four coefficient-scaled K^T, R^T (C x d each) in the
+    compute type, reads the entry state (V1, S1, V2, S2: 4 hid d fp32), writes
+    the exit state.  global_bwd_carry (one backward chunk): reads the ten
+    operands of the entry-adjoint products (Zkbar, Zqbar, Gbar, Hk, Hq: C x hid;
+    K, Q, R, Ykbar, dO: C x d) in the compute type, reads the state and the exit
+    adjoint, writes the entry adjoint (each 4 hid d fp32)."""
+    chains = cfg.B * cfg.H
+    d, h, C, L = cfg.d, cfg.hid, cfg.C_G, cfg.L
+    cts = 2 if cfg.dtype == 1 else 4
+    st = 4 * h * d * 4
+    if name == "global_scan":
+        return chains * (L * (3 * 4 + 6 * 4) + (L // C) * 16)
+    if name == "global_carry":
+        return chains * ((2 * h + 4 * d) * C * cts + 2 * st)
+    if name == "global_bwd_carry":
+        return chains * (5 * (h + d) * C * cts + 3 * st)
+    return None
+
+
+# labels timed inside another launch (reported separately, never the dominant launch)
+SECTIONS = ("global_carry", "global_bwd_carry")
+
+
 def launch_flops(cfg, name):
     """Algorithmic FLOPs one launch of `name` processes (None if not a GEMM kernel)."""
     tok = cfg.B * cfg.H * cfg.L
@@ -90,7 +121,36 @@ LAUNCH_SOURCES = {
     "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_common.h"] + _COMMON,
     "global_bwd_chunk": ["tnt_global_bwd.hip", "tnt_global_blk.hip"] + _COMMON,
     "global_fwd_chunk": ["tnt_global_fwd.hip", "tnt_global_blk.hip"] + _COMMON,
+    "global_scan": ["tnt_global_fwd.hip"] + _COMMON,
+    "global_carry": ["tnt_global_fwd.hip", "tnt_global_blk.hip"] + _COMMON,
+    "global_bwd_carry": ["tnt_global_bwd.hip", "tnt_global_blk.hip"] + _COMMON,
 }
+MFMA_FILE = {2: "mfma_ops_pretrain_B4H8L8192.txt"}
+
+
+def all_sources_hash():
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2511_07343_amd", "csrc")
+    for fn in sorted(os.listdir(d)):
+        with open(os.path.join(d, fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_mfma(workload):
+    """MFMA FLOPs per step counted by rocprofv3 (committed summary), or None
+    once any kernel source changed since the count was taken."""
+    fn = MFMA_FILE.get(workload)
+    path = os.path.join(ROOT, "profiles", fn) if fn else None
+    if not path or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            t = line.split()
+            if len(t) >= 6 and t[0] == "step" and t[1] == "sha256":
+                return float(t[5]) if t[2] == all_sources_hash() else None
+    return None
 
 
 def sources_hash(label):
@@ -156,6 +216,9 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the warmup (the "
                          "reference dispatch that scales HBM traffic counters)")
+    ap.add_argument("--mfma-probe", type=int, default=0, metavar="N",
+                    help="run one N x N x N bf16 matmul before the warmup (the reference "
+                         "dispatch that scales MFMA operation counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -184,6 +247,13 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.mfma_probe:
+        n = args.mfma_probe
+        a_ = torch.ones(n, n, dtype=torch.bfloat16, device=dev)
+        b_ = torch.ones(n, n, dtype=torch.bfloat16, device=dev)
+        torch.matmul(a_, b_)
+        torch.cuda.synchronize()
+        del a_, b_
 
     def step():
         s1 = tnt.tnt_mem_fwd(cfg, x["q"], x["k"], x["v"], x["lr"], x["mom"], x["decay"], x["W1"],
@@ -219,7 +289,7 @@ def main():
     peak = PEAK_BF16 if bf else PEAK_FP32
 
     # dominant kernel by total event time in the timed region
-    dom = max(kt.items(), key=lambda kv: kv[1][0])
+    dom = max(((k, v) for k, v in kt.items() if k not in SECTIONS), key=lambda kv: kv[1][0])
     name, (tot_ms, n) = dom
     fl = launch_flops(cfg, name)
     avg_ms = tot_ms / n
@@ -230,6 +300,27 @@ def main():
         ach = fl / (avg_ms * 1e-3) / 1e12
         roof.update(achieved=ach, frac=ach * 1e12 / peak, flops_per_launch=fl)
     roof["traffic"] = measured_traffic(args.workload, name)
+    # HBM-bound steps: the gate scan and the global state carry (forward, backward)
+    hbm = {}
+    for lab in ("global_scan",) + SECTIONS:
+        if lab not in kt or hbm_bytes(cfg, lab) is None:
+            continue
+        t_ms, n_l = kt[lab]
+        avg = t_ms / n_l
+        ab = hbm_bytes(cfg, lab)
+        tb = measured_traffic(args.workload, lab)
+        hbm[lab] = {"avg_launch_ms": avg, "launches": n_l, "alg_bytes": ab,
+                    "alg_GBps": ab / (avg * 1e-3) / 1e9,
+                    "alg_frac": ab / (avg * 1e-3) / PEAK_HBM,
+                    "counter_bytes": tb,
+                    "counter_GBps": None if tb is None else tb / (avg * 1e-3) / 1e9,
+                    "peak_GBps": PEAK_HBM / 1e9}
+    mf = measured_mfma(args.workload)
+    mfma = None
+    if mf is not None:
+        mfma = {"flops_per_step": mf, "tflops": mf / (ms_step * 1e-3) / 1e12,
+                "frac": mf / (ms_step * 1e-3) / peak, "source": "rocprofv3 PMC "
+                "SQ_INSTS_VALU_MFMA_MOPS_BF16 + _F32, scaled by a known bf16 GEMM"}
     props = torch.cuda.get_device_properties(dev)
     clk = getattr(props, "clock_rate", None)
     device = {"name": props.name, "compute_units": props.multi_processor_count,
@@ -248,8 +339,11 @@ def main():
         "algorithmic_tflops": flops / elapsed * args.steps / 1e12,
         "algorithmic_frac_of_peak": flops / elapsed * args.steps / peak,
         "roofline": roof,
+        "mfma_counted": mfma,
+        "hbm_kernels": hbm,
         "device": device,
-        "kernels_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())},
+        "kernels_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())
+                                if k not in SECTIONS},
     }
     if not args.no_cpu_baseline:
         unit = cfg.locals_[0][1] if cfg.locals_ else cfg.C_G

@@ -484,6 +484,21 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
 
 }  // namespace
 
+namespace tnt {
+int section_begin(const char* name, hipStream_t st) {
+  if (!g_timing.on || g_timing.rec.size() >= TIMING_CAP) return -1;
+  TimedLaunch t{name, g_timing.get(), g_timing.get()};
+  if (!t.a || !t.b) return -1;
+  if (hipEventRecord(t.a, st) != hipSuccess) return -1;
+  g_timing.rec.push_back(t);
+  return (int)g_timing.rec.size() - 1;
+}
+
+void section_end(int handle, hipStream_t st) {
+  if (handle >= 0 && handle < (int)g_timing.rec.size()) hipEventRecord(g_timing.rec[handle].b, st);
+}
+}  // namespace tnt
+
 extern "C" {
 
 int32_t tnt_abi_version(void) { return 1; }

@@ -579,8 +579,11 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
   const int ns = C / GTK;
+  const int sec = section_begin("global_carry", st);
   hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H>), dim3(ns, 4, chains), dim3(512), 0, st, a);
-  return launch_global_carry_reduce(a, n, ns, st);
+  const hipError_t e = launch_global_carry_reduce(a, n, ns, st);
+  section_end(sec, st);
+  return e;
 }
 
 template <typename IO, typename ACT_T, int ACT, int D, int H>
@@ -598,8 +601,11 @@ static hipError_t gbwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
   const int ns = C / GTK;
+  const int sec = section_begin("global_bwd_carry", st);
   hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H>), dim3(ns, 2, chains), dim3(512), 0, st, a);
-  return launch_gbwd_state_reduce(a, n, ns, st);
+  const hipError_t e = launch_gbwd_state_reduce(a, n, ns, st);
+  section_end(sec, st);
+  return e;
 }
 
 bool launch_global_fwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err) {

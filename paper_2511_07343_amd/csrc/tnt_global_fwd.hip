@@ -18,13 +18,22 @@
 namespace tnt {
 
 // ---------------------------------------------------------------------------
-// gate coefficients of a global chunk (one wavefront per (chunk, chain)).
+// gate coefficients of a global chunk (one 512-thread workgroup per (chunk,
+// chain); each thread owns a contiguous segment of the chunk's tokens).
 // tokc[t] = {cC_t, b_t, la_t, lb_t, s_t, e^{lb_C - lb_t}}; chunkc[n] = {A_C, B_C, E_C, 0} with
 //   cC_t = eta_t s_t,  s_t = sum_{m>=t} e^{la_C - la_m + lb_m - lb_t}
 //        = e^{la_C - la_t} + beta_{t+1} s_{t+1}          (suffix affine scan)
 //   b_t  = eta_t e^{lb_C - lb_t},  E_C = beta_0 s_0.
+// The prefix sums la, lb and the suffix scan of s run as wavefront scans
+// joined across the workgroup's waves through LDS.
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
+constexpr int GSCAN_THREADS = 512;
+constexpr int GSCAN_WAVES = GSCAN_THREADS / WAVE;
+
+__global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a) {
+  __shared__ float wa[GSCAN_WAVES], wb[GSCAN_WAVES];      // per-wave gate log sums
+  __shared__ float wp[GSCAN_WAVES], wq[GSCAN_WAVES];      // per-wave affine maps
+  __shared__ float s_in[GSCAN_WAVES + 1];                 // s at each wave's end
   const int n = blockIdx.x, chain = blockIdx.y;
   const int C = a.D.C, L = a.D.L;
   const size_t base = (size_t)chain * L + (size_t)n * C;
@@ -32,24 +41,37 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
   const float* mom = a.mom + base;
   const float* dec = a.decay + base;
   float* tk = a.tokc + base * TKS;
-  const int l = lane_id();
-  const int E = (C + WAVE - 1) / WAVE;
-  const int i0 = min(l * E, C), i1 = min(i0 + E, C);
+  const int l = lane_id(), w = wave_id(), t = threadIdx.x;
+  const int E = (C + GSCAN_THREADS - 1) / GSCAN_THREADS;
+  const int i0 = min(t * E, C), i1 = min(i0 + E, C);
   float sa = 0.f, sb = 0.f;
   for (int i = i0; i < i1; ++i) {
     sa += log_keep(dec[i]);
     sb += log_mom(mom[i]);
   }
   const float ia = wave_incl_sum(sa), ib = wave_incl_sum(sb);
-  const float laC = __shfl(ia, WAVE - 1, WAVE), lbC = __shfl(ib, WAVE - 1, WAVE);
-  float pa = ia - sa, pb = ib - sb;
+  if (l == WAVE - 1) {
+    wa[w] = ia;
+    wb[w] = ib;
+  }
+  __syncthreads();
+  float oa = 0.f, ob = 0.f, laC = 0.f, lbC = 0.f;
+  for (int v = 0; v < GSCAN_WAVES; ++v) {
+    if (v < w) {
+      oa += wa[v];
+      ob += wb[v];
+    }
+    laC += wa[v];
+    lbC += wb[v];
+  }
+  float pa = oa + ia - sa, pb = ob + ib - sb;
   for (int i = i0; i < i1; ++i) {
     pa += log_keep(dec[i]);
     pb += log_mom(mom[i]);
     tk[(size_t)i * TKS + 2] = pa;
     tk[(size_t)i * TKS + 3] = pb;
   }
-  // segment affine map s_{i0} = P s_{i1} + Q (own writes are visible to the lane)
+  // segment affine map s_{i0} = P s_{i1} + Q (own writes are visible to the thread)
   float P = 1.f, Q = 0.f;
   for (int i = i1 - 1; i >= i0; --i) {
     const float ai = expf(laC - tk[(size_t)i * TKS + 2]);
@@ -57,7 +79,7 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
     Q = ai + mi * Q;
     P = mi * P;
   }
-  // suffix composition over lanes: G_l = F_l o F_{l+1} o ... o F_63
+  // suffix composition over the wave's lanes: G_l = F_l o F_{l+1} o ... o F_63
 #pragma unroll
   for (int o = 1; o < WAVE; o <<= 1) {
     const float Po = __shfl_down(P, o, WAVE), Qo = __shfl_down(Q, o, WAVE);
@@ -66,9 +88,23 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
       P = P * Po;
     }
   }
-  float sin = __shfl_down(Q, 1, WAVE);  // s at the first token of the next segment
-  if (l == WAVE - 1) sin = 0.f;
-  float sv = sin;
+  if (l == 0) {
+    wp[w] = P;
+    wq[w] = Q;
+  }
+  __syncthreads();
+  if (t == 0) {  // s at the end of each wave's tokens, from the chunk's end (s = 0) back
+    float sv = 0.f;
+    s_in[GSCAN_WAVES] = 0.f;
+    for (int v = GSCAN_WAVES - 1; v >= 0; --v) {
+      s_in[v + 1] = sv;
+      sv = wp[v] * sv + wq[v];
+    }
+  }
+  __syncthreads();
+  const float send = s_in[w + 1];  // s at the first token after this wave's tokens
+  const float Pn = __shfl_down(P, 1, WAVE), Qn = __shfl_down(Q, 1, WAVE);
+  float sv = (l == WAVE - 1) ? send : Pn * send + Qn;  // s at this thread's i1
   for (int i = i1 - 1; i >= i0; --i) {
     const float ai = expf(laC - tk[(size_t)i * TKS + 2]);
     const float mi = (i + 1 < C) ? mom[i + 1] : 0.f;
@@ -79,18 +115,18 @@ __global__ void __launch_bounds__(64) global_scan_kernel(GlobalArgs a) {
     tk[(size_t)i * TKS + 4] = sv;
     tk[(size_t)i * TKS + 5] = ebt;
   }
-  if (l == 0) {
+  if (t == 0) {
     float* cc = a.chunkc + ((size_t)chain * (L / C) + n) * 4;
     cc[0] = expf(laC);
     cc[1] = expf(lbC);
-    cc[2] = (C > 0 ? mom[0] : 0.f) * sv;  // lane 0 ends at i = 0: sv = s_0
+    cc[2] = (C > 0 ? mom[0] : 0.f) * sv;  // thread 0 ends at i = 0: sv = s_0
     cc[3] = 0.f;
   }
 }
 
 hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st) {
   dim3 grid(a.D.L / a.D.C, a.D.B * a.D.H);
-  hipLaunchKernelGGL(global_scan_kernel, grid, dim3(64), 0, st, a);
+  hipLaunchKernelGGL(global_scan_kernel, grid, dim3(GSCAN_THREADS), 0, st, a);
   return hipGetLastError();
 }
 

@@ -151,6 +151,12 @@ int global_blk_splits(const Dims& D);
 hipError_t launch_global_carry_reduce(const GlobalArgs& a, int n, int nsplit, hipStream_t st);
 hipError_t launch_gbwd_state_reduce(const GlobalArgs& a, int n, int nsplit, hipStream_t st);
 bool launch_global_fwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err);
+// Opt-in timing of one step inside a composite launch (the global state-carry
+// GEMMs and their reduction): section_begin records a start event on `st` and
+// returns a handle (-1 while launch timing is off); section_end records the
+// matching stop event.  The pair is reported under `name` with the launches.
+int section_begin(const char* name, hipStream_t st);
+void section_end(int handle, hipStream_t st);
 bool launch_global_bwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err);
 int global_bwd_splits(const Dims& D);
 constexpr int GRED_BLOCKS = 16;  // blocks per chain of the split reductions
