@@ -216,6 +216,10 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the warmup (the "
                          "reference dispatch that scales HBM traffic counters)")
+    ap.add_argument("--seq", type=int, default=0,
+                    help="override the workload's sequence length (global chunk and local "
+                         "shard are capped at it); the counter summaries then do not apply")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
     ap.add_argument("--mfma-probe", type=int, default=0, metavar="N",
                     help="run one N x N x N bf16 matmul before the warmup (the reference "
                          "dispatch that scales MFMA operation counters)")
@@ -229,7 +233,19 @@ def main():
     from paper_2511_07343_amd import inputs, tnt
 
     cfg = inputs.WORKLOADS[args.workload]
-    inp = inputs.make_inputs(cfg, args.workload)
+    seed = args.workload
+    prof_key = args.workload  # committed counter summaries describe the unmodified workloads
+    if args.seq or args.batch:
+        import dataclasses
+        L = args.seq or cfg.L
+        B = args.batch or cfg.B
+        loc = tuple((c, min(s_, L)) for c, s_ in cfg.locals_)
+        cfg = dataclasses.replace(
+            cfg, B=B, L=L, C_G=min(cfg.C_G, L), locals_=loc,
+            name=f"{cfg.name.split(' B')[0]} B{B} H{cfg.H} L{L} d{cfg.d} h{cfg.hid} "
+                 f"CG{min(cfg.C_G, L)} " + " ".join(f"CL{c} SL{s_}" for c, s_ in loc))
+        prof_key = None
+    inp = inputs.make_inputs(cfg, seed)
     dev = torch.device("cuda:0")
     x = tnt.device_inputs(inp, cfg, device=dev)
     u8 = lambda n: torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
@@ -299,7 +315,7 @@ def main():
     if fl is not None:
         ach = fl / (avg_ms * 1e-3) / 1e12
         roof.update(achieved=ach, frac=ach * 1e12 / peak, flops_per_launch=fl)
-    roof["traffic"] = measured_traffic(args.workload, name)
+    roof["traffic"] = measured_traffic(prof_key, name)
     # HBM-bound steps: the gate scan and the global state carry (forward, backward)
     hbm = {}
     for lab in ("global_scan",) + SECTIONS:
@@ -308,14 +324,14 @@ def main():
         t_ms, n_l = kt[lab]
         avg = t_ms / n_l
         ab = hbm_bytes(cfg, lab)
-        tb = measured_traffic(args.workload, lab)
+        tb = measured_traffic(prof_key, lab)
         hbm[lab] = {"avg_launch_ms": avg, "launches": n_l, "alg_bytes": ab,
                     "alg_GBps": ab / (avg * 1e-3) / 1e9,
                     "alg_frac": ab / (avg * 1e-3) / PEAK_HBM,
                     "counter_bytes": tb,
                     "counter_GBps": None if tb is None else tb / (avg * 1e-3) / 1e9,
                     "peak_GBps": PEAK_HBM / 1e9}
-    mf = measured_mfma(args.workload)
+    mf = measured_mfma(prof_key)
     mfma = None
     if mf is not None:
         mfma = {"flops_per_step": mf, "tflops": mf / (ms_step * 1e-3) / 1e12,
