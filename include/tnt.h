@@ -141,6 +141,45 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
                        float* dmom, float* ddecay, float* dW1_init, float* dW2_init,
                        void* workspace, size_t ws_bytes, void* stream);
 
+/* ---- Step-wise forward (prefill / decode) from a carried state ----------
+ * Within a chunk every gradient is taken at the chunk-entry weights W^ and
+ * folded in with momentum and decay (Sec. 2.2; App. D), so the chunkwise rule
+ * runs token by token once W^ is carried beside the running weights:
+ *     S_t = mom_t S_{t-1} - lr_t grad l(W^; k_t, v_t),  W_t = (1 - decay_t) W_{t-1} + S_t,
+ * with W^ <- W at each chunk start.  The global memory answers f(V^, q_t)
+ * (entry state, Sec. 4.1.2 retrieval box); a local memory resets (W^, W, S, M)
+ * to (W_init, W_init, 0, 0) at each shard start and answers f(W_t, M_t q_t)
+ * after the update (Sec. 4.1.1 local update, Sec. 4.1.2; App. C).  Feeding a
+ * sequence through tnt_mem_step in pieces of any length gives, token for
+ * token, the o of tnt_mem_fwd on the whole sequence (to rounding).  cfg->L is
+ * ignored by these three calls (the sequence is open-ended); every other
+ * field is validated as for tnt_mem_fwd.  The state is device memory owned by
+ * the caller: per memory m and per (batch row, head) chain, fp32
+ *     W^1 [hid][d], W^2 [d][hid], W1 [hid][d], W2 [d][hid], S1 [hid][d],
+ *     S2 [d][hid], M [d][d]       (M unused for the global memory),
+ * blocks ordered [M][B][H].  Calls on one state must be serialised (same
+ * stream); the work is one workgroup per chain, latency- and HBM-bound. */
+
+/* Bytes of the carried state (0 if the config is invalid). */
+size_t tnt_mem_state_size(const tnt_config* cfg);
+
+/* Sets `state` to the start of a sequence: every memory at its initial
+ * weights (W^ = W = W_init of the chain's head), zero momenta and Q-K sums. */
+tnt_status tnt_mem_state_init(const tnt_config* cfg, const float* W1_init,
+                              const float* W2_init, void* state, void* stream);
+
+/* Forward over T >= 0 further tokens of every chain, advancing `state`.
+ *   pos   : tokens `state` has consumed so far (0 after tnt_mem_state_init);
+ *           chunk and shard boundaries are taken from pos + t.  A pos that
+ *           does not match the state's history gives undefined outputs.
+ *   q, k, v, o : [B][H][T][d] (I/O dtype);  lr, mom, decay : [M][B][H][T] fp32;
+ *   W1_init, W2_init : as for tnt_mem_fwd (read at local shard starts).
+ * T == 0 enqueues nothing.  TNT_ERR_SHAPE for pos < 0 or T < 0. */
+tnt_status tnt_mem_step(const tnt_config* cfg, int64_t pos, int32_t T, const void* q,
+                        const void* k, const void* v, const float* lr, const float* mom,
+                        const float* decay, const float* W1_init, const float* W2_init,
+                        void* state, void* o, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* tnt_strerror(tnt_status status);
 

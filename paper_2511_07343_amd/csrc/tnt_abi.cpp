@@ -28,20 +28,23 @@ bool one_of(int x, std::initializer_list<int> v) {
   return false;
 }
 
-tnt_status validate(const tnt_config* c) {
+// need_L = false: the step-wise entry points, where the sequence is open-ended
+// and L is ignored
+tnt_status validate(const tnt_config* c, bool need_L = true) {
   if (!c) return TNT_ERR_NULL;
   if (c->act < 0 || c->act > 1 || c->qk_proj < 0 || c->qk_proj > 1 || c->qk_scope < 0 ||
       c->qk_scope > 1 || c->dtype < 0 || c->dtype > 1 || c->has_global < 0 || c->has_global > 1)
     return TNT_ERR_ARG;
-  if (c->B <= 0 || c->H <= 0 || c->L <= 0 || c->d <= 0 || c->hid <= 0) return TNT_ERR_SHAPE;
+  if (c->B <= 0 || c->H <= 0 || (need_L && c->L <= 0) || c->d <= 0 || c->hid <= 0)
+    return TNT_ERR_SHAPE;
   if (c->n_local < 0 || c->n_local > TNT_MAX_LOCAL) return TNT_ERR_SHAPE;
   if (c->has_global + c->n_local < 1) return TNT_ERR_SHAPE;
   if (c->has_global) {
-    if (c->C_G <= 0 || c->L % c->C_G) return TNT_ERR_SHAPE;
+    if (c->C_G <= 0 || (need_L && c->L % c->C_G)) return TNT_ERR_SHAPE;
   }
   for (int i = 0; i < c->n_local; ++i) {
     if (c->C_L[i] <= 0 || c->S_L[i] <= 0) return TNT_ERR_SHAPE;
-    if (c->S_L[i] % c->C_L[i] || c->L % c->S_L[i]) return TNT_ERR_SHAPE;
+    if (c->S_L[i] % c->C_L[i] || (need_L && c->L % c->S_L[i])) return TNT_ERR_SHAPE;
   }
   if (!one_of(c->d, {16, 32, 64, 128})) return TNT_ERR_UNSUPPORTED;
   if (!one_of(c->hid, {16, 32, 64, 128, 256, 512})) return TNT_ERR_UNSUPPORTED;
@@ -622,6 +625,67 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
   }
   return run_backward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, dO, sv, dq, dk, dv,
                       dlr, dmom, ddecay, dW1_init, dW2_init, ws, st);
+}
+
+size_t tnt_mem_state_size(const tnt_config* cfg) {
+  if (validate(cfg, false) != TNT_OK) return 0;
+  const size_t M = (size_t)cfg->has_global + cfg->n_local;
+  return M * cfg->B * cfg->H * step_state_floats(cfg->d, cfg->hid) * sizeof(float);
+}
+
+}  // extern "C"
+
+namespace {
+StepArgs step_args(const tnt_config* c) {
+  static_assert(1 + TNT_MAX_LOCAL <= (int)(sizeof(StepArgs::C) / sizeof(int)), "StepArgs::C");
+  StepArgs a{};
+  a.B = c->B; a.H = c->H; a.d = c->d; a.hid = c->hid;
+  a.M = c->has_global + c->n_local;
+  a.has_global = c->has_global; a.act = c->act; a.qk_proj = c->qk_proj;
+  a.qk_scope = c->qk_scope; a.bf16 = c->dtype == TNT_BF16;
+  int m = 0;
+  if (c->has_global) { a.C[m] = c->C_G; a.S[m] = 0; ++m; }
+  for (int i = 0; i < c->n_local; ++i, ++m) { a.C[m] = c->C_L[i]; a.S[m] = c->S_L[i]; }
+  a.mem_stride = step_state_floats(c->d, c->hid);
+  return a;
+}
+}  // namespace
+
+extern "C" {
+
+tnt_status tnt_mem_state_init(const tnt_config* cfg, const float* W1_init, const float* W2_init,
+                              void* state, void* stream) {
+  tnt_status s = validate(cfg, false);
+  if (s != TNT_OK) return s;
+  if (!W1_init || !W2_init || !state) return TNT_ERR_NULL;
+  for (const void* p : {(const void*)W1_init, (const void*)W2_init, (const void*)state})
+    if (misaligned(p)) return TNT_ERR_ALIGN;
+  StepArgs a = step_args(cfg);
+  a.W1i = W1_init; a.W2i = W2_init; a.state = (float*)state;
+  return launch_step_init(a, (hipStream_t)stream) == hipSuccess ? TNT_OK : TNT_ERR_HIP;
+}
+
+tnt_status tnt_mem_step(const tnt_config* cfg, int64_t pos, int32_t T, const void* q,
+                        const void* k, const void* v, const float* lr, const float* mom,
+                        const float* decay, const float* W1_init, const float* W2_init,
+                        void* state, void* o, void* stream) {
+  tnt_status s = validate(cfg, false);
+  if (s != TNT_OK) return s;
+  if (pos < 0 || T < 0) return TNT_ERR_SHAPE;
+  if (T == 0) return TNT_OK;
+  if (!q || !k || !v || !lr || !mom || !decay || !W1_init || !W2_init || !state || !o)
+    return TNT_ERR_NULL;
+  for (const void* p : {(const void*)q, (const void*)k, (const void*)v, (const void*)lr,
+                        (const void*)mom, (const void*)decay, (const void*)W1_init,
+                        (const void*)W2_init, (const void*)state, (const void*)o})
+    if (misaligned(p)) return TNT_ERR_ALIGN;
+  StepArgs a = step_args(cfg);
+  a.T = T; a.pos = pos;
+  a.q = q; a.k = k; a.v = v; a.lr = lr; a.mom = mom; a.decay = decay;
+  a.W1i = W1_init; a.W2i = W2_init; a.state = (float*)state; a.o = o;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = timed("step", st, [&]() { return launch_step(a, st); });
+  return e == hipSuccess ? TNT_OK : TNT_ERR_HIP;
 }
 
 }  // extern "C"

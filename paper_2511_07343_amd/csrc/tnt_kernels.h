@@ -160,6 +160,25 @@ void section_end(int handle, hipStream_t st);
 bool launch_global_bwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_t* err);
 int global_bwd_splits(const Dims& D);
 constexpr int GRED_BLOCKS = 16;  // blocks per chain of the split reductions
+
+// Step-wise forward from a carried state (tnt_mem_step).  Memory m's chunk is
+// C[m] and, for a local memory, its shard S[m].  state: per (memory, chain) a
+// block of mem_stride fp32 = W^1, W^2 (chunk-entry), W1, W2, S1, S2 (each
+// hid*d) and the Q-K sum M (d*d).
+struct StepArgs {
+  int B, H, T, d, hid, M, has_global, act, qk_proj, qk_scope, bf16;
+  long long pos;       // tokens the state has consumed before this call
+  int C[9], S[9];
+  const void *q, *k, *v;                      // [B][H][T][d]
+  const float *lr, *mom, *decay;              // [M][B][H][T]
+  const float *W1i, *W2i;                     // [M][H][hid][d], [M][H][d][hid]
+  float* state;
+  void* o;                                    // [B][H][T][d]
+  size_t mem_stride;
+};
+size_t step_state_floats(int d, int hid);
+hipError_t launch_step_init(const StepArgs& a, hipStream_t st);
+hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
 struct SumJobs {  // up to three (partials, output) pairs summed by one launch
   const float* parts[3];

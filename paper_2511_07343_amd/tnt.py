@@ -23,7 +23,8 @@ TNT_WS_FWD, TNT_WS_BWD, TNT_WS_BWD_RECOMPUTE = 0, 1, 2
 STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPPORTED",
           4: "TNT_ERR_WORKSPACE", 5: "TNT_ERR_ALIGN", 6: "TNT_ERR_HIP", 7: "TNT_ERR_ARG"}
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
-            "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read"]
+            "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read",
+            "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step"]
 
 
 class TntError(RuntimeError):
@@ -61,6 +62,12 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_mem_fwd.restype = ctypes.c_int
     L.tnt_mem_bwd.argtypes = [cp] + [vp] * 19 + [sz, vp]
     L.tnt_mem_bwd.restype = ctypes.c_int
+    L.tnt_mem_state_size.argtypes = [cp]
+    L.tnt_mem_state_size.restype = sz
+    L.tnt_mem_state_init.argtypes = [cp, vp, vp, vp, vp]
+    L.tnt_mem_state_init.restype = ctypes.c_int
+    L.tnt_mem_step.argtypes = [cp, ctypes.c_int64, i32] + [vp] * 11
+    L.tnt_mem_step.restype = ctypes.c_int
     L.tnt_strerror.argtypes = [ctypes.c_int]
     L.tnt_strerror.restype = ctypes.c_char_p
     L.tnt_abi_version.argtypes = []
@@ -128,6 +135,24 @@ def tnt_mem_bwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, dO, saved, dq, d
                              _p(W1_init), _p(W2_init), _p(dO), _p(saved), _p(dq), _p(dk),
                              _p(dv), _p(dlr), _p(dmom), _p(ddecay), _p(dW1_init),
                              _p(dW2_init), _p(workspace), ws_bytes, _stream(stream))
+
+
+def tnt_mem_state_size(cfg: LayerConfig) -> int:
+    return lib().tnt_mem_state_size(ctypes.byref(to_c(cfg)))
+
+
+def tnt_mem_state_init(cfg, W1_init, W2_init, state, stream=None) -> int:
+    c = to_c(cfg)
+    return lib().tnt_mem_state_init(ctypes.byref(c), _p(W1_init), _p(W2_init), _p(state),
+                                    _stream(stream))
+
+
+def tnt_mem_step(cfg, pos, T, q, k, v, lr, mom, decay, W1_init, W2_init, state, o,
+                 stream=None) -> int:
+    c = to_c(cfg)
+    return lib().tnt_mem_step(ctypes.byref(c), pos, T, _p(q), _p(k), _p(v), _p(lr), _p(mom),
+                              _p(decay), _p(W1_init), _p(W2_init), _p(state), _p(o),
+                              _stream(stream))
 
 
 def tnt_timing_enable(on: bool) -> int:
@@ -207,3 +232,33 @@ def backward(cfg: LayerConfig, x: Dict[str, torch.Tensor], dO: torch.Tensor,
     if st != 0:
         raise TntError(st, "tnt_mem_bwd")
     return g
+
+
+def step_forward(cfg: LayerConfig, x: Dict[str, torch.Tensor], pieces, state=None, pos: int = 0,
+                 stream=None):
+    """Feed the sequence in ``x`` through tnt_mem_step in consecutive pieces of
+    the given lengths (starting at token ``pos`` of ``x`` with ``state``, or
+    from a fresh state); returns (o of the fed tokens [B,H,sum(pieces),d], state)."""
+    dev = x["q"].device
+    if state is None:
+        state = _bytes(tnt_mem_state_size(cfg), dev)
+        st = tnt_mem_state_init(cfg, x["W1"], x["W2"], state, stream=stream)
+        if st != 0:
+            raise TntError(st, "tnt_mem_state_init")
+    outs = []
+    t0 = pos
+    for T in pieces:
+        sl = slice(t0, t0 + T)
+        # fresh copies: a slice that is already contiguous would be an offset
+        # view, not 16-byte aligned in general
+        cp = lambda t: t.clone(memory_format=torch.contiguous_format)
+        q, k, v = (cp(x[n][:, :, sl]) for n in ("q", "k", "v"))
+        lr, mom, dec = (cp(x[n][..., sl]) for n in ("lr", "mom", "decay"))
+        o = torch.empty_like(q)
+        st = tnt_mem_step(cfg, t0, T, q, k, v, lr, mom, dec, x["W1"], x["W2"], state, o,
+                          stream=stream)
+        if st != 0:
+            raise TntError(st, "tnt_mem_step")
+        outs.append(o)
+        t0 += T
+    return torch.cat(outs, 2), state

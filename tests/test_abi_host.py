@@ -93,3 +93,45 @@ def test_null_and_alignment_and_workspace():
     c = tnt.to_c(cfg.replace(has_global=0))
     st = tnt.lib().tnt_mem_fwd(ctypes.byref(c), *([256] * 9), 256, None, 256, 1 << 40, None)
     assert st == 2
+
+
+# ---------------------------------------------------------------- step-wise entry points
+def test_state_size_formula():
+    cfg = WORKLOADS[3]  # global + two locals, d 64, hid 256
+    M = cfg.has_global + len(cfg.locals_)
+    per = 6 * cfg.hid * cfg.d + cfg.d * cfg.d
+    assert tnt.tnt_mem_state_size(cfg) == M * cfg.B * cfg.H * per * 4
+
+
+def test_state_size_ignores_L():
+    """The step-wise calls take an open-ended sequence: L need not be a
+    multiple of the chunk or shard sizes."""
+    cfg = small_config(L=1)
+    assert tnt.tnt_mem_state_size(cfg) > 0
+    assert tnt.tnt_mem_state_size(small_config(d=24)) == 0
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(locals_=((8, 12),)), 2),         # S_L % C_L
+    (dict(d=24), 3),
+    (dict(act=5), 7),
+    (dict(B=0), 2),
+])
+def test_step_rejects_bad_config(bad, code):
+    import dataclasses
+    cfg = dataclasses.replace(small_config(), **bad)
+    p = 256
+    assert tnt.tnt_mem_step(cfg, 0, 4, p, p, p, p, p, p, p, p, p, p, stream=0) == code
+    assert tnt.tnt_mem_state_init(cfg, p, p, p, stream=0) == code
+
+
+def test_step_rejects_bad_arguments():
+    cfg = small_config()
+    p = 256
+    assert tnt.tnt_mem_step(cfg, -1, 4, p, p, p, p, p, p, p, p, p, p, stream=0) == 2
+    assert tnt.tnt_mem_step(cfg, 0, -1, p, p, p, p, p, p, p, p, p, p, stream=0) == 2
+    assert tnt.tnt_mem_step(cfg, 0, 4, p, p, p, p, p, p, p, p, None, p, stream=0) == 1
+    assert tnt.tnt_mem_step(cfg, 0, 4, p + 8, p, p, p, p, p, p, p, p, p, stream=0) == 5
+    assert tnt.tnt_mem_state_init(cfg, p, p, None, stream=0) == 1
+    # T == 0 enqueues nothing and succeeds without touching the pointers
+    assert tnt.tnt_mem_step(cfg, 0, 0, p, p, p, p, p, p, p, p, p, p, stream=0) == 0

@@ -1,0 +1,106 @@
+"""GPU parity of the step-wise forward (tnt_mem_state_init + tnt_mem_step).
+
+The sequence is fed in pieces whose boundaries fall inside chunks and shards
+(and one token at a time); the outputs are compared element by element with
+the fp64 oracle's whole-sequence forward (tolerance: max_i |gpu - oracle| /
+max_i |oracle| <= 1e-4 for fp32 inputs, 2e-2 for bf16), with the chunk-parallel
+tnt_mem_fwd on the same inputs, and with themselves: the per-token work does
+not depend on how the sequence is cut, so every cut gives bitwise the same o.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2511_07343_amd import tnt
+from paper_2511_07343_amd.inputs import (ACT_GELU, ACT_SILU, BF16, F32, QK_CHUNK, make_inputs,
+                                         max_rel_err, small_config)
+
+pytestmark = pytest.mark.gpu
+torch.set_num_threads(4)
+
+
+def tol(cfg):
+    return 2e-2 if cfg.dtype == BF16 else 1e-4
+
+
+CASES = [
+    (small_config(F32, ACT_GELU, B=2, H=2, L=64, d=16, hid=32, C_G=16,
+                  locals_=((8, 32), (4, 16)), name="f32 global + two locals"),
+     [5, 11, 1, 1, 16, 30]),
+    (small_config(F32, ACT_SILU, B=1, H=2, L=48, d=16, hid=32, C_G=24, locals_=((8, 16),),
+                  qk_scope=QK_CHUNK, name="f32 chunk-scope Q-K"),
+     [7, 9, 32]),
+    (small_config(F32, ACT_SILU, B=1, H=1, L=32, d=32, hid=64, C_G=32, locals_=((4, 16),),
+                  has_global=0, qk_proj=0, name="f32 local only, no Q-K"),
+     [3, 29]),
+    (small_config(BF16, ACT_SILU, B=1, H=2, L=128, d=64, hid=256, C_G=64, locals_=((16, 64),),
+                  name="bf16 d64 h256"),
+     [37, 1, 1, 25, 64]),
+    (small_config(BF16, ACT_GELU, B=1, H=1, L=64, d=128, hid=512, C_G=32, locals_=((16, 32),),
+                  name="bf16 d128 h512"),
+     [20, 44]),
+]
+
+
+def oracle_o(cfg, inp):
+    ref = O.forward_pairs(inp, cfg, O.all_pairs(cfg))
+    return ref.numpy().reshape(cfg.B, cfg.H, cfg.L, cfg.d)
+
+
+@pytest.mark.parametrize("cfg,pieces", CASES, ids=lambda c: c.name if hasattr(c, "name") else "")
+def test_step_pieces_match_oracle_and_forward(cfg, pieces):
+    assert sum(pieces) == cfg.L
+    inp = make_inputs(cfg, 401)
+    print(f"\n[case] step {cfg.name} pieces {pieces}", flush=True)
+    x = tnt.device_inputs(inp, cfg)
+    o_step, _ = tnt.step_forward(cfg, x, pieces)
+    o_fwd, _, _ = tnt.forward(cfg, x, save=False)
+    torch.cuda.synchronize()
+    got = o_step.float().cpu().numpy()
+    ref = oracle_o(cfg, inp)
+    e = max_rel_err(got, ref)
+    e2 = max_rel_err(got, o_fwd.float().cpu().numpy())
+    print(f"  o vs oracle {e:.3e}, vs tnt_mem_fwd {e2:.3e}", flush=True)
+    assert np.isfinite(got).all()
+    assert e <= tol(cfg)
+    assert e2 <= 2 * tol(cfg)
+
+
+@pytest.mark.parametrize("idx", [0, 3])
+def test_step_cut_invariance(idx):
+    """One call over the whole sequence, one token per call, and a prefill
+    followed by decode give bitwise the same outputs."""
+    cfg, pieces = CASES[idx]
+    inp = make_inputs(cfg, 402)
+    print(f"\n[case] cut invariance {cfg.name}", flush=True)
+    x = tnt.device_inputs(inp, cfg)
+    whole, s_whole = tnt.step_forward(cfg, x, [cfg.L])
+    single, s_single = tnt.step_forward(cfg, x, [1] * cfg.L)
+    half = cfg.L // 2 + 3
+    pre, state = tnt.step_forward(cfg, x, [half])
+    dec, state = tnt.step_forward(cfg, x, [1] * (cfg.L - half), state=state, pos=half)
+    torch.cuda.synchronize()
+    assert torch.equal(whole, single)
+    assert torch.equal(whole, torch.cat([pre, dec], 2))
+    assert torch.equal(s_whole, s_single)
+    assert torch.equal(s_whole, state)
+
+
+def test_step_global_final_state():
+    """After the whole sequence the global memory's running (W1, W2, S1, S2)
+    in the carried state equal the oracle's final global state."""
+    cfg, _ = CASES[0]
+    inp = make_inputs(cfg, 403)
+    x = tnt.device_inputs(inp, cfg)
+    _, state = tnt.step_forward(cfg, x, [cfg.L])
+    torch.cuda.synchronize()
+    hd, dd = cfg.hid * cfg.d, cfg.d * cfg.d
+    st = state[: cfg.B * cfg.H * (6 * hd + dd) * 4].view(torch.float32)
+    st = st.view(cfg.B * cfg.H, 6 * hd + dd)[:, 2 * hd: 6 * hd].cpu().numpy()
+    pairs = O.all_pairs(cfg)
+    _, fin = O.forward_pairs(inp, cfg, pairs, with_final=True)
+    ref = np.concatenate([f.numpy().reshape(len(pairs), -1) for f in fin], 1)
+    e = max_rel_err(st, ref)
+    print(f"  final global state vs oracle {e:.3e}", flush=True)
+    assert e <= tol(cfg)
