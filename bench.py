@@ -203,6 +203,73 @@ def cpu_baseline(cfg, inp, budget_tokens):
                       f"(fp64 torch CPU autograd, {dt:.1f} s)"}
 
 
+def decode_bench(args, cfg, x, dev):
+    """Step-wise forward: `args.steps` calls of tnt_mem_step with `args.decode`
+    tokens per chain each, continuing one carried state; one JSON line."""
+    import torch
+    from paper_2511_07343_amd import tnt
+
+    T = args.decode
+    M = cfg.has_global + len(cfg.locals_)
+    state = torch.empty(tnt.tnt_mem_state_size(cfg), dtype=torch.uint8, device=dev)
+    if tnt.tnt_mem_state_init(cfg, x["W1"], x["W2"], state):
+        raise RuntimeError("tnt_mem_state_init failed")
+    n_calls = args.warmup + args.steps
+    if n_calls * T > cfg.L:
+        raise SystemExit(f"--decode {T} x {n_calls} calls exceeds the workload's {cfg.L} tokens")
+    cp = lambda t: t.clone(memory_format=torch.contiguous_format)
+    pieces = []
+    for c in range(n_calls):
+        sl = slice(c * T, (c + 1) * T)
+        pieces.append([cp(x[n][:, :, sl]) for n in ("q", "k", "v")] +
+                      [cp(x[n][..., sl]) for n in ("lr", "mom", "decay")])
+    o = torch.empty_like(pieces[0][0])
+    stream = torch.cuda.current_stream(dev)
+
+    def call(c):
+        q, k, v, lr, mom, dec = pieces[c]
+        st = tnt.tnt_mem_step(cfg, c * T, T, q, k, v, lr, mom, dec, x["W1"], x["W2"], state, o,
+                              stream=stream)
+        if st:
+            raise tnt.TntError(st, "tnt_mem_step")
+
+    for c in range(args.warmup):
+        call(c)
+    torch.cuda.synchronize()
+    tnt.tnt_timing_read()
+    tnt.tnt_timing_enable(True)
+    t0 = time.perf_counter()
+    for c in range(args.warmup, n_calls):
+        call(c)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    tnt.tnt_timing_enable(False)
+    kt = tnt.tnt_timing_read()
+    ms_call = 1e3 * (t1 - t0) / args.steps
+    ev_ms = kt["step"][0] / kt["step"][1]
+    # per token and memory: read W^1, W^2, W1, W2, S1, S2, write W1, W2, S1, S2 (fp32)
+    alg = M * cfg.B * cfg.H * T * 10 * cfg.hid * cfg.d * 4
+    res = {
+        "metric": f"step-wise forward tokens/s ({T} token(s) per chain per call)",
+        "value": cfg.B * T * args.steps / (t1 - t0), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_call,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 state, " + ("bf16" if cfg.dtype == inputs_bf16() else "f32") + " I/O",
+        "data": "synthetic (seeded Gaussian, unit q/k)",
+        "config": {"workload": cfg.name, "batch": cfg.B, "heads": cfg.H, "tokens_per_call": T},
+        "roofline": {"bound": "hbm", "kernel": "step", "achieved": alg / (ev_ms * 1e-3) / 1e9,
+                     "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": alg / (ev_ms * 1e-3) / PEAK_HBM, "traffic": None,
+                     "avg_launch_ms": ev_ms, "alg_bytes_per_launch": alg},
+    }
+    print(json.dumps(res), flush=True)
+
+
+def inputs_bf16():
+    from paper_2511_07343_amd import inputs
+    return inputs.BF16
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -220,6 +287,9 @@ def main():
                     help="override the workload's sequence length (global chunk and local "
                          "shard are capped at it); the counter summaries then do not apply")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
+    ap.add_argument("--decode", type=int, default=0, metavar="T",
+                    help="time the step-wise forward (tnt_mem_step) with T tokens per chain "
+                         "per call instead of the fwd+bwd step")
     ap.add_argument("--mfma-probe", type=int, default=0, metavar="N",
                     help="run one N x N x N bf16 matmul before the warmup (the reference "
                          "dispatch that scales MFMA operation counters)")
@@ -248,6 +318,8 @@ def main():
     inp = inputs.make_inputs(cfg, seed)
     dev = torch.device("cuda:0")
     x = tnt.device_inputs(inp, cfg, device=dev)
+    if args.decode:
+        return decode_bench(args, cfg, x, dev)
     u8 = lambda n: torch.empty(max(n, 16), dtype=torch.uint8, device=dev)
     o = torch.empty_like(x["q"])
     saved = u8(tnt.tnt_mem_saved_size(cfg))
