@@ -27,35 +27,84 @@ namespace {
 
 constexpr int STEP_THREADS = 512;
 constexpr int STEP_MAX_D = 128, STEP_MAX_H = 512;
+constexpr int SEG4 = 16;                  // 16-byte loads a thread issues before reducing
+constexpr int STEP_PART = 4096;           // LDS floats of the partial sums
 
-// y[r] = sum_c A[r][c] x[c] for r < R (a wave per row, lanes over columns)
-__device__ __forceinline__ void row_dots(const float* A, int R, int N, const float* x, float* y) {
-  for (int r = wave_id(); r < R; r += num_waves()) {
-    float s = 0.f;
-    for (int c = lane_id(); c < N; c += WAVE) s += A[(size_t)r * N + c] * x[c];
-    s = wave_sum(s);
-    if (lane_id() == 0) y[r] = s;
+// y[r] = sum_c A[r][c] x[c] for r < R.  Each row is cut into segments of up
+// to SEG4 float4; a thread loads a whole segment, then reduces it; the
+// segment sums meet in `part` (R * segments <= STEP_PART / 4 here).
+__device__ __forceinline__ void row_dots(const float* A, int R, int N, const float* x, float* y,
+                                         float* part) {
+  const int n4 = N / 4;
+  const int seg4 = n4 < SEG4 ? n4 : SEG4;
+  const int S = n4 / seg4;
+  const f4* A4 = reinterpret_cast<const f4*>(A);
+  const f4* x4 = reinterpret_cast<const f4*>(x);
+  for (int it = threadIdx.x; it < R * S; it += blockDim.x) {
+    const int r = it / S, sg = it - r * S;
+    const f4* row = A4 + (size_t)r * n4 + sg * seg4;
+    f4 buf[SEG4];
+#pragma unroll
+    for (int c = 0; c < SEG4; ++c)
+      if (c < seg4) buf[c] = row[c];
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < SEG4; ++c)
+      if (c < seg4) {
+        const f4 xv = x4[sg * seg4 + c];
+        acc += buf[c][0] * xv[0] + buf[c][1] * xv[1] + buf[c][2] * xv[2] + buf[c][3] * xv[3];
+      }
+    part[it] = acc;
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < R; r += blockDim.x) {
+    float acc = 0.f;
+    for (int sg = 0; sg < S; ++sg) acc += part[r * S + sg];
+    y[r] = acc;
   }
 }
 
-// y[c] = sum_r A[r][c] x[r] for c < N (a thread per column)
-__device__ __forceinline__ void col_dots(const float* A, int R, int N, const float* x, float* y) {
+// y[c] = sum_r A[r][c] x[r] for c < N.  A thread takes four columns (one
+// float4) over a run of up to SEG4 rows, loading the run first; the run sums
+// meet in `part` (N/4 * runs * 4 <= STEP_PART here).
+__device__ __forceinline__ void col_dots(const float* A, int R, int N, const float* x, float* y,
+                                         float* part) {
+  const int n4 = N / 4;
+  const int run = R < SEG4 ? R : SEG4;
+  const int nr = R / run;
+  const f4* A4 = reinterpret_cast<const f4*>(A);
+  f4* p4 = reinterpret_cast<f4*>(part);
+  for (int it = threadIdx.x; it < n4 * nr; it += blockDim.x) {
+    const int c4 = it % n4, rr = it / n4;
+    const int r0 = rr * run;
+    f4 buf[SEG4];
+#pragma unroll
+    for (int i = 0; i < SEG4; ++i)
+      if (i < run) buf[i] = A4[(size_t)(r0 + i) * n4 + c4];
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < SEG4; ++i)
+      if (i < run) acc += buf[i] * x[r0 + i];
+    p4[it] = acc;
+  }
+  __syncthreads();
   for (int c = threadIdx.x; c < N; c += blockDim.x) {
-    float s = 0.f;
-    for (int r = 0; r < R; ++r) s += A[(size_t)r * N + c] * x[r];
-    y[c] = s;
+    const int c4 = c >> 2, e = c & 3;
+    float acc = 0.f;
+    for (int rr = 0; rr < nr; ++rr) acc += part[(size_t)(rr * n4 + c4) * 4 + e];
+    y[c] = acc;
   }
 }
 
 // f(W, x) = W2 s(W1 x) added into acc[d]; z, a: hid-sized LDS vectors
 template <int ACT>
 __device__ void retrieve_add(const float* W1, const float* W2, int d, int hid, const float* x,
-                             float* z, float* a, float* y, float* acc) {
-  row_dots(W1, hid, d, x, z);
+                             float* z, float* a, float* y, float* acc, float* part) {
+  row_dots(W1, hid, d, x, z, part);
   __syncthreads();
   for (int j = threadIdx.x; j < hid; j += blockDim.x) a[j] = act_f<ACT>(z[j]);
   __syncthreads();
-  row_dots(W2, d, hid, a, y);
+  row_dots(W2, d, hid, a, y, part);
   __syncthreads();
   for (int i = threadIdx.x; i < d; i += blockDim.x) acc[i] += y[i];
   __syncthreads();
@@ -65,9 +114,10 @@ __device__ void retrieve_add(const float* W1, const float* W2, int d, int hid, c
 
 template <typename IO, int ACT>
 __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
-  __shared__ float sq[STEP_MAX_D], sk[STEP_MAX_D], sv[STEP_MAX_D], sx[STEP_MAX_D],
+  __shared__ __align__(16) float sq[STEP_MAX_D], sk[STEP_MAX_D], sv[STEP_MAX_D], sx[STEP_MAX_D],
       sy[STEP_MAX_D], sr[STEP_MAX_D], so[STEP_MAX_D];
-  __shared__ float sz[STEP_MAX_H], sa[STEP_MAX_H], sp[STEP_MAX_H], sg[STEP_MAX_H];
+  __shared__ __align__(16) float sz[STEP_MAX_H], sa[STEP_MAX_H], sp[STEP_MAX_H], sg[STEP_MAX_H];
+  __shared__ __align__(16) float part[STEP_PART];
   __shared__ float red[STEP_THREADS / WAVE];
   const int chain = blockIdx.x;
   const int B = a.B, H = a.H, T = a.T, d = a.d, hid = a.hid;
@@ -124,11 +174,11 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
       __syncthreads();
 
       // global retrieval at the chunk-entry state
-      if (global) retrieve_add<ACT>(Wh1, Wh2, d, hid, sq, sz, sa, sy, so);
+      if (global) retrieve_add<ACT>(Wh1, Wh2, d, hid, sq, sz, sa, sy, so, part);
 
       // inner gradient at the chunk-entry weights:
       // z = W^1 k, r = (2/d)(W^2 s(z) - v), delta = (W^2^T r) * s'(z)
-      row_dots(Wh1, hid, d, sk, sz);
+      row_dots(Wh1, hid, d, sk, sz, part);
       __syncthreads();
       for (int j = threadIdx.x; j < hid; j += blockDim.x) {
         const ActVals av = act_all<ACT>(sz[j]);
@@ -136,26 +186,52 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
         sp[j] = av.d1;
       }
       __syncthreads();
-      row_dots(Wh2, d, hid, sa, sy);
+      row_dots(Wh2, d, hid, sa, sy, part);
       __syncthreads();
       for (int i = threadIdx.x; i < d; i += blockDim.x) sr[i] = rs * (sy[i] - sv[i]);
       __syncthreads();
-      col_dots(Wh2, d, hid, sr, sg);
+      col_dots(Wh2, d, hid, sr, sg, part);
       __syncthreads();
       for (int j = threadIdx.x; j < hid; j += blockDim.x) sg[j] *= sp[j];
       __syncthreads();
 
       // gated update: u1 = delta k^T (hid x d), u2 = r s(z)^T (d x hid)
+      // (16-byte accesses, UNR of them per array in flight per thread)
       const float keep = 1.0f - alpha;
-      for (size_t e = threadIdx.x; e < hd; e += blockDim.x) {
-        const int j1 = (int)(e / d), l1 = (int)(e - (size_t)j1 * d);
-        const float s1 = beta * S1[e] - eta * sg[j1] * sk[l1];
-        S1[e] = s1;
-        W1[e] = keep * W1[e] + s1;
-        const int i2 = (int)(e / hid), j2 = (int)(e - (size_t)i2 * hid);
-        const float s2 = beta * S2[e] - eta * sr[i2] * sa[j2];
-        S2[e] = s2;
-        W2[e] = keep * W2[e] + s2;
+      {
+        constexpr int UNR = 4;
+        const int hd4 = (int)(hd / 4);
+        f4 *S14 = reinterpret_cast<f4*>(S1), *W14 = reinterpret_cast<f4*>(W1),
+           *S24 = reinterpret_cast<f4*>(S2), *W24 = reinterpret_cast<f4*>(W2);
+        const f4* k4 = reinterpret_cast<const f4*>(sk);
+        const f4* a4 = reinterpret_cast<const f4*>(sa);
+        for (int e0 = threadIdx.x; e0 < hd4; e0 += UNR * blockDim.x) {
+          f4 s1[UNR], w1[UNR], s2[UNR], w2[UNR];
+#pragma unroll
+          for (int u = 0; u < UNR; ++u) {
+            const int e = e0 + u * blockDim.x;
+            if (e < hd4) {
+              s1[u] = S14[e];
+              w1[u] = W14[e];
+              s2[u] = S24[e];
+              w2[u] = W24[e];
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < UNR; ++u) {
+            const int e = e0 + u * blockDim.x;
+            if (e < hd4) {
+              const int j1 = (4 * e) / d, l4 = (4 * e - j1 * d) / 4;   // W1, S1: [hid][d]
+              const int i2 = (4 * e) / hid, j4 = (4 * e - i2 * hid) / 4;  // W2, S2: [d][hid]
+              const f4 n1 = beta * s1[u] - (eta * sg[j1]) * k4[l4];
+              const f4 n2 = beta * s2[u] - (eta * sr[i2]) * a4[j4];
+              S14[e] = n1;
+              W14[e] = keep * w1[u] + n1;
+              S24[e] = n2;
+              W24[e] = keep * w2[u] + n2;
+            }
+          }
+        }
       }
       if (!global) {
         for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
@@ -168,11 +244,11 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
       if (!global) {  // local retrieval at W_t, queried at M_t q_t (or q_t)
         const float* xq = sq;
         if (a.qk_proj) {
-          row_dots(Mq, d, d, sq, sx);
+          row_dots(Mq, d, d, sq, sx, part);
           __syncthreads();
           xq = sx;
         }
-        retrieve_add<ACT>(W1, W2, d, hid, xq, sz, sa, sy, so);
+        retrieve_add<ACT>(W1, W2, d, hid, xq, sz, sa, sy, so, part);
       }
     }
     for (int i = threadIdx.x; i < d; i += blockDim.x) o[(size_t)t * d + i] = from_f<IO>(so[i]);
