@@ -359,11 +359,19 @@ def main():
     tnt.tnt_timing_read()
     tnt.tnt_timing_enable(True)
     torch.cuda.synchronize()
+    # per-step events on the caller's stream (the helper stream forks from and
+    # joins back into it inside every call, so they bracket the whole step)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    median_ms = per_step[len(per_step) // 2] if len(per_step) % 2 else \
+        0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
     tnt.tnt_timing_enable(False)
     kt = tnt.tnt_timing_read()
     assert torch.isfinite(o.float()).all() and torch.isfinite(g["dq"].float()).all()
@@ -419,6 +427,7 @@ def main():
     res = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "median_ms_per_step": median_ms, "min_ms_per_step": per_step[0],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if bf else "f32", "data": "synthetic (seeded Gaussian, unit q/k)",
         "config": {"workload": cfg.name, "global_batch": cfg.B, "seq_len": cfg.L,
