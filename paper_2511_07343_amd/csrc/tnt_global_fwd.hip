@@ -68,8 +68,7 @@ __global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a
   for (int i = i0; i < i1; ++i) {
     pa += log_keep(dec[i]);
     pb += log_mom(mom[i]);
-    tk[(size_t)i * TKS + 2] = pa;
-    tk[(size_t)i * TKS + 3] = pb;
+    *reinterpret_cast<float2*>(tk + (size_t)i * TKS + 2) = make_float2(pa, pb);
   }
   // segment affine map s_{i0} = P s_{i1} + Q (own writes are visible to the thread)
   float P = 1.f, Q = 0.f;
@@ -110,10 +109,8 @@ __global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a
     const float mi = (i + 1 < C) ? mom[i + 1] : 0.f;
     sv = ai + mi * sv;
     const float ebt = expf(lbC - tk[(size_t)i * TKS + 3]);
-    tk[(size_t)i * TKS + 0] = lr[i] * sv;
-    tk[(size_t)i * TKS + 1] = lr[i] * ebt;
-    tk[(size_t)i * TKS + 4] = sv;
-    tk[(size_t)i * TKS + 5] = ebt;
+    *reinterpret_cast<float2*>(tk + (size_t)i * TKS + 0) = make_float2(lr[i] * sv, lr[i] * ebt);
+    *reinterpret_cast<float2*>(tk + (size_t)i * TKS + 4) = make_float2(sv, ebt);
   }
   if (t == 0) {
     float* cc = a.chunkc + ((size_t)chain * (L / C) + n) * 4;
@@ -396,10 +393,11 @@ hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {
 // ---------------------------------------------------------------------------
 // o = sum of the per-memory fp32 partials, written in the I/O dtype
 // ---------------------------------------------------------------------------
-template <typename IO>
-__global__ void sum_out_kernel(SumJobs jobs, int njobs, int nparts, size_t stride, size_t n) {
-  // fixed-order sum of `nparts` fp32 partials, 8 elements per thread (two 16-byte
-  // loads per partial, one store), jobs along blockIdx.y
+template <typename IO, int NP>
+__global__ void sum_out_kernel(SumJobs jobs, int njobs, size_t stride, size_t n) {
+  // fixed-order sum of NP fp32 partials, 8 elements per thread (two 16-byte
+  // loads per partial, all issued before the sum, one store), jobs along
+  // blockIdx.y
   const int y = blockIdx.y;
   if (y >= njobs) return;
   const float* parts = jobs.parts[y];
@@ -407,45 +405,62 @@ __global__ void sum_out_kernel(SumJobs jobs, int njobs, int nparts, size_t strid
   const size_t n8 = n / 8;
   for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < n8;
        v += (size_t)gridDim.x * blockDim.x) {
-    float sacc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int p = 0; p < nparts; ++p) {
-      const float* q = parts + p * stride + v * 8;
-      const f32x4 x0 = *reinterpret_cast<const f32x4*>(q), x1 = *reinterpret_cast<const f32x4*>(q + 4);
+    f32x4 x0[NP], x1[NP];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        sacc[t] += x0[t];
-        sacc[t + 4] += x1[t];
-      }
+    for (int p = 0; p < NP; ++p) {
+      const float* q = parts + p * stride + v * 8;
+      x0[p] = *reinterpret_cast<const f32x4*>(q);
+      x1[p] = *reinterpret_cast<const f32x4*>(q + 4);
+    }
+    f32x4 s0 = x0[0], s1 = x1[0];
+#pragma unroll
+    for (int p = 1; p < NP; ++p) {
+      s0 += x0[p];
+      s1 += x1[p];
     }
     if constexpr (sizeof(IO) == 2) {
       bf16x8 o;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) o[t] = (__bf16)sacc[t];
+      for (int t = 0; t < 4; ++t) {
+        o[t] = (__bf16)s0[t];
+        o[t + 4] = (__bf16)s1[t];
+      }
       *reinterpret_cast<bf16x8*>(out + v * 8) = o;
     } else {
-      *reinterpret_cast<f32x4*>(out + v * 8) = f32x4{sacc[0], sacc[1], sacc[2], sacc[3]};
-      *reinterpret_cast<f32x4*>(out + v * 8 + 4) = f32x4{sacc[4], sacc[5], sacc[6], sacc[7]};
+      *reinterpret_cast<f32x4*>(out + v * 8) = s0;
+      *reinterpret_cast<f32x4*>(out + v * 8 + 4) = s1;
     }
   }
   // tail (n not a multiple of 8)
   for (size_t e = n8 * 8 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
        e += (size_t)gridDim.x * blockDim.x) {
     float sacc = 0.f;
-    for (int p = 0; p < nparts; ++p) sacc += parts[p * stride + e];
+    for (int p = 0; p < NP; ++p) sacc += parts[p * stride + e];
     out[e] = from_f<IO>(sacc);
   }
 }
 
+template <typename IO>
+static hipError_t sum_outs_io(const SumJobs& jobs, int njobs, int nparts, size_t stride, size_t n,
+                              hipStream_t st) {
+  // one 8-element vector per thread where the grid allows it
+  const int blocks = (int)std::max<size_t>(1, std::min<size_t>((n / 8 + 255) / 256, 65535));
+  const dim3 g(blocks, njobs), b(256);
+  switch (nparts) {
+    case 1: hipLaunchKernelGGL((sum_out_kernel<IO, 1>), g, b, 0, st, jobs, njobs, stride, n); break;
+    case 2: hipLaunchKernelGGL((sum_out_kernel<IO, 2>), g, b, 0, st, jobs, njobs, stride, n); break;
+    case 3: hipLaunchKernelGGL((sum_out_kernel<IO, 3>), g, b, 0, st, jobs, njobs, stride, n); break;
+    case 4: hipLaunchKernelGGL((sum_out_kernel<IO, 4>), g, b, 0, st, jobs, njobs, stride, n); break;
+    case 5: hipLaunchKernelGGL((sum_out_kernel<IO, 5>), g, b, 0, st, jobs, njobs, stride, n); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_sum_outs(const SumJobs& jobs, int njobs, int nparts, size_t stride, size_t n,
                            int bf16, hipStream_t st) {
-  const int blocks = (int)std::max<size_t>(1, std::min<size_t>((n / 8 + 255) / 256, 4096));
-  if (bf16)
-    hipLaunchKernelGGL(sum_out_kernel<__bf16>, dim3(blocks, njobs), dim3(256), 0, st, jobs, njobs,
-                       nparts, stride, n);
-  else
-    hipLaunchKernelGGL(sum_out_kernel<float>, dim3(blocks, njobs), dim3(256), 0, st, jobs, njobs,
-                       nparts, stride, n);
-  return hipGetLastError();
+  return bf16 ? sum_outs_io<__bf16>(jobs, njobs, nparts, stride, n, st)
+              : sum_outs_io<float>(jobs, njobs, nparts, stride, n, st);
 }
 
 hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
