@@ -187,7 +187,8 @@ const char* tnt_strerror(tnt_status status);
 int32_t tnt_abi_version(void);
 
 /* Opt-in kernel timing, for benchmarks.  While enabled (on != 0), every
- * kernel launch of tnt_mem_fwd / tnt_mem_bwd is bracketed by a pair of
+ * kernel launch of tnt_mem_fwd / tnt_mem_bwd / tnt_mem_step (and the
+ * state-carry section of each global chunk step) is bracketed by a pair of
  * hipEvents recorded on the launch stream (at most 65536 launches are kept).
  * tnt_timing_read synchronises on the recorded events, writes one entry per
  * kernel name (names: 32-byte NUL-terminated slots; total_ms: summed event
