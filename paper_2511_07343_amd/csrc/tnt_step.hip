@@ -30,38 +30,83 @@ constexpr int STEP_MAX_D = 128, STEP_MAX_H = 512;
 constexpr int SEG4 = 16;                  // 16-byte loads a thread issues before reducing
 constexpr int STEP_PART = 4096;           // LDS floats of the partial sums
 
-// y[r] = sum_c A[r][c] x[c] for r < R.  Each row is cut into segments of up
-// to SEG4 float4; a thread loads a whole segment, then reduces it; the
-// segment sums meet in `part` (R * segments <= STEP_PART / 4 here).
-__device__ __forceinline__ void row_dots(const float* A, int R, int N, const float* x, float* y,
-                                         float* part) {
-  const int n4 = N / 4;
-  const int seg4 = n4 < SEG4 ? n4 : SEG4;
-  const int S = n4 / seg4;
-  const f4* A4 = reinterpret_cast<const f4*>(A);
-  const f4* x4 = reinterpret_cast<const f4*>(x);
-  for (int it = threadIdx.x; it < R * S; it += blockDim.x) {
-    const int r = it / S, sg = it - r * S;
-    const f4* row = A4 + (size_t)r * n4 + sg * seg4;
+// One row-dot job: y[r] = A[r] . x (and y2[r] = A[r] . x2 when x2 is set) for r < R.
+struct RowJob {
+  const float* A;
+  int R, N;
+  const float *x, *x2;
+  float *y, *y2;
+};
+
+// Runs up to two jobs in one pass.  Each row is cut into segments of up to
+// SEG4 float4; a thread loads a whole segment, then forms its dots with the
+// job's vectors; the segment sums meet in `part` (at most STEP_PART floats:
+// R * segments * vectors summed over the jobs).
+__device__ __forceinline__ void row_dots_2(const RowJob j0, const RowJob j1, float* part) {
+  const int s0 = (j0.N / 4) < SEG4 ? 1 : (j0.N / 4) / SEG4;
+  const int s1 = (j1.N / 4) < SEG4 ? 1 : (j1.N / 4) / SEG4;
+  const int n0 = j0.R * s0, n1 = j1.R * s1;
+  const int v0 = j0.x2 ? 2 : 1;
+  float* part1 = part + v0 * n0;
+  for (int it = threadIdx.x; it < n0 + n1; it += blockDim.x) {
+    const bool first = it < n0;
+    // the job's fields picked by value (a reference would put the jobs in scratch)
+    const float* jA = first ? j0.A : j1.A;
+    const float* jx = first ? j0.x : j1.x;
+    const float* jx2 = first ? j0.x2 : j1.x2;
+    const int jN = first ? j0.N : j1.N;
+    const int S = first ? s0 : s1, ii = first ? it : it - n0;
+    const int n4 = jN / 4, seg4 = n4 < SEG4 ? n4 : SEG4;
+    const int r = ii / S, sg = ii - r * S;
+    const f4* row = reinterpret_cast<const f4*>(jA) + (size_t)r * n4 + sg * seg4;
     f4 buf[SEG4];
 #pragma unroll
     for (int c = 0; c < SEG4; ++c)
       if (c < seg4) buf[c] = row[c];
+    const f4* x4 = reinterpret_cast<const f4*>(jx) + sg * seg4;
     float acc = 0.f;
 #pragma unroll
     for (int c = 0; c < SEG4; ++c)
       if (c < seg4) {
-        const f4 xv = x4[sg * seg4 + c];
+        const f4 xv = x4[c];
         acc += buf[c][0] * xv[0] + buf[c][1] * xv[1] + buf[c][2] * xv[2] + buf[c][3] * xv[3];
       }
-    part[it] = acc;
+    (first ? part : part1)[ii] = acc;
+    if (jx2) {
+      const f4* y4 = reinterpret_cast<const f4*>(jx2) + sg * seg4;
+      float acc2 = 0.f;
+#pragma unroll
+      for (int c = 0; c < SEG4; ++c)
+        if (c < seg4) {
+          const f4 xv = y4[c];
+          acc2 += buf[c][0] * xv[0] + buf[c][1] * xv[1] + buf[c][2] * xv[2] + buf[c][3] * xv[3];
+        }
+      (first ? part + n0 : part1 + n1)[ii] = acc2;
+    }
   }
   __syncthreads();
-  for (int r = threadIdx.x; r < R; r += blockDim.x) {
+  for (int r = threadIdx.x; r < j0.R + j1.R; r += blockDim.x) {
+    const bool first = r < j0.R;
+    float* jy = first ? j0.y : j1.y;
+    float* jy2 = first ? j0.y2 : j1.y2;
+    const bool two = first ? j0.x2 != nullptr : j1.x2 != nullptr;
+    const int S = first ? s0 : s1, rr = first ? r : r - j0.R, n = first ? n0 : n1;
+    const float* pp = first ? part : part1;
     float acc = 0.f;
-    for (int sg = 0; sg < S; ++sg) acc += part[r * S + sg];
-    y[r] = acc;
+    for (int sg = 0; sg < S; ++sg) acc += pp[rr * S + sg];
+    jy[rr] = acc;
+    if (two) {
+      float acc2 = 0.f;
+      for (int sg = 0; sg < S; ++sg) acc2 += pp[n + rr * S + sg];
+      jy2[rr] = acc2;
+    }
   }
+}
+
+__device__ __forceinline__ void row_dots(const float* A, int R, int N, const float* x, float* y,
+                                         float* part) {
+  const RowJob j0{A, R, N, x, nullptr, y, nullptr}, none{A, 0, N, x, nullptr, y, nullptr};
+  row_dots_2(j0, none, part);
 }
 
 // y[c] = sum_r A[r][c] x[r] for c < N.  A thread takes four columns (one
@@ -96,27 +141,15 @@ __device__ __forceinline__ void col_dots(const float* A, int R, int N, const flo
   }
 }
 
-// f(W, x) = W2 s(W1 x) added into acc[d]; z, a: hid-sized LDS vectors
-template <int ACT>
-__device__ void retrieve_add(const float* W1, const float* W2, int d, int hid, const float* x,
-                             float* z, float* a, float* y, float* acc, float* part) {
-  row_dots(W1, hid, d, x, z, part);
-  __syncthreads();
-  for (int j = threadIdx.x; j < hid; j += blockDim.x) a[j] = act_f<ACT>(z[j]);
-  __syncthreads();
-  row_dots(W2, d, hid, a, y, part);
-  __syncthreads();
-  for (int i = threadIdx.x; i < d; i += blockDim.x) acc[i] += y[i];
-  __syncthreads();
-}
-
 }  // namespace
 
 template <typename IO, int ACT>
 __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
   __shared__ __align__(16) float sq[STEP_MAX_D], sk[STEP_MAX_D], sv[STEP_MAX_D], sx[STEP_MAX_D],
       sy[STEP_MAX_D], sr[STEP_MAX_D], so[STEP_MAX_D];
-  __shared__ __align__(16) float sz[STEP_MAX_H], sa[STEP_MAX_H], sp[STEP_MAX_H], sg[STEP_MAX_H];
+  __shared__ __align__(16) float sz[STEP_MAX_H], sa[STEP_MAX_H], sp[STEP_MAX_H], sg[STEP_MAX_H],
+      szq[STEP_MAX_H], saq[STEP_MAX_H];
+  __shared__ __align__(16) float syq[STEP_MAX_D];
   __shared__ __align__(16) float part[STEP_PART];
   __shared__ float red[STEP_THREADS / WAVE];
   const int chain = blockIdx.x;
@@ -138,9 +171,13 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
       so[i] = 0.f;
     }
     __syncthreads();
-    float kk = 0.f;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) kk += sk[i] * sk[i];
+    float kk = 0.f, kq = 0.f;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+      kk += sk[i] * sk[i];
+      kq += sk[i] * sq[i];
+    }
     kk = block_sum(kk, red);
+    kq = block_sum(kq, red);
     const float ikk = kk > 0.f ? 1.0f / kk : 0.f;
 
     for (int m = 0; m < a.M; ++m) {
@@ -173,38 +210,55 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
       }
       __syncthreads();
 
-      // global retrieval at the chunk-entry state
-      if (global) retrieve_add<ACT>(Wh1, Wh2, d, hid, sq, sz, sa, sy, so, part);
-
-      // inner gradient at the chunk-entry weights:
-      // z = W^1 k, r = (2/d)(W^2 s(z) - v), delta = (W^2^T r) * s'(z)
-      row_dots(Wh1, hid, d, sk, sz, part);
+      // phase 1: z = W^1 k, and in the same pass the global retrieval's W^1 q
+      // or a local memory's M_{t-1} q
+      const bool proj = !global && a.qk_proj;
+      {
+        const RowJob g1{Wh1, hid, d, sk, global ? sq : nullptr, sz, global ? szq : nullptr};
+        const RowJob g2{Mq, proj ? d : 0, d, sq, nullptr, sx, nullptr};
+        row_dots_2(g1, g2, part);
+      }
       __syncthreads();
       for (int j = threadIdx.x; j < hid; j += blockDim.x) {
         const ActVals av = act_all<ACT>(sz[j]);
         sa[j] = av.s;
         sp[j] = av.d1;
+        if (global) saq[j] = act_f<ACT>(szq[j]);
       }
       __syncthreads();
-      row_dots(Wh2, d, hid, sa, sy, part);
+      // phase 2: y = W^2 s(z) (and the global retrieval W^2 s(W^1 q))
+      {
+        const RowJob g1{Wh2, d, hid, sa, global ? saq : nullptr, sy, global ? syq : nullptr};
+        const RowJob none{Wh2, 0, hid, sa, nullptr, sy, nullptr};
+        row_dots_2(g1, none, part);
+      }
       __syncthreads();
-      for (int i = threadIdx.x; i < d; i += blockDim.x) sr[i] = rs * (sy[i] - sv[i]);
+      for (int i = threadIdx.x; i < d; i += blockDim.x) {
+        sr[i] = rs * (sy[i] - sv[i]);
+        if (global) so[i] += syq[i];
+        // local query x = M_t q = M_{t-1} q + k (k . q) / ||k||^2, or q
+        if (!global) sx[i] = proj ? sx[i] + sk[i] * (kq * ikk) : sq[i];
+      }
       __syncthreads();
+      // phase 3: delta = (W^2^T r) * s'(z)
       col_dots(Wh2, d, hid, sr, sg, part);
       __syncthreads();
       for (int j = threadIdx.x; j < hid; j += blockDim.x) sg[j] *= sp[j];
       __syncthreads();
 
-      // gated update: u1 = delta k^T (hid x d), u2 = r s(z)^T (d x hid)
-      // (16-byte accesses, UNR of them per array in flight per thread)
+      // phase 4: gated update, u1 = delta k^T (hid x d), u2 = r s(z)^T (d x hid),
+      // 16-byte accesses, UNR per array in flight per thread.  A local memory
+      // also forms z'[j] = W1_t[j] . x here: the d/4 lanes holding one row of
+      // W1 are adjacent within a wave and sum by shuffles (fixed order).
       const float keep = 1.0f - alpha;
       {
         constexpr int UNR = 4;
-        const int hd4 = (int)(hd / 4);
+        const int hd4 = (int)(hd / 4), g4 = d / 4;
         f4 *S14 = reinterpret_cast<f4*>(S1), *W14 = reinterpret_cast<f4*>(W1),
            *S24 = reinterpret_cast<f4*>(S2), *W24 = reinterpret_cast<f4*>(W2);
         const f4* k4 = reinterpret_cast<const f4*>(sk);
         const f4* a4 = reinterpret_cast<const f4*>(sa);
+        const f4* x4 = reinterpret_cast<const f4*>(sx);
         for (int e0 = threadIdx.x; e0 < hd4; e0 += UNR * blockDim.x) {
           f4 s1[UNR], w1[UNR], s2[UNR], w2[UNR];
 #pragma unroll
@@ -220,15 +274,22 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
 #pragma unroll
           for (int u = 0; u < UNR; ++u) {
             const int e = e0 + u * blockDim.x;
-            if (e < hd4) {
-              const int j1 = (4 * e) / d, l4 = (4 * e - j1 * d) / 4;   // W1, S1: [hid][d]
+            if (e < hd4) {  // hd4 is a multiple of 64: whole waves take this branch
+              const int j1 = e / g4, l4 = e - j1 * g4;                   // W1, S1: [hid][d]
               const int i2 = (4 * e) / hid, j4 = (4 * e - i2 * hid) / 4;  // W2, S2: [d][hid]
               const f4 n1 = beta * s1[u] - (eta * sg[j1]) * k4[l4];
               const f4 n2 = beta * s2[u] - (eta * sr[i2]) * a4[j4];
+              const f4 nw1 = keep * w1[u] + n1;
               S14[e] = n1;
-              W14[e] = keep * w1[u] + n1;
+              W14[e] = nw1;
               S24[e] = n2;
               W24[e] = keep * w2[u] + n2;
+              if (!global) {
+                const f4 xv = x4[l4];
+                float zp = nw1[0] * xv[0] + nw1[1] * xv[1] + nw1[2] * xv[2] + nw1[3] * xv[3];
+                for (int o_ = 1; o_ < g4; o_ <<= 1) zp += __shfl_xor(zp, o_, WAVE);
+                if (l4 == 0) sz[j1] = zp;
+              }
             }
           }
         }
@@ -241,14 +302,13 @@ __global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
       }
       __syncthreads();
 
-      if (!global) {  // local retrieval at W_t, queried at M_t q_t (or q_t)
-        const float* xq = sq;
-        if (a.qk_proj) {
-          row_dots(Mq, d, d, sq, sx, part);
-          __syncthreads();
-          xq = sx;
-        }
-        retrieve_add<ACT>(W1, W2, d, hid, xq, sz, sa, sy, so, part);
+      if (!global) {  // local retrieval at W_t: o += W2_t s(z')
+        for (int j = threadIdx.x; j < hid; j += blockDim.x) sa[j] = act_f<ACT>(sz[j]);
+        __syncthreads();
+        row_dots(W2, d, hid, sa, sy, part);
+        __syncthreads();
+        for (int i = threadIdx.x; i < d; i += blockDim.x) so[i] += sy[i];
+        __syncthreads();
       }
     }
     for (int i = threadIdx.x; i < d; i += blockDim.x) o[(size_t)t * d + i] = from_f<IO>(so[i]);
