@@ -157,8 +157,12 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
  * the caller: per memory m and per (batch row, head) chain, fp32
  *     W^1 [hid][d], W^2 [d][hid], W1 [hid][d], W2 [d][hid], S1 [hid][d],
  *     S2 [d][hid], M [d][d]       (M unused for the global memory),
- * blocks ordered [M][B][H].  Calls on one state must be serialised (same
- * stream); the work is one workgroup per chain, latency- and HBM-bound. */
+ * blocks ordered [M][B][H], followed by a scratch area of M*B*H blocks of
+ * 2*hid + d + 3*G*d floats (G = hid / min(64, hid)), each rounded up to a
+ * multiple of 64 floats, whose contents are undefined between calls.  Calls
+ * on one state must be serialised (same stream).  Each token takes three
+ * launches over (hidden-unit slice, chain, memory) workgroups; the work is
+ * matrix-vector products and rank-one updates of the fp32 state. */
 
 /* Bytes of the carried state (0 if the config is invalid). */
 size_t tnt_mem_state_size(const tnt_config* cfg);

@@ -630,7 +630,9 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
 size_t tnt_mem_state_size(const tnt_config* cfg) {
   if (validate(cfg, false) != TNT_OK) return 0;
   const size_t M = (size_t)cfg->has_global + cfg->n_local;
-  return M * cfg->B * cfg->H * step_state_floats(cfg->d, cfg->hid) * sizeof(float);
+  return M * cfg->B * cfg->H *
+         (step_state_floats(cfg->d, cfg->hid) + step_scratch_floats(cfg->d, cfg->hid)) *
+         sizeof(float);
 }
 
 }  // extern "C"
@@ -647,6 +649,9 @@ StepArgs step_args(const tnt_config* c) {
   if (c->has_global) { a.C[m] = c->C_G; a.S[m] = 0; ++m; }
   for (int i = 0; i < c->n_local; ++i, ++m) { a.C[m] = c->C_L[i]; a.S[m] = c->S_L[i]; }
   a.mem_stride = step_state_floats(c->d, c->hid);
+  a.HS = c->hid < 64 ? c->hid : 64;
+  a.G = c->hid / a.HS;
+  a.sc_stride = step_scratch_floats(c->d, c->hid);
   return a;
 }
 }  // namespace
@@ -683,6 +688,7 @@ tnt_status tnt_mem_step(const tnt_config* cfg, int64_t pos, int32_t T, const voi
   a.T = T; a.pos = pos;
   a.q = q; a.k = k; a.v = v; a.lr = lr; a.mom = mom; a.decay = decay;
   a.W1i = W1_init; a.W2i = W2_init; a.state = (float*)state; a.o = o;
+  a.scratch = a.state + (size_t)a.M * a.B * a.H * a.mem_stride;
   hipStream_t st = (hipStream_t)stream;
   hipError_t e = timed("step", st, [&]() { return launch_step(a, st); });
   return e == hipSuccess ? TNT_OK : TNT_ERR_HIP;

@@ -175,8 +175,14 @@ struct StepArgs {
   float* state;
   void* o;                                    // [B][H][T][d]
   size_t mem_stride;
+  // per-token launches: hidden units split into G slices of HS; the scratch
+  // area (after every state block) holds sc_stride floats per (memory, chain)
+  int G, HS, t;
+  float* scratch;
+  size_t sc_stride;
 };
 size_t step_state_floats(int d, int hid);
+size_t step_scratch_floats(int d, int hid);
 hipError_t launch_step_init(const StepArgs& a, hipStream_t st);
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);

@@ -13,11 +13,21 @@
 // k_t k_t^T / ||k_t||^2 to its Q-K sum M and reads at W_t after the update,
 // o_i = f(W_t, M q_t) (Sec. 4.1.1 local update, Sec. 4.1.2; App. C).
 //
-// One workgroup per (batch row, head) chain walks the step's tokens and the
-// layer's memories in order.  The work per token is a handful of matrix-vector
-// products and rank-one updates of the fp32 state (HBM-bound), done with
-// coalesced wave-per-row dot products, thread-per-column dot products and
-// elementwise passes; there is no contraction long enough for MFMA tiles.
+// The state of every (memory, chain) is split by hidden unit into G slices of
+// HS = min(64, hid): slice g owns rows [g HS, (g+1) HS) of W^1, W1, S1 and the
+// same columns of W^2, W2, S2, and one workgroup per (slice, chain, memory)
+// touches nothing else of the state.  Each token takes three launches:
+//   K1: chunk / shard boundary of the slice; z = W^1 k (and the global
+//       retrieval's W^1 q) for the slice's rows; s(z), s'(z) to scratch; the
+//       slice's share of W^2 s(z) (and W^2 s(W^1 q)); a local memory's query
+//       x = M_t q (slice 0);
+//   K2: r = (2/d)(sum of the shares - v); the slice's delta = (W^2^T r) s'(z);
+//       the gated update of the slice; a local memory's W1_t x on the fresh
+//       rows and its share of W2_t s(W1_t x); M += k k^T / ||k||^2 (slice 0);
+//   K3: o = sum of the retrieval shares (global memory first, fixed order).
+// The work is matrix-vector products and rank-one updates of the fp32 state
+// (HBM-bound), with 16-byte loads issued in batches; there is no contraction
+// long enough for MFMA tiles.
 #include "tnt_device.h"
 #include "tnt_kernels.h"
 
@@ -25,7 +35,7 @@ namespace tnt {
 
 namespace {
 
-constexpr int STEP_THREADS = 512;
+constexpr int STEP_THREADS = 256;
 constexpr int STEP_MAX_D = 128, STEP_MAX_H = 512;
 constexpr int SEG4 = 16;                  // 16-byte loads a thread issues before reducing
 constexpr int STEP_PART = 4096;           // LDS floats of the partial sums
@@ -33,7 +43,7 @@ constexpr int STEP_PART = 4096;           // LDS floats of the partial sums
 // One row-dot job: y[r] = A[r] . x (and y2[r] = A[r] . x2 when x2 is set) for r < R.
 struct RowJob {
   const float* A;
-  int R, N;
+  int R, N, lda;  // rows, row length, row stride (floats)
   const float *x, *x2;
   float *y, *y2;
 };
@@ -54,11 +64,11 @@ __device__ __forceinline__ void row_dots_2(const RowJob j0, const RowJob j1, flo
     const float* jA = first ? j0.A : j1.A;
     const float* jx = first ? j0.x : j1.x;
     const float* jx2 = first ? j0.x2 : j1.x2;
-    const int jN = first ? j0.N : j1.N;
+    const int jN = first ? j0.N : j1.N, jld = first ? j0.lda : j1.lda;
     const int S = first ? s0 : s1, ii = first ? it : it - n0;
     const int n4 = jN / 4, seg4 = n4 < SEG4 ? n4 : SEG4;
     const int r = ii / S, sg = ii - r * S;
-    const f4* row = reinterpret_cast<const f4*>(jA) + (size_t)r * n4 + sg * seg4;
+    const f4* row = reinterpret_cast<const f4*>(jA + (size_t)r * jld) + sg * seg4;
     f4 buf[SEG4];
 #pragma unroll
     for (int c = 0; c < SEG4; ++c)
@@ -105,16 +115,16 @@ __device__ __forceinline__ void row_dots_2(const RowJob j0, const RowJob j1, flo
 
 __device__ __forceinline__ void row_dots(const float* A, int R, int N, const float* x, float* y,
                                          float* part) {
-  const RowJob j0{A, R, N, x, nullptr, y, nullptr}, none{A, 0, N, x, nullptr, y, nullptr};
+  const RowJob j0{A, R, N, N, x, nullptr, y, nullptr}, none{A, 0, N, N, x, nullptr, y, nullptr};
   row_dots_2(j0, none, part);
 }
 
 // y[c] = sum_r A[r][c] x[r] for c < N.  A thread takes four columns (one
 // float4) over a run of up to SEG4 rows, loading the run first; the run sums
 // meet in `part` (N/4 * runs * 4 <= STEP_PART here).
-__device__ __forceinline__ void col_dots(const float* A, int R, int N, const float* x, float* y,
-                                         float* part) {
-  const int n4 = N / 4;
+__device__ __forceinline__ void col_dots(const float* A, int R, int N, int lda, const float* x,
+                                         float* y, float* part) {
+  const int n4 = N / 4, ld4 = lda / 4;
   const int run = R < SEG4 ? R : SEG4;
   const int nr = R / run;
   const f4* A4 = reinterpret_cast<const f4*>(A);
@@ -125,7 +135,7 @@ __device__ __forceinline__ void col_dots(const float* A, int R, int N, const flo
     f4 buf[SEG4];
 #pragma unroll
     for (int i = 0; i < SEG4; ++i)
-      if (i < run) buf[i] = A4[(size_t)(r0 + i) * n4 + c4];
+      if (i < run) buf[i] = A4[(size_t)(r0 + i) * ld4 + c4];
     f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < SEG4; ++i)
@@ -143,176 +153,260 @@ __device__ __forceinline__ void col_dots(const float* A, int R, int N, const flo
 
 }  // namespace
 
+// scratch of one (memory, chain), floats: s(z) [hid], s'(z) [hid], x [d],
+// then per slice the shares W^2 s(z) [G][d], global W^2 s(W^1 q) [G][d] and
+// local W2_t s(W1_t x) [G][d]
+struct StepScr {
+  float *a, *sp, *x, *yp, *yq, *y2;
+};
+__device__ __forceinline__ StepScr step_scr(const StepArgs& a, int m, int chain) {
+  float* b = a.scratch + ((size_t)m * a.B * a.H + chain) * a.sc_stride;
+  StepScr s;
+  s.a = b;
+  s.sp = b + a.hid;
+  s.x = b + 2 * a.hid;
+  s.yp = s.x + a.d;
+  s.yq = s.yp + (size_t)a.G * a.d;
+  s.y2 = s.yq + (size_t)a.G * a.d;
+  return s;
+}
+
 template <typename IO, int ACT>
-__global__ void __launch_bounds__(STEP_THREADS) step_kernel(StepArgs a) {
-  __shared__ __align__(16) float sq[STEP_MAX_D], sk[STEP_MAX_D], sv[STEP_MAX_D], sx[STEP_MAX_D],
-      sy[STEP_MAX_D], sr[STEP_MAX_D], so[STEP_MAX_D];
-  __shared__ __align__(16) float sz[STEP_MAX_H], sa[STEP_MAX_H], sp[STEP_MAX_H], sg[STEP_MAX_H],
-      szq[STEP_MAX_H], saq[STEP_MAX_H];
-  __shared__ __align__(16) float syq[STEP_MAX_D];
+__global__ void __launch_bounds__(STEP_THREADS) step_k1(StepArgs a) {
+  __shared__ __align__(16) float sq[STEP_MAX_D], sk[STEP_MAX_D], sx[STEP_MAX_D], sy[STEP_MAX_D],
+      syq[STEP_MAX_D];
+  __shared__ __align__(16) float sz[64], sa[64], szq[64], saq[64];
   __shared__ __align__(16) float part[STEP_PART];
   __shared__ float red[STEP_THREADS / WAVE];
-  const int chain = blockIdx.x;
-  const int B = a.B, H = a.H, T = a.T, d = a.d, hid = a.hid;
-  const int b = chain / H, h = chain - b * H;
+  const int g = blockIdx.x, chain = blockIdx.y, m = blockIdx.z;
+  const int H = a.H, d = a.d, hid = a.hid, HS = a.HS, j0 = g * HS;
+  const int b = chain / H, h = chain - b * H, t = a.t;
+  const long long p = a.pos + t;
+  const bool global = a.has_global && m == 0;
   const size_t hd = (size_t)hid * d;
-  const IO* q = (const IO*)a.q + (size_t)chain * T * d;
-  const IO* k = (const IO*)a.k + (size_t)chain * T * d;
-  const IO* v = (const IO*)a.v + (size_t)chain * T * d;
-  IO* o = (IO*)a.o + (size_t)chain * T * d;
-  const float rs = 2.0f / (float)d;
+  float* base = a.state + ((size_t)m * a.B * H + chain) * a.mem_stride;
+  float *Wh1 = base, *Wh2 = base + hd, *W1 = base + 2 * hd, *W2 = base + 3 * hd,
+        *S1 = base + 4 * hd, *S2 = base + 5 * hd, *Mq = base + 6 * hd;
+  const StepScr sc = step_scr(a, m, chain);
+  const size_t tok = ((size_t)chain * a.T + t) * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    sq[i] = to_f(((const IO*)a.q)[tok + i]);
+    sk[i] = to_f(((const IO*)a.k)[tok + i]);
+  }
 
-  for (int t = 0; t < T; ++t) {
-    const long long p = a.pos + t;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) {
-      sq[i] = to_f(q[(size_t)t * d + i]);
-      sk[i] = to_f(k[(size_t)t * d + i]);
-      sv[i] = to_f(v[(size_t)t * d + i]);
-      so[i] = 0.f;
+  // chunk / shard boundary, restricted to the slice (and M on slice 0)
+  const bool reset = !global && p % a.S[m] == 0;
+  if (reset || p % a.C[m] == 0) {
+    const float* W1i = a.W1i + ((size_t)m * H + h) * hd;
+    const float* W2i = a.W2i + ((size_t)m * H + h) * hd;
+    for (int e = threadIdx.x; e < HS * d; e += blockDim.x) {  // rows of W^1, W1, S1
+      const size_t i1 = (size_t)j0 * d + e;
+      if (reset) {
+        Wh1[i1] = W1[i1] = W1i[i1];
+        S1[i1] = 0.f;
+      } else {
+        Wh1[i1] = W1[i1];
+      }
     }
-    __syncthreads();
-    float kk = 0.f, kq = 0.f;
+    for (int e = threadIdx.x; e < HS * d; e += blockDim.x) {  // columns of W^2, W2, S2
+      const int i = e / HS, jj = e - i * HS;
+      const size_t i2 = (size_t)i * hid + j0 + jj;
+      if (reset) {
+        Wh2[i2] = W2[i2] = W2i[i2];
+        S2[i2] = 0.f;
+      } else {
+        Wh2[i2] = W2[i2];
+      }
+    }
+    if (!global && g == 0 && (reset || a.qk_scope == 1))
+      for (int e = threadIdx.x; e < d * d; e += blockDim.x) Mq[e] = 0.f;
+  }
+  __syncthreads();
+
+  // z = W^1 k on the slice's rows (and the global retrieval's W^1 q); a local
+  // memory's M_{t-1} q on slice 0
+  const bool proj = !global && a.qk_proj && g == 0;
+  {
+    const RowJob r1{Wh1 + (size_t)j0 * d, HS, d, d, sk, global ? sq : nullptr, sz,
+                    global ? szq : nullptr};
+    const RowJob r2{Mq, proj ? d : 0, d, d, sq, nullptr, sx, nullptr};
+    row_dots_2(r1, r2, part);
+  }
+  __syncthreads();
+  for (int jj = threadIdx.x; jj < HS; jj += blockDim.x) {
+    const ActVals av = act_all<ACT>(sz[jj]);
+    sa[jj] = av.s;
+    sc.a[j0 + jj] = av.s;
+    sc.sp[j0 + jj] = av.d1;
+    if (global) saq[jj] = act_f<ACT>(szq[jj]);
+  }
+  __syncthreads();
+  // the slice's share of W^2 s(z) (and of W^2 s(W^1 q))
+  {
+    const RowJob r1{Wh2 + j0, d, HS, hid, sa, global ? saq : nullptr, sy, global ? syq : nullptr};
+    const RowJob none{Wh2, 0, HS, hid, sa, nullptr, sy, nullptr};
+    row_dots_2(r1, none, part);
+  }
+  float kk = 0.f, kq = 0.f;
+  if (!global && g == 0) {
     for (int i = threadIdx.x; i < d; i += blockDim.x) {
       kk += sk[i] * sk[i];
       kq += sk[i] * sq[i];
     }
-    kk = block_sum(kk, red);
-    kq = block_sum(kq, red);
-    const float ikk = kk > 0.f ? 1.0f / kk : 0.f;
+  }
+  kk = block_sum(kk, red);  // (barrier inside: the shares are complete)
+  kq = block_sum(kq, red);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    sc.yp[(size_t)g * d + i] = sy[i];
+    if (global) sc.yq[(size_t)g * d + i] = syq[i];
+    // local query x = M_t q = M_{t-1} q + k (k . q) / ||k||^2, or q
+    if (!global && g == 0) {
+      const float ikk = kk > 0.f ? 1.0f / kk : 0.f;
+      sc.x[i] = a.qk_proj ? sx[i] + sk[i] * (kq * ikk) : sq[i];
+    }
+  }
+}
 
-    for (int m = 0; m < a.M; ++m) {
-      const bool global = a.has_global && m == 0;
-      const int C = a.C[m];
-      float* base = a.state + ((size_t)m * B * H + chain) * a.mem_stride;
-      float *Wh1 = base, *Wh2 = base + hd, *W1 = base + 2 * hd, *W2 = base + 3 * hd,
-            *S1 = base + 4 * hd, *S2 = base + 5 * hd, *Mq = base + 6 * hd;
-      const size_t gi = (((size_t)m * B + b) * H + h) * T + t;
-      const float eta = a.lr[gi], beta = a.mom[gi], alpha = a.decay[gi];
+template <typename IO, int ACT>
+__global__ void __launch_bounds__(STEP_THREADS) step_k2(StepArgs a) {
+  __shared__ __align__(16) float sk[STEP_MAX_D], sr[STEP_MAX_D], sx[STEP_MAX_D], sy[STEP_MAX_D];
+  __shared__ __align__(16) float sa[64], sp[64], sg[64], sz[64];
+  __shared__ __align__(16) float part[STEP_PART];
+  __shared__ float red[STEP_THREADS / WAVE];
+  const int g = blockIdx.x, chain = blockIdx.y, m = blockIdx.z;
+  const int B = a.B, H = a.H, d = a.d, hid = a.hid, HS = a.HS, G = a.G, j0 = g * HS;
+  const int b = chain / H, h = chain - b * H, t = a.t;
+  const bool global = a.has_global && m == 0;
+  const size_t hd = (size_t)hid * d;
+  float* base = a.state + ((size_t)m * B * H + chain) * a.mem_stride;
+  float *Wh2 = base + hd, *W1 = base + 2 * hd, *W2 = base + 3 * hd, *S1 = base + 4 * hd,
+        *S2 = base + 5 * hd, *Mq = base + 6 * hd;
+  const StepScr sc = step_scr(a, m, chain);
+  const size_t tok = ((size_t)chain * a.T + t) * d;
+  const size_t gi = (((size_t)m * B + b) * H + h) * a.T + t;
+  const float eta = a.lr[gi], beta = a.mom[gi], alpha = a.decay[gi];
+  const float rs = 2.0f / (float)d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    sk[i] = to_f(((const IO*)a.k)[tok + i]);
+    float y = 0.f;
+    for (int gg = 0; gg < G; ++gg) y += sc.yp[(size_t)gg * d + i];
+    sr[i] = rs * (y - to_f(((const IO*)a.v)[tok + i]));
+    if (!global) sx[i] = sc.x[i];
+  }
+  for (int jj = threadIdx.x; jj < HS; jj += blockDim.x) {
+    sa[jj] = sc.a[j0 + jj];
+    sp[jj] = sc.sp[j0 + jj];
+  }
+  __syncthreads();
+  // delta = (W^2^T r) * s'(z) on the slice
+  col_dots(Wh2 + j0, d, HS, hid, sr, sg, part);
+  __syncthreads();
+  for (int jj = threadIdx.x; jj < HS; jj += blockDim.x) sg[jj] *= sp[jj];
+  __syncthreads();
 
-      // chunk / shard boundaries
-      if (!global && p % a.S[m] == 0) {
-        const float* W1i = a.W1i + ((size_t)m * H + h) * hd;
-        const float* W2i = a.W2i + ((size_t)m * H + h) * hd;
-        for (size_t e = threadIdx.x; e < hd; e += blockDim.x) {
-          Wh1[e] = W1[e] = W1i[e];
-          Wh2[e] = W2[e] = W2i[e];
-          S1[e] = 0.f;
-          S2[e] = 0.f;
-        }
-        for (int e = threadIdx.x; e < d * d; e += blockDim.x) Mq[e] = 0.f;
-      } else if (p % C == 0) {
-        for (size_t e = threadIdx.x; e < hd; e += blockDim.x) {
-          Wh1[e] = W1[e];
-          Wh2[e] = W2[e];
-        }
-        if (!global && a.qk_scope == 1)
-          for (int e = threadIdx.x; e < d * d; e += blockDim.x) Mq[e] = 0.f;
-      }
-      __syncthreads();
-
-      // phase 1: z = W^1 k, and in the same pass the global retrieval's W^1 q
-      // or a local memory's M_{t-1} q
-      const bool proj = !global && a.qk_proj;
-      {
-        const RowJob g1{Wh1, hid, d, sk, global ? sq : nullptr, sz, global ? szq : nullptr};
-        const RowJob g2{Mq, proj ? d : 0, d, sq, nullptr, sx, nullptr};
-        row_dots_2(g1, g2, part);
-      }
-      __syncthreads();
-      for (int j = threadIdx.x; j < hid; j += blockDim.x) {
-        const ActVals av = act_all<ACT>(sz[j]);
-        sa[j] = av.s;
-        sp[j] = av.d1;
-        if (global) saq[j] = act_f<ACT>(szq[j]);
-      }
-      __syncthreads();
-      // phase 2: y = W^2 s(z) (and the global retrieval W^2 s(W^1 q))
-      {
-        const RowJob g1{Wh2, d, hid, sa, global ? saq : nullptr, sy, global ? syq : nullptr};
-        const RowJob none{Wh2, 0, hid, sa, nullptr, sy, nullptr};
-        row_dots_2(g1, none, part);
-      }
-      __syncthreads();
-      for (int i = threadIdx.x; i < d; i += blockDim.x) {
-        sr[i] = rs * (sy[i] - sv[i]);
-        if (global) so[i] += syq[i];
-        // local query x = M_t q = M_{t-1} q + k (k . q) / ||k||^2, or q
-        if (!global) sx[i] = proj ? sx[i] + sk[i] * (kq * ikk) : sq[i];
-      }
-      __syncthreads();
-      // phase 3: delta = (W^2^T r) * s'(z)
-      col_dots(Wh2, d, hid, sr, sg, part);
-      __syncthreads();
-      for (int j = threadIdx.x; j < hid; j += blockDim.x) sg[j] *= sp[j];
-      __syncthreads();
-
-      // phase 4: gated update, u1 = delta k^T (hid x d), u2 = r s(z)^T (d x hid),
-      // 16-byte accesses, UNR per array in flight per thread.  A local memory
-      // also forms z'[j] = W1_t[j] . x here: the d/4 lanes holding one row of
-      // W1 are adjacent within a wave and sum by shuffles (fixed order).
-      const float keep = 1.0f - alpha;
-      {
-        constexpr int UNR = 4;
-        const int hd4 = (int)(hd / 4), g4 = d / 4;
-        f4 *S14 = reinterpret_cast<f4*>(S1), *W14 = reinterpret_cast<f4*>(W1),
-           *S24 = reinterpret_cast<f4*>(S2), *W24 = reinterpret_cast<f4*>(W2);
-        const f4* k4 = reinterpret_cast<const f4*>(sk);
-        const f4* a4 = reinterpret_cast<const f4*>(sa);
-        const f4* x4 = reinterpret_cast<const f4*>(sx);
-        for (int e0 = threadIdx.x; e0 < hd4; e0 += UNR * blockDim.x) {
-          f4 s1[UNR], w1[UNR], s2[UNR], w2[UNR];
+  // gated update of the slice (16-byte accesses, UNR per array in flight);
+  // a local memory also forms z'[j] = W1_t[j] . x from the fresh rows (the
+  // d/4 lanes of a row are adjacent in a wave and sum by shuffles)
+  const float keep = 1.0f - alpha;
+  constexpr int UNR = 4;
+  const int g4 = d / 4, h4 = HS / 4, n4 = HS * d / 4;  // n4: a multiple of 64
+  const f4* k4 = reinterpret_cast<const f4*>(sk);
+  const f4* x4 = reinterpret_cast<const f4*>(sx);
+  const f4* a4 = reinterpret_cast<const f4*>(sa);
+  {
+    f4 *S14 = reinterpret_cast<f4*>(S1 + (size_t)j0 * d), *W14 = reinterpret_cast<f4*>(W1 + (size_t)j0 * d);
+    for (int e0 = threadIdx.x; e0 < n4; e0 += UNR * blockDim.x) {
+      f4 s1[UNR], w1[UNR];
 #pragma unroll
-          for (int u = 0; u < UNR; ++u) {
-            const int e = e0 + u * blockDim.x;
-            if (e < hd4) {
-              s1[u] = S14[e];
-              w1[u] = W14[e];
-              s2[u] = S24[e];
-              w2[u] = W24[e];
-            }
-          }
+      for (int u = 0; u < UNR; ++u) {
+        const int e = e0 + u * blockDim.x;
+        if (e < n4) {
+          s1[u] = S14[e];
+          w1[u] = W14[e];
+        }
+      }
 #pragma unroll
-          for (int u = 0; u < UNR; ++u) {
-            const int e = e0 + u * blockDim.x;
-            if (e < hd4) {  // hd4 is a multiple of 64: whole waves take this branch
-              const int j1 = e / g4, l4 = e - j1 * g4;                   // W1, S1: [hid][d]
-              const int i2 = (4 * e) / hid, j4 = (4 * e - i2 * hid) / 4;  // W2, S2: [d][hid]
-              const f4 n1 = beta * s1[u] - (eta * sg[j1]) * k4[l4];
-              const f4 n2 = beta * s2[u] - (eta * sr[i2]) * a4[j4];
-              const f4 nw1 = keep * w1[u] + n1;
-              S14[e] = n1;
-              W14[e] = nw1;
-              S24[e] = n2;
-              W24[e] = keep * w2[u] + n2;
-              if (!global) {
-                const f4 xv = x4[l4];
-                float zp = nw1[0] * xv[0] + nw1[1] * xv[1] + nw1[2] * xv[2] + nw1[3] * xv[3];
-                for (int o_ = 1; o_ < g4; o_ <<= 1) zp += __shfl_xor(zp, o_, WAVE);
-                if (l4 == 0) sz[j1] = zp;
-              }
-            }
+      for (int u = 0; u < UNR; ++u) {
+        const int e = e0 + u * blockDim.x;
+        if (e < n4) {  // whole waves take this branch
+          const int jj = e / g4, l4 = e - jj * g4;
+          const f4 n1 = beta * s1[u] - (eta * sg[jj]) * k4[l4];
+          const f4 nw = keep * w1[u] + n1;
+          S14[e] = n1;
+          W14[e] = nw;
+          if (!global) {
+            const f4 xv = x4[l4];
+            float zp = nw[0] * xv[0] + nw[1] * xv[1] + nw[2] * xv[2] + nw[3] * xv[3];
+            for (int o_ = 1; o_ < g4; o_ <<= 1) zp += __shfl_xor(zp, o_, WAVE);
+            if (l4 == 0) sz[jj] = zp;
           }
         }
-      }
-      if (!global) {
-        for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
-          const int i = e / d, j = e - i * d;
-          Mq[e] += sk[i] * sk[j] * ikk;
-        }
-      }
-      __syncthreads();
-
-      if (!global) {  // local retrieval at W_t: o += W2_t s(z')
-        for (int j = threadIdx.x; j < hid; j += blockDim.x) sa[j] = act_f<ACT>(sz[j]);
-        __syncthreads();
-        row_dots(W2, d, hid, sa, sy, part);
-        __syncthreads();
-        for (int i = threadIdx.x; i < d; i += blockDim.x) so[i] += sy[i];
-        __syncthreads();
       }
     }
-    for (int i = threadIdx.x; i < d; i += blockDim.x) o[(size_t)t * d + i] = from_f<IO>(so[i]);
-    __syncthreads();
+  }
+  {
+    for (int e0 = threadIdx.x; e0 < n4; e0 += UNR * blockDim.x) {
+      f4 s2[UNR], w2[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int e = e0 + u * blockDim.x;
+        if (e < n4) {
+          const int i = e / h4, c4 = e - i * h4;
+          const size_t ofs = (size_t)i * hid + j0 + 4 * c4;
+          s2[u] = *reinterpret_cast<const f4*>(S2 + ofs);
+          w2[u] = *reinterpret_cast<const f4*>(W2 + ofs);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int e = e0 + u * blockDim.x;
+        if (e < n4) {
+          const int i = e / h4, c4 = e - i * h4;
+          const size_t ofs = (size_t)i * hid + j0 + 4 * c4;
+          const f4 n2 = beta * s2[u] - (eta * sr[i]) * a4[c4];
+          *reinterpret_cast<f4*>(S2 + ofs) = n2;
+          *reinterpret_cast<f4*>(W2 + ofs) = keep * w2[u] + n2;
+        }
+      }
+    }
+  }
+  if (!global && g == 0) {
+    float kk = 0.f;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) kk += sk[i] * sk[i];
+    kk = block_sum(kk, red);
+    const float ikk = kk > 0.f ? 1.0f / kk : 0.f;
+    for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
+      const int i = e / d, j = e - i * d;
+      Mq[e] += sk[i] * sk[j] * ikk;
+    }
+  }
+  if (global) return;
+  __syncthreads();
+  // the slice's share of the local retrieval W2_t s(W1_t x)
+  for (int jj = threadIdx.x; jj < HS; jj += blockDim.x) sa[jj] = act_f<ACT>(sz[jj]);
+  __syncthreads();
+  {
+    const RowJob r1{W2 + j0, d, HS, hid, sa, nullptr, sy, nullptr};
+    const RowJob none{W2, 0, HS, hid, sa, nullptr, sy, nullptr};
+    row_dots_2(r1, none, part);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < d; i += blockDim.x) sc.y2[(size_t)g * d + i] = sy[i];
+}
+
+// o = the global retrieval's shares, then each local memory's (fixed order)
+template <typename IO>
+__global__ void __launch_bounds__(128) step_k3(StepArgs a) {
+  const int chain = blockIdx.x, d = a.d, G = a.G;
+  IO* o = (IO*)a.o + ((size_t)chain * a.T + a.t) * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    float acc = 0.f;
+    for (int m = 0; m < a.M; ++m) {
+      const StepScr sc = step_scr(a, m, chain);
+      const float* sh = (a.has_global && m == 0) ? sc.yq : sc.y2;
+      for (int gg = 0; gg < G; ++gg) acc += sh[(size_t)gg * d + i];
+    }
+    o[i] = from_f<IO>(acc);
   }
 }
 
@@ -336,26 +430,35 @@ __global__ void __launch_bounds__(256) step_init_kernel(StepArgs a) {
 
 size_t step_state_floats(int d, int hid) { return 6 * (size_t)hid * d + (size_t)d * d; }
 
+size_t step_scratch_floats(int d, int hid) {
+  const int HS = hid < 64 ? hid : 64, G = hid / HS;
+  const size_t n = 2 * (size_t)hid + d + 3 * (size_t)G * d;
+  return (n + 63) / 64 * 64;
+}
+
 hipError_t launch_step_init(const StepArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(step_init_kernel, dim3(a.B * a.H, a.M), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
-hipError_t launch_step(const StepArgs& a, hipStream_t st) {
-  if (a.d > STEP_MAX_D || a.hid > STEP_MAX_H) return hipErrorInvalidValue;
-  const dim3 grid(a.B * a.H), block(STEP_THREADS);
-  if (a.bf16) {
-    if (a.act == ACT_SILU)
-      hipLaunchKernelGGL((step_kernel<__bf16, ACT_SILU>), grid, block, 0, st, a);
-    else
-      hipLaunchKernelGGL((step_kernel<__bf16, ACT_GELU>), grid, block, 0, st, a);
-  } else {
-    if (a.act == ACT_SILU)
-      hipLaunchKernelGGL((step_kernel<float, ACT_SILU>), grid, block, 0, st, a);
-    else
-      hipLaunchKernelGGL((step_kernel<float, ACT_GELU>), grid, block, 0, st, a);
+template <typename IO, int ACT>
+static hipError_t step_tokens(StepArgs a, hipStream_t st) {
+  const dim3 grid(a.G, a.B * a.H, a.M), block(STEP_THREADS);
+  for (int t = 0; t < a.T; ++t) {
+    a.t = t;
+    hipLaunchKernelGGL((step_k1<IO, ACT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((step_k2<IO, ACT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((step_k3<IO>), dim3(a.B * a.H), dim3(128), 0, st, a);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_step(const StepArgs& a, hipStream_t st) {
+  if (a.d > STEP_MAX_D || a.hid > STEP_MAX_H || a.HS > 64 || a.G * a.HS != a.hid || !a.scratch)
+    return hipErrorInvalidValue;
+  if (a.bf16)
+    return a.act == ACT_SILU ? step_tokens<__bf16, ACT_SILU>(a, st) : step_tokens<__bf16, ACT_GELU>(a, st);
+  return a.act == ACT_SILU ? step_tokens<float, ACT_SILU>(a, st) : step_tokens<float, ACT_GELU>(a, st);
 }
 
 }  // namespace tnt

@@ -100,7 +100,9 @@ def test_state_size_formula():
     cfg = WORKLOADS[3]  # global + two locals, d 64, hid 256
     M = cfg.has_global + len(cfg.locals_)
     per = 6 * cfg.hid * cfg.d + cfg.d * cfg.d
-    assert tnt.tnt_mem_state_size(cfg) == M * cfg.B * cfg.H * per * 4
+    G = cfg.hid // min(64, cfg.hid)
+    scratch = -(-(2 * cfg.hid + cfg.d + 3 * G * cfg.d) // 64) * 64
+    assert tnt.tnt_mem_state_size(cfg) == M * cfg.B * cfg.H * (per + scratch) * 4
 
 
 def test_state_size_ignores_L():

@@ -83,8 +83,11 @@ def test_step_cut_invariance(idx):
     torch.cuda.synchronize()
     assert torch.equal(whole, single)
     assert torch.equal(whole, torch.cat([pre, dec], 2))
-    assert torch.equal(s_whole, s_single)
-    assert torch.equal(s_whole, state)
+    # the state blocks (the scratch area after them is undefined between calls)
+    M = cfg.has_global + len(cfg.locals_)
+    nb = M * cfg.B * cfg.H * (6 * cfg.hid * cfg.d + cfg.d * cfg.d) * 4
+    assert torch.equal(s_whole[:nb], s_single[:nb])
+    assert torch.equal(s_whole[:nb], state[:nb])
 
 
 def test_step_global_final_state():
