@@ -107,3 +107,27 @@ def test_step_global_final_state():
     e = max_rel_err(st, ref)
     print(f"  final global state vs oracle {e:.3e}", flush=True)
     assert e <= tol(cfg)
+
+
+@pytest.mark.parametrize("w", [1, 2, 3, 4])
+def test_step_fullsize_against_oracle_samples(w):
+    """The step-wise forward over the whole of each full-size workload (every
+    chain, one call of L tokens), compared at the stored oracle samples of
+    tests/golden/workload{w}_bwd.npz (every batch row of head H // 2 at chunk
+    and shard edges and seeded positions), bound 2e-2 (bf16 inputs)."""
+    import os
+    from paper_2511_07343_amd.inputs import WORKLOADS
+    cfg = WORKLOADS[w]
+    print(f"\n[case] step full size, workload {w}: {cfg.name}", flush=True)
+    ref = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                               f"workload{w}_bwd.npz"))
+    hs = cfg.H // 2
+    rows = torch.as_tensor(ref["rows"])
+    x = tnt.device_inputs(make_inputs(cfg, w), cfg)
+    o, _ = tnt.step_forward(cfg, x, [cfg.L])
+    torch.cuda.synchronize()
+    got = o[:, hs].float().cpu()[:, rows].numpy()
+    assert got.shape == ref["o"].shape
+    e = max_rel_err(got, ref["o"])
+    print(f"  o max rel err {e:.3e}", flush=True)
+    assert np.isfinite(got).all() and e <= 2e-2
