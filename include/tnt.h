@@ -172,6 +172,16 @@ size_t tnt_mem_state_size(const tnt_config* cfg);
 tnt_status tnt_mem_state_init(const tnt_config* cfg, const float* W1_init,
                               const float* W2_init, void* state, void* stream);
 
+/* Carried state after tnt_mem_fwd over a prefix of cfg->L tokens (a multiple
+ * of C_G and of every S_L, as tnt_mem_fwd requires), for decoding on from
+ * pos = cfg->L: the global memory takes the forward's final_state (V1, V2,
+ * S1, S2; required when has_global), each local memory is set as by
+ * tnt_mem_state_init (it resets at the next token, a shard start, anyway).
+ * The chunk-parallel forward then serves as the prefill of tnt_mem_step. */
+tnt_status tnt_mem_state_from_fwd(const tnt_config* cfg, const float* final_state,
+                                  const float* W1_init, const float* W2_init, void* state,
+                                  void* stream);
+
 /* Forward over T >= 0 further tokens of every chain, advancing `state`.
  *   pos   : tokens `state` has consumed so far (0 after tnt_mem_state_init);
  *           chunk and shard boundaries are taken from pos + t.  A pos that

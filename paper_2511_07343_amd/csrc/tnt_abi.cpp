@@ -670,6 +670,22 @@ tnt_status tnt_mem_state_init(const tnt_config* cfg, const float* W1_init, const
   return launch_step_init(a, (hipStream_t)stream) == hipSuccess ? TNT_OK : TNT_ERR_HIP;
 }
 
+tnt_status tnt_mem_state_from_fwd(const tnt_config* cfg, const float* final_state,
+                                  const float* W1_init, const float* W2_init, void* state,
+                                  void* stream) {
+  tnt_status s = validate(cfg);  // L: the prefix the forward ran over
+  if (s != TNT_OK) return s;
+  if (!W1_init || !W2_init || !state || (cfg->has_global && !final_state)) return TNT_ERR_NULL;
+  for (const void* p : {(const void*)W1_init, (const void*)W2_init, (const void*)state,
+                        (const void*)final_state})
+    if (p && misaligned(p)) return TNT_ERR_ALIGN;
+  StepArgs a = step_args(cfg);
+  a.W1i = W1_init; a.W2i = W2_init; a.state = (float*)state;
+  a.scratch = a.state + (size_t)a.M * a.B * a.H * a.mem_stride;
+  return launch_step_from_final(a, final_state, (hipStream_t)stream) == hipSuccess ? TNT_OK
+                                                                                   : TNT_ERR_HIP;
+}
+
 tnt_status tnt_mem_step(const tnt_config* cfg, int64_t pos, int32_t T, const void* q,
                         const void* k, const void* v, const float* lr, const float* mom,
                         const float* decay, const float* W1_init, const float* W2_init,

@@ -184,6 +184,7 @@ struct StepArgs {
 size_t step_state_floats(int d, int hid);
 size_t step_scratch_floats(int d, int hid);
 hipError_t launch_step_init(const StepArgs& a, hipStream_t st);
+hipError_t launch_step_from_final(const StepArgs& a, const float* fin, hipStream_t st);
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
 struct SumJobs {  // up to three (partials, output) pairs summed by one launch

@@ -428,6 +428,28 @@ __global__ void __launch_bounds__(256) step_init_kernel(StepArgs a) {
   for (size_t e = 6 * hd + threadIdx.x; e < a.mem_stride; e += blockDim.x) base[e] = 0.f;
 }
 
+// the global memory's block from a forward's final state [chain][4][hid*d]
+// (V1, V2, S1, S2): W^1 = W1 = V1, W^2 = W2 = V2, S1, S2
+__global__ void __launch_bounds__(256) step_from_final_kernel(StepArgs a, const float* fin) {
+  const int chain = blockIdx.x;
+  const size_t hd = (size_t)a.hid * a.d;
+  float* base = a.state + (size_t)chain * a.mem_stride;  // memory 0
+  const float* f = fin + (size_t)chain * 4 * hd;
+  for (size_t e = threadIdx.x; e < hd; e += blockDim.x) {
+    base[e] = base[2 * hd + e] = f[e];
+    base[hd + e] = base[3 * hd + e] = f[hd + e];
+    base[4 * hd + e] = f[2 * hd + e];
+    base[5 * hd + e] = f[3 * hd + e];
+  }
+}
+
+hipError_t launch_step_from_final(const StepArgs& a, const float* fin, hipStream_t st) {
+  hipLaunchKernelGGL(step_init_kernel, dim3(a.B * a.H, a.M), dim3(256), 0, st, a);
+  if (a.has_global && fin)
+    hipLaunchKernelGGL(step_from_final_kernel, dim3(a.B * a.H), dim3(256), 0, st, a, fin);
+  return hipGetLastError();
+}
+
 size_t step_state_floats(int d, int hid) { return 6 * (size_t)hid * d + (size_t)d * d; }
 
 size_t step_scratch_floats(int d, int hid) {

@@ -24,7 +24,7 @@ STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPP
           4: "TNT_ERR_WORKSPACE", 5: "TNT_ERR_ALIGN", 6: "TNT_ERR_HIP", 7: "TNT_ERR_ARG"}
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
             "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read",
-            "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step"]
+            "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step", "tnt_mem_state_from_fwd"]
 
 
 class TntError(RuntimeError):
@@ -67,6 +67,8 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_mem_state_init.argtypes = [cp, vp, vp, vp, vp]
     L.tnt_mem_state_init.restype = ctypes.c_int
     L.tnt_mem_step.argtypes = [cp, ctypes.c_int64, i32] + [vp] * 11
+    L.tnt_mem_state_from_fwd.argtypes = [cp] + [vp] * 5
+    L.tnt_mem_state_from_fwd.restype = ctypes.c_int
     L.tnt_mem_step.restype = ctypes.c_int
     L.tnt_strerror.argtypes = [ctypes.c_int]
     L.tnt_strerror.restype = ctypes.c_char_p
@@ -145,6 +147,12 @@ def tnt_mem_state_init(cfg, W1_init, W2_init, state, stream=None) -> int:
     c = to_c(cfg)
     return lib().tnt_mem_state_init(ctypes.byref(c), _p(W1_init), _p(W2_init), _p(state),
                                     _stream(stream))
+
+
+def tnt_mem_state_from_fwd(cfg, final_state, W1_init, W2_init, state, stream=None) -> int:
+    c = to_c(cfg)
+    return lib().tnt_mem_state_from_fwd(ctypes.byref(c), _p(final_state), _p(W1_init),
+                                        _p(W2_init), _p(state), _stream(stream))
 
 
 def tnt_mem_step(cfg, pos, T, q, k, v, lr, mom, decay, W1_init, W2_init, state, o,

@@ -137,3 +137,12 @@ def test_step_rejects_bad_arguments():
     assert tnt.tnt_mem_state_init(cfg, p, p, None, stream=0) == 1
     # T == 0 enqueues nothing and succeeds without touching the pointers
     assert tnt.tnt_mem_step(cfg, 0, 0, p, p, p, p, p, p, p, p, p, p, stream=0) == 0
+
+
+def test_state_from_fwd_validation():
+    cfg = small_config()  # has a global memory
+    p = 256
+    assert tnt.tnt_mem_state_from_fwd(cfg, None, p, p, p, stream=0) == 1
+    import dataclasses
+    assert tnt.tnt_mem_state_from_fwd(dataclasses.replace(cfg, L=100), p, p, p, p, stream=0) == 2
+    assert tnt.tnt_mem_state_from_fwd(cfg, p + 4, p, p, p, stream=0) == 5

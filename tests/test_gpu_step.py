@@ -131,3 +131,35 @@ def test_step_fullsize_against_oracle_samples(w):
     e = max_rel_err(got, ref["o"])
     print(f"  o max rel err {e:.3e}", flush=True)
     assert np.isfinite(got).all() and e <= 2e-2
+
+
+@pytest.mark.parametrize("cfg,L0,pieces", [
+    (small_config(F32, ACT_GELU, B=2, H=2, L=96, d=16, hid=32, C_G=16,
+                  locals_=((8, 32), (4, 16)), name="f32 handoff"), 64, [1] * 8 + [24]),
+    (small_config(BF16, ACT_SILU, B=1, H=2, L=192, d=64, hid=256, C_G=64,
+                  locals_=((16, 64),), name="bf16 handoff"), 128, [1, 1, 62]),
+], ids=lambda c: c.name if hasattr(c, "name") else str(c))
+def test_prefill_by_forward_then_decode(cfg, L0, pieces):
+    """tnt_mem_fwd over the first L0 tokens (its final_state), then
+    tnt_mem_state_from_fwd and tnt_mem_step over the rest: the decoded outputs
+    match the oracle's whole-sequence forward on those tokens."""
+    import dataclasses
+    assert L0 + sum(pieces) == cfg.L
+    inp = make_inputs(cfg, 404)
+    print(f"\n[case] prefill-then-decode {cfg.name}", flush=True)
+    x = tnt.device_inputs(inp, cfg)
+    cfg0 = dataclasses.replace(cfg, L=L0)
+    x0 = {n: (t[:, :, :L0] if n in ("q", "k", "v", "dO") else
+              t[..., :L0] if n in ("lr", "mom", "decay") else t).contiguous()
+          for n, t in x.items()}
+    _, _, fin = tnt.forward(cfg0, x0, save=False, final_state=True)
+    state = torch.empty(tnt.tnt_mem_state_size(cfg), dtype=torch.uint8, device=x["q"].device)
+    st = tnt.tnt_mem_state_from_fwd(cfg0, fin, x["W1"], x["W2"], state)
+    assert st == 0, tnt.strerror(st)
+    o_dec, _ = tnt.step_forward(cfg, x, pieces, state=state, pos=L0)
+    torch.cuda.synchronize()
+    got = o_dec.float().cpu().numpy()
+    ref = oracle_o(cfg, inp)[:, :, L0:]
+    e = max_rel_err(got, ref)
+    print(f"  decoded o vs oracle {e:.3e}", flush=True)
+    assert np.isfinite(got).all() and e <= tol(cfg)
