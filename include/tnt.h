@@ -194,6 +194,21 @@ tnt_status tnt_mem_step(const tnt_config* cfg, int64_t pos, int32_t T, const voi
                         const float* decay, const float* W1_init, const float* W2_init,
                         void* state, void* o, void* stream);
 
+/* Debug: the per-token quantities of one chunk's inner gradient (the chain
+ * rule of the recall loss, Sec. 2.1; every token of the chunk at the same
+ * weights, Sec. 2.2) for the chain (b, h), tokens [t0, t0 + C):
+ *     Zk = K W1^T (C x hid),  R = (2/d) (s(Zk) W2^T - V) (C x d),
+ *     D1 = (R W2) * s'(Zk) (C x hid),
+ * so that token t's gradients are u1_t = D1_t^T k_t and u2_t = R_t^T s(Zk_t).
+ *   k, v   : [B][H][L][d] as for tnt_mem_fwd (cfg->dtype);
+ *   W1, W2 : [hid][d], [d][hid] fp32, the weights the gradients are taken at;
+ *   Zk, D1 : [C][hid] fp32;  R : [C][d] fp32 (device, caller-owned).
+ * 1 <= C <= 64 and t0 + C <= L (TNT_ERR_SHAPE otherwise).  fp32 arithmetic,
+ * one workgroup: a check of the gradient math, not a fast path. */
+tnt_status tnt_dbg_chunk_grads(const tnt_config* cfg, int32_t b, int32_t h, int32_t t0,
+                               int32_t C, const void* k, const void* v, const float* W1,
+                               const float* W2, float* Zk, float* R, float* D1, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* tnt_strerror(tnt_status status);
 

@@ -670,6 +670,25 @@ tnt_status tnt_mem_state_init(const tnt_config* cfg, const float* W1_init, const
   return launch_step_init(a, (hipStream_t)stream) == hipSuccess ? TNT_OK : TNT_ERR_HIP;
 }
 
+tnt_status tnt_dbg_chunk_grads(const tnt_config* cfg, int32_t b, int32_t h, int32_t t0,
+                               int32_t C, const void* k, const void* v, const float* W1,
+                               const float* W2, float* Zk, float* R, float* D1, void* stream) {
+  tnt_status s = validate(cfg);
+  if (s != TNT_OK) return s;
+  if (b < 0 || b >= cfg->B || h < 0 || h >= cfg->H || t0 < 0 || C < 1 || C > 64 ||
+      t0 > cfg->L - C)
+    return TNT_ERR_SHAPE;
+  if (!k || !v || !W1 || !W2 || !Zk || !R || !D1) return TNT_ERR_NULL;
+  for (const void* p : {(const void*)k, (const void*)v, (const void*)W1, (const void*)W2,
+                        (const void*)Zk, (const void*)R, (const void*)D1})
+    if (misaligned(p)) return TNT_ERR_ALIGN;
+  DbgArgs a{};
+  a.d = cfg->d; a.hid = cfg->hid; a.C = C; a.act = cfg->act; a.bf16 = cfg->dtype == TNT_BF16;
+  a.tok0 = ((size_t)b * cfg->H + h) * cfg->L + t0;
+  a.k = k; a.v = v; a.W1 = W1; a.W2 = W2; a.Zk = Zk; a.R = R; a.D1 = D1;
+  return launch_dbg_chunk_grads(a, (hipStream_t)stream) == hipSuccess ? TNT_OK : TNT_ERR_HIP;
+}
+
 tnt_status tnt_mem_state_from_fwd(const tnt_config* cfg, const float* final_state,
                                   const float* W1_init, const float* W2_init, void* state,
                                   void* stream) {

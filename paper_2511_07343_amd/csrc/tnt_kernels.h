@@ -187,6 +187,17 @@ hipError_t launch_step_init(const StepArgs& a, hipStream_t st);
 hipError_t launch_step_from_final(const StepArgs& a, const float* fin, hipStream_t st);
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_global_gate_bwd(const GlobalArgs& a, hipStream_t st);
+
+// tnt_dbg_chunk_grads: one chunk (tokens tok0 .. tok0 + C of a chain's rows in
+// k, v) at the weights W1 [hid][d], W2 [d][hid]
+struct DbgArgs {
+  int d, hid, C, act, bf16;
+  size_t tok0;         // row of the chunk's first token in the [B*H*L][d] arrays
+  const void *k, *v;
+  const float *W1, *W2;
+  float *Zk, *R, *D1;  // [C][hid], [C][d], [C][hid]
+};
+hipError_t launch_dbg_chunk_grads(const DbgArgs& a, hipStream_t st);
 struct SumJobs {  // up to three (partials, output) pairs summed by one launch
   const float* parts[3];
   void* out[3];

@@ -24,7 +24,8 @@ STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPP
           4: "TNT_ERR_WORKSPACE", 5: "TNT_ERR_ALIGN", 6: "TNT_ERR_HIP", 7: "TNT_ERR_ARG"}
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
             "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read",
-            "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step", "tnt_mem_state_from_fwd"]
+            "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step", "tnt_mem_state_from_fwd",
+            "tnt_dbg_chunk_grads"]
 
 
 class TntError(RuntimeError):
@@ -67,6 +68,8 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_mem_state_init.argtypes = [cp, vp, vp, vp, vp]
     L.tnt_mem_state_init.restype = ctypes.c_int
     L.tnt_mem_step.argtypes = [cp, ctypes.c_int64, i32] + [vp] * 11
+    L.tnt_dbg_chunk_grads.argtypes = [cp, i32, i32, i32, i32] + [vp] * 8
+    L.tnt_dbg_chunk_grads.restype = ctypes.c_int
     L.tnt_mem_state_from_fwd.argtypes = [cp] + [vp] * 5
     L.tnt_mem_state_from_fwd.restype = ctypes.c_int
     L.tnt_mem_step.restype = ctypes.c_int
@@ -147,6 +150,12 @@ def tnt_mem_state_init(cfg, W1_init, W2_init, state, stream=None) -> int:
     c = to_c(cfg)
     return lib().tnt_mem_state_init(ctypes.byref(c), _p(W1_init), _p(W2_init), _p(state),
                                     _stream(stream))
+
+
+def tnt_dbg_chunk_grads(cfg, b, h, t0, C, k, v, W1, W2, Zk, R, D1, stream=None) -> int:
+    c = to_c(cfg)
+    return lib().tnt_dbg_chunk_grads(ctypes.byref(c), b, h, t0, C, _p(k), _p(v), _p(W1), _p(W2),
+                                     _p(Zk), _p(R), _p(D1), _stream(stream))
 
 
 def tnt_mem_state_from_fwd(cfg, final_state, W1_init, W2_init, state, stream=None) -> int:

@@ -146,3 +146,14 @@ def test_state_from_fwd_validation():
     import dataclasses
     assert tnt.tnt_mem_state_from_fwd(dataclasses.replace(cfg, L=100), p, p, p, p, stream=0) == 2
     assert tnt.tnt_mem_state_from_fwd(cfg, p + 4, p, p, p, stream=0) == 5
+
+
+def test_dbg_chunk_grads_validation():
+    cfg = small_config()  # B1 H2 L64
+    p = 256
+    args = (p,) * 7
+    assert tnt.tnt_dbg_chunk_grads(cfg, 1, 0, 0, 8, *args, stream=0) == 2     # b >= B
+    assert tnt.tnt_dbg_chunk_grads(cfg, 0, 2, 0, 8, *args, stream=0) == 2     # h >= H
+    assert tnt.tnt_dbg_chunk_grads(cfg, 0, 0, 60, 8, *args, stream=0) == 2    # t0 + C > L
+    assert tnt.tnt_dbg_chunk_grads(cfg, 0, 0, 0, 65, *args, stream=0) == 2    # C > 64
+    assert tnt.tnt_dbg_chunk_grads(cfg, 0, 0, 0, 8, None, *args[1:], stream=0) == 1
