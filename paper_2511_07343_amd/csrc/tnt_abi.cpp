@@ -306,31 +306,11 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     HIP_TRY(hipStreamWaitEvent(fk->side, fk->e0, 0));
     st = fk->side;
   }
-  if (c->has_global) {
-    GlobalArgs g{};
-    g.q = q; g.k = k; g.v = v;
-    g.lr = lr; g.mom = mom; g.decay = decay;
-    g.W1i = W1i; g.W2i = W2i;
-    g.o_part = opart;
-    g.states = sv ? (float*)(sv + y.sv_g) : (float*)(ws + y.ring_g);
-    g.nslots = sv ? y.g_chunks + 1 : 2;
-    g.tokc = (float*)(ws + y.w_tokc);
-    g.chunkc = (float*)(ws + y.w_chunkc);
-    g.Rbuf = (float*)(ws + y.w_R);
-    g.part = (float*)(ws + y.w_part);
-    g.packT = ws + y.w_gpack;
-    g.opT = ws + y.w_gop;
-    g.D = dims_of(c, c->C_G, c->L);
-    g.force_generic = generic_only();
-    HIP_TIMED("global_scan", launch_global_scan(g, st));
-    HIP_TIMED("global_init", launch_global_init(g, st));
-    for (int n = 0; n < y.g_chunks; ++n) HIP_TIMED("global_fwd_chunk", launch_global_fwd_chunk(g, n, st));
-    if (final_state)
-      HIP_TIMED("copy_final", launch_copy_final(g.states, g.nslots, y.BH, 4 * y.hd, y.g_chunks % g.nslots,
-                                final_state, st));
-    m = 1;
-  }
+  // the local walks first: their workgroups are the critical path, and the
+  // dispatcher places work in the order it is enqueued (the global chain's
+  // tile grids would otherwise take the CUs before the walk starts)
   st = main_st;
+  m = c->has_global;
   for (int i = 0; i < c->n_local; ++i, ++m) {
     LocalFwdArgs a{};
     a.q = q; a.k = k; a.v = v;
@@ -352,6 +332,31 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.force_generic = generic_only();
     HIP_TIMED("local_fwd", launch_local_fwd(a, y.l_units[i], st));
   }
+  if (c->has_global) {
+    st = fk ? fk->side : main_st;
+    GlobalArgs g{};
+    g.q = q; g.k = k; g.v = v;
+    g.lr = lr; g.mom = mom; g.decay = decay;
+    g.W1i = W1i; g.W2i = W2i;
+    g.o_part = opart;
+    g.states = sv ? (float*)(sv + y.sv_g) : (float*)(ws + y.ring_g);
+    g.nslots = sv ? y.g_chunks + 1 : 2;
+    g.tokc = (float*)(ws + y.w_tokc);
+    g.chunkc = (float*)(ws + y.w_chunkc);
+    g.Rbuf = (float*)(ws + y.w_R);
+    g.part = (float*)(ws + y.w_part);
+    g.packT = ws + y.w_gpack;
+    g.opT = ws + y.w_gop;
+    g.D = dims_of(c, c->C_G, c->L);
+    g.force_generic = generic_only();
+    HIP_TIMED("global_scan", launch_global_scan(g, st));
+    HIP_TIMED("global_init", launch_global_init(g, st));
+    for (int n = 0; n < y.g_chunks; ++n) HIP_TIMED("global_fwd_chunk", launch_global_fwd_chunk(g, n, st));
+    if (final_state)
+      HIP_TIMED("copy_final", launch_copy_final(g.states, g.nslots, y.BH, 4 * y.hd, y.g_chunks % g.nslots,
+                                final_state, st));
+  }
+  st = main_st;
   if (fk) {
     HIP_TRY(hipEventRecord(fk->e1, fk->side));
     HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
