@@ -20,6 +20,9 @@ Memorization", arXiv 2511.07343), per (batch, head) chain, in fp64:
 * Global memory (Sec. 4.1.1 box, global update; App. E general form): chunks
   of C_G, state carried across chunks, never reset; retrieval at the
   chunk-entry state V_{xi(t, C_G)} (Sec. 4.1.2 box; App. E retrieval rule).
+  ``intra=True`` takes the other reading: the chunkwise retrieval rule of
+  Sec. 2.2 applied to the global memory, o_t = f(V_t, q_t) with V_t the state
+  after token t's own update (gradients still at the chunk-entry state).
 * Local memories (Sec. 4.1.1 box, local update; App. E): chunks of C_L, state
   reset to the learned init (and momentum to zero) every S_L tokens; retrieval
   at W_t, i.e. after token t's own update (Sec. 2.1 / 2.2 retrieval rules).
@@ -142,12 +145,30 @@ def _global_accumulate(V1, V2, S1, S2, V1h, V2h, k, v, eta, beta, alpha, kind):
     return V1, V2, S1, S2
 
 
+def _global_accumulate_intra(V1, V2, S1, S2, V1h, V2h, q, k, v, eta, beta, alpha, kind):
+    """As ``_global_accumulate``, and after each token's update the memory is
+    read at the updated state: o_t = f(V_t, q_t) (Sec. 2.2 chunkwise retrieval
+    rule, the intra-chunk reading of the global memory)."""
+    g1, g2 = inner_grad(V1h[:, None], V2h[:, None], k, v, kind)
+    outs = []
+    for i in range(k.shape[1]):
+        V1, V2, S1, S2 = _gated_step(V1, V2, S1, S2, g1[:, i], g2[:, i],
+                                     eta[:, i], beta[:, i], alpha[:, i])
+        outs.append(memory_fn(V1, V2, q[:, i], kind))
+    return V1, V2, S1, S2, torch.stack(outs, 1)
+
+
 def global_memory(q, k, v, eta, beta, alpha, W1, W2, C_G: int, kind: str,
-                  ckpt: bool = False, block: int = 64, states: Optional[list] = None):
+                  ckpt: bool = False, block: int = 64, states: Optional[list] = None,
+                  intra: bool = False):
     """Global memory of every chain.  q,k,v [P,L,d]; gates [P,L]; W1 [P,h,d].
 
     Returns (o [P,L,d], (V1, V2, S1, S2) after the last token).  When
-    ``states`` is a list, the chunk-entry states are appended to it.
+    ``states`` is a list, the chunk-entry states are appended to it.  A chunk's
+    tokens are accumulated in sub-blocks of ``block`` tokens (a bound on the
+    size of the batched gradient only: every sub-block takes its gradients at
+    the chunk-entry state).  ``intra``: retrieval after each token's update
+    instead of at the chunk-entry state.
     """
     P, L, d = q.shape
     if L % C_G:
@@ -161,15 +182,22 @@ def global_memory(q, k, v, eta, beta, alpha, W1, W2, C_G: int, kind: str,
         V1h, V2h = V1, V2
         if states is not None:
             states.append((V1, V2, S1, S2))
-        outs.append(_global_retrieve(V1h, V2h, q[:, t0:t0 + C_G], kind))
+        if not intra:
+            outs.append(_global_retrieve(V1h, V2h, q[:, t0:t0 + C_G], kind))
         for b0 in range(t0, t0 + C_G, block):
             b1 = min(b0 + block, t0 + C_G)
-            args = (V1, V2, S1, S2, V1h, V2h, k[:, b0:b1], v[:, b0:b1],
-                    eta[:, b0:b1], beta[:, b0:b1], alpha[:, b0:b1], kind)
-            if ckpt:
-                V1, V2, S1, S2 = _ckpt.checkpoint(_global_accumulate, *args, use_reentrant=False)
+            if intra:
+                args = (V1, V2, S1, S2, V1h, V2h, q[:, b0:b1], k[:, b0:b1], v[:, b0:b1],
+                        eta[:, b0:b1], beta[:, b0:b1], alpha[:, b0:b1], kind)
+                fn = _global_accumulate_intra
             else:
-                V1, V2, S1, S2 = _global_accumulate(*args)
+                args = (V1, V2, S1, S2, V1h, V2h, k[:, b0:b1], v[:, b0:b1],
+                        eta[:, b0:b1], beta[:, b0:b1], alpha[:, b0:b1], kind)
+                fn = _global_accumulate
+            res = (_ckpt.checkpoint(fn, *args, use_reentrant=False) if ckpt else fn(*args))
+            V1, V2, S1, S2 = res[:4]
+            if intra:
+                outs.append(res[4])
     return torch.cat(outs, 1), (V1, V2, S1, S2)
 
 
@@ -238,6 +266,10 @@ def _kind(cfg) -> str:
     return _ACT_NAMES[a] if isinstance(a, int) else a
 
 
+def _intra(cfg) -> bool:
+    return bool(getattr(cfg, "global_intra", 0))
+
+
 def _scope(cfg) -> str:
     s = getattr(cfg, "qk_scope", 0)
     return {0: "shard", 1: "chunk"}[s] if isinstance(s, int) else s
@@ -249,7 +281,8 @@ def layer_forward(q, k, v, lr, mom, decay, W1, W2, cfg, ckpt: bool = False,
     alpha); W1 [M,P,h,d], W2 [M,P,d,h] (the head's init for every chain).
 
     ``cfg`` supplies C_G, locals_ = ((C_L, S_L), ...), act, has_global,
-    qk_proj, qk_scope.  Memory 0 is the global memory when has_global.
+    qk_proj, qk_scope and optionally global_intra (the global memory's
+    retrieval reading).  Memory 0 is the global memory when has_global.
     ``shards`` restricts the local memories to some shards (for sampling; the
     output is then only meaningful on those shards and without the global).
     """
@@ -259,7 +292,7 @@ def layer_forward(q, k, v, lr, mom, decay, W1, W2, cfg, ckpt: bool = False,
     final = None
     if cfg.has_global:
         og, final = global_memory(q, k, v, lr[0], mom[0], decay[0], W1[0], W2[0],
-                                  cfg.C_G, kind, ckpt=ckpt)
+                                  cfg.C_G, kind, ckpt=ckpt, intra=_intra(cfg))
         o = o + og
         m = 1
     for (C_L, S_L) in cfg.locals_:
@@ -298,7 +331,8 @@ def layer_backward(q, k, v, lr, mom, decay, W1, W2, dO, cfg, ckpt: bool = True):
                dW2=torch.zeros_like(W2), o=torch.zeros_like(q))
     m = 0
     if cfg.has_global:
-        _global_backward(q, k, v, lr[0], mom[0], decay[0], W1[0], W2[0], dO, cfg.C_G, kind, out, 0)
+        _global_backward(q, k, v, lr[0], mom[0], decay[0], W1[0], W2[0], dO, cfg.C_G, kind, out, 0,
+                         intra=_intra(cfg))
         m = 1
     for (C_L, S_L) in cfg.locals_:
         _local_backward(q, k, v, lr[m], mom[m], decay[m], W1[m], W2[m], dO, C_L, S_L, kind,
@@ -325,7 +359,8 @@ def _vjp(fn, args, diff, grad_outs):
     return [o.detach() for o in outs], gs
 
 
-def _global_backward(q, k, v, eta, beta, alpha, W1, W2, dO, C_G, kind, out, m, block=64):
+def _global_backward(q, k, v, eta, beta, alpha, W1, W2, dO, C_G, kind, out, m, block=64,
+                     intra=False):
     P, L, d = q.shape
     V1, V2 = W1, W2
     S1 = torch.zeros_like(W1)
@@ -349,9 +384,19 @@ def _global_backward(q, k, v, eta, beta, alpha, W1, W2, dO, C_G, kind, out, m, b
         V1h, V2h = chunks_entry(blocks)
         dV1h, dV2h = torch.zeros_like(W1), torch.zeros_like(W2)
         for (b0, b1, a1, a2, s1, s2) in reversed(blocks):
-            args = (a1, a2, s1, s2, V1h, V2h, k[:, b0:b1], v[:, b0:b1], eta[:, b0:b1],
-                    beta[:, b0:b1], alpha[:, b0:b1], kind)
-            _, g = _vjp(_global_accumulate, args, range(11), (dV1, dV2, dS1, dS2))
+            if intra:
+                # the sub-block's outputs f(V_t, q_t) receive dO as well
+                args = (a1, a2, s1, s2, V1h, V2h, q[:, b0:b1], k[:, b0:b1], v[:, b0:b1],
+                        eta[:, b0:b1], beta[:, b0:b1], alpha[:, b0:b1], kind)
+                o, g = _vjp(_global_accumulate_intra, args, range(12),
+                            (dV1, dV2, dS1, dS2, dO[:, b0:b1]))
+                out["o"][:, b0:b1] += o[4]
+                out["dq"][:, b0:b1] += g[6]
+                g = g[:6] + g[7:]
+            else:
+                args = (a1, a2, s1, s2, V1h, V2h, k[:, b0:b1], v[:, b0:b1], eta[:, b0:b1],
+                        beta[:, b0:b1], alpha[:, b0:b1], kind)
+                _, g = _vjp(_global_accumulate, args, range(11), (dV1, dV2, dS1, dS2))
             dV1, dV2, dS1, dS2 = g[0], g[1], g[2], g[3]
             dV1h = dV1h + g[4]
             dV2h = dV2h + g[5]
@@ -360,13 +405,14 @@ def _global_backward(q, k, v, eta, beta, alpha, W1, W2, dO, C_G, kind, out, m, b
             out["dlr"][m, :, b0:b1] += g[8]
             out["dmom"][m, :, b0:b1] += g[9]
             out["ddecay"][m, :, b0:b1] += g[10]
-        sl = slice(t0, t0 + C_G)
-        o, g = _vjp(lambda a, b, x, kd: (_global_retrieve(a, b, x, kd),), (V1h, V2h, q[:, sl], kind),
-                    range(3), (dO[:, sl],))
-        out["o"][:, sl] += o[0]
-        dV1h = dV1h + g[0]
-        dV2h = dV2h + g[1]
-        out["dq"][:, sl] += g[2]
+        if not intra:
+            sl = slice(t0, t0 + C_G)
+            o, g = _vjp(lambda a, b, x, kd: (_global_retrieve(a, b, x, kd),),
+                        (V1h, V2h, q[:, sl], kind), range(3), (dO[:, sl],))
+            out["o"][:, sl] += o[0]
+            dV1h = dV1h + g[0]
+            dV2h = dV2h + g[1]
+            out["dq"][:, sl] += g[2]
         # the chunk-entry state is both the running state and V_hat
         dV1 = dV1 + dV1h
         dV2 = dV2 + dV2h

@@ -58,6 +58,9 @@ class LayerConfig:
     qk_scope: int = QK_SHARD
     norm_v: bool = False
     name: str = ""
+    # retrieval of the global memory: 0 = at the chunk-entry state (Sec. 4.1.2
+    # box), 1 = after each token's own update (Sec. 2.2 chunkwise retrieval)
+    global_intra: int = 0
 
     @property
     def n_local(self) -> int:
@@ -182,9 +185,10 @@ def max_rel_err(x: np.ndarray, ref: np.ndarray) -> float:
 
 def small_config(dtype: int = F32, act: int = ACT_GELU, *, B=1, H=2, L=64, d=16,
                  hid=32, C_G=16, locals_=((8, 32),), has_global=1, qk_proj=1,
-                 qk_scope=QK_SHARD, norm_v=False, name: Optional[str] = None) -> LayerConfig:
+                 qk_scope=QK_SHARD, norm_v=False, global_intra=0,
+                 name: Optional[str] = None) -> LayerConfig:
     """A small shape for CPU tests and multi-tile GPU parity cases."""
     return LayerConfig(B=B, H=H, L=L, d=d, hid=hid, C_G=C_G, locals_=tuple(locals_),
                        act=act, dtype=dtype, has_global=has_global, qk_proj=qk_proj,
-                       qk_scope=qk_scope, norm_v=norm_v,
+                       qk_scope=qk_scope, norm_v=norm_v, global_intra=global_intra,
                        name=name or f"small B{B} H{H} L{L} d{d} h{hid}")

@@ -398,3 +398,149 @@ def test_segmented_backward_equals_plain_autograd(scope):
     b = O.layer_backward(*args, g["dO"], cfg, ckpt=False)
     for n in b:
         assert (a[n] - b[n]).abs().max() <= 1e-12 * max(1.0, b[n].abs().max().item()), n
+
+
+# ---------------------------------------------------------------- global sub-blocks
+# A global chunk is accumulated in sub-blocks (a memory bound of the batched
+# gradient); every sub-block must take its gradients at the chunk-entry state.
+# The path with more than one sub-block per chunk runs at every full-size
+# workload (C_G > 64), so it is pinned on its own here with small blocks.
+def _global_closed_form_check(kind, block, intra):
+    """C_G = L in sub-blocks of `block`: the final state is the closed form of
+    the gated sum of gradients all taken at V_init (explicit products); the
+    outputs are f(V_init, q_t) (chunk-entry reading) or f(V_t, q_t) with V_t
+    from the same closed form up to t (intra-chunk reading)."""
+    rng = np.random.default_rng(18)
+    P, L, d, h = 1, 12, 3, 5
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, P, L, d, h)
+    o, (V1, V2, S1, S2) = O.global_memory(q, k, v, eta, beta, alpha, W1, W2, L, kind,
+                                          block=block, intra=intra)
+    W1n, W2n = W1[0].numpy(), W2[0].numpy()
+    u1 = np.zeros((L, h, d)); u2 = np.zeros((L, d, h))
+    for t in range(L):
+        g1, g2 = O.inner_grad(W1, W2, k[:, t], v[:, t], kind)
+        u1[t], u2[t] = g1[0].numpy(), g2[0].numpy()
+    for t in range(L):
+        if intra:
+            A, c, _ = _closed_form_coeffs(eta[0].numpy(), beta[0].numpy(), alpha[0].numpy(), t)
+            W1t = A * W1n - np.einsum("t,thd->hd", c, u1[: t + 1])
+            W2t = A * W2n - np.einsum("t,tdh->dh", c, u2[: t + 1])
+        else:
+            W1t, W2t = W1n, W2n
+        np.testing.assert_allclose(o[0, t].numpy(), _np_f(W1t, W2t, q[0, t].numpy(), kind),
+                                   rtol=1e-11, atol=1e-13)
+    A, c, b = _closed_form_coeffs(eta[0].numpy(), beta[0].numpy(), alpha[0].numpy(), L - 1)
+    refs = (A * W1n - np.einsum("t,thd->hd", c, u1), A * W2n - np.einsum("t,tdh->dh", c, u2),
+            -np.einsum("t,thd->hd", b, u1), -np.einsum("t,tdh->dh", b, u2))
+    for got, ref in zip((V1, V2, S1, S2), refs):
+        np.testing.assert_allclose(got[0].numpy(), ref, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("block", [1, 5, 64])
+def test_global_subblocks_closed_form(kind, block):
+    """Sub-blocks of 1, 5 (three of them, the last ragged) and one whole
+    block give the closed form with every gradient at V_init."""
+    _global_closed_form_check(kind, block, intra=False)
+
+
+def test_global_subblock_backward_equals_one_pass_autograd():
+    """The segmented global backward with several sub-blocks per chunk (block
+    5 at C_G = 12, ragged last block, three chunks) equals one autograd pass
+    through the forward."""
+    rng = np.random.default_rng(19)
+    P, L, d, h, C_G = 2, 36, 3, 4, 12
+    xs = _rand_chain(rng, P, L, d, h)
+    dO = _t(rng.standard_normal((P, L, d)))
+    for intra in (False, True):
+        out = dict(dq=torch.zeros(P, L, d, dtype=torch.float64),
+                   dk=torch.zeros(P, L, d, dtype=torch.float64),
+                   dv=torch.zeros(P, L, d, dtype=torch.float64),
+                   dlr=torch.zeros(1, P, L, dtype=torch.float64),
+                   dmom=torch.zeros(1, P, L, dtype=torch.float64),
+                   ddecay=torch.zeros(1, P, L, dtype=torch.float64),
+                   dW1=torch.zeros(1, P, h, d, dtype=torch.float64),
+                   dW2=torch.zeros(1, P, d, h, dtype=torch.float64),
+                   o=torch.zeros(P, L, d, dtype=torch.float64))
+        q, k, v, eta, beta, alpha, W1, W2 = xs
+        O.tnt_oracle._global_backward(q, k, v, eta, beta, alpha, W1, W2, dO, C_G, "silu", out, 0,
+                                      block=5, intra=intra)
+        leaves = [x.detach().clone().requires_grad_(True) for x in xs]
+        o, _ = O.global_memory(*leaves, C_G, "silu", block=C_G, intra=intra)
+        grads = torch.autograd.grad((o * dO).sum(), leaves)
+        names = ("dq", "dk", "dv", "dlr", "dmom", "ddecay", "dW1", "dW2")
+        for n, gr in zip(names, grads):
+            got = out[n][0] if n in ("dlr", "dmom", "ddecay", "dW1", "dW2") else out[n]
+            err = (got - gr).abs().max().item()
+            assert err <= 1e-12 * max(1.0, gr.abs().max().item()), (intra, n, err)
+        assert (out["o"] - o.detach()).abs().max() < 1e-13
+
+
+def test_planted_subblock_gradient_point_fails_the_pin(monkeypatch):
+    """Taking a sub-block's gradients at the running state (instead of the
+    chunk-entry state) changes nothing while a chunk is one sub-block, and
+    must be caught by the closed-form pin as soon as it has several."""
+    def wrong(V1, V2, S1, S2, V1h, V2h, k, v, eta, beta, alpha, kind):
+        g1, g2 = O.inner_grad(V1[:, None], V2[:, None], k, v, kind)   # running state
+        for i in range(k.shape[1]):
+            V1, V2, S1, S2 = O.tnt_oracle._gated_step(V1, V2, S1, S2, g1[:, i], g2[:, i],
+                                                      eta[:, i], beta[:, i], alpha[:, i])
+        return V1, V2, S1, S2
+
+    monkeypatch.setattr(O.tnt_oracle, "_global_accumulate", wrong)
+    _global_closed_form_check("silu", 64, intra=False)       # one sub-block: still exact
+    with pytest.raises(AssertionError):
+        _global_closed_form_check("silu", 5, intra=False)
+
+
+# ---------------------------------------------------------------- intra-chunk global reading
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("block", [5, 64])
+def test_global_intra_closed_form(kind, block):
+    """Intra-chunk reading (Sec. 2.2 chunkwise retrieval applied to the global
+    memory), C_G = L: o_t = f(V_t, q_t) with V_t = A_t V_init - sum_{tau<=t}
+    c_{t,tau} u_tau(V_init) from explicit products."""
+    _global_closed_form_check(kind, block, intra=True)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_global_intra_chunk_one_is_per_token_rule(kind):
+    """C_G = 1 with the intra-chunk reading: update at the current state, then
+    read the updated state (the Sec. 2.1 per-token rule, no reset)."""
+    rng = np.random.default_rng(20)
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, 2, 20, 4, 6)
+    o, fin = O.global_memory(q, k, v, eta, beta, alpha, W1, W2, 1, kind, intra=True)
+    ref, rfin = O.sequential(q, k, v, eta, beta, alpha, W1, W2, kind)
+    assert (o - ref).abs().max() < 1e-12
+    for a, b in zip(fin, rfin):
+        assert (a - b).abs().max() < 1e-12
+
+
+def test_global_intra_is_an_unprojected_local_memory_without_reset():
+    """The intra-chunk global reading is the local rule with C_L = C_G, no
+    reset within the sequence (S_L = L) and no Q-K projection."""
+    rng = np.random.default_rng(21)
+    q, k, v, eta, beta, alpha, W1, W2 = _rand_chain(rng, 2, 48, 4, 6)
+    o, _ = O.global_memory(q, k, v, eta, beta, alpha, W1, W2, 12, "gelu", block=5, intra=True)
+    ref = O.local_memory(q, k, v, eta, beta, alpha, W1, W2, 12, 48, "gelu", qk_proj=False)
+    assert (o - ref).abs().max() < 1e-12
+
+
+def test_global_intra_layer_gradcheck():
+    """Autograd through the layer with the intra-chunk global reading matches
+    finite differences."""
+    cfg = _cfg(act=ACT_SILU, H=1, L=8, d=3, hid=4, C_G=4, locals_=((2, 4),), global_intra=1)
+    inp = make_inputs(cfg, 22)
+    g = O.gather_pairs(inp, O.all_pairs(cfg))
+    names = ("q", "k", "v", "lr", "mom", "decay", "W1", "W2")
+    leaves = tuple(g[n].clone().requires_grad_(True) for n in names)
+    dO = g["dO"]
+
+    def fn(*xs):
+        return (O.layer_forward(*xs, cfg) * dO).sum()
+
+    assert torch.autograd.gradcheck(fn, leaves, eps=1e-6, atol=1e-7, rtol=1e-6)
+    seg = O.layer_backward(*[g[n] for n in names], dO, cfg, ckpt=True)
+    one = O.layer_backward(*[g[n] for n in names], dO, cfg, ckpt=False)
+    for n in one:
+        assert (seg[n] - one[n]).abs().max() <= 1e-12 * max(1.0, one[n].abs().max().item()), n
