@@ -86,6 +86,11 @@ typedef struct {
   int32_t qk_scope;        /* TNT_QK_SHARD: M_t sums from the shard start (App. C);
                               TNT_QK_CHUNK: from the chunk start (retrieval box literal)    */
   int32_t dtype;           /* tnt_dtype of q, k, v, o, dO, dq, dk, dv                      */
+  int32_t global_intra;    /* retrieval of the global memory: 0 = at the chunk-entry state
+                              V_xi (Sec. 4.1.2 retrieval box; App. E); 1 = at V_t after
+                              token t's own update, the chunkwise retrieval rule of
+                              Sec. 2.2 applied to the global memory (gradients still at
+                              the chunk-entry state).  Ignored without a global memory.    */
 } tnt_config;
 
 /* Supported sizes: d in {16, 32, 64, 128}, hid in {16, 32, 64, 128, 256, 512},
@@ -102,44 +107,64 @@ typedef enum {
 /* Bytes of device workspace the call needs (0 if the config is invalid). */
 size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind);
 
-/* Bytes of the optional saved-state buffer: the chunk-entry states of every
- * memory (fp32, plus transposed copies of the local memories' states in the
- * compute type), written by tnt_mem_fwd and read by tnt_mem_bwd so that the
- * backward does not recompute the forward's state chain.  Opaque layout.  For
- * the local-memory shapes whose backward runs chunk-parallel from forward
- * records (also saved here), the backward reads the local states only through
- * their compute-type copies, and the forward leaves their fp32 slots unwritten
- * beyond a two-slot ring.  The environment switches TNT_GENERIC_KERNELS and
- * TNT_LOCAL_BWD_SINGLE (kernel selection for testing) make the forward write
- * every fp32 slot, which the kernels they select read: set them alike for a
- * tnt_mem_fwd and the tnt_mem_bwd that uses its buffer (the size and layout do
- * not depend on them); with them differing, that backward reads unwritten
- * slots (inside the buffer) and its results are undefined. */
+/* Kernel families.  TNT_FAMILY_DEFAULT takes the fixed-size kernels where a
+ * shape has them (the local backward in three passes); TNT_FAMILY_GENERIC
+ * runs every shape on the runtime-sized kernels; TNT_FAMILY_SINGLE_WALK keeps
+ * the fixed-size local backward in one reverse walk per unit.  All three
+ * compute the same function (to rounding); the non-default ones exist to test
+ * one family against another.  The family is process-wide. */
+typedef enum {
+  TNT_FAMILY_DEFAULT = 0,
+  TNT_FAMILY_GENERIC = 1,
+  TNT_FAMILY_SINGLE_WALK = 2
+} tnt_kernel_family;
+
+/* Selects the kernel family of later calls; returns the previous one, or -1
+ * (nothing changed) for an unknown value.  Sizes (tnt_mem_saved_size,
+ * tnt_mem_workspace_size) depend on the family: size buffers after choosing
+ * it.  A saved buffer can only be used by a tnt_mem_bwd under the family (and
+ * configuration) of the tnt_mem_fwd that wrote it (TNT_ERR_ARG otherwise). */
+int32_t tnt_set_kernel_family(int32_t family);
+
+/* Bytes of the optional saved-state buffer: a header, then the chunk-entry
+ * states of every memory (fp32, plus transposed copies of the local memories'
+ * states in the compute type) and, for the local shapes whose backward runs
+ * chunk-parallel, the forward records, written by tnt_mem_fwd and read by
+ * tnt_mem_bwd so that the backward does not recompute the forward.  Opaque
+ * layout.  For those shapes the backward reads the local states only through
+ * their compute-type copies, and only the forward walk's two-slot fp32 ring is
+ * reserved for them (the runtime-sized and single-walk families keep every
+ * fp32 slot).  The header records the configuration, the kernel family and
+ * the layout; tnt_mem_fwd also keeps that record per buffer on the host, and
+ * tnt_mem_bwd refuses (TNT_ERR_ARG, before enqueuing anything) a buffer that
+ * no tnt_mem_fwd of this process wrote for the same configuration and family. */
 size_t tnt_mem_saved_size(const tnt_config* cfg);
 
 /* Forward pass: o = TNT layer output (see the file comment).
  *   final_state : may be NULL; else receives the global memory's (V1, V2, S1, S2)
  *                 after the last token (requires has_global).
- *   saved       : may be NULL; else tnt_mem_saved_size bytes that receive the
+ *   saved       : may be NULL; else saved_bytes >= tnt_mem_saved_size(cfg)
+ *                 (TNT_ERR_WORKSPACE otherwise) that receive the header and the
  *                 chunk-entry states for a later tnt_mem_bwd.
  *   workspace   : ws_bytes >= tnt_mem_workspace_size(cfg, TNT_WS_FWD). */
 tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
                        const float* lr, const float* mom, const float* decay,
                        const float* W1_init, const float* W2_init, void* o,
-                       float* final_state, void* saved, void* workspace, size_t ws_bytes,
-                       void* stream);
+                       float* final_state, void* saved, size_t saved_bytes, void* workspace,
+                       size_t ws_bytes, void* stream);
 
 /* Backward pass: gradients of sum(dO * o) with respect to every input of the
  * forward, exact (second-order terms through the inner gradient included).
- *   saved : the buffer filled by tnt_mem_fwd on the same inputs, or NULL to
+ *   saved : the buffer filled by tnt_mem_fwd on the same inputs (same
+ *           configuration and kernel family; TNT_ERR_ARG otherwise), or NULL to
  *           recompute the states (then ws_bytes must cover TNT_WS_BWD_RECOMPUTE).
  * dq, dk, dv have the I/O dtype; the others are fp32 in the layouts above. */
 tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
                        const float* lr, const float* mom, const float* decay,
                        const float* W1_init, const float* W2_init, const void* dO,
-                       const void* saved, void* dq, void* dk, void* dv, float* dlr,
-                       float* dmom, float* ddecay, float* dW1_init, float* dW2_init,
-                       void* workspace, size_t ws_bytes, void* stream);
+                       const void* saved, size_t saved_bytes, void* dq, void* dk, void* dv,
+                       float* dlr, float* dmom, float* ddecay, float* dW1_init,
+                       float* dW2_init, void* workspace, size_t ws_bytes, void* stream);
 
 /* ---- Step-wise forward (prefill / decode) from a carried state ----------
  * Within a chunk every gradient is taken at the chunk-entry weights W^ and

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -11,6 +12,7 @@
 #include <vector>
 
 #include "../../include/tnt.h"
+#include "tnt_entry.h"
 #include "tnt_kernels.h"
 #include "tnt_local_bwd_layout.h"
 #include "tnt_local_record.h"
@@ -33,7 +35,8 @@ bool one_of(int x, std::initializer_list<int> v) {
 tnt_status validate(const tnt_config* c, bool need_L = true) {
   if (!c) return TNT_ERR_NULL;
   if (c->act < 0 || c->act > 1 || c->qk_proj < 0 || c->qk_proj > 1 || c->qk_scope < 0 ||
-      c->qk_scope > 1 || c->dtype < 0 || c->dtype > 1 || c->has_global < 0 || c->has_global > 1)
+      c->qk_scope > 1 || c->dtype < 0 || c->dtype > 1 || c->has_global < 0 || c->has_global > 1 ||
+      c->global_intra < 0 || c->global_intra > 1)
     return TNT_ERR_ARG;
   if (c->B <= 0 || c->H <= 0 || (need_L && c->L <= 0) || c->d <= 0 || c->hid <= 0)
     return TNT_ERR_SHAPE;
@@ -86,8 +89,11 @@ struct Layout {
   BwdLayout blay[TNT_MAX_LOCAL];
 };
 
-int generic_only();
-int single_walk_only();
+// Kernel family (tnt_set_kernel_family): which of the kernel families the
+// calls take; fixed per saved buffer (recorded in its header).
+std::atomic<int> g_family{TNT_FAMILY_DEFAULT};
+int generic_only() { return g_family.load() == TNT_FAMILY_GENERIC ? 1 : 0; }
+int single_walk_only() { return g_family.load() == TNT_FAMILY_SINGLE_WALK ? 1 : 0; }
 
 Layout layout_of(const tnt_config* c) {
   Layout y{};
@@ -100,8 +106,8 @@ Layout layout_of(const tnt_config* c) {
   const size_t f = sizeof(float);
   const size_t dd = (size_t)c->d * c->d;
 
-  // saved states
-  size_t off = 0;
+  // saved states, behind the buffer's header
+  size_t off = SAVED_HEADER_BYTES;
   if (c->has_global) {
     y.g_chunks = c->L / c->C_G;
     y.sv_g = off;
@@ -112,14 +118,15 @@ Layout layout_of(const tnt_config* c) {
     y.l_chunks[i] = c->S_L[i] / c->C_L[i];
     // Shapes with both chunk-parallel kernels save forward records, and their
     // backward reads the states only through the compute-type transposes: the
-    // walk then cycles its fp32 carry through two slots instead of writing every
-    // slot (unless a switch asks for the kernels that recompute from the fp32
-    // states).  The space stays reserved, so the layout does not depend on it.
+    // walk then cycles its fp32 carry through two slots per unit instead of
+    // writing every slot, and only those two are reserved.  The families that
+    // recompute from the fp32 states (one-walk, runtime-sized) keep every slot.
     const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
     const bool recs = local_fwd_split_bytes(D, y.l_units[i]) && local_bwd_split_bytes(D, y.l_units[i]);
     y.l_fslots[i] = (recs && !single_walk_only() && !generic_only()) ? 2 : 0;
     y.sv_l[i] = off;
-    off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * 4 * y.hd * f);
+    off += up((size_t)y.l_units[i] * (y.l_fslots[i] ? y.l_fslots[i] : y.l_chunks[i] + 1) * 4 *
+              y.hd * f);
     y.sv_m[i] = off;
     off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * dd * f);
     y.sv_t[i] = off;  // CT transposes of every slot, written by the forward
@@ -203,18 +210,58 @@ Layout layout_of(const tnt_config* c) {
 
 bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
 
-// TNT_GENERIC_KERNELS=1 in the environment routes every shape through the
-// runtime-sized kernels (used by the tests to cover both kernel families).
-int generic_only() {
-  const char* e = std::getenv("TNT_GENERIC_KERNELS");
-  return (e && e[0] == '1') ? 1 : 0;
+// ---- the saved buffer's header: what wrote it and for which call.  The
+// forward writes it into the first SAVED_HEADER_BYTES of `saved` (device) and
+// records it per buffer on the host; the backward compares the host record
+// with its own call before it enqueues anything.
+uint64_t config_hash(const tnt_config* c) {
+  tnt_config n = *c;  // entries the call does not use do not count
+  for (int i = n.n_local; i < TNT_MAX_LOCAL; ++i) n.C_L[i] = n.S_L[i] = 0;
+  if (!n.has_global) n.C_G = n.global_intra = 0;
+  uint64_t h = 1469598103934665603ull;  // FNV-1a over the configuration's bytes
+  const unsigned char* p = (const unsigned char*)&n;
+  for (size_t i = 0; i < sizeof(tnt_config); ++i) h = (h ^ p[i]) * 1099511628211ull;
+  return h;
 }
 
-// TNT_LOCAL_BWD_SINGLE=1 keeps the local backward in one reverse walk per unit
-// (the single-walk fixed-size kernel) instead of the three-pass kernels.
-int single_walk_only() {
-  const char* e = std::getenv("TNT_LOCAL_BWD_SINGLE");
-  return (e && e[0] == '1') ? 1 : 0;
+SavedHeader header_of(const tnt_config* c, const Layout& y) {
+  SavedHeader h{};
+  h.magic = SAVED_MAGIC;
+  h.layout_version = SAVED_LAYOUT_VERSION;
+  h.family = (uint32_t)g_family.load();
+  for (int i = 0; i < TNT_MAX_LOCAL; ++i) h.fslots[i] = i < c->n_local ? (uint32_t)y.l_fslots[i] : 0;
+  h.cfg_hash = config_hash(c);
+  h.bytes = y.saved_bytes;
+  return h;
+}
+
+bool same_header(const SavedHeader& a, const SavedHeader& b) {
+  return std::memcmp(&a, &b, sizeof(SavedHeader)) == 0;
+}
+
+std::mutex g_saved_mu;
+std::vector<std::pair<const void*, SavedHeader>> g_saved;  // most recent last
+constexpr size_t SAVED_RECORDS = 4096;
+
+void remember_saved(const void* p, const SavedHeader& h) {
+  std::lock_guard<std::mutex> lk(g_saved_mu);
+  for (size_t i = 0; i < g_saved.size(); ++i)
+    if (g_saved[i].first == p) {
+      g_saved.erase(g_saved.begin() + i);
+      break;
+    }
+  if (g_saved.size() >= SAVED_RECORDS) g_saved.erase(g_saved.begin());
+  g_saved.emplace_back(p, h);
+}
+
+bool recorded_saved(const void* p, SavedHeader* out) {
+  std::lock_guard<std::mutex> lk(g_saved_mu);
+  for (size_t i = g_saved.size(); i-- > 0;)
+    if (g_saved[i].first == p) {
+      *out = g_saved[i].second;
+      return true;
+    }
+  return false;
 }
 
 // ---- opt-in launch timing (hipEvent pairs per launch)
@@ -290,17 +337,18 @@ hipError_t fork_of(Fork** out) {
 
 // forward pass into a given state area (`sv` = saved buffer, or nullptr to use
 // the two-slot rings in the workspace)
+// `fork`: false keeps every launch on `st` (no helper stream is created or used).
 tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, const void* k,
                        const void* v, const float* lr, const float* mom, const float* decay,
                        const float* W1i, const float* W2i, void* o, float* final_state,
-                       char* sv, char* ws, hipStream_t st) {
+                       char* sv, char* ws, hipStream_t st, bool fork = true) {
   const size_t G = y.gates;
   float* opart = (float*)(ws + y.w_opart);
   int m = 0;
   std::unique_lock<std::mutex> lock(g_fork_mu);
   Fork* fk = nullptr;
   const hipStream_t main_st = st;
-  if (c->has_global && c->n_local) {
+  if (fork && c->has_global && c->n_local) {
     HIP_TRY(fork_of(&fk));
     HIP_TRY(hipEventRecord(fk->e0, main_st));
     HIP_TRY(hipStreamWaitEvent(fk->side, fk->e0, 0));
@@ -509,7 +557,12 @@ void section_end(int handle, hipStream_t st) {
 
 extern "C" {
 
-int32_t tnt_abi_version(void) { return 1; }
+int32_t tnt_abi_version(void) { return 2; }
+
+int32_t tnt_set_kernel_family(int32_t family) {
+  if (family < TNT_FAMILY_DEFAULT || family > TNT_FAMILY_SINGLE_WALK) return -1;
+  return g_family.exchange(family);
+}
 
 int32_t tnt_timing_enable(int32_t on) {
   const int32_t prev = g_timing.on ? 1 : 0;
@@ -583,7 +636,19 @@ size_t tnt_mem_saved_size(const tnt_config* cfg) {
 tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
                        const float* lr, const float* mom, const float* decay,
                        const float* W1_init, const float* W2_init, void* o, float* final_state,
-                       void* saved, void* workspace, size_t ws_bytes, void* stream) {
+                       void* saved, size_t saved_bytes, void* workspace, size_t ws_bytes,
+                       void* stream) {
+  return tnt::forward_entry(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
+                            saved, saved_bytes, workspace, ws_bytes, true, (hipStream_t)stream);
+}
+}  // extern "C"
+
+namespace tnt {
+tnt_status forward_entry(const tnt_config* cfg, const void* q, const void* k, const void* v,
+                         const float* lr, const float* mom, const float* decay,
+                         const float* W1_init, const float* W2_init, void* o,
+                         float* final_state, void* saved, size_t saved_bytes, void* workspace,
+                         size_t ws_bytes, bool fork, hipStream_t stream) {
   tnt_status s = validate(cfg);
   if (s != TNT_OK) return s;
   if (!q || !k || !v || !lr || !mom || !decay || !W1_init || !W2_init || !o || !workspace)
@@ -596,16 +661,25 @@ tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, cons
     if (p && misaligned(p)) return TNT_ERR_ALIGN;
   const Layout y = layout_of(cfg);
   if (ws_bytes < y.fwd_bytes) return TNT_ERR_WORKSPACE;
-  return run_forward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
-                     (char*)saved, (char*)workspace, (hipStream_t)stream);
+  if (saved && saved_bytes < y.saved_bytes) return TNT_ERR_WORKSPACE;
+  const SavedHeader hdr = header_of(cfg, y);
+  s = run_forward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
+                  (char*)saved, (char*)workspace, stream, fork);
+  if (s != TNT_OK || !saved) return s;
+  if (launch_write_header(saved, hdr, stream) != hipSuccess) return TNT_ERR_HIP;
+  remember_saved(saved, hdr);
+  return TNT_OK;
 }
+}  // namespace tnt
+
+extern "C" {
 
 tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
                        const float* lr, const float* mom, const float* decay,
                        const float* W1_init, const float* W2_init, const void* dO,
-                       const void* saved, void* dq, void* dk, void* dv, float* dlr, float* dmom,
-                       float* ddecay, float* dW1_init, float* dW2_init, void* workspace,
-                       size_t ws_bytes, void* stream) {
+                       const void* saved, size_t saved_bytes, void* dq, void* dk, void* dv,
+                       float* dlr, float* dmom, float* ddecay, float* dW1_init,
+                       float* dW2_init, void* workspace, size_t ws_bytes, void* stream) {
   tnt_status s = validate(cfg);
   if (s != TNT_OK) return s;
   if (!q || !k || !v || !lr || !mom || !decay || !W1_init || !W2_init || !dO || !dq || !dk ||
@@ -620,6 +694,13 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
     if (p && misaligned(p)) return TNT_ERR_ALIGN;
   const Layout y = layout_of(cfg);
   if (ws_bytes < (saved ? y.bwd_bytes : y.bwd_re_bytes)) return TNT_ERR_WORKSPACE;
+  if (saved) {
+    // the buffer must hold what a forward of this very configuration and
+    // kernel family wrote (its layout and which slots were written depend on both)
+    SavedHeader rec{};
+    if (!recorded_saved(saved, &rec) || !same_header(rec, header_of(cfg, y))) return TNT_ERR_ARG;
+    if (saved_bytes < y.saved_bytes) return TNT_ERR_WORKSPACE;
+  }
   char* ws = (char*)workspace;
   char* sv = saved ? (char*)saved : ws + y.b_states;
   hipStream_t st = (hipStream_t)stream;

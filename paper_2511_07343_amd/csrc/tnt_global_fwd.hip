@@ -489,4 +489,17 @@ hipError_t launch_copy_final(const float* states, int nslots, int nchains, size_
   return hipGetLastError();
 }
 
+// The saved buffer's header, one 4-byte word per thread.
+__global__ void write_header_kernel(uint32_t* dst, SavedHeader h) {
+  constexpr int W = (int)(sizeof(SavedHeader) / 4);
+  static_assert(sizeof(SavedHeader) % 4 == 0, "whole words");
+  const int i = threadIdx.x;
+  if (i < W) dst[i] = reinterpret_cast<const uint32_t*>(&h)[i];
+}
+
+hipError_t launch_write_header(void* dst, const SavedHeader& h, hipStream_t st) {
+  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, st, (uint32_t*)dst, h);
+  return hipGetLastError();
+}
+
 }  // namespace tnt

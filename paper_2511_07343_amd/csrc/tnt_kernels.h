@@ -8,6 +8,19 @@
 
 namespace tnt {
 
+// Header at the start of a saved buffer (tnt_mem_fwd -> tnt_mem_bwd): which
+// layout, kernel family, ring sizes and configuration wrote it.
+constexpr uint32_t SAVED_MAGIC = 0x544e5453u;  // "STNT"
+constexpr uint32_t SAVED_LAYOUT_VERSION = 2;
+constexpr size_t SAVED_HEADER_BYTES = 256;
+struct SavedHeader {
+  uint32_t magic, layout_version, family, pad;
+  uint32_t fslots[4];
+  uint64_t cfg_hash, bytes;
+};
+static_assert(sizeof(SavedHeader) <= SAVED_HEADER_BYTES, "header fits its reserved bytes");
+hipError_t launch_write_header(void* dst, const SavedHeader& h, hipStream_t st);
+
 // Sizes of one memory's pass, shared by every kernel.
 struct Dims {
   int B, H, L, d, hid;
@@ -45,9 +58,10 @@ struct LocalFwdArgs {
   void* frec; float* frec_f;                             // null, or the forward records (saved
                                                          // buffer) the backward passes read
   int nslots;
-  int fslots;                                            // 0: the walk writes every fp32 slot;
-                                                         // else it cycles through the first
-                                                         // fslots of each unit's nslots (the
+  int fslots;                                            // 0: the walk writes every fp32 slot
+                                                         // ([units][nslots][4*hid*d]); else
+                                                         // `states` is [units][fslots][4*hid*d],
+                                                         // a ring the walk cycles through (the
                                                          // backward then reads only statesT)
   void* scratch;                                         // units * plan.elems CT
   LocalPlan plan;

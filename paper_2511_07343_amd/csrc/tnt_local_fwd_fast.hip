@@ -138,7 +138,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const float* mom = a.mom + chain * Dm.L;
   const float* dec = a.decay + chain * Dm.L;
   const int fsl = a.fslots ? a.fslots : a.nslots;  // fp32 state slots the walk cycles through
-  float* st = a.states + (size_t)u * a.nslots * 4 * hd;
+  float* st = a.states + (size_t)u * fsl * 4 * hd;
   float* mst = a.mstates + (size_t)u * a.nslots * D * D;
   constexpr size_t PS = 4 * hd + (size_t)D * D;  // CT elements per transposed slot
   CT* const pku = a.statesT ? (CT*)a.statesT + (size_t)u * a.nslots * PS : nullptr;

@@ -25,7 +25,8 @@ STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPP
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
             "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read",
             "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step", "tnt_mem_state_from_fwd",
-            "tnt_dbg_chunk_grads"]
+            "tnt_dbg_chunk_grads", "tnt_set_kernel_family"]
+FAMILY_DEFAULT, FAMILY_GENERIC, FAMILY_SINGLE_WALK = 0, 1, 2
 
 
 class TntError(RuntimeError):
@@ -41,7 +42,8 @@ class tnt_config(ctypes.Structure):
                 ("n_local", ctypes.c_int32),
                 ("C_L", ctypes.c_int32 * TNT_MAX_LOCAL), ("S_L", ctypes.c_int32 * TNT_MAX_LOCAL),
                 ("act", ctypes.c_int32), ("qk_proj", ctypes.c_int32),
-                ("qk_scope", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("qk_scope", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("global_intra", ctypes.c_int32)]
 
 
 def lib(path: Optional[str] = None) -> ctypes.CDLL:
@@ -59,9 +61,9 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_mem_workspace_size.restype = sz
     L.tnt_mem_saved_size.argtypes = [cp]
     L.tnt_mem_saved_size.restype = sz
-    L.tnt_mem_fwd.argtypes = [cp] + [vp] * 12 + [sz, vp]
+    L.tnt_mem_fwd.argtypes = [cp] + [vp] * 11 + [sz, vp, sz, vp]
     L.tnt_mem_fwd.restype = ctypes.c_int
-    L.tnt_mem_bwd.argtypes = [cp] + [vp] * 19 + [sz, vp]
+    L.tnt_mem_bwd.argtypes = [cp] + [vp] * 10 + [sz] + [vp] * 9 + [sz, vp]
     L.tnt_mem_bwd.restype = ctypes.c_int
     L.tnt_mem_state_size.argtypes = [cp]
     L.tnt_mem_state_size.restype = sz
@@ -77,6 +79,8 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_strerror.restype = ctypes.c_char_p
     L.tnt_abi_version.argtypes = []
     L.tnt_abi_version.restype = i32
+    L.tnt_set_kernel_family.argtypes = [i32]
+    L.tnt_set_kernel_family.restype = i32
     L.tnt_timing_enable.argtypes = [i32]
     L.tnt_timing_enable.restype = i32
     L.tnt_timing_read.argtypes = [i32, ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -94,6 +98,7 @@ def to_c(cfg: LayerConfig) -> tnt_config:
     for i, (cl, sl) in enumerate(cfg.locals_):
         c.C_L[i], c.S_L[i] = cl, sl
     c.act, c.qk_proj, c.qk_scope, c.dtype = cfg.act, cfg.qk_proj, cfg.qk_scope, cfg.dtype
+    c.global_intra = getattr(cfg, "global_intra", 0)
     return c
 
 
@@ -123,23 +128,57 @@ def tnt_mem_saved_size(cfg: LayerConfig) -> int:
     return lib().tnt_mem_saved_size(ctypes.byref(to_c(cfg)))
 
 
+def _nbytes(t, given):
+    if given is not None:
+        return given
+    if t is None or isinstance(t, int):
+        return 0
+    return t.numel() * t.element_size()
+
+
 def tnt_mem_fwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state, saved,
-                workspace, ws_bytes=None, stream=None) -> int:
-    ws_bytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+                workspace, ws_bytes=None, stream=None, saved_bytes=None) -> int:
+    ws_bytes = _nbytes(workspace, ws_bytes)
     c = to_c(cfg)
     return lib().tnt_mem_fwd(ctypes.byref(c), _p(q), _p(k), _p(v), _p(lr), _p(mom), _p(decay),
                              _p(W1_init), _p(W2_init), _p(o), _p(final_state), _p(saved),
-                             _p(workspace), ws_bytes, _stream(stream))
+                             _nbytes(saved, saved_bytes), _p(workspace), ws_bytes,
+                             _stream(stream))
 
 
 def tnt_mem_bwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, dO, saved, dq, dk, dv, dlr,
-                dmom, ddecay, dW1_init, dW2_init, workspace, ws_bytes=None, stream=None) -> int:
-    ws_bytes = workspace.numel() * workspace.element_size() if ws_bytes is None else ws_bytes
+                dmom, ddecay, dW1_init, dW2_init, workspace, ws_bytes=None, stream=None,
+                saved_bytes=None) -> int:
+    ws_bytes = _nbytes(workspace, ws_bytes)
     c = to_c(cfg)
     return lib().tnt_mem_bwd(ctypes.byref(c), _p(q), _p(k), _p(v), _p(lr), _p(mom), _p(decay),
-                             _p(W1_init), _p(W2_init), _p(dO), _p(saved), _p(dq), _p(dk),
-                             _p(dv), _p(dlr), _p(dmom), _p(ddecay), _p(dW1_init),
-                             _p(dW2_init), _p(workspace), ws_bytes, _stream(stream))
+                             _p(W1_init), _p(W2_init), _p(dO), _p(saved),
+                             _nbytes(saved, saved_bytes), _p(dq), _p(dk), _p(dv), _p(dlr),
+                             _p(dmom), _p(ddecay), _p(dW1_init), _p(dW2_init), _p(workspace),
+                             ws_bytes, _stream(stream))
+
+
+def tnt_set_kernel_family(family: int) -> int:
+    return lib().tnt_set_kernel_family(family)
+
+
+class kernel_family:
+    """Context manager: run the enclosed calls under another kernel family
+    (tnt_set_kernel_family), restoring the previous one on exit."""
+
+    def __init__(self, family: int):
+        self.family = family
+        self.prev = None
+
+    def __enter__(self):
+        self.prev = tnt_set_kernel_family(self.family)
+        if self.prev < 0:
+            raise ValueError(f"unknown kernel family {self.family}")
+        return self
+
+    def __exit__(self, *exc):
+        tnt_set_kernel_family(self.prev)
+        return False
 
 
 def tnt_mem_state_size(cfg: LayerConfig) -> int:

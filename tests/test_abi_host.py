@@ -45,7 +45,7 @@ def test_binding_argument_counts_match_header():
 
 
 def test_abi_version():
-    assert tnt.lib().tnt_abi_version() == 1
+    assert tnt.lib().tnt_abi_version() == 2
 
 
 def test_strerror_names():
@@ -78,6 +78,7 @@ def _fwd_status(cfg, ptr=256, ws=1 << 40):
     (dict(qk_scope=2), 7),
     (dict(B=0), 2),
     (dict(has_global=0, locals_=()), 2),
+    (dict(global_intra=2), 7),
 ])
 def test_validation_codes(bad, code):
     cfg = small_config(L=64, C_G=16, locals_=((8, 32),)).replace(**bad)
@@ -91,8 +92,50 @@ def test_null_and_alignment_and_workspace():
     assert _fwd_status(cfg, ws=16) == 4
     # final_state without a global memory is a shape error
     c = tnt.to_c(cfg.replace(has_global=0))
-    st = tnt.lib().tnt_mem_fwd(ctypes.byref(c), *([256] * 9), 256, None, 256, 1 << 40, None)
+    st = tnt.lib().tnt_mem_fwd(ctypes.byref(c), *([256] * 9), 256, None, 0, 256, 1 << 40, None)
     assert st == 2
+
+
+def test_saved_buffer_size_and_record_checked_before_launch():
+    """A saved buffer smaller than tnt_mem_saved_size is refused by the
+    forward (TNT_ERR_WORKSPACE); a backward given a buffer that no forward of
+    this process wrote for this configuration and kernel family is refused
+    (TNT_ERR_ARG).  Both before anything is enqueued (no GPU here)."""
+    cfg = small_config(L=64, C_G=16, locals_=((8, 32),))
+    p = 256
+    need = tnt.tnt_mem_saved_size(cfg)
+    st = tnt.tnt_mem_fwd(cfg, p, p, p, p, p, p, p, p, p, None, p, p, ws_bytes=1 << 40, stream=0,
+                         saved_bytes=need - 16)
+    assert st == 4
+    args = [p] * 10
+    st = tnt.tnt_mem_bwd(cfg, *args[:9], 4096, *([p] * 8), p, ws_bytes=1 << 40, stream=0,
+                         saved_bytes=need)
+    assert st == 7
+
+
+def test_kernel_family_setting():
+    assert tnt.tnt_set_kernel_family(-1) == -1
+    assert tnt.tnt_set_kernel_family(3) == -1
+    prev = tnt.tnt_set_kernel_family(tnt.FAMILY_GENERIC)
+    assert prev == tnt.FAMILY_DEFAULT
+    assert tnt.tnt_set_kernel_family(prev) == tnt.FAMILY_GENERIC
+
+
+def test_saved_size_reserves_only_the_fp32_ring():
+    """At the pre-training workload the default family's local walk keeps its
+    fp32 carry in a two-slot ring per unit (the backward reads the compute-type
+    copies), so the saved buffer reserves two fp32 slots per unit instead of one
+    per chunk boundary: 128 units x 31 slots x 256 KB less than the families
+    that read every fp32 slot."""
+    cfg = WORKLOADS[2]
+    small = tnt.tnt_mem_saved_size(cfg)
+    with tnt.kernel_family(tnt.FAMILY_SINGLE_WALK):
+        full = tnt.tnt_mem_saved_size(cfg)
+    units = cfg.B * cfg.H * (cfg.L // cfg.locals_[0][1])
+    chunks = cfg.locals_[0][1] // cfg.locals_[0][0]
+    slot = 4 * cfg.hid * cfg.d * 4
+    assert full - small == units * (chunks + 1 - 2) * slot
+    assert full - small > 1.0e9
 
 
 # ---------------------------------------------------------------- step-wise entry points

@@ -11,6 +11,7 @@ import oracle as O
 from paper_2511_07343_amd import tnt
 from paper_2511_07343_amd.inputs import (ACT_GELU, ACT_SILU, BF16, F32, QK_CHUNK, WORKLOADS,
                                          make_inputs, max_rel_err, small_config)
+from parity_log import check_err
 
 pytestmark = pytest.mark.gpu
 torch.set_num_threads(4)
@@ -59,12 +60,12 @@ def test_forward_small_all_chains(cfg):
     ref = ref.numpy().reshape(cfg.B, cfg.H, cfg.L, cfg.d)
     err = max_rel_err(got, ref)
     print(f"o max rel err {err:.3e}", flush=True)
-    assert err <= tol(cfg)
+    assert check_err(f"fwd {cfg.name}", "o", err, tol(cfg))
     if cfg.has_global:
         rf = np.stack([r.numpy().reshape(len(pairs), -1) for r in rfin], 1)
         e2 = max_rel_err(fin.reshape(len(pairs), 4, -1), rf)
         print(f"final state max rel err {e2:.3e}", flush=True)
-        assert e2 <= tol(cfg)
+        assert check_err(f"fwd {cfg.name}", "final_state", e2, tol(cfg))
 
 
 SAVE_RING = [
@@ -88,15 +89,15 @@ def test_forward_save_and_ring_agree(cfg):
 
 
 @pytest.mark.parametrize("cfg", SAVE_RING[2:], ids=lambda c: c.name)
-def test_forward_state_ring_agrees(cfg, monkeypatch):
+def test_forward_state_ring_agrees(cfg):
     """With forward records saved, the walk cycles its fp32 carry through two
-    slots; a kernel-selection switch makes it write every slot instead.  The
-    outputs are the same bits either way."""
+    slots; the single-walk kernel family makes it write every slot instead.
+    The outputs are the same bits either way."""
     inp = make_inputs(cfg, 106)
     print(f"\n[case] state ring {cfg.name}", flush=True)
     a, _ = gpu_forward(cfg, inp, save=True)
-    monkeypatch.setenv("TNT_LOCAL_BWD_SINGLE", "1")
-    b, _ = gpu_forward(cfg, inp, save=True)
+    with tnt.kernel_family(tnt.FAMILY_SINGLE_WALK):
+        b, _ = gpu_forward(cfg, inp, save=True)
     assert np.array_equal(a, b)
 
 
@@ -141,18 +142,19 @@ def test_forward_full_size_sampled_chain(idx):
     ref = O.forward_pairs(inp, cfg, [(b, h)]).numpy()[0]
     err = max_rel_err(got[b, h], ref)
     print(f"chain ({b},{h}) o max rel err {err:.3e}", flush=True)
-    assert err <= tol(cfg)
+    assert check_err(f"fwd full-size chain w{idx}", "o", err, tol(cfg))
 
 
 @pytest.mark.parametrize("cfg", [WORKLOADS[0], SMALL[0], SMALL[2], SMALL[4]], ids=lambda c: c.name)
-def test_forward_generic_kernels(cfg, monkeypatch):
+def test_forward_generic_kernels(cfg):
     """The runtime-sized kernels (used for shapes without a fixed-size kernel)
     against the oracle, and against the fixed-size kernels where both exist."""
     inp = make_inputs(cfg, 105)
     fast, _ = gpu_forward(cfg, inp)
-    monkeypatch.setenv("TNT_GENERIC_KERNELS", "1")
-    gen, _ = gpu_forward(cfg, inp)
+    with tnt.kernel_family(tnt.FAMILY_GENERIC):
+        gen, _ = gpu_forward(cfg, inp)
     ref = O.forward_pairs(inp, cfg, O.all_pairs(cfg)).numpy().reshape(gen.shape)
     e_gen, e_fast = max_rel_err(gen, ref), max_rel_err(fast, ref)
     print(f"\n[case] {cfg.name}: generic {e_gen:.3e} fixed-size {e_fast:.3e}", flush=True)
-    assert e_gen <= tol(cfg) and e_fast <= tol(cfg)
+    ok_gen = check_err(f"fwd generic {cfg.name}", "o", e_gen, tol(cfg))
+    assert check_err(f"fwd {cfg.name} (2)", "o", e_fast, tol(cfg)) and ok_gen
