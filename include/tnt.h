@@ -166,6 +166,25 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
                        float* dlr, float* dmom, float* ddecay, float* dW1_init,
                        float* dW2_init, void* workspace, size_t ws_bytes, void* stream);
 
+/* ---- Forward pass without a caller-provided workspace --------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the forward
+ * of tnt_mem_fwd with no workspace and no saved buffer arguments.  Its
+ * workspace is a device array of TNT_NOALLOC_WORKSPACE_BYTES that the library
+ * holds on each GPU it runs on from the first call there until the process
+ * ends; configurations whose forward workspace (tnt_mem_workspace_size(cfg,
+ * TNT_WS_FWD)) is larger get TNT_ERR_WORKSPACE.  The call allocates nothing
+ * (no hipMalloc / hipFree, no helper stream: every launch is on `stream`), and
+ * the forward writes every part of that array it reads, so the previous
+ * call's contents do not matter.  All calls on one GPU share the array: calls
+ * that overlap on one GPU (other streams, other host threads) race, and the
+ * caller must serialise them.  Results equal tnt_mem_fwd's (same kernels). */
+#define TNT_NOALLOC_WORKSPACE_BYTES (128u << 20)
+tnt_status tnt_mem_fwd_noalloc(const tnt_config* cfg, const void* q, const void* k,
+                               const void* v, const float* lr, const float* mom,
+                               const float* decay, const float* W1_init, const float* W2_init,
+                               void* o, float* final_state, void* stream);
+
 /* ---- Step-wise forward (prefill / decode) from a carried state ----------
  * Within a chunk every gradient is taken at the chunk-entry weights W^ and
  * folded in with momentum and decay (Sec. 2.2; App. D), so the chunkwise rule

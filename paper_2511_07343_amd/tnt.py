@@ -25,7 +25,8 @@ STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPP
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",
             "tnt_strerror", "tnt_abi_version", "tnt_timing_enable", "tnt_timing_read",
             "tnt_mem_state_size", "tnt_mem_state_init", "tnt_mem_step", "tnt_mem_state_from_fwd",
-            "tnt_dbg_chunk_grads", "tnt_set_kernel_family"]
+            "tnt_dbg_chunk_grads", "tnt_set_kernel_family", "tnt_mem_fwd_noalloc"]
+NOALLOC_WORKSPACE_BYTES = 128 << 20
 FAMILY_DEFAULT, FAMILY_GENERIC, FAMILY_SINGLE_WALK = 0, 1, 2
 
 
@@ -79,6 +80,8 @@ def lib(path: Optional[str] = None) -> ctypes.CDLL:
     L.tnt_strerror.restype = ctypes.c_char_p
     L.tnt_abi_version.argtypes = []
     L.tnt_abi_version.restype = i32
+    L.tnt_mem_fwd_noalloc.argtypes = [cp] + [vp] * 11
+    L.tnt_mem_fwd_noalloc.restype = ctypes.c_int
     L.tnt_set_kernel_family.argtypes = [i32]
     L.tnt_set_kernel_family.restype = i32
     L.tnt_timing_enable.argtypes = [i32]
@@ -156,6 +159,14 @@ def tnt_mem_bwd(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, dO, saved, dq, d
                              _nbytes(saved, saved_bytes), _p(dq), _p(dk), _p(dv), _p(dlr),
                              _p(dmom), _p(ddecay), _p(dW1_init), _p(dW2_init), _p(workspace),
                              ws_bytes, _stream(stream))
+
+
+def tnt_mem_fwd_noalloc(cfg, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
+                        stream=None) -> int:
+    c = to_c(cfg)
+    return lib().tnt_mem_fwd_noalloc(ctypes.byref(c), _p(q), _p(k), _p(v), _p(lr), _p(mom),
+                                     _p(decay), _p(W1_init), _p(W2_init), _p(o),
+                                     _p(final_state), _stream(stream))
 
 
 def tnt_set_kernel_family(family: int) -> int:
