@@ -60,11 +60,19 @@ enum { ACT_GELU = 0, ACT_SILU = 1 };
 
 struct ActVals { float s, d1, d2; };  // sigma(z), sigma'(z), sigma''(z)
 
+// The logistic function from the hardware exponential and reciprocal
+// (v_exp_f32, v_rcp_f32: about 1 ulp each), not the correctly rounded library
+// forms: every value it feeds is rounded to bf16 or summed in fp32 next.  For
+// z below about -88 the exponential overflows to +inf and the reciprocal
+// gives 0, the limit.
+__device__ __forceinline__ float sigmoid_fast(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+}
+
 template <int ACT>
 __device__ __forceinline__ float act_f(float z) {
   if (ACT == ACT_GELU) return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
-  float sg = 1.0f / (1.0f + expf(-z));
-  return z * sg;
+  return z * sigmoid_fast(z);
 }
 
 template <int ACT>
@@ -77,7 +85,7 @@ __device__ __forceinline__ ActVals act_all(float z) {
     r.d1 = cdf + z * pdf;
     r.d2 = pdf * (2.0f - z * z);
   } else {
-    float sg = 1.0f / (1.0f + expf(-z));
+    float sg = sigmoid_fast(z);
     r.s = z * sg;
     r.d1 = sg * (1.0f + z * (1.0f - sg));
     r.d2 = sg * (1.0f - sg) * (2.0f + z * (1.0f - 2.0f * sg));

@@ -23,47 +23,6 @@
 
 namespace tnt {
 
-// The carry's coefficients only (cC, b, A_C, B_C, E_C), without the C x C
-// matrix: cC_t = eta_t y_t with y_t = sum_{m >= t} e^{(la_C - la_m) + (lb_m - lb_t)}
-// obeys y_t = e^{la_C - la_t} + e^{lb_{t+1} - lb_t} y_{t+1}, a suffix affine scan
-// over the lanes whose terms and multipliers are all at most 1.  One wave;
-// ends with a barrier.  Overwrites those fields of `cf` (the walk and the
-// one-walk kernel both take the carry from here, so their states agree bitwise).
-__device__ __forceinline__ void carry_coefs(CoefF& cf, const float* lr, const float* mom,
-                                            const float* dec, int tok0, int C, int Cp) {
-  if (wave_id() == 0) {
-    const int i = lane_id();
-    const bool in = i < C;
-    const float eta = in ? lr[tok0 + i] : 0.f;
-    const float lmb = in ? log_mom(mom[tok0 + i]) : 0.f;
-    const float lka = in ? log_keep(dec[tok0 + i]) : 0.f;
-    const float la = wave_incl_sum(lka), lb = wave_incl_sum(lmb);
-    const float laC = __shfl(la, C - 1, WAVE), lbC = __shfl(lb, C - 1, WAVE);
-    const float lbn = __shfl_down(lb, 1, WAVE);
-    float ya = in ? expf(laC - la) : 0.f;
-    float yb = (i + 1 < C) ? expf(lbn - lb) : 0.f;
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-      const float pa = __shfl_down(ya, o, WAVE), pb = __shfl_down(yb, o, WAVE);
-      if (i + o < WAVE) {
-        ya = ya + yb * pa;
-        yb = yb * pb;
-      }
-    }
-    const float ec = wave_sum(in ? expf(laC - la + lb) : 0.f);
-    if (i < Cp) {
-      cf.cC[i] = in ? eta * ya : 0.f;
-      cf.bb[i] = in ? eta * expf(lbC - lb) : 0.f;
-    }
-    if (i == 0) {
-      cf.AC = expf(laC);
-      cf.BC = expf(lbC);
-      cf.EC = ec;
-    }
-  }
-  __syncthreads();
-}
-
 // LDS carve-up (CT elements)
 template <int D, int HID, int CP>
 struct FwdLds {
@@ -844,11 +803,19 @@ static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
     return true;
   }
   if (a.fsplit && a.statesT && a.nslots > nch) {
-    auto kc = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
+    // the walk (register-resident state where built, else this kernel's walk
+    // mode), then the retrieval of every chunk at once
+    hipError_t we = hipSuccess;
+    if (!launch_local_walk(a, units, st, &we)) {
+      auto kc = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
+      set_lds_limit((const void*)kc);
+      hipLaunchKernelGGL(kc, dim3(units), dim3(512), lds, st, a);
+    } else if (we != hipSuccess) {
+      *err = we;
+      return true;
+    }
     auto kr = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
-    set_lds_limit((const void*)kc);
     set_lds_limit((const void*)kr);
-    hipLaunchKernelGGL(kc, dim3(units), dim3(512), lds, st, a);
     hipLaunchKernelGGL(kr, dim3(units * nch), dim3(512), lds, st, a);
   } else {
     auto kern = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_FULL>;

@@ -79,26 +79,37 @@ SAVE_RING = [
 
 @pytest.mark.parametrize("cfg", SAVE_RING, ids=lambda c: c.name)
 def test_forward_save_and_ring_agree(cfg):
-    """The saved-state path and the two-slot ring path give identical outputs
-    (for the fixed-size bf16 kernels: the walk plus the chunk-parallel retrieval
-    against the one-walk kernel)."""
+    """The saved-state path and the two-slot ring path agree (for the
+    fixed-size bf16 kernels: the register-resident walk plus the chunk-parallel
+    retrieval against the one-walk kernel, which round in different orders),
+    and both match the oracle."""
     inp = make_inputs(cfg, 102)
+    print(f"\n[case] save vs ring {cfg.name}", flush=True)
     a, _ = gpu_forward(cfg, inp, save=True)
     b, _ = gpu_forward(cfg, inp, save=False)
-    assert np.array_equal(a, b)
+    ref = O.forward_pairs(inp, cfg, O.all_pairs(cfg)).numpy().reshape(a.shape)
+    ea, eb, eab = max_rel_err(a, ref), max_rel_err(b, ref), max_rel_err(a, b)
+    print(f"  saved {ea:.3e} ring {eb:.3e} between {eab:.3e}", flush=True)
+    assert check_err(f"fwd saved {cfg.name}", "o", ea, tol(cfg))
+    assert check_err(f"fwd ring {cfg.name}", "o", eb, tol(cfg))
+    assert eab <= tol(cfg)
 
 
 @pytest.mark.parametrize("cfg", SAVE_RING[2:], ids=lambda c: c.name)
 def test_forward_state_ring_agrees(cfg):
-    """With forward records saved, the walk cycles its fp32 carry through two
-    slots; the single-walk kernel family makes it write every slot instead.
-    The outputs are the same bits either way."""
+    """With forward records saved, the default walk keeps its state on chip
+    and writes only the compute-type copies; the single-walk kernel family
+    takes the walk that writes every fp32 slot.  Both agree within rounding and
+    match the oracle."""
     inp = make_inputs(cfg, 106)
     print(f"\n[case] state ring {cfg.name}", flush=True)
     a, _ = gpu_forward(cfg, inp, save=True)
     with tnt.kernel_family(tnt.FAMILY_SINGLE_WALK):
         b, _ = gpu_forward(cfg, inp, save=True)
-    assert np.array_equal(a, b)
+    ref = O.forward_pairs(inp, cfg, O.all_pairs(cfg)).numpy().reshape(a.shape)
+    assert check_err(f"fwd default walk {cfg.name}", "o", max_rel_err(a, ref), tol(cfg))
+    assert check_err(f"fwd fp32-slot walk {cfg.name}", "o", max_rel_err(b, ref), tol(cfg))
+    assert max_rel_err(a, b) <= tol(cfg)
 
 
 def test_forward_deterministic():
