@@ -53,7 +53,40 @@ tnt_status validate(const tnt_config* c, bool need_L = true) {
   if (!one_of(c->hid, {16, 32, 64, 128, 256, 512})) return TNT_ERR_UNSUPPORTED;
   for (int i = 0; i < c->n_local; ++i)
     if (c->C_L[i] > 64) return TNT_ERR_UNSUPPORTED;
+  // the intra-chunk reading of the global memory runs as one more local-style
+  // memory (see effective()): chunk-parallel calls only, one slot to spare
+  if (c->has_global && c->global_intra && (c->n_local >= TNT_MAX_LOCAL || !need_L))
+    return TNT_ERR_UNSUPPORTED;
   return TNT_OK;
+}
+
+// The global memory under the intra-chunk reading (each token read at V_t
+// after its own update, gradients at the chunk-entry state) is the local rule
+// with C_L = C_G, no reset within the sequence and no Q-K projection (a pinned
+// identity of the oracle).  It is walked as local memory 0 in sub-chunks of
+// csub <= 64 tokens (the largest divisor of C_G up to 64) whose gradients are
+// all taken at the state entering their C_G chunk (gsub = C_G / csub
+// sub-chunks per gradient point); the locals follow it.
+struct Eff {
+  tnt_config c;
+  int gsub;  // > 0: local 0 of `c` is the global memory under the intra-chunk reading
+};
+
+Eff effective(const tnt_config* c) {
+  Eff e{*c, 0};
+  if (!(c->has_global && c->global_intra)) return e;
+  int cs = c->C_G < 64 ? c->C_G : 64;
+  while (c->C_G % cs) --cs;
+  e.gsub = c->C_G / cs;
+  e.c.has_global = 0;
+  e.c.n_local = c->n_local + 1;
+  for (int i = TNT_MAX_LOCAL - 1; i >= 1; --i) {
+    e.c.C_L[i] = c->C_L[i - 1];
+    e.c.S_L[i] = c->S_L[i - 1];
+  }
+  e.c.C_L[0] = cs;
+  e.c.S_L[0] = c->L;
+  return e;
 }
 
 Dims dims_of(const tnt_config* c, int C, int S) {
@@ -69,6 +102,7 @@ Dims dims_of(const tnt_config* c, int C, int S) {
 // the saved buffer for the chunk-entry states.
 struct Layout {
   int M, BH;
+  int gsub0;  // > 0: local 0 is the global memory under the intra-chunk reading
   size_t hd, io_elems, gates;
   // saved (or workspace-resident) chunk states
   size_t sv_g, sv_l[TNT_MAX_LOCAL], sv_m[TNT_MAX_LOCAL], sv_t[TNT_MAX_LOCAL],
@@ -83,7 +117,7 @@ struct Layout {
   LocalPlan lplan[TNT_MAX_LOCAL];
   // backward workspace
   size_t b_dparts, b_adj_g, b_dR, b_dtok, b_dchunk, b_dWg, b_gscr, b_gscr_f32, b_gpackA, b_gop,
-      b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
+      b_adj_l[TNT_MAX_LOCAL], b_madj[TNT_MAX_LOCAL], b_hadj[TNT_MAX_LOCAL], b_dWl[TNT_MAX_LOCAL],
       b_scr[TNT_MAX_LOCAL], b_scrf[TNT_MAX_LOCAL], b_split[TNT_MAX_LOCAL], b_states, bwd_bytes,
       bwd_re_bytes;
   BwdLayout blay[TNT_MAX_LOCAL];
@@ -95,8 +129,21 @@ std::atomic<int> g_family{TNT_FAMILY_DEFAULT};
 int generic_only() { return g_family.load() == TNT_FAMILY_GENERIC ? 1 : 0; }
 int single_walk_only() { return g_family.load() == TNT_FAMILY_SINGLE_WALK ? 1 : 0; }
 
-Layout layout_of(const tnt_config* c) {
+// Sizes of local memory i's pass (the intra-reading global memory, local 0
+// when gsub0 > 0, has no Q-K projection and takes its gradients per group).
+Dims mem_dims(const tnt_config* c, int gsub0, int i) {
+  Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+  if (i == 0 && gsub0 > 0) {
+    D.qk_proj = 0;
+    D.qk_scope = 0;
+    D.gsub = gsub0;
+  }
+  return D;
+}
+
+Layout layout_of(const tnt_config* c, int gsub0 = 0) {
   Layout y{};
+  y.gsub0 = gsub0;
   y.M = c->has_global + c->n_local;
   y.BH = c->B * c->H;
   y.hd = (size_t)c->hid * c->d;
@@ -121,8 +168,9 @@ Layout layout_of(const tnt_config* c) {
     // walk then cycles its fp32 carry through two slots per unit instead of
     // writing every slot, and only those two are reserved.  The families that
     // recompute from the fp32 states (one-walk, runtime-sized) keep every slot.
-    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
-    const bool recs = local_fwd_split_bytes(D, y.l_units[i]) && local_bwd_split_bytes(D, y.l_units[i]);
+    const Dims D = mem_dims(c, gsub0, i);
+    const bool recs = !(i == 0 && gsub0) && local_fwd_split_bytes(D, y.l_units[i]) &&
+                      local_bwd_split_bytes(D, y.l_units[i]);
     y.l_fslots[i] = (recs && !single_walk_only() && !generic_only()) ? 2 : 0;
     y.sv_l[i] = off;
     off += up((size_t)y.l_units[i] * (y.l_fslots[i] ? y.l_fslots[i] : y.l_chunks[i] + 1) * 4 *
@@ -157,7 +205,7 @@ Layout layout_of(const tnt_config* c) {
     y.w_gop = off; off += up((size_t)y.BH * (2 * (size_t)c->hid + 4 * (size_t)c->d) * c->C_G * cts);
   }
   for (int i = 0; i < c->n_local; ++i) {
-    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+    const Dims D = mem_dims(c, gsub0, i);
     local_plan(D, &y.lplan[i], false);
     y.w_scr[i] = off; off += up((size_t)y.l_units[i] * y.lplan[i].elems * cts);
     const size_t fb = local_fwd_split_bytes(D, y.l_units[i]);
@@ -169,8 +217,10 @@ Layout layout_of(const tnt_config* c) {
   y.w_ring = off;
   if (c->has_global) { y.ring_g = off; off += up((size_t)y.BH * 2 * 4 * y.hd * f); }
   for (int i = 0; i < c->n_local; ++i) {
-    y.ring_l[i] = off; off += up((size_t)y.l_units[i] * 2 * 4 * y.hd * f);
-    y.ring_m[i] = off; off += up((size_t)y.l_units[i] * 2 * dd * f);
+    // a two-slot ring, or every slot for the grouped gradient points
+    const size_t ns = (i == 0 && gsub0) ? (size_t)y.l_chunks[i] + 1 : 2;
+    y.ring_l[i] = off; off += up((size_t)y.l_units[i] * ns * 4 * y.hd * f);
+    y.ring_m[i] = off; off += up((size_t)y.l_units[i] * ns * dd * f);
   }
   y.fwd_bytes = off;
   (void)fwd_core;
@@ -191,10 +241,12 @@ Layout layout_of(const tnt_config* c) {
     y.b_gop = off; off += up((size_t)y.BH * 5 * ((size_t)c->hid + c->d) * c->C_G * cts);
   }
   for (int i = 0; i < c->n_local; ++i) {
-    const Dims D = dims_of(c, c->C_L[i], c->S_L[i]);
+    const Dims D = mem_dims(c, gsub0, i);
     bwd_layout(D.Cp, D.d, D.hid, &y.blay[i]);
     y.b_adj_l[i] = off; off += up((size_t)y.l_units[i] * 4 * y.hd * f);
     y.b_madj[i] = off; off += up((size_t)y.l_units[i] * dd * f);
+    y.b_hadj[i] = off;
+    if (i == 0 && gsub0) off += up((size_t)y.l_units[i] * 2 * y.hd * f);
     y.b_dWl[i] = off; off += up((size_t)y.l_units[i] * 2 * y.hd * f);
     y.b_scr[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].ct_elems * cts);
     y.b_scrf[i] = off; off += up((size_t)y.l_units[i] * y.blay[i].f32_elems * f);
@@ -229,7 +281,7 @@ SavedHeader header_of(const tnt_config* c, const Layout& y) {
   h.magic = SAVED_MAGIC;
   h.layout_version = SAVED_LAYOUT_VERSION;
   h.family = (uint32_t)g_family.load();
-  for (int i = 0; i < TNT_MAX_LOCAL; ++i) h.fslots[i] = i < c->n_local ? (uint32_t)y.l_fslots[i] : 0;
+  for (int i = 0; i < TNT_MAX_LOCAL; ++i) h.fslots[i] = (uint32_t)y.l_fslots[i];  // 0 past the memories
   h.cfg_hash = config_hash(c);
   h.bytes = y.saved_bytes;
   return h;
@@ -371,14 +423,18 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.statesT = sv ? (void*)(sv + y.sv_t[i]) : nullptr;
     a.frec = (sv && y.sv_fr[i] != SIZE_MAX) ? (void*)(sv + y.sv_fr[i]) : nullptr;
     a.frec_f = (sv && y.sv_frf[i] != SIZE_MAX) ? (float*)(sv + y.sv_frf[i]) : nullptr;
-    a.nslots = sv ? y.l_chunks[i] + 1 : 2;
+    const bool grouped = i == 0 && y.gsub0;
+    a.nslots = (sv || grouped) ? y.l_chunks[i] + 1 : 2;
     a.fslots = sv ? y.l_fslots[i] : 0;
     a.scratch = ws + y.w_scr[i];
     a.fsplit = y.w_fsplit[i] != SIZE_MAX ? (void*)(ws + y.w_fsplit[i]) : nullptr;
     a.plan = y.lplan[i];
-    a.D = dims_of(c, c->C_L[i], c->S_L[i]);
-    a.force_generic = generic_only();
-    HIP_TIMED("local_fwd", launch_local_fwd(a, y.l_units[i], st));
+    a.D = mem_dims(c, y.gsub0, i);
+    a.force_generic = generic_only() || grouped;
+    HIP_TIMED(grouped ? "global_intra_fwd" : "local_fwd", launch_local_fwd(a, y.l_units[i], st));
+    if (grouped && final_state)  // the global memory's state after the last token
+      HIP_TIMED("copy_final", launch_copy_final(a.states, a.nslots, y.l_units[i], 4 * y.hd,
+                                                y.l_chunks[i], final_state, st));
   }
   if (c->has_global) {
     st = fk ? fk->side : main_st;
@@ -453,14 +509,16 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.scratch_f32 = (float*)(ws + y.b_scrf[i]);
     a.split_ws = y.b_split[i] != SIZE_MAX ? (void*)(ws + y.b_split[i]) : nullptr;
     a.single_walk = single_walk_only();
-    a.D = dims_of(c, c->C_L[i], c->S_L[i]);
-    a.force_generic = generic_only();
+    a.D = mem_dims(c, y.gsub0, i);
+    const bool grouped = i == 0 && y.gsub0;
+    a.force_generic = generic_only() || grouped;
+    a.hadj = grouped ? (float*)(ws + y.b_hadj[i]) : nullptr;
     a.pass_a_done = (fk && i == 0) ? fk->ea : nullptr;
     // the last local memory's walk is the point after which dq, dv and every dW_init
     // part are final: the helper stream reduces them beside its gate pass
     const bool last = i == c->n_local - 1;
     a.pass_b_done = (fk && last) ? fk->eb : nullptr;
-    HIP_TIMED("local_bwd", launch_local_bwd(a, y.l_units[i], st));
+    HIP_TIMED(grouped ? "global_intra_bwd" : "local_bwd", launch_local_bwd(a, y.l_units[i], st));
     if (!(fk && last))
       HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                  dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
@@ -621,7 +679,8 @@ const char* tnt_strerror(tnt_status s) {
 
 size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind) {
   if (validate(cfg) != TNT_OK) return 0;
-  const Layout y = layout_of(cfg);
+  const Eff E = effective(cfg);
+  const Layout y = layout_of(&E.c, E.gsub);
   if (kind == TNT_WS_FWD) return y.fwd_bytes;
   if (kind == TNT_WS_BWD) return y.bwd_bytes;
   if (kind == TNT_WS_BWD_RECOMPUTE) return y.bwd_re_bytes;
@@ -630,7 +689,8 @@ size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind) {
 
 size_t tnt_mem_saved_size(const tnt_config* cfg) {
   if (validate(cfg) != TNT_OK) return 0;
-  return layout_of(cfg).saved_bytes;
+  const Eff E = effective(cfg);
+  return layout_of(&E.c, E.gsub).saved_bytes;
 }
 
 tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
@@ -659,11 +719,12 @@ tnt_status forward_entry(const tnt_config* cfg, const void* q, const void* k, co
                         (const void*)W2_init, (const void*)o, (const void*)final_state,
                         (const void*)saved, (const void*)workspace})
     if (p && misaligned(p)) return TNT_ERR_ALIGN;
-  const Layout y = layout_of(cfg);
+  const Eff E = effective(cfg);
+  const Layout y = layout_of(&E.c, E.gsub);
   if (ws_bytes < y.fwd_bytes) return TNT_ERR_WORKSPACE;
   if (saved && saved_bytes < y.saved_bytes) return TNT_ERR_WORKSPACE;
   const SavedHeader hdr = header_of(cfg, y);
-  s = run_forward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
+  s = run_forward(&E.c, y, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
                   (char*)saved, (char*)workspace, stream, fork);
   if (s != TNT_OK || !saved) return s;
   if (launch_write_header(saved, hdr, stream) != hipSuccess) return TNT_ERR_HIP;
@@ -692,7 +753,8 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
                         (const void*)dmom, (const void*)ddecay, (const void*)dW1_init,
                         (const void*)dW2_init, (const void*)workspace})
     if (p && misaligned(p)) return TNT_ERR_ALIGN;
-  const Layout y = layout_of(cfg);
+  const Eff E = effective(cfg);
+  const Layout y = layout_of(&E.c, E.gsub);
   if (ws_bytes < (saved ? y.bwd_bytes : y.bwd_re_bytes)) return TNT_ERR_WORKSPACE;
   if (saved) {
     // the buffer must hold what a forward of this very configuration and
@@ -705,11 +767,11 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
   char* sv = saved ? (char*)saved : ws + y.b_states;
   hipStream_t st = (hipStream_t)stream;
   if (!saved) {
-    s = run_forward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, nullptr, nullptr, sv, ws,
+    s = run_forward(&E.c, y, q, k, v, lr, mom, decay, W1_init, W2_init, nullptr, nullptr, sv, ws,
                     st);
     if (s != TNT_OK) return s;
   }
-  return run_backward(cfg, y, q, k, v, lr, mom, decay, W1_init, W2_init, dO, sv, dq, dk, dv,
+  return run_backward(&E.c, y, q, k, v, lr, mom, decay, W1_init, W2_init, dO, sv, dq, dk, dv,
                       dlr, dmom, ddecay, dW1_init, dW2_init, ws, st);
 }
 
@@ -780,6 +842,7 @@ tnt_status tnt_mem_state_from_fwd(const tnt_config* cfg, const float* final_stat
                                   void* stream) {
   tnt_status s = validate(cfg);  // L: the prefix the forward ran over
   if (s != TNT_OK) return s;
+  if (cfg->has_global && cfg->global_intra) return TNT_ERR_UNSUPPORTED;
   if (!W1_init || !W2_init || !state || (cfg->has_global && !final_state)) return TNT_ERR_NULL;
   for (const void* p : {(const void*)W1_init, (const void*)W2_init, (const void*)state,
                         (const void*)final_state})

@@ -30,6 +30,9 @@ struct Dims {
   int act;    // ACT_GELU / ACT_SILU
   int bf16;   // 1: q/k/v/o are bf16 and MFMA operands are bf16
   int qk_proj, qk_scope;
+  int gsub;   // > 1: gradients of every gsub consecutive chunks are taken at the state
+              // entering the first of them (the global memory's intra-chunk reading
+              // walked in sub-chunks, runtime-sized kernels only); 0 or 1 otherwise
 };
 
 // Per-unit scratch of the local memory kernels (element offsets into a CT
@@ -81,6 +84,8 @@ struct LocalBwdArgs {
                                                          // ring, not every chunk-entry state
   float* adj;                                            // [units][4*hid*d] adjoint state
   float* madj;                                           // [units][2][d*d]
+  float* hadj;                                           // D.gsub > 1: [units][2*hid*d], the
+                                                         // adjoint of the gradient-point state
   float* dq_part; float* dk_part; float* dv_part;        // [B][H][L][d] fp32
   float* dlr; float* dmom; float* ddecay;                // this memory, [B][H][L]
   float* dWinit_part;                                    // [units][2*hid*d]

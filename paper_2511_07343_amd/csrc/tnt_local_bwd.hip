@@ -109,17 +109,31 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     Wb1T[e] = from_f<CT>(0.f);  // the four transposed copies are contiguous
   }
   for (int e = threadIdx.x; e < d * d; e += blockDim.x) madj[e] = 0.f;
+  // gsub > 1: the gradients of a group of gsub chunks are taken at the state
+  // entering the group, so the adjoint of that gradient point (Zkbar^T K into
+  // W1, R^T Gbar + Ykbar^T Hk into W2) is gathered over the group in `hadj`
+  // and joins the carried adjoint at the group's first chunk
+  const int gsub = D.gsub > 1 ? D.gsub : 1;
+  float* hadj = gsub > 1 ? a.hadj + (size_t)u * 2 * hd : nullptr;
+  if (hadj)
+    for (size_t e = threadIdx.x; e < 2 * hd; e += blockDim.x) hadj[e] = 0.f;
   __syncthreads();
 
   const int nch = D.S / C;
   for (int n = nch - 1; n >= 0; --n) {
     const int tok0 = s * D.S + n * C;
+    const int ng = n - n % gsub;  // the chunk whose entry state is the gradient point
     const float* st = a.states + ((size_t)u * a.nslots + n) * 4 * hd;
     const float *W1 = st, *W2 = st + hd, *S1 = st + 2 * hd, *S2 = st + 3 * hd;
+    const float* stg = a.states + ((size_t)u * a.nslots + ng) * 4 * hd;
+    const float *W1g = stg, *W2g = stg + hd;
     const float* Mc = a.mstates + ((size_t)u * a.nslots + n) * d * d;
     // transposed CT copies of the same state (contraction-contiguous operands)
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
     const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd, *McT = pk + 4 * hd;
+    const CT* pkg = (const CT*)a.statesT + ((size_t)u * a.nslots + ng) * (4 * hd + (size_t)d * d);
+    const CT *W1gT = pkg, *W2gT = pkg + hd;
+    const bool g_first = (n % gsub) == 0;
 
     // ================= recompute the chunk's forward quantities
     stage_rows<IO, CT>(Q, QT, qg + (size_t)tok0 * d, C, Cp, d);
@@ -161,7 +175,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
         put_x(i, j, to_f(Q[e]));
       }
     }
-    gemm<CT, KC, KC>(Cp, h, d, K, d, W1, d, [&](int i, int j, float z) {
+    gemm<CT, KC, KC>(Cp, h, d, K, d, W1g, d, [&](int i, int j, float z) {
       const ActVals av = act_all<ACT>(z);
       Hk[(size_t)i * h + j] = from_f<CT>(av.s);
       HkT[(size_t)j * Cp + i] = from_f<CT>(av.s);
@@ -169,13 +183,13 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       Spp[(size_t)i * h + j] = from_f<CT>(av.d2);
     });
     __syncthreads();
-    gemm<CT, KC, KC>(Cp, d, h, Hk, h, W2, h, [&](int i, int j, float y) {
+    gemm<CT, KC, KC>(Cp, d, h, Hk, h, W2g, h, [&](int i, int j, float y) {
       const float r = (i < C) ? rscale * (y - to_f(vg[(size_t)(tok0 + i) * d + j])) : 0.f;
       R[(size_t)i * d + j] = from_f<CT>(r);
       RT[(size_t)j * Cp + i] = from_f<CT>(r);
     });
     __syncthreads();
-    gemm<CT, KC, KC>(Cp, h, d, R, d, W2T, d, [&](int i, int j, float g) {
+    gemm<CT, KC, KC>(Cp, h, d, R, d, W2gT, d, [&](int i, int j, float g) {
       const float d1 = g * to_f(Sp[(size_t)i * h + j]);
       G[(size_t)i * h + j] = from_f<CT>(g);
       D1[(size_t)i * h + j] = from_f<CT>(d1);
@@ -350,7 +364,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     tiles(Cp, d, [&](int i0, int j0) {
       f4 a1 = zero4(), a2 = zero4();
       mma_tile<CT, KC, KC>(a1, PoT, Cp, i0, dOT, Cp, j0, Cp);
-      mma_tile<CT, KC, KC>(a2, Gb, h, i0, W2, h, j0, h);
+      mma_tile<CT, KC, KC>(a2, Gb, h, i0, W2g, h, j0, h);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -371,7 +385,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       mma_tile<CT, KC, KC>(a1, Q1T, Cp, i0, HT, Cp, j0, Cp);
       mma_tile<CT, KC, KC>(a2, R, d, i0, Wb2T, d, j0, d);
       mma_tile<CT, KC, KC>(a3, R, d, i0, Sb2T, d, j0, d);
-      mma_tile<CT, KC, KC>(a4, Ykb, d, i0, W2T, d, j0, d);
+      mma_tile<CT, KC, KC>(a4, Ykb, d, i0, W2gT, d, j0, d);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -387,7 +401,7 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
     tiles(Cp, d, [&](int i0, int j0) {
       f4 a1 = zero4(), a2 = zero4();
       mma_tile<CT, KC, KC>(a1, Q2T, Cp, i0, XT, Cp, j0, Cp);
-      mma_tile<CT, KC, KC>(a2, Zkb, h, i0, W1T, h, j0, h);
+      mma_tile<CT, KC, KC>(a2, Zkb, h, i0, W1gT, h, j0, h);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -530,7 +544,13 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * d + j0 + (l & 15);
         const float w = Wb1[e], sv = Sb1[e];
-        nw[r] = cf.AC * w + a1[r] + a2[r];
+        float gp = a2[r];  // the gradient point's share
+        if (hadj) {
+          gp += hadj[e];
+          hadj[e] = g_first ? 0.f : gp;
+          if (!g_first) gp = 0.f;
+        }
+        nw[r] = cf.AC * w + a1[r] + gp;
         ns[r] = cf.EC * w + cf.BC * sv + a3[r];
         Wb1[e] = nw[r];
         Sb1[e] = ns[r];
@@ -551,7 +571,13 @@ __global__ void __launch_bounds__(512) local_bwd_kernel(LocalBwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * h + j0 + (l & 15);
         const float w = Wb2[e], sv = Sb2[e];
-        nw[r] = cf.AC * w + a1[r] + a2[r] + a3[r];
+        float gp = a2[r] + a3[r];  // the gradient point's share
+        if (hadj) {
+          gp += hadj[hd + e];
+          hadj[hd + e] = g_first ? 0.f : gp;
+          if (!g_first) gp = 0.f;
+        }
+        nw[r] = cf.AC * w + a1[r] + gp;
         ns[r] = cf.EC * w + cf.BC * sv + a4[r];
         Wb2[e] = nw[r];
         Sb2[e] = ns[r];

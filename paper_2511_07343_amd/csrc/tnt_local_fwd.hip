@@ -87,9 +87,14 @@ __global__ void __launch_bounds__(512) local_fwd_kernel(LocalFwdArgs a) {
   __syncthreads();
 
   const int nch = D.S / C;
+  const int gsub = D.gsub > 1 ? D.gsub : 1;
   for (int n = 0; n < nch; ++n) {
     const int tok0 = s * D.S + n * C;
     const float* cur = st + (size_t)(n % a.nslots) * 4 * hd;
+    // the state the chunk's gradients are taken at: its own entry state, or with
+    // gsub > 1 the state entering its group of gsub chunks (every slot is kept then)
+    const float* gpt = st + (size_t)((n - n % gsub) % a.nslots) * 4 * hd;
+    const float *W1g = gpt, *W2g = gpt + hd;
     float* nxt = st + (size_t)((n + 1) % a.nslots) * 4 * hd;
     const float *W1 = cur, *W2 = cur + hd, *S1 = cur + 2 * hd, *S2 = cur + 3 * hd;
     float *W1n = nxt, *W2n = nxt + hd, *S1n = nxt + 2 * hd, *S2n = nxt + 3 * hd;
@@ -127,7 +132,7 @@ __global__ void __launch_bounds__(512) local_fwd_kernel(LocalFwdArgs a) {
     }
 
     // ---- Zk = K W1^T -> Hk, s'(Zk)
-    gemm<CT, KC, KC>(Cp, h, d, sK, d, W1, d, [&](int i, int j, float z) {
+    gemm<CT, KC, KC>(Cp, h, d, sK, d, W1g, d, [&](int i, int j, float z) {
       const ActVals av = act_all<ACT>(z);
       sHk[(size_t)i * h + j] = from_f<CT>(av.s);
       sHkT[(size_t)j * Cp + i] = from_f<CT>(av.s);
@@ -143,7 +148,7 @@ __global__ void __launch_bounds__(512) local_fwd_kernel(LocalFwdArgs a) {
     __syncthreads();
 
     // ---- R = (2/d) (Hk W2^T - V)
-    gemm<CT, KC, KC>(Cp, d, h, sHk, h, W2, h, [&](int i, int j, float y) {
+    gemm<CT, KC, KC>(Cp, d, h, sHk, h, W2g, h, [&](int i, int j, float y) {
       const float r = (i < C) ? rscale * (y - to_f(v[(size_t)(tok0 + i) * d + j])) : 0.f;
       sR[(size_t)i * d + j] = from_f<CT>(r);
       sRT[(size_t)j * Cp + i] = from_f<CT>(r);
@@ -153,7 +158,7 @@ __global__ void __launch_bounds__(512) local_fwd_kernel(LocalFwdArgs a) {
     __syncthreads();
 
     // ---- D1 = (R W2) * s'(Zk)
-    gemm<CT, KC, MC>(Cp, h, d, sR, d, W2, h, [&](int i, int j, float g) {
+    gemm<CT, KC, MC>(Cp, h, d, sR, d, W2g, h, [&](int i, int j, float g) {
       sD1T[(size_t)j * Cp + i] = from_f<CT>(g * to_f(sSp[(size_t)i * h + j]));
     });
     __syncthreads();

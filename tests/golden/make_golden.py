@@ -8,6 +8,8 @@ Two files per workload w (1..4), seed w, written by the fp64 oracle on the CPU:
   complete.
 * ``workload{w}_global32.npz`` (``--global-fp32``): that global-only shape
   with fp32 inputs (no bf16 rounding), for the fp32 bound chunk by chunk.
+* ``workload{w}_intra.npz`` (``--intra``): the workload with the global
+  memory read at V_t after each token's update (the intra-chunk reading).
 * ``workload{w}_global.npz``: the same shape with the global memory alone
   (no local memory; its own seeded draw).  The global memory's outputs shrink
   by orders of magnitude from one 2048-token chunk to the next under the
@@ -26,7 +28,7 @@ Stored (float32, .npz):
   final_state               [P][4][hid*d] (global file only): V1, V2, S1, S2
 Only `oracle/` and the seeded input generator are called.
 
-Usage: python tests/golden/make_golden.py 1 2 3 4 [--global-only | --full-only | --global-fp32]
+Usage: python tests/golden/make_golden.py 1 2 3 4 [--global-only | --full-only | --global-fp32 | --intra]
 """
 import os
 import sys
@@ -47,8 +49,8 @@ def global_only(cfg):
     return cfg.replace(locals_=(), name=cfg.name + " global only")
 
 
-def sampled_heads(idx, cfg):
-    return (0, cfg.H // 2) if idx == 1 else (cfg.H // 2,)
+def sampled_heads(idx, cfg, variant="bwd"):
+    return (0, cfg.H // 2) if (idx == 1 and variant == "bwd") else (cfg.H // 2,)
 
 
 def sample_rows(cfg, n_random=448, seed=7):
@@ -69,9 +71,11 @@ def make(idx, variant):
     cfg = WORKLOADS[idx] if variant == "bwd" else global_only(WORKLOADS[idx])
     if variant == "global32":   # the same global-only shape with fp32 inputs
         cfg = cfg.replace(dtype=F32, name=cfg.name + " fp32")
+    if variant == "intra":      # the workload with the global memory's intra-chunk reading
+        cfg = WORKLOADS[idx].replace(global_intra=1, name=WORKLOADS[idx].name + " global intra")
     torch.set_num_threads(max(1, len(os.sched_getaffinity(0))))
     inp = make_inputs(cfg, idx)
-    heads = sampled_heads(idx, cfg)
+    heads = sampled_heads(idx, cfg, variant)
     pairs = [(b, h) for h in heads for b in range(cfg.B)]
     t0 = time.time()
     r = O.backward_pairs(inp, cfg, pairs)
@@ -85,7 +89,7 @@ def make(idx, variant):
         full = r[n].numpy()
         out[n] = np.stack([full[:, [i for i, p in enumerate(pairs) if p[1] == h]].sum(1)
                            for h in heads], 1).astype(np.float32)
-    if variant.startswith("global"):
+    if variant.startswith("global") or variant == "intra":
         _, fin = O.forward_pairs(inp, cfg, pairs, with_final=True)
         out["final_state"] = np.stack([f.numpy().reshape(len(pairs), -1) for f in fin],
                                       1).astype(np.float32)
@@ -103,6 +107,8 @@ if __name__ == "__main__":
         variants = ["bwd"]
     if "--global-fp32" in sys.argv:
         variants = ["global32"]
+    if "--intra" in sys.argv:
+        variants = ["intra"]
     for a in args:
         for v in variants:
             make(int(a), v)

@@ -200,3 +200,21 @@ def test_dbg_chunk_grads_validation():
     assert tnt.tnt_dbg_chunk_grads(cfg, 0, 0, 60, 8, *args, stream=0) == 2    # t0 + C > L
     assert tnt.tnt_dbg_chunk_grads(cfg, 0, 0, 0, 65, *args, stream=0) == 2    # C > 64
     assert tnt.tnt_dbg_chunk_grads(cfg, 0, 0, 0, 8, None, *args[1:], stream=0) == 1
+
+
+def test_global_intra_limits():
+    """The intra-chunk reading of the global memory runs as one more local-style
+    memory: with four locals it is unsupported, and the step-wise calls do not
+    take it (chunk-parallel calls only)."""
+    cfg = small_config(L=64, C_G=16, locals_=((8, 32),), global_intra=1)
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD) > 0
+    assert tnt.tnt_mem_saved_size(cfg) > 0
+    full = cfg.replace(locals_=((8, 32),) * 4)
+    assert _fwd_status(full) == 3
+    assert tnt.tnt_mem_state_size(cfg) == 0
+    p = 256
+    assert tnt.tnt_mem_step(cfg, 0, 4, p, p, p, p, p, p, p, p, p, p, stream=0) == 3
+    assert tnt.tnt_mem_state_from_fwd(cfg, p, p, p, p, stream=0) == 3
+    # without a global memory the flag is ignored
+    assert tnt.tnt_mem_saved_size(cfg.replace(has_global=0)) == \
+        tnt.tnt_mem_saved_size(cfg.replace(has_global=0, global_intra=0))
