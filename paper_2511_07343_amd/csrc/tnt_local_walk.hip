@@ -38,12 +38,11 @@
 // record's s'(Zk), s''(Zk) and G.  Nothing is read back from memory.
 #include "tnt_local_common.h"
 #include "tnt_local_record.h"
+#include "tnt_regtile.h"
 
 namespace tnt {
 
 namespace {
-
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int WMAXC = 64;
 struct WalkCoef {
@@ -73,40 +72,6 @@ struct WalkLds {
   static constexpr int Sp = RbT + D * LT;     // s'(Zk), each wave's tiles, lane-major
   static constexpr int total = Sp + CP * HID;
 };
-
-__device__ __forceinline__ bf16x4 cvt4(const f4& a) {
-  bf16x4 b;
-  b[0] = (__bf16)a[0]; b[1] = (__bf16)a[1]; b[2] = (__bf16)a[2]; b[3] = (__bf16)a[3];
-  return b;
-}
-
-__device__ __forceinline__ bf16x8 join(const bf16x4& a, const bf16x4& b) {
-  bf16x8 f;
-  f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
-  f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];
-  return f;
-}
-
-// A operand rows `row` of a contraction-contiguous LDS array, contraction
-// indices k0 + 4g + j and k0 + 16 + 4g + j (j = 0..3), matching a B operand
-// made of two stacked accumulator tiles; `hi` = false zero-fills the second
-// half (a contraction of 16).
-__device__ __forceinline__ bf16x8 a_pair(const __bf16* A, int ld, int row, int k0, int g,
-                                         bool hi = true) {
-  const __bf16* p = A + (size_t)row * ld + k0 + 4 * g;
-  const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
-  bf16x4 y;
-  if (hi) {
-    y = *reinterpret_cast<const bf16x4*>(p + 16);
-  } else {
-    y[0] = y[1] = y[2] = y[3] = (__bf16)0.0f;
-  }
-  return join(x, y);
-}
-
-__device__ __forceinline__ void mma32(f4& acc, const bf16x8& a, const bf16x8& b) {
-  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
-}
 
 }  // namespace
 
@@ -151,7 +116,7 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
   float* const mst = a.mstates + (size_t)u * a.nslots * D * D;
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
   const float rscale = 2.0f / (float)D;
-  const int l = lane_id(), w = wave_id(), g = l >> 4, lc = l & 15;
+  const int l = lane_id(), w = wave_id_uniform(), g = l >> 4, lc = l & 15;
   constexpr size_t FS = 2 * (size_t)CP * HID + (size_t)CP * D;  // Hk, D1^T, R per chunk
   constexpr rec::RecLayout RL = rec::make_rec_layout(CP, D, HID);
 
@@ -441,7 +406,7 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
         f4 w2 = AC * W2[dt][ht] + EC * S2[dt][ht];
         f4 s2 = BC * S2[dt][ht];
         if constexpr (TM == 1) {
-          const bf16x4 z = {(__bf16)0.f, (__bf16)0.f, (__bf16)0.f, (__bf16)0.f};
+          const bf16x4 z = zero_bf4();
           const bf16x8 bd = join(d1[0][ht], z), bh = join(hk[0][ht], z);
           mma32(w1, a_pair(sKcT, LT, row, 0, g, false), bd);
           mma32(s1, a_pair(sKbT, LT, row, 0, g, false), bd);
