@@ -95,11 +95,36 @@ def hbm_bytes(cfg, name):
         return chains * ((2 * h + 4 * d) * C * cts + 2 * st)
     if name == "global_bwd_carry":
         return chains * (5 * (h + d) * C * cts + 3 * st)
+    if name == "local_carry":
+        return local_carry_bytes(cfg)["alg_bytes"]
     return None
 
 
+def local_carry_bytes(cfg):
+    """Algorithmic HBM bytes of one local-memory walk (the state carry), averaged
+    over the layer's local memories (one walk launch each).
+
+    With the state resident on chip across the chunk loop the walk must read the
+    chunk's keys and values (compute type) and its three gates (fp32), and write
+    the chunk-entry state the backward needs (W1, W2, S1, S2 and the d x d Q-K
+    sum, compute type): that is ``alg_bytes``.  ``spilled_state_bytes`` is what a
+    walk that kept the fp32 state in memory would move on top (read and write
+    4 h d fp32 per chunk)."""
+    d, h = cfg.d, cfg.hid
+    cts = 2 if cfg.dtype == 1 else 4
+    alg = spill = 0
+    for (C, S) in cfg.locals_:
+        units = cfg.B * cfg.H * (cfg.L // S)
+        nch = S // C
+        per_chunk = 2 * C * d * cts + 3 * C * 4 + (4 * h * d + d * d) * cts
+        alg += units * nch * per_chunk
+        spill += units * nch * 2 * 4 * h * d * 4
+    n = max(1, len(cfg.locals_))
+    return {"alg_bytes": alg // n, "spilled_state_bytes": spill // n}
+
+
 # labels timed inside another launch (reported separately, never the dominant launch)
-SECTIONS = ("global_carry", "global_bwd_carry")
+SECTIONS = ("global_carry", "global_bwd_carry", "local_carry", "local_bwd_walk")
 
 
 def launch_flops(cfg, name):
@@ -126,8 +151,12 @@ def launch_flops(cfg, name):
 TRAFFIC_FILE = {2: "hbm_traffic_pretrain_B4H8L8192.txt"}
 _COMMON = ["tnt_device.h", "tnt_kernels.h"]
 LAUNCH_SOURCES = {
-    "local_bwd": ["tnt_local_bwd_split.hip", "tnt_local_bwd_helpers.h", "tnt_local_common.h"] + _COMMON,
-    "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_common.h"] + _COMMON,
+    "local_bwd": ["tnt_local_bwd_split.hip", "tnt_local_bwd_helpers.h", "tnt_local_common.h",
+                  "tnt_local_record.h"] + _COMMON,
+    "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_walk.hip", "tnt_regtile.h", "tnt_local_common.h",
+                  "tnt_local_record.h"] + _COMMON,
+    "local_carry": ["tnt_local_walk.hip", "tnt_regtile.h", "tnt_local_common.h",
+                    "tnt_local_record.h"] + _COMMON,
     "global_bwd_chunk": ["tnt_global_bwd.hip", "tnt_global_blk.hip"] + _COMMON,
     "global_fwd_chunk": ["tnt_global_fwd.hip", "tnt_global_blk.hip"] + _COMMON,
     "global_scan": ["tnt_global_fwd.hip"] + _COMMON,
@@ -204,12 +233,40 @@ def cpu_baseline(cfg, inp, budget_tokens):
     args = [cut(g["q"], 1), cut(g["k"], 1), cut(g["v"], 1), cut(g["lr"], 2), cut(g["mom"], 2),
             cut(g["decay"], 2), g["W1"], g["W2"]]
     t0 = time.perf_counter()
-    O.layer_backward(*args, cut(g["dO"], 1), sub)
+    ref = O.layer_backward(*args, cut(g["dO"], 1), sub)
     dt = time.perf_counter() - t0
     return {"value": L / dt, "unit": "tokens/s", "cores": torch.get_num_threads(),
             "kind": "oracle",
             "sample": f"fwd+bwd of one (batch 0, head 0) chain, first {L} tokens "
-                      f"(fp64 torch CPU autograd, {dt:.1f} s)"}
+                      f"(fp64 torch CPU autograd, {dt:.1f} s)"}, ref
+
+
+def sample_parity(cfg, ref, o, g, L):
+    """Per-tensor max |gpu - oracle| / max |oracle| of the timed run's last step on
+    the oracle sample's chain (batch 0, head 0).  The outputs of a causal layer
+    on the first L tokens do not depend on later tokens, so o is compared on any
+    sample; the gradients only when the sample is the whole chain."""
+    import numpy as np
+    from paper_2511_07343_amd.inputs import max_rel_err
+    got = {"o": o[0, 0, :L]}
+    if L == cfg.L:
+        for n in ("dq", "dk", "dv"):
+            got[n] = g[n][0, 0]
+        for n in ("dlr", "dmom", "ddecay"):
+            got[n] = g[n][:, 0, 0]
+    out = {}
+    for n, t in got.items():
+        want = ref[n].numpy()
+        want = want[0] if n in ("o", "dq", "dk", "dv") else want[:, 0]
+        mine = t.float().cpu().numpy()
+        if n in ("dlr", "dmom", "ddecay"):   # each memory against its own scale
+            out[n] = max(max_rel_err(mine[m], want[m]) for m in range(cfg.M))
+        else:
+            out[n] = max_rel_err(mine, want)
+    return {"max_rel_err": out, "bound": 2e-2 if cfg.dtype == 1 else 1e-4,
+            "pass": all(np.isfinite(v) and v <= (2e-2 if cfg.dtype == 1 else 1e-4)
+                        for v in out.values()),
+            "sample": f"chain (batch 0, head 0), tokens 0..{L - 1}, against the fp64 oracle"}
 
 
 def decode_bench(args, cfg, x, dev):
@@ -408,7 +465,7 @@ def main():
     # HBM-bound steps: the gate scan and the global state carry (forward, backward)
     hbm = {}
     for lab in ("global_scan",) + SECTIONS:
-        if lab not in kt or hbm_bytes(cfg, lab) is None:
+        if lab not in kt or hbm_bytes(cfg, lab) is None or lab == "local_carry":
             continue
         t_ms, n_l = kt[lab]
         avg = t_ms / n_l
@@ -420,6 +477,20 @@ def main():
                     "counter_bytes": tb,
                     "counter_GBps": None if tb is None else tb / (avg * 1e-3) / 1e9,
                     "peak_GBps": PEAK_HBM / 1e9}
+    carry = None
+    if "local_carry" in kt and cfg.locals_:
+        t_ms, n_l = kt["local_carry"]
+        avg = t_ms / n_l
+        cb = local_carry_bytes(cfg)
+        tb = measured_traffic(prof_key, "local_carry")
+        carry = {"avg_launch_ms": avg, "launches": n_l, "alg_bytes": cb["alg_bytes"],
+                 "alg_GBps": cb["alg_bytes"] / (avg * 1e-3) / 1e9,
+                 "alg_frac": cb["alg_bytes"] / (avg * 1e-3) / PEAK_HBM,
+                 "state": "resident (registers) across the chunk loop",
+                 "spilled_state_bytes_avoided": cb["spilled_state_bytes"],
+                 "counter_bytes": tb,
+                 "counter_GBps": None if tb is None else tb / (avg * 1e-3) / 1e9,
+                 "peak_GBps": PEAK_HBM / 1e9}
     mf = measured_mfma(prof_key)
     mfma = None
     if mf is not None:
@@ -448,6 +519,9 @@ def main():
         "paper_context": PAPER_CONTEXT,
         "mfma_counted": mfma,
         "hbm_kernels": hbm,
+        "local_state_carry": carry,
+        "sections_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())
+                                 if k in SECTIONS},
         "device": device,
         "kernels_ms_per_step": {k: v[0] / args.steps for k, v in sorted(kt.items())
                                 if k not in SECTIONS},
@@ -455,7 +529,8 @@ def main():
     if not args.no_cpu_baseline:
         unit = cfg.locals_[0][1] if cfg.locals_ else cfg.C_G
         ctoks = args.cpu_tokens or min(cfg.L, 4 * unit)
-        res["cpu_baseline"] = cpu_baseline(cfg, inp, ctoks)
+        res["cpu_baseline"], ref = cpu_baseline(cfg, inp, ctoks)
+        res["parity"] = sample_parity(cfg, ref, o, g, ctoks)
     print(json.dumps(res), flush=True)
 
 

@@ -146,6 +146,19 @@ inline void set_lds_limit(const void* fn) {
     (void)hipGetLastError();
 }
 
+// Whether a compiled kernel's static LDS (as the runtime reports it) plus `dyn`
+// bytes of dynamic LDS fit one CU's 160 KB: checked before every launch of a
+// fixed-size kernel, so that a layout change that outgrows the LDS is refused
+// (hipErrorInvalidConfiguration) instead of launched.
+inline bool lds_fits(const void* fn, size_t dyn) {
+  hipFuncAttributes at{};
+  if (hipFuncGetAttributes(&at, fn) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return at.sharedSizeBytes + dyn <= 160 * 1024;
+}
+
 size_t local_plan(const Dims& D, LocalPlan* p, bool backward);
 
 hipError_t launch_local_fwd(const LocalFwdArgs& a, int units, hipStream_t st);

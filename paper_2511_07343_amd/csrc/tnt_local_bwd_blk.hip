@@ -931,6 +931,10 @@ static bool try_blk(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t
   constexpr size_t lds = bwd_blk_lds_bytes<CT, CP, D, H>();
   if (lds + 40 * 1024 > 160 * 1024) return false;  // static LDS is just under 40 KB
   auto kern = local_bwd_blk_kernel<IO, CT, ACT, D, H, CP>;
+  if (!lds_fits((const void*)kern, lds)) {  // the compiled static LDS, not the estimate
+    *err = hipErrorInvalidConfiguration;
+    return true;
+  }
   set_lds_limit((const void*)kern);
   hipLaunchKernelGGL(kern, dim3(units), dim3(512), lds, st, a);
   *err = hipGetLastError();

@@ -1090,11 +1090,16 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   auto ka = local_bwd_ret_kernel<IO, CT, ACT, D, H, CP>;
   auto kb = local_bwd_chain_kernel<IO, CT, ACT, D, H, CP>;
   auto kc = local_bwd_gate_kernel<CT, D, H, CP>;
+  constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, D, H>(),
+                   lds_c = split_c_lds<CP, D>();
+  if (!lds_fits((const void*)ka, lds_a) || !lds_fits((const void*)kb, lds_b) ||
+      !lds_fits((const void*)kc, lds_c)) {  // the compiled static LDS, not the estimate
+    *err = hipErrorInvalidConfiguration;
+    return true;
+  }
   set_lds_limit((const void*)ka);
   set_lds_limit((const void*)kb);
   set_lds_limit((const void*)kc);
-  constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, D, H>(),
-                   lds_c = split_c_lds<CP, D>();
   hipLaunchKernelGGL(ka, dim3(std::min(total, SPLIT_GRID_A)), dim3(512), lds_a, st, *a, P);
   if (a->pass_a_done) {
     const hipError_t e = hipEventRecord(a->pass_a_done, st);
@@ -1103,7 +1108,9 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
       return true;
     }
   }
+  const int sec = section_begin("local_bwd_walk", st);  // the walk of the carried adjoint alone
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
+  section_end(sec, st);
   if (a->pass_b_done) {
     const hipError_t e = hipEventRecord(a->pass_b_done, st);
     if (e != hipSuccess) {

@@ -802,15 +802,28 @@ static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
     *bytes = (size_t)units * nch * fwd_split_elems<D, HID, CP>() * sizeof(CT);
     return true;
   }
+  {  // the compiled static LDS of every mode, not the estimate
+    auto k0 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_FULL>;
+    auto k1 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
+    auto k2 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
+    if (!lds_fits((const void*)k0, lds) || !lds_fits((const void*)k1, lds) ||
+        !lds_fits((const void*)k2, lds)) {
+      *err = hipErrorInvalidConfiguration;
+      return true;
+    }
+  }
   if (a.fsplit && a.statesT && a.nslots > nch) {
     // the walk (register-resident state where built, else this kernel's walk
     // mode), then the retrieval of every chunk at once
     hipError_t we = hipSuccess;
+    const int sec = section_begin("local_carry", st);  // the state carry alone, for its GB/s
     if (!launch_local_walk(a, units, st, &we)) {
       auto kc = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
       set_lds_limit((const void*)kc);
       hipLaunchKernelGGL(kc, dim3(units), dim3(512), lds, st, a);
-    } else if (we != hipSuccess) {
+    }
+    section_end(sec, st);
+    if (we != hipSuccess) {
       *err = we;
       return true;
     }

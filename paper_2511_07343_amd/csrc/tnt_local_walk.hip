@@ -441,6 +441,10 @@ static bool try_walk(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
   constexpr size_t lds = walk_lds_bytes<D, HID, CP>();
   static_assert(lds + 2 * sizeof(WalkCoef) <= 160 * 1024, "LDS of one CU");
   auto kern = local_walk_kernel<IO, ACT, D, HID, CP>;
+  if (!lds_fits((const void*)kern, lds)) {  // the compiled static LDS, not the estimate
+    *err = hipErrorInvalidConfiguration;
+    return true;
+  }
   set_lds_limit((const void*)kern);
   hipLaunchKernelGGL(kern, dim3(units), dim3(512), lds, st, a);
   *err = hipGetLastError();

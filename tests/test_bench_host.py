@@ -57,3 +57,15 @@ def test_committed_summaries_parse():
     mf = os.path.join(ROOT, "profiles", bench.MFMA_FILE[2])
     steps = [line.split() for line in open(mf) if line.startswith("step sha256")]
     assert len(steps) == 1 and float(steps[0][5]) > 0
+
+
+def test_local_carry_bytes_workload2():
+    """The local state carry's algorithmic bytes at the pre-training shape, by hand:
+    128 units x 32 chunks, each reading K and V (64 x 64 bf16) and three gates
+    (64 fp32), writing the bf16 entry state (4 x 256 x 64 + 64 x 64)."""
+    cfg = WORKLOADS[2]
+    per_chunk = 2 * 64 * 64 * 2 + 3 * 64 * 4 + (4 * 256 * 64 + 64 * 64) * 2
+    cb = bench.local_carry_bytes(cfg)
+    assert cb["alg_bytes"] == 128 * 32 * per_chunk == 640679936
+    assert cb["spilled_state_bytes"] == 128 * 32 * 2 * 4 * 256 * 64 * 4
+    assert bench.hbm_bytes(cfg, "local_carry") == cb["alg_bytes"]
