@@ -103,15 +103,20 @@ __device__ __forceinline__ void chunk_coefs(Coef& cf, const float* lr, const flo
   __syncthreads();
 }
 
-// The coefficients without ct / ebt (retrieval and carry only; smaller LDS footprint).
-struct CoefF {
-  float c[MAXC][MAXC + 1];
-  float A[MAXC], E[MAXC], la[MAXC], lb[MAXC], eta[MAXC], cC[MAXC], bb[MAXC];
-  float knorm[MAXC];
+// The coefficients without ct / ebt (retrieval and carry only; smaller LDS
+// footprint), for chunks of at most N (padded) positions.
+template <int N>
+struct CoefFN {
+  static_assert(N <= MAXC, "one wave scans a chunk");
+  float c[N][N + 1];
+  float A[N], E[N], la[N], lb[N], eta[N], cC[N], bb[N];
+  float knorm[N];
   float AC, BC, EC;
 };
+using CoefF = CoefFN<MAXC>;
 
-__device__ __forceinline__ void chunk_coefs_f(CoefF& cf, const float* lr, const float* mom,
+template <int N>
+__device__ __forceinline__ void chunk_coefs_f(CoefFN<N>& cf, const float* lr, const float* mom,
                                               const float* dec, int tok0, int C, int Cp) {
   if (wave_id() == 0) {
     const int i = lane_id();
@@ -121,13 +126,15 @@ __device__ __forceinline__ void chunk_coefs_f(CoefF& cf, const float* lr, const 
     const float lka = in ? log_keep(dec[tok0 + i]) : 0.f;
     const float la = wave_incl_sum(lka);
     const float lb = wave_incl_sum(lmb);
-    cf.la[i] = la;
-    cf.lb[i] = lb;
-    cf.eta[i] = eta;
-    cf.A[i] = expf(la);
+    if (i < N) {
+      cf.la[i] = la;
+      cf.lb[i] = lb;
+      cf.eta[i] = eta;
+      cf.A[i] = expf(la);
+    }
   }
   __syncthreads();
-  coef_columns<MAXC + 1>(cf.la, cf.lb, cf.eta, Cp, nullptr, cf.c, cf.E);
+  coef_columns<N + 1>(cf.la, cf.lb, cf.eta, Cp, nullptr, cf.c, cf.E);
   __syncthreads();
   if (wave_id() == 0) {
     const int tau = lane_id();

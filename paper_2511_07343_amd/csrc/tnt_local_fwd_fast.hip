@@ -23,26 +23,42 @@
 
 namespace tnt {
 
-// LDS carve-up (CT elements)
-template <int D, int HID, int CP>
+// LDS carve-up (CT elements).  Rows of every matrix are PD elements longer
+// than the matrix (leading dimensions LDD, LDC, LDH): with PD = 8 the 16-byte
+// operand reads of consecutive rows start 16 bytes apart in the bank cycle
+// instead of on the same banks (rows of 128 or 512 bytes).  The retrieval
+// mode pads; the walk modes, whose LDS also holds a copy of W2, do not.
+template <int D, int HID, int CP, int PD>
 struct FwdLds {
   static constexpr int cmax(int x, int y) { return x > y ? x : y; }
-  static constexpr int USZ = cmax(cmax(CP, D) * HID, 3 * CP * D + CP * CP);
-  static constexpr int Hk = 0;
-  static constexpr int D1 = Hk + CP * HID;
-  static constexpr int U = D1 + CP * HID;
-  static constexpr int X = U + USZ;
-  static constexpr int K = X + CP * D;
-  static constexpr int R = K + CP * D;
-  static constexpr int P = R + CP * D;
-  static constexpr int total = P + CP * CP;
-  // inside U during the Q-K phase
-  static constexpr int uQ = U, uN = U + CP * D, uNT = U + 2 * CP * D, uS = U + 3 * CP * D;
+  static constexpr int LDD = D + PD, LDC = CP + PD, LDH = HID + PD;
+  // U: H [CP][LDH] and the Q-K temporaries; the walk modes (PD = 0) also hold
+  // the chunk-entry W2 ([D][HID] or W2^T [HID][D]) and K^T, R^T [D][CP] there
+  static constexpr int USZ = cmax(cmax(CP * LDH, 2 * CP * LDD + D * LDC + CP * LDC),
+                                  PD == 0 ? cmax(D * HID, 2 * D * CP) : 0);
+  static constexpr int Hk = 0;                 // [CP][LDH]
+  static constexpr int D1 = Hk + CP * LDH;     // D1^T [HID][LDC]
+  static constexpr int U = D1 + HID * LDC;
+  static constexpr int X = U + USZ;            // [CP][LDD]
+  static constexpr int K = X + CP * LDD;
+  static constexpr int R = K + CP * LDD;
+  static constexpr int P = R + CP * LDD;       // [CP][LDC]
+  static constexpr int total = P + CP * LDC;
+  // inside U during the Q-K phase: Q, N [CP][LDD], N^T [D][LDC], tril(Q N^T) [CP][LDC]
+  static constexpr int uQ = U, uN = U + CP * LDD, uNT = U + 2 * CP * LDD, uS = uNT + D * LDC;
+  static_assert(USZ % 8 == 0 && D1 % 8 == 0 && U % 8 == 0 && X % 8 == 0 && K % 8 == 0 &&
+                    R % 8 == 0 && P % 8 == 0 && uNT % 8 == 0 && uS % 8 == 0,
+                "16-byte aligned rows");
 };
 
-template <typename CT, int D, int HID, int CP>
+template <int MODE>
+constexpr int fwd_pad() {
+  return MODE == 2 ? 8 : 0;  // FWD_RET pads its rows
+}
+
+template <typename CT, int D, int HID, int CP, int PD>
 constexpr size_t fwd_fast_lds_bytes() {
-  return (size_t)FwdLds<D, HID, CP>::total * sizeof(CT);
+  return (size_t)FwdLds<D, HID, CP, PD>::total * sizeof(CT);
 }
 
 // Modes of the kernel.  FWD_FULL: one workgroup per unit walks its chunks and
@@ -63,8 +79,11 @@ template <typename IO, typename CT, int ACT, int D, int HID, int CP, int MODE>
 __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   constexpr bool WALK = MODE != FWD_RET, RETR = MODE != FWD_CHAIN;
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ CoefF cf;
-  using Ly = FwdLds<D, HID, CP>;
+  __shared__ CoefFN<CP> cf;  // the coefficients of a CP-row chunk
+  constexpr int PD = fwd_pad<MODE>();
+  using Ly = FwdLds<D, HID, CP, PD>;
+  constexpr int LDD = Ly::LDD, LDC = Ly::LDC, LDH = Ly::LDH;
+  static_assert(PD == 0 || !WALK, "the walk modes keep unpadded rows (their U holds W2)");
   constexpr int NW = 8;                       // waves
   constexpr int TNH = HID / 16, TMC = CP / 16;
   constexpr int KS = Mma<CT>::KS;
@@ -160,22 +179,23 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       static_assert((CP * D / VEC) % WAVE == 0, "whole waves stage");
       for (int e = threadIdx.x * VEC; e < CP * D; e += blockDim.x * VEC) {
         const int i = e / D;
+        const int el = i * LDD + (e - i * D);  // LDS position of element e
         float ss = 0.f;
         if (i < C) {
           const IO* pq = q + (size_t)tok0 * D + e;
           const IO* pk = k + (size_t)tok0 * D + e;
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
-            if (RETR) sQ[e + j] = from_f<CT>(to_f(pq[j]));
+            if (RETR) sQ[el + j] = from_f<CT>(to_f(pq[j]));
             const CT kv = from_f<CT>(to_f(pk[j]));
-            sK[e + j] = kv;
+            sK[el + j] = kv;
             ss += to_f(kv) * to_f(kv);
           }
         } else {
 #pragma unroll
           for (int j = 0; j < VEC; ++j) {
-            if (RETR) sQ[e + j] = from_f<CT>(0.f);
-            sK[e + j] = from_f<CT>(0.f);
+            if (RETR) sQ[el + j] = from_f<CT>(0.f);
+            sK[el + j] = from_f<CT>(0.f);
           }
         }
 #pragma unroll
@@ -189,14 +209,14 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
         const int i = e / D, j = e - i * D;
         const float nr = cf.knorm[i];
-        const float x = (i < C && nr > 0.f) ? to_f(sK[e]) / nr : 0.f;
-        sN[e] = from_f<CT>(x);
-        sNT[(size_t)j * CP + i] = from_f<CT>(x);
+        const float x = (i < C && nr > 0.f) ? to_f(sK[i * LDD + j]) / nr : 0.f;
+        sN[i * LDD + j] = from_f<CT>(x);
+        sNT[(size_t)j * LDC + i] = from_f<CT>(x);
       }
       __syncthreads();
       if (RETR) {
-      gemm<CT, KC, KC>(CP, CP, D, sQ, D, sN, D, [&](int i, int j, float x) {
-        sS[(size_t)i * CP + j] = from_f<CT>(j <= i ? x : 0.f);
+      gemm<CT, KC, KC>(CP, CP, D, sQ, LDD, sN, LDD, [&](int i, int j, float x) {
+        sS[(size_t)i * LDC + j] = from_f<CT>(j <= i ? x : 0.f);
       });
       __syncthreads();
       {
@@ -213,12 +233,12 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           if (shard_qk) {
 #pragma unroll
             for (int ks = 0; ks < NKD; ++ks) {
-              auto a = Mma<CT>::template load<KC>(sQ, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
+              auto a = Mma<CT>::template load<KC>(sQ, LDD, i0 + (l & 15), ks * KS + ko, D, nullptr);
               Mma<CT>::mma(acc, a, bm[ks].get());
             }
           }
-          mma_tile<CT, KC, KC>(acc, sS, CP, i0, sNT, CP, j0, CP);
-          tile_each(acc, i0, j0, [&](int i, int j, float x) { sX[(size_t)i * D + j] = from_f<CT>(x); });
+          mma_tile<CT, KC, KC>(acc, sS, LDC, i0, sNT, LDC, j0, CP);
+          tile_each(acc, i0, j0, [&](int i, int j, float x) { sX[(size_t)i * LDD + j] = from_f<CT>(x); });
         }
       }
       }
@@ -230,7 +250,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) mo[r] = Mc[(size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15)];
           f4 acc = zero4();
-          mma_tile<CT, KC, KC>(acc, sNT, CP, i0, sNT, CP, j0, CP);
+          mma_tile<CT, KC, KC>(acc, sNT, LDC, i0, sNT, LDC, j0, CP);
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             acc[r] += mo[r];
@@ -240,7 +260,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         }
       }
     } else if (RETR) {
-      for (int e = threadIdx.x; e < CP * D; e += blockDim.x) sX[e] = sQ[e];
+      for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
+        const int el = (e / D) * LDD + e % D;
+        sX[el] = sQ[el];
+      }
     }
 
     if constexpr (MODE == FWD_RET) {
@@ -248,9 +271,10 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       constexpr int V8 = 16 / sizeof(CT);
       for (size_t e = threadIdx.x * V8; e < FS; e += blockDim.x * V8) {
         const bf16x8 x = *reinterpret_cast<const bf16x8*>(fsn + e);
-        CT* dst = e < (size_t)CP * HID ? sHk + e
-                  : e < 2 * (size_t)CP * HID ? sD1 + (e - (size_t)CP * HID)
-                                             : sR + (e - 2 * (size_t)CP * HID);
+        const size_t e1 = e - (size_t)CP * HID, e2 = e - 2 * (size_t)CP * HID;
+        CT* dst = e < (size_t)CP * HID ? sHk + (e / HID) * LDH + e % HID
+                  : e < 2 * (size_t)CP * HID ? sD1 + (e1 / CP) * LDC + e1 % CP
+                                             : sR + (e2 / D) * LDD + e2 % D;
         *reinterpret_cast<bf16x8*>(dst) = x;
       }
       __syncthreads();
@@ -273,18 +297,20 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           const size_t e0 = (size_t)v * 8;
           const int i = (int)(e0 / D);                       // row-major: one row
           const int jt = (int)(e0 / CP), it = (int)(e0 % CP);  // transposed [D][CP]: rows it..it+7
-          cp8(rec::K, e0, sK + e0);
-          cp8(rec::R, e0, sR + e0);
-          cp8(rec::X, e0, sX + e0);
+          const size_t ed = (e0 / D) * LDD + e0 % D;       // [CP][D] element e0 in LDS
+          const size_t ec = (e0 / CP) * LDC + e0 % CP;     // [D][CP] element e0 in LDS
+          cp8(rec::K, e0, sK + ed);
+          cp8(rec::R, e0, sR + ed);
+          cp8(rec::X, e0, sX + ed);
           float kc[8], kb[8], rc[8], rb[8], kt[8], rt[8], xt[8], xa[8], xe[8], qt[8];
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
-            const float kx = to_f(sK[e0 + q]), rx = to_f(sR[e0 + q]);
+            const float kx = to_f(sK[ed + q]), rx = to_f(sR[ed + q]);
             kc[q] = cf.cC[i] * kx;
             kb[q] = cf.bb[i] * kx;
             rc[q] = cf.cC[i] * rx;
             rb[q] = cf.bb[i] * rx;
-            const size_t es = (size_t)(it + q) * D + jt;
+            const size_t es = (size_t)(it + q) * LDD + jt;
             kt[q] = to_f(sK[es]);
             rt[q] = to_f(sR[es]);
             xt[q] = to_f(sX[es]);
@@ -303,8 +329,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           st8(rec::XET, e0, xe);
           st8(rec::QT, e0, qt);
           if (qk) {
-            cp8(rec::N, e0, sN + e0);
-            cp8(rec::NT, e0, sNT + e0);
+            cp8(rec::N, e0, sN + ed);
+            cp8(rec::NT, e0, sNT + ec);
           }
         }
         if (qk)
@@ -313,19 +339,19 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             const int jt = (int)(e0 / CP), it = (int)(e0 % CP);
             float x[8];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) x[q] = to_f(sS[(size_t)(it + q) * CP + jt]);
+            for (int q = 0; q < 8; ++q) x[q] = to_f(sS[(size_t)(it + q) * LDC + jt]);
             st8(rec::StrT, e0, x);
           }
         for (int v = threadIdx.x; v < CP * HID / 8; v += blockDim.x) {
           const size_t e0 = (size_t)v * 8;
           const int jt = (int)(e0 / CP), it = (int)(e0 % CP);    // [HID][CP]
           const int i = (int)(e0 / HID), j = (int)(e0 % HID);    // [CP][HID]
-          cp8(rec::Hk, e0, sHk + e0);
+          cp8(rec::Hk, e0, sHk + (size_t)i * LDH + j);
           float ht[8], d1[8];
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
-            ht[q] = to_f(sHk[(size_t)(it + q) * HID + jt]);
-            d1[q] = to_f(sD1[(size_t)(j + q) * CP + i]);
+            ht[q] = to_f(sHk[(size_t)(it + q) * LDH + jt]);
+            d1[q] = to_f(sD1[(size_t)(j + q) * LDC + i]);
           }
           st8(rec::HkT, e0, ht);
           st8(rec::D1, e0, d1);
@@ -384,7 +410,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           f4 acc = zero4();
 #pragma unroll
           for (int ks = 0; ks < NKD; ++ks) {
-            auto a = Mma<CT>::template load<KC>(sK, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
+            auto a = Mma<CT>::template load<KC>(sK, LDD, i0 + (l & 15), ks * KS + ko, D, nullptr);
             Mma<CT>::mma(acc, a, bw[y][ks]);
           }
           f4 d1v, d2v;
@@ -392,7 +418,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           for (int r = 0; r < 4; ++r) {
             const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
             const ActVals av = act_all<ACT>(acc[r]);
-            sHk[(size_t)i * HID + j] = from_f<CT>(av.s);
+            sHk[(size_t)i * LDH + j] = from_f<CT>(av.s);
             spr[y][it][r] = from_f<CT>(av.d1);
             d1v[r] = av.d1;
             d2v[r] = av.d2;
@@ -453,14 +479,14 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
         if constexpr (MODE == FWD_CHAIN)
-          mma_tile<CT, KC, MC>(acc, sHk, HID, i0, sW2, D, j0, HID);  // sW2 = W2^T
+          mma_tile<CT, KC, MC>(acc, sHk, LDH, i0, sW2, D, j0, HID);  // sW2 = W2^T
         else
-          mma_tile<CT, KC, KC>(acc, sHk, HID, i0, sW2, HID, j0, HID);
+          mma_tile<CT, KC, KC>(acc, sHk, LDH, i0, sW2, HID, j0, HID);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
           const float rv = (i < C) ? rscale * (acc[r] - vv[x][r]) : 0.f;
-          sR[(size_t)i * D + j] = from_f<CT>(rv);
+          sR[(size_t)i * LDD + j] = from_f<CT>(rv);
         }
       }
     }
@@ -476,13 +502,13 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int i0 = it * 16, j0 = sidx * 16;
         f4 acc = zero4();
         if constexpr (MODE == FWD_CHAIN)
-          mma_tile<CT, KC, KC>(acc, sR, D, i0, sW2, D, j0, D);  // sW2 = W2^T
+          mma_tile<CT, KC, KC>(acc, sR, LDD, i0, sW2, D, j0, D);  // sW2 = W2^T
         else
-          mma_tile<CT, KC, MC>(acc, sR, D, i0, sW2, HID, j0, D);
+          mma_tile<CT, KC, MC>(acc, sR, LDD, i0, sW2, HID, j0, D);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          sD1[(size_t)j * CP + i] = from_f<CT>(acc[r] * to_f(spr[y][it][r]));  // D1^T
+          sD1[(size_t)j * LDC + i] = from_f<CT>(acc[r] * to_f(spr[y][it][r]));  // D1^T
         }
         if (MODE == FWD_CHAIN && fr) store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(i0, j0, l), acc);
       }
@@ -494,8 +520,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     CT* sRT = sU + CP * D;     // [D][CP]
     for (int e = threadIdx.x; e < CP * D; e += blockDim.x) {
       const int i = e / D, j = e - i * D;
-      sKT[(size_t)j * CP + i] = sK[e];
-      sRT[(size_t)j * CP + i] = sR[e];
+      sKT[(size_t)j * CP + i] = sK[i * LDD + j];
+      sRT[(size_t)j * CP + i] = sR[i * LDD + j];
     }
     __syncthreads();
     if constexpr (MODE == FWD_CHAIN) {
@@ -532,8 +558,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 aw = zero4(), as = zero4();
         // A[i][tau] = D1^T[i][tau] (x cC_tau or b_tau), B[tau][j] = K^T[j][tau]
-        mma_tile<CT, KC, KC>(aw, sD1, CP, i0, sKT, CP, j0, CP, cf.cC);
-        mma_tile<CT, KC, KC>(as, sD1, CP, i0, sKT, CP, j0, CP, cf.bb);
+        mma_tile<CT, KC, KC>(aw, sD1, LDC, i0, sKT, CP, j0, CP, cf.cC);
+        mma_tile<CT, KC, KC>(as, sD1, LDC, i0, sKT, CP, j0, CP, cf.bb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * D + j0 + (l & 15);
@@ -575,8 +601,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 aw = zero4(), as = zero4();
         // A[i][tau] = R^T[i][tau] (x cC_tau or b_tau), B[tau][j] = Hk[tau][j]
-        mma_tile<CT, KC, MC>(aw, sRT, CP, i0, sHk, HID, j0, CP, cf.cC);
-        mma_tile<CT, KC, MC>(as, sRT, CP, i0, sHk, HID, j0, CP, cf.bb);
+        mma_tile<CT, KC, MC>(aw, sRT, CP, i0, sHk, LDH, j0, CP, cf.cC);
+        mma_tile<CT, KC, MC>(as, sRT, CP, i0, sHk, LDH, j0, CP, cf.bb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const size_t e = (size_t)(i0 + 4 * (l >> 4) + r) * HID + j0 + (l & 15);
@@ -603,13 +629,13 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       for (int t = w; t < nt; t += NW) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
-        mma_tile<CT, KC, KC>(acc, sX, D, i0, sK, D, j0, D);
+        mma_tile<CT, KC, KC>(acc, sX, LDD, i0, sK, LDD, j0, D);
         f4 pv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
           pv[r] = j <= i ? cf.c[i][j] * acc[r] : 0.f;
-          sP[(size_t)i * CP + j] = from_f<CT>(pv[r]);
+          sP[(size_t)i * LDC + j] = from_f<CT>(pv[r]);
         }
         if (fr) {
           store4<float>(frf + RL.ff.o[rec::XK] + frag_ofs<CP, CP>(i0, j0, l), acc);
@@ -666,11 +692,11 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           f4 a1 = zero4(), a2 = zero4(), a3 = zero4();
 #pragma unroll
           for (int ks = 0; ks < NKD; ++ks) {
-            auto a = Mma<CT>::template load<KC>(sX, D, i0 + (l & 15), ks * KS + ko, D, nullptr);
+            auto a = Mma<CT>::template load<KC>(sX, LDD, i0 + (l & 15), ks * KS + ko, D, nullptr);
             Mma<CT>::mma(a1, a, bw[ks]);
             Mma<CT>::mma(a2, a, bs[ks]);
           }
-          mma_tile<CT, KC, KC>(a3, sP, CP, i0, sD1, CP, j0, CP);
+          mma_tile<CT, KC, KC>(a3, sP, LDC, i0, sD1, LDC, j0, CP);
           f4 hv, szv;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -678,11 +704,11 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             const float z = cf.A[i] * a1[r] + cf.E[i] * a2[r] - a3[r];
             if (fr) {
               const ActVals av = act_all<ACT>(z);
-              sH[(size_t)i * HID + j] = from_f<CT>(av.s);
+              sH[(size_t)i * LDH + j] = from_f<CT>(av.s);
               hv[r] = av.s;
               szv[r] = av.d1;
             } else {
-              sH[(size_t)i * HID + j] = from_f<CT>(act_f<ACT>(z));
+              sH[(size_t)i * LDH + j] = from_f<CT>(act_f<ACT>(z));
             }
           }
           if (fr) {
@@ -698,13 +724,13 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       for (int t = w; t < nt; t += NW) {
         const int i0 = (t / tn) * 16, j0 = (t % tn) * 16;
         f4 acc = zero4();
-        mma_tile<CT, KC, KC>(acc, sH, HID, i0, sHk, HID, j0, HID);
+        mma_tile<CT, KC, KC>(acc, sH, LDH, i0, sHk, LDH, j0, HID);
         f4 pv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
           pv[r] = j <= i ? cf.c[i][j] * acc[r] : 0.f;
-          sP[(size_t)i * CP + j] = from_f<CT>(pv[r]);
+          sP[(size_t)i * LDC + j] = from_f<CT>(pv[r]);
         }
         if (fr) {
           store4<float>(frf + RL.ff.o[rec::HH] + frag_ofs<CP, CP>(i0, j0, l), acc);
@@ -760,7 +786,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
           for (int kk = 0; kk < HALF; ++kk)
             if (hb + kk < NKH) {
-              auto a = Mma<CT>::template load<KC>(sH, HID, i0 + (l & 15), (hb + kk) * KS + ko, HID,
+              auto a = Mma<CT>::template load<KC>(sH, LDH, i0 + (l & 15), (hb + kk) * KS + ko, HID,
                                                   nullptr);
               Mma<CT>::mma(a1[x], a, bw[kk]);
               Mma<CT>::mma(a2[x], a, bs[kk]);
@@ -773,7 +799,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
         if (t >= nt) continue;
         const int i0 = (t / tn) * 16, j0 = cs * 16;
         f4 a3 = zero4();
-        mma_tile<CT, KC, MC>(a3, sP, CP, i0, sR, D, j0, CP);
+        mma_tile<CT, KC, MC>(a3, sP, LDC, i0, sR, LDD, j0, CP);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
@@ -795,8 +821,9 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 template <typename IO, typename CT, int ACT, int D, int HID, int CP>
 static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err, size_t* bytes) {
   if (a.D.d != D || a.D.hid != HID || a.D.Cp != CP || a.D.act != ACT) return false;
-  constexpr size_t lds = fwd_fast_lds_bytes<CT, D, HID, CP>();
-  if (lds + sizeof(CoefF) > 160 * 1024) return false;
+  constexpr size_t lds = fwd_fast_lds_bytes<CT, D, HID, CP, 0>();
+  constexpr size_t lds_ret = fwd_fast_lds_bytes<CT, D, HID, CP, fwd_pad<FWD_RET>()>();
+  if (lds + sizeof(CoefFN<CP>) > 160 * 1024 || lds_ret + sizeof(CoefFN<CP>) > 160 * 1024) return false;
   const int nch = a.D.S / a.D.C;
   if (bytes) {  // size query: the split forward's per-chunk buffer
     *bytes = (size_t)units * nch * fwd_split_elems<D, HID, CP>() * sizeof(CT);
@@ -807,7 +834,7 @@ static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
     auto k1 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
     auto k2 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
     if (!lds_fits((const void*)k0, lds) || !lds_fits((const void*)k1, lds) ||
-        !lds_fits((const void*)k2, lds)) {
+        !lds_fits((const void*)k2, lds_ret)) {
       *err = hipErrorInvalidConfiguration;
       return true;
     }
@@ -829,7 +856,7 @@ static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
     }
     auto kr = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
     set_lds_limit((const void*)kr);
-    hipLaunchKernelGGL(kr, dim3(units * nch), dim3(512), lds, st, a);
+    hipLaunchKernelGGL(kr, dim3(units * nch), dim3(512), lds_ret, st, a);
   } else {
     auto kern = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_FULL>;
     set_lds_limit((const void*)kern);
