@@ -153,7 +153,8 @@ _COMMON = ["tnt_device.h", "tnt_kernels.h"]
 LAUNCH_SOURCES = {
     "local_bwd": ["tnt_local_bwd_split.hip", "tnt_local_bwd_helpers.h", "tnt_local_common.h",
                   "tnt_local_record.h"] + _COMMON,
-    "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_walk.hip", "tnt_regtile.h", "tnt_local_common.h",
+    "local_fwd": ["tnt_local_fwd_fast.hip", "tnt_local_walk.hip", "tnt_local_ret.hip", "tnt_regtile.h",
+                  "tnt_local_common.h",
                   "tnt_local_record.h"] + _COMMON,
     "local_carry": ["tnt_local_walk.hip", "tnt_regtile.h", "tnt_local_common.h",
                     "tnt_local_record.h"] + _COMMON,

@@ -166,6 +166,8 @@ size_t local_fwd_split_bytes(const Dims& D, int units);  // 0: no fixed-size for
 bool launch_local_fwd_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err);
 // the register-resident forward walk (saved states, fixed sizes); false: not built for `a`
 bool launch_local_walk(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err);
+// the retrieval of every (unit, chunk) after the walk (same shapes); false: not built for `a`
+bool launch_local_ret(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err);
 hipError_t launch_pack_states(const float* states, const float* mstates, void* out, int units,
                                int nslots, int d, int hid, int with_m, int bf16, hipStream_t st);
 hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st);

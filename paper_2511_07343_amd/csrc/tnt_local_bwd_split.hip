@@ -248,7 +248,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
           const int ii = i + r;
           const float x = acc[rb][cb][r];
           const bool lo = j <= ii;
-          qv[r] = lo ? cf.c[ii][j] * x : 0.f;
+          qv[r] = lo ? cf.cc(ii, j) * x : 0.f;
           Q1[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
           fCb[ii * Cp + j] = lo ? -hh[r] * x : 0.f;
         }
@@ -297,7 +297,7 @@ __global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, Spli
           const int ii = i + r;
           const float x = acc[rb][cb][r];
           const bool lo = j <= ii;
-          qv[r] = lo ? cf.c[ii][j] * x : 0.f;
+          qv[r] = lo ? cf.cc(ii, j) * x : 0.f;
           Q2[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
           if (lo) fCb[ii * Cp + j] -= xk[r] * x;
         }

@@ -44,26 +44,32 @@ __device__ __forceinline__ void affine_scan_up(float& a, float& b) {  // inclusi
     }
   }
 }
-template <int STRIDE>
-__device__ __forceinline__ void coef_columns(const float* la, const float* lb, const float* eta,
-                                             int Cp, float (*ct)[STRIDE], float (*c)[STRIDE],
-                                             float* E) {
+// `put(r, tau, ct)` receives ct_{r,tau} for every row r < Cp of every column.
+template <typename Put>
+__device__ __forceinline__ void coef_scan_columns(const float* la, const float* lb, int Cp,
+                                                  const Put& put, float* E) {
   const int r = lane_id();
   const float lar = la[r < Cp ? r : Cp - 1], lbr = lb[r < Cp ? r : Cp - 1];
   const float ar = r > 0 && r < Cp ? expf(lar - la[r - 1]) : 0.f;
   for (int tau = wave_id(); tau < Cp; tau += num_waves()) {
     float a = ar, b = (r >= tau && r < Cp) ? expf(lbr - lb[tau]) : 0.f;
     affine_scan_up(a, b);
-    if (r < Cp) {
-      if (ct) ct[r][tau] = b;
-      c[r][tau] = eta[tau] * b;
-    }
+    if (r < Cp) put(r, tau, b);
   }
   if (wave_id() == 0) {
     float a = ar, b = r < Cp ? expf(lbr) : 0.f;
     affine_scan_up(a, b);
     if (r < Cp) E[r] = b;
   }
+}
+template <int STRIDE>
+__device__ __forceinline__ void coef_columns(const float* la, const float* lb, const float* eta,
+                                             int Cp, float (*ct)[STRIDE], float (*c)[STRIDE],
+                                             float* E) {
+  coef_scan_columns(la, lb, Cp, [&](int r, int tau, float b) {
+    if (ct) ct[r][tau] = b;
+    c[r][tau] = eta[tau] * b;
+  }, E);
 }
 
 // Fill `cf` for the chunk whose first token is `tok0` (gate arrays already
@@ -108,10 +114,15 @@ __device__ __forceinline__ void chunk_coefs(Coef& cf, const float* lr, const flo
 template <int N>
 struct CoefFN {
   static_assert(N <= MAXC, "one wave scans a chunk");
-  float c[N][N + 1];
+  // the lower triangle of c (c_{i,tau} = 0 for tau > i), row after row:
+  // c_{i,tau} at i (i + 1) / 2 + tau
+  float c[N * (N + 1) / 2];
   float A[N], E[N], la[N], lb[N], eta[N], cC[N], bb[N];
   float knorm[N];
   float AC, BC, EC;
+  // c_{i,j}; for j > i the value read is another entry's, to be masked by the
+  // caller (every index stays inside the array)
+  __device__ __forceinline__ float cc(int i, int j) const { return c[i * (i + 1) / 2 + j]; }
 };
 using CoefF = CoefFN<MAXC>;
 
@@ -134,14 +145,16 @@ __device__ __forceinline__ void chunk_coefs_f(CoefFN<N>& cf, const float* lr, co
     }
   }
   __syncthreads();
-  coef_columns<N + 1>(cf.la, cf.lb, cf.eta, Cp, nullptr, cf.c, cf.E);
+  coef_scan_columns(cf.la, cf.lb, Cp, [&](int r, int tau, float b) {
+    if (tau <= r) cf.c[r * (r + 1) / 2 + tau] = cf.eta[tau] * b;
+  }, cf.E);
   __syncthreads();
   if (wave_id() == 0) {
     const int tau = lane_id();
     if (tau < Cp) {
       const float et = (tau < C) ? expf(cf.lb[C - 1] - cf.lb[tau]) : 0.f;
       cf.bb[tau] = cf.eta[tau] * et;
-      cf.cC[tau] = cf.c[C - 1][tau];
+      cf.cC[tau] = tau < C ? cf.cc(C - 1, tau) : 0.f;
     }
     if (tau == 0) {
       cf.AC = cf.A[C - 1];

@@ -23,11 +23,8 @@
 
 namespace tnt {
 
-// LDS carve-up (CT elements).  Rows of every matrix are PD elements longer
-// than the matrix (leading dimensions LDD, LDC, LDH): with PD = 8 the 16-byte
-// operand reads of consecutive rows start 16 bytes apart in the bank cycle
-// instead of on the same banks (rows of 128 or 512 bytes).  The retrieval
-// mode pads; the walk modes, whose LDS also holds a copy of W2, do not.
+// LDS carve-up (CT elements); leading dimensions LDD, LDC, LDH are the
+// matrices' own widths plus PD (0 here: the walk modes' LDS also holds W2).
 template <int D, int HID, int CP, int PD>
 struct FwdLds {
   static constexpr int cmax(int x, int y) { return x > y ? x : y; }
@@ -51,11 +48,6 @@ struct FwdLds {
                 "16-byte aligned rows");
 };
 
-template <int MODE>
-constexpr int fwd_pad() {
-  return MODE == 2 ? 8 : 0;  // FWD_RET pads its rows
-}
-
 template <typename CT, int D, int HID, int CP, int PD>
 constexpr size_t fwd_fast_lds_bytes() {
   return (size_t)FwdLds<D, HID, CP, PD>::total * sizeof(CT);
@@ -65,9 +57,11 @@ constexpr size_t fwd_fast_lds_bytes() {
 // does everything.  When every chunk-entry state is saved, the walk is split:
 // FWD_CHAIN walks the chunks doing only what the next state needs (keys, the
 // chunk gradient, the carry, the Q-K sum) and leaves Hk, D1^T and R of every
-// chunk in a buffer; FWD_RET then takes the retrieval of every (unit, chunk) at
-// once, one workgroup each, from the saved entry state and that buffer.
-enum { FWD_FULL = 0, FWD_CHAIN = 1, FWD_RET = 2 };
+// chunk in a buffer (for the shapes and kernel families the register-resident
+// walk does not take); local_ret_kernel then takes the retrieval of every
+// (unit, chunk) at once, one workgroup each, from the saved entry state and
+// that buffer.
+enum { FWD_FULL = 0, FWD_CHAIN = 1 };
 
 // per-chunk buffer of the split forward: Hk [CP][HID], D1^T [HID][CP], R [CP][D]
 template <int D, int HID, int CP>
@@ -77,13 +71,11 @@ constexpr size_t fwd_split_elems() {
 
 template <typename IO, typename CT, int ACT, int D, int HID, int CP, int MODE>
 __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
-  constexpr bool WALK = MODE != FWD_RET, RETR = MODE != FWD_CHAIN;
+  constexpr bool WALK = true, RETR = MODE != FWD_CHAIN;
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ CoefFN<CP> cf;  // the coefficients of a CP-row chunk
-  constexpr int PD = fwd_pad<MODE>();
-  using Ly = FwdLds<D, HID, CP, PD>;
+  using Ly = FwdLds<D, HID, CP, 0>;
   constexpr int LDD = Ly::LDD, LDC = Ly::LDC, LDH = Ly::LDH;
-  static_assert(PD == 0 || !WALK, "the walk modes keep unpadded rows (their U holds W2)");
   constexpr int NW = 8;                       // waves
   constexpr int TNH = HID / 16, TMC = CP / 16;
   constexpr int KS = Mma<CT>::KS;
@@ -104,7 +96,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   const int C = Dm.C;
   const int nshard = Dm.L / Dm.S;
   const int nch = Dm.S / C;
-  const int u = MODE == FWD_RET ? (int)blockIdx.x / nch : (int)blockIdx.x;
+  const int u = (int)blockIdx.x;
   const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
   constexpr size_t hd = (size_t)HID * D;
   const size_t chain = (size_t)b * Dm.H + hh;
@@ -155,9 +147,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
   }
   __syncthreads();
 
-  const int n_begin = MODE == FWD_RET ? (int)blockIdx.x % nch : 0;
-  const int n_end = MODE == FWD_RET ? n_begin + 1 : nch;
-  for (int n = n_begin; n < n_end; ++n) {
+  for (int n = 0; n < nch; ++n) {
     CT* const fsn = (MODE == FWD_FULL) ? nullptr : (CT*)a.fsplit + ((size_t)u * nch + n) * FS;
     // the chunk's forward record (walk: s'(Zk), s''(Zk), G; retrieval: the rest)
     CT* const fr = (MODE != FWD_FULL && a.frec) ? (CT*)a.frec + ((size_t)u * nch + n) * RL.fc.n : nullptr;
@@ -266,109 +256,6 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       }
     }
 
-    if constexpr (MODE == FWD_RET) {
-      // Hk, D1^T, R of this chunk, left by the walk
-      constexpr int V8 = 16 / sizeof(CT);
-      for (size_t e = threadIdx.x * V8; e < FS; e += blockDim.x * V8) {
-        const bf16x8 x = *reinterpret_cast<const bf16x8*>(fsn + e);
-        const size_t e1 = e - (size_t)CP * HID, e2 = e - 2 * (size_t)CP * HID;
-        CT* dst = e < (size_t)CP * HID ? sHk + (e / HID) * LDH + e % HID
-                  : e < 2 * (size_t)CP * HID ? sD1 + (e1 / CP) * LDC + e1 % CP
-                                             : sR + (e2 / D) * LDD + e2 % D;
-        *reinterpret_cast<bf16x8*>(dst) = x;
-      }
-      __syncthreads();
-      if (fr) {
-        // the forward record: K, Q, N, Str, X, R, Hk, D1 and their scaled / transposed
-        // forms from LDS (destination-ordered writes), per-position coefficients
-        CT* const rp = fr;
-        // eight destination elements per thread, 16-byte stores; transposed
-        // destinations gather their eight sources from LDS
-        auto st8 = [&](int field, size_t e0, const float (&x)[8]) {
-          bf16x8 v;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] = (__bf16)x[q];
-          *reinterpret_cast<bf16x8*>(rp + RL.fc.o[field] + e0) = v;
-        };
-        auto cp8 = [&](int field, size_t e0, const CT* src) {
-          *reinterpret_cast<bf16x8*>(rp + RL.fc.o[field] + e0) = *reinterpret_cast<const bf16x8*>(src);
-        };
-        for (int v = threadIdx.x; v < CP * D / 8; v += blockDim.x) {
-          const size_t e0 = (size_t)v * 8;
-          const int i = (int)(e0 / D);                       // row-major: one row
-          const int jt = (int)(e0 / CP), it = (int)(e0 % CP);  // transposed [D][CP]: rows it..it+7
-          const size_t ed = (e0 / D) * LDD + e0 % D;       // [CP][D] element e0 in LDS
-          const size_t ec = (e0 / CP) * LDC + e0 % CP;     // [D][CP] element e0 in LDS
-          cp8(rec::K, e0, sK + ed);
-          cp8(rec::R, e0, sR + ed);
-          cp8(rec::X, e0, sX + ed);
-          float kc[8], kb[8], rc[8], rb[8], kt[8], rt[8], xt[8], xa[8], xe[8], qt[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const float kx = to_f(sK[ed + q]), rx = to_f(sR[ed + q]);
-            kc[q] = cf.cC[i] * kx;
-            kb[q] = cf.bb[i] * kx;
-            rc[q] = cf.cC[i] * rx;
-            rb[q] = cf.bb[i] * rx;
-            const size_t es = (size_t)(it + q) * LDD + jt;
-            kt[q] = to_f(sK[es]);
-            rt[q] = to_f(sR[es]);
-            xt[q] = to_f(sX[es]);
-            xa[q] = cf.A[it + q] * xt[q];
-            xe[q] = cf.E[it + q] * xt[q];
-            qt[q] = to_f(sQ[es]);
-          }
-          st8(rec::KcC, e0, kc);
-          st8(rec::Kb, e0, kb);
-          st8(rec::RcC, e0, rc);
-          st8(rec::Rb, e0, rb);
-          st8(rec::KT, e0, kt);
-          st8(rec::RT, e0, rt);
-          st8(rec::XT, e0, xt);
-          st8(rec::XAT, e0, xa);
-          st8(rec::XET, e0, xe);
-          st8(rec::QT, e0, qt);
-          if (qk) {
-            cp8(rec::N, e0, sN + ed);
-            cp8(rec::NT, e0, sNT + ec);
-          }
-        }
-        if (qk)
-          for (int v = threadIdx.x; v < CP * CP / 8; v += blockDim.x) {
-            const size_t e0 = (size_t)v * 8;
-            const int jt = (int)(e0 / CP), it = (int)(e0 % CP);
-            float x[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) x[q] = to_f(sS[(size_t)(it + q) * LDC + jt]);
-            st8(rec::StrT, e0, x);
-          }
-        for (int v = threadIdx.x; v < CP * HID / 8; v += blockDim.x) {
-          const size_t e0 = (size_t)v * 8;
-          const int jt = (int)(e0 / CP), it = (int)(e0 % CP);    // [HID][CP]
-          const int i = (int)(e0 / HID), j = (int)(e0 % HID);    // [CP][HID]
-          cp8(rec::Hk, e0, sHk + (size_t)i * LDH + j);
-          float ht[8], d1[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            ht[q] = to_f(sHk[(size_t)(it + q) * LDH + jt]);
-            d1[q] = to_f(sD1[(size_t)(j + q) * LDC + i]);
-          }
-          st8(rec::HkT, e0, ht);
-          st8(rec::D1, e0, d1);
-        }
-        if (threadIdx.x < CP) {
-          const int i = threadIdx.x;
-          frf[RL.ff.o[rec::kn] + i] = cf.knorm[i];
-          frf[RL.ff.o[rec::cC] + i] = cf.cC[i];
-          frf[RL.ff.o[rec::bb] + i] = cf.bb[i];
-        }
-        if (threadIdx.x == 0) {
-          frf[RL.ff.o[rec::sc] + 0] = cf.AC;
-          frf[RL.ff.o[rec::sc] + 1] = cf.BC;
-          frf[RL.ff.o[rec::sc] + 2] = cf.EC;
-        }
-      }
-    }
     if constexpr (WALK) {
     // ---- Zk = K W1^T -> Hk (LDS), s'(Zk) (registers); each wave owns NS column strips
     CT spr[NS][TMC][4];  // s'(Zk) in the compute type
@@ -413,13 +300,14 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             auto a = Mma<CT>::template load<KC>(sK, LDD, i0 + (l & 15), ks * KS + ko, D, nullptr);
             Mma<CT>::mma(acc, a, bw[y][ks]);
           }
-          f4 d1v, d2v;
+          f4 hv, d1v, d2v;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
             const ActVals av = act_all<ACT>(acc[r]);
             sHk[(size_t)i * LDH + j] = from_f<CT>(av.s);
             spr[y][it][r] = from_f<CT>(av.d1);
+            hv[r] = av.s;
             d1v[r] = av.d1;
             d2v[r] = av.d2;
           }
@@ -427,6 +315,8 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
             const size_t fo = frag_ofs<CP, HID>(i0, j0, l);
             store4<CT>(fr + RL.fc.o[rec::Sp] + fo, d1v);
             store4<CT>(fr + RL.fc.o[rec::Spp] + fo, d2v);
+            // Hk^T [HID][CP]: the lane's four rows are contiguous
+            store4<CT>(fr + RL.fc.o[rec::HkT] + (size_t)(j0 + (l & 15)) * CP + i0 + 4 * (l >> 4), hv);
           }
         }
       }
@@ -505,12 +395,19 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
           mma_tile<CT, KC, KC>(acc, sR, LDD, i0, sW2, D, j0, D);  // sW2 = W2^T
         else
           mma_tile<CT, KC, MC>(acc, sR, LDD, i0, sW2, HID, j0, D);
+        f4 dv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          sD1[(size_t)j * LDC + i] = from_f<CT>(acc[r] * to_f(spr[y][it][r]));  // D1^T
+          dv[r] = acc[r] * to_f(spr[y][it][r]);
+          sD1[(size_t)j * LDC + i] = from_f<CT>(dv[r]);  // D1^T
         }
-        if (MODE == FWD_CHAIN && fr) store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(i0, j0, l), acc);
+        if (MODE == FWD_CHAIN && fr) {
+          store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(i0, j0, l), acc);
+          CT* const d1r = fr + RL.fc.o[rec::D1] + (size_t)(i0 + 4 * (l >> 4)) * HID + j0 + (l & 15);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) d1r[(size_t)r * HID] = from_f<CT>(dv[r]);  // D1 [CP][HID]
+        }
       }
     }
     __syncthreads();
@@ -525,12 +422,14 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
     }
     __syncthreads();
     if constexpr (MODE == FWD_CHAIN) {
-      // Hk, D1^T, R for the retrieval pass (LDS reads only; overlaps the carry)
+      // Hk (into the forward record when there is one), D1^T, R for the retrieval
+      // pass (LDS reads only; overlaps the carry)
       for (size_t e = threadIdx.x * 8; e < FS; e += blockDim.x * 8) {
         const CT* src = e < (size_t)CP * HID ? sHk + e
                         : e < 2 * (size_t)CP * HID ? sD1 + (e - (size_t)CP * HID)
                                                    : sR + (e - 2 * (size_t)CP * HID);
-        *reinterpret_cast<bf16x8*>(fsn + e) = *reinterpret_cast<const bf16x8*>(src);
+        CT* dst = (fr && e < (size_t)CP * HID) ? fr + RL.fc.o[rec::Hk] + e : fsn + e;
+        *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(src);
       }
     }
     {
@@ -634,7 +533,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          pv[r] = j <= i ? cf.c[i][j] * acc[r] : 0.f;
+          pv[r] = j <= i ? cf.cc(i, j) * acc[r] : 0.f;
           sP[(size_t)i * LDC + j] = from_f<CT>(pv[r]);
         }
         if (fr) {
@@ -644,36 +543,13 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
       }
     }
     {
-      // the retrieval's W1, S1 from the walk's bf16 copies W1^T, S1^T [D][HID] (the same
-      // rounding as a conversion of the fp32 state at load): contraction-major reads, half
-      // the bytes, every strip's requested before the barrier
-      typename Mma<CT>::frag bwr[MODE == FWD_RET ? NS : 1][NKD], bsr[MODE == FWD_RET ? NS : 1][NKD];
-      if constexpr (MODE == FWD_RET)
-#pragma unroll
-        for (int y = 0; y < NS; ++y) {
-          const int sidx = w + NW * y;
-          if (sidx < TNH)
-#pragma unroll
-            for (int ks = 0; ks < NKD; ++ks) {
-              bwr[y][ks] = Mma<CT>::template load<MC>(pkc, HID, sidx * 16 + (l & 15), ks * KS + ko, D,
-                                                      nullptr);
-              bsr[y][ks] = Mma<CT>::template load<MC>(pkc + 2 * hd, HID, sidx * 16 + (l & 15),
-                                                      ks * KS + ko, D, nullptr);
-            }
-        }
       __syncthreads();  // P ready; K^T / R^T in U are dead
 #pragma unroll
       for (int y = 0; y < NS; ++y) {
         const int sidx = w + NW * y;
         if (sidx >= TNH) continue;
         typename Mma<CT>::frag bw[NKD], bs[NKD];
-        if constexpr (MODE == FWD_RET) {
-#pragma unroll
-          for (int ks = 0; ks < NKD; ++ks) {
-            bw[ks] = bwr[y][ks];
-            bs[ks] = bsr[y][ks];
-          }
-        } else {
+        {
           RawFrag<CT, float> rw[NKD], rs[NKD];
 #pragma unroll
           for (int ks = 0; ks < NKD; ++ks) {
@@ -729,7 +605,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = i0 + 4 * (l >> 4) + r, j = j0 + (l & 15);
-          pv[r] = j <= i ? cf.c[i][j] * acc[r] : 0.f;
+          pv[r] = j <= i ? cf.cc(i, j) * acc[r] : 0.f;
           sP[(size_t)i * LDC + j] = from_f<CT>(pv[r]);
         }
         if (fr) {
@@ -751,16 +627,7 @@ __global__ void __launch_bounds__(512) local_fwd_fast_kernel(LocalFwdArgs a) {
 #pragma unroll
       for (int hb = 0; hb < NKH; hb += HALF) {
         typename Mma<CT>::frag bw[HALF], bs[HALF];
-        if constexpr (MODE == FWD_RET) {  // W2^T, S2^T [HID][D] of the walk
-#pragma unroll
-          for (int kk = 0; kk < HALF; ++kk)
-            if (hb + kk < NKH) {
-              bw[kk] = Mma<CT>::template load<MC>(pkc + hd, D, cs * 16 + (l & 15), (hb + kk) * KS + ko,
-                                                  HID, nullptr);
-              bs[kk] = Mma<CT>::template load<MC>(pkc + 3 * hd, D, cs * 16 + (l & 15),
-                                                  (hb + kk) * KS + ko, HID, nullptr);
-            }
-        } else {
+        {
           RawFrag<CT, float> rw[HALF], rs[HALF];
 #pragma unroll
           for (int kk = 0; kk < HALF; ++kk)
@@ -822,8 +689,7 @@ template <typename IO, typename CT, int ACT, int D, int HID, int CP>
 static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_t* err, size_t* bytes) {
   if (a.D.d != D || a.D.hid != HID || a.D.Cp != CP || a.D.act != ACT) return false;
   constexpr size_t lds = fwd_fast_lds_bytes<CT, D, HID, CP, 0>();
-  constexpr size_t lds_ret = fwd_fast_lds_bytes<CT, D, HID, CP, fwd_pad<FWD_RET>()>();
-  if (lds + sizeof(CoefFN<CP>) > 160 * 1024 || lds_ret + sizeof(CoefFN<CP>) > 160 * 1024) return false;
+  if (lds + sizeof(CoefFN<CP>) > 160 * 1024) return false;
   const int nch = a.D.S / a.D.C;
   if (bytes) {  // size query: the split forward's per-chunk buffer
     *bytes = (size_t)units * nch * fwd_split_elems<D, HID, CP>() * sizeof(CT);
@@ -832,9 +698,7 @@ static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
   {  // the compiled static LDS of every mode, not the estimate
     auto k0 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_FULL>;
     auto k1 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_CHAIN>;
-    auto k2 = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
-    if (!lds_fits((const void*)k0, lds) || !lds_fits((const void*)k1, lds) ||
-        !lds_fits((const void*)k2, lds_ret)) {
+    if (!lds_fits((const void*)k0, lds) || !lds_fits((const void*)k1, lds)) {
       *err = hipErrorInvalidConfiguration;
       return true;
     }
@@ -854,9 +718,12 @@ static bool try_fast(const LocalFwdArgs& a, int units, hipStream_t st, hipError_
       *err = we;
       return true;
     }
-    auto kr = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_RET>;
-    set_lds_limit((const void*)kr);
-    hipLaunchKernelGGL(kr, dim3(units * nch), dim3(512), lds_ret, st, a);
+    hipError_t re = hipSuccess;
+    if (!launch_local_ret(a, units, st, &re)) re = hipErrorInvalidConfiguration;
+    if (re != hipSuccess) {
+      *err = re;
+      return true;
+    }
   } else {
     auto kern = local_fwd_fast_kernel<IO, CT, ACT, D, HID, CP, FWD_FULL>;
     set_lds_limit((const void*)kern);

@@ -34,8 +34,9 @@
 //
 // Per chunk the walk writes what the chunk-parallel retrieval and the
 // backward read: the compute-type transposes of the next state slot, the Q-K
-// sum (fp32 and transposed), Hk, D1^T and R of the chunk, and the forward
-// record's s'(Zk), s''(Zk) and G.  Nothing is read back from memory.
+// sum (fp32 and transposed), D1^T and R of the chunk for the retrieval, and
+// the forward record's Hk, Hk^T, D1, s'(Zk), s''(Zk) and G (without a record,
+// Hk goes to the retrieval's buffer).  Nothing is read back from memory.
 #include "tnt_local_common.h"
 #include "tnt_local_record.h"
 #include "tnt_regtile.h"
@@ -306,6 +307,8 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
           const size_t fo = frag_ofs<CP, HID>(it * 16, j0, l);
           store4<CT>(fr + RL.fc.o[rec::Sp] + fo, d1v);
           store4<CT>(fr + RL.fc.o[rec::Spp] + fo, d2v);
+          // Hk^T [HID][CP]: the lane's four rows are contiguous
+          store4<CT>(fr + RL.fc.o[rec::HkT] + (size_t)(j0 + lc) * CP + it * 16 + 4 * g, hv);
         }
       }
     }
@@ -372,15 +375,22 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) dv[r] = acc[r] * (float)sp[r];
         d1[it][ht] = cvt4(dv);
-        if (fr) store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(it * 16, j0, l), acc);
+        if (fr) {
+          store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(it * 16, j0, l), acc);
+          CT* const d1r = fr + RL.fc.o[rec::D1] + (size_t)(it * 16 + 4 * g) * HID + j0 + lc;  // [CP][HID]
+#pragma unroll
+          for (int r = 0; r < 4; ++r) d1r[(size_t)r * HID] = (CT)dv[r];
+        }
         // D1^T [HID][CP] for the retrieval: the lane's four rows are contiguous
         store4<CT>(fsn + (size_t)CP * HID + (size_t)(j0 + lc) * CP + it * 16 + 4 * g, dv);
       }
     }
-    // Hk [CP][HID] and R [CP][D] for the retrieval (LDS -> 16-byte stores)
+    // Hk [CP][HID] (into the forward record when there is one, else the
+    // retrieval's buffer) and R [CP][D] for the retrieval (LDS -> 16-byte stores)
+    CT* const hkd = fr ? fr + RL.fc.o[rec::Hk] : fsn;
     for (int e = threadIdx.x * 8; e < CP * HID; e += blockDim.x * 8) {
       const int i = e / HID, j = e - i * HID;
-      *reinterpret_cast<bf16x8*>(fsn + e) = *reinterpret_cast<const bf16x8*>(sHk + (size_t)i * LH + j);
+      *reinterpret_cast<bf16x8*>(hkd + e) = *reinterpret_cast<const bf16x8*>(sHk + (size_t)i * LH + j);
     }
     for (int e = threadIdx.x * 8; e < CP * D; e += blockDim.x * 8) {
       const int i = e / D, j = e - i * D;
