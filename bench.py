@@ -354,6 +354,10 @@ def main():
                     help="override the workload's sequence length (global chunk and local "
                          "shard are capped at it); the counter summaries then do not apply")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch")
+    ap.add_argument("--local-chunk", type=int, default=0, metavar="C",
+                    help="override every local memory's chunk C_L (the small chunks of the "
+                         "second training stage, C_L in {1, 2, 4}); the counter summaries then "
+                         "do not apply")
     ap.add_argument("--decode", type=int, default=0, metavar="T",
                     help="time the step-wise forward (tnt_mem_step) with T tokens per chain "
                          "per call instead of the fwd+bwd step")
@@ -372,11 +376,11 @@ def main():
     cfg = inputs.WORKLOADS[args.workload]
     seed = args.workload
     prof_key = args.workload  # committed counter summaries describe the unmodified workloads
-    if args.seq or args.batch:
+    if args.seq or args.batch or args.local_chunk:
         import dataclasses
         L = args.seq or cfg.L
         B = args.batch or cfg.B
-        loc = tuple((c, min(s_, L)) for c, s_ in cfg.locals_)
+        loc = tuple((args.local_chunk or c, min(s_, L)) for c, s_ in cfg.locals_)
         cfg = dataclasses.replace(
             cfg, B=B, L=L, C_G=min(cfg.C_G, L), locals_=loc,
             name=f"{cfg.name.split(' B')[0]} B{B} H{cfg.H} L{L} d{cfg.d} h{cfg.hid} "
