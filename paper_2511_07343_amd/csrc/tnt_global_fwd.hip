@@ -25,12 +25,17 @@ namespace tnt {
 //        = e^{la_C - la_t} + beta_{t+1} s_{t+1}          (suffix affine scan)
 //   b_t  = eta_t e^{lb_C - lb_t},  E_C = beta_0 s_0.
 // The prefix sums la, lb and the suffix scan of s run as wavefront scans
-// joined across the workgroup's waves through LDS.
+// joined across the workgroup's waves through LDS.  When the chunk's records
+// fit in LDS (C_G <= GSCAN_STAGE_MAX) they are assembled there and written out
+// whole, consecutive threads on consecutive 16-byte pieces, so every 32-byte
+// record reaches memory as one full sector (the unused two floats as zeros).
 // ---------------------------------------------------------------------------
 constexpr int GSCAN_THREADS = 512;
 constexpr int GSCAN_WAVES = GSCAN_THREADS / WAVE;
+constexpr int GSCAN_STAGE_MAX = 4096;  // tokens of a chunk whose records are staged in LDS
 
-__global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a) {
+__global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a, int stage) {
+  extern __shared__ __align__(16) float srec[];           // [C][TKS] when staged
   __shared__ float wa[GSCAN_WAVES], wb[GSCAN_WAVES];      // per-wave gate log sums
   __shared__ float wp[GSCAN_WAVES], wq[GSCAN_WAVES];      // per-wave affine maps
   __shared__ float s_in[GSCAN_WAVES + 1];                 // s at each wave's end
@@ -40,7 +45,8 @@ __global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a
   const float* lr = a.lr + base;
   const float* mom = a.mom + base;
   const float* dec = a.decay + base;
-  float* tk = a.tokc + base * TKS;
+  float* const tkg = a.tokc + base * TKS;
+  float* const tk = stage ? srec : tkg;  // where the records are assembled
   const int l = lane_id(), w = wave_id(), t = threadIdx.x;
   const int E = (C + GSCAN_THREADS - 1) / GSCAN_THREADS;
   const int i0 = min(t * E, C), i1 = min(i0 + E, C);
@@ -69,6 +75,7 @@ __global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a
     pa += log_keep(dec[i]);
     pb += log_mom(mom[i]);
     *reinterpret_cast<float2*>(tk + (size_t)i * TKS + 2) = make_float2(pa, pb);
+    if (stage) *reinterpret_cast<float2*>(tk + (size_t)i * TKS + 6) = make_float2(0.f, 0.f);
   }
   // segment affine map s_{i0} = P s_{i1} + Q (own writes are visible to the thread)
   float P = 1.f, Q = 0.f;
@@ -119,11 +126,20 @@ __global__ void __launch_bounds__(GSCAN_THREADS) global_scan_kernel(GlobalArgs a
     cc[2] = (C > 0 ? mom[0] : 0.f) * sv;  // thread 0 ends at i = 0: sv = s_0
     cc[3] = 0.f;
   }
+  if (stage) {
+    __syncthreads();
+    static_assert(TKS % 4 == 0, "whole 16-byte pieces per record");
+    for (int e = t * 4; e < C * TKS; e += GSCAN_THREADS * 4)
+      *reinterpret_cast<f32x4*>(tkg + e) = *reinterpret_cast<const f32x4*>(srec + e);
+  }
 }
 
 hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st) {
   dim3 grid(a.D.L / a.D.C, a.D.B * a.D.H);
-  hipLaunchKernelGGL(global_scan_kernel, grid, dim3(GSCAN_THREADS), 0, st, a);
+  const int stage = a.D.C <= GSCAN_STAGE_MAX;
+  const size_t lds = stage ? (size_t)a.D.C * TKS * sizeof(float) : 0;
+  if (stage) set_lds_limit((const void*)global_scan_kernel);
+  hipLaunchKernelGGL(global_scan_kernel, grid, dim3(GSCAN_THREADS), lds, st, a, stage);
   return hipGetLastError();
 }
 
