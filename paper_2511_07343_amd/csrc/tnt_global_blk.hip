@@ -27,7 +27,11 @@ namespace tnt {
 
 namespace {
 
-constexpr int GTK = 256;  // tokens per split of the carry / state GEMMs
+// tokens per split of the carry / state GEMMs: the forward carry takes GTK_LONG
+// where the chunk length allows (fewer fp32 partials written and read back),
+// the backward's state GEMMs GTK
+constexpr int GTK = 256, GTK_LONG = 1024;
+inline int gtk_of(int C) { return C % GTK_LONG == 0 ? GTK_LONG : GTK; }
 
 template <int H>
 constexpr int gtile_rows() {
@@ -233,7 +237,7 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
 //   m = 0: D1^T (cC K) -> V1 slot,  m = 1: D1^T (b K) -> S1 slot   (hid x d)
 //   m = 2: (cC R)^T Hk -> V2 slot,  m = 3: (b R)^T Hk -> S2 slot   (d x hid)
 // ---------------------------------------------------------------------------
-template <typename CT, int D, int H>
+template <typename CT, int D, int H, int TK>
 __global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
   const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
   const int C = a.D.C;
@@ -241,7 +245,7 @@ __global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
   const CT* op = (const CT*)a.opT + (size_t)chain * (2 * (size_t)H + 4 * (size_t)D) * C;
   const CT *D1T = op, *HkT = D1T + (size_t)H * C, *KcT = HkT + (size_t)H * C,
            *KbT = KcT + (size_t)D * C, *RcT = KbT + (size_t)D * C, *RbT = RcT + (size_t)D * C;
-  const size_t k0 = (size_t)split * GTK;
+  const size_t k0 = (size_t)split * TK;
   float* P = a.part + ((size_t)chain * ns + split) * 4 * hd;
   if (m < 2) {
     using BK = Blk<H, D>;
@@ -250,7 +254,7 @@ __global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
     for_blocks<H, D>([&](int i0, int j0) {
       f4 acc[BK::RB][BK::CB];
       zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, D1T + k0, C, i0, B, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, D1T + k0, C, i0, B, C, j0);
       blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
@@ -263,7 +267,7 @@ __global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
     for_blocks<D, H>([&](int i0, int j0) {
       f4 acc[BK::RB][BK::CB];
       zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, A, C, i0, HkT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, A, C, i0, HkT + k0, C, j0);
       blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * H + j] = acc[rb][cb_][r];
@@ -517,7 +521,7 @@ __global__ void __launch_bounds__(512) gbwd_tile_kernel(GlobalArgs a, int n) {
 //   m = 0: Zkbar^T K + Zqbar^T Q            -> V1 slot (hid x d)
 //   m = 1: R^T Gbar + Ykbar^T Hk + dO^T Hq  -> V2 slot (d x hid)
 // ---------------------------------------------------------------------------
-template <typename CT, int D, int H>
+template <typename CT, int D, int H, int TK>
 __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
   const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
   const int C = a.D.C;
@@ -527,15 +531,15 @@ __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
            *HkT = GbT + (size_t)H * C, *HqT = HkT + (size_t)H * C, *KT = HqT + (size_t)H * C,
            *QT = KT + (size_t)D * C, *RT = QT + (size_t)D * C, *YkbT = RT + (size_t)D * C,
            *dOT = YkbT + (size_t)D * C;
-  const size_t k0 = (size_t)split * GTK;
+  const size_t k0 = (size_t)split * TK;
   float* P = a.part + ((size_t)chain * ns + split) * 4 * hd;
   if (m == 0) {
     using BK = Blk<H, D>;
     for_blocks<H, D>([&](int i0, int j0) {
       f4 acc[BK::RB][BK::CB];
       zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, ZkbT + k0, C, i0, KT + k0, C, j0);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, ZqbT + k0, C, i0, QT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, ZkbT + k0, C, i0, KT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, ZqbT + k0, C, i0, QT + k0, C, j0);
       blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) P[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
@@ -546,9 +550,9 @@ __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
     for_blocks<D, H>([&](int i0, int j0) {
       f4 acc[BK::RB][BK::CB];
       zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, RT + k0, C, i0, GbT + k0, C, j0);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, YkbT + k0, C, i0, HkT + k0, C, j0);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, GTK>(acc, dOT + k0, C, i0, HqT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, RT + k0, C, i0, GbT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, YkbT + k0, C, i0, HkT + k0, C, j0);
+      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, dOT + k0, C, i0, HqT + k0, C, j0);
       blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) P[hd + (size_t)(i + r) * H + j] = acc[rb][cb_][r];
@@ -578,9 +582,12 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H>;
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
-  const int ns = C / GTK;
+  const int tk = gtk_of(C), ns = C / tk;
   const int sec = section_begin("global_carry", st);
-  hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H>), dim3(ns, 4, chains), dim3(512), 0, st, a);
+  if (tk == GTK_LONG)
+    hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK_LONG>), dim3(ns, 4, chains), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK>), dim3(ns, 4, chains), dim3(512), 0, st, a);
   const hipError_t e = launch_global_carry_reduce(a, n, ns, st);
   section_end(sec, st);
   return e;
@@ -600,9 +607,9 @@ static hipError_t gbwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   auto k1 = gbwd_tile_kernel<IO, CT, ACT, D, H>;
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
-  const int ns = C / GTK;
+  const int ns = C / GTK;  // the longer splits measured slower here
   const int sec = section_begin("global_bwd_carry", st);
-  hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H>), dim3(ns, 2, chains), dim3(512), 0, st, a);
+  hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK>), dim3(ns, 2, chains), dim3(512), 0, st, a);
   const hipError_t e = launch_gbwd_state_reduce(a, n, ns, st);
   section_end(sec, st);
   return e;
@@ -629,6 +636,6 @@ bool launch_global_bwd_blk(const GlobalArgs& a, int n, hipStream_t st, hipError_
 }
 
 // splits used by the fixed-size path (the partial buffer must hold them)
-int global_blk_splits(const Dims& D) { return D.C / GTK; }
+int global_blk_splits(const Dims& D) { return D.C / GTK; }  // the larger count of the two
 
 }  // namespace tnt
