@@ -123,12 +123,15 @@ static void launch_gtranspose(const float* src, size_t src_stride, CT* dst, size
 template <typename IO, typename CT, int ACT, int D, int H>
 __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   constexpr int TT = gtile_rows<H>();
+  // rows padded by 16 bytes: the 16-byte operand reads of consecutive rows do
+  // not start on the same LDS banks
+  constexpr int LD = D + 8, LH = H + 8;
   extern __shared__ __align__(16) unsigned char smem[];
-  CT* sQ = reinterpret_cast<CT*>(smem);  // [TT][D], later R
-  CT* sK = sQ + TT * D;                  // [TT][D]
-  CT* sHq = sK + TT * D;                 // [TT][H]
-  CT* sHk = sHq + TT * H;                // [TT][H]
-  CT* sSp = sHk + TT * H;                // [TT][H]  s'(Zk)
+  CT* sQ = reinterpret_cast<CT*>(smem);  // [TT][LD], later R
+  CT* sK = sQ + TT * LD;                 // [TT][LD]
+  CT* sHq = sK + TT * LD;                // [TT][LH]
+  CT* sHk = sHq + TT * LH;               // [TT][LH]
+  CT* sSp = sHk + TT * LH;               // [TT][LH]  s'(Zk)
   __shared__ float cC[TT], bb[TT];
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -159,8 +162,8 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
     float qx[8], kx[8];
     gload8(q + (size_t)i * D + j0, qx);
     gload8(k + (size_t)i * D + j0, kx);
-    gstore8<CT>(sQ + (size_t)i * D + j0, qx);
-    gstore8<CT>(sK + (size_t)i * D + j0, kx);
+    gstore8<CT>(sQ + (size_t)i * LD + j0, qx);
+    gstore8<CT>(sK + (size_t)i * LD + j0, kx);
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       const size_t et = (size_t)(j0 + t) * C + r0 + i;
@@ -176,13 +179,13 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
     f4 aq[BH::RB][BH::CB], ak[BH::RB][BH::CB];
     zero_blk(aq);
     zero_blk(ak);
-    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(aq, sQ, D, i0, V1, D, j0);
-    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ak, sK, D, i0, V1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(aq, sQ, LD, i0, V1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ak, sK, LD, i0, V1, D, j0);
     blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
       f4 hv;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const size_t e = (size_t)(i + r) * H + j;
+        const size_t e = (size_t)(i + r) * LH + j;
         const ActVals z = act_all<ACT>(ak[rb][cb_][r]);
         sHq[e] = from_f<CT>(act_f<ACT>(aq[rb][cb_][r]));
         sHk[e] = from_f<CT>(z.s);
@@ -199,8 +202,8 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
     f4 ao[BD::RB][BD::CB], ay[BD::RB][BD::CB];
     zero_blk(ao);
     zero_blk(ay);
-    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ao, sHq, H, i0, V2, H, j0);
-    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ay, sHk, H, i0, V2, H, j0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ao, sHq, LH, i0, V2, H, j0);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ay, sHk, LH, i0, V2, H, j0);
     blk_each4<BD::RB, BD::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
       f4 rc, rbv;
 #pragma unroll
@@ -209,7 +212,7 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
         const size_t e = (size_t)ii * D + j;
         o[e] = ao[rb][cb_][r];
         const float rv = rscale * (ay[rb][cb_][r] - to_f(v[e]));
-        sR[e] = from_f<CT>(rv);
+        sR[(size_t)ii * LD + j] = from_f<CT>(rv);
         rc[r] = cC[ii] * rv;
         rbv[r] = bb[ii] * rv;
       }
@@ -222,11 +225,11 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   for_blocks<TT, H>([&](int i0, int j0) {
     f4 ag[BH::RB][BH::CB];
     zero_blk(ag);
-    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ag, sR, D, i0, V2T, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ag, sR, LD, i0, V2T, D, j0);
     blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
       f4 dv;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) dv[r] = ag[rb][cb_][r] * to_f(sSp[(size_t)(i + r) * H + j]);
+      for (int r = 0; r < 4; ++r) dv[r] = ag[rb][cb_][r] * to_f(sSp[(size_t)(i + r) * LH + j]);
       store4<CT>(D1T + (size_t)j * C + r0 + i, dv);
     });
   });
@@ -578,7 +581,7 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   constexpr size_t hd = (size_t)H * D;
   launch_gtranspose<CT>(a.states + (size_t)(n % a.nslots) * 4 * hd, (size_t)a.nslots * 4 * hd,
                         (CT*)a.packT, 4 * hd, (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
-  const size_t l1 = (2 * (size_t)TT * D + 3 * (size_t)TT * H) * sizeof(CT);
+  const size_t l1 = (2 * (size_t)TT * (D + 8) + 3 * (size_t)TT * (H + 8)) * sizeof(CT);  // padded rows
   auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H>;
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
