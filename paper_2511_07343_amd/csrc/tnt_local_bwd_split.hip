@@ -113,8 +113,11 @@ struct SplitPtrs {
 // ===========================================================================
 // pass A: backward of the retrieval of every chunk, from dO and the forward record
 // ===========================================================================
+// Chunks of at most 32 rows are built for 128 VGPRs: with their LDS (66 KB at 32
+// rows) two workgroups then share a CU and overlap each other's waits.
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
-__global__ void __launch_bounds__(512) local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CP <= 32 ? 4 : 1, 8)))
+local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
   __shared__ CoefF cf;
   __shared__ float gA[MAXC], gE[MAXC];
   __shared__ float dpa[D / 8][MAXC], dpe[D / 8][MAXC];  // partial dA, dE per 8-column block
