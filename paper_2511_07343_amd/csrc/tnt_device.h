@@ -275,6 +275,14 @@ __device__ __forceinline__ void for_blocks(F&& f) {
   for (int b = wave_id(); b < BK::NB; b += num_waves())
     f((b / BK::NBN) * BK::RB * 16, (b % BK::NBN) * BK::CB * 16);
 }
+// the same over the blocks of Blk<M, N, NWB> (NWB > 8: smaller blocks, several
+// per wave, fewer accumulators live at a time)
+template <int M, int N, int NWB, typename F>
+__device__ __forceinline__ void for_blocks_n(F&& f) {
+  using BK = Blk<M, N, NWB>;
+  for (int b = wave_id(); b < BK::NB; b += num_waves())
+    f((b / BK::NBN) * BK::RB * 16, (b % BK::NBN) * BK::CB * 16);
+}
 
 template <int RB, int CB>
 __device__ __forceinline__ void zero_blk(f4 (&a)[RB][CB]) {

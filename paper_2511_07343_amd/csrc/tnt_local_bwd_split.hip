@@ -37,36 +37,56 @@ namespace {
 // ---------------------------------------------------------------------------
 // temporaries (element offsets; CT = compute type)
 // ---------------------------------------------------------------------------
-// pass-A temporaries, one set per resident workgroup
-enum ATmpCT {
-  adO, adOA, adOE, aXb, aXbT,          // C x d
-  aQ1, aQ2, aQ2T, adXN, adXNT,         // C x C
-  A_CT
-};
-
 struct SplitLayout {
   rec::RecLayout r;
-  rec::Lay<A_CT> ac;
 };
 
 constexpr SplitLayout make_split_layout(int Cp, int d, int h) {
-  const size_t C = Cp, Cd = C * d, CC = C * C;
-  const size_t sac[A_CT] = {Cd, Cd, Cd, Cd, Cd, CC, CC, CC, CC, CC};
-  return SplitLayout{rec::make_rec_layout(Cp, d, h), rec::make_lay(sac)};
+  return SplitLayout{rec::make_rec_layout(Cp, d, h)};
 }
 
-constexpr int SPLIT_GRID_A = 512;  // resident pass-A workgroups (grid-stride over chunks)
+// Dynamic LDS of pass A (CT = compute type, fp32 where named):
+//   Zb   [CP][H] CT  Zbar (phases 2-4), then Kbar, Nbar [CP][D] fp32 each
+//   pA, pE  [(D/16)][CP] fp32  partial row sums of the Xbar epilogue
+//   U    one region used in turn:
+//        phases 0-2: dO [CP][D] CT, Q1 [CP][CP] CT, partial dA, dE [D/8][CP] fp32
+//        phases 3-:  Q2, Q2T [CP][CP] CT (later dXN, dXNT), Xbar [CP][D], Xbar^T [D][CP] CT
+// cbar stays in the registers of the wave that owns its tiles (phases 1 and 3
+// walk the same C x C blocks); the retrieval's dA, dE in the registers of the
+// thread of their position.  About 66 KB at 64 rows with the chunk
+// coefficients' 10 KB: two workgroups per CU.
+template <typename CT, int CP, int D, int H>
+struct ALds {
+  static constexpr size_t cmax(size_t x, size_t y) { return x > y ? x : y; }
+  static constexpr size_t zb = 0;
+  static constexpr size_t pa = zb + cmax((size_t)CP * H * sizeof(CT), 2 * (size_t)CP * D * sizeof(float));
+  static constexpr size_t pe = pa + (size_t)(D / 16) * CP * sizeof(float);
+  static constexpr size_t u = pe + (size_t)(D / 16) * CP * sizeof(float);
+  // phases 0-2
+  static constexpr size_t dO = u;
+  static constexpr size_t q1 = dO + (size_t)CP * D * sizeof(CT);
+  static constexpr size_t dpa = q1 + (size_t)CP * CP * sizeof(CT);
+  static constexpr size_t dpe = dpa + (size_t)(D / 8) * CP * sizeof(float);
+  static constexpr size_t ua = dpe + (size_t)(D / 8) * CP * sizeof(float) - u;
+  // phases 3-
+  static constexpr size_t q2 = u;
+  static constexpr size_t q2t = q2 + (size_t)CP * CP * sizeof(CT);
+  static constexpr size_t xb = q2t + (size_t)CP * CP * sizeof(CT);
+  static constexpr size_t xbt = xb + (size_t)CP * D * sizeof(CT);
+  static constexpr size_t ub = xbt + (size_t)D * CP * sizeof(CT) - u;
+  static constexpr size_t total = u + cmax(ua, ub);
+  static_assert(pa % 16 == 0 && u % 16 == 0 && q1 % 16 == 0 && dpa % 16 == 0 && q2t % 16 == 0 &&
+                    xb % 16 == 0 && xbt % 16 == 0,
+                "16-byte aligned regions");
+};
 
-// dynamic LDS of pass A: cbar (CP x CP fp32), partial row sums pA, pE
-// ((D/16) x CP fp32 each), one CP x H compute-type slot (Zbar), the chunk's
-// compute-type temporaries (dO and its scaled forms, Xbar, Q1, Q2, dXN, ...)
+
 template <typename CT, int CP, int D, int H>
 constexpr size_t split_a_lds() {
-  return ((size_t)CP * CP + 2 * (size_t)(D / 16) * CP) * sizeof(float) + (size_t)CP * H * sizeof(CT) +
-         make_split_layout(CP, D, H).ac.n * sizeof(CT);
+  return ALds<CT, CP, D, H>::total;
 }
-// static LDS of pass A: the chunk coefficients and the per-row partial sums
-constexpr size_t SPLIT_A_STATIC = 24 * 1024;
+// static LDS of pass A: the chunk coefficients
+constexpr size_t SPLIT_A_STATIC = sizeof(CoefF);
 
 // pass B: a CP x H compute-type slot (Gbar, then Zkbar); T3, T4 and T5, T6
 // (fragment-major fp32, CP x D each; the T5/T6 space holds Zkbar^T, H x CP
@@ -113,21 +133,32 @@ struct SplitPtrs {
 // ===========================================================================
 // pass A: backward of the retrieval of every chunk, from dO and the forward record
 // ===========================================================================
-// Chunks of at most 32 rows are built for 128 VGPRs: with their LDS (66 KB at 32
-// rows) two workgroups then share a CU and overlap each other's waits.
+// Built for 128 VGPRs and ALds' LDS, so that two workgroups share a CU and
+// overlap each other's waits.  One workgroup per chunk: a grid-stride loop lets
+// the compiler hoist every per-lane address out of the loop, and at 128 VGPRs
+// those hoisted values spill.
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CP <= 32 ? 4 : 1, 8)))
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 8)))
 local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
   __shared__ CoefF cf;
-  __shared__ float gA[MAXC], gE[MAXC];
-  __shared__ float dpa[D / 8][MAXC], dpe[D / 8][MAXC];  // partial dA, dE per 8-column block
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int d = D, h = H, Cp = CP;
-  float* fCb = reinterpret_cast<float*>(smem);
-  float* pA = fCb + Cp * Cp;
-  float* pE = pA + (D / 16) * Cp;
-  CT* Zb = reinterpret_cast<CT*>(pE + (D / 16) * Cp);  // C x h slot
-  CT* const ta = Zb + CP * H;                           // compute-type temporaries
+  using AL = ALds<CT, CP, D, H>;
+  CT* const Zb = reinterpret_cast<CT*>(smem + AL::zb);  // C x h slot
+  float* const pA = reinterpret_cast<float*>(smem + AL::pa);
+  float* const pE = reinterpret_cast<float*>(smem + AL::pe);
+  CT* const dO = reinterpret_cast<CT*>(smem + AL::dO);
+  CT* const Q1 = reinterpret_cast<CT*>(smem + AL::q1);
+  float* const dpa = reinterpret_cast<float*>(smem + AL::dpa);  // [D/8][CP] partial dA, dE
+  float* const dpe = reinterpret_cast<float*>(smem + AL::dpe);
+  CT* const Q2 = reinterpret_cast<CT*>(smem + AL::q2);
+  CT* const Q2T = reinterpret_cast<CT*>(smem + AL::q2t);
+  CT* const dXN = Q2;    // the Q-K phase, once Q2 and Q2^T are dead
+  CT* const dXNT = Q2T;
+  CT* const Xb = reinterpret_cast<CT*>(smem + AL::xb);
+  CT* const XbT = reinterpret_cast<CT*>(smem + AL::xbt);
+  // Kbar and Nbar (fp32 C x d each) take the Zbar slot once Xbar has read it
+  float *fKb = reinterpret_cast<float*>(smem + AL::zb), *fNb = fKb + CP * D;
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -137,8 +168,14 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
   constexpr size_t hd = (size_t)h * d;
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
+  using BCD = Blk<CP, D>;
+  using BCC = Blk<CP, CP>;
+  using BDD = Blk<D, D>;
+  constexpr int NWH = 16;  // C x h products in blocks of half the usual size
+  using BCH = Blk<CP, H, NWH>;
+  static_assert(BCC::NB <= 8, "each wave owns at most one C x C block (its cbar tiles)");
 
-  for (int t = blockIdx.x; t < total; t += gridDim.x) {
+  if (const int t = blockIdx.x; t < total) {  // one chunk per workgroup
     const int u = t / nch, n = t - u * nch;
     const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
     const CT* fr = (const CT*)a.frec + (size_t)t * Y.r.fc.n;
@@ -157,26 +194,20 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
 #define FRF_(x) (frf + Y.r.ff.o[rec::x])
 #define BR_(x) (br + Y.r.bc.o[rec::x])
 #define BRF_(x) (brf + Y.r.bf.o[rec::x])
-#define A_(x) (ta + Y.ac.o[x])
     const CT *HkT = FR_(HkT), *D1 = FR_(D1), *Sz = FR_(Sz), *KT = FR_(KT), *R = FR_(R),
-             *X = FR_(X), *XT = FR_(XT), *N = FR_(N), *NT = FR_(NT), *QT = FR_(QT),
-             *StrT = FR_(StrT);
+             *XT = FR_(XT), *N = FR_(N), *NT = FR_(NT), *QT = FR_(QT), *StrT = FR_(StrT);
     const float *fXK = FRF_(XK), *fHH = FRF_(HH), *fHW2 = FRF_(HW2), *fHS2 = FRF_(HS2),
                 *knorm = FRF_(kn);
     CT *ZbT = BR_(ZbT), *Q1T = BR_(Q1T), *dOT = BR_(dOT), *dOAT = BR_(dOAT), *dOET = BR_(dOET);
-    CT *dO = A_(adO), *dOA = A_(adOA), *dOE = A_(adOE), *Xb = A_(aXb), *XbT = A_(aXbT);
-    CT *Q1 = A_(aQ1), *Q2 = A_(aQ2), *Q2T = A_(aQ2T), *dXN = A_(adXN), *dXNT = A_(adXNT);
-    // Kbar and Nbar (fp32 C x d each) take the Zbar slot once Xbar has read it
-    static_assert((size_t)CP * H * sizeof(CT) >= 2 * (size_t)CP * D * sizeof(float), "Zbar slot");
-    float *fKb = reinterpret_cast<float*>(Zb), *fNb = fKb + CP * D;
     const int tok0 = s * Dm.S + n * C;
     const int l = lane_id_local();
     const CT* pk = (const CT*)a.statesT + ((size_t)u * a.nslots + n) * (4 * hd + (size_t)d * d);
     const CT *W1T = pk, *W2T = pk + hd, *S1T = pk + 2 * hd, *S2T = pk + 3 * hd, *McT = pk + 4 * hd;
 
     // ---- chunk coefficients; stage dO (one (row, 8-column block) per thread,
-    // consecutive threads on consecutive rows) with its scaled and transposed
-    // forms; partial dA, dE of the retrieval, sum_k dO_ik (H W2^T)_ik (S2 likewise)
+    // consecutive threads on consecutive rows) and its scaled and transposed
+    // forms for the backward record; partial dA, dE of the retrieval,
+    // sum_k dO_ik (H W2^T)_ik (S2 likewise)
     chunk_coefs_f(cf, a.lr + cbase, a.mom + cbase, a.decay + cbase, tok0, C, Cp);  // ends with a barrier
     constexpr int JB = D / 8, ITEMS = CP * JB, PER = (ITEMS + 511) / 512;
 #pragma unroll
@@ -185,7 +216,7 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
       if (e < ITEMS) {
         const int i = e % CP, j0 = (e / CP) * 8;
         const size_t en = (size_t)i * d + j0;
-        float ox[8], va[8], ve[8];
+        float ox[8];
         if (i < C) {
           load8(dOg + (size_t)(tok0 + i) * d + j0, ox);
         } else {
@@ -197,44 +228,31 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
         for (int q = 0; q < 8; ++q) {
           const size_t et = (size_t)(j0 + q) * Cp + i;  // consecutive lanes: consecutive i
           const float w2 = fHW2[et], s2 = fHS2[et];
-          va[q] = cf.A[i] * ox[q];
-          ve[q] = cf.E[i] * ox[q];
           dOT[et] = from_f<CT>(ox[q]);
-          dOAT[et] = from_f<CT>(va[q]);
-          dOET[et] = from_f<CT>(ve[q]);
+          dOAT[et] = from_f<CT>(cf.A[i] * ox[q]);
+          dOET[et] = from_f<CT>(cf.E[i] * ox[q]);
           const float oq = to_f(from_f<CT>(ox[q]));  // dO as the contractions see it
           sa += oq * w2;
           se += oq * s2;
         }
         store8<CT>(dO + en, ox);
-        store8<CT>(dOA + en, va);
-        store8<CT>(dOE + en, ve);
-        dpa[j0 / 8][i] = sa;
-        dpe[j0 / 8][i] = se;
+        dpa[(j0 / 8) * CP + i] = sa;
+        dpe[(j0 / 8) * CP + i] = se;
       }
     }
     __syncthreads();
-    if (threadIdx.x < MAXC) {
+    float gAi = 0.f, gEi = 0.f;  // thread i's retrieval dA_i, dE_i
+    if (threadIdx.x < Cp) {
       const int i = threadIdx.x;
-      float sa = 0.f, se = 0.f;
-      if (i < Cp)
 #pragma unroll
-        for (int q = 0; q < JB; ++q) {  // fixed order: deterministic
-          sa += dpa[q][i];
-          se += dpe[q][i];
-        }
-      gA[i] = sa;
-      gE[i] = se;
+      for (int q = 0; q < JB; ++q) {  // fixed order: deterministic
+        gAi += dpa[q * CP + i];
+        gEi += dpe[q * CP + i];
+      }
     }
-    using BCD = Blk<CP, D>;
-    using BCH = Blk<CP, H>;
-    using BCC = Blk<CP, CP>;
-    using BDD = Blk<D, D>;
-    auto fofs = [&](int i0, int j0, int rb, int cb) -> size_t {
-      const int blk = (i0 / (BCH::RB * 16)) * BCH::NBN + j0 / (BCH::CB * 16);
-      return ((size_t)((blk * BCH::RB + rb) * BCH::CB + cb) * WAVE + l) * 4;
-    };
-    // dOR = dO R^T ; Q1 = c o dOR ; cbar = -HH o dOR
+    // dOR = dO R^T ; Q1 = c o dOR ; cbar = -HH o dOR (kept in the wave's registers)
+    f4 cbr[BCC::RB][BCC::CB];
+    zero_blk(cbr);
     for_blocks<CP, CP>([&](int i0, int j0) {
       f4 hhv[BCC::RB][BCC::CB];  // H Hk^T, requested ahead of the product
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int, int) {
@@ -244,7 +262,7 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
       zero_blk(acc);
       mma_blk<CT, KC, KC, BCC::RB, BCC::CB, D>(acc, dO, d, i0, R, d, j0);
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
-        const f4 hh = hhv[rb][cb];
+        const f4 hv = hhv[rb][cb];
         f4 qv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -253,37 +271,40 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
           const bool lo = j <= ii;
           qv[r] = lo ? cf.cc(ii, j) * x : 0.f;
           Q1[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
-          fCb[ii * Cp + j] = lo ? -hh[r] * x : 0.f;
+          cbr[rb][cb][r] = lo ? -hv[r] * x : 0.f;
         }
         store4<CT>(Q1T + (size_t)j * Cp + i, qv);
       });
     });
     __syncthreads();
     // Hbar = diag(A) dO W2 + diag(E) dO S2 - Q1 Hk ; Zbar = Hbar * s'(Z)
-    for_blocks<CP, H>([&](int i0, int j0) {
+    for_blocks_n<CP, H, NWH>([&](int i0, int j0) {
       typedef CT ct4 __attribute__((ext_vector_type(4)));
       ct4 szv[BCH::RB][BCH::CB];  // s'(Z), requested ahead of the products
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int, int) {
-        szv[rb][cb] = *reinterpret_cast<const ct4*>(Sz + fofs(i0, j0, rb, cb));
+        szv[rb][cb] = *reinterpret_cast<const ct4*>(Sz + frag_ofs<CP, H>(i0 + 16 * rb, j0 + 16 * cb, l));
       });
-      f4 a1[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
+      f4 a1[BCH::RB][BCH::CB], a2[BCH::RB][BCH::CB], a3[BCH::RB][BCH::CB];
       zero_blk(a1);
+      zero_blk(a2);
       zero_blk(a3);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dOA, d, i0, W2T, d, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dOE, d, i0, S2T, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, dO, d, i0, W2T, d, j0);
+      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a2, dO, d, i0, S2T, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a3, Q1, Cp, i0, HkT, Cp, j0);
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         f4 zv;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          zv[r] = (a1[rb][cb][r] - a3[rb][cb][r]) * to_f(szv[rb][cb][r]);
-          Zb[(size_t)(i + r) * h + j] = from_f<CT>(zv[r]);
+          const int ii = i + r;
+          zv[r] = (cf.A[ii] * a1[rb][cb][r] + cf.E[ii] * a2[rb][cb][r] - a3[rb][cb][r]) *
+                  to_f(szv[rb][cb][r]);
+          Zb[(size_t)ii * h + j] = from_f<CT>(zv[r]);
         }
         store4<CT>(ZbT + (size_t)j * Cp + i, zv);
       });
     });
-    __syncthreads();
-    // dZD1 = Zbar D1^T ; Q2 = c o dZD1 ; cbar -= XK o dZD1
+    __syncthreads();  // dO and Q1 are dead: their region takes Q2, Q2^T, Xbar, Xbar^T
+    // dZD1 = Zbar D1^T ; Q2 = c o dZD1 ; cbar -= XK o dZD1, then cbar to the record
     for_blocks<CP, CP>([&](int i0, int j0) {
       f4 xkv[BCC::RB][BCC::CB];  // X K^T, requested ahead of the product
       blk_each4<BCC::RB, BCC::CB>(i0, j0, [&](int rb, int cb, int, int) {
@@ -302,7 +323,8 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
           const bool lo = j <= ii;
           qv[r] = lo ? cf.cc(ii, j) * x : 0.f;
           Q2[(size_t)ii * Cp + j] = from_f<CT>(qv[r]);
-          if (lo) fCb[ii * Cp + j] -= xk[r] * x;
+          if (lo) cbr[rb][cb][r] -= xk[r] * x;
+          BRF_(Cb)[(size_t)ii * Cp + j] = cbr[rb][cb][r];
         }
         store4<CT>(Q2T + (size_t)j * Cp + i, qv);
       });
@@ -351,19 +373,18 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
         for (int r = 0; r < 4; ++r) fKb[(size_t)(i + r) * d + j] = -a1[rb][cb][r];
       });
     });
-    __syncthreads();
-    for (int i = threadIdx.x; i < Cp; i += blockDim.x) {
+    __syncthreads();  // Q2, Q2^T are dead: their space takes dXN, dXN^T
+    if (threadIdx.x < Cp) {
+      const int i = threadIdx.x;
       float sa = 0.f, se = 0.f;
 #pragma unroll
       for (int q = 0; q < (d >> 4); ++q) {
         sa += pA[q * Cp + i];
         se += pE[q * Cp + i];
       }
-      BRF_(gA)[i] = gA[i] + sa;
-      BRF_(gE)[i] = gE[i] + se;
+      BRF_(gA)[i] = gAi + sa;
+      BRF_(gE)[i] = gEi + se;
     }
-    for (int e = threadIdx.x * 4; e < Cp * Cp; e += blockDim.x * 4)
-      *reinterpret_cast<f32x4*>(BRF_(Cb) + e) = *reinterpret_cast<const f32x4*>(fCb + e);
     if (Dm.qk_proj) {
       // dXN = tril(Xbar N^T)
       for_blocks<CP, CP>([&](int i0, int j0) {
@@ -432,7 +453,6 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
 #undef FRF_
 #undef BR_
 #undef BRF_
-#undef A_
   }
 }
 
@@ -1103,7 +1123,7 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   set_lds_limit((const void*)ka);
   set_lds_limit((const void*)kb);
   set_lds_limit((const void*)kc);
-  hipLaunchKernelGGL(ka, dim3(std::min(total, SPLIT_GRID_A)), dim3(512), lds_a, st, *a, P);
+  hipLaunchKernelGGL(ka, dim3(total), dim3(512), lds_a, st, *a, P);
   if (a->pass_a_done) {
     const hipError_t e = hipEventRecord(a->pass_a_done, st);
     if (e != hipSuccess) {
