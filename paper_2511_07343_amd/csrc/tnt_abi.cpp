@@ -453,6 +453,7 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     g.opT = ws + y.w_gop;
     g.D = dims_of(c, c->C_G, c->L);
     g.force_generic = generic_only();
+    g.skip_final_carry = final_state == nullptr;
     HIP_TIMED("global_scan", launch_global_scan(g, st));
     HIP_TIMED("global_init", launch_global_init(g, st));
     for (int n = 0; n < y.g_chunks; ++n) HIP_TIMED("global_fwd_chunk", launch_global_fwd_chunk(g, n, st));

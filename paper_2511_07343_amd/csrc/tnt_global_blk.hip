@@ -118,9 +118,16 @@ static void launch_gtranspose(const float* src, size_t src_stride, CT* dst, size
 }
 
 // ---------------------------------------------------------------------------
-// forward, token tiles of TT rows of chunk n
+// forward, token tiles of TT rows of chunk n.  KS = false: the retrieval alone
+// (Zq -> Hq -> O), for a chunk whose carry nobody reads
 // ---------------------------------------------------------------------------
-template <typename IO, typename CT, int ACT, int D, int H>
+template <int D, int H, bool KS>
+constexpr size_t gfwd_tile_lds() {  // padded rows, compute type (2 bytes)
+  return (KS ? 2 * (size_t)gtile_rows<H>() * (D + 8) + 3 * (size_t)gtile_rows<H>() * (H + 8)
+             : (size_t)gtile_rows<H>() * (D + 8) + (size_t)gtile_rows<H>() * (H + 8)) * 2;
+}
+
+template <typename IO, typename CT, int ACT, int D, int H, bool KS>
 __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   constexpr int TT = gtile_rows<H>();
   // rows padded by 16 bytes: the 16-byte operand reads of consecutive rows do
@@ -128,10 +135,10 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   constexpr int LD = D + 8, LH = H + 8;
   extern __shared__ __align__(16) unsigned char smem[];
   CT* sQ = reinterpret_cast<CT*>(smem);  // [TT][LD], later R
-  CT* sK = sQ + TT * LD;                 // [TT][LD]
-  CT* sHq = sK + TT * LD;                // [TT][LH]
-  CT* sHk = sHq + TT * LH;               // [TT][LH]
-  CT* sSp = sHk + TT * LH;               // [TT][LH]  s'(Zk)
+  CT* sK = sQ + TT * LD;                 // [TT][LD]   (KS only)
+  CT* sHq = KS ? sK + TT * LD : sK;      // [TT][LH]
+  CT* sHk = sHq + TT * LH;               // [TT][LH]   (KS only)
+  CT* sSp = sHk + TT * LH;               // [TT][LH]  s'(Zk)   (KS only)
   __shared__ float cC[TT], bb[TT];
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -159,16 +166,19 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   __syncthreads();
   for (int e = threadIdx.x; e < TT * (D / 8); e += blockDim.x) {
     const int i = e % TT, j0 = (e / TT) * 8;
-    float qx[8], kx[8];
+    float qx[8];
     gload8(q + (size_t)i * D + j0, qx);
-    gload8(k + (size_t)i * D + j0, kx);
     gstore8<CT>(sQ + (size_t)i * LD + j0, qx);
-    gstore8<CT>(sK + (size_t)i * LD + j0, kx);
+    if constexpr (KS) {
+      float kx[8];
+      gload8(k + (size_t)i * D + j0, kx);
+      gstore8<CT>(sK + (size_t)i * LD + j0, kx);
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const size_t et = (size_t)(j0 + t) * C + r0 + i;
-      KcT[et] = from_f<CT>(cC[i] * kx[t]);
-      KbT[et] = from_f<CT>(bb[i] * kx[t]);
+      for (int t = 0; t < 8; ++t) {
+        const size_t et = (size_t)(j0 + t) * C + r0 + i;
+        KcT[et] = from_f<CT>(cC[i] * kx[t]);
+        KbT[et] = from_f<CT>(bb[i] * kx[t]);
+      }
     }
   }
   __syncthreads();
@@ -178,21 +188,25 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   for_blocks<TT, H>([&](int i0, int j0) {
     f4 aq[BH::RB][BH::CB], ak[BH::RB][BH::CB];
     zero_blk(aq);
-    zero_blk(ak);
     mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(aq, sQ, LD, i0, V1, D, j0);
-    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ak, sK, LD, i0, V1, D, j0);
+    if constexpr (KS) {
+      zero_blk(ak);
+      mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ak, sK, LD, i0, V1, D, j0);
+    }
     blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
       f4 hv;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const size_t e = (size_t)(i + r) * LH + j;
-        const ActVals z = act_all<ACT>(ak[rb][cb_][r]);
         sHq[e] = from_f<CT>(act_f<ACT>(aq[rb][cb_][r]));
-        sHk[e] = from_f<CT>(z.s);
-        sSp[e] = from_f<CT>(z.d1);
-        hv[r] = z.s;
+        if constexpr (KS) {
+          const ActVals z = act_all<ACT>(ak[rb][cb_][r]);
+          sHk[e] = from_f<CT>(z.s);
+          sSp[e] = from_f<CT>(z.d1);
+          hv[r] = z.s;
+        }
       }
-      store4<CT>(HkT + (size_t)j * C + r0 + i, hv);
+      if constexpr (KS) store4<CT>(HkT + (size_t)j * C + r0 + i, hv);
     });
   });
   __syncthreads();
@@ -201,9 +215,11 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
   for_blocks<TT, D>([&](int i0, int j0) {
     f4 ao[BD::RB][BD::CB], ay[BD::RB][BD::CB];
     zero_blk(ao);
-    zero_blk(ay);
     mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ao, sHq, LH, i0, V2, H, j0);
-    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ay, sHk, LH, i0, V2, H, j0);
+    if constexpr (KS) {
+      zero_blk(ay);
+      mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(ay, sHk, LH, i0, V2, H, j0);
+    }
     blk_each4<BD::RB, BD::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
       f4 rc, rbv;
 #pragma unroll
@@ -211,15 +227,20 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
         const int ii = i + r;
         const size_t e = (size_t)ii * D + j;
         o[e] = ao[rb][cb_][r];
-        const float rv = rscale * (ay[rb][cb_][r] - to_f(v[e]));
-        sR[(size_t)ii * LD + j] = from_f<CT>(rv);
-        rc[r] = cC[ii] * rv;
-        rbv[r] = bb[ii] * rv;
+        if constexpr (KS) {
+          const float rv = rscale * (ay[rb][cb_][r] - to_f(v[e]));
+          sR[(size_t)ii * LD + j] = from_f<CT>(rv);
+          rc[r] = cC[ii] * rv;
+          rbv[r] = bb[ii] * rv;
+        }
       }
-      store4<CT>(RcT + (size_t)j * C + r0 + i, rc);
-      store4<CT>(RbT + (size_t)j * C + r0 + i, rbv);
+      if constexpr (KS) {
+        store4<CT>(RcT + (size_t)j * C + r0 + i, rc);
+        store4<CT>(RbT + (size_t)j * C + r0 + i, rbv);
+      }
     });
   });
+  if constexpr (!KS) return;
   __syncthreads();
   // G = R V2, D1 = G * s'(Zk)
   for_blocks<TT, H>([&](int i0, int j0) {
@@ -581,10 +602,19 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   constexpr size_t hd = (size_t)H * D;
   launch_gtranspose<CT>(a.states + (size_t)(n % a.nslots) * 4 * hd, (size_t)a.nslots * 4 * hd,
                         (CT*)a.packT, 4 * hd, (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
-  const size_t l1 = (2 * (size_t)TT * (D + 8) + 3 * (size_t)TT * (H + 8)) * sizeof(CT);  // padded rows
-  auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H>;
+  static_assert(sizeof(CT) == 2, "gfwd_tile_lds counts 2-byte elements");
+  // the backward reads the chunk-entry states only: the carry out of the last
+  // chunk (and the tile's key side that feeds it) runs when the caller asks for
+  // the final state
+  if (a.skip_final_carry && n + 1 == a.D.L / C) {
+    auto kq = gfwd_tile_kernel<IO, CT, ACT, D, H, false>;
+    set_lds_limit((const void*)kq);
+    hipLaunchKernelGGL(kq, dim3(C / TT, chains), dim3(512), (gfwd_tile_lds<D, H, false>()), st, a, n);
+    return hipGetLastError();
+  }
+  auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H, true>;
   set_lds_limit((const void*)k1);
-  hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
+  hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), (gfwd_tile_lds<D, H, true>()), st, a, n);
   const int tk = gtk_of(C), ns = C / tk;
   const int sec = section_begin("global_carry", st);
   if (tk == GTK_LONG)

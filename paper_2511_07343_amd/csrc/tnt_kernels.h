@@ -135,6 +135,8 @@ struct GlobalArgs {
   void* opT;                                             // CT per-chain transposed chunk operands
   Dims D;
   int force_generic;                                     // 1: skip fixed-size kernels
+  int skip_final_carry;                                  // 1: the state after the last chunk
+                                                         // is not read (no final-state output)
 };
 
 constexpr int TKS = 8;  // floats per token in GlobalArgs::tokc
