@@ -57,6 +57,13 @@ def global_fwd_flops(d, h):
     return 18 * d * h     # chunk gradients 6dh, retrieval 4dh, carry 8dh
 
 
+def global_fwd_step_flops(cfg):
+    """The global forward's FLOPs per step: the last chunk's carry and its
+    chunk gradients feed only the final state, which the step does not ask for."""
+    tok = cfg.B * cfg.H * cfg.L
+    return global_fwd_flops(cfg.d, cfg.hid) * tok - 14 * cfg.d * cfg.hid * cfg.B * cfg.H * cfg.C_G
+
+
 def global_bwd_flops(d, h):
     return 36 * d * h
 
@@ -65,7 +72,7 @@ def step_flops(cfg):
     tok = cfg.B * cfg.H * cfg.L
     f = 0
     if cfg.has_global:
-        f += (global_fwd_flops(cfg.d, cfg.hid) + global_bwd_flops(cfg.d, cfg.hid)) * tok
+        f += global_fwd_step_flops(cfg) + global_bwd_flops(cfg.d, cfg.hid) * tok
     for (C, _) in cfg.locals_:
         f += (local_fwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj) +
               local_bwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj)) * tok
@@ -136,8 +143,10 @@ def launch_flops(cfg, name):
     if name == "local_bwd":
         return local_bwd_flops(cfg.d, cfg.hid, C, cfg.qk_proj) * tok
     per_chunk = cfg.B * cfg.H * cfg.C_G
-    if name == "global_fwd_chunk":
-        return global_fwd_flops(cfg.d, cfg.hid) * per_chunk
+    G = cfg.L // cfg.C_G
+    dh = cfg.d * cfg.hid
+    if name == "global_fwd_chunk":   # mean over the step's launches (the last chunk: its
+        return (18 * dh * (G - 1) + 4 * dh) * per_chunk / G   # retrieval only)
     if name == "global_bwd_chunk":
         return global_bwd_flops(cfg.d, cfg.hid) * per_chunk
     return None
