@@ -113,12 +113,12 @@ template <typename CT, int CP, int D, int H>
 constexpr size_t split_b_lds() {
   return SplitBLds<CT, CP, D, H>::total;
 }
-// pass C: cbar, U (CP x CP fp32 each) and the gate partials (5 x 8 x CP fp32);
-// the Q-K term uses the same space first (Nbar: CP x D, Msym: D x D fp32)
-template <int CP, int D>
+// pass C: cbar (CP x CP fp32) and the gate partials (5 x 8 x CP fp32); the Q-K
+// term uses the same space first (Nbar: CP x D fp32, Msym: D x D compute type)
+template <typename CT, int CP, int D>
 constexpr size_t split_c_lds() {
-  const size_t gate = (2 * (size_t)CP * CP + 40 * (size_t)CP) * sizeof(float);
-  const size_t qk = ((size_t)CP * D + (size_t)D * D) * sizeof(float);
+  const size_t gate = ((size_t)CP * CP + 40 * (size_t)CP) * sizeof(float);
+  const size_t qk = (size_t)CP * D * sizeof(float) + (size_t)D * D * sizeof(CT);
   return gate > qk ? gate : qk;
 }
 
@@ -873,17 +873,19 @@ __global__ void __launch_bounds__(256) split_madj_scan_kernel(float* rec_f, size
 // ===========================================================================
 // pass C: gate adjoints and the carried Q-K term of dk, every chunk at once
 // ===========================================================================
+// Sized so that four workgroups share a CU: packed coefficients, Msym in the
+// compute type, and the affine scan's rows U folded into their column sums in
+// the registers of the wave that scans them.
 template <typename CT, int D, int H, int CP>
 __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, SplitPtrs P) {
-  __shared__ Coef cf;
-  __shared__ float gA[MAXC], gE[MAXC], gCC[MAXC], gB[MAXC], dots[4];
+  __shared__ CoefGN<CP> cf;
+  __shared__ float gA[CP], gE[CP], gCC[CP], gB[CP], dots[4];
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int d = D, Cp = CP;
   float* fCb = reinterpret_cast<float*>(smem);
-  float* fU = fCb + Cp * Cp;
-  float* gpart = fU + Cp * Cp;  // [5][8][Cp]
-  float* fNb = fCb;             // Q-K term first: Nbar [Cp][d], Msym [d][d]
-  float* fMs = fCb + Cp * d;
+  float* gpart = fCb + Cp * Cp;  // [5][8][Cp]
+  float* fNb = fCb;              // Q-K term first: Nbar [Cp][d] fp32, Msym [d][d] CT
+  CT* sMs = reinterpret_cast<CT*>(fCb + Cp * d);
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -905,19 +907,20 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
 
   if (shard_qk && n < nch - 1) {
     // Kbar += (Nbar' - N (N . Nbar')) / ||k||, Nbar' = N (Mbar + Mbar^T), Mbar the
-    // suffix sum of Xbar^T Q over the shard's later chunks
+    // suffix sum of Xbar^T Q over the shard's later chunks (Msym rounded to the
+    // compute type here, where the MFMA would round it)
     const CT* N = rc + Y.r.fc.o[rec::N];
     const float* Mb = bqf + Y.r.bf.o[rec::XbQ];
     for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
       const int i = e / d, j = e - i * d;
-      fMs[e] = Mb[e] + Mb[(size_t)j * d + i];
+      sMs[e] = from_f<CT>(Mb[e] + Mb[(size_t)j * d + i]);
     }
     __syncthreads();
     using BCD = Blk<CP, D>;
     for_blocks<CP, D>([&](int i0, int j0) {
       f4 n1[BCD::RB][BCD::CB];
       zero_blk(n1);
-      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, D>(n1, N, d, i0, fMs, d, j0);
+      mma_blk<CT, KC, KC, BCD::RB, BCD::CB, D>(n1, N, d, i0, sMs, d, j0);
       blk_each4<BCD::RB, BCD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) fNb[(size_t)(i + r) * d + j] = n1[rb][cb][r];
@@ -940,7 +943,7 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
     __syncthreads();  // LDS is reused below
   }
 
-  chunk_coefs(cf, a.lr + cbase, mom, dec, tok0, C, Cp);  // ends with a barrier
+  chunk_coefs_g(cf, a.lr + cbase, mom, dec, tok0, C, Cp);  // ends with a barrier
   for (int e = threadIdx.x * 4; e < Cp * Cp; e += blockDim.x * 4)
     *reinterpret_cast<f32x4*>(fCb + e) = *reinterpret_cast<const f32x4*>(bqf + Y.r.bf.o[rec::Cb] + e);
   if (threadIdx.x < Cp) {
@@ -972,19 +975,23 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
       for (int r = r0; r < r1; ++r) {
         if (r >= i) {
           const float cb = fCb[r * Cp + i];
-          eb += cb * cf.ct[r][i];
-          cols += cb * cf.c[r][i];
+          eb += cb * cf.ctt(r, i);
+          cols += cb * cf.cc(r, i);
         }
-        if (r <= i) rows += fCb[i * Cp + r] * cf.c[i][r];
+        if (r <= i) rows += fCb[i * Cp + r] * cf.cc(i, r);
       }
       gpart[(0 * 8 + w) * Cp + i] = eb;
       gpart[(1 * 8 + w) * Cp + i] = cols;
       gpart[(2 * 8 + w) * Cp + i] = rows;
     }
     // U_{i, j} = beta'_j U_{i, j-1} + cbar_{i j} eta_j (j <= i), beta'_j = e^{lb_j - lb_{j-1}},
-    // for this wave's rows i, as an affine scan over the lanes j
+    // for this wave's rows i, as an affine scan over the lanes j; each lane keeps
+    // the column sums over those rows
+    //   T_j = sum_{i >= j} e^{la_i - la_j} U_{i j},  Y_j = sum_{i >= j} e^{la_i - la_j} Ebar_i
     const int j = l;
     const float aj = (j < Cp) ? expf(cf.lb[j] - (j > 0 ? cf.lb[j - 1] : 0.f)) : 0.f;
+    const float laj = (j < Cp) ? cf.la[j] : 0.f;
+    float T = 0.f, Yv = 0.f;
     for (int ri = r0; ri < r1; ++ri) {
       float sa = aj, sx = (j <= ri && j < Cp) ? fCb[ri * Cp + j] * cf.eta[j] : 0.f;
 #pragma unroll
@@ -995,23 +1002,11 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
           sa = sa * pa_;
         }
       }
-      if (j < Cp) fU[ri * Cp + j] = (j <= ri) ? sx : 0.f;
-    }
-  }
-  __syncthreads();
-  {
-    // T_j = sum_{i >= j} e^{la_i - la_j} U_{i j},  Y_j = sum_{i >= j} e^{la_i - la_j} Ebar_i
-    const int w = wave_id(), j = l;
-    const int r0 = w * (Cp / 8), r1 = r0 + Cp / 8;
-    float T = 0.f, Yv = 0.f;
-    if (j < C) {
-#pragma unroll 4
-      for (int i = r0; i < r1; ++i)
-        if (i >= j) {
-          const float e = expf(cf.la[i] - cf.la[j]);
-          T += e * fU[i * Cp + j];
-          Yv += e * gE[i];
-        }
+      if (j < C && ri >= j) {
+        const float e = expf(cf.la[ri] - laj);
+        T += e * sx;
+        Yv += e * gE[ri];
+      }
     }
     if (j < Cp) {
       gpart[(3 * 8 + w) * Cp + j] = T;
@@ -1062,7 +1057,7 @@ constexpr bool split_fits() {
   // pass C's static LDS is under 40 KB
   return split_a_lds<CT, CP, D, H>() + SPLIT_A_STATIC <= 160 * 1024 &&
          split_b_lds<CT, CP, D, H>() + 2 * 1024 <= 160 * 1024 &&
-         split_c_lds<CP, D>() + 40 * 1024 <= 160 * 1024;
+         split_c_lds<CT, CP, D>() + 40 * 1024 <= 160 * 1024;
 }
 
 struct SplitSizes {
@@ -1114,7 +1109,7 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   auto kb = local_bwd_chain_kernel<IO, CT, ACT, D, H, CP>;
   auto kc = local_bwd_gate_kernel<CT, D, H, CP>;
   constexpr size_t lds_a = split_a_lds<CT, CP, D, H>(), lds_b = split_b_lds<CT, CP, D, H>(),
-                   lds_c = split_c_lds<CP, D>();
+                   lds_c = split_c_lds<CT, CP, D>();
   if (!lds_fits((const void*)ka, lds_a) || !lds_fits((const void*)kb, lds_b) ||
       !lds_fits((const void*)kc, lds_c)) {  // the compiled static LDS, not the estimate
     *err = hipErrorInvalidConfiguration;

@@ -165,6 +165,55 @@ __device__ __forceinline__ void chunk_coefs_f(CoefFN<N>& cf, const float* lr, co
   __syncthreads();
 }
 
+// The coefficients of the gate adjoints, for chunks of at most N (padded)
+// positions: ct packed like CoefFN's c.  c_{i,tau} = eta_tau ct_{i,tau} is the
+// product the scan forms for c, so cc() equals the stored c bit for bit.
+template <int N>
+struct CoefGN {
+  static_assert(N <= MAXC, "one wave scans a chunk");
+  float ct[N * (N + 1) / 2];
+  float A[N], E[N], la[N], lb[N], eta[N], bb[N], ebt[N];
+  float BC;
+  // ct_{i,j} and c_{i,j} for j <= i
+  __device__ __forceinline__ float ctt(int i, int j) const { return ct[i * (i + 1) / 2 + j]; }
+  __device__ __forceinline__ float cc(int i, int j) const { return eta[j] * ct[i * (i + 1) / 2 + j]; }
+};
+
+template <int N>
+__device__ __forceinline__ void chunk_coefs_g(CoefGN<N>& cf, const float* lr, const float* mom,
+                                              const float* dec, int tok0, int C, int Cp) {
+  if (wave_id() == 0) {
+    const int i = lane_id();
+    const bool in = i < C;
+    const float eta = in ? lr[tok0 + i] : 0.f;
+    const float lmb = in ? log_mom(mom[tok0 + i]) : 0.f;
+    const float lka = in ? log_keep(dec[tok0 + i]) : 0.f;
+    const float la = wave_incl_sum(lka);
+    const float lb = wave_incl_sum(lmb);
+    if (i < N) {
+      cf.la[i] = la;
+      cf.lb[i] = lb;
+      cf.eta[i] = eta;
+      cf.A[i] = expf(la);
+    }
+  }
+  __syncthreads();
+  coef_scan_columns(cf.la, cf.lb, Cp, [&](int r, int tau, float b) {
+    if (tau <= r) cf.ct[r * (r + 1) / 2 + tau] = b;
+  }, cf.E);
+  __syncthreads();
+  if (wave_id() == 0) {
+    const int tau = lane_id();
+    if (tau < Cp) {
+      const float et = (tau < C) ? expf(cf.lb[C - 1] - cf.lb[tau]) : 0.f;
+      cf.ebt[tau] = et;
+      cf.bb[tau] = cf.eta[tau] * et;
+    }
+    if (tau == 0) cf.BC = expf(cf.lb[C - 1]);
+  }
+  __syncthreads();
+}
+
 // Stage a [Cp][d] tile of an I/O tensor (rows >= C zero) into CT storage,
 // optionally also its transpose [d][Cp].
 template <typename IO, typename CT>
