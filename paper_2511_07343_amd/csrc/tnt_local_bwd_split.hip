@@ -547,12 +547,10 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
   using BCH0 = Blk<CP, H>;
   static_assert(BCH0::NB <= 8, "each wave owns at most one C x h block");
 
-  for (size_t e = threadIdx.x; e < 4 * hd; e += blockDim.x) {
-    adj0[e] = 0.f;
-  }
-  __syncthreads();
-
+  // the adjoint leaving the shard's last chunk is zero: that chunk skips every
+  // product with it and writes the adjoint without reading it
   for (int n = nch - 1; n >= 0; --n) {
+    const bool zadj = n == nch - 1;
     const size_t t = (size_t)u * nch + n;
     const CT* rc = (const CT*)a.frec + t * Y.r.fc.n;
     const float* rf = a.frec_f + t * Y.r.ff.n;
@@ -627,10 +625,12 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
         for (int rb = 0; rb < RBN; ++rb)
           mxv[rb] = *reinterpret_cast<const ct4*>(MT + (size_t)(j0 + (l & 15)) * Cp + 16 * rb + 4 * (l >> 4));
       }
-      if (pair == 0)
+      if (zadj) {
+      } else if (pair == 0) {
         mma_pair_dots<RBN, H, 4, KC, MC>(t0, t1, D1, h, Wb1, Sb1, d, j0, W1T, S1T, h, pa, pe, pb);
-      else
+      } else {
         mma_pair_dots<RBN, H, 4, MC>(t0, t1, Hk, h, Wb2, Sb2, h, j0, W2T, S2T, d, pa, pe, pb);
+      }
       pa = wave_sum(pa);
       pe = wave_sum(pe);
       pb = wave_sum(pb);
@@ -676,11 +676,13 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
       zero_blk(a1);
       zero_blk(a2);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a1, PzT, Cp, i0, ZbT, Cp, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, KcC, d, i0, Wb1, d, j0);
-      mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, Kb, d, i0, Sb1, d, j0);
       mma_blk<CT, KC, KC, BCH::RB, BCH::CB, CP>(a2, Q1T, Cp, i0, HT, Cp, j0);
-      mma_blk<CT, KC, MC, BCH::RB, BCH::CB, D>(a2, RcC, d, i0, Wb2, h, j0);
-      mma_blk<CT, KC, MC, BCH::RB, BCH::CB, D>(a2, Rb, d, i0, Sb2, h, j0);
+      if (!zadj) {
+        mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, KcC, d, i0, Wb1, d, j0);
+        mma_blk<CT, KC, KC, BCH::RB, BCH::CB, D>(a1, Kb, d, i0, Sb1, d, j0);
+        mma_blk<CT, KC, MC, BCH::RB, BCH::CB, D>(a2, RcC, d, i0, Wb2, h, j0);
+        mma_blk<CT, KC, MC, BCH::RB, BCH::CB, D>(a2, Rb, d, i0, Sb2, h, j0);
+      }
       blk_each4<BCH::RB, BCH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
         f4 gv, zp;
 #pragma unroll
@@ -790,13 +792,16 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     using BDH = Blk<D, H>;
     for_blocks<H, D>([&](int i0, int j0) {  // W1bar, S1bar : h x d
       f4 a1[BHD::RB][BHD::CB], a3[BHD::RB][BHD::CB], ow[BHD::RB][BHD::CB], os[BHD::RB][BHD::CB];
-      blk_each4<BHD::RB, BHD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+      zero_blk(ow);
+      zero_blk(os);
+      if (!zadj)
+        blk_each4<BHD::RB, BHD::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          ow[rb][cb][r] = Wb1[(size_t)(i + r) * d + j];
-          os[rb][cb][r] = Sb1[(size_t)(i + r) * d + j];
-        }
-      });
+          for (int r = 0; r < 4; ++r) {
+            ow[rb][cb][r] = Wb1[(size_t)(i + r) * d + j];
+            os[rb][cb][r] = Sb1[(size_t)(i + r) * d + j];
+          }
+        });
       zero_blk(a1);
       zero_blk(a3);
       mma_blk_shared<CT, BHD::RB, BHD::CB, CP, true>(a1, a3, ZbT, ZbT, Cp, i0, XAT, XET, Cp, j0);
@@ -816,13 +821,16 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
     });
     for_blocks<D, H>([&](int i0, int j0) {  // W2bar, S2bar : d x h
       f4 a1[BDH::RB][BDH::CB], a4[BDH::RB][BDH::CB], ow[BDH::RB][BDH::CB], os[BDH::RB][BDH::CB];
-      blk_each4<BDH::RB, BDH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
+      zero_blk(ow);
+      zero_blk(os);
+      if (!zadj)
+        blk_each4<BDH::RB, BDH::CB>(i0, j0, [&](int rb, int cb, int i, int j) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          ow[rb][cb][r] = Wb2[(size_t)(i + r) * h + j];
-          os[rb][cb][r] = Sb2[(size_t)(i + r) * h + j];
-        }
-      });
+          for (int r = 0; r < 4; ++r) {
+            ow[rb][cb][r] = Wb2[(size_t)(i + r) * h + j];
+            os[rb][cb][r] = Sb2[(size_t)(i + r) * h + j];
+          }
+        });
       zero_blk(a1);
       zero_blk(a4);
       mma_blk_shared<CT, BDH::RB, BDH::CB, CP, false>(a1, a4, dOAT, dOET, Cp, i0, HT, HT, Cp, j0);
