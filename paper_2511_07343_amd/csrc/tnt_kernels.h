@@ -105,6 +105,10 @@ struct LocalBwdArgs {
                                                          // dv and dWinit_part are final (after the
                                                          // walk; before the gate pass, which adds
                                                          // only to dk and the gate adjoints)
+  hipStream_t aux;                                       // null, or a second stream for work that
+  hipEvent_t aux_done;                                   // needs pass A only (with pass_a_done set):
+                                                         // it waits for pass_a_done there, and the
+                                                         // gate pass waits for aux_done
   int force_generic;                                     // 1: skip fixed-size kernels
 };
 

@@ -1127,27 +1127,34 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   set_lds_limit((const void*)kb);
   set_lds_limit((const void*)kc);
   hipLaunchKernelGGL(ka, dim3(total), dim3(512), lds_a, st, *a, P);
-  if (a->pass_a_done) {
-    const hipError_t e = hipEventRecord(a->pass_a_done, st);
-    if (e != hipSuccess) {
-      *err = e;
-      return true;
-    }
+  auto fail = [&](hipError_t e) {
+    *err = e;
+    return true;
+  };
+  hipError_t e;
+  if (a->pass_a_done && (e = hipEventRecord(a->pass_a_done, st)) != hipSuccess) return fail(e);
+  // the suffix sums of pass A's Xbar^T Q over later chunks (read by the gate
+  // pass): on the second stream beside the walk when there is one
+  const bool scan = Dm.qk_proj && Dm.qk_scope == 0;
+  const bool on_aux = scan && a->aux && a->aux_done && a->pass_a_done;
+  auto launch_scan = [&](hipStream_t s) {
+    const size_t thr = (size_t)units * D * D;
+    hipLaunchKernelGGL(split_madj_scan_kernel, dim3((unsigned)((thr + 255) / 256)), dim3(256), 0, s,
+                       P.brec_f, Y.r.bf.n, Y.r.bf.o[rec::XbQ], units, nch, D * D);
+  };
+  if (on_aux) {
+    if ((e = hipStreamWaitEvent(a->aux, a->pass_a_done, 0)) != hipSuccess) return fail(e);
+    launch_scan(a->aux);
+    if ((e = hipEventRecord(a->aux_done, a->aux)) != hipSuccess) return fail(e);
   }
   const int sec = section_begin("local_bwd_walk", st);  // the walk of the carried adjoint alone
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
   section_end(sec, st);
-  if (a->pass_b_done) {
-    const hipError_t e = hipEventRecord(a->pass_b_done, st);
-    if (e != hipSuccess) {
-      *err = e;
-      return true;
-    }
-  }
-  if (Dm.qk_proj && Dm.qk_scope == 0) {
-    const size_t thr = (size_t)units * D * D;
-    hipLaunchKernelGGL(split_madj_scan_kernel, dim3((unsigned)((thr + 255) / 256)), dim3(256), 0, st,
-                       P.brec_f, Y.r.bf.n, Y.r.bf.o[rec::XbQ], units, nch, D * D);
+  if (a->pass_b_done && (e = hipEventRecord(a->pass_b_done, st)) != hipSuccess) return fail(e);
+  if (on_aux) {
+    if ((e = hipStreamWaitEvent(st, a->aux_done, 0)) != hipSuccess) return fail(e);
+  } else if (scan) {
+    launch_scan(st);
   }
   hipLaunchKernelGGL(kc, dim3(total), dim3(512), lds_c, st, *a, P);
   *err = hipGetLastError();
