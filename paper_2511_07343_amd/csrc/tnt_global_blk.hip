@@ -27,10 +27,11 @@ namespace tnt {
 
 namespace {
 
-// tokens per split of the carry / state GEMMs: the forward carry takes GTK_LONG
-// where the chunk length allows (fewer fp32 partials written and read back),
-// the backward's state GEMMs GTK
+// tokens per split of the carry / state GEMMs: GTK_LONG where the chunk length
+// allows (fewer fp32 partials written and read back)
 constexpr int GTK = 256, GTK_LONG = 1024;
+// K slab of the LDS-staged carry GEMMs (tokens per round trip)
+constexpr int GCARRY_KT = 128;
 inline int gtk_of(int C) { return C % GTK_LONG == 0 ? GTK_LONG : GTK; }
 
 template <int H>
@@ -257,12 +258,93 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
 }
 
 // ---------------------------------------------------------------------------
+// acc (the wave's block of an MB x NB output) += sum over the NT terms of
+// A_t B_t^T, A_t: MB rows, B_t: NB rows, both K long and contraction-contiguous
+// (row stride ld), compute type.  The K range goes through LDS in slabs of KT:
+// every thread requests its 16-byte share of the next slab before the MFMAs of
+// the current one, so a slab costs one memory round trip for the whole
+// workgroup instead of one per K step and wave, and each operand row is read
+// from memory once, not once per wave that uses it.  The K order of the
+// accumulation is that of the plain block product.  `lds`: (MB + NB) (KT + 8)
+// compute-type elements (rows padded by 16 bytes).
+// ---------------------------------------------------------------------------
+template <typename CT, int MB, int NB, int KT, int NT>
+constexpr size_t lds_gemm_bytes() {
+  return (size_t)(MB + NB) * (KT + 8) * sizeof(CT);
+}
+
+template <typename CT, int MB, int NB, int KT, int NT, int RB, int CB>
+__device__ __forceinline__ void lds_gemm_nt(f4 (&acc)[RB][CB], int i0, int j0,
+                                            const CT* const (&A)[NT], const CT* const (&B)[NT],
+                                            int ld, int K, CT* lds) {
+  static_assert(sizeof(CT) == 2 && KT % 32 == 0, "bf16 slabs of whole K steps");
+  typedef Mma<CT> MM;
+  constexpr int LK = KT + 8, CPR = KT / 8, ITEMS = (MB + NB) * CPR;
+  constexpr int PER = (ITEMS + 511) / 512;
+  CT* const sA = lds;
+  CT* const sB = lds + MB * LK;
+  const int spt = K / KT, S = NT * spt;
+  bf16x8 pre[PER];
+  auto gload = [&](int st) {
+    const int t = st / spt, kk = (st - t * spt) * KT;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = threadIdx.x + p * 512;
+      if (e < ITEMS) {
+        const int row = e / CPR, c = e - row * CPR;
+        const CT* src = row < MB ? A[t] + (size_t)row * ld : B[t] + (size_t)(row - MB) * ld;
+        pre[p] = *reinterpret_cast<const bf16x8*>(src + kk + 8 * c);
+      }
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int e = threadIdx.x + p * 512;
+      if (e < ITEMS) {
+        const int row = e / CPR, c = e - row * CPR;
+        *reinterpret_cast<bf16x8*>(lds + (size_t)row * LK + 8 * c) = pre[p];
+      }
+    }
+  };
+  const int l = lane_id_local();
+  const int ko = MM::kofs(l);
+  gload(0);
+  lstore();
+  __syncthreads();
+#pragma unroll 1
+  for (int st = 0; st < S; ++st) {
+    if (st + 1 < S) gload(st + 1);
+#pragma unroll
+    for (int kk = 0; kk < KT; kk += MM::KS) {
+      typename MM::frag fa[RB], fb[CB];
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+        fa[r] = *reinterpret_cast<const bf16x8*>(sA + (size_t)(i0 + 16 * r + (l & 15)) * LK + kk + ko);
+#pragma unroll
+      for (int c = 0; c < CB; ++c)
+        fb[c] = *reinterpret_cast<const bf16x8*>(sB + (size_t)(j0 + 16 * c + (l & 15)) * LK + kk + ko);
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+#pragma unroll
+        for (int c = 0; c < CB; ++c) MM::mma(acc[r][c], fa[r], fb[c]);
+    }
+    if (st + 1 < S) {
+      __syncthreads();  // every wave is done with this slab
+      lstore();
+      __syncthreads();
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // forward carry partials of token split `blockIdx.x`:
 //   m = 0: D1^T (cC K) -> V1 slot,  m = 1: D1^T (b K) -> S1 slot   (hid x d)
 //   m = 2: (cC R)^T Hk -> V2 slot,  m = 3: (b R)^T Hk -> S2 slot   (d x hid)
 // ---------------------------------------------------------------------------
 template <typename CT, int D, int H, int TK>
 __global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
   const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
   const int C = a.D.C;
   constexpr size_t hd = (size_t)H * D;
@@ -271,31 +353,34 @@ __global__ void __launch_bounds__(512) gfwd_carry_kernel(GlobalArgs a) {
            *KbT = KcT + (size_t)D * C, *RcT = KbT + (size_t)D * C, *RbT = RcT + (size_t)D * C;
   const size_t k0 = (size_t)split * TK;
   float* P = a.part + ((size_t)chain * ns + split) * 4 * hd;
+  CT* lds = reinterpret_cast<CT*>(smem);
   if (m < 2) {
     using BK = Blk<H, D>;
-    const CT* B = (m == 0 ? KcT : KbT) + k0;
+    static_assert(BK::NB == 8, "one block per wave");
+    const CT* const As[1] = {D1T + k0};
+    const CT* const Bs[1] = {(m == 0 ? KcT : KbT) + k0};
     float* out = P + (m == 0 ? 0 : 2 * hd);
-    for_blocks<H, D>([&](int i0, int j0) {
-      f4 acc[BK::RB][BK::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, D1T + k0, C, i0, B, C, j0);
-      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+    const int i0 = (wave_id() / BK::NBN) * BK::RB * 16, j0 = (wave_id() % BK::NBN) * BK::CB * 16;
+    f4 acc[BK::RB][BK::CB];
+    zero_blk(acc);
+    lds_gemm_nt<CT, H, D, GCARRY_KT, 1>(acc, i0, j0, As, Bs, C, TK, lds);
+    blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
-      });
+      for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
     });
   } else {
     using BK = Blk<D, H>;
-    const CT* A = (m == 2 ? RcT : RbT) + k0;
+    static_assert(BK::NB == 8, "one block per wave");
+    const CT* const As[1] = {(m == 2 ? RcT : RbT) + k0};
+    const CT* const Bs[1] = {HkT + k0};
     float* out = P + (m == 2 ? hd : 3 * hd);
-    for_blocks<D, H>([&](int i0, int j0) {
-      f4 acc[BK::RB][BK::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, A, C, i0, HkT + k0, C, j0);
-      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+    const int i0 = (wave_id() / BK::NBN) * BK::RB * 16, j0 = (wave_id() % BK::NBN) * BK::CB * 16;
+    f4 acc[BK::RB][BK::CB];
+    zero_blk(acc);
+    lds_gemm_nt<CT, D, H, GCARRY_KT, 1>(acc, i0, j0, As, Bs, C, TK, lds);
+    blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * H + j] = acc[rb][cb_][r];
-      });
+      for (int r = 0; r < 4; ++r) out[(size_t)(i + r) * H + j] = acc[rb][cb_][r];
     });
   }
 }
@@ -547,6 +632,7 @@ __global__ void __launch_bounds__(512) gbwd_tile_kernel(GlobalArgs a, int n) {
 // ---------------------------------------------------------------------------
 template <typename CT, int D, int H, int TK>
 __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
   const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
   const int C = a.D.C;
   constexpr size_t hd = (size_t)H * D;
@@ -557,30 +643,32 @@ __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
            *dOT = YkbT + (size_t)D * C;
   const size_t k0 = (size_t)split * TK;
   float* P = a.part + ((size_t)chain * ns + split) * 4 * hd;
+  CT* lds = reinterpret_cast<CT*>(smem);
   if (m == 0) {
     using BK = Blk<H, D>;
-    for_blocks<H, D>([&](int i0, int j0) {
-      f4 acc[BK::RB][BK::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, ZkbT + k0, C, i0, KT + k0, C, j0);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, ZqbT + k0, C, i0, QT + k0, C, j0);
-      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+    static_assert(BK::NB == 8, "one block per wave");
+    const CT* const As[2] = {ZkbT + k0, ZqbT + k0};
+    const CT* const Bs[2] = {KT + k0, QT + k0};
+    const int i0 = (wave_id() / BK::NBN) * BK::RB * 16, j0 = (wave_id() % BK::NBN) * BK::CB * 16;
+    f4 acc[BK::RB][BK::CB];
+    zero_blk(acc);
+    lds_gemm_nt<CT, H, D, GCARRY_KT, 2>(acc, i0, j0, As, Bs, C, TK, lds);
+    blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) P[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
-      });
+      for (int r = 0; r < 4; ++r) P[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
     });
   } else {
     using BK = Blk<D, H>;
-    for_blocks<D, H>([&](int i0, int j0) {
-      f4 acc[BK::RB][BK::CB];
-      zero_blk(acc);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, RT + k0, C, i0, GbT + k0, C, j0);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, YkbT + k0, C, i0, HkT + k0, C, j0);
-      mma_blk<CT, KC, KC, BK::RB, BK::CB, TK>(acc, dOT + k0, C, i0, HqT + k0, C, j0);
-      blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+    static_assert(BK::NB == 8, "one block per wave");
+    const CT* const As[3] = {RT + k0, YkbT + k0, dOT + k0};
+    const CT* const Bs[3] = {GbT + k0, HkT + k0, HqT + k0};
+    const int i0 = (wave_id() / BK::NBN) * BK::RB * 16, j0 = (wave_id() % BK::NBN) * BK::CB * 16;
+    f4 acc[BK::RB][BK::CB];
+    zero_blk(acc);
+    lds_gemm_nt<CT, D, H, GCARRY_KT, 3>(acc, i0, j0, As, Bs, C, TK, lds);
+    blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) P[hd + (size_t)(i + r) * H + j] = acc[rb][cb_][r];
-      });
+      for (int r = 0; r < 4; ++r) P[hd + (size_t)(i + r) * H + j] = acc[rb][cb_][r];
     });
   }
 }
@@ -617,10 +705,13 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), (gfwd_tile_lds<D, H, true>()), st, a, n);
   const int tk = gtk_of(C), ns = C / tk;
   const int sec = section_begin("global_carry", st);
+  constexpr size_t lc = lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>();
+  set_lds_limit((const void*)gfwd_carry_kernel<CT, D, H, GTK_LONG>);
+  set_lds_limit((const void*)gfwd_carry_kernel<CT, D, H, GTK>);
   if (tk == GTK_LONG)
-    hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK_LONG>), dim3(ns, 4, chains), dim3(512), 0, st, a);
+    hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK_LONG>), dim3(ns, 4, chains), dim3(512), lc, st, a);
   else
-    hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK>), dim3(ns, 4, chains), dim3(512), 0, st, a);
+    hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK>), dim3(ns, 4, chains), dim3(512), lc, st, a);
   const hipError_t e = launch_global_carry_reduce(a, n, ns, st);
   section_end(sec, st);
   return e;
@@ -640,9 +731,16 @@ static hipError_t gbwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   auto k1 = gbwd_tile_kernel<IO, CT, ACT, D, H>;
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
-  const int ns = C / GTK;  // the longer splits measured slower here
+  const int tk = gtk_of(C), ns = C / tk;
   const int sec = section_begin("global_bwd_carry", st);
-  hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK>), dim3(ns, 2, chains), dim3(512), 0, st, a);
+  set_lds_limit((const void*)gbwd_state_kernel<CT, D, H, GTK>);
+  set_lds_limit((const void*)gbwd_state_kernel<CT, D, H, GTK_LONG>);
+  if (tk == GTK_LONG)
+    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK_LONG>), dim3(ns, 2, chains), dim3(512),
+                       (lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>()), st, a);
+  else
+    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK>), dim3(ns, 2, chains), dim3(512),
+                       (lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>()), st, a);
   const hipError_t e = launch_gbwd_state_reduce(a, n, ns, st);
   section_end(sec, st);
   return e;
