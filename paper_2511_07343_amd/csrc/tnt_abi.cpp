@@ -357,7 +357,8 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
 // threads serialise their enqueues here.
 struct Fork {
   hipStream_t side = nullptr;
-  hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr, eb = nullptr, eg = nullptr, es = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr, eb = nullptr, eg = nullptr, es = nullptr,
+            ec = nullptr;
 };
 constexpr int MAX_DEV = 64;
 Fork g_fork[MAX_DEV];
@@ -377,6 +378,7 @@ hipError_t fork_of(Fork** out) {
     if ((e = hipEventCreateWithFlags(&f.eb, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.eg, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.es, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.ec, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &f;
   return hipSuccess;
@@ -518,6 +520,7 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     a.pass_a_done = (fk && i == 0) ? fk->ea : nullptr;
     a.aux = (fk && i == 0) ? fk->side : nullptr;  // ahead of the global chain there
     a.aux_done = (fk && i == 0) ? fk->es : nullptr;
+    a.aux_mid = (fk && i == 0) ? fk->ec : nullptr;
     // the last local memory's walk is the point after which dq, dv and every dW_init
     // part are final: the helper stream reduces them beside its gate pass
     const bool last = i == c->n_local - 1;

@@ -109,6 +109,8 @@ struct LocalBwdArgs {
   hipEvent_t aux_done;                                   // needs pass A only (with pass_a_done set):
                                                          // it waits for pass_a_done there, and the
                                                          // gate pass waits for aux_done
+  hipEvent_t aux_mid;                                    // with aux: recorded there once the lower
+                                                         // half of the chunks has its pass A
   int force_generic;                                     // 1: skip fixed-size kernels
 };
 
@@ -144,6 +146,17 @@ struct GlobalArgs {
 };
 
 constexpr int TKS = 8;  // floats per token in GlobalArgs::tokc
+
+// Compute units of the current device (0 if the query fails).
+inline int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return n;
+}
 
 // Allow a kernel the whole LDS of a CU for its dynamic shared memory.
 inline void set_lds_limit(const void* fn) {

@@ -128,6 +128,7 @@ struct SplitPtrs {
   void* brec;       // CT   [units * nch][r.bc.n]  backward records
   float* brec_f;    // fp32 [units * nch][r.bf.n]
   int units;
+  int n0, nc;       // passes A and B: the chunks n0 .. n0 + nc - 1 of every unit
 };
 
 // ===========================================================================
@@ -164,7 +165,7 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
   const int C = Dm.C;
   const int nshard = Dm.L / Dm.S;
   const int nch = Dm.S / C;
-  const int total = P.units * nch;
+  const int total = P.units * P.nc;
   constexpr size_t hd = (size_t)h * d;
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
@@ -175,8 +176,9 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
   using BCH = Blk<CP, H, NWH>;
   static_assert(BCC::NB <= 8, "each wave owns at most one C x C block (its cbar tiles)");
 
-  if (const int t = blockIdx.x; t < total) {  // one chunk per workgroup
-    const int u = t / nch, n = t - u * nch;
+  if (const int tl = blockIdx.x; tl < total) {  // one chunk per workgroup
+    const int u = tl / P.nc, n = P.n0 + (tl - u * P.nc);
+    const int t = u * nch + n;
     const int b = u / (Dm.H * nshard), hh = (u / nshard) % Dm.H, s = u % nshard;
     const CT* fr = (const CT*)a.frec + (size_t)t * Y.r.fc.n;
     const float* frf = a.frec_f + (size_t)t * Y.r.ff.n;
@@ -549,7 +551,7 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 
   // the adjoint leaving the shard's last chunk is zero: that chunk skips every
   // product with it and writes the adjoint without reading it
-  for (int n = nch - 1; n >= 0; --n) {
+  for (int n = P.n0 + P.nc - 1; n >= P.n0; --n) {
     const bool zadj = n == nch - 1;
     const size_t t = (size_t)u * nch + n;
     const CT* rc = (const CT*)a.frec + t * Y.r.fc.n;
@@ -855,9 +857,11 @@ __global__ void __launch_bounds__(512) local_bwd_chain_kernel(LocalBwdArgs a, Sp
 #undef BQ_
 #undef BQF_
   }
-  // adjoint of the learned init for this unit
-  float* dst = a.dWinit_part + (size_t)u * 2 * hd;
-  for (size_t e = threadIdx.x; e < 2 * hd; e += blockDim.x) dst[e] = adj0[e];
+  // adjoint of the learned init for this unit (after the launch that walks chunk 0)
+  if (P.n0 == 0) {
+    float* dst = a.dWinit_part + (size_t)u * 2 * hd;
+    for (size_t e = threadIdx.x; e < 2 * hd; e += blockDim.x) dst[e] = adj0[e];
+  }
 }
 
 // ===========================================================================
@@ -1110,9 +1114,20 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   const SplitSizes z = split_sizes<CT, CP, D, H>(units, nch);
   if (bytes) *bytes = total_bytes<CT>(z);
   if (!a) return true;
-  const SplitPtrs P = carve<CT>(ws, z, units);
+  SplitPtrs P = carve<CT>(ws, z, units);
   constexpr SplitLayout Y = make_split_layout(CP, D, H);
   const int total = units * nch;
+  // When the walks leave half the CUs free and are long (32 chunks or more), the
+  // chunks are cut in two: passes A and B take the upper half first, and the
+  // lower half's pass A runs on the second stream beside the walk of the upper
+  // half (the walk reaches the lower half only after it).  Each half's pass A
+  // writes only that half's records and dq, dk rows.  The second stream runs the
+  // global chain after it, so with short walks the split only delays that chain.
+  const bool halves = a->aux && a->aux_mid && a->aux_done && a->pass_a_done && nch >= 32 &&
+                      2 * units <= device_cus();
+  const int nlo = halves ? nch / 2 : 0;
+  P.n0 = nlo;
+  P.nc = nch - nlo;
   auto ka = local_bwd_ret_kernel<IO, CT, ACT, D, H, CP>;
   auto kb = local_bwd_chain_kernel<IO, CT, ACT, D, H, CP>;
   auto kc = local_bwd_gate_kernel<CT, D, H, CP>;
@@ -1126,13 +1141,21 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   set_lds_limit((const void*)ka);
   set_lds_limit((const void*)kb);
   set_lds_limit((const void*)kc);
-  hipLaunchKernelGGL(ka, dim3(total), dim3(512), lds_a, st, *a, P);
+  hipLaunchKernelGGL(ka, dim3(units * P.nc), dim3(512), lds_a, st, *a, P);
   auto fail = [&](hipError_t e) {
     *err = e;
     return true;
   };
   hipError_t e;
   if (a->pass_a_done && (e = hipEventRecord(a->pass_a_done, st)) != hipSuccess) return fail(e);
+  SplitPtrs Plo = P;
+  Plo.n0 = 0;
+  Plo.nc = nlo;
+  if (halves) {
+    if ((e = hipStreamWaitEvent(a->aux, a->pass_a_done, 0)) != hipSuccess) return fail(e);
+    hipLaunchKernelGGL(ka, dim3(units * nlo), dim3(512), lds_a, a->aux, *a, Plo);
+    if ((e = hipEventRecord(a->aux_mid, a->aux)) != hipSuccess) return fail(e);
+  }
   // the suffix sums of pass A's Xbar^T Q over later chunks (read by the gate
   // pass): on the second stream beside the walk when there is one
   const bool scan = Dm.qk_proj && Dm.qk_scope == 0;
@@ -1143,12 +1166,16 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
                        P.brec_f, Y.r.bf.n, Y.r.bf.o[rec::XbQ], units, nch, D * D);
   };
   if (on_aux) {
-    if ((e = hipStreamWaitEvent(a->aux, a->pass_a_done, 0)) != hipSuccess) return fail(e);
+    if (!halves && (e = hipStreamWaitEvent(a->aux, a->pass_a_done, 0)) != hipSuccess) return fail(e);
     launch_scan(a->aux);
     if ((e = hipEventRecord(a->aux_done, a->aux)) != hipSuccess) return fail(e);
   }
   const int sec = section_begin("local_bwd_walk", st);  // the walk of the carried adjoint alone
   hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, P);
+  if (halves) {
+    if ((e = hipStreamWaitEvent(st, a->aux_mid, 0)) != hipSuccess) return fail(e);
+    hipLaunchKernelGGL(kb, dim3(units), dim3(512), lds_b, st, *a, Plo);
+  }
   section_end(sec, st);
   if (a->pass_b_done && (e = hipEventRecord(a->pass_b_done, st)) != hipSuccess) return fail(e);
   if (on_aux) {
