@@ -101,7 +101,12 @@ typedef struct {
 typedef enum {
   TNT_WS_FWD = 0,          /* tnt_mem_fwd                                       */
   TNT_WS_BWD = 1,          /* tnt_mem_bwd given the forward's saved buffer     */
-  TNT_WS_BWD_RECOMPUTE = 2 /* tnt_mem_bwd with saved == NULL                   */
+  TNT_WS_BWD_RECOMPUTE = 2,/* tnt_mem_bwd with saved == NULL                   */
+  TNT_WS_FWD_MIN = 3       /* the least tnt_mem_fwd accepts: with saved == NULL
+                              and less than TNT_WS_FWD, each local memory's
+                              forward runs as one walk per shard instead of the
+                              walk plus the chunk-parallel retrieval (same
+                              results to rounding, slower)                      */
 } tnt_ws_kind;
 
 /* Bytes of device workspace the call needs (0 if the config is invalid). */
@@ -146,7 +151,9 @@ size_t tnt_mem_saved_size(const tnt_config* cfg);
  *   saved       : may be NULL; else saved_bytes >= tnt_mem_saved_size(cfg)
  *                 (TNT_ERR_WORKSPACE otherwise) that receive the header and the
  *                 chunk-entry states for a later tnt_mem_bwd.
- *   workspace   : ws_bytes >= tnt_mem_workspace_size(cfg, TNT_WS_FWD). */
+ *   workspace   : ws_bytes >= tnt_mem_workspace_size(cfg, TNT_WS_FWD_MIN); with
+ *                 saved == NULL, ws_bytes >= tnt_mem_workspace_size(cfg, TNT_WS_FWD)
+ *                 lets the local memories take the two-pass forward. */
 tnt_status tnt_mem_fwd(const tnt_config* cfg, const void* q, const void* k, const void* v,
                        const float* lr, const float* mom, const float* decay,
                        const float* W1_init, const float* W2_init, void* o,
@@ -172,8 +179,9 @@ tnt_status tnt_mem_bwd(const tnt_config* cfg, const void* q, const void* k, cons
  * of tnt_mem_fwd with no workspace and no saved buffer arguments.  Its
  * workspace is a device array of TNT_NOALLOC_WORKSPACE_BYTES that the library
  * holds on each GPU it runs on from the first call there until the process
- * ends; configurations whose forward workspace (tnt_mem_workspace_size(cfg,
- * TNT_WS_FWD)) is larger get TNT_ERR_WORKSPACE.  The call allocates nothing
+ * ends; configurations whose smallest forward workspace (tnt_mem_workspace_size(cfg,
+ * TNT_WS_FWD_MIN)) is larger get TNT_ERR_WORKSPACE (the forward takes the faster
+ * two-pass local path when TNT_WS_FWD also fits).  The call allocates nothing
  * (no hipMalloc / hipFree, no helper stream: every launch is on `stream`), and
  * the forward writes every part of that array it reads, so the previous
  * call's contents do not matter.  All calls on one GPU share the array: calls

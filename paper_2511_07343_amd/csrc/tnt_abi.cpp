@@ -113,6 +113,9 @@ struct Layout {
   size_t w_opart, w_tokc, w_chunkc, w_R, w_part, w_gpack, w_gop, w_scr[TNT_MAX_LOCAL],
       w_fsplit[TNT_MAX_LOCAL], w_ring,
       fwd_bytes;
+  // without a saved buffer, the two-pass local forward's every-slot compute-type
+  // state copies and fp32 Q-K states (SIZE_MAX: that memory walks in one pass)
+  size_t w_nt[TNT_MAX_LOCAL], w_nm[TNT_MAX_LOCAL], fwd_two_bytes;
   size_t ring_g, ring_l[TNT_MAX_LOCAL], ring_m[TNT_MAX_LOCAL];
   LocalPlan lplan[TNT_MAX_LOCAL];
   // backward workspace
@@ -224,6 +227,16 @@ Layout layout_of(const tnt_config* c, int gsub0 = 0) {
   }
   y.fwd_bytes = off;
   (void)fwd_core;
+  // the two-pass local forward without a saved buffer: past the smallest forward
+  // workspace (the backward workspace may reuse this space: it never runs a
+  // forward without saving)
+  for (int i = 0; i < c->n_local; ++i) {
+    y.w_nt[i] = y.w_nm[i] = SIZE_MAX;
+    if (!y.l_fslots[i]) continue;  // the memories whose forward has both passes
+    y.w_nt[i] = off; off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * (4 * y.hd + dd) * cts);
+    y.w_nm[i] = off; off += up((size_t)y.l_units[i] * (y.l_chunks[i] + 1) * dd * f);
+  }
+  y.fwd_two_bytes = off;
 
   // backward workspace (shares the forward's front part for recomputation)
   off = y.fwd_bytes;
@@ -396,7 +409,11 @@ hipError_t fork_of(Fork** out) {
 tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, const void* k,
                        const void* v, const float* lr, const float* mom, const float* decay,
                        const float* W1i, const float* W2i, void* o, float* final_state,
-                       char* sv, char* ws, hipStream_t st, bool fork = true) {
+                       char* sv, char* ws, hipStream_t st, bool fork = true,
+                       size_t ws_bytes = 0) {
+  // no saved buffer: the two-pass local forward still runs when the workspace
+  // holds its state copies
+  const bool two = !sv && ws_bytes >= y.fwd_two_bytes;
   const size_t G = y.gates;
   float* opart = (float*)(ws + y.w_opart);
   int m = 0;
@@ -421,14 +438,15 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     a.W1i = W1i + (size_t)m * c->H * y.hd;
     a.W2i = W2i + (size_t)m * c->H * y.hd;
     a.o_part = opart + (size_t)m * y.io_elems;
+    const bool two_i = two && y.w_nt[i] != SIZE_MAX;
     a.states = sv ? (float*)(sv + y.sv_l[i]) : (float*)(ws + y.ring_l[i]);
-    a.mstates = sv ? (float*)(sv + y.sv_m[i]) : (float*)(ws + y.ring_m[i]);
-    a.statesT = sv ? (void*)(sv + y.sv_t[i]) : nullptr;
+    a.mstates = sv ? (float*)(sv + y.sv_m[i]) : two_i ? (float*)(ws + y.w_nm[i]) : (float*)(ws + y.ring_m[i]);
+    a.statesT = sv ? (void*)(sv + y.sv_t[i]) : two_i ? (void*)(ws + y.w_nt[i]) : nullptr;
     a.frec = (sv && y.sv_fr[i] != SIZE_MAX) ? (void*)(sv + y.sv_fr[i]) : nullptr;
     a.frec_f = (sv && y.sv_frf[i] != SIZE_MAX) ? (float*)(sv + y.sv_frf[i]) : nullptr;
     const bool grouped = i == 0 && y.gsub0;
-    a.nslots = (sv || grouped) ? y.l_chunks[i] + 1 : 2;
-    a.fslots = sv ? y.l_fslots[i] : 0;
+    a.nslots = (sv || grouped || two_i) ? y.l_chunks[i] + 1 : 2;
+    a.fslots = sv ? y.l_fslots[i] : two_i ? 2 : 0;  // two_i: the two-slot fp32 ring
     a.scratch = ws + y.w_scr[i];
     a.fsplit = y.w_fsplit[i] != SIZE_MAX ? (void*)(ws + y.w_fsplit[i]) : nullptr;
     a.plan = y.lplan[i];
@@ -688,7 +706,8 @@ size_t tnt_mem_workspace_size(const tnt_config* cfg, int kind) {
   if (validate(cfg) != TNT_OK) return 0;
   const Eff E = effective(cfg);
   const Layout y = layout_of(&E.c, E.gsub);
-  if (kind == TNT_WS_FWD) return y.fwd_bytes;
+  if (kind == TNT_WS_FWD) return y.fwd_two_bytes;
+  if (kind == TNT_WS_FWD_MIN) return y.fwd_bytes;
   if (kind == TNT_WS_BWD) return y.bwd_bytes;
   if (kind == TNT_WS_BWD_RECOMPUTE) return y.bwd_re_bytes;
   return 0;
@@ -732,7 +751,7 @@ tnt_status forward_entry(const tnt_config* cfg, const void* q, const void* k, co
   if (saved && saved_bytes < y.saved_bytes) return TNT_ERR_WORKSPACE;
   const SavedHeader hdr = header_of(cfg, y);
   s = run_forward(&E.c, y, q, k, v, lr, mom, decay, W1_init, W2_init, o, final_state,
-                  (char*)saved, (char*)workspace, stream, fork);
+                  (char*)saved, (char*)workspace, stream, fork, ws_bytes);
   if (s != TNT_OK || !saved) return s;
   if (launch_write_header(saved, hdr, stream) != hipSuccess) return TNT_ERR_HIP;
   remember_saved(saved, hdr);

@@ -45,7 +45,7 @@ extern "C" tnt_status tnt_mem_fwd_noalloc(const tnt_config* cfg, const void* q, 
                                           const float* W2_init, void* o, float* final_state,
                                           void* stream) {
   if (!cfg) return TNT_ERR_NULL;
-  if (tnt_mem_workspace_size(cfg, TNT_WS_FWD) > (size_t)TNT_NOALLOC_WORKSPACE_BYTES) {
+  if (tnt_mem_workspace_size(cfg, TNT_WS_FWD_MIN) > (size_t)TNT_NOALLOC_WORKSPACE_BYTES) {
     // an invalid configuration sizes to 0 and gets its own error below
     return TNT_ERR_WORKSPACE;
   }

@@ -19,7 +19,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtnt.so"
 _lib = None
 
 TNT_MAX_LOCAL = 4
-TNT_WS_FWD, TNT_WS_BWD, TNT_WS_BWD_RECOMPUTE = 0, 1, 2
+TNT_WS_FWD, TNT_WS_BWD, TNT_WS_BWD_RECOMPUTE, TNT_WS_FWD_MIN = 0, 1, 2, 3
 STATUS = {0: "TNT_OK", 1: "TNT_ERR_NULL", 2: "TNT_ERR_SHAPE", 3: "TNT_ERR_UNSUPPORTED",
           4: "TNT_ERR_WORKSPACE", 5: "TNT_ERR_ALIGN", 6: "TNT_ERR_HIP", 7: "TNT_ERR_ARG"}
 EXPORTED = ["tnt_mem_workspace_size", "tnt_mem_saved_size", "tnt_mem_fwd", "tnt_mem_bwd",

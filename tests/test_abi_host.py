@@ -55,8 +55,12 @@ def test_strerror_names():
 
 @pytest.mark.parametrize("cfg", WORKLOADS, ids=lambda c: c.name.split()[0] + str(c.L))
 def test_workspace_sizes_positive(cfg):
-    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD) > 0
-    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD) > tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD)
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD_MIN) > 0
+    # the full forward workspace adds the no-save two-pass forward's state copies
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD) >= \
+        tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD_MIN)
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD) > \
+        tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD_MIN)
     assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD_RECOMPUTE) >= \
         tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_BWD) + tnt.tnt_mem_saved_size(cfg)
     assert tnt.tnt_mem_saved_size(cfg) > 0

@@ -21,9 +21,15 @@ def tol(cfg):
     return 2e-2 if cfg.dtype == BF16 else 1e-4
 
 
-def gpu_forward(cfg, inp, save=True, final=False):
+def gpu_forward(cfg, inp, save=True, final=False, min_workspace=False):
+    """min_workspace: only the smallest forward workspace (TNT_WS_FWD_MIN), so
+    that without a saved buffer the local memories walk in one pass."""
     x = tnt.device_inputs(inp, cfg)
-    o, saved, fin = tnt.forward(cfg, x, save=save, final_state=final)
+    ws = None
+    if min_workspace:
+        ws = torch.empty(max(tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD_MIN), 16),
+                         dtype=torch.uint8, device=x["q"].device)
+    o, saved, fin = tnt.forward(cfg, x, save=save, final_state=final, workspace=ws)
     torch.cuda.synchronize()
     return (o.float().cpu().numpy(), None if fin is None else fin.cpu().numpy())
 
@@ -79,14 +85,15 @@ SAVE_RING = [
 
 @pytest.mark.parametrize("cfg", SAVE_RING, ids=lambda c: c.name)
 def test_forward_save_and_ring_agree(cfg):
-    """The saved-state path and the two-slot ring path agree (for the
-    fixed-size bf16 kernels: the register-resident walk plus the chunk-parallel
-    retrieval against the one-walk kernel, which round in different orders),
-    and both match the oracle."""
+    """The saved-state path and the two-slot ring path (no saved buffer, the
+    smallest workspace) agree (for the fixed-size bf16 kernels: the
+    register-resident walk plus the chunk-parallel retrieval against the
+    one-walk kernel, which round in different orders), and both match the
+    oracle."""
     inp = make_inputs(cfg, 102)
     print(f"\n[case] save vs ring {cfg.name}", flush=True)
     a, _ = gpu_forward(cfg, inp, save=True)
-    b, _ = gpu_forward(cfg, inp, save=False)
+    b, _ = gpu_forward(cfg, inp, save=False, min_workspace=True)
     ref = O.forward_pairs(inp, cfg, O.all_pairs(cfg)).numpy().reshape(a.shape)
     ea, eb, eab = max_rel_err(a, ref), max_rel_err(b, ref), max_rel_err(a, b)
     print(f"  saved {ea:.3e} ring {eb:.3e} between {eab:.3e}", flush=True)
@@ -110,6 +117,18 @@ def test_forward_state_ring_agrees(cfg):
     assert check_err(f"fwd default walk {cfg.name}", "o", max_rel_err(a, ref), tol(cfg))
     assert check_err(f"fwd fp32-slot walk {cfg.name}", "o", max_rel_err(b, ref), tol(cfg))
     assert max_rel_err(a, b) <= tol(cfg)
+
+
+@pytest.mark.parametrize("cfg", SAVE_RING, ids=lambda c: c.name)
+def test_forward_without_saving_takes_both_passes(cfg):
+    """Without a saved buffer but with the full forward workspace, the local
+    memories run the walk plus the chunk-parallel retrieval from state copies in
+    the workspace: the output equals the saving forward's bit for bit."""
+    inp = make_inputs(cfg, 107)
+    print(f"\n[case] no-save two-pass {cfg.name}", flush=True)
+    a, _ = gpu_forward(cfg, inp, save=True, final=bool(cfg.has_global))
+    b, _ = gpu_forward(cfg, inp, save=False, final=bool(cfg.has_global))
+    assert np.array_equal(a, b)
 
 
 def test_forward_deterministic():

@@ -33,7 +33,7 @@ def test_noalloc_forward_matches_tnt_mem_fwd_two_calls():
     outs = []
     for cfg, seed in ((BIG, 601), (SMALL, 602)):   # the second call is the smaller one
         print(f"\n[case] {cfg.name}", flush=True)
-        assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD) <= tnt.NOALLOC_WORKSPACE_BYTES
+        assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD_MIN) <= tnt.NOALLOC_WORKSPACE_BYTES
         inp = make_inputs(cfg, seed)
         x = tnt.device_inputs(inp, cfg)
         o_na, fin_na = _noalloc(cfg, x)
@@ -52,6 +52,6 @@ def test_noalloc_forward_matches_tnt_mem_fwd_two_calls():
 
 def test_noalloc_rejects_oversized_config():
     cfg = WORKLOADS[2]   # forward workspace ~785 MiB
-    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD) > tnt.NOALLOC_WORKSPACE_BYTES
+    assert tnt.tnt_mem_workspace_size(cfg, tnt.TNT_WS_FWD_MIN) > tnt.NOALLOC_WORKSPACE_BYTES
     p = 256
     assert tnt.tnt_mem_fwd_noalloc(cfg, p, p, p, p, p, p, p, p, p, None, stream=0) == 4
