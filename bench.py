@@ -88,7 +88,8 @@ def hbm_bytes(cfg, name):
     global_carry (one forward chunk): reads the chunk's carry operands D1^T, Hk^T
     (C x hid each) and the four coefficient-scaled K^T, R^T (C x d each) in the
     compute type, reads the entry state (V1, S1, V2, S2: 4 hid d fp32), writes
-    the exit state.  global_bwd_carry (one backward chunk): reads the ten
+    the exit state and the next chunk's compute-type copies of V1, V2 (as they
+    are and transposed: 4 hid d elements).  global_bwd_carry (one backward chunk): reads the ten
     operands of the entry-adjoint products (Zkbar, Zqbar, Gbar, Hk, Hq: C x hid;
     K, Q, R, Ykbar, dO: C x d) in the compute type, reads the state and the exit
     adjoint, writes the entry adjoint (each 4 hid d fp32)."""
@@ -99,7 +100,7 @@ def hbm_bytes(cfg, name):
     if name == "global_scan":
         return chains * (L * (3 * 4 + 6 * 4) + (L // C) * 16)
     if name == "global_carry":
-        return chains * ((2 * h + 4 * d) * C * cts + 2 * st)
+        return chains * ((2 * h + 4 * d) * C * cts + 2 * st + 4 * h * d * cts)
     if name == "global_bwd_carry":
         return chains * (5 * (h + d) * C * cts + 3 * st)
     if name == "local_carry":

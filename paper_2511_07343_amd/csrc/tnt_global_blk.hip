@@ -109,6 +109,53 @@ __global__ void __launch_bounds__(256) gtranspose_kernel(const float* src, size_
   for (int k = ty; k < 32; k += 8) o[(size_t)(c0 + k) * R + r0 + tx] = from_f<CT>(t[tx][k]);
 }
 
+// The carry's reduction fused with the next chunk's state copies: per 32 x 32
+// tile of the pair (W_m, S_m) (m = 0: W1, S1 [hid][d]; m = 1: W2, S2 [d][hid]),
+//   W' = A_C W + E_C S - sum_splits dW,  S' = B_C S - sum_splits dS
+// (fixed split order, four consecutive elements a thread as the unfused
+// reduction forms them) into fp32 slot n + 1, and W' in bf16 transposed into
+// packT (W1^T, W2^T) and as it is (W1, W2 after 2 hd), the layout the next
+// chunk's tile reads.
+template <typename CT>
+__global__ void __launch_bounds__(256) gcarry_reduce_pack_kernel(GlobalArgs a, int n, int nsplit) {
+  __shared__ float t[32][33];
+  const Dims D = a.D;
+  const int m = blockIdx.z, chain = blockIdx.y;
+  const int d = D.d, h = D.hid;
+  const size_t hd = (size_t)h * d;
+  const int R = m ? d : h, Cc = m ? h : d;  // rows and columns of W_m
+  const int tc = Cc / 32;
+  const int r0 = (blockIdx.x / tc) * 32, c0 = (blockIdx.x % tc) * 32;
+  const float* V = a.states + ((size_t)chain * a.nslots + (n % a.nslots)) * 4 * hd;
+  float* Vn = a.states + ((size_t)chain * a.nslots + ((n + 1) % a.nslots)) * 4 * hd;
+  const float* P = a.part + (size_t)chain * nsplit * 4 * hd;
+  const float* cc = a.chunkc + ((size_t)chain * (D.L / D.C) + n) * 4;
+  const float AC = cc[0], BC = cc[1], EC = cc[2];
+  CT* pk = (CT*)a.packT + (size_t)chain * 4 * hd;
+  {
+    const int k = threadIdx.x >> 3, c4 = (threadIdx.x & 7) * 4;
+    const size_t e = (size_t)(r0 + k) * Cc + c0 + c4;
+    const size_t ew = (size_t)m * hd + e, es = (size_t)(2 + m) * hd + e;
+    f32x4 dw = {0.f, 0.f, 0.f, 0.f}, ds = dw;
+    for (int sp = 0; sp < nsplit; ++sp) {
+      dw += *reinterpret_cast<const f32x4*>(P + (size_t)sp * 4 * hd + ew);
+      ds += *reinterpret_cast<const f32x4*>(P + (size_t)sp * 4 * hd + es);
+    }
+    const f32x4 w = *reinterpret_cast<const f32x4*>(V + ew);
+    const f32x4 sv = *reinterpret_cast<const f32x4*>(V + es);
+    const f32x4 nw = AC * w + EC * sv - dw;
+    *reinterpret_cast<f32x4*>(Vn + ew) = nw;
+    *reinterpret_cast<f32x4*>(Vn + es) = BC * sv - ds;
+    store4<CT>(pk + 2 * hd + ew, nw);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) t[k][c4 + q] = nw[q];
+  }
+  __syncthreads();
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  CT* o = pk + (size_t)m * hd;
+  for (int k = ty; k < 32; k += 8) o[(size_t)(c0 + k) * R + r0 + tx] = from_f<CT>(t[tx][k]);
+}
+
 template <typename CT>
 static void launch_gtranspose(const float* src, size_t src_stride, CT* dst, size_t dst_stride,
                               CT* dstn, size_t dstn_stride, int chains, int d, int h, int mask,
@@ -688,8 +735,11 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   constexpr int TT = gtile_rows<H>();
   const int chains = a.D.B * a.D.H, C = a.D.C;
   constexpr size_t hd = (size_t)H * D;
-  launch_gtranspose<CT>(a.states + (size_t)(n % a.nslots) * 4 * hd, (size_t)a.nslots * 4 * hd,
-                        (CT*)a.packT, 4 * hd, (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
+  // chunk 0's state copies; every later chunk's are written by the reduction
+  // that forms its state
+  if (n == 0)
+    launch_gtranspose<CT>(a.states, (size_t)a.nslots * 4 * hd, (CT*)a.packT, 4 * hd,
+                          (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
   static_assert(sizeof(CT) == 2, "gfwd_tile_lds counts 2-byte elements");
   // the backward reads the chunk-entry states only: the carry out of the last
   // chunk (and the tile's key side that feeds it) runs when the caller asks for
@@ -712,9 +762,10 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
     hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK_LONG>), dim3(ns, 4, chains), dim3(512), lc, st, a);
   else
     hipLaunchKernelGGL((gfwd_carry_kernel<CT, D, H, GTK>), dim3(ns, 4, chains), dim3(512), lc, st, a);
-  const hipError_t e = launch_global_carry_reduce(a, n, ns, st);
+  hipLaunchKernelGGL(gcarry_reduce_pack_kernel<CT>, dim3((unsigned)(hd / 1024), chains, 2), dim3(256), 0,
+                     st, a, n, ns);
   section_end(sec, st);
-  return e;
+  return hipGetLastError();
 }
 
 template <typename IO, typename ACT_T, int ACT, int D, int H>

@@ -41,8 +41,9 @@ def test_hbm_bytes_workload2():
     chains = cfg.B * cfg.H
     assert bench.hbm_bytes(cfg, "global_scan") == chains * (cfg.L * 36 + (cfg.L // cfg.C_G) * 16)
     st = 4 * cfg.hid * cfg.d * 4
+    # operands, entry and exit state, and the next chunk's four bf16 state copies
     assert bench.hbm_bytes(cfg, "global_carry") == \
-        chains * ((2 * cfg.hid + 4 * cfg.d) * cfg.C_G * 2 + 2 * st)
+        chains * ((2 * cfg.hid + 4 * cfg.d) * cfg.C_G * 2 + 2 * st + 4 * cfg.hid * cfg.d * 2)
     assert bench.hbm_bytes(cfg, "local_bwd") is None
 
 
