@@ -26,7 +26,7 @@ enum FwdCT {
   Hk, HkT, D1, HT, Sp, Spp, G, Sz,              // C x h (Sp, Spp, G, Sz fragment-major)
   PzT, PoT, StrT,                               // C x C
   K, KT, KcC, Kb, R, RT, RcC, Rb,               // C x d
-  X, XT, XAT, XET, N, NT, QT,                   // C x d
+  XT, XAT, XET, N, NT, QT,                      // C x d
   FWD_CT
 };
 // forward record, fp32
@@ -78,7 +78,7 @@ struct RecLayout {
 __host__ __device__ constexpr RecLayout make_rec_layout(int Cp, int d, int h) {
   const size_t C = Cp, Cd = C * d, Ch = C * h, CC = C * C, dd = (size_t)d * d;
   const size_t sfc[FWD_CT] = {Ch, Ch, Ch, Ch, Ch, Ch, Ch, Ch, CC, CC, CC, Cd, Cd, Cd, Cd,
-                              Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd};
+                              Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd};
   const size_t sff[FWD_F] = {CC, CC, Cd, Cd, C, C, C, 4};
   const size_t sbc[BWD_CT] = {Ch, CC, Cd, Cd, Cd};
   const size_t sbf[BWD_F] = {CC, C, C, dd, C, C, 4};

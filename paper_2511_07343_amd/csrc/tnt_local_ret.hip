@@ -196,7 +196,8 @@ local_ret_kernel(LocalFwdArgs a) {
   }
   __syncthreads();
 
-  // ---- the forward record: K, R, X and their scaled / transposed forms, Q^T,
+  // ---- the forward record: K, R and their scaled / transposed forms, X^T scaled
+  // and as it is, Q^T,
   // N, N^T, tril(Q N^T)^T (eight destination elements per thread, 16-byte
   // stores; transposed destinations gather their eight sources from LDS)
   if (fr) {
@@ -217,7 +218,6 @@ local_ret_kernel(LocalFwdArgs a) {
       const size_t ec = (size_t)jt * LDC + it;             // [D][CP] element e0 in LDS
       cp8(rec::K, e0, sK + ed);
       cp8(rec::R, e0, sR + ed);
-      cp8(rec::X, e0, sX + ed);
       float kc[8], kb[8], rc[8], rb[8], kt[8], rt[8], xt[8], xa[8], xe[8], qt[8];
 #pragma unroll
       for (int qq = 0; qq < 8; ++qq) {
