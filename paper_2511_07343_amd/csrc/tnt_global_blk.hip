@@ -673,11 +673,104 @@ __global__ void __launch_bounds__(512) gbwd_tile_kernel(GlobalArgs a, int n) {
 }
 
 // ---------------------------------------------------------------------------
+// backward tile of the last chunk, whose exit adjoint is zero: every term of
+// the key side (T3..T6, D1bar, Gbar, Rbar, Ykbar, Hkbar, Zkbar) vanishes, so dk
+// and dv of its tokens are zero and only the query side remains, Zq -> Hq,
+// Zqbar = (dO V2) * s'(Zq), dq = Zqbar V1, with the operands of the entry-adjoint
+// products that do not vanish (Zqbar^T Q, dO^T Hq)
+// ---------------------------------------------------------------------------
+template <typename IO, typename CT, int ACT, int D, int H>
+__global__ void __launch_bounds__(512) gbwd_tile_last_kernel(GlobalArgs a, int n) {
+  constexpr int TT = gtile_rows<H>();
+  extern __shared__ __align__(16) unsigned char smem[];
+  CT* sQ = reinterpret_cast<CT*>(smem);  // [TT][D]
+  CT* sdO = sQ + TT * D;                 // [TT][D]
+  CT* sZqb = sdO + TT * D;               // [TT][H]
+  const Dims Dm = a.D;
+  const int C = Dm.C;
+  const int chain = blockIdx.y, r0 = blockIdx.x * TT;
+  constexpr size_t hd = (size_t)H * D;
+  const CT* pS = (const CT*)a.packT + (size_t)chain * 4 * hd;
+  const CT *V1T = pS, *V2T = pS + hd, *V1 = pS + 2 * hd;
+  CT* op = (CT*)a.opT + (size_t)chain * 5 * ((size_t)H + D) * C;
+  CT *ZqbT = op + (size_t)H * C, *HqT = op + 4 * (size_t)H * C, *QT = op + 5 * (size_t)H * C + (size_t)D * C,
+     *dOT = op + 5 * (size_t)H * C + 4 * (size_t)D * C;
+  const size_t tok0 = (size_t)n * C + r0;
+  const size_t cb = (size_t)chain * Dm.L + tok0;
+  const IO* q = (const IO*)a.q + cb * D;
+  const IO* dO = (const IO*)a.dO + cb * D;
+  float* dtk = a.dtok + cb * 4;
+  float* dqp = a.dq_part + cb * D;
+  float* dkp = a.dk_part + cb * D;
+  float* dvp = a.dv_part + cb * D;
+
+  for (int e = threadIdx.x; e < TT * (D / 8); e += blockDim.x) {
+    const int i = e % TT, j0 = (e / TT) * 8;
+    float qx[8], ox[8];
+    gload8(q + (size_t)i * D + j0, qx);
+    gload8(dO + (size_t)i * D + j0, ox);
+    gstore8<CT>(sQ + (size_t)i * D + j0, qx);
+    gstore8<CT>(sdO + (size_t)i * D + j0, ox);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const size_t et = (size_t)(j0 + t) * C + r0 + i;
+      QT[et] = from_f<CT>(qx[t]);
+      dOT[et] = from_f<CT>(ox[t]);
+    }
+  }
+  for (int e = threadIdx.x * 4; e < TT * D; e += blockDim.x * 4) {
+    *reinterpret_cast<f32x4*>(dkp + e) = f32x4{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f32x4*>(dvp + e) = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  if (threadIdx.x < TT) {
+    dtk[(size_t)threadIdx.x * 4 + 0] = 0.f;
+    dtk[(size_t)threadIdx.x * 4 + 1] = 0.f;
+  }
+  __syncthreads();
+  using BH = Blk<TT, H>;
+  using BD = Blk<TT, D>;
+  // Zq -> Hq ; Zqbar = (dO V2) * s'(Zq)
+  for_blocks<TT, H>([&](int i0, int j0) {
+    f4 aq[BH::RB][BH::CB], ap[BH::RB][BH::CB];
+    zero_blk(aq);
+    zero_blk(ap);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(aq, sQ, D, i0, V1, D, j0);
+    mma_blk<CT, KC, KC, BH::RB, BH::CB, D>(ap, sdO, D, i0, V2T, D, j0);
+    blk_each4<BH::RB, BH::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+      f4 hq, zq;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const ActVals z = act_all<ACT>(aq[rb][cb_][r]);
+        hq[r] = z.s;
+        zq[r] = ap[rb][cb_][r] * z.d1;
+        sZqb[(size_t)(i + r) * H + j] = from_f<CT>(zq[r]);
+      }
+      const size_t et = (size_t)j * C + r0 + i;
+      store4<CT>(HqT + et, hq);
+      store4<CT>(ZqbT + et, zq);
+    });
+  });
+  __syncthreads();
+  // dq = Zqbar V1
+  for_blocks<TT, D>([&](int i0, int j0) {
+    f4 aq[BD::RB][BD::CB];
+    zero_blk(aq);
+    mma_blk<CT, KC, KC, BD::RB, BD::CB, H>(aq, sZqb, H, i0, V1T, H, j0);
+    blk_each4<BD::RB, BD::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dqp[(size_t)(i + r) * D + j] = aq[rb][cb_][r];
+    });
+  });
+}
+
+// ---------------------------------------------------------------------------
 // backward entry-adjoint partials of token split `blockIdx.x`:
 //   m = 0: Zkbar^T K + Zqbar^T Q            -> V1 slot (hid x d)
 //   m = 1: R^T Gbar + Ykbar^T Hk + dO^T Hq  -> V2 slot (d x hid)
 // ---------------------------------------------------------------------------
-template <typename CT, int D, int H, int TK>
+// ZA: the chunk's exit adjoint is zero (its key-side operands vanish): only
+// Zqbar^T Q and dO^T Hq remain
+template <typename CT, int D, int H, int TK, bool ZA = false>
 __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int split = blockIdx.x, m = blockIdx.y, chain = blockIdx.z, ns = gridDim.x;
@@ -694,12 +787,18 @@ __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
   if (m == 0) {
     using BK = Blk<H, D>;
     static_assert(BK::NB == 8, "one block per wave");
-    const CT* const As[2] = {ZkbT + k0, ZqbT + k0};
-    const CT* const Bs[2] = {KT + k0, QT + k0};
     const int i0 = (wave_id() / BK::NBN) * BK::RB * 16, j0 = (wave_id() % BK::NBN) * BK::CB * 16;
     f4 acc[BK::RB][BK::CB];
     zero_blk(acc);
-    lds_gemm_nt<CT, H, D, GCARRY_KT, 2>(acc, i0, j0, As, Bs, C, TK, lds);
+    if constexpr (ZA) {
+      const CT* const As[1] = {ZqbT + k0};
+      const CT* const Bs[1] = {QT + k0};
+      lds_gemm_nt<CT, H, D, GCARRY_KT, 1>(acc, i0, j0, As, Bs, C, TK, lds);
+    } else {
+      const CT* const As[2] = {ZkbT + k0, ZqbT + k0};
+      const CT* const Bs[2] = {KT + k0, QT + k0};
+      lds_gemm_nt<CT, H, D, GCARRY_KT, 2>(acc, i0, j0, As, Bs, C, TK, lds);
+    }
     blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) P[(size_t)(i + r) * D + j] = acc[rb][cb_][r];
@@ -707,12 +806,18 @@ __global__ void __launch_bounds__(512) gbwd_state_kernel(GlobalArgs a) {
   } else {
     using BK = Blk<D, H>;
     static_assert(BK::NB == 8, "one block per wave");
-    const CT* const As[3] = {RT + k0, YkbT + k0, dOT + k0};
-    const CT* const Bs[3] = {GbT + k0, HkT + k0, HqT + k0};
     const int i0 = (wave_id() / BK::NBN) * BK::RB * 16, j0 = (wave_id() % BK::NBN) * BK::CB * 16;
     f4 acc[BK::RB][BK::CB];
     zero_blk(acc);
-    lds_gemm_nt<CT, D, H, GCARRY_KT, 3>(acc, i0, j0, As, Bs, C, TK, lds);
+    if constexpr (ZA) {
+      const CT* const As[1] = {dOT + k0};
+      const CT* const Bs[1] = {HqT + k0};
+      lds_gemm_nt<CT, D, H, GCARRY_KT, 1>(acc, i0, j0, As, Bs, C, TK, lds);
+    } else {
+      const CT* const As[3] = {RT + k0, YkbT + k0, dOT + k0};
+      const CT* const Bs[3] = {GbT + k0, HkT + k0, HqT + k0};
+      lds_gemm_nt<CT, D, H, GCARRY_KT, 3>(acc, i0, j0, As, Bs, C, TK, lds);
+    }
     blk_each4<BK::RB, BK::CB>(i0, j0, [&](int rb, int cb_, int i, int j) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) P[hd + (size_t)(i + r) * H + j] = acc[rb][cb_][r];
@@ -774,24 +879,39 @@ static hipError_t gbwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   constexpr int TT = gtile_rows<H>();
   const int chains = a.D.B * a.D.H, C = a.D.C;
   constexpr size_t hd = (size_t)H * D;
+  // the last chunk (walked first) leaves with a zero adjoint: its tile and
+  // state products keep only the terms that do not vanish
+  const bool za = n + 1 == a.D.L / C;
   launch_gtranspose<CT>(a.states + (size_t)n * 4 * hd, (size_t)a.nslots * 4 * hd, (CT*)a.packT,
                         4 * hd, (CT*)a.packT + 2 * hd, 4 * hd, chains, D, H, 0x3, st);
-  launch_gtranspose<CT>(a.adj + (size_t)((n + 1) & 1) * 4 * hd, 2 * 4 * hd, (CT*)a.packA, 8 * hd,
-                        (CT*)a.packA + 4 * hd, 8 * hd, chains, D, H, 0xf, st);
-  const size_t l1 = (3 * (size_t)TT * D + 4 * (size_t)TT * H) * sizeof(CT);
-  auto k1 = gbwd_tile_kernel<IO, CT, ACT, D, H>;
-  set_lds_limit((const void*)k1);
-  hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
+  if (za) {
+    const size_t lz = (2 * (size_t)TT * D + (size_t)TT * H) * sizeof(CT);
+    hipLaunchKernelGGL((gbwd_tile_last_kernel<IO, CT, ACT, D, H>), dim3(C / TT, chains), dim3(512), lz,
+                       st, a, n);
+  } else {
+    launch_gtranspose<CT>(a.adj + (size_t)((n + 1) & 1) * 4 * hd, 2 * 4 * hd, (CT*)a.packA, 8 * hd,
+                          (CT*)a.packA + 4 * hd, 8 * hd, chains, D, H, 0xf, st);
+    const size_t l1 = (3 * (size_t)TT * D + 4 * (size_t)TT * H) * sizeof(CT);
+    auto k1 = gbwd_tile_kernel<IO, CT, ACT, D, H>;
+    set_lds_limit((const void*)k1);
+    hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), l1, st, a, n);
+  }
   const int tk = gtk_of(C), ns = C / tk;
   const int sec = section_begin("global_bwd_carry", st);
+  constexpr size_t ls = lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>();
   set_lds_limit((const void*)gbwd_state_kernel<CT, D, H, GTK>);
   set_lds_limit((const void*)gbwd_state_kernel<CT, D, H, GTK_LONG>);
-  if (tk == GTK_LONG)
-    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK_LONG>), dim3(ns, 2, chains), dim3(512),
-                       (lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>()), st, a);
+  set_lds_limit((const void*)gbwd_state_kernel<CT, D, H, GTK, true>);
+  set_lds_limit((const void*)gbwd_state_kernel<CT, D, H, GTK_LONG, true>);
+  const dim3 gs(ns, 2, chains);
+  if (tk == GTK_LONG && za)
+    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK_LONG, true>), gs, dim3(512), ls, st, a);
+  else if (tk == GTK_LONG)
+    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK_LONG>), gs, dim3(512), ls, st, a);
+  else if (za)
+    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK, true>), gs, dim3(512), ls, st, a);
   else
-    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK>), dim3(ns, 2, chains), dim3(512),
-                       (lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>()), st, a);
+    hipLaunchKernelGGL((gbwd_state_kernel<CT, D, H, GTK>), gs, dim3(512), ls, st, a);
   const hipError_t e = launch_gbwd_state_reduce(a, n, ns, st);
   section_end(sec, st);
   return e;
