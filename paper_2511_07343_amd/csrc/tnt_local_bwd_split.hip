@@ -114,11 +114,13 @@ constexpr size_t split_b_lds() {
   return SplitBLds<CT, CP, D, H>::total;
 }
 // pass C: cbar (CP x CP fp32) and the gate partials (5 x 8 x CP fp32); the Q-K
-// term uses the same space first (Nbar: CP x D fp32, Msym: D x D compute type)
+// term uses the same space first (Mbar in padded rows, D x (D + 1) fp32, then
+// Nbar, CP x D fp32, in the same place; Msym: D x D compute type after it)
 template <typename CT, int CP, int D>
 constexpr size_t split_c_lds() {
+  static_assert(CP <= D + 1, "Nbar fits where Mbar was");
   const size_t gate = ((size_t)CP * CP + 40 * (size_t)CP) * sizeof(float);
-  const size_t qk = (size_t)CP * D * sizeof(float) + (size_t)D * D * sizeof(CT);
+  const size_t qk = (size_t)D * (D + 1) * sizeof(float) + (size_t)D * D * sizeof(CT);
   return gate > qk ? gate : qk;
 }
 
@@ -896,8 +898,8 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
   constexpr int d = D, Cp = CP;
   float* fCb = reinterpret_cast<float*>(smem);
   float* gpart = fCb + Cp * Cp;  // [5][8][Cp]
-  float* fNb = fCb;              // Q-K term first: Nbar [Cp][d] fp32, Msym [d][d] CT
-  CT* sMs = reinterpret_cast<CT*>(fCb + Cp * d);
+  float* fNb = fCb;              // Q-K term first: Nbar [Cp][d] fp32 (Mbar [d][d + 1]
+  CT* sMs = reinterpret_cast<CT*>(fCb + D * (D + 1));  // fp32 before it), Msym [d][d] CT
 
   const Dims Dm = a.D;
   const int C = Dm.C;
@@ -919,13 +921,38 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
 
   if (shard_qk && n < nch - 1) {
     // Kbar += (Nbar' - N (N . Nbar')) / ||k||, Nbar' = N (Mbar + Mbar^T), Mbar the
-    // suffix sum of Xbar^T Q over the shard's later chunks (Msym rounded to the
-    // compute type here, where the MFMA would round it)
+    // suffix sum of Xbar^T Q over the shard's later chunks (Mbar + Mbar^T formed
+    // through a padded LDS copy of Mbar and rounded to the compute type, where the
+    // MFMA would round it)
     const CT* N = rc + Y.r.fc.o[rec::N];
     const float* Mb = bqf + Y.r.bf.o[rec::XbQ];
+    float* const fMt = fCb;  // Mbar, rows padded to d + 1 (dead before Nbar is written)
+    float* dkp = a.dk_part + (cbase + tok0) * d;
+    const float* kn = rf + Y.r.ff.o[rec::kn];
+    // this thread's eight elements of a row of dk and N, requested ahead of the
+    // product: rows i, columns c0 .. c0 + 7 (eight threads a row, one wave's
+    // lanes 8r .. 8r + 7)
+    constexpr int CPR = D / 8, ITEMS = CP * CPR;
+    static_assert(ITEMS <= 512 && 64 % CPR == 0, "one item per thread, a row's threads in one wave");
+    const int qi = threadIdx.x / CPR, qc = (threadIdx.x % CPR) * 8;
+    const bool qrow = threadIdx.x < ITEMS && qi < C;
+    f32x4 k0v = {0.f, 0.f, 0.f, 0.f}, k1v = k0v;
+    float nv[8];
+    if (qrow) {
+      k0v = *reinterpret_cast<const f32x4*>(dkp + (size_t)qi * d + qc);
+      k1v = *reinterpret_cast<const f32x4*>(dkp + (size_t)qi * d + qc + 4);
+      load8(N + (size_t)qi * d + qc, nv);
+    }
+    for (int e = threadIdx.x * 4; e < d * d; e += blockDim.x * 4) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(Mb + e);
+      const int i = e / d, j = e - i * d;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) fMt[i * (d + 1) + j + q] = v[q];
+    }
+    __syncthreads();
     for (int e = threadIdx.x; e < d * d; e += blockDim.x) {
       const int i = e / d, j = e - i * d;
-      sMs[e] = from_f<CT>(Mb[e] + Mb[(size_t)j * d + i]);
+      sMs[e] = from_f<CT>(fMt[i * (d + 1) + j] + fMt[j * (d + 1) + i]);
     }
     __syncthreads();
     using BCD = Blk<CP, D>;
@@ -939,18 +966,29 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
       });
     });
     __syncthreads();
-    float* dkp = a.dk_part + (cbase + tok0) * d;
-    const float* kn = rf + Y.r.ff.o[rec::kn];
-    for (int i = wave_id(); i < C; i += num_waves()) {
-      const float nr = kn[i];
-      float dt = 0.f;
-      for (int j = l; j < d; j += WAVE) dt += to_f(N[(size_t)i * d + j]) * fNb[(size_t)i * d + j];
-      dt = wave_sum(dt);
-      if (nr > 0.f)
-        for (int j = l; j < d; j += WAVE) {
-          const size_t e = (size_t)i * d + j;
-          dkp[e] += (fNb[e] - to_f(N[e]) * dt) / nr;
+    {
+      float f8[8], dt = 0.f;
+      if (qrow) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          f8[q] = fNb[(size_t)qi * d + qc + q];
+          dt += nv[q] * f8[q];
         }
+      }
+#pragma unroll
+      for (int o = 1; o < CPR; o <<= 1) dt += __shfl_xor(dt, o, WAVE);  // the row's threads
+      if (qrow) {
+        const float nr = kn[qi];
+        if (nr > 0.f) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            k0v[q] += (f8[q] - nv[q] * dt) / nr;
+            k1v[q] += (f8[q + 4] - nv[q + 4] * dt) / nr;
+          }
+          *reinterpret_cast<f32x4*>(dkp + (size_t)qi * d + qc) = k0v;
+          *reinterpret_cast<f32x4*>(dkp + (size_t)qi * d + qc + 4) = k1v;
+        }
+      }
     }
     __syncthreads();  // LDS is reused below
   }
