@@ -11,7 +11,7 @@ namespace tnt {
 // Header at the start of a saved buffer (tnt_mem_fwd -> tnt_mem_bwd): which
 // layout, kernel family, ring sizes and configuration wrote it.
 constexpr uint32_t SAVED_MAGIC = 0x544e5453u;  // "STNT"
-constexpr uint32_t SAVED_LAYOUT_VERSION = 3;
+constexpr uint32_t SAVED_LAYOUT_VERSION = 4;
 constexpr size_t SAVED_HEADER_BYTES = 256;
 struct SavedHeader {
   uint32_t magic, layout_version, family, pad;

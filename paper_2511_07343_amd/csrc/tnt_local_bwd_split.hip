@@ -212,7 +212,10 @@ local_bwd_ret_kernel(LocalBwdArgs a, SplitPtrs P) {
     // consecutive threads on consecutive rows) and its scaled and transposed
     // forms for the backward record; partial dA, dE of the retrieval,
     // sum_k dO_ik (H W2^T)_ik (S2 likewise)
-    chunk_coefs_f(cf, a.lr + cbase, a.mom + cbase, a.decay + cbase, tok0, C, Cp);  // ends with a barrier
+    if constexpr (rec::rec_coefs(CP))
+      coefs_from_record_f(cf, FRF_(Cc), FRF_(cA), FRF_(cE), Cp);  // ends with a barrier
+    else
+      chunk_coefs_f(cf, a.lr + cbase, a.mom + cbase, a.decay + cbase, tok0, C, Cp);  // likewise
     constexpr int JB = D / 8, ITEMS = CP * JB, PER = (ITEMS + 511) / 512;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {

@@ -112,7 +112,7 @@ __device__ __forceinline__ void chunk_coefs(Coef& cf, const float* lr, const flo
 // The coefficients without ct / ebt (retrieval and carry only; smaller LDS
 // footprint), for chunks of at most N (padded) positions.
 template <int N>
-struct CoefFN {
+struct alignas(16) CoefFN {  // 16-byte aligned: c is copied in 16-byte groups
   static_assert(N <= MAXC, "one wave scans a chunk");
   // the lower triangle of c (c_{i,tau} = 0 for tau > i), row after row:
   // c_{i,tau} at i (i + 1) / 2 + tau
@@ -210,6 +210,27 @@ __device__ __forceinline__ void chunk_coefs_g(CoefGN<N>& cf, const float* lr, co
       cf.bb[tau] = cf.eta[tau] * et;
     }
     if (tau == 0) cf.BC = expf(cf.lb[C - 1]);
+  }
+  __syncthreads();
+}
+
+// The retrieval's chunk coefficients c (packed), A, E from a forward record: the
+// values chunk_coefs_f forms, bit for bit (the retrieval computed them from the
+// same gates).  All threads call; ends with a barrier.
+template <int N>
+__device__ __forceinline__ void coefs_from_record_f(CoefFN<N>& cf, const float* cc, const float* vA,
+                                                    const float* vE, int Cp) {
+  for (int e = threadIdx.x; e < Cp; e += blockDim.x) {
+    cf.A[e] = vA[e];
+    cf.E[e] = vE[e];
+  }
+  const int np = Cp * (Cp + 1) / 2;
+  for (int e = threadIdx.x * 4; e < np; e += blockDim.x * 4) {
+    if (e + 4 <= np) {
+      *reinterpret_cast<f32x4*>(cf.c + e) = *reinterpret_cast<const f32x4*>(cc + e);
+    } else {
+      for (int q = e; q < np; ++q) cf.c[q] = cc[q];
+    }
   }
   __syncthreads();
 }

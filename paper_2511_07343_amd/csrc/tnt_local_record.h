@@ -35,6 +35,9 @@ enum FwdF {
   HW2, HS2,      // d x C  (H W2^T)^T, (H S2^T)^T
   kn, cC, bb,    // C      key norms, cC, b
   sc,            // 4      A_C, B_C, E_C
+  Cc,            // C(C+1)/2  the chunk coefficients c_{i,tau} (tau <= i), row after row
+  cA, cE,        // C      A_i, E_i (pass A of the backward reads these and Cc instead of
+                 //        recomputing them; empty unless rec_coefs(C))
   FWD_F
 };
 // backward record, compute type
@@ -75,11 +78,17 @@ struct RecLayout {
   Lay<BWD_F> bf;
 };
 
+// Whether the forward record keeps the chunk coefficients for the backward.  At
+// chunks of up to 32 positions, recomputing them (one wave's scan) costs pass A
+// more than reading them back; at 64 the 8 KB per chunk they take costs more.
+__host__ __device__ constexpr bool rec_coefs(int Cp) { return Cp <= 32; }
+
 __host__ __device__ constexpr RecLayout make_rec_layout(int Cp, int d, int h) {
   const size_t C = Cp, Cd = C * d, Ch = C * h, CC = C * C, dd = (size_t)d * d;
   const size_t sfc[FWD_CT] = {Ch, Ch, Ch, Ch, Ch, Ch, Ch, Ch, CC, CC, CC, Cd, Cd, Cd, Cd,
                               Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd, Cd};
-  const size_t sff[FWD_F] = {CC, CC, Cd, Cd, C, C, C, 4};
+  const size_t cr = rec_coefs(Cp) ? C : 0;
+  const size_t sff[FWD_F] = {CC, CC, Cd, Cd, C, C, C, 4, cr * (cr + 1) / 2, cr, cr};
   const size_t sbc[BWD_CT] = {Ch, CC, Cd, Cd, Cd};
   const size_t sbf[BWD_F] = {CC, C, C, dd, C, C, 4};
   return RecLayout{make_lay(sfc), make_lay(sff), make_lay(sbc), make_lay(sbf)};

@@ -263,6 +263,16 @@ local_ret_kernel(LocalFwdArgs a) {
       frf[RL.ff.o[rec::kn] + i] = cf.knorm[i];
       frf[RL.ff.o[rec::cC] + i] = cf.cC[i];
       frf[RL.ff.o[rec::bb] + i] = cf.bb[i];
+      if constexpr (rec::rec_coefs(CP)) {
+        frf[RL.ff.o[rec::cA] + i] = cf.A[i];
+        frf[RL.ff.o[rec::cE] + i] = cf.E[i];
+      }
+    }
+    if constexpr (rec::rec_coefs(CP)) {  // the packed coefficient matrix, 16-byte stores
+      constexpr int NP = CP * (CP + 1) / 2;
+      static_assert(NP % 4 == 0, "whole 16-byte groups");
+      for (int e = threadIdx.x * 4; e < NP; e += 512 * 4)
+        *reinterpret_cast<f32x4*>(frf + RL.ff.o[rec::Cc] + e) = *reinterpret_cast<const f32x4*>(cf.c + e);
     }
     if (threadIdx.x == 0) {
       frf[RL.ff.o[rec::sc] + 0] = cf.AC;
