@@ -509,6 +509,10 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
   // pass is done (that pass fills the chip; the walk after it leaves half the
   // CUs to the global chain).
   if (c->has_global && c->n_local) HIP_TRY(fork_of(&fk));
+  // the last local memory's gate pass, when its walk ran beside the global chain:
+  // launched after that chain (and the separate dk sum folded into it)
+  int gate_deferred = 0;
+  LocalBwdArgs last_local{};
   for (int i = 0, m = c->has_global; i < c->n_local; ++i, ++m) {
     LocalBwdArgs a{};
     a.q = q; a.k = k; a.v = v; a.dO = dO;
@@ -543,7 +547,10 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     // part are final: the helper stream reduces them beside its gate pass
     const bool last = i == c->n_local - 1;
     a.pass_b_done = (fk && last) ? fk->eb : nullptr;
+    a.defer_gate = fk && last && !grouped;
+    a.gate_deferred = &gate_deferred;
     HIP_TIMED(grouped ? "global_intra_bwd" : "local_bwd", launch_local_bwd(a, y.l_units[i], st));
+    if (last) last_local = a;
     if (!(fk && last))
       HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                  dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
@@ -606,9 +613,20 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     HIP_TRY(hipEventRecord(fk->e1, fk->side));
     st = main_st;
     HIP_TRY(hipStreamWaitEvent(main_st, fk->eg, 0));
-    SumJobs mainj{};
-    mainj.parts[0] = dkp; mainj.out[0] = dk;
-    HIP_TIMED("sum_grads", launch_sum_outs(mainj, 1, y.M, y.io_elems, y.io_elems, bf, st));
+    if (gate_deferred) {
+      // every other memory's dk part is final: the gate pass writes dk itself
+      LocalBwdArgs a = last_local;
+      a.dk_out = dk;
+      a.dk_parts = dkp;
+      a.dk_stride = y.io_elems;
+      a.dk_nparts = y.M;
+      a.dk_self = c->has_global + c->n_local - 1;
+      HIP_TIMED("local_bwd_gate", launch_local_bwd_gate(a, y.l_units[c->n_local - 1], st));
+    } else {
+      SumJobs mainj{};
+      mainj.parts[0] = dkp; mainj.out[0] = dk;
+      HIP_TIMED("sum_grads", launch_sum_outs(mainj, 1, y.M, y.io_elems, y.io_elems, bf, st));
+    }
     HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
     return TNT_OK;
   }

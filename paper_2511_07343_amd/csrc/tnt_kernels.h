@@ -112,6 +112,17 @@ struct LocalBwdArgs {
   hipEvent_t aux_mid;                                    // with aux: recorded there once the lower
                                                          // half of the chunks has its pass A
   int force_generic;                                     // 1: skip fixed-size kernels
+  // Host side: with defer_gate set, the three-pass kernels may leave their gate
+  // pass out (setting *gate_deferred) for launch_local_bwd_gate to run later.
+  int defer_gate;
+  int* gate_deferred;
+  // The final dk, when every other memory's dk part is done before the gate pass:
+  // the gate pass writes dk_out (I/O dtype) = the fixed-order sum of dk_nparts fp32
+  // parts dk_stride elements apart, this memory's (part dk_self) from registers.
+  void* dk_out;
+  const float* dk_parts;
+  size_t dk_stride;
+  int dk_nparts, dk_self;
 };
 
 struct GlobalArgs {
@@ -193,6 +204,8 @@ hipError_t launch_local_bwd(const LocalBwdArgs& a, int units, hipStream_t st);
 bool launch_local_bwd_blk(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err);
 size_t local_bwd_split_bytes(const Dims& D, int units);  // 0: no three-pass kernels for D
 bool launch_local_bwd_split(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err);
+// the gate pass that launch_local_bwd_split deferred (same arguments)
+hipError_t launch_local_bwd_gate(const LocalBwdArgs& a, int units, hipStream_t st);
 hipError_t launch_global_scan(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_init(const GlobalArgs& a, hipStream_t st);
 hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st);

@@ -922,7 +922,17 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
   const int l = lane_id();
   const bool shard_qk = Dm.qk_proj && Dm.qk_scope == 0;
 
-  if (shard_qk && n < nch - 1) {
+  // this thread's eight elements of a row of dk: rows i, columns c0 .. c0 + 7
+  // (eight threads a row, one wave's lanes 8r .. 8r + 7)
+  constexpr int CPR = D / 8, ITEMS = CP * CPR;
+  static_assert(ITEMS <= 512 && 64 % CPR == 0, "one item per thread, a row's threads in one wave");
+  const int qi = threadIdx.x / CPR, qc = (threadIdx.x % CPR) * 8;
+  const bool qrow = threadIdx.x < ITEMS && qi < C;
+  float* dkp = a.dk_part + (cbase + tok0) * d;
+  const bool fuse = a.dk_out != nullptr;  // write the final dk (every other part is done)
+  const bool qk_here = shard_qk && n < nch - 1;
+  f32x4 k0v = {0.f, 0.f, 0.f, 0.f}, k1v = k0v;
+  if (qk_here) {
     // Kbar += (Nbar' - N (N . Nbar')) / ||k||, Nbar' = N (Mbar + Mbar^T), Mbar the
     // suffix sum of Xbar^T Q over the shard's later chunks (Mbar + Mbar^T formed
     // through a padded LDS copy of Mbar and rounded to the compute type, where the
@@ -930,16 +940,8 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
     const CT* N = rc + Y.r.fc.o[rec::N];
     const float* Mb = bqf + Y.r.bf.o[rec::XbQ];
     float* const fMt = fCb;  // Mbar, rows padded to d + 1 (dead before Nbar is written)
-    float* dkp = a.dk_part + (cbase + tok0) * d;
     const float* kn = rf + Y.r.ff.o[rec::kn];
-    // this thread's eight elements of a row of dk and N, requested ahead of the
-    // product: rows i, columns c0 .. c0 + 7 (eight threads a row, one wave's
-    // lanes 8r .. 8r + 7)
-    constexpr int CPR = D / 8, ITEMS = CP * CPR;
-    static_assert(ITEMS <= 512 && 64 % CPR == 0, "one item per thread, a row's threads in one wave");
-    const int qi = threadIdx.x / CPR, qc = (threadIdx.x % CPR) * 8;
-    const bool qrow = threadIdx.x < ITEMS && qi < C;
-    f32x4 k0v = {0.f, 0.f, 0.f, 0.f}, k1v = k0v;
+    // the row elements of dk and N, requested ahead of the product
     float nv[8];
     if (qrow) {
       k0v = *reinterpret_cast<const f32x4*>(dkp + (size_t)qi * d + qc);
@@ -988,12 +990,45 @@ __global__ void __launch_bounds__(512) local_bwd_gate_kernel(LocalBwdArgs a, Spl
             k0v[q] += (f8[q] - nv[q] * dt) / nr;
             k1v[q] += (f8[q + 4] - nv[q + 4] * dt) / nr;
           }
-          *reinterpret_cast<f32x4*>(dkp + (size_t)qi * d + qc) = k0v;
-          *reinterpret_cast<f32x4*>(dkp + (size_t)qi * d + qc + 4) = k1v;
+          if (!fuse) {
+            *reinterpret_cast<f32x4*>(dkp + (size_t)qi * d + qc) = k0v;
+            *reinterpret_cast<f32x4*>(dkp + (size_t)qi * d + qc + 4) = k1v;
+          }
         }
       }
     }
     __syncthreads();  // LDS is reused below
+  }
+  if (fuse && qrow) {
+    // the final dk of the row: every memory's part in a fixed order (the order of
+    // the separate sum), this memory's from the registers
+    if (!qk_here) {
+      k0v = *reinterpret_cast<const f32x4*>(dkp + (size_t)qi * d + qc);
+      k1v = *reinterpret_cast<const f32x4*>(dkp + (size_t)qi * d + qc + 4);
+    }
+    const size_t e = (cbase + tok0 + qi) * d + qc;
+    f32x4 s0 = k0v, s1 = k1v;
+    for (int p = 0; p < a.dk_nparts; ++p) {
+      f32x4 y0 = k0v, y1 = k1v;
+      if (p != a.dk_self) {
+        y0 = *reinterpret_cast<const f32x4*>(a.dk_parts + p * a.dk_stride + e);
+        y1 = *reinterpret_cast<const f32x4*>(a.dk_parts + p * a.dk_stride + e + 4);
+      }
+      if (p == 0) {
+        s0 = y0;
+        s1 = y1;
+      } else {
+        s0 += y0;
+        s1 += y1;
+      }
+    }
+    bf16x8 ov;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      ov[q] = (__bf16)s0[q];
+      ov[q + 4] = (__bf16)s1[q];
+    }
+    *reinterpret_cast<bf16x8*>(reinterpret_cast<__bf16*>(a.dk_out) + e) = ov;
   }
 
   chunk_coefs_g(cf, a.lr + cbase, mom, dec, tok0, C, Cp);  // ends with a barrier
@@ -1147,6 +1182,17 @@ bool split_match(const Dims& Dm) {
 }
 
 // size query (ws == nullptr) or launch
+// the gate pass over every chunk of every unit
+template <typename CT, int D, int H, int CP>
+void launch_gate(const LocalBwdArgs& a, int units, int nch, hipStream_t st) {
+  SplitPtrs P = carve<CT>(a.split_ws, split_sizes<CT, CP, D, H>(units, nch), units);
+  P.n0 = 0;
+  P.nc = nch;
+  auto kc = local_bwd_gate_kernel<CT, D, H, CP>;
+  constexpr size_t lds = split_c_lds<CT, CP, D>();
+  hipLaunchKernelGGL(kc, dim3(units * nch), dim3(512), lds, st, a, P);
+}
+
 template <typename IO, typename CT, int ACT, int D, int H, int CP>
 bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipStream_t st,
                hipError_t* err, size_t* bytes) {
@@ -1222,12 +1268,29 @@ bool try_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, hipSt
   }
   section_end(sec, st);
   if (a->pass_b_done && (e = hipEventRecord(a->pass_b_done, st)) != hipSuccess) return fail(e);
+  if (a->defer_gate && a->gate_deferred && halves && (on_aux || !scan)) {
+    // the caller launches the gate pass later (launch_local_bwd_gate)
+    *a->gate_deferred = 1;
+    *err = hipGetLastError();
+    return true;
+  }
   if (on_aux) {
     if ((e = hipStreamWaitEvent(st, a->aux_done, 0)) != hipSuccess) return fail(e);
   } else if (scan) {
     launch_scan(st);
   }
-  hipLaunchKernelGGL(kc, dim3(total), dim3(512), lds_c, st, *a, P);
+  launch_gate<CT, D, H, CP>(*a, units, nch, st);
+  *err = hipGetLastError();
+  return true;
+}
+
+template <typename IO, typename CT, int ACT, int D, int H, int CP>
+bool try_gate(const LocalBwdArgs& a, const Dims& Dm, int units, hipStream_t st, hipError_t* err) {
+  if (!split_match<IO, CT, ACT, D, H, CP>(Dm)) return false;
+  // the suffix scan ran on the second stream (a deferral needs it there)
+  if (Dm.qk_proj && Dm.qk_scope == 0 && (*err = hipStreamWaitEvent(st, a.aux_done, 0)) != hipSuccess)
+    return true;
+  launch_gate<CT, D, H, CP>(a, units, Dm.S / Dm.C, st);
   *err = hipGetLastError();
   return true;
 }
@@ -1243,7 +1306,21 @@ bool dispatch_split(const LocalBwdArgs* a, const Dims& Dm, int units, void* ws, 
          try_split<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, Dm, units, ws, st, err, bytes);
 }
 
+bool dispatch_gate(const LocalBwdArgs& a, int units, hipStream_t st, hipError_t* err) {
+  const Dims& Dm = a.D;
+  if (!Dm.bf16) return false;
+  return try_gate<__bf16, __bf16, ACT_SILU, 64, 256, 64>(a, Dm, units, st, err) ||
+         try_gate<__bf16, __bf16, ACT_SILU, 64, 256, 32>(a, Dm, units, st, err) ||
+         try_gate<__bf16, __bf16, ACT_SILU, 64, 256, 16>(a, Dm, units, st, err) ||
+         try_gate<__bf16, __bf16, ACT_GELU, 64, 256, 64>(a, Dm, units, st, err);
+}
+
 }  // namespace
+
+hipError_t launch_local_bwd_gate(const LocalBwdArgs& a, int units, hipStream_t st) {
+  hipError_t e = hipSuccess;
+  return dispatch_gate(a, units, st, &e) ? e : hipErrorInvalidValue;
+}
 
 size_t local_bwd_split_bytes(const Dims& D, int units) {
   size_t bytes = 0;
