@@ -371,7 +371,7 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
 struct Fork {
   hipStream_t side = nullptr;
   hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr, eb = nullptr, eg = nullptr, es = nullptr,
-            ec = nullptr;
+            ec = nullptr, er = nullptr, et = nullptr;
 };
 constexpr int MAX_DEV = 64;
 Fork g_fork[MAX_DEV];
@@ -392,6 +392,8 @@ hipError_t fork_of(Fork** out) {
     if ((e = hipEventCreateWithFlags(&f.eg, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.es, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.ec, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.er, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.et, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &f;
   return hipSuccess;
@@ -457,6 +459,12 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
       HIP_TIMED("copy_final", launch_copy_final(a.states, a.nslots, y.l_units[i], 4 * y.hd,
                                                 y.l_chunks[i], final_state, st));
   }
+  // With the helper stream and no final state: the last global chunk's tile writes
+  // the layer output of its tokens, and the caller's stream sums the other tokens'
+  // parts once the tile of the chunk before it is done (beside the last carry).
+  int o_fused = 0, tile_rec = 0;
+  const bool fuse_o = fk && o && !final_state;
+  if (fuse_o) HIP_TRY(hipEventRecord(fk->er, main_st));
   if (c->has_global) {
     st = fk ? fk->side : main_st;
     GlobalArgs g{};
@@ -475,6 +483,16 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
     g.D = dims_of(c, c->C_G, c->L);
     g.force_generic = generic_only();
     g.skip_final_carry = final_state == nullptr;
+    if (fuse_o) {
+      g.o_final = o;
+      g.o_stride = y.io_elems;
+      g.o_nparts = y.M;
+      g.parts_ready = fk->er;
+      g.tile_done = fk->et;
+      g.tile_done_n = y.g_chunks - 2;
+      g.o_fused = &o_fused;
+      g.tile_recorded = &tile_rec;
+    }
     HIP_TIMED("global_scan", launch_global_scan(g, st));
     HIP_TIMED("global_init", launch_global_init(g, st));
     for (int n = 0; n < y.g_chunks; ++n) HIP_TIMED("global_fwd_chunk", launch_global_fwd_chunk(g, n, st));
@@ -483,11 +501,20 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
                                 final_state, st));
   }
   st = main_st;
+  const int bf = c->dtype == TNT_BF16;
+  if (o_fused && y.g_chunks >= 2) {
+    // the tokens of every global chunk but the last (the last tile wrote the rest)
+    const hipEvent_t ready = tile_rec ? fk->et : fk->e1;
+    if (!tile_rec) HIP_TRY(hipEventRecord(fk->e1, fk->side));
+    HIP_TRY(hipStreamWaitEvent(main_st, ready, 0));
+    const size_t per = (size_t)c->L * c->d, seg = (size_t)(y.g_chunks - 1) * c->C_G * c->d;
+    HIP_TIMED("sum_out", launch_sum_out_runs(opart, y.M, y.io_elems, y.BH, per, seg, o, bf, st));
+  }
   if (fk) {
     HIP_TRY(hipEventRecord(fk->e1, fk->side));
     HIP_TRY(hipStreamWaitEvent(main_st, fk->e1, 0));
   }
-  if (o) HIP_TIMED("sum_out", launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, c->dtype == TNT_BF16, st));
+  if (o && !o_fused) HIP_TIMED("sum_out", launch_sum_out(opart, y.M, y.io_elems, y.io_elems, o, bf, st));
   return TNT_OK;
 }
 

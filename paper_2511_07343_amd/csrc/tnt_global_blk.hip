@@ -274,7 +274,13 @@ __global__ void __launch_bounds__(512) gfwd_tile_kernel(GlobalArgs a, int n) {
       for (int r = 0; r < 4; ++r) {
         const int ii = i + r;
         const size_t e = (size_t)ii * D + j;
-        o[e] = ao[rb][cb_][r];
+        if (KS || !a.o_final) {
+          o[e] = ao[rb][cb_][r];
+        } else {  // the layer output: every memory's part in the fixed order
+          float sv = ao[rb][cb_][r];
+          for (int p = 1; p < a.o_nparts; ++p) sv += o[p * a.o_stride + e];
+          reinterpret_cast<IO*>(a.o_final)[cb * D + e] = from_f<IO>(sv);
+        }
         if constexpr (KS) {
           const float rv = rscale * (ay[rb][cb_][r] - to_f(v[e]));
           sR[(size_t)ii * LD + j] = from_f<CT>(rv);
@@ -850,14 +856,25 @@ static hipError_t gfwd_blk_chunk(const GlobalArgs& a, int n, hipStream_t st) {
   // chunk (and the tile's key side that feeds it) runs when the caller asks for
   // the final state
   if (a.skip_final_carry && n + 1 == a.D.L / C) {
+    GlobalArgs b = a;
+    if (b.o_final) {
+      hipError_t e = b.parts_ready ? hipStreamWaitEvent(st, b.parts_ready, 0) : hipErrorInvalidValue;
+      if (e != hipSuccess) b.o_final = nullptr;  // no fused sum (the caller sums)
+    }
     auto kq = gfwd_tile_kernel<IO, CT, ACT, D, H, false>;
     set_lds_limit((const void*)kq);
-    hipLaunchKernelGGL(kq, dim3(C / TT, chains), dim3(512), (gfwd_tile_lds<D, H, false>()), st, a, n);
+    hipLaunchKernelGGL(kq, dim3(C / TT, chains), dim3(512), (gfwd_tile_lds<D, H, false>()), st, b, n);
+    if (b.o_final && b.o_fused) *b.o_fused = 1;
     return hipGetLastError();
   }
   auto k1 = gfwd_tile_kernel<IO, CT, ACT, D, H, true>;
   set_lds_limit((const void*)k1);
   hipLaunchKernelGGL(k1, dim3(C / TT, chains), dim3(512), (gfwd_tile_lds<D, H, true>()), st, a, n);
+  if (a.tile_done && n == a.tile_done_n) {
+    const hipError_t e = hipEventRecord(a.tile_done, st);
+    if (e != hipSuccess) return e;
+    if (a.tile_recorded) *a.tile_recorded = 1;
+  }
   const int tk = gtk_of(C), ns = C / tk;
   const int sec = section_begin("global_carry", st);
   constexpr size_t lc = lds_gemm_bytes<CT, H, D, GCARRY_KT, 1>();

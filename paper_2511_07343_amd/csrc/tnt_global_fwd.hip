@@ -410,17 +410,20 @@ hipError_t launch_global_fwd_chunk(const GlobalArgs& a, int n, hipStream_t st) {
 // o = sum of the per-memory fp32 partials, written in the I/O dtype
 // ---------------------------------------------------------------------------
 template <typename IO, int NP>
-__global__ void sum_out_kernel(SumJobs jobs, int njobs, size_t stride, size_t n) {
+__global__ void sum_out_kernel(SumJobs jobs, int njobs, size_t stride, size_t n, size_t per8,
+                               size_t seg8) {
   // fixed-order sum of NP fp32 partials, 8 elements per thread (two 16-byte
   // loads per partial, all issued before the sum, one store), jobs along
-  // blockIdx.y
+  // blockIdx.y; the 8-element vectors taken are the first seg8 of every per8
+  // (n: the count of elements taken)
   const int y = blockIdx.y;
   if (y >= njobs) return;
   const float* parts = jobs.parts[y];
   IO* out = (IO*)jobs.out[y];
   const size_t n8 = n / 8;
-  for (size_t v = (size_t)blockIdx.x * blockDim.x + threadIdx.x; v < n8;
-       v += (size_t)gridDim.x * blockDim.x) {
+  for (size_t u = (size_t)blockIdx.x * blockDim.x + threadIdx.x; u < n8;
+       u += (size_t)gridDim.x * blockDim.x) {
+    const size_t v = seg8 == per8 ? u : (u / seg8) * per8 + u % seg8;
     f32x4 x0[NP], x1[NP];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
@@ -447,7 +450,7 @@ __global__ void sum_out_kernel(SumJobs jobs, int njobs, size_t stride, size_t n)
       *reinterpret_cast<f32x4*>(out + v * 8 + 4) = s1;
     }
   }
-  // tail (n not a multiple of 8)
+  // tail (n not a multiple of 8; whole runs only)
   for (size_t e = n8 * 8 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
        e += (size_t)gridDim.x * blockDim.x) {
     float sacc = 0.f;
@@ -458,16 +461,16 @@ __global__ void sum_out_kernel(SumJobs jobs, int njobs, size_t stride, size_t n)
 
 template <typename IO>
 static hipError_t sum_outs_io(const SumJobs& jobs, int njobs, int nparts, size_t stride, size_t n,
-                              hipStream_t st) {
+                              size_t per8, size_t seg8, hipStream_t st) {
   // one 8-element vector per thread where the grid allows it
   const int blocks = (int)std::max<size_t>(1, std::min<size_t>((n / 8 + 255) / 256, 65535));
   const dim3 g(blocks, njobs), b(256);
   switch (nparts) {
-    case 1: hipLaunchKernelGGL((sum_out_kernel<IO, 1>), g, b, 0, st, jobs, njobs, stride, n); break;
-    case 2: hipLaunchKernelGGL((sum_out_kernel<IO, 2>), g, b, 0, st, jobs, njobs, stride, n); break;
-    case 3: hipLaunchKernelGGL((sum_out_kernel<IO, 3>), g, b, 0, st, jobs, njobs, stride, n); break;
-    case 4: hipLaunchKernelGGL((sum_out_kernel<IO, 4>), g, b, 0, st, jobs, njobs, stride, n); break;
-    case 5: hipLaunchKernelGGL((sum_out_kernel<IO, 5>), g, b, 0, st, jobs, njobs, stride, n); break;
+    case 1: hipLaunchKernelGGL((sum_out_kernel<IO, 1>), g, b, 0, st, jobs, njobs, stride, n, per8, seg8); break;
+    case 2: hipLaunchKernelGGL((sum_out_kernel<IO, 2>), g, b, 0, st, jobs, njobs, stride, n, per8, seg8); break;
+    case 3: hipLaunchKernelGGL((sum_out_kernel<IO, 3>), g, b, 0, st, jobs, njobs, stride, n, per8, seg8); break;
+    case 4: hipLaunchKernelGGL((sum_out_kernel<IO, 4>), g, b, 0, st, jobs, njobs, stride, n, per8, seg8); break;
+    case 5: hipLaunchKernelGGL((sum_out_kernel<IO, 5>), g, b, 0, st, jobs, njobs, stride, n, per8, seg8); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -475,8 +478,20 @@ static hipError_t sum_outs_io(const SumJobs& jobs, int njobs, int nparts, size_t
 
 hipError_t launch_sum_outs(const SumJobs& jobs, int njobs, int nparts, size_t stride, size_t n,
                            int bf16, hipStream_t st) {
-  return bf16 ? sum_outs_io<__bf16>(jobs, njobs, nparts, stride, n, st)
-              : sum_outs_io<float>(jobs, njobs, nparts, stride, n, st);
+  return bf16 ? sum_outs_io<__bf16>(jobs, njobs, nparts, stride, n, n / 8, n / 8, st)
+              : sum_outs_io<float>(jobs, njobs, nparts, stride, n, n / 8, n / 8, st);
+}
+
+hipError_t launch_sum_out_runs(const float* parts, int nparts, size_t stride, size_t nseq, size_t per,
+                               size_t seg, void* out, int bf16, hipStream_t st) {
+  if (per % 8 || seg % 8 || seg > per) return hipErrorInvalidValue;
+  if (seg == 0 || nseq == 0) return hipSuccess;
+  SumJobs jobs{};
+  jobs.parts[0] = parts;
+  jobs.out[0] = out;
+  const size_t n = nseq * seg;
+  return bf16 ? sum_outs_io<__bf16>(jobs, 1, nparts, stride, n, per / 8, seg / 8, st)
+              : sum_outs_io<float>(jobs, 1, nparts, stride, n, per / 8, seg / 8, st);
 }
 
 hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,

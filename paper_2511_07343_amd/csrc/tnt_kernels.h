@@ -154,6 +154,19 @@ struct GlobalArgs {
   int force_generic;                                     // 1: skip fixed-size kernels
   int skip_final_carry;                                  // 1: the state after the last chunk
                                                          // is not read (no final-state output)
+  // Forward, the last chunk's retrieval-only tile (skip_final_carry): with o_final
+  // set it writes the layer output of its tokens (I/O dtype) = the fixed-order sum
+  // of o_nparts fp32 parts o_stride elements apart, the global memory's (part 0)
+  // from registers, after waiting on its stream for parts_ready; *o_fused is set
+  // when that tile was launched.  tile_done (host side): recorded after the tile of
+  // chunk tile_done_n.
+  void* o_final;
+  size_t o_stride;
+  int o_nparts;
+  hipEvent_t parts_ready, tile_done;
+  int tile_done_n;
+  int* o_fused;
+  int* tile_recorded;  // set when tile_done was recorded
 };
 
 constexpr int TKS = 8;  // floats per token in GlobalArgs::tokc
@@ -274,6 +287,10 @@ hipError_t launch_sum_outs(const SumJobs& jobs, int njobs, int nparts, size_t st
                            int bf16, hipStream_t st);
 hipError_t launch_sum_out(const float* parts, int nparts, size_t stride, size_t n, void* out,
                           int bf16, hipStream_t st);
+// the same sum over the first `seg` of every `per` elements (nseq runs; seg and per
+// multiples of 8)
+hipError_t launch_sum_out_runs(const float* parts, int nparts, size_t stride, size_t nseq, size_t per,
+                               size_t seg, void* out, int bf16, hipStream_t st);
 hipError_t launch_reduce_init(const float* parts, int B, int H, int nshard, size_t hd2,
                               float* dW1, float* dW2, int d, int hid, int accumulate,
                               hipStream_t st);
