@@ -46,6 +46,9 @@
  *    joined back into `stream` with events, so it overlaps the local memories.
  *    Calls from several host threads serialise their enqueue on a lock; calls
  *    on different streams with distinct workspaces may run concurrently.
+ *  - tnt_mem_fwd and tnt_mem_bwd can be captured into a HIP graph on `stream`
+ *    (they enqueue no memset or copy; the fork and join become graph edges) and
+ *    replayed while the buffers they were captured with stay allocated.
  */
 #ifndef TNT_H_
 #define TNT_H_
