@@ -131,6 +131,27 @@ def test_forward_without_saving_takes_both_passes(cfg):
     assert np.array_equal(a, b)
 
 
+FUSED_OUT = [
+    small_config(BF16, ACT_SILU, B=1, H=2, L=512, d=64, hid=256, C_G=512, locals_=((64, 256),),
+                 name="bf16 one global chunk B1 H2 L512 d64 h256 CG512 CL64 SL256"),
+    small_config(BF16, ACT_SILU, B=1, H=2, L=1024, d=64, hid=256, C_G=256, locals_=((16, 256), (32, 512)),
+                 name="bf16 four global chunks two locals B1 H2 L1024 d64 h256 CG256"),
+    WORKLOADS[2],
+]
+
+
+@pytest.mark.parametrize("cfg", FUSED_OUT, ids=lambda c: c.name)
+def test_forward_output_with_and_without_final_state(cfg):
+    """Without a final state the last global chunk's tile writes the layer output
+    of its tokens itself (and the caller's stream sums the others); with one, the
+    whole output is summed after the chain.  Both give the same bits."""
+    inp = make_inputs(cfg, 109)
+    print(f"\n[case] fused output sum {cfg.name}", flush=True)
+    a, _ = gpu_forward(cfg, inp, final=True)
+    b, _ = gpu_forward(cfg, inp, final=False)
+    assert np.array_equal(a, b)
+
+
 def test_forward_deterministic():
     cfg = SMALL[2]
     inp = make_inputs(cfg, 103)
