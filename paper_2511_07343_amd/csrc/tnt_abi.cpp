@@ -369,9 +369,9 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
 // Default priority; events are reused under a lock, so concurrent host
 // threads serialise their enqueues here.
 struct Fork {
-  hipStream_t side = nullptr;
+  hipStream_t side = nullptr, side2 = nullptr;  // side2: local memories after the first
   hipEvent_t e0 = nullptr, e1 = nullptr, ea = nullptr, eb = nullptr, eg = nullptr, es = nullptr,
-            ec = nullptr, er = nullptr, et = nullptr;
+            ec = nullptr, er = nullptr, et = nullptr, e2 = nullptr;
 };
 constexpr int MAX_DEV = 64;
 Fork g_fork[MAX_DEV];
@@ -394,6 +394,8 @@ hipError_t fork_of(Fork** out) {
     if ((e = hipEventCreateWithFlags(&f.ec, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.er, hipEventDisableTiming)) != hipSuccess) return e;
     if ((e = hipEventCreateWithFlags(&f.et, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipStreamCreateWithFlags(&f.side2, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&f.e2, hipEventDisableTiming)) != hipSuccess) return e;
   }
   *out = &f;
   return hipSuccess;
@@ -430,10 +432,15 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
   }
   // the local walks first: their workgroups are the critical path, and the
   // dispatcher places work in the order it is enqueued (the global chain's
-  // tile grids would otherwise take the CUs before the walk starts)
-  st = main_st;
+  // tile grids would otherwise take the CUs before the walk starts).  With two or
+  // more local memories (none of them the grouped global memory) every one after
+  // the first runs on a second helper stream beside the first: they share nothing
+  // (each has its own workspace and saved regions and its own output part).
+  const bool conc = fk && c->n_local >= 2 && !y.gsub0;
+  if (conc) HIP_TRY(hipStreamWaitEvent(fk->side2, fk->e0, 0));
   m = c->has_global;
   for (int i = 0; i < c->n_local; ++i, ++m) {
+    st = (conc && i > 0) ? fk->side2 : main_st;
     LocalFwdArgs a{};
     a.q = q; a.k = k; a.v = v;
     a.lr = lr + m * G; a.mom = mom + m * G; a.decay = decay + m * G;
@@ -462,6 +469,11 @@ tnt_status run_forward(const tnt_config* c, const Layout& y, const void* q, cons
   // With the helper stream and no final state: the last global chunk's tile writes
   // the layer output of its tokens, and the caller's stream sums the other tokens'
   // parts once the tile of the chunk before it is done (beside the last carry).
+  st = main_st;
+  if (conc) {
+    HIP_TRY(hipEventRecord(fk->e2, fk->side2));
+    HIP_TRY(hipStreamWaitEvent(main_st, fk->e2, 0));
+  }
   int o_fused = 0, tile_rec = 0;
   const bool fuse_o = fk && o && !final_state;
   if (fuse_o) HIP_TRY(hipEventRecord(fk->er, main_st));
@@ -540,7 +552,15 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
   // launched after that chain (and the separate dk sum folded into it)
   int gate_deferred = 0;
   LocalBwdArgs last_local{};
+  // two or more local memories: every one after the first on a second helper
+  // stream beside the first (as in the forward)
+  const bool conc = fk && c->n_local >= 2 && !y.gsub0;
+  if (conc) {
+    HIP_TRY(hipEventRecord(fk->e0, main_st));
+    HIP_TRY(hipStreamWaitEvent(fk->side2, fk->e0, 0));
+  }
   for (int i = 0, m = c->has_global; i < c->n_local; ++i, ++m) {
+    st = (conc && i > 0) ? fk->side2 : main_st;
     LocalBwdArgs a{};
     a.q = q; a.k = k; a.v = v; a.dO = dO;
     a.lr = lr + m * G; a.mom = mom + m * G; a.decay = decay + m * G;
@@ -573,8 +593,8 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
     // the last local memory's walk is the point after which dq, dv and every dW_init
     // part are final: the helper stream reduces them beside its gate pass
     const bool last = i == c->n_local - 1;
-    a.pass_b_done = (fk && last) ? fk->eb : nullptr;
-    a.defer_gate = fk && last && !grouped;
+    a.pass_b_done = (fk && last && !conc) ? fk->eb : nullptr;
+    a.defer_gate = fk && last && !grouped && !conc;
     a.gate_deferred = &gate_deferred;
     HIP_TIMED(grouped ? "global_intra_bwd" : "local_bwd", launch_local_bwd(a, y.l_units[i], st));
     if (last) last_local = a;
@@ -582,6 +602,12 @@ tnt_status run_backward(const tnt_config* c, const Layout& y, const void* q, con
       HIP_TIMED("reduce_init", launch_reduce_init(a.dWinit_part, c->B, c->H, c->L / c->S_L[i], 2 * y.hd,
                                  dW1 + (size_t)m * c->H * y.hd, dW2 + (size_t)m * c->H * y.hd,
                                  c->d, c->hid, 0, st));
+  }
+  st = main_st;
+  if (conc) {  // dq, dv and every dW_init part are final once both streams are done
+    HIP_TRY(hipEventRecord(fk->e2, fk->side2));
+    HIP_TRY(hipStreamWaitEvent(main_st, fk->e2, 0));
+    HIP_TRY(hipEventRecord(fk->eb, main_st));
   }
   if (c->has_global) {
     if (fk) {
