@@ -43,7 +43,8 @@
  *    clamped at -80, so mom below e^-80 acts as e^-80.
  *  - The global memory's chunk chain runs on a helper stream that the library
  *    creates (default priority) on first use for each device, forked from and
- *    joined back into `stream` with events, so it overlaps the local memories.
+ *    joined back into `stream` with events, so it overlaps the local memories;
+ *    local memories after the first run on a second such stream.
  *    Calls from several host threads serialise their enqueue on a lock; calls
  *    on different streams with distinct workspaces may run concurrently.
  *  - tnt_mem_fwd and tnt_mem_bwd can be captured into a HIP graph on `stream`
