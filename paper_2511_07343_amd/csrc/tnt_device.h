@@ -413,6 +413,36 @@ __device__ __forceinline__ void gemm_blk(const EA* A, int lda, const EB* B, int 
   });
 }
 
+// a lane's value from another lane of its quad (DPP quad_perm pattern CTRL)
+template <int CTRL>
+__device__ __forceinline__ float quad_perm(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// 4 x 4 transpose within each quad of lanes: before, lane q (= lane & 3) holds
+// column q of the quad's block (rows 0..3 in v[0..3]); after, it holds row q
+// (columns 0..3).  Two exchanges, with lane q ^ 1 (rows of the lane's parity kept)
+// and with lane q ^ 2.
+__device__ __forceinline__ f4 quad_transpose(const f4& v) {
+  const int q = lane_id() & 3;
+  const bool odd = q & 1, hi = q & 2;
+  const float x = quad_perm<0xB1>(odd ? v[0] : v[1]);  // from lane q ^ 1
+  const float y = quad_perm<0xB1>(odd ? v[2] : v[3]);
+  f4 b;
+  b[0] = odd ? x : v[0];
+  b[1] = odd ? v[1] : x;
+  b[2] = odd ? y : v[2];
+  b[3] = odd ? v[3] : y;
+  const float z = quad_perm<0x4E>(hi ? b[0] : b[2]);  // from lane q ^ 2
+  const float w = quad_perm<0x4E>(hi ? b[1] : b[3]);
+  f4 u;
+  u[0] = hi ? z : b[0];
+  u[1] = hi ? w : b[1];
+  u[2] = hi ? b[2] : z;
+  u[3] = hi ? b[3] : w;
+  return u;
+}
+
 // four consecutive compute-type elements from one f4 (8- or 16-byte store)
 template <typename CT> __device__ __forceinline__ void store4(CT* p, const f4& v);
 template <> __device__ __forceinline__ void store4<float>(float* p, const f4& v) {

@@ -152,12 +152,24 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
 #pragma unroll
       for (int ht = 0; ht < HT; ++ht) {
         const int h = (w * HT + ht) * 16 + lc, d0 = dt * 16 + 4 * g;
+        // W1^T, S1^T [D][HID]: the lane holds four rows of one column.  For chunks of
+        // up to 32 rows (many chunks per shard) a transpose within the lane's quad
+        // gives it four columns of one row, one 8-byte store instead of four 2-byte
+        // ones (fewer stores in flight when the next chunk waits for its keys); at 64
+        // rows the four stores measured faster.
+        if constexpr (CP < 64) {
+          const int q = lc & 3;
+          store4<CT>(pk + (size_t)(d0 + q) * HID + (h - q), quad_transpose(W1T[dt][ht]));
+          store4<CT>(pk + 2 * hd + (size_t)(d0 + q) * HID + (h - q), quad_transpose(S1T[dt][ht]));
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pk[(size_t)(d0 + r) * HID + h] = (CT)W1T[dt][ht][r];           // W1^T [D][HID]
-          pk[2 * hd + (size_t)(d0 + r) * HID + h] = (CT)S1T[dt][ht][r];  // S1^T [D][HID]
-          sW2[(size_t)(d0 + r) * LH + h] = (CT)W2[dt][ht][r];
+          for (int r = 0; r < 4; ++r) {
+            pk[(size_t)(d0 + r) * HID + h] = (CT)W1T[dt][ht][r];
+            pk[2 * hd + (size_t)(d0 + r) * HID + h] = (CT)S1T[dt][ht][r];
+          }
         }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sW2[(size_t)(d0 + r) * LH + h] = (CT)W2[dt][ht][r];
         store4<CT>(pk + hd + (size_t)h * D + d0, W2[dt][ht]);      // W2^T [HID][D]
         store4<CT>(pk + 3 * hd + (size_t)h * D + d0, S2[dt][ht]);  // S2^T [HID][D]
       }
