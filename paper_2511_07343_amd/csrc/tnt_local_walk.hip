@@ -389,9 +389,15 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
         d1[it][ht] = cvt4(dv);
         if (fr) {
           store4<CT>(fr + RL.fc.o[rec::G] + frag_ofs<CP, HID>(it * 16, j0, l), acc);
-          CT* const d1r = fr + RL.fc.o[rec::D1] + (size_t)(it * 16 + 4 * g) * HID + j0 + lc;  // [CP][HID]
+          if constexpr (CP < 64) {  // [CP][HID]: one row of four columns after the quad transpose
+            const int q = lc & 3;
+            store4<CT>(fr + RL.fc.o[rec::D1] + (size_t)(it * 16 + 4 * g + q) * HID + j0 + lc - q,
+                       quad_transpose(dv));
+          } else {
+            CT* const d1r = fr + RL.fc.o[rec::D1] + (size_t)(it * 16 + 4 * g) * HID + j0 + lc;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) d1r[(size_t)r * HID] = (CT)dv[r];
+            for (int r = 0; r < 4; ++r) d1r[(size_t)r * HID] = (CT)dv[r];
+          }
         }
         // D1^T [HID][CP] for the retrieval: the lane's four rows are contiguous
         store4<CT>(fsn + (size_t)CP * HID + (size_t)(j0 + lc) * CP + it * 16 + 4 * g, dv);
