@@ -178,8 +178,13 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
       for (int x = 0; x < 2; ++x) {
         const int t = 2 * w + x, i0 = (t / DT) * 16, j0 = (t % DT) * 16;
         store4<CT>(pk + 4 * hd + (size_t)(j0 + lc) * D + i0 + 4 * g, M[x]);  // M^T
+        if constexpr (CP < 64) {  // by rows after the quad transpose, as the copies above
+          const int q = lc & 3;
+          store4<float>(ms + (size_t)(i0 + 4 * g + q) * D + j0 + lc - q, quad_transpose(M[x]));
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) ms[(size_t)(i0 + 4 * g + r) * D + j0 + lc] = M[x][r];
+          for (int r = 0; r < 4; ++r) ms[(size_t)(i0 + 4 * g + r) * D + j0 + lc] = M[x][r];
+        }
       }
   };
   write_slot(pku, mst);
