@@ -168,8 +168,13 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
             pk[2 * hd + (size_t)(d0 + r) * HID + h] = (CT)S1T[dt][ht][r];
           }
         }
+        if constexpr (CP < 64) {
+          const int q = lc & 3;
+          *reinterpret_cast<bf16x4*>(sW2 + (size_t)(d0 + q) * LH + h - q) = cvt4(quad_transpose(W2[dt][ht]));
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sW2[(size_t)(d0 + r) * LH + h] = (CT)W2[dt][ht][r];
+          for (int r = 0; r < 4; ++r) sW2[(size_t)(d0 + r) * LH + h] = (CT)W2[dt][ht][r];
+        }
         store4<CT>(pk + hd + (size_t)h * D + d0, W2[dt][ht]);      // W2^T [HID][D]
         store4<CT>(pk + 3 * hd + (size_t)h * D + d0, S2[dt][ht]);  // S2^T [HID][D]
       }
@@ -316,7 +321,12 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
           hv[r] = av.s;
           d1v[r] = av.d1;
           d2v[r] = av.d2;
-          sHk[(size_t)(it * 16 + 4 * g + r) * LH + j0 + lc] = (CT)av.s;
+          if constexpr (CP >= 64) sHk[(size_t)(it * 16 + 4 * g + r) * LH + j0 + lc] = (CT)av.s;
+        }
+        if constexpr (CP < 64) {  // one 8-byte LDS write by rows after the quad transpose
+          const int q = lc & 3;
+          *reinterpret_cast<bf16x4*>(sHk + (size_t)(it * 16 + 4 * g + q) * LH + j0 + lc - q) =
+              cvt4(quad_transpose(hv));
         }
         hk[it][ht] = cvt4(hv);
         *reinterpret_cast<bf16x4*>(sSp + 4 * (64 * ((w * TM + it) * HT + ht) + l)) = cvt4(d1v);
