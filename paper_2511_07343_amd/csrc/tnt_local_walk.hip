@@ -224,6 +224,49 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
   };
   bf16x8 k_next = load_rows(k, s * Dm.S);
   load_gates(s * Dm.S);
+  // the carry's coefficients of a chunk from its gates (wave 0; the same suffix
+  // scan as carry_coefs).  For chunks of up to 32 rows they are formed at the end
+  // of the chunk before (gates loaded a chunk ahead), where they overlap the slot
+  // stores instead of holding the chunk's first barrier; at 64 rows, where that
+  // measured slower, at the chunk's start from the gates loaded during the carry
+  // before.
+  constexpr bool EARLY = CP < 64;
+  auto scan_coefs = [&](WalkCoef& cf) {
+    if (w == 0) {
+      const int i = lane_id();
+      const bool in = i < C;
+      const float eta = in ? g_lr : 0.f;
+      const float lmb = in ? log_mom(g_mom) : 0.f;
+      const float lka = in ? log_keep(g_dec) : 0.f;
+      const float la = wave_incl_sum(lka), lb = wave_incl_sum(lmb);
+      const float laC = __shfl(la, C - 1, WAVE), lbC = __shfl(lb, C - 1, WAVE);
+      const float lbn = __shfl_down(lb, 1, WAVE);
+      float ya = in ? __expf(laC - la) : 0.f;
+      float yb = (i + 1 < C) ? __expf(lbn - lb) : 0.f;
+  #pragma unroll
+      for (int o = 1; o < WAVE; o <<= 1) {
+        const float pa = __shfl_down(ya, o, WAVE), pb = __shfl_down(yb, o, WAVE);
+        if (i + o < WAVE) {
+          ya = ya + yb * pa;
+          yb = yb * pb;
+        }
+      }
+      const float ec = wave_sum(in ? __expf(laC - la + lb) : 0.f);
+      if (i < CP) {
+        cf.cC[i] = in ? eta * ya : 0.f;
+        cf.bb[i] = in ? eta * __expf(lbC - lb) : 0.f;
+      }
+      if (i == 0) {
+        cf.AC = __expf(laC);
+        cf.BC = __expf(lbC);
+        cf.EC = ec;
+      }
+    }
+  };
+  if constexpr (EARLY) {
+    scan_coefs(cfs[0]);
+    if (nch > 1) load_gates(s * Dm.S + C);  // one chunk ahead of their scan
+  }
 
   for (int n = 0; n < nch; ++n) {
     WalkCoef& cf = cfs[n & 1];
@@ -249,38 +292,7 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
         if ((threadIdx.x & (LPR - 1)) == 0) cf.knorm[i] = ss > 0.f ? __builtin_amdgcn_rsqf(ss) : 0.f;
       }
     }
-    // ---- the carry's coefficients from the prefetched gates (wave 0; the same
-    // suffix scan as carry_coefs)
-    if (w == 0) {
-      const int i = lane_id();
-      const bool in = i < C;
-      const float eta = in ? g_lr : 0.f;
-      const float lmb = in ? log_mom(g_mom) : 0.f;
-      const float lka = in ? log_keep(g_dec) : 0.f;
-      const float la = wave_incl_sum(lka), lb = wave_incl_sum(lmb);
-      const float laC = __shfl(la, C - 1, WAVE), lbC = __shfl(lb, C - 1, WAVE);
-      const float lbn = __shfl_down(lb, 1, WAVE);
-      float ya = in ? __expf(laC - la) : 0.f;
-      float yb = (i + 1 < C) ? __expf(lbn - lb) : 0.f;
-#pragma unroll
-      for (int o = 1; o < WAVE; o <<= 1) {
-        const float pa = __shfl_down(ya, o, WAVE), pb = __shfl_down(yb, o, WAVE);
-        if (i + o < WAVE) {
-          ya = ya + yb * pa;
-          yb = yb * pb;
-        }
-      }
-      const float ec = wave_sum(in ? __expf(laC - la + lb) : 0.f);
-      if (i < CP) {
-        cf.cC[i] = in ? eta * ya : 0.f;
-        cf.bb[i] = in ? eta * __expf(lbC - lb) : 0.f;
-      }
-      if (i == 0) {
-        cf.AC = __expf(laC);
-        cf.BC = __expf(lbC);
-        cf.EC = ec;
-      }
-    }
+    if constexpr (!EARLY) scan_coefs(cf);
     __syncthreads();
     // the chunk's values into sR (each Yk tile's owner reads them there and
     // overwrites them with R)
@@ -434,7 +446,7 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
     // ---- the next chunk's keys and gates (in flight during the carry)
     if (n + 1 < nch) {
       k_next = load_rows(k, tok0 + C);
-      load_gates(tok0 + C);
+      if constexpr (!EARLY) load_gates(tok0 + C);
     }
     // ---- the carry into the next state
     const float AC = cf.AC, BC = cf.BC, EC = cf.EC;
@@ -473,6 +485,10 @@ __global__ void __launch_bounds__(512) local_walk_kernel(LocalFwdArgs a) {
       }
     }
     write_slot(pku + (size_t)(n + 1) * PS, mst + (size_t)(n + 1) * D * D);
+    if (EARLY && n + 1 < nch) {  // the next chunk's coefficients (its buffer was chunk n - 1's)
+      scan_coefs(cfs[(n + 1) & 1]);
+      if (n + 2 < nch) load_gates(tok0 + 2 * C);
+    }
   }
 }
 
